@@ -1,0 +1,220 @@
+/*
+ * prr.h -- C ABI of the speculate-reuse-repair decode path for dynamic sparse
+ * attention on AMD Instinct MI355X (gfx950).
+ *
+ * One decode step of one layer, batch 1, is:
+ *
+ *   select   prr_score_topk   Quest page metadata -> GQA criticality -> top-K set A
+ *   predict  prr_predict      EMA update with this step's scores -> predicted set P
+ *   speculate prr_spec_attn   split-K flash-decode over P (may run while select runs)
+ *   repair   prr_repair       attend the missed pages A \ P and merge, so the result
+ *                             is attention over exactly A (or over P u A, on request)
+ *
+ * Citations name sections, equations and the appendix of "Predict, Reuse, and
+ * Repair: Accelerating Dynamic Sparse Attention for Long-Context LLM Decoding".
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every call returns prr_status.  PRR_OK is 0.  Arguments are validated on the host
+ *   before anything is launched; on an error nothing is launched, the outputs are
+ *   untouched and prr_last_error() (thread-local) says why.
+ * - Every call is asynchronous on the hipStream_t it is given (NULL = the legacy
+ *   default stream).  Device faults surface at the caller's next synchronisation.
+ * - All device memory is owned by the caller.  The library never allocates, frees or
+ *   synchronises.  Inputs are read-only.  Pointers marked "device" must be device
+ *   memory (or host memory the device can access); "host" pointers are read during
+ *   the call only.
+ * - Layouts are dense row-major in the order written, with no padding.  Per-page
+ *   arrays of a KV head have a row stride of max_pages entries; page lists have a row
+ *   stride of `cap` entries.
+ * - Calls are re-entrant.  Calls on different streams may run concurrently if they
+ *   write disjoint memory and do not share one workspace region (see
+ *   prr_workspace_size).
+ * - Query head j belongs to KV head j / G (G = num_q_heads / num_kv_heads).
+ * - Attention statistics: m is the maximum of the scaled logits q.k/sqrt(head_dim)
+ *   (natural-log units), l = sum exp(logit - m), o is normalised (divided by l).
+ *   The empty state is o = 0, m = -inf, l = 0.
+ * - Page ids in lists are logical pages.  The logical page p holds tokens
+ *   [p*page_size, (p+1)*page_size); tokens at or beyond num_tokens are masked.
+ *   A device-side list entry outside [0, num_pages) is skipped (never dereferenced);
+ *   lists must be duplicate-free, otherwise results are unspecified (but no memory
+ *   outside the arguments is touched).
+ */
+#ifndef PRR_H_
+#define PRR_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t prr_status;
+
+#define PRR_OK 0
+#define PRR_ERR_INVALID_ARG 1 /* a size, pointer or flag is out of range */
+#define PRR_ERR_UNSUPPORTED 2 /* shape or dtype without a compiled kernel instance */
+#define PRR_ERR_WORKSPACE 3   /* workspace missing, too small or misaligned */
+#define PRR_ERR_HIP 4         /* a HIP runtime call failed (launch error) */
+
+#define PRR_F16 0  /* IEEE binary16 */
+#define PRR_BF16 1 /* bfloat16 */
+
+#define PRR_META_MINMAX 0 /* Quest: channel-wise min and max key per page (Appendix A.1) */
+#define PRR_META_MEAN 1   /* mean-pooled block key (the InfLLM-v2 style compression, Section 2.1) */
+
+#define PRR_EXACT_SELECTED 0 /* output = attention over exactly A */
+#define PRR_KEEP_WASTED 1    /* output = attention over P u A (wasted pages kept as context, Section 1) */
+
+/* Shape of one layer's paged KV cache.
+ *   head_dim   128 (the only compiled value)
+ *   page_size  16 or 64 tokens
+ *   max_pages  page slots per KV head in the cache; also the row stride of per-page arrays
+ *   dtype      PRR_F16 or PRR_BF16, for q, keys, values, min/max metadata and out_o
+ *   meta_kind  PRR_META_MINMAX or PRR_META_MEAN
+ * Constraints: 1 <= num_kv_heads, num_q_heads = G * num_kv_heads with 1 <= G <= 16. */
+typedef struct {
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t page_size;
+  int32_t max_pages;
+  int32_t dtype;
+  int32_t meta_kind;
+} prr_dims;
+
+/* Largest supported values. */
+#define PRR_MAX_PAGES 16384 /* num_pages per KV head handled by one select */
+#define PRR_MAX_CAP 1024    /* entries of a page list (|A|, |P|) */
+#define PRR_MAX_FORCED 64   /* forced pages */
+
+const char* prr_status_string(prr_status status);
+const char* prr_last_error(void);
+
+/* Bytes of workspace used by prr_score_topk and prr_repair for lists of at most
+ * `cap` pages and speculation chunks of `chunk_pages` pages.  The workspace holds
+ * three disjoint regions (selection counters, repair counters, repair partial
+ * states); one prr_score_topk and one prr_repair may use the same workspace at the
+ * same time, two calls of the same entry point may not.  Returns 0 if the
+ * arguments are invalid. */
+size_t prr_workspace_size(const prr_dims* dims, int32_t cap, int32_t chunk_pages);
+
+/* Zero a workspace (device, `bytes` long, 256-byte aligned) with a fill kernel on
+ * `stream`.  Required once before first use; every call leaves its counters at zero
+ * again when it finishes. */
+prr_status prr_workspace_init(void* workspace, size_t bytes, hipStream_t stream);
+
+/* Size in floats of the speculation output of prr_spec_attn for lists of at most
+ * `cap` pages: part_o [Hkv][ceil(cap/C)][G][128], part_m and part_l
+ * [Hkv][ceil(cap/C)][G], page_m [Hkv][cap][G]. */
+size_t prr_spec_state_floats(const prr_dims* dims, int32_t cap, int32_t chunk_pages,
+                             size_t* part_o_floats, size_t* part_ml_floats, size_t* page_m_floats);
+
+/* Page metadata (Appendix A.1; block means for PRR_META_MEAN, Section 2.1).
+ *   k_cache     device [Hkv][max_pages][page_size][128] dtype (physical pages)
+ *   page_table  device [max_pages] int32 logical -> physical page, or NULL = identity
+ *   num_tokens  tokens in the cache; a partial last page uses its valid tokens only
+ *   page_begin, page_end   logical pages [begin, end) to (re)build; end <= ceil(num_tokens/page_size)
+ *   meta        device, MINMAX: [Hkv][max_pages][2][128] dtype (row 0 = min, row 1 = max),
+ *               MEAN: [Hkv][max_pages][128] float32.  Only pages [begin, end) are written.
+ * Min and max are exact; the mean is summed in float32. */
+prr_status prr_build_page_meta(const prr_dims* dims, const void* k_cache, const int32_t* page_table,
+                               int32_t num_tokens, int32_t page_begin, int32_t page_end, void* meta,
+                               hipStream_t stream);
+
+/* Criticality scores and top-K page selection (Appendix A.1; Section 1).
+ *   q            device [Hq][128] dtype, this step's query
+ *   meta         device, as written by prr_build_page_meta
+ *   num_pages    logical pages in the cache, 1..PRR_MAX_PAGES
+ *   k_select     budget K >= 0 in pages
+ *   forced       host [n_forced] int32 distinct pages in [0, num_pages) always selected
+ *                (copied into the launch), or NULL if n_forced = 0
+ *   forced_in_budget  1: |A| = max(K, n_forced) (forced pages count against K);
+ *                0: |A| = K + n_forced.  |A| is capped at num_pages.
+ *   scores       device [Hkv][max_pages] float32 out: IS = sum_i max(qbar_i m_i, qbar_i M_i)
+ *                (MEAN: qbar . kbar), unscaled, with qbar the mean of the group's queries
+ *   selected     device [Hkv][cap] int32 out: A in ascending page order
+ *   selected_count device [Hkv] int32 out: |A|
+ *   cap          row stride of `selected`, >= |A|, <= PRR_MAX_CAP
+ * Ranking key: (float32 score descending, page index ascending).
+ * Uses the selection-counter region of the workspace. */
+prr_status prr_score_topk(const prr_dims* dims, const void* q, const void* meta, int32_t num_pages,
+                          int32_t k_select, const int32_t* forced, int32_t n_forced, int32_t forced_in_budget,
+                          float* scores, int32_t* selected, int32_t* selected_count, int32_t cap,
+                          void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* EMA predictor (Section 4.1, Eqs. (2)-(3)) and the predicted set P (Eq. (1)).
+ *   ema_level, ema_trend  device [Hkv][max_pages] float32 in/out (level l and trend v)
+ *   ema_init_bits         device [Hkv][ceil(max_pages/32)] uint32 in/out: bit p set once
+ *                         page p has state; zero them when the cache is (re)filled
+ *   scores       device [Hkv][max_pages] float32 this step's IS, or NULL = predict only.
+ *                With scores: for a page without state, l = IS, v = 0 and the bit is set;
+ *                otherwise v = beta (IS - l) + (1 - beta) v, then l = alpha IS + (1 - alpha) l.
+ *   alpha in (0,1], beta in (0,1], gamma in [0,1]
+ *   p_select, forced, n_forced, forced_in_budget  as k_select etc. of prr_score_topk
+ *   predicted    device [Hkv][cap] int32 out: the p_select pages with the largest
+ *                l + gamma v (pages without state are never predicted unless forced),
+ *                ascending page order, ties to the lower page index
+ *   predicted_count device [Hkv] int32 out
+ * One workgroup per KV head; no workspace. */
+prr_status prr_predict(const prr_dims* dims, float* ema_level, float* ema_trend, uint32_t* ema_init_bits,
+                       const float* scores, int32_t num_pages, float alpha, float beta, float gamma,
+                       int32_t p_select, const int32_t* forced, int32_t n_forced, int32_t forced_in_budget,
+                       int32_t* predicted, int32_t* predicted_count, int32_t cap, hipStream_t stream);
+
+/* Speculative split-K sparse flash-decode over a page list (Section 4.3,
+ * "Instrumented speculative kernel").
+ *   q, k_cache, v_cache  device, [Hq][128], [Hkv][max_pages][page_size][128] dtype
+ *   page_table   device [max_pages] int32 or NULL (identity)
+ *   num_tokens   tokens in the cache (masks a partial last page)
+ *   pages        device [Hkv][cap] int32 list (normally P), page_count device [Hkv] int32
+ *   chunk_pages  C, 1..16: consecutive list entries [cC, cC+C) form chunk c
+ *   part_o       device [Hkv][ceil(cap/C)][G][128] float32 out: normalised o of each chunk
+ *   part_m, part_l device [Hkv][ceil(cap/C)][G] float32 out
+ *   page_m       device [Hkv][cap][G] float32 out: max scaled logit of each listed page,
+ *                or NULL (then prr_repair recomputes every chunk that holds a wasted page)
+ * Only chunks with at least one listed page are written. */
+prr_status prr_spec_attn(const prr_dims* dims, const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* page_table, int32_t num_tokens, const int32_t* pages,
+                         const int32_t* page_count, int32_t cap, int32_t chunk_pages, float* part_o,
+                         float* part_m, float* part_l, float* page_m, hipStream_t stream);
+
+/* Repair (Section 4.3, Eqs. (6)-(8)): fold the missed pages M = A \ P into the
+ * speculative state and merge, in one kernel.
+ *   selected, selected_count   A and |A| (device, as from prr_score_topk)
+ *   predicted, predicted_count P and |P| (device, as given to prr_spec_attn), or both
+ *                NULL: P is empty and every page of A is attended here (the serial
+ *                select-then-attend path)
+ *   part_o, part_m, part_l, page_m   the speculation output of prr_spec_attn over P
+ *                with the same cap and chunk_pages (ignored when P is NULL)
+ *   mode         PRR_EXACT_SELECTED: chunks of P that hold a wasted page (P \ A) have
+ *                the wasted pages' contribution removed (re-attended and subtracted when
+ *                they carry at most half of the chunk's softmax mass, otherwise the
+ *                chunk's pages of A are re-attended); PRR_KEEP_WASTED: P u A is attended
+ *   out_o32      device [Hq][128] float32 out, out_o device [Hq][128] dtype out or NULL
+ *   out_m, out_l device [Hq] float32 out
+ *   missed_count, wasted_count  device [Hkv] int32 out: |A \ P|, |P \ A|
+ * Uses the repair regions of the workspace. */
+prr_status prr_repair(const prr_dims* dims, const void* q, const void* k_cache, const void* v_cache,
+                      const int32_t* page_table, int32_t num_tokens, int32_t num_pages,
+                      const int32_t* selected, const int32_t* selected_count, const int32_t* predicted,
+                      const int32_t* predicted_count, int32_t cap, int32_t chunk_pages,
+                      const float* part_o, const float* part_m, const float* part_l, const float* page_m,
+                      int32_t mode, float* out_o32, void* out_o, float* out_m, float* out_l,
+                      int32_t* missed_count, int32_t* wasted_count, void* workspace, size_t ws_bytes,
+                      hipStream_t stream);
+
+/* Merge n_states partial states per row (Eqs. (6)-(8) for arbitrary states).
+ *   o  device [n_states][rows][d] float32, m, l device [n_states][rows] float32
+ *   out_o device [rows][d], out_m, out_l device [rows]; d <= 1024; states with l = 0 are empty. */
+prr_status prr_merge_states(int32_t n_states, int32_t rows, int32_t d, const float* o, const float* m,
+                            const float* l, float* out_o, float* out_m, float* out_l, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PRR_H_ */

@@ -1,0 +1,187 @@
+"""ctypes binding of libprr.so: the C ABI of include/prr.h with the same names.
+
+Argument marshalling only: every step of the decode path runs in the HIP kernels of
+the shared library.  Pointer arguments accept a torch tensor (its data_ptr), a plain
+integer address, or None (NULL).  Every call raises PrrError when the library returns
+a status other than PRR_OK.  Importing this module fails loudly when the library has
+not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libprr.so")
+
+PRR_OK = 0
+PRR_ERR_INVALID_ARG = 1
+PRR_ERR_UNSUPPORTED = 2
+PRR_ERR_WORKSPACE = 3
+PRR_ERR_HIP = 4
+PRR_F16 = 0
+PRR_BF16 = 1
+PRR_META_MINMAX = 0
+PRR_META_MEAN = 1
+PRR_EXACT_SELECTED = 0
+PRR_KEEP_WASTED = 1
+PRR_MAX_PAGES = 16384
+PRR_MAX_CAP = 1024
+PRR_MAX_FORCED = 64
+
+# every function declared in include/prr.h
+EXPORTED = (
+    "prr_status_string", "prr_last_error", "prr_workspace_size", "prr_workspace_init",
+    "prr_spec_state_floats", "prr_build_page_meta", "prr_score_topk", "prr_predict",
+    "prr_spec_attn", "prr_repair", "prr_merge_states",
+)
+
+
+class PrrError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{status_string(status)}: {message}")
+        self.status = status
+
+
+class prr_dims(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32) for name in
+                ("num_q_heads", "num_kv_heads", "head_dim", "page_size", "max_pages", "dtype", "meta_kind")]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"libprr.so is not built ({LIB_PATH}); run __graft_entry__.build() first")
+_lib = ctypes.CDLL(LIB_PATH)
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int32
+_F = ctypes.c_float
+_S = ctypes.c_size_t
+_DIMS = ctypes.POINTER(prr_dims)
+
+_SIGS = {
+    "prr_status_string": (ctypes.c_char_p, [_I]),
+    "prr_last_error": (ctypes.c_char_p, []),
+    "prr_workspace_size": (_S, [_DIMS, _I, _I]),
+    "prr_workspace_init": (_I, [_P, _S, _P]),
+    "prr_spec_state_floats": (_S, [_DIMS, _I, _I, ctypes.POINTER(_S), ctypes.POINTER(_S), ctypes.POINTER(_S)]),
+    "prr_build_page_meta": (_I, [_DIMS, _P, _P, _I, _I, _I, _P, _P]),
+    "prr_score_topk": (_I, [_DIMS, _P, _P, _I, _I, _P, _I, _I, _P, _P, _P, _I, _P, _S, _P]),
+    "prr_predict": (_I, [_DIMS, _P, _P, _P, _P, _I, _F, _F, _F, _I, _P, _I, _I, _P, _P, _I, _P]),
+    "prr_spec_attn": (_I, [_DIMS, _P, _P, _P, _P, _I, _P, _P, _I, _I, _P, _P, _P, _P, _P]),
+    "prr_repair": (_I, [_DIMS, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _I,
+                        _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "prr_merge_states": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _P]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+
+def status_string(status: int) -> str:
+    return _lib.prr_status_string(status).decode()
+
+
+def last_error() -> str:
+    return _lib.prr_last_error().decode()
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        if torch.cuda.is_available():
+            return torch.cuda.current_stream().cuda_stream
+        return None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status: int):
+    if status != PRR_OK:
+        raise PrrError(status, last_error())
+
+
+def _forced(forced: Optional[Sequence[int]]):
+    if not forced:
+        return None, 0
+    arr = (ctypes.c_int32 * len(forced))(*[int(x) for x in forced])
+    return arr, len(forced)
+
+
+def make_dims(num_q_heads, num_kv_heads, page_size, max_pages, dtype, meta_kind=PRR_META_MINMAX, head_dim=128):
+    return prr_dims(num_q_heads, num_kv_heads, head_dim, page_size, max_pages, dtype, meta_kind)
+
+
+def prr_workspace_size(dims: prr_dims, cap: int, chunk_pages: int) -> int:
+    return int(_lib.prr_workspace_size(ctypes.byref(dims), cap, chunk_pages))
+
+
+def prr_workspace_init(workspace, nbytes: int, stream=None):
+    _check(_lib.prr_workspace_init(_ptr(workspace), nbytes, _stream(stream)))
+
+
+def prr_spec_state_floats(dims: prr_dims, cap: int, chunk_pages: int):
+    po, pml, pm = _S(), _S(), _S()
+    total = _lib.prr_spec_state_floats(ctypes.byref(dims), cap, chunk_pages, ctypes.byref(po), ctypes.byref(pml),
+                                       ctypes.byref(pm))
+    return int(total), int(po.value), int(pml.value), int(pm.value)
+
+
+def prr_build_page_meta(dims, k_cache, page_table, num_tokens, page_begin, page_end, meta, stream=None):
+    _check(_lib.prr_build_page_meta(ctypes.byref(dims), _ptr(k_cache), _ptr(page_table), num_tokens, page_begin,
+                                    page_end, _ptr(meta), _stream(stream)))
+
+
+def prr_score_topk(dims, q, meta, num_pages, k_select, forced, forced_in_budget, scores, selected, selected_count,
+                   cap, workspace, ws_bytes, stream=None):
+    farr, nf = _forced(forced)
+    _check(_lib.prr_score_topk(ctypes.byref(dims), _ptr(q), _ptr(meta), num_pages, k_select,
+                               ctypes.cast(farr, _P) if farr is not None else None, nf, int(bool(forced_in_budget)),
+                               _ptr(scores), _ptr(selected), _ptr(selected_count), cap, _ptr(workspace), ws_bytes,
+                               _stream(stream)))
+
+
+def prr_predict(dims, ema_level, ema_trend, ema_init_bits, scores, num_pages, alpha, beta, gamma, p_select, forced,
+                forced_in_budget, predicted, predicted_count, cap, stream=None):
+    farr, nf = _forced(forced)
+    _check(_lib.prr_predict(ctypes.byref(dims), _ptr(ema_level), _ptr(ema_trend), _ptr(ema_init_bits), _ptr(scores),
+                            num_pages, alpha, beta, gamma, p_select,
+                            ctypes.cast(farr, _P) if farr is not None else None, nf, int(bool(forced_in_budget)),
+                            _ptr(predicted), _ptr(predicted_count), cap, _stream(stream)))
+
+
+def prr_spec_attn(dims, q, k_cache, v_cache, page_table, num_tokens, pages, page_count, cap, chunk_pages, part_o,
+                  part_m, part_l, page_m, stream=None):
+    _check(_lib.prr_spec_attn(ctypes.byref(dims), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table), num_tokens,
+                              _ptr(pages), _ptr(page_count), cap, chunk_pages, _ptr(part_o), _ptr(part_m),
+                              _ptr(part_l), _ptr(page_m), _stream(stream)))
+
+
+def prr_repair(dims, q, k_cache, v_cache, page_table, num_tokens, num_pages, selected, selected_count, predicted,
+               predicted_count, cap, chunk_pages, part_o, part_m, part_l, page_m, mode, out_o32, out_o, out_m, out_l,
+               missed_count, wasted_count, workspace, ws_bytes, stream=None):
+    _check(_lib.prr_repair(ctypes.byref(dims), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table), num_tokens,
+                           num_pages, _ptr(selected), _ptr(selected_count), _ptr(predicted), _ptr(predicted_count),
+                           cap, chunk_pages, _ptr(part_o), _ptr(part_m), _ptr(part_l), _ptr(page_m), mode,
+                           _ptr(out_o32), _ptr(out_o), _ptr(out_m), _ptr(out_l), _ptr(missed_count),
+                           _ptr(wasted_count), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def prr_merge_states(n_states, rows, d, o, m, l, out_o, out_m, out_l, stream=None):
+    _check(_lib.prr_merge_states(n_states, rows, d, _ptr(o), _ptr(m), _ptr(l), _ptr(out_o), _ptr(out_m), _ptr(out_l),
+                                 _stream(stream)))
+
+
+def library():
+    """The loaded ctypes.CDLL (for symbol checks)."""
+    return _lib

@@ -1,0 +1,410 @@
+// C ABI of libprr: argument validation, workspace carving, dispatch to the launchers.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "prr.h"
+#include "prr_launch.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+prr_status fail(prr_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+prr_status ok() {
+  g_last_error[0] = '\0';
+  return PRR_OK;
+}
+
+prr_status hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(PRR_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int div_up(int a, int b) { return (a + b - 1) / b; }
+
+prr_status check_dims(const prr_dims* d) {
+  if (!d) return fail(PRR_ERR_INVALID_ARG, "dims is NULL");
+  if (d->head_dim != 128) return fail(PRR_ERR_UNSUPPORTED, "head_dim %d: only 128 is compiled", d->head_dim);
+  if (d->page_size != 16 && d->page_size != 64)
+    return fail(PRR_ERR_UNSUPPORTED, "page_size %d: only 16 and 64 are compiled", d->page_size);
+  if (d->num_kv_heads < 1) return fail(PRR_ERR_INVALID_ARG, "num_kv_heads %d < 1", d->num_kv_heads);
+  if (d->num_q_heads < 1 || d->num_q_heads % d->num_kv_heads != 0)
+    return fail(PRR_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d", d->num_q_heads,
+                d->num_kv_heads);
+  const int g = d->num_q_heads / d->num_kv_heads;
+  if (g > 16) return fail(PRR_ERR_UNSUPPORTED, "group size %d > 16", g);
+  if (d->max_pages < 1) return fail(PRR_ERR_INVALID_ARG, "max_pages %d < 1", d->max_pages);
+  if (d->dtype != PRR_F16 && d->dtype != PRR_BF16) return fail(PRR_ERR_INVALID_ARG, "dtype %d", d->dtype);
+  if (d->meta_kind != PRR_META_MINMAX && d->meta_kind != PRR_META_MEAN)
+    return fail(PRR_ERR_INVALID_ARG, "meta_kind %d", d->meta_kind);
+  return ok();
+}
+
+prr_status check_ptr(const void* p, const char* name, size_t align) {
+  if (!p) return fail(PRR_ERR_INVALID_ARG, "%s is NULL", name);
+  if (!aligned(p, align)) return fail(PRR_ERR_INVALID_ARG, "%s is not %zu-byte aligned", name, align);
+  return ok();
+}
+
+#define PRR_TRY(expr)              \
+  do {                             \
+    const prr_status _s = (expr);  \
+    if (_s != PRR_OK) return _s;   \
+  } while (0)
+
+struct WsLayout {
+  size_t flags, sel_cnt, rep_cnt, rep_o, rep_ml, total;
+  int nchunks, nwork_max;
+};
+
+bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
+  if (check_dims(d) != PRR_OK || cap < 1 || cap > PRR_MAX_CAP || chunk < 1 || chunk > 16) return false;
+  const int hkv = d->num_kv_heads, g = d->num_q_heads / d->num_kv_heads;
+  L.nchunks = div_up(cap, chunk);
+  L.nwork_max = 2 * L.nchunks;
+  size_t off = 0;
+  L.flags = off;
+  off += 256;
+  L.sel_cnt = off;
+  off = align_up(off + (size_t)hkv * 4, 256);
+  L.rep_cnt = off;
+  off = align_up(off + (size_t)2 * hkv * 4, 256);
+  L.rep_o = off;
+  off = align_up(off + (size_t)hkv * L.nwork_max * g * 128 * 4, 256);
+  L.rep_ml = off;
+  off = align_up(off + (size_t)hkv * L.nwork_max * g * 2 * 4, 256);
+  L.total = off;
+  return true;
+}
+
+prr_status check_forced(const int32_t* forced, int n_forced, int num_pages) {
+  if (n_forced < 0 || n_forced > PRR_MAX_FORCED)
+    return fail(PRR_ERR_INVALID_ARG, "n_forced %d outside [0, %d]", n_forced, PRR_MAX_FORCED);
+  if (n_forced > 0 && !forced) return fail(PRR_ERR_INVALID_ARG, "forced is NULL with n_forced %d", n_forced);
+  for (int i = 0; i < n_forced; ++i) {
+    if (forced[i] < 0 || forced[i] >= num_pages)
+      return fail(PRR_ERR_INVALID_ARG, "forced[%d] = %d outside [0, %d)", i, forced[i], num_pages);
+    for (int j = 0; j < i; ++j)
+      if (forced[j] == forced[i]) return fail(PRR_ERR_INVALID_ARG, "forced page %d listed twice", forced[i]);
+  }
+  return ok();
+}
+
+// |A| for a budget and forced set, and the number of non-forced pages to pick.
+void budget(int k_select, int n_forced, int forced_in_budget, int num_pages, int& total, int& kextra) {
+  kextra = forced_in_budget ? std::max(0, k_select - n_forced) : k_select;
+  total = std::min(num_pages, n_forced + kextra);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* prr_status_string(prr_status s) {
+  switch (s) {
+    case PRR_OK: return "PRR_OK";
+    case PRR_ERR_INVALID_ARG: return "PRR_ERR_INVALID_ARG";
+    case PRR_ERR_UNSUPPORTED: return "PRR_ERR_UNSUPPORTED";
+    case PRR_ERR_WORKSPACE: return "PRR_ERR_WORKSPACE";
+    case PRR_ERR_HIP: return "PRR_ERR_HIP";
+    default: return "PRR_ERR_UNKNOWN";
+  }
+}
+
+const char* prr_last_error(void) { return g_last_error; }
+
+size_t prr_workspace_size(const prr_dims* dims, int32_t cap, int32_t chunk_pages) {
+  WsLayout L;
+  if (!ws_layout(dims, cap, chunk_pages, L)) return 0;
+  return L.total;
+}
+
+prr_status prr_workspace_init(void* workspace, size_t bytes, hipStream_t stream) {
+  PRR_TRY(check_ptr(workspace, "workspace", 256));
+  if (bytes % 16 != 0) return fail(PRR_ERR_WORKSPACE, "workspace size %zu is not a multiple of 16", bytes);
+  return hip_status(prr::launch_fill_zero(workspace, bytes, stream), "workspace fill");
+}
+
+size_t prr_spec_state_floats(const prr_dims* dims, int32_t cap, int32_t chunk_pages, size_t* part_o_floats,
+                             size_t* part_ml_floats, size_t* page_m_floats) {
+  if (check_dims(dims) != PRR_OK || cap < 1 || cap > PRR_MAX_CAP || chunk_pages < 1 || chunk_pages > 16) return 0;
+  const size_t hkv = dims->num_kv_heads, g = dims->num_q_heads / dims->num_kv_heads;
+  const size_t nch = (size_t)div_up(cap, chunk_pages);
+  const size_t po = hkv * nch * g * 128, pml = hkv * nch * g, pm = hkv * (size_t)cap * g;
+  if (part_o_floats) *part_o_floats = po;
+  if (part_ml_floats) *part_ml_floats = pml;
+  if (page_m_floats) *page_m_floats = pm;
+  return po + 2 * pml + pm;
+}
+
+prr_status prr_build_page_meta(const prr_dims* dims, const void* k_cache, const int32_t* page_table,
+                               int32_t num_tokens, int32_t page_begin, int32_t page_end, void* meta,
+                               hipStream_t stream) {
+  PRR_TRY(check_dims(dims));
+  PRR_TRY(check_ptr(k_cache, "k_cache", 16));
+  PRR_TRY(check_ptr(meta, "meta", 16));
+  if (page_table && !aligned(page_table, 4)) return fail(PRR_ERR_INVALID_ARG, "page_table misaligned");
+  if (num_tokens < 1 || (int64_t)num_tokens > (int64_t)dims->max_pages * dims->page_size)
+    return fail(PRR_ERR_INVALID_ARG, "num_tokens %d outside [1, max_pages*page_size]", num_tokens);
+  const int npages = div_up(num_tokens, dims->page_size);
+  if (page_begin < 0 || page_end > npages || page_begin > page_end)
+    return fail(PRR_ERR_INVALID_ARG, "page range [%d, %d) outside [0, %d]", page_begin, page_end, npages);
+  prr::MetaLaunch a;
+  a.k_cache = k_cache;
+  a.page_table = page_table;
+  a.meta = meta;
+  a.num_kv_heads = dims->num_kv_heads;
+  a.max_pages = dims->max_pages;
+  a.page_size = dims->page_size;
+  a.num_tokens = num_tokens;
+  a.page_begin = page_begin;
+  a.page_end = page_end;
+  a.bf16 = dims->dtype == PRR_BF16;
+  a.meta_mean = dims->meta_kind == PRR_META_MEAN;
+  return hip_status(prr::launch_meta(a, stream), "build_page_meta launch");
+}
+
+prr_status prr_score_topk(const prr_dims* dims, const void* q, const void* meta, int32_t num_pages, int32_t k_select,
+                          const int32_t* forced, int32_t n_forced, int32_t forced_in_budget, float* scores,
+                          int32_t* selected, int32_t* selected_count, int32_t cap, void* workspace, size_t ws_bytes,
+                          hipStream_t stream) {
+  PRR_TRY(check_dims(dims));
+  PRR_TRY(check_ptr(q, "q", 16));
+  PRR_TRY(check_ptr(meta, "meta", 16));
+  PRR_TRY(check_ptr(scores, "scores", 4));
+  PRR_TRY(check_ptr(selected, "selected", 4));
+  PRR_TRY(check_ptr(selected_count, "selected_count", 4));
+  if (num_pages < 1 || num_pages > PRR_MAX_PAGES || num_pages > dims->max_pages)
+    return fail(PRR_ERR_INVALID_ARG, "num_pages %d outside [1, min(max_pages, %d)]", num_pages, PRR_MAX_PAGES);
+  if (k_select < 0) return fail(PRR_ERR_INVALID_ARG, "k_select %d < 0", k_select);
+  PRR_TRY(check_forced(forced, n_forced, num_pages));
+  if (cap < 1 || cap > PRR_MAX_CAP) return fail(PRR_ERR_INVALID_ARG, "cap %d outside [1, %d]", cap, PRR_MAX_CAP);
+  int total, kextra;
+  budget(k_select, n_forced, forced_in_budget, num_pages, total, kextra);
+  if (total > cap) return fail(PRR_ERR_INVALID_ARG, "|A| = %d exceeds cap %d", total, cap);
+  PRR_TRY(check_ptr(workspace, "workspace", 256));
+  WsLayout L;
+  if (!ws_layout(dims, cap, 1, L) || ws_bytes < L.rep_cnt)
+    return fail(PRR_ERR_WORKSPACE, "workspace of %zu bytes too small", ws_bytes);
+  prr::ScoreLaunch a;
+  memset(&a, 0, sizeof(a));
+  a.q = q;
+  a.meta = meta;
+  a.scores = scores;
+  a.selected = selected;
+  a.selected_count = selected_count;
+  a.counters = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + L.sel_cnt);
+  a.num_kv_heads = dims->num_kv_heads;
+  a.group = dims->num_q_heads / dims->num_kv_heads;
+  a.max_pages = dims->max_pages;
+  a.num_pages = num_pages;
+  a.kextra = kextra;
+  a.cap = cap;
+  a.n_forced = n_forced;
+  a.bf16 = dims->dtype == PRR_BF16;
+  a.meta_mean = dims->meta_kind == PRR_META_MEAN;
+  for (int i = 0; i < n_forced; ++i) a.forced[i] = forced[i];
+  return hip_status(prr::launch_score_topk(a, stream), "score_topk launch");
+}
+
+prr_status prr_predict(const prr_dims* dims, float* ema_level, float* ema_trend, uint32_t* ema_init_bits,
+                       const float* scores, int32_t num_pages, float alpha, float beta, float gamma, int32_t p_select,
+                       const int32_t* forced, int32_t n_forced, int32_t forced_in_budget, int32_t* predicted,
+                       int32_t* predicted_count, int32_t cap, hipStream_t stream) {
+  PRR_TRY(check_dims(dims));
+  PRR_TRY(check_ptr(ema_level, "ema_level", 4));
+  PRR_TRY(check_ptr(ema_trend, "ema_trend", 4));
+  PRR_TRY(check_ptr(ema_init_bits, "ema_init_bits", 4));
+  if (scores && !aligned(scores, 4)) return fail(PRR_ERR_INVALID_ARG, "scores misaligned");
+  PRR_TRY(check_ptr(predicted, "predicted", 4));
+  PRR_TRY(check_ptr(predicted_count, "predicted_count", 4));
+  if (num_pages < 1 || num_pages > PRR_MAX_PAGES || num_pages > dims->max_pages)
+    return fail(PRR_ERR_INVALID_ARG, "num_pages %d outside [1, min(max_pages, %d)]", num_pages, PRR_MAX_PAGES);
+  if (!(alpha > 0.f && alpha <= 1.f) || !(beta > 0.f && beta <= 1.f) || !(gamma >= 0.f && gamma <= 1.f))
+    return fail(PRR_ERR_INVALID_ARG, "alpha %g, beta %g, gamma %g outside (0,1], (0,1], [0,1]", alpha, beta, gamma);
+  if (p_select < 0) return fail(PRR_ERR_INVALID_ARG, "p_select %d < 0", p_select);
+  PRR_TRY(check_forced(forced, n_forced, num_pages));
+  if (cap < 1 || cap > PRR_MAX_CAP) return fail(PRR_ERR_INVALID_ARG, "cap %d outside [1, %d]", cap, PRR_MAX_CAP);
+  int total, kextra;
+  budget(p_select, n_forced, forced_in_budget, num_pages, total, kextra);
+  if (total > cap) return fail(PRR_ERR_INVALID_ARG, "|P| = %d exceeds cap %d", total, cap);
+  prr::PredictLaunch a;
+  memset(&a, 0, sizeof(a));
+  a.level = ema_level;
+  a.trend = ema_trend;
+  a.init_bits = ema_init_bits;
+  a.scores = scores;
+  a.predicted = predicted;
+  a.predicted_count = predicted_count;
+  a.alpha = alpha;
+  a.beta = beta;
+  a.gamma = gamma;
+  a.num_kv_heads = dims->num_kv_heads;
+  a.max_pages = dims->max_pages;
+  a.num_pages = num_pages;
+  a.kextra = kextra;
+  a.cap = cap;
+  a.n_forced = n_forced;
+  for (int i = 0; i < n_forced; ++i) a.forced[i] = forced[i];
+  return hip_status(prr::launch_predict(a, stream), "predict launch");
+}
+
+prr_status prr_spec_attn(const prr_dims* dims, const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* page_table, int32_t num_tokens, const int32_t* pages,
+                         const int32_t* page_count, int32_t cap, int32_t chunk_pages, float* part_o, float* part_m,
+                         float* part_l, float* page_m, hipStream_t stream) {
+  PRR_TRY(check_dims(dims));
+  PRR_TRY(check_ptr(q, "q", 16));
+  PRR_TRY(check_ptr(k_cache, "k_cache", 16));
+  PRR_TRY(check_ptr(v_cache, "v_cache", 16));
+  PRR_TRY(check_ptr(pages, "pages", 4));
+  PRR_TRY(check_ptr(page_count, "page_count", 4));
+  PRR_TRY(check_ptr(part_o, "part_o", 16));
+  PRR_TRY(check_ptr(part_m, "part_m", 4));
+  PRR_TRY(check_ptr(part_l, "part_l", 4));
+  if (page_m && !aligned(page_m, 4)) return fail(PRR_ERR_INVALID_ARG, "page_m misaligned");
+  if (page_table && !aligned(page_table, 4)) return fail(PRR_ERR_INVALID_ARG, "page_table misaligned");
+  if (num_tokens < 1 || (int64_t)num_tokens > (int64_t)dims->max_pages * dims->page_size)
+    return fail(PRR_ERR_INVALID_ARG, "num_tokens %d outside [1, max_pages*page_size]", num_tokens);
+  if (cap < 1 || cap > PRR_MAX_CAP) return fail(PRR_ERR_INVALID_ARG, "cap %d outside [1, %d]", cap, PRR_MAX_CAP);
+  if (chunk_pages < 1 || chunk_pages > 16) return fail(PRR_ERR_INVALID_ARG, "chunk_pages %d outside [1, 16]", chunk_pages);
+  prr::SpecLaunch a;
+  memset(&a, 0, sizeof(a));
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.page_table = page_table;
+  a.pages = pages;
+  a.page_count = page_count;
+  a.part_o = part_o;
+  a.part_m = part_m;
+  a.part_l = part_l;
+  a.page_m = page_m;
+  a.num_kv_heads = dims->num_kv_heads;
+  a.group = dims->num_q_heads / dims->num_kv_heads;
+  a.max_pages = dims->max_pages;
+  a.num_pages = div_up(num_tokens, dims->page_size);
+  a.num_tokens = num_tokens;
+  a.page_size = dims->page_size;
+  a.cap = cap;
+  a.chunk = chunk_pages;
+  a.nchunks = div_up(cap, chunk_pages);
+  a.bf16 = dims->dtype == PRR_BF16;
+  return hip_status(prr::launch_spec_attn(a, stream), "spec_attn launch");
+}
+
+prr_status prr_repair(const prr_dims* dims, const void* q, const void* k_cache, const void* v_cache,
+                      const int32_t* page_table, int32_t num_tokens, int32_t num_pages, const int32_t* selected,
+                      const int32_t* selected_count, const int32_t* predicted, const int32_t* predicted_count,
+                      int32_t cap, int32_t chunk_pages, const float* part_o, const float* part_m, const float* part_l,
+                      const float* page_m, int32_t mode, float* out_o32, void* out_o, float* out_m, float* out_l,
+                      int32_t* missed_count, int32_t* wasted_count, void* workspace, size_t ws_bytes,
+                      hipStream_t stream) {
+  PRR_TRY(check_dims(dims));
+  PRR_TRY(check_ptr(q, "q", 16));
+  PRR_TRY(check_ptr(k_cache, "k_cache", 16));
+  PRR_TRY(check_ptr(v_cache, "v_cache", 16));
+  PRR_TRY(check_ptr(selected, "selected", 4));
+  PRR_TRY(check_ptr(selected_count, "selected_count", 4));
+  if ((predicted == nullptr) != (predicted_count == nullptr))
+    return fail(PRR_ERR_INVALID_ARG, "predicted and predicted_count must both be set or both be NULL");
+  if (predicted) {
+    PRR_TRY(check_ptr(predicted, "predicted", 4));
+    PRR_TRY(check_ptr(predicted_count, "predicted_count", 4));
+    PRR_TRY(check_ptr(part_o, "part_o", 16));
+    PRR_TRY(check_ptr(part_m, "part_m", 4));
+    PRR_TRY(check_ptr(part_l, "part_l", 4));
+    if (page_m && !aligned(page_m, 4)) return fail(PRR_ERR_INVALID_ARG, "page_m misaligned");
+  }
+  PRR_TRY(check_ptr(out_o32, "out_o32", 4));
+  if (out_o && !aligned(out_o, 2)) return fail(PRR_ERR_INVALID_ARG, "out_o misaligned");
+  PRR_TRY(check_ptr(out_m, "out_m", 4));
+  PRR_TRY(check_ptr(out_l, "out_l", 4));
+  if (page_table && !aligned(page_table, 4)) return fail(PRR_ERR_INVALID_ARG, "page_table misaligned");
+  if (mode != PRR_EXACT_SELECTED && mode != PRR_KEEP_WASTED) return fail(PRR_ERR_INVALID_ARG, "mode %d", mode);
+  if (num_tokens < 1 || (int64_t)num_tokens > (int64_t)dims->max_pages * dims->page_size)
+    return fail(PRR_ERR_INVALID_ARG, "num_tokens %d outside [1, max_pages*page_size]", num_tokens);
+  const int npages_tok = div_up(num_tokens, dims->page_size);
+  if (num_pages < 1 || num_pages > npages_tok || num_pages > PRR_MAX_PAGES)
+    return fail(PRR_ERR_INVALID_ARG, "num_pages %d outside [1, min(ceil(num_tokens/page_size), %d)]", num_pages,
+                PRR_MAX_PAGES);
+  if (cap < 1 || cap > PRR_MAX_CAP) return fail(PRR_ERR_INVALID_ARG, "cap %d outside [1, %d]", cap, PRR_MAX_CAP);
+  if (chunk_pages < 1 || chunk_pages > 16) return fail(PRR_ERR_INVALID_ARG, "chunk_pages %d outside [1, 16]", chunk_pages);
+  PRR_TRY(check_ptr(workspace, "workspace", 256));
+  WsLayout L;
+  if (!ws_layout(dims, cap, chunk_pages, L) || ws_bytes < L.total)
+    return fail(PRR_ERR_WORKSPACE, "workspace of %zu bytes too small (need %zu)", ws_bytes,
+                ws_layout(dims, cap, chunk_pages, L) ? L.total : (size_t)0);
+  const int g = dims->num_q_heads / dims->num_kv_heads;
+  prr::RepairLaunch a;
+  memset(&a, 0, sizeof(a));
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.page_table = page_table;
+  a.selected = selected;
+  a.selected_count = selected_count;
+  a.predicted = predicted;
+  a.predicted_count = predicted_count;
+  a.part_o = part_o;
+  a.part_m = part_m;
+  a.part_l = part_l;
+  a.page_m = predicted ? page_m : nullptr;
+  a.out_o32 = out_o32;
+  a.out_o = out_o;
+  a.out_m = out_m;
+  a.out_l = out_l;
+  a.missed_count = missed_count;
+  a.wasted_count = wasted_count;
+  char* ws = static_cast<char*>(workspace);
+  a.ws_o = reinterpret_cast<float*>(ws + L.rep_o);
+  a.ws_ml = reinterpret_cast<float*>(ws + L.rep_ml);
+  a.ws_cnt = reinterpret_cast<uint32_t*>(ws + L.rep_cnt);
+  a.flags = reinterpret_cast<uint32_t*>(ws + L.flags);
+  a.num_kv_heads = dims->num_kv_heads;
+  a.group = g;
+  a.max_pages = dims->max_pages;
+  a.num_pages = num_pages;
+  a.num_tokens = num_tokens;
+  a.page_size = dims->page_size;
+  a.cap = cap;
+  a.chunk = chunk_pages;
+  a.nchunks = L.nchunks;
+  a.nwork = (predicted && mode == PRR_EXACT_SELECTED) ? 2 * L.nchunks : L.nchunks;
+  a.nmerge_per_kv = div_up(g, 2);
+  a.mode = mode;
+  a.bf16 = dims->dtype == PRR_BF16;
+  return hip_status(prr::launch_repair(a, stream), "repair launch");
+}
+
+prr_status prr_merge_states(int32_t n_states, int32_t rows, int32_t d, const float* o, const float* m, const float* l,
+                            float* out_o, float* out_m, float* out_l, hipStream_t stream) {
+  if (n_states < 0 || rows < 1 || d < 1 || d > 1024)
+    return fail(PRR_ERR_INVALID_ARG, "n_states %d, rows %d, d %d", n_states, rows, d);
+  if (n_states > 0) {
+    PRR_TRY(check_ptr(o, "o", 4));
+    PRR_TRY(check_ptr(m, "m", 4));
+    PRR_TRY(check_ptr(l, "l", 4));
+  }
+  PRR_TRY(check_ptr(out_o, "out_o", 4));
+  PRR_TRY(check_ptr(out_m, "out_m", 4));
+  PRR_TRY(check_ptr(out_l, "out_l", 4));
+  return hip_status(prr::launch_merge_states(n_states, rows, d, o, m, l, out_o, out_m, out_l, stream),
+                    "merge_states launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,160 @@
+// Device-side helpers shared by the gfx950 kernels: 16-bit storage conversions,
+// order-preserving score keys, wave64 reductions and scans, block scans.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace prr {
+
+constexpr int kHeadDim = 128;
+constexpr int kWave = 64;
+constexpr float kLog2e = 1.4426950408889634f;
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+
+// ------------------------------------------------------------------ 16-bit storage
+
+template <bool BF16>
+__device__ __forceinline__ float h2f(uint32_t bits16) {
+  if constexpr (BF16) {
+    return __uint_as_float(bits16 << 16);
+  } else {
+    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
+  }
+}
+
+// Exact conversion back to storage for values that came from storage (min / max).
+template <bool BF16>
+__device__ __forceinline__ uint32_t f2h_exact(float f) {
+  if constexpr (BF16) {
+    return __float_as_uint(f) >> 16;
+  } else {
+    return __builtin_bit_cast(uint16_t, static_cast<_Float16>(f));
+  }
+}
+
+// Round-to-nearest-even conversion of an arbitrary float to storage.
+template <bool BF16>
+__device__ __forceinline__ uint32_t f2h_rne(float f) {
+  if constexpr (BF16) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;  // quiet NaN
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+  } else {
+    return __builtin_bit_cast(uint16_t, static_cast<_Float16>(f));
+  }
+}
+
+// Element e (0..7) of eight 16-bit values packed in a uint4.
+template <bool BF16>
+__device__ __forceinline__ float u4_elem(const uint4& v, int e) {
+  const uint32_t w = (e < 2) ? v.x : (e < 4) ? v.y : (e < 6) ? v.z : v.w;
+  return h2f<BF16>((e & 1) ? (w >> 16) : (w & 0xffffu));
+}
+
+// ------------------------------------------------------------------ score keys
+
+// Order-preserving map of a float to uint32 (larger float -> larger key); -0 and +0
+// map to the same key, so equal scores tie and fall back to the page index.
+__device__ __forceinline__ uint32_t score_key(float f) {
+  if (f == 0.0f) f = 0.0f;
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// ------------------------------------------------------------------ wave64 helpers
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+__device__ __forceinline__ int lanes_below(uint64_t mask) {
+  const int lane = lane_id();
+  return __popcll(mask & ((1ull << lane) - 1ull));
+}
+
+__device__ __forceinline__ float wave_max16(float v) {  // over lanes l, l^1, .., l^8
+  v = fmaxf(v, __shfl_xor(v, 8));
+  v = fmaxf(v, __shfl_xor(v, 4));
+  v = fmaxf(v, __shfl_xor(v, 2));
+  v = fmaxf(v, __shfl_xor(v, 1));
+  return v;
+}
+
+__device__ __forceinline__ float sum16(float v) {  // butterfly: identical result in all 16 lanes
+  v += __shfl_xor(v, 8);
+  v += __shfl_xor(v, 4);
+  v += __shfl_xor(v, 2);
+  v += __shfl_xor(v, 1);
+  return v;
+}
+
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// Block-wide exclusive scan of one int per thread; `wave_tot` needs NT/64 ints of LDS.
+// Returns the exclusive prefix; `total` receives the sum over the block.
+template <int NT>
+__device__ __forceinline__ int block_exclusive_scan(int v, int* wave_tot, int& total) {
+  constexpr int NW = NT / kWave;
+  const int w = threadIdx.x / kWave;
+  const int inc = wave_inclusive_scan(v);
+  if (lane_id() == kWave - 1) wave_tot[w] = inc;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const int s = wave_tot[i];
+    base += (i < w) ? s : 0;
+    tot += s;
+  }
+  __syncthreads();
+  total = tot;
+  return base + inc - v;
+}
+
+template <int NT>
+__device__ __forceinline__ int block_sum(int v, int* wave_tot) {
+  int total;
+  block_exclusive_scan<NT>(v, wave_tot, total);
+  return total;
+}
+
+template <int NT>
+__device__ __forceinline__ void block_minmax_u32(uint32_t& lo, uint32_t& hi, uint32_t* scratch) {
+  constexpr int NW = NT / kWave;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    lo = min(lo, (uint32_t)__shfl_xor((int)lo, o));
+    hi = max(hi, (uint32_t)__shfl_xor((int)hi, o));
+  }
+  const int w = threadIdx.x / kWave;
+  if (lane_id() == 0) {
+    scratch[w] = lo;
+    scratch[NW + w] = hi;
+  }
+  __syncthreads();
+  lo = 0xffffffffu;
+  hi = 0u;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    lo = min(lo, scratch[i]);
+    hi = max(hi, scratch[NW + i]);
+  }
+  __syncthreads();
+}
+
+// Sticky error bits written by kernels into the workspace flag word.
+constexpr uint32_t kFlagBadListEntry = 1u;
+constexpr uint32_t kFlagSpinTimeout = 2u;
+
+}  // namespace prr

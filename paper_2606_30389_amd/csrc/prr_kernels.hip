@@ -1,0 +1,1201 @@
+// gfx950 (CDNA4) kernels of the speculate-reuse-repair decode path.
+//
+//   meta_minmax / meta_mean   page metadata (Appendix A.1; block means)
+//   score_topk                GQA criticality of every page + top-K select, one launch:
+//                             every workgroup scores a slice of pages, the last one to
+//                             finish (per KV head) selects in LDS
+//   predict                   EMA update and prediction (Section 4.1, Eqs. (2)-(3)) + top-|P|
+//   spec_attn                 split-K flash-decode over a page list (Section 4.3)
+//   repair                    set difference, missed / unmerge work units, merge
+//                             (Section 4.3, Eqs. (6)-(8)), one launch
+//   merge_states              stand-alone merge of partial states
+//
+// Wave64 throughout.  Attention uses MFMA: q.k^T as 16x16x32 bf16/f16 tiles (16 tokens x
+// 16 query heads, contraction over the 128 channels), p.V as 16x16x4 fp32 tiles so that
+// the softmax weights stay in fp32.
+#include <map>
+#include <mutex>
+
+#include "prr_device.h"
+#include "prr_launch.h"
+
+namespace prr {
+
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
+
+// =====================================================================================
+// workspace fill
+// =====================================================================================
+
+__global__ void fill_zero_kernel(u32x4_t* __restrict__ p, size_t n16) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) p[i] = u32x4_t{0, 0, 0, 0};
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream) {
+  const size_t n16 = bytes / 16;
+  if (n16 == 0) return hipSuccess;
+  size_t nb = (n16 + 255) / 256;
+  const unsigned grid = (unsigned)(nb < 1024 ? nb : 1024);
+  u32x4_t* ptr = reinterpret_cast<u32x4_t*>(p);
+  size_t n = n16;
+  void* args[] = {&ptr, &n};
+  return hipLaunchKernel((const void*)fill_zero_kernel, dim3(grid), dim3(256), args, 0, stream);
+}
+
+// =====================================================================================
+// page metadata
+// =====================================================================================
+// One wave per page.  Lane l covers channels 8*(l%16) .. +8 of token rows l/16, l/16+4, ..
+// (16-byte loads, a wave load covers 4 full rows); the four row groups are combined with
+// cross-lane shuffles.
+
+template <bool BF16, int PS>
+__global__ __launch_bounds__(256) void meta_minmax_kernel(const uint16_t* __restrict__ k, const int32_t* __restrict__ ptab,
+                                                          int num_tokens, int page_begin, int page_end, int max_pages,
+                                                          uint16_t* __restrict__ meta) {
+  const int h = blockIdx.y;
+  const int lane = lane_id(), w = threadIdx.x / kWave;
+  const int page = page_begin + blockIdx.x * 4 + w;
+  if (page >= page_end) return;
+  const int phys = ptab ? ptab[page] : page;
+  if (phys < 0 || phys >= max_pages) return;
+  const int cg = lane & 15, rg = lane >> 4;
+  const int valid = min(PS, num_tokens - page * PS);
+  const uint16_t* src = k + ((size_t)h * max_pages + phys) * PS * kHeadDim + cg * 8;
+  float mn[8], mx[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    mn[e] = __builtin_inff();
+    mx[e] = -__builtin_inff();
+  }
+#pragma unroll
+  for (int r0 = 0; r0 < PS; r0 += 4) {
+    const int r = r0 + rg;
+    if (r < valid) {
+      const uint4 v = *reinterpret_cast<const uint4*>(src + (size_t)r * kHeadDim);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float f = u4_elem<BF16>(v, e);
+        mn[e] = fminf(mn[e], f);
+        mx[e] = fmaxf(mx[e], f);
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    mn[e] = fminf(mn[e], __shfl_xor(mn[e], 16));
+    mn[e] = fminf(mn[e], __shfl_xor(mn[e], 32));
+    mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 16));
+    mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 32));
+  }
+  if (rg < 2) {
+    const float* v = rg == 0 ? mn : mx;
+    uint4 o;
+    o.x = f2h_exact<BF16>(v[0]) | (f2h_exact<BF16>(v[1]) << 16);
+    o.y = f2h_exact<BF16>(v[2]) | (f2h_exact<BF16>(v[3]) << 16);
+    o.z = f2h_exact<BF16>(v[4]) | (f2h_exact<BF16>(v[5]) << 16);
+    o.w = f2h_exact<BF16>(v[6]) | (f2h_exact<BF16>(v[7]) << 16);
+    *reinterpret_cast<uint4*>(meta + (((size_t)h * max_pages + page) * 2 + rg) * kHeadDim + cg * 8) = o;
+  }
+}
+
+template <bool BF16, int PS>
+__global__ __launch_bounds__(256) void meta_mean_kernel(const uint16_t* __restrict__ k, const int32_t* __restrict__ ptab,
+                                                        int num_tokens, int page_begin, int page_end, int max_pages,
+                                                        float* __restrict__ meta) {
+  const int h = blockIdx.y;
+  const int lane = lane_id(), w = threadIdx.x / kWave;
+  const int page = page_begin + blockIdx.x * 4 + w;
+  if (page >= page_end) return;
+  const int phys = ptab ? ptab[page] : page;
+  if (phys < 0 || phys >= max_pages) return;
+  const int cg = lane & 15, rg = lane >> 4;
+  const int valid = min(PS, num_tokens - page * PS);
+  const uint16_t* src = k + ((size_t)h * max_pages + phys) * PS * kHeadDim + cg * 8;
+  float sm[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) sm[e] = 0.0f;
+#pragma unroll
+  for (int r0 = 0; r0 < PS; r0 += 4) {
+    const int r = r0 + rg;
+    if (r < valid) {
+      const uint4 v = *reinterpret_cast<const uint4*>(src + (size_t)r * kHeadDim);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sm[e] += u4_elem<BF16>(v, e);
+    }
+  }
+  const float inv = 1.0f / (float)valid;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    sm[e] += __shfl_xor(sm[e], 16);
+    sm[e] += __shfl_xor(sm[e], 32);
+  }
+  if (rg == 0) {
+    float4* dst = reinterpret_cast<float4*>(meta + ((size_t)h * max_pages + page) * kHeadDim + cg * 8);
+    dst[0] = make_float4(sm[0] * inv, sm[1] * inv, sm[2] * inv, sm[3] * inv);
+    dst[1] = make_float4(sm[4] * inv, sm[5] * inv, sm[6] * inv, sm[7] * inv);
+  }
+}
+
+hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream) {
+  const int np = a.page_end - a.page_begin;
+  if (np <= 0) return hipSuccess;
+  dim3 grid((np + 3) / 4, a.num_kv_heads);
+  const uint16_t* k = static_cast<const uint16_t*>(a.k_cache);
+  const int32_t* ptab = a.page_table;
+  int nt = a.num_tokens, pb = a.page_begin, pe = a.page_end, mp = a.max_pages;
+  void* meta = a.meta;
+  void* args[] = {&k, &ptab, &nt, &pb, &pe, &mp, &meta};
+  const void* f;
+  if (a.meta_mean) {
+    f = a.bf16 ? (a.page_size == 16 ? (const void*)meta_mean_kernel<true, 16> : (const void*)meta_mean_kernel<true, 64>)
+               : (a.page_size == 16 ? (const void*)meta_mean_kernel<false, 16> : (const void*)meta_mean_kernel<false, 64>);
+  } else {
+    f = a.bf16 ? (a.page_size == 16 ? (const void*)meta_minmax_kernel<true, 16> : (const void*)meta_minmax_kernel<true, 64>)
+               : (a.page_size == 16 ? (const void*)meta_minmax_kernel<false, 16> : (const void*)meta_minmax_kernel<false, 64>);
+  }
+  return hipLaunchKernel(f, grid, dim3(256), args, 0, stream);
+}
+
+// =====================================================================================
+// block top-K select (shared by score_topk and predict)
+// =====================================================================================
+// Candidates are the pages whose bit is set in `candb`; pages in `forceb` are always
+// selected.  The threshold key T (the kextra-th largest candidate key) is found by
+// radix passes over the key range [lo, hi] with 4096 bins: each pass keeps only the
+// bin that holds the wanted rank, so at most three passes are needed and usually two.
+// Then every candidate above T and the lowest-indexed candidates equal to T are
+// emitted in ascending page order (ballot compaction over contiguous per-wave ranges).
+
+constexpr int kSelLog2Bins = 12;
+constexpr int kSelBins = 1 << kSelLog2Bins;
+
+struct SelectScratch {
+  uint32_t hist[kSelBins];
+  int red[64];
+  uint32_t ured[64];
+};
+
+template <int NT>
+__device__ void select_topk_block(const uint32_t* keys, const uint32_t* candb, const uint32_t* forceb, int n,
+                                  int kextra, int32_t* __restrict__ out, int cap, int32_t* __restrict__ out_count,
+                                  SelectScratch& ss) {
+  constexpr int NW = NT / kWave;
+  const int t = threadIdx.x;
+  const int lane = lane_id(), w = t / kWave;
+
+  int cnt = 0;
+  uint32_t lo = 0xffffffffu, hi = 0u;
+  for (int p = t; p < n; p += NT) {
+    if ((candb[p >> 5] >> (p & 31)) & 1u) {
+      const uint32_t key = keys[p];
+      ++cnt;
+      lo = min(lo, key);
+      hi = max(hi, key);
+    }
+  }
+  cnt = block_sum<NT>(cnt, ss.red);
+  block_minmax_u32<NT>(lo, hi, ss.ured);
+
+  int mode;  // 0: no candidate taken, 1: all candidates, 2: threshold
+  uint32_t T = 0;
+  int need_eq = 0;
+  if (kextra <= 0 || cnt == 0) {
+    mode = 0;
+  } else if (kextra >= cnt) {
+    mode = 1;
+  } else {
+    mode = 2;
+    int r = kextra;  // rank (1 = largest) of the threshold among keys in [lo, hi]
+    for (int pass = 0; pass < 4; ++pass) {
+      const uint32_t range = hi - lo;
+      if (range == 0) {
+        T = lo;
+        break;
+      }
+      const int bits = 32 - __clz(range);
+      const int shift = bits > kSelLog2Bins ? bits - kSelLog2Bins : 0;
+      for (int b = t; b < kSelBins; b += NT) ss.hist[b] = 0u;
+      __syncthreads();
+      for (int p = t; p < n; p += NT) {
+        if ((candb[p >> 5] >> (p & 31)) & 1u) {
+          const uint32_t key = keys[p];
+          if (key >= lo && key <= hi) atomicAdd(&ss.hist[(key - lo) >> shift], 1u);
+        }
+      }
+      __syncthreads();
+      constexpr int BPT = kSelBins / NT;
+      const int top = kSelBins - t * BPT;  // this thread owns bins [top - BPT, top)
+      int local = 0;
+#pragma unroll
+      for (int i = 1; i <= BPT; ++i) local += (int)ss.hist[top - i];
+      int tot;
+      const int before = block_exclusive_scan<NT>(local, ss.red, tot);
+      if (before < r && before + local >= r) {
+        int run = before;
+        for (int i = 1; i <= BPT; ++i) {
+          const int b = top - i;
+          const int c = (int)ss.hist[b];
+          if (run + c >= r) {
+            ss.red[NW] = b;
+            ss.red[NW + 1] = run;
+            break;
+          }
+          run += c;
+        }
+      }
+      __syncthreads();
+      const int bstar = ss.red[NW];
+      const int above = ss.red[NW + 1];
+      __syncthreads();
+      r -= above;
+      const uint32_t nlo = lo + ((uint32_t)bstar << shift);
+      const uint64_t nhi = (uint64_t)nlo + ((1ull << shift) - 1ull);
+      hi = (uint32_t)min((uint64_t)hi, nhi);
+      lo = nlo;
+      if (shift == 0) {
+        T = lo;
+        break;
+      }
+    }
+    need_eq = r;
+  }
+
+  // compaction in ascending page order
+  const int ppw = (((n + NW - 1) / NW) + 63) & ~63;
+  const int wb = w * ppw, we = min(n, wb + ppw);
+  int gtf = 0, eqc = 0;
+  for (int base = wb; base < we; base += kWave) {
+    const int p = base + lane;
+    bool f = false, g = false, e = false;
+    if (p < we) {
+      f = (forceb[p >> 5] >> (p & 31)) & 1u;
+      if ((candb[p >> 5] >> (p & 31)) & 1u) {
+        if (mode == 1) {
+          g = true;
+        } else if (mode == 2) {
+          const uint32_t key = keys[p];
+          g = key > T;
+          e = key == T;
+        }
+      }
+    }
+    gtf += __popcll(__ballot(f || g));
+    eqc += __popcll(__ballot(e));
+  }
+  if (lane == 0) {
+    ss.red[w] = gtf;
+    ss.red[NW + w] = eqc;
+  }
+  __syncthreads();
+  int eq_base = 0, sel_base = 0, total = 0;
+  {
+    int eb = 0, sb = 0;
+    for (int i = 0; i < NW; ++i) {
+      const int gi = ss.red[i], ei = ss.red[NW + i];
+      const int take = max(0, min(ei, need_eq - eb));
+      if (i == w) {
+        eq_base = eb;
+        sel_base = sb;
+      }
+      eb += ei;
+      sb += gi + take;
+    }
+    total = sb;
+  }
+  __syncthreads();
+  int eq_run = eq_base, sel_run = sel_base;
+  for (int base = wb; base < we; base += kWave) {
+    const int p = base + lane;
+    bool f = false, g = false, e = false;
+    if (p < we) {
+      f = (forceb[p >> 5] >> (p & 31)) & 1u;
+      if ((candb[p >> 5] >> (p & 31)) & 1u) {
+        if (mode == 1) {
+          g = true;
+        } else if (mode == 2) {
+          const uint32_t key = keys[p];
+          g = key > T;
+          e = key == T;
+        }
+      }
+    }
+    const uint64_t em = __ballot(e);
+    const bool take_eq = e && (eq_run + lanes_below(em) < need_eq);
+    const bool sel = f || g || take_eq;
+    const uint64_t sm = __ballot(sel);
+    if (sel) {
+      const int pos = sel_run + lanes_below(sm);
+      if (pos < cap) out[pos] = p;
+    }
+    eq_run += __popcll(em);
+    sel_run += __popcll(sm);
+  }
+  if (t == 0) *out_count = min(total, cap);
+}
+
+// Dynamic LDS layout of a select: keys [n] | candb [nw] | forceb [nw] | SelectScratch.
+__host__ __device__ inline size_t select_lds_bytes(int n) {
+  const size_t nw = (size_t)(n + 31) / 32;
+  size_t b = (size_t)n * 4 + 2 * nw * 4;
+  b = (b + 15) & ~(size_t)15;
+  return b + sizeof(SelectScratch);
+}
+
+struct SelectLds {
+  uint32_t* keys;
+  uint32_t* candb;
+  uint32_t* forceb;
+  SelectScratch* ss;
+};
+
+__device__ inline SelectLds carve_select_lds(uint32_t* dyn, int n) {
+  SelectLds s;
+  const int nw = (n + 31) / 32;
+  s.keys = dyn;
+  s.candb = dyn + n;
+  s.forceb = s.candb + nw;
+  size_t off = ((size_t)n * 4 + 2 * (size_t)nw * 4 + 15) & ~(size_t)15;
+  s.ss = reinterpret_cast<SelectScratch*>(reinterpret_cast<char*>(dyn) + off);
+  return s;
+}
+
+// =====================================================================================
+// score + top-K
+// =====================================================================================
+// grid (ceil(num_pages / 64), Hkv), 256 threads.  Wave w of a workgroup scores pages
+// base + it*16 + w*4 + (lane/16) for it = 0..3; lane%16 covers channels 8*(lane%16)..+8.
+
+constexpr int kScorePagesPerWg = 64;
+
+template <bool BF16, bool MEAN>
+__global__ __launch_bounds__(256) void score_topk_kernel(const ScoreLaunch a) {
+  extern __shared__ uint32_t dyn_lds[];
+  __shared__ float qbar[kHeadDim];
+  __shared__ int s_last;
+  const int h = blockIdx.y;
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  const int G = a.group;
+  const uint16_t* q = static_cast<const uint16_t*>(a.q);
+
+  if (t < kHeadDim) {
+    float s = 0.0f;
+    for (int g = 0; g < G; ++g) s += h2f<BF16>(q[(size_t)(h * G + g) * kHeadDim + t]);
+    qbar[t] = s / (float)G;
+  }
+  __syncthreads();
+
+  const int cg = lane & 15, pi = lane >> 4;
+  float qb[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) qb[e] = qbar[cg * 8 + e];
+
+  const int base = blockIdx.x * kScorePagesPerWg;
+  float* scores = a.scores + (size_t)h * a.max_pages;
+  if constexpr (!MEAN) {
+    const uint16_t* meta = static_cast<const uint16_t*>(a.meta);
+    uint4 mn[4], mx[4];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int page = base + it * 16 + w * 4 + pi;
+      if (page < a.num_pages) {
+        const uint16_t* row = meta + ((size_t)h * a.max_pages + page) * 2 * kHeadDim + cg * 8;
+        mn[it] = *reinterpret_cast<const uint4*>(row);
+        mx[it] = *reinterpret_cast<const uint4*>(row + kHeadDim);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int page = base + it * 16 + w * 4 + pi;
+      float s = 0.0f;
+      if (page < a.num_pages) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s += fmaxf(qb[e] * u4_elem<BF16>(mn[it], e), qb[e] * u4_elem<BF16>(mx[it], e));
+      }
+      s = sum16(s);
+      if (cg == 0 && page < a.num_pages) scores[page] = s;
+    }
+  } else {
+    const float* meta = static_cast<const float*>(a.meta);
+    float4 m0[4], m1[4];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int page = base + it * 16 + w * 4 + pi;
+      if (page < a.num_pages) {
+        const float4* row = reinterpret_cast<const float4*>(meta + ((size_t)h * a.max_pages + page) * kHeadDim + cg * 8);
+        m0[it] = row[0];
+        m1[it] = row[1];
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int page = base + it * 16 + w * 4 + pi;
+      float s = 0.0f;
+      if (page < a.num_pages) {
+        s = qb[0] * m0[it].x;
+        s += qb[1] * m0[it].y;
+        s += qb[2] * m0[it].z;
+        s += qb[3] * m0[it].w;
+        s += qb[4] * m1[it].x;
+        s += qb[5] * m1[it].y;
+        s += qb[6] * m1[it].z;
+        s += qb[7] * m1[it].w;
+      }
+      s = sum16(s);
+      if (cg == 0 && page < a.num_pages) scores[page] = s;
+    }
+  }
+
+  // the last workgroup of this KV head selects
+  __threadfence();
+  __syncthreads();
+  if (t == 0) {
+    const uint32_t old = atomicAdd(&a.counters[h], 1u);
+    s_last = (old == (uint32_t)(gridDim.x - 1));
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+
+  const int n = a.num_pages;
+  const int nw = (n + 31) / 32;
+  SelectLds L = carve_select_lds(dyn_lds, n);
+  for (int p = t; p < n; p += 256) L.keys[p] = score_key(scores[p]);
+  for (int i = t; i < nw; i += 256) {
+    const int rem = n - i * 32;
+    L.candb[i] = rem >= 32 ? 0xffffffffu : ((1u << rem) - 1u);
+    L.forceb[i] = 0u;
+  }
+  __syncthreads();
+  if (t < a.n_forced) {
+    const int p = a.forced[t];
+    atomicOr(&L.forceb[p >> 5], 1u << (p & 31));
+    atomicAnd(&L.candb[p >> 5], ~(1u << (p & 31)));
+  }
+  __syncthreads();
+  select_topk_block<256>(L.keys, L.candb, L.forceb, n, a.kextra, a.selected + (size_t)h * a.cap, a.cap,
+                         a.selected_count + h, *L.ss);
+  if (t == 0) atomicExch(&a.counters[h], 0u);
+}
+
+// =====================================================================================
+// EMA predictor
+// =====================================================================================
+
+template <int NT>
+__global__ __launch_bounds__(NT) void predict_kernel(const PredictLaunch a) {
+  extern __shared__ uint32_t dyn_lds[];
+  const int h = blockIdx.x;
+  const int t = threadIdx.x, lane = lane_id();
+  const int n = a.num_pages;
+  const int nwmax = (a.max_pages + 31) / 32;
+  SelectLds L = carve_select_lds(dyn_lds, n);
+  float* level = a.level + (size_t)h * a.max_pages;
+  float* trend = a.trend + (size_t)h * a.max_pages;
+  uint32_t* bits = a.init_bits + (size_t)h * nwmax;
+  const float* scores = a.scores ? a.scores + (size_t)h * a.max_pages : nullptr;
+  const int nround = (n + NT - 1) / NT;
+  for (int r = 0; r < nround; ++r) {
+    const int p = r * NT + t;  // a wave covers 64 consecutive pages = two bit words
+    const bool inr = p < n;
+    bool has = false;
+    float pred = 0.0f;
+    if (inr) {
+      has = (bits[p >> 5] >> (p & 31)) & 1u;
+      float lv = level[p], tv = trend[p];
+      if (scores) {
+        const float s = scores[p];
+        if (has) {
+          tv = a.beta * (s - lv) + (1.0f - a.beta) * tv;  // Eq. (3): the trend reads the previous level
+          lv = a.alpha * s + (1.0f - a.alpha) * lv;
+        } else {
+          lv = s;
+          tv = 0.0f;
+          has = true;
+        }
+        level[p] = lv;
+        trend[p] = tv;
+      }
+      pred = lv + a.gamma * tv;  // Eq. (2)
+      L.keys[p] = score_key(pred);
+    }
+    const uint64_t hm = __ballot(has);
+    const uint64_t vm = __ballot(inr);
+    if (lane == 0 || lane == 32) {
+      const int wd = (r * NT + (t & ~63) + lane) >> 5;
+      const uint32_t hbits = (uint32_t)(lane == 0 ? hm : (hm >> 32));
+      const uint32_t vbits = (uint32_t)(lane == 0 ? vm : (vm >> 32));
+      if (vbits) {
+        L.candb[wd] = hbits;
+        L.forceb[wd] = 0u;
+        if (scores) bits[wd] = (bits[wd] & ~vbits) | hbits;
+      }
+    }
+  }
+  __syncthreads();
+  if (t < a.n_forced) {
+    const int p = a.forced[t];
+    atomicOr(&L.forceb[p >> 5], 1u << (p & 31));
+    atomicAnd(&L.candb[p >> 5], ~(1u << (p & 31)));
+  }
+  __syncthreads();
+  select_topk_block<NT>(L.keys, L.candb, L.forceb, n, a.kextra, a.predicted + (size_t)h * a.cap, a.cap,
+                        a.predicted_count + h, *L.ss);
+}
+
+// =====================================================================================
+// attention over a short page list (one workgroup, four waves)
+// =====================================================================================
+// Wave w takes list entries w, w+4, w+8, w+12 (a list holds at most 16 pages) and runs
+// an online softmax over their 16-token tiles; the four wave states are merged in LDS.
+//
+// q.k^T per tile: S^T (16 tokens x 16 heads) = K (16 x 128) . Q^T (128 x 16) as four
+// 16x16x32 MFMAs.  The contraction index is permuted so that each lane reads 64
+// contiguous bytes of its key row: for k-step s, lane 16j+r supplies channels
+// 32j+8s .. +8 of token r (A operand) and lane 16j+n channels 32j+8s .. +8 of query head n
+// (B operand).  The result gives lane 16j+n the logits of tokens 4j..4j+3 for head n.
+//
+// p.V per tile: O (16 heads x 128) += P (16 x 16 tokens) . V (16 x 128) as 32 16x16x4
+// fp32 MFMAs.  Call (tg, cg) contracts tokens {tg, 4+tg, 8+tg, 12+tg}: lane 16j+n
+// supplies p[head n][token 4j+tg] (its own logit register tg) and V[token 4j+tg]
+// [channel 8n+cg] (from one 16-byte row load per tg); accumulator cg holds
+// O[head 4j+i][channel 8n+cg] in lane 16j+n.
+
+struct AttnCtx {
+  const uint16_t* q;  // q + h*G*128
+  const uint16_t* k;  // k_cache + h*max_pages*PS*128
+  const uint16_t* v;
+  const int32_t* ptab;
+  int max_pages, num_pages, num_tokens, G;
+};
+
+struct UnitLds {
+  float wo[4][16][kHeadDim];
+  float wm[4][16];
+  float wl[4][16];
+};
+
+template <bool BF16>
+__device__ __forceinline__ f32x4_t mfma_qk(const u32x4_t& a, const u32x4_t& b, f32x4_t c) {
+  if constexpr (BF16) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
+                                                   0, 0, 0);
+  } else {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c, 0,
+                                                  0, 0);
+  }
+}
+
+template <bool BF16>
+__device__ __forceinline__ float v_elem(const u32x4_t& v, int e) {
+  const uint32_t wd = v[e >> 1];
+  return h2f<BF16>((e & 1) ? (wd >> 16) : (wd & 0xffffu));
+}
+
+// Result for thread t: head t/16, channels 8*(t%16)..+8: normalised o, m, l.
+struct UnitResult {
+  float o[8];
+  float m, l;
+};
+
+template <bool BF16, int PS>
+__device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, float* page_m_out, UnitLds& sm,
+                            uint32_t* flags, UnitResult& res) {
+  constexpr int TPP = PS / 16;
+  constexpr int NT = 4 * TPP;  // tiles per wave (4 list entries at most)
+  const float kNegInf = -__builtin_inff();
+  const float scale = 0.08838834764831845f;  // 1/sqrt(128)
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  const int j = lane >> 4, n = lane & 15;
+  const int G = c.G;
+
+  u32x4_t qf[4];
+  if (n < G) {
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(c.q + (size_t)n * kHeadDim + 32 * j);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qf[s] = src[s];
+  } else {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qf[s] = u32x4_t{0, 0, 0, 0};
+  }
+
+  size_t off[4];
+  int tok0[4];
+  bool ok[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const int i = w + 4 * kk;
+    ok[kk] = false;
+    off[kk] = 0;
+    tok0[kk] = 0;
+    if (i < cnt) {
+      const int pg = pages[i];
+      if (pg >= 0 && pg < c.num_pages) {
+        const int phys = c.ptab ? c.ptab[pg] : pg;
+        if (phys >= 0 && phys < c.max_pages) {
+          ok[kk] = true;
+          off[kk] = (size_t)phys * PS * kHeadDim;
+          tok0[kk] = pg * PS;
+        } else if (flags && lane == 0) {
+          atomicOr(flags, kFlagBadListEntry);
+        }
+      } else if (flags && lane == 0) {
+        atomicOr(flags, kFlagBadListEntry);
+      }
+    }
+  }
+
+  f32x4_t acc[8];
+#pragma unroll
+  for (int cg = 0; cg < 8; ++cg) acc[cg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = kNegInf, l_run = 0.0f;
+
+  auto load_tile = [&](int f, u32x4_t (&kf)[4], u32x4_t (&vf)[4]) {
+    const int kk = f / TPP, tt = f % TPP;
+    if (ok[kk]) {
+      const uint16_t* kt = c.k + off[kk] + (size_t)tt * 16 * kHeadDim;
+      const uint16_t* vt = c.v + off[kk] + (size_t)tt * 16 * kHeadDim;
+      const u32x4_t* ks = reinterpret_cast<const u32x4_t*>(kt + (size_t)n * kHeadDim + 32 * j);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) kf[s] = ks[s];
+#pragma unroll
+      for (int tg = 0; tg < 4; ++tg) vf[tg] = *reinterpret_cast<const u32x4_t*>(vt + (size_t)(4 * j + tg) * kHeadDim + 8 * n);
+    }
+  };
+
+  float pm = kNegInf;  // max logit of the current page, per head
+  auto compute_tile = [&](int f, const u32x4_t (&kf)[4], const u32x4_t (&vf)[4]) {
+    const int kk = f / TPP, tt = f % TPP;
+    if (!ok[kk]) return;
+    if (tt == 0) pm = kNegInf;
+    f32x4_t st = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) st = mfma_qk<BF16>(kf[s], qf[s], st);
+    float sv[4];
+    float mx = kNegInf;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int tok = tok0[kk] + tt * 16 + 4 * j + i;
+      sv[i] = tok < c.num_tokens ? st[i] * scale : kNegInf;
+      mx = fmaxf(mx, sv[i]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    pm = fmaxf(pm, mx);
+    const float mnew = fmaxf(m_run, mx);
+    float alpha = 1.0f;
+    float p[4] = {0.f, 0.f, 0.f, 0.f};
+    if (mnew != kNegInf) {
+      alpha = exp2f((m_run - mnew) * kLog2e);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p[i] = exp2f((sv[i] - mnew) * kLog2e);
+    }
+    float ls = (p[0] + p[1]) + (p[2] + p[3]);
+    ls += __shfl_xor(ls, 16);
+    ls += __shfl_xor(ls, 32);
+    l_run = l_run * alpha + ls;
+    m_run = mnew;
+    float a4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a4[i] = __shfl(alpha, 4 * j + i);
+#pragma unroll
+    for (int cg = 0; cg < 8; ++cg) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[cg][i] *= a4[i];
+    }
+#pragma unroll
+    for (int tg = 0; tg < 4; ++tg) {
+#pragma unroll
+      for (int cg = 0; cg < 8; ++cg)
+        acc[cg] = __builtin_amdgcn_mfma_f32_16x16x4f32(p[tg], v_elem<BF16>(vf[tg], cg), acc[cg], 0, 0, 0);
+    }
+    if (tt == TPP - 1 && page_m_out && j == 0 && n < G) page_m_out[(size_t)(w + 4 * kk) * G + n] = pm;
+  };
+
+  // software pipeline: the next tile's loads are in flight while this one computes
+  u32x4_t ka[4], va[4], kb[4], vb[4];
+  load_tile(0, ka, va);
+#pragma unroll
+  for (int f = 0; f < NT; f += 2) {
+    if (f + 1 < NT) load_tile(f + 1, kb, vb);
+    compute_tile(f, ka, va);
+    if (f + 1 < NT) {
+      if (f + 2 < NT) load_tile(f + 2, ka, va);
+      compute_tile(f + 1, kb, vb);
+    }
+  }
+
+  // merge the four wave states
+  if (j == 0) {
+    sm.wm[w][n] = m_run;
+    sm.wl[w][n] = l_run;
+  }
+#pragma unroll
+  for (int cg = 0; cg < 8; ++cg) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sm.wo[w][4 * j + i][8 * n + cg] = acc[cg][i];
+  }
+  __syncthreads();
+  const int hh = t >> 4, c0 = (t & 15) * 8;
+  float mw[4], fw[4];
+  float ms = kNegInf;
+#pragma unroll
+  for (int ww = 0; ww < 4; ++ww) {
+    mw[ww] = sm.wm[ww][hh];
+    if (sm.wl[ww][hh] > 0.0f) ms = fmaxf(ms, mw[ww]);
+  }
+  float L = 0.0f;
+#pragma unroll
+  for (int ww = 0; ww < 4; ++ww) {
+    const float lw = sm.wl[ww][hh];
+    fw[ww] = lw > 0.0f ? exp2f((mw[ww] - ms) * kLog2e) : 0.0f;
+    L += lw * fw[ww];
+  }
+  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float o = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww) o += sm.wo[ww][hh][c0 + e] * fw[ww];
+    res.o[e] = o * inv;
+  }
+  res.m = L > 0.0f ? ms : kNegInf;
+  res.l = L;
+  __syncthreads();
+}
+
+template <bool BF16, int PS>
+__global__ __launch_bounds__(256) void spec_attn_kernel(const SpecLaunch a) {
+  __shared__ UnitLds sm;
+  const int c = blockIdx.x, h = blockIdx.y;
+  const int total = min(max(a.page_count[h], 0), a.cap);
+  const int start = c * a.chunk;
+  if (start >= total) return;
+  const int cnt = min(a.chunk, total - start);
+  const int G = a.group;
+  AttnCtx ctx;
+  ctx.q = static_cast<const uint16_t*>(a.q) + (size_t)h * G * kHeadDim;
+  ctx.k = static_cast<const uint16_t*>(a.k_cache) + (size_t)h * a.max_pages * a.page_size * kHeadDim;
+  ctx.v = static_cast<const uint16_t*>(a.v_cache) + (size_t)h * a.max_pages * a.page_size * kHeadDim;
+  ctx.ptab = a.page_table;
+  ctx.max_pages = a.max_pages;
+  ctx.num_pages = a.num_pages;
+  ctx.num_tokens = a.num_tokens;
+  ctx.G = G;
+  UnitResult r;
+  float* pmo = a.page_m ? a.page_m + ((size_t)h * a.cap + start) * G : nullptr;
+  attend_unit<BF16, PS>(ctx, a.pages + (size_t)h * a.cap + start, cnt, pmo, sm, nullptr, r);
+  const int t = threadIdx.x, hh = t >> 4, c0 = (t & 15) * 8;
+  if (hh < G) {
+    const size_t row = ((size_t)h * a.nchunks + c) * G + hh;
+    float4* dst = reinterpret_cast<float4*>(a.part_o + row * kHeadDim + c0);
+    dst[0] = make_float4(r.o[0], r.o[1], r.o[2], r.o[3]);
+    dst[1] = make_float4(r.o[4], r.o[5], r.o[6], r.o[7]);
+    if ((t & 15) == 0) {
+      a.part_m[row] = r.m;
+      a.part_l[row] = r.l;
+    }
+  }
+}
+
+// =====================================================================================
+// repair
+// =====================================================================================
+// Grid: Hkv * nwork work workgroups, then Hkv * ceil(G/2) merge workgroups.  Every
+// workgroup first builds the plan of its KV head in LDS (bitmaps of A and P, the
+// missed list in A's order, the chunks of P that hold a wasted page).
+// Work unit u < ceil(|M|/C): attend missed pages [uC, uC+C).
+// Work unit u >= that (exact mode): one contaminated chunk c of P: attend its wasted
+//   pages W; if they carry at most kMaxWastedShare of the chunk's softmax mass for every
+//   head, subtract them from the chunk's speculative state (the clean part's maximum
+//   comes from the per-page maxima of the speculation); otherwise attend the chunk's
+//   pages of A afresh.  Either way the unit's state replaces chunk c.
+// Merge workgroups wait (bounded spin) until every work workgroup of their KV head has
+// published its state, merge the clean chunks and all unit states, and write the output.
+
+constexpr float kMaxWastedShare = 0.875f;
+constexpr int kSpinLimit = 1 << 24;
+
+struct RepairLds {
+  uint32_t bitA[PRR_MAX_PAGES_DEV / 32];
+  uint32_t bitP[PRR_MAX_PAGES_DEV / 32];
+  int32_t listA[PRR_MAX_CAP_DEV];
+  int32_t listP[PRR_MAX_CAP_DEV];
+  int32_t missed[PRR_MAX_CAP_DEV];
+  int32_t contam[PRR_MAX_CAP_DEV];
+  uint32_t contam_bits[PRR_MAX_CAP_DEV / 32];
+  int32_t wpages[16];
+  int32_t xpages[16];
+  int32_t xslots[16];
+  int red[64];
+  int nM, nW, nCont, nWp, nXp, bad;
+  UnitLds unit;
+};
+
+template <bool BF16, int PS>
+__global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
+  __shared__ RepairLds S;
+  const int t = threadIdx.x;
+  const int G = a.group, C = a.chunk;
+  const int work_wgs = a.num_kv_heads * a.nwork;
+  const int bid = blockIdx.x;
+  const bool is_merge = bid >= work_wgs;
+  int h, u = 0, pair = 0;
+  if (!is_merge) {
+    h = bid / a.nwork;
+    u = bid % a.nwork;
+  } else {
+    const int m = bid - work_wgs;
+    h = m / a.nmerge_per_kv;
+    pair = m % a.nmerge_per_kv;
+  }
+  const bool exact = a.mode == PRR_EXACT_SELECTED;
+  const int n = a.num_pages;
+  const int nwords = (n + 31) / 32;
+  const int nA = min(max(a.selected_count[h], 0), a.cap);
+  const int nP = a.predicted ? min(max(a.predicted_count[h], 0), a.cap) : 0;
+
+  // ---- plan
+  for (int i = t; i < nwords; i += 256) {
+    S.bitA[i] = 0u;
+    S.bitP[i] = 0u;
+  }
+  for (int i = t; i < nA; i += 256) S.listA[i] = a.selected[(size_t)h * a.cap + i];
+  for (int i = t; i < nP; i += 256) S.listP[i] = a.predicted[(size_t)h * a.cap + i];
+  __syncthreads();
+  bool bad_entry = false;
+  for (int i = t; i < nA; i += 256) {
+    const int p = S.listA[i];
+    if (p >= 0 && p < n) atomicOr(&S.bitA[p >> 5], 1u << (p & 31));
+    else bad_entry = true;
+  }
+  for (int i = t; i < nP; i += 256) {
+    const int p = S.listP[i];
+    if (p >= 0 && p < n) atomicOr(&S.bitP[p >> 5], 1u << (p & 31));
+    else bad_entry = true;
+  }
+  if (bad_entry && bid == 0) atomicOr(a.flags, kFlagBadListEntry);
+  __syncthreads();
+  {
+    // missed = A \ P in A's order: thread t owns entries [4t, 4t+4)
+    int flags = 0, cntm = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int i = 4 * t + e;
+      if (i < nA) {
+        const int p = S.listA[i];
+        if (p >= 0 && p < n && !((S.bitP[p >> 5] >> (p & 31)) & 1u)) {
+          flags |= 1 << e;
+          ++cntm;
+        }
+      }
+    }
+    int tot;
+    int pos = block_exclusive_scan<256>(cntm, S.red, tot);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (flags & (1 << e)) S.missed[pos++] = S.listA[4 * t + e];
+    if (t == 0) S.nM = tot;
+    // wasted = P \ A
+    int cw = 0;
+    for (int i = t; i < nP; i += 256) {
+      const int p = S.listP[i];
+      if (p >= 0 && p < n && !((S.bitA[p >> 5] >> (p & 31)) & 1u)) ++cw;
+    }
+    cw = block_sum<256>(cw, S.red);
+    if (t == 0) S.nW = cw;
+    // contaminated chunks (exact mode), in chunk order: thread t owns chunks [4t, 4t+4)
+    const int nch = (nP + C - 1) / C;
+    int cf = 0, cc = 0;
+    if (exact) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int ch = 4 * t + e;
+        if (ch < nch) {
+          bool dirty = false;
+          for (int i = ch * C; i < min(nP, ch * C + C); ++i) {
+            const int p = S.listP[i];
+            if (p >= 0 && p < n && !((S.bitA[p >> 5] >> (p & 31)) & 1u)) dirty = true;
+          }
+          if (dirty) {
+            cf |= 1 << e;
+            ++cc;
+          }
+        }
+      }
+    }
+    pos = block_exclusive_scan<256>(cc, S.red, tot);
+    for (int i = t; i < PRR_MAX_CAP_DEV / 32; i += 256) S.contam_bits[i] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (cf & (1 << e)) {
+        const int ch = 4 * t + e;
+        S.contam[pos++] = ch;
+        atomicOr(&S.contam_bits[ch >> 5], 1u << (ch & 31));
+      }
+    }
+    if (t == 0) S.nCont = tot;
+  }
+  __syncthreads();
+  const int nM = S.nM, nCont = S.nCont;
+  const int nMU = (nM + C - 1) / C;
+
+  AttnCtx ctx;
+  ctx.q = static_cast<const uint16_t*>(a.q) + (size_t)h * G * kHeadDim;
+  ctx.k = static_cast<const uint16_t*>(a.k_cache) + (size_t)h * a.max_pages * a.page_size * kHeadDim;
+  ctx.v = static_cast<const uint16_t*>(a.v_cache) + (size_t)h * a.max_pages * a.page_size * kHeadDim;
+  ctx.ptab = a.page_table;
+  ctx.max_pages = a.max_pages;
+  ctx.num_pages = n;
+  ctx.num_tokens = a.num_tokens;
+  ctx.G = G;
+  const int hh = t >> 4, c0 = (t & 15) * 8;
+
+  if (!is_merge) {
+    // ---- work
+    UnitResult r;
+    bool have = false;
+    if (u < nMU) {
+      const int start = u * C;
+      attend_unit<BF16, PS>(ctx, S.missed + start, min(C, nM - start), nullptr, S.unit, a.flags, r);
+      have = true;
+    } else if (exact && u - nMU < nCont) {
+      const int ch = S.contam[u - nMU];
+      if (t == 0) {
+        int nw = 0, nx = 0;
+        for (int i = ch * C; i < min(nP, ch * C + C); ++i) {
+          const int p = S.listP[i];
+          if (p < 0 || p >= n) continue;
+          if ((S.bitA[p >> 5] >> (p & 31)) & 1u) {
+            S.xpages[nx] = p;
+            S.xslots[nx] = i;
+            ++nx;
+          } else {
+            S.wpages[nw++] = p;
+          }
+        }
+        S.nWp = nw;
+        S.nXp = nx;
+      }
+      __syncthreads();
+      const int nwp = S.nWp, nxp = S.nXp;
+      bool recompute = true;
+      if (a.page_m && nxp > 0 && nwp > 0) {
+        attend_unit<BF16, PS>(ctx, S.wpages, nwp, nullptr, S.unit, a.flags, r);
+        const size_t crow = ((size_t)h * a.nchunks + ch) * G;
+        bool bad = false;
+        float mx = -__builtin_inff(), mc = 0.f, lc = 0.f;
+        if (hh < G) {
+          mc = a.part_m[crow + hh];
+          lc = a.part_l[crow + hh];
+          const float share = (lc > 0.f && r.l > 0.f) ? r.l * exp2f((r.m - mc) * kLog2e) / lc : (r.l > 0.f ? 2.f : 0.f);
+          bad = !(share <= kMaxWastedShare);
+          for (int x = 0; x < nxp; ++x) mx = fmaxf(mx, a.page_m[((size_t)h * a.cap + S.xslots[x]) * G + hh]);
+        }
+        bad = __syncthreads_or(bad);
+        if (!bad) {
+          recompute = false;
+          if (hh < G) {
+            const float ec = lc * exp2f((mc - mx) * kLog2e);
+            const float ew = r.l > 0.f ? r.l * exp2f((r.m - mx) * kLog2e) : 0.f;
+            const float lx = ec - ew;
+            const float inv = 1.0f / lx;
+            const float4* oc = reinterpret_cast<const float4*>(a.part_o + (crow + hh) * kHeadDim + c0);
+            const float4 o0 = oc[0], o1 = oc[1];
+            const float ocv[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) r.o[e] = (ec * ocv[e] - ew * r.o[e]) * inv;
+            r.m = mx;
+            r.l = lx;
+          }
+        }
+      }
+      if (recompute) attend_unit<BF16, PS>(ctx, S.xpages, nxp, nullptr, S.unit, a.flags, r);
+      have = true;
+    }
+    if (have && hh < G) {
+      const size_t row = ((size_t)h * a.nwork + u) * G + hh;
+      float4* dst = reinterpret_cast<float4*>(a.ws_o + row * kHeadDim + c0);
+      dst[0] = make_float4(r.o[0], r.o[1], r.o[2], r.o[3]);
+      dst[1] = make_float4(r.o[4], r.o[5], r.o[6], r.o[7]);
+      if ((t & 15) == 0) {
+        a.ws_ml[row * 2] = r.m;
+        a.ws_ml[row * 2 + 1] = r.l;
+      }
+    }
+    __threadfence();
+    __syncthreads();
+    if (t == 0) atomicAdd(&a.ws_cnt[h], 1u);
+    return;
+  }
+
+  // ---- merge
+  if (t == 0) {
+    int it = 0;
+    while (__hip_atomic_load(&a.ws_cnt[h], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)a.nwork) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++it > kSpinLimit) {
+        atomicOr(a.flags, kFlagSpinTimeout);
+        break;
+      }
+    }
+  }
+  __syncthreads();
+  __threadfence();
+  const int g = pair * 2 + (t >> 7);
+  const int ch = t & 127;
+  const int nchP = (nP + C - 1) / C;
+  const int nUnits = nMU + (exact ? nCont : 0);
+  if (g < G) {
+    const float kNegInf = -__builtin_inff();
+    float ms = kNegInf;
+    for (int c = 0; c < nchP; ++c) {
+      if (exact && ((S.contam_bits[c >> 5] >> (c & 31)) & 1u)) continue;
+      const size_t row = ((size_t)h * a.nchunks + c) * G + g;
+      if (a.part_l[row] > 0.f) ms = fmaxf(ms, a.part_m[row]);
+    }
+    for (int uu = 0; uu < nUnits; ++uu) {
+      const size_t row = ((size_t)h * a.nwork + uu) * G + g;
+      if (a.ws_ml[row * 2 + 1] > 0.f) ms = fmaxf(ms, a.ws_ml[row * 2]);
+    }
+    float L = 0.f, O = 0.f;
+    for (int c = 0; c < nchP; ++c) {
+      if (exact && ((S.contam_bits[c >> 5] >> (c & 31)) & 1u)) continue;
+      const size_t row = ((size_t)h * a.nchunks + c) * G + g;
+      const float l = a.part_l[row];
+      if (l > 0.f) {
+        const float wgt = l * exp2f((a.part_m[row] - ms) * kLog2e);
+        L += wgt;
+        O += wgt * a.part_o[row * kHeadDim + ch];
+      }
+    }
+    for (int uu = 0; uu < nUnits; ++uu) {
+      const size_t row = ((size_t)h * a.nwork + uu) * G + g;
+      const float l = a.ws_ml[row * 2 + 1];
+      if (l > 0.f) {
+        const float wgt = l * exp2f((a.ws_ml[row * 2] - ms) * kLog2e);
+        L += wgt;
+        O += wgt * a.ws_o[row * kHeadDim + ch];
+      }
+    }
+    const float o = L > 0.f ? O / L : 0.f;
+    const size_t orow = (size_t)h * G + g;
+    a.out_o32[orow * kHeadDim + ch] = o;
+    if (a.out_o) static_cast<uint16_t*>(a.out_o)[orow * kHeadDim + ch] = (uint16_t)f2h_rne<BF16>(o);
+    if (ch == 0) {
+      a.out_m[orow] = L > 0.f ? ms : kNegInf;
+      a.out_l[orow] = L;
+    }
+  }
+  if (pair == 0 && t == 0) {
+    if (a.missed_count) a.missed_count[h] = nM;
+    if (a.wasted_count) a.wasted_count[h] = S.nW;
+  }
+  __syncthreads();
+  if (t == 0) {
+    const uint32_t old = atomicAdd(&a.ws_cnt[a.num_kv_heads + h], 1u);
+    if (old == (uint32_t)(a.nmerge_per_kv - 1)) {
+      atomicExch(&a.ws_cnt[h], 0u);
+      atomicExch(&a.ws_cnt[a.num_kv_heads + h], 0u);
+    }
+  }
+}
+
+// =====================================================================================
+// merge of arbitrary partial states
+// =====================================================================================
+
+__global__ __launch_bounds__(256) void merge_states_kernel(int n_states, int rows, int d, const float* __restrict__ o,
+                                                           const float* __restrict__ m, const float* __restrict__ l,
+                                                           float* __restrict__ out_o, float* __restrict__ out_m,
+                                                           float* __restrict__ out_l) {
+  const int row = blockIdx.x;
+  const float kNegInf = -__builtin_inff();
+  float ms = kNegInf;
+  for (int s = 0; s < n_states; ++s) {
+    const size_t i = (size_t)s * rows + row;
+    if (l[i] > 0.f) ms = fmaxf(ms, m[i]);
+  }
+  float L = 0.f;
+  for (int s = 0; s < n_states; ++s) {
+    const size_t i = (size_t)s * rows + row;
+    if (l[i] > 0.f) L += l[i] * exp2f((m[i] - ms) * kLog2e);
+  }
+  for (int c = threadIdx.x; c < d; c += blockDim.x) {
+    float O = 0.f;
+    for (int s = 0; s < n_states; ++s) {
+      const size_t i = (size_t)s * rows + row;
+      if (l[i] > 0.f) O += l[i] * exp2f((m[i] - ms) * kLog2e) * o[i * d + c];
+    }
+    out_o[(size_t)row * d + c] = L > 0.f ? O / L : 0.f;
+  }
+  if (threadIdx.x == 0) {
+    out_m[row] = L > 0.f ? ms : kNegInf;
+    out_l[row] = L;
+  }
+}
+
+// =====================================================================================
+// launchers
+// =====================================================================================
+
+// Dynamic LDS above 48 KiB needs the kernel's limit raised; the limit only ever grows,
+// so after the first (eager) call of a shape no attribute call is made, which keeps
+// graph capture free of them.  A failed attribute call is cleared from HIP's last-error
+// state so that it is not mistaken for a launch error of the caller.
+static std::mutex g_lds_mutex;
+static std::map<const void*, size_t> g_lds_limit;
+
+static void allow_lds(const void* f, size_t bytes) {
+  if (bytes <= 48 * 1024) return;
+  std::lock_guard<std::mutex> lock(g_lds_mutex);
+  size_t& cur = g_lds_limit[f];
+  if (cur >= bytes) return;
+  if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) == hipSuccess) cur = bytes;
+  else (void)hipGetLastError();
+}
+
+// Launch a kernel taking one by-value descriptor and return the launch's own status.
+template <typename A>
+static hipError_t launch1(const void* f, dim3 grid, dim3 block, size_t lds, hipStream_t stream, const A& arg) {
+  allow_lds(f, lds);
+  void* args[] = {const_cast<A*>(&arg)};
+  return hipLaunchKernel(f, grid, block, args, lds, stream);
+}
+
+hipError_t launch_score_topk(const ScoreLaunch& a, hipStream_t stream) {
+  dim3 grid((a.num_pages + kScorePagesPerWg - 1) / kScorePagesPerWg, a.num_kv_heads);
+  const size_t lds = select_lds_bytes(a.num_pages);
+  const void* f = a.bf16 ? (a.meta_mean ? (const void*)score_topk_kernel<true, true> : (const void*)score_topk_kernel<true, false>)
+                         : (a.meta_mean ? (const void*)score_topk_kernel<false, true> : (const void*)score_topk_kernel<false, false>);
+  return launch1(f, grid, dim3(256), lds, stream, a);
+}
+
+hipError_t launch_predict(const PredictLaunch& a, hipStream_t stream) {
+  const size_t lds = select_lds_bytes(a.num_pages);
+  return launch1((const void*)predict_kernel<256>, dim3(a.num_kv_heads), dim3(256), lds, stream, a);
+}
+
+hipError_t launch_spec_attn(const SpecLaunch& a, hipStream_t stream) {
+  dim3 grid(a.nchunks, a.num_kv_heads);
+  const void* f = a.bf16 ? (a.page_size == 16 ? (const void*)spec_attn_kernel<true, 16> : (const void*)spec_attn_kernel<true, 64>)
+                         : (a.page_size == 16 ? (const void*)spec_attn_kernel<false, 16> : (const void*)spec_attn_kernel<false, 64>);
+  return launch1(f, grid, dim3(256), 0, stream, a);
+}
+
+hipError_t launch_repair(const RepairLaunch& a, hipStream_t stream) {
+  const int grid = a.num_kv_heads * (a.nwork + a.nmerge_per_kv);
+  const void* f = a.bf16 ? (a.page_size == 16 ? (const void*)repair_kernel<true, 16> : (const void*)repair_kernel<true, 64>)
+                         : (a.page_size == 16 ? (const void*)repair_kernel<false, 16> : (const void*)repair_kernel<false, 64>);
+  return launch1(f, dim3(grid), dim3(256), 0, stream, a);
+}
+
+hipError_t launch_merge_states(int n_states, int rows, int d, const float* o, const float* m, const float* l,
+                               float* out_o, float* out_m, float* out_l, hipStream_t stream) {
+  void* args[] = {&n_states, &rows, &d, &o, &m, &l, &out_o, &out_m, &out_l};
+  return hipLaunchKernel((const void*)merge_states_kernel, dim3(rows), dim3(256), args, 0, stream);
+}
+
+}  // namespace prr

@@ -1,0 +1,99 @@
+// Launch descriptors passed by value to the kernels, and the launchers the C ABI calls
+// after it has validated every argument.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "prr.h"
+
+#define PRR_MAX_PAGES_DEV PRR_MAX_PAGES
+#define PRR_MAX_CAP_DEV PRR_MAX_CAP
+
+namespace prr {
+
+struct MetaLaunch {
+  const void* k_cache;
+  const int32_t* page_table;
+  void* meta;
+  int num_kv_heads, max_pages, page_size, num_tokens, page_begin, page_end;
+  bool bf16, meta_mean;
+};
+
+struct ScoreLaunch {
+  const void* q;
+  const void* meta;
+  float* scores;
+  int32_t* selected;
+  int32_t* selected_count;
+  uint32_t* counters;  // [Hkv], zero between calls
+  int num_kv_heads, group, max_pages, num_pages, kextra, cap, n_forced;
+  bool bf16, meta_mean;
+  int32_t forced[PRR_MAX_FORCED];
+};
+
+struct PredictLaunch {
+  float* level;
+  float* trend;
+  uint32_t* init_bits;
+  const float* scores;
+  int32_t* predicted;
+  int32_t* predicted_count;
+  float alpha, beta, gamma;
+  int num_kv_heads, max_pages, num_pages, kextra, cap, n_forced;
+  int32_t forced[PRR_MAX_FORCED];
+};
+
+struct SpecLaunch {
+  const void* q;
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* page_table;
+  const int32_t* pages;
+  const int32_t* page_count;
+  float* part_o;
+  float* part_m;
+  float* part_l;
+  float* page_m;
+  int num_kv_heads, group, max_pages, num_pages, num_tokens, page_size, cap, chunk, nchunks;
+  bool bf16;
+};
+
+struct RepairLaunch {
+  const void* q;
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* page_table;
+  const int32_t* selected;
+  const int32_t* selected_count;
+  const int32_t* predicted;
+  const int32_t* predicted_count;
+  const float* part_o;
+  const float* part_m;
+  const float* part_l;
+  const float* page_m;
+  float* out_o32;
+  void* out_o;
+  float* out_m;
+  float* out_l;
+  int32_t* missed_count;
+  int32_t* wasted_count;
+  float* ws_o;        // [Hkv][nwork][G][128]
+  float* ws_ml;       // [Hkv][nwork][G][2]
+  uint32_t* ws_cnt;   // [2*Hkv], zero between calls
+  uint32_t* flags;    // sticky error bits
+  int num_kv_heads, group, max_pages, num_pages, num_tokens, page_size, cap, chunk, nchunks, nwork, nmerge_per_kv, mode;
+  bool bf16;
+};
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
+hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream);
+hipError_t launch_score_topk(const ScoreLaunch& a, hipStream_t stream);
+hipError_t launch_predict(const PredictLaunch& a, hipStream_t stream);
+hipError_t launch_spec_attn(const SpecLaunch& a, hipStream_t stream);
+hipError_t launch_repair(const RepairLaunch& a, hipStream_t stream);
+hipError_t launch_merge_states(int n_states, int rows, int d, const float* o, const float* m, const float* l,
+                               float* out_o, float* out_m, float* out_l, hipStream_t stream);
+
+}  // namespace prr

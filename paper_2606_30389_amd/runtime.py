@@ -1,0 +1,194 @@
+"""Two-stream decode-step runtime over the C ABI (device memory and streams via torch).
+
+Per layer and decode step t (Fig. 1; Section 4):
+
+    stream S (critical):    score_topk(q_t) -> IS^t, A^t   | repair(A^t, P^t, spec) -> o_t
+    stream P (speculation): spec_attn(q_t, P^t)            | predict(IS^t) -> P^{t+1}
+
+spec_attn needs only q_t and P^t (predicted at the end of step t-1), so it runs while
+the selection is in flight; repair waits for both; the EMA update and the next
+prediction wait for the selection only and are off the critical path.  The serial
+baseline is score_topk followed by repair with no prediction, on one stream.
+
+All arithmetic happens in libprr.so; this module only allocates, uploads and orders.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import _lib as L
+
+
+@dataclasses.dataclass
+class PathConfig:
+    num_q_heads: int
+    num_kv_heads: int
+    page_size: int
+    num_tokens: int
+    k_select: int
+    forced: Sequence[int] = ()
+    forced_in_budget: bool = True
+    dtype: str = "bf16"  # "bf16" | "f16"
+    meta_kind: str = "minmax"  # "minmax" | "mean"
+    alpha: float = 0.5
+    beta: float = 0.5
+    gamma: float = 0.0
+    p_select: Optional[int] = None  # |P| budget; default = k_select (delta = 1)
+    chunk_pages: int = 8
+    mode: int = L.PRR_EXACT_SELECTED
+    max_pages: Optional[int] = None
+
+    @property
+    def group(self):
+        return self.num_q_heads // self.num_kv_heads
+
+    @property
+    def num_pages(self):
+        return (self.num_tokens + self.page_size - 1) // self.page_size
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float16
+
+    def dims(self):
+        return L.make_dims(self.num_q_heads, self.num_kv_heads, self.page_size, self.max_pages or self.num_pages,
+                           L.PRR_BF16 if self.dtype == "bf16" else L.PRR_F16,
+                           L.PRR_META_MEAN if self.meta_kind == "mean" else L.PRR_META_MINMAX)
+
+    def list_cap(self):
+        nf = len(self.forced)
+        def size(k):
+            return min(self.num_pages, max(k, nf) if self.forced_in_budget else k + nf)
+        return max(1, size(self.k_select), size(self.p_select if self.p_select is not None else self.k_select))
+
+
+def bits_tensor(bits: np.ndarray, dtype: torch.dtype, device) -> torch.Tensor:
+    """Upload 16-bit storage patterns as a tensor of the given 16-bit dtype."""
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.to(device).view(dtype)
+
+
+class LayerState:
+    """Device memory of one layer: KV cache, metadata, EMA state, lists, partials, outputs."""
+
+    def __init__(self, cfg: PathConfig, device, k=None, v=None, page_table=None):
+        self.cfg = cfg
+        self.dims = cfg.dims()
+        hkv, g, d = cfg.num_kv_heads, cfg.group, 128
+        mp = self.dims.max_pages
+        dev = device
+        self.cap = cfg.list_cap()
+        f32 = dict(dtype=torch.float32, device=dev)
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.k = k if k is not None else torch.zeros(hkv, mp, cfg.page_size, d, dtype=cfg.torch_dtype, device=dev)
+        self.v = v if v is not None else torch.zeros_like(self.k)
+        self.page_table = page_table
+        if cfg.meta_kind == "mean":
+            self.meta = torch.zeros(hkv, mp, d, **f32)
+        else:
+            self.meta = torch.zeros(hkv, mp, 2, d, dtype=cfg.torch_dtype, device=dev)
+        self.scores = torch.zeros(hkv, mp, **f32)
+        self.level = torch.zeros(hkv, mp, **f32)
+        self.trend = torch.zeros(hkv, mp, **f32)
+        self.init_bits = torch.zeros(hkv, (mp + 31) // 32, **i32)
+        self.sel = torch.zeros(hkv, self.cap, **i32)
+        self.sel_count = torch.zeros(hkv, **i32)
+        self.pred = [torch.zeros(hkv, self.cap, **i32) for _ in range(2)]
+        self.pred_count = [torch.zeros(hkv, **i32) for _ in range(2)]
+        _, po, pml, pm = L.prr_spec_state_floats(self.dims, self.cap, cfg.chunk_pages)
+        self.part_o = torch.zeros(po, **f32)
+        self.part_m = torch.zeros(pml, **f32)
+        self.part_l = torch.zeros(pml, **f32)
+        self.page_m = torch.zeros(pm, **f32)
+        self.out_o32 = torch.zeros(cfg.num_q_heads, d, **f32)
+        self.out_o = torch.zeros(cfg.num_q_heads, d, dtype=cfg.torch_dtype, device=dev)
+        self.out_m = torch.zeros(cfg.num_q_heads, **f32)
+        self.out_l = torch.zeros(cfg.num_q_heads, **f32)
+        self.missed = torch.zeros(hkv, **i32)
+        self.wasted = torch.zeros(hkv, **i32)
+        self.ws_bytes = L.prr_workspace_size(self.dims, self.cap, cfg.chunk_pages)
+        self.workspace = torch.empty(self.ws_bytes // 4 + 64, dtype=torch.int32, device=dev)
+        L.prr_workspace_init(self.workspace, self.ws_bytes)
+        self.cur = 0  # which predicted-list buffer holds P^t
+
+    # --------------------------------------------------------------- steps
+    def build_meta(self, stream=None, page_begin=0, page_end=None):
+        cfg = self.cfg
+        L.prr_build_page_meta(self.dims, self.k, self.page_table, cfg.num_tokens, page_begin,
+                              cfg.num_pages if page_end is None else page_end, self.meta, stream)
+
+    def select(self, q, stream=None):
+        cfg = self.cfg
+        L.prr_score_topk(self.dims, q, self.meta, cfg.num_pages, cfg.k_select, cfg.forced, cfg.forced_in_budget,
+                         self.scores, self.sel, self.sel_count, self.cap, self.workspace, self.ws_bytes, stream)
+
+    def predict(self, with_scores=True, stream=None):
+        """EMA update with this step's scores, then P for the next step (into the other buffer)."""
+        cfg = self.cfg
+        nxt = 1 - self.cur
+        L.prr_predict(self.dims, self.level, self.trend, self.init_bits, self.scores if with_scores else None,
+                      cfg.num_pages, cfg.alpha, cfg.beta, cfg.gamma,
+                      cfg.k_select if cfg.p_select is None else cfg.p_select, cfg.forced, cfg.forced_in_budget,
+                      self.pred[nxt], self.pred_count[nxt], self.cap, stream)
+
+    def advance(self):
+        self.cur = 1 - self.cur
+
+    def speculate(self, q, stream=None, pages=None, counts=None):
+        cfg = self.cfg
+        L.prr_spec_attn(self.dims, q, self.k, self.v, self.page_table, cfg.num_tokens,
+                        self.pred[self.cur] if pages is None else pages,
+                        self.pred_count[self.cur] if counts is None else counts,
+                        self.cap, cfg.chunk_pages, self.part_o, self.part_m, self.part_l, self.page_m, stream)
+
+    def repair(self, q, stream=None, serial=False, mode=None, pages=None, counts=None):
+        cfg = self.cfg
+        pred = None if serial else (self.pred[self.cur] if pages is None else pages)
+        cnt = None if serial else (self.pred_count[self.cur] if counts is None else counts)
+        L.prr_repair(self.dims, q, self.k, self.v, self.page_table, cfg.num_tokens, cfg.num_pages, self.sel,
+                     self.sel_count, pred, cnt, self.cap, cfg.chunk_pages, self.part_o, self.part_m, self.part_l,
+                     self.page_m, cfg.mode if mode is None else mode, self.out_o32, self.out_o, self.out_m,
+                     self.out_l, self.missed, self.wasted, self.workspace, self.ws_bytes, stream)
+
+
+class TwoStream:
+    """Fork/join orchestration of one layer step on two HIP streams (default priority)."""
+
+    def __init__(self, device):
+        self.s = torch.cuda.Stream(device=device)
+        self.p = torch.cuda.Stream(device=device)
+        self._events = []
+
+    def _ev(self):
+        return torch.cuda.Event()
+
+    def prr_layer(self, st: LayerState, q, mode=None):
+        s, p = self.s, self.p
+        fork = self._ev()
+        fork.record(s)
+        p.wait_event(fork)
+        st.select(q, stream=s)
+        sel = self._ev()
+        sel.record(s)
+        st.speculate(q, stream=p)
+        spec = self._ev()
+        spec.record(p)
+        s.wait_event(spec)
+        st.repair(q, stream=s, mode=mode)
+        p.wait_event(sel)
+        st.predict(stream=p)
+        done = self._ev()
+        done.record(p)
+        return done
+
+    def serial_layer(self, st: LayerState, q):
+        st.select(q, stream=self.s)
+        st.repair(q, stream=self.s, serial=True)
+
+    def join(self, events: List[torch.cuda.Event]):
+        for e in events:
+            self.s.wait_event(e)

@@ -1,0 +1,157 @@
+"""Host-side tests of the C ABI (no GPU needed): the library loads, exports every
+function include/prr.h declares, and rejects invalid arguments before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2606_30389_amd as P
+    return P
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "prr.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(prr_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(P):
+    names = declared_functions()
+    assert len(names) >= 11
+    lib = P.library()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(P.EXPORTED) == names
+
+
+def test_status_strings(P):
+    assert P.status_string(0) == "PRR_OK"
+    assert P.status_string(P.PRR_ERR_INVALID_ARG) == "PRR_ERR_INVALID_ARG"
+    assert P.status_string(99) == "PRR_ERR_UNKNOWN"
+
+
+def test_workspace_and_spec_state_sizes(P):
+    d = P.make_dims(32, 2, 16, 8192, P.PRR_BF16)
+    ws = P.prr_workspace_size(d, 256, 8)
+    nch = 32
+    # flags + counters + per-work-unit partial states (2 * 32 units, 16 heads, 130 floats)
+    assert ws >= 2 * 2 * nch * 16 * 130 * 4 and ws % 256 == 0
+    tot, po, pml, pm = P.prr_spec_state_floats(d, 256, 8)
+    assert (po, pml, pm) == (2 * nch * 16 * 128, 2 * nch * 16, 2 * 256 * 16)
+    assert tot == po + 2 * pml + pm
+    assert P.prr_workspace_size(d, 0, 8) == 0
+    assert P.prr_workspace_size(d, 256, 17) == 0
+    bad = P.make_dims(32, 2, 16, 8192, P.PRR_BF16, head_dim=64)
+    assert P.prr_workspace_size(bad, 256, 8) == 0
+
+
+FAKE = 0x10000  # an aligned non-null address; every case below fails validation before use
+
+
+def _expect(P, status, fn, *args, **kwargs):
+    with pytest.raises(P.PrrError) as ei:
+        fn(*args, **kwargs)
+    assert ei.value.status == status, str(ei.value)
+    assert P.last_error()
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 64, 2), ("page_size", 32, 2), ("num_kv_heads", 0, 1), ("num_q_heads", 33, 1),
+    ("num_q_heads", 34, 2), ("max_pages", 0, 1), ("dtype", 5, 1), ("meta_kind", 3, 1)])
+def test_bad_dims(P, field, value, status):
+    kw = dict(num_q_heads=32, num_kv_heads=2, page_size=16, max_pages=100, dtype=P.PRR_BF16)
+    d = P.make_dims(**kw)
+    setattr(d, field, value)
+    _expect(P, status, P.prr_build_page_meta, d, FAKE, None, 1600, 0, 100, FAKE, None)
+
+
+def test_bad_meta_args(P):
+    d = P.make_dims(32, 2, 16, 100, P.PRR_BF16)
+    _expect(P, 1, P.prr_build_page_meta, d, None, None, 1600, 0, 100, FAKE, None)
+    _expect(P, 1, P.prr_build_page_meta, d, FAKE + 2, None, 1600, 0, 100, FAKE, None)
+    _expect(P, 1, P.prr_build_page_meta, d, FAKE, None, 0, 0, 1, FAKE, None)
+    _expect(P, 1, P.prr_build_page_meta, d, FAKE, None, 1601, 0, 100, FAKE, None)
+    _expect(P, 1, P.prr_build_page_meta, d, FAKE, None, 1600, 0, 101, FAKE, None)
+    _expect(P, 1, P.prr_build_page_meta, d, FAKE, None, 1600, 5, 4, FAKE, None)
+
+
+def test_bad_score_topk_args(P):
+    d = P.make_dims(32, 2, 16, 100, P.PRR_BF16)
+    ws = P.prr_workspace_size(d, 16, 8)
+    args = dict(q=FAKE, meta=FAKE, num_pages=100, k=16, forced=[], fib=True, scores=FAKE, sel=FAKE, cnt=FAKE,
+                cap=16, ws=FAKE, wsb=ws)
+
+    def call(**over):
+        a = dict(args, **over)
+        P.prr_score_topk(d, a["q"], a["meta"], a["num_pages"], a["k"], a["forced"], a["fib"], a["scores"], a["sel"],
+                         a["cnt"], a["cap"], a["ws"], a["wsb"])
+
+    _expect(P, 1, call, num_pages=0)
+    _expect(P, 1, call, num_pages=101)
+    _expect(P, 1, call, k=-1)
+    _expect(P, 1, call, k=17)  # |A| exceeds cap
+    _expect(P, 1, call, forced=[3, 3])
+    _expect(P, 1, call, forced=[100])
+    _expect(P, 1, call, forced=[1], fib=False)  # 16 + 1 > cap
+    _expect(P, 1, call, forced=list(range(65)))
+    _expect(P, 1, call, cap=0)
+    _expect(P, 1, call, cap=2000)
+    _expect(P, 1, call, q=FAKE + 8)
+    _expect(P, 3, call, wsb=16)
+    _expect(P, 1, call, ws=FAKE + 64)
+
+
+def test_bad_predict_args(P):
+    d = P.make_dims(4, 1, 16, 128, P.PRR_F16)
+
+    def call(alpha=0.5, beta=0.5, gamma=0.0, p=16, cap=16, n=128):
+        P.prr_predict(d, FAKE, FAKE, FAKE, None, n, alpha, beta, gamma, p, [], True, FAKE, FAKE, cap)
+
+    _expect(P, 1, call, alpha=0.0)
+    _expect(P, 1, call, alpha=1.5)
+    _expect(P, 1, call, beta=0.0)
+    _expect(P, 1, call, gamma=-0.1)
+    _expect(P, 1, call, gamma=1.1)
+    _expect(P, 1, call, p=-1)
+    _expect(P, 1, call, p=17)
+    _expect(P, 1, call, n=129)
+
+
+def test_bad_spec_and_repair_args(P):
+    d = P.make_dims(32, 2, 16, 100, P.PRR_BF16)
+    ws = P.prr_workspace_size(d, 16, 8)
+    _expect(P, 1, P.prr_spec_attn, d, FAKE, FAKE, FAKE, None, 1600, FAKE, FAKE, 16, 0, FAKE, FAKE, FAKE, None)
+    _expect(P, 1, P.prr_spec_attn, d, FAKE, FAKE, FAKE, None, 1600, FAKE, FAKE, 16, 17, FAKE, FAKE, FAKE, None)
+    _expect(P, 1, P.prr_spec_attn, d, FAKE, FAKE, FAKE, None, 0, FAKE, FAKE, 16, 8, FAKE, FAKE, FAKE, None)
+    _expect(P, 1, P.prr_spec_attn, d, FAKE, FAKE, FAKE, None, 1600, FAKE, FAKE, 16, 8, FAKE + 4, FAKE, FAKE, None)
+
+    def rep(pred=FAKE, pcnt=FAKE, mode=0, nt=1600, npg=100, wsb=ws, chunk=8):
+        P.prr_repair(d, FAKE, FAKE, FAKE, None, nt, npg, FAKE, FAKE, pred, pcnt, 16, chunk, FAKE, FAKE, FAKE, None,
+                     mode, FAKE, None, FAKE, FAKE, None, None, FAKE, wsb)
+
+    _expect(P, 1, rep, pcnt=None)
+    _expect(P, 1, rep, mode=2)
+    _expect(P, 1, rep, npg=101)
+    _expect(P, 1, rep, nt=1500)  # num_pages exceeds ceil(num_tokens / page_size)
+    _expect(P, 3, rep, wsb=ws - 256)
+    _expect(P, 3, rep, chunk=4)  # workspace sized for chunk 8 is too small for chunk 4
+    _expect(P, 1, P.prr_merge_states, 1, 1, 2000, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    _expect(P, 1, P.prr_workspace_init, FAKE + 16, 256)
+
+
+def test_last_error_is_thread_local(P):
+    import threading
+    d = P.make_dims(32, 2, 16, 100, P.PRR_BF16)
+    with pytest.raises(P.PrrError):
+        P.prr_build_page_meta(d, None, None, 1600, 0, 100, FAKE, None)
+    msg = []
+    t = threading.Thread(target=lambda: msg.append(P.last_error()))
+    t.start()
+    t.join()
+    assert msg == [""] and "k_cache" in P.last_error()
