@@ -153,6 +153,32 @@ __device__ __forceinline__ void block_minmax_u32(uint32_t& lo, uint32_t& hi, uin
   __syncthreads();
 }
 
+// ------------------------------------------------------------------ cross-workgroup publishing
+// Data that one workgroup hands to another inside the same launch is written with
+// device-coherent stores (they bypass the per-XCD L2s' non-coherent caching), the
+// writer waits for its stores to complete before it bumps a counter, and the reader
+// loads the data with device-coherent loads after it has observed the counter.  This
+// avoids the whole-L2 write-back and invalidate of a device-scope fence.
+
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// every store of this thread has completed before anything after this point is issued
+__device__ __forceinline__ void stores_complete() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+__device__ __forceinline__ uint32_t counter_add(uint32_t* p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Sticky error bits written by kernels into the workspace flag word.
 constexpr uint32_t kFlagBadListEntry = 1u;
 constexpr uint32_t kFlagSpinTimeout = 2u;

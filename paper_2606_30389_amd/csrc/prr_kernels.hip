@@ -161,42 +161,75 @@ hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream) {
 // =====================================================================================
 // block top-K select (shared by score_topk and predict)
 // =====================================================================================
-// Candidates are the pages whose bit is set in `candb`; pages in `forceb` are always
-// selected.  The threshold key T (the kextra-th largest candidate key) is found by
-// radix passes over the key range [lo, hi] with 4096 bins: each pass keeps only the
-// bin that holds the wanted rank, so at most three passes are needed and usually two.
-// Then every candidate above T and the lowest-indexed candidates equal to T are
-// emitted in ascending page order (ballot compaction over contiguous per-wave ranges).
+// 256 threads; thread (wave w, lane) owns pages p_j = w*J*64 + j*64 + lane, j < J, with
+// their keys in registers.  Candidates have their bit set in `cand`, pages in `force`
+// are always selected.  The threshold key T (the kextra-th largest candidate key) is
+// found by radix passes over the key range [lo, hi] with 4096 LDS bins: each pass keeps
+// only the bin that holds the wanted rank, so at most three passes are needed and
+// usually two.  Every candidate above T and the lowest-indexed candidates equal to T
+// are then emitted in ascending page order by ballot compaction.
 
+constexpr int kSelThreads = 256;
 constexpr int kSelLog2Bins = 12;
 constexpr int kSelBins = 1 << kSelLog2Bins;
 
 struct SelectScratch {
   uint32_t hist[kSelBins];
+  uint32_t forceb[PRR_MAX_PAGES_DEV / 32];
   int red[64];
   uint32_t ured[64];
 };
 
-template <int NT>
-__device__ void select_topk_block(const uint32_t* keys, const uint32_t* candb, const uint32_t* forceb, int n,
-                                  int kextra, int32_t* __restrict__ out, int cap, int32_t* __restrict__ out_count,
-                                  SelectScratch& ss) {
-  constexpr int NW = NT / kWave;
-  const int t = threadIdx.x;
-  const int lane = lane_id(), w = t / kWave;
+__host__ __device__ inline int select_j(int n) {
+  int j = 1;
+  while (j * kSelThreads < n) j <<= 1;
+  return j;
+}
 
-  int cnt = 0;
+__device__ __forceinline__ int sel_page(int j, int J) {
+  return (threadIdx.x / kWave) * J * kWave + j * kWave + lane_id();
+}
+
+template <int J>
+__device__ __forceinline__ void select_topk_regs(const uint32_t (&key)[J], uint64_t cand, uint64_t force, int n,
+                                                 int kextra, int32_t* __restrict__ out, int cap,
+                                                 int32_t* __restrict__ out_count, SelectScratch& ss) {
+  constexpr int MAXJ = J;
+  constexpr int NT = kSelThreads, NW = NT / kWave;
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+
+  int cnt = __popcll(cand);
   uint32_t lo = 0xffffffffu, hi = 0u;
-  for (int p = t; p < n; p += NT) {
-    if ((candb[p >> 5] >> (p & 31)) & 1u) {
-      const uint32_t key = keys[p];
-      ++cnt;
-      lo = min(lo, key);
-      hi = max(hi, key);
+#pragma unroll
+  for (int j = 0; j < MAXJ; ++j) {
+    if ((cand >> j) & 1ull) {
+      lo = min(lo, key[j]);
+      hi = max(hi, key[j]);
     }
   }
-  cnt = block_sum<NT>(cnt, ss.red);
-  block_minmax_u32<NT>(lo, hi, ss.ured);
+  // one exchange for count, min and max
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    cnt += __shfl_xor(cnt, o);
+    lo = min(lo, (uint32_t)__shfl_xor((int)lo, o));
+    hi = max(hi, (uint32_t)__shfl_xor((int)hi, o));
+  }
+  if (lane == 0) {
+    ss.red[w] = cnt;
+    ss.ured[w] = lo;
+    ss.ured[NW + w] = hi;
+  }
+  __syncthreads();
+  cnt = 0;
+  lo = 0xffffffffu;
+  hi = 0u;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    cnt += ss.red[i];
+    lo = min(lo, ss.ured[i]);
+    hi = max(hi, ss.ured[NW + i]);
+  }
+  __syncthreads();
 
   int mode;  // 0: no candidate taken, 1: all candidates, 2: threshold
   uint32_t T = 0;
@@ -218,18 +251,16 @@ __device__ void select_topk_block(const uint32_t* keys, const uint32_t* candb, c
       const int shift = bits > kSelLog2Bins ? bits - kSelLog2Bins : 0;
       for (int b = t; b < kSelBins; b += NT) ss.hist[b] = 0u;
       __syncthreads();
-      for (int p = t; p < n; p += NT) {
-        if ((candb[p >> 5] >> (p & 31)) & 1u) {
-          const uint32_t key = keys[p];
-          if (key >= lo && key <= hi) atomicAdd(&ss.hist[(key - lo) >> shift], 1u);
-        }
+#pragma unroll
+      for (int j = 0; j < MAXJ; ++j) {
+        if (((cand >> j) & 1ull) && key[j] >= lo && key[j] <= hi) atomicAdd(&ss.hist[(key[j] - lo) >> shift], 1u);
       }
       __syncthreads();
       constexpr int BPT = kSelBins / NT;
       const int top = kSelBins - t * BPT;  // this thread owns bins [top - BPT, top)
       int local = 0;
 #pragma unroll
-      for (int i = 1; i <= BPT; ++i) local += (int)ss.hist[top - i];
+      for (int i = 0; i < BPT; ++i) local += (int)ss.hist[top - 1 - ((i + t) & (BPT - 1))];  // rotated: few bank conflicts
       int tot;
       const int before = block_exclusive_scan<NT>(local, ss.red, tot);
       if (before < r && before + local >= r) {
@@ -262,72 +293,53 @@ __device__ void select_topk_block(const uint32_t* keys, const uint32_t* candb, c
     need_eq = r;
   }
 
-  // compaction in ascending page order
-  const int ppw = (((n + NW - 1) / NW) + 63) & ~63;
-  const int wb = w * ppw, we = min(n, wb + ppw);
-  int gtf = 0, eqc = 0;
-  for (int base = wb; base < we; base += kWave) {
-    const int p = base + lane;
-    bool f = false, g = false, e = false;
-    if (p < we) {
-      f = (forceb[p >> 5] >> (p & 31)) & 1u;
-      if ((candb[p >> 5] >> (p & 31)) & 1u) {
-        if (mode == 1) {
-          g = true;
-        } else if (mode == 2) {
-          const uint32_t key = keys[p];
-          g = key > T;
-          e = key == T;
-        }
-      }
+  // compaction in ascending page order: wave w owns pages [w*J*64, (w+1)*J*64)
+  uint64_t gt = 0, eq = 0;
+#pragma unroll
+  for (int j = 0; j < MAXJ; ++j) {
+    if ((cand >> j) & 1ull) {
+      if (mode == 1 || (mode == 2 && key[j] > T)) gt |= 1ull << j;
+      if (mode == 2 && key[j] == T) eq |= 1ull << j;
     }
-    gtf += __popcll(__ballot(f || g));
-    eqc += __popcll(__ballot(e));
+  }
+  gt |= force;
+  int gtf = __popcll(gt), eqc = __popcll(eq);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    gtf += __shfl_xor(gtf, o);
+    eqc += __shfl_xor(eqc, o);
   }
   if (lane == 0) {
     ss.red[w] = gtf;
     ss.red[NW + w] = eqc;
   }
   __syncthreads();
-  int eq_base = 0, sel_base = 0, total = 0;
+  int eq_run = 0, sel_run = 0, total = 0;
   {
     int eb = 0, sb = 0;
+#pragma unroll
     for (int i = 0; i < NW; ++i) {
       const int gi = ss.red[i], ei = ss.red[NW + i];
       const int take = max(0, min(ei, need_eq - eb));
       if (i == w) {
-        eq_base = eb;
-        sel_base = sb;
+        eq_run = eb;
+        sel_run = sb;
       }
       eb += ei;
       sb += gi + take;
     }
     total = sb;
   }
-  __syncthreads();
-  int eq_run = eq_base, sel_run = sel_base;
-  for (int base = wb; base < we; base += kWave) {
-    const int p = base + lane;
-    bool f = false, g = false, e = false;
-    if (p < we) {
-      f = (forceb[p >> 5] >> (p & 31)) & 1u;
-      if ((candb[p >> 5] >> (p & 31)) & 1u) {
-        if (mode == 1) {
-          g = true;
-        } else if (mode == 2) {
-          const uint32_t key = keys[p];
-          g = key > T;
-          e = key == T;
-        }
-      }
-    }
+#pragma unroll
+  for (int j = 0; j < MAXJ; ++j) {
+    const bool e = (eq >> j) & 1ull;
     const uint64_t em = __ballot(e);
     const bool take_eq = e && (eq_run + lanes_below(em) < need_eq);
-    const bool sel = f || g || take_eq;
+    const bool sel = ((gt >> j) & 1ull) || take_eq;
     const uint64_t sm = __ballot(sel);
     if (sel) {
       const int pos = sel_run + lanes_below(sm);
-      if (pos < cap) out[pos] = p;
+      if (pos < cap) out[pos] = sel_page(j, J);
     }
     eq_run += __popcll(em);
     sel_run += __popcll(sm);
@@ -335,30 +347,24 @@ __device__ void select_topk_block(const uint32_t* keys, const uint32_t* candb, c
   if (t == 0) *out_count = min(total, cap);
 }
 
-// Dynamic LDS layout of a select: keys [n] | candb [nw] | forceb [nw] | SelectScratch.
-__host__ __device__ inline size_t select_lds_bytes(int n) {
-  const size_t nw = (size_t)(n + 31) / 32;
-  size_t b = (size_t)n * 4 + 2 * nw * 4;
-  b = (b + 15) & ~(size_t)15;
-  return b + sizeof(SelectScratch);
-}
-
-struct SelectLds {
-  uint32_t* keys;
-  uint32_t* candb;
-  uint32_t* forceb;
-  SelectScratch* ss;
-};
-
-__device__ inline SelectLds carve_select_lds(uint32_t* dyn, int n) {
-  SelectLds s;
+// Forced pages as a bitmap in LDS; returns this thread's J-bit mask.
+template <int J>
+__device__ __forceinline__ uint64_t forced_mask(const int32_t* forced, int n_forced, int n, uint32_t* forceb) {
   const int nw = (n + 31) / 32;
-  s.keys = dyn;
-  s.candb = dyn + n;
-  s.forceb = s.candb + nw;
-  size_t off = ((size_t)n * 4 + 2 * (size_t)nw * 4 + 15) & ~(size_t)15;
-  s.ss = reinterpret_cast<SelectScratch*>(reinterpret_cast<char*>(dyn) + off);
-  return s;
+  for (int i = threadIdx.x; i < nw; i += kSelThreads) forceb[i] = 0u;
+  __syncthreads();
+  if ((int)threadIdx.x < n_forced) {
+    const int p = forced[threadIdx.x];
+    atomicOr(&forceb[p >> 5], 1u << (p & 31));
+  }
+  __syncthreads();
+  uint64_t m = 0;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int p = min(sel_page(j, J), n - 1);
+    if (sel_page(j, J) < n && ((forceb[p >> 5] >> (p & 31)) & 1u)) m |= 1ull << j;
+  }
+  return m;
 }
 
 // =====================================================================================
@@ -369,22 +375,53 @@ __device__ inline SelectLds carve_select_lds(uint32_t* dyn, int n) {
 
 constexpr int kScorePagesPerWg = 64;
 
+// The selecting workgroup: this KV head's scores (published by every workgroup with
+// device-coherent stores) into registers, then the block select.
+template <int J>
+__device__ __forceinline__ void select_scores(const float* scores, int n, const ScoreLaunch& a, int h,
+                                              SelectScratch& ss) {
+  uint32_t key[J];
+  uint64_t cand = 0;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int p = sel_page(j, J);
+    key[j] = score_key(ld_dev(&scores[min(p, n - 1)]));
+    if (p < n) cand |= 1ull << j;
+  }
+  const uint64_t force = forced_mask<J>(a.forced, a.n_forced, n, ss.forceb);
+  cand &= ~force;
+  select_topk_regs<J>(key, cand, force, n, a.kextra, a.selected + (size_t)h * a.cap, a.cap, a.selected_count + h,
+                      ss);
+}
+
 template <bool BF16, bool MEAN>
 __global__ __launch_bounds__(256) void score_topk_kernel(const ScoreLaunch a) {
-  extern __shared__ uint32_t dyn_lds[];
+  __shared__ uint32_t dyn_lds[sizeof(SelectScratch) / 4];
   __shared__ float qbar[kHeadDim];
+  __shared__ float qpart[16][kHeadDim];
   __shared__ int s_last;
   const int h = blockIdx.y;
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int G = a.group;
   const uint16_t* q = static_cast<const uint16_t*>(a.q);
 
-  if (t < kHeadDim) {
-    float s = 0.0f;
-    for (int g = 0; g < G; ++g) s += h2f<BF16>(q[(size_t)(h * G + g) * kHeadDim + t]);
-    qbar[t] = s / (float)G;
+  {
+    // thread t loads 8 channels of query head t/16 of this group (one 16-byte load);
+    // the group mean is then summed in head order from LDS
+    const int g = t >> 4, c8 = (t & 15) * 8;
+    if (g < G) {
+      const uint4 v = *reinterpret_cast<const uint4*>(q + (size_t)(h * G + g) * kHeadDim + c8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qpart[g][c8 + e] = u4_elem<BF16>(v, e);
+    }
+    __syncthreads();
+    if (t < kHeadDim) {
+      float s = 0.0f;
+      for (int gg = 0; gg < G; ++gg) s += qpart[gg][t];
+      qbar[t] = s / (float)G;
+    }
+    __syncthreads();
   }
-  __syncthreads();
 
   const int cg = lane & 15, pi = lane >> 4;
   float qb[8];
@@ -414,7 +451,7 @@ __global__ __launch_bounds__(256) void score_topk_kernel(const ScoreLaunch a) {
         for (int e = 0; e < 8; ++e) s += fmaxf(qb[e] * u4_elem<BF16>(mn[it], e), qb[e] * u4_elem<BF16>(mx[it], e));
       }
       s = sum16(s);
-      if (cg == 0 && page < a.num_pages) scores[page] = s;
+      if (cg == 0 && page < a.num_pages) st_dev(&scores[page], s);
     }
   } else {
     const float* meta = static_cast<const float*>(a.meta);
@@ -443,39 +480,32 @@ __global__ __launch_bounds__(256) void score_topk_kernel(const ScoreLaunch a) {
         s += qb[7] * m1[it].w;
       }
       s = sum16(s);
-      if (cg == 0 && page < a.num_pages) scores[page] = s;
+      if (cg == 0 && page < a.num_pages) st_dev(&scores[page], s);
     }
   }
 
-  // the last workgroup of this KV head selects
-  __threadfence();
+  // the last workgroup of this KV head selects: scores are published with device-coherent
+  // stores, completed before the counter is bumped, and read back the same way
+  stores_complete();
   __syncthreads();
   if (t == 0) {
-    const uint32_t old = atomicAdd(&a.counters[h], 1u);
+    const uint32_t old = counter_add(&a.counters[h], 1u);
     s_last = (old == (uint32_t)(gridDim.x - 1));
   }
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
 
   const int n = a.num_pages;
-  const int nw = (n + 31) / 32;
-  SelectLds L = carve_select_lds(dyn_lds, n);
-  for (int p = t; p < n; p += 256) L.keys[p] = score_key(scores[p]);
-  for (int i = t; i < nw; i += 256) {
-    const int rem = n - i * 32;
-    L.candb[i] = rem >= 32 ? 0xffffffffu : ((1u << rem) - 1u);
-    L.forceb[i] = 0u;
+  SelectScratch& ss = *reinterpret_cast<SelectScratch*>(dyn_lds);
+  switch (select_j(n)) {
+    case 1: select_scores<1>(scores, n, a, h, ss); break;
+    case 2: select_scores<2>(scores, n, a, h, ss); break;
+    case 4: select_scores<4>(scores, n, a, h, ss); break;
+    case 8: select_scores<8>(scores, n, a, h, ss); break;
+    case 16: select_scores<16>(scores, n, a, h, ss); break;
+    case 32: select_scores<32>(scores, n, a, h, ss); break;
+    default: select_scores<64>(scores, n, a, h, ss); break;
   }
-  __syncthreads();
-  if (t < a.n_forced) {
-    const int p = a.forced[t];
-    atomicOr(&L.forceb[p >> 5], 1u << (p & 31));
-    atomicAnd(&L.candb[p >> 5], ~(1u << (p & 31)));
-  }
-  __syncthreads();
-  select_topk_block<256>(L.keys, L.candb, L.forceb, n, a.kextra, a.selected + (size_t)h * a.cap, a.cap,
-                         a.selected_count + h, *L.ss);
   if (t == 0) atomicExch(&a.counters[h], 0u);
 }
 
@@ -483,65 +513,75 @@ __global__ __launch_bounds__(256) void score_topk_kernel(const ScoreLaunch a) {
 // EMA predictor
 // =====================================================================================
 
-template <int NT>
-__global__ __launch_bounds__(NT) void predict_kernel(const PredictLaunch a) {
-  extern __shared__ uint32_t dyn_lds[];
-  const int h = blockIdx.x;
-  const int t = threadIdx.x, lane = lane_id();
+template <int J>
+__device__ __forceinline__ void predict_head(const PredictLaunch& a, int h, SelectScratch& ss) {
+  const int lane = lane_id();
   const int n = a.num_pages;
   const int nwmax = (a.max_pages + 31) / 32;
-  SelectLds L = carve_select_lds(dyn_lds, n);
   float* level = a.level + (size_t)h * a.max_pages;
   float* trend = a.trend + (size_t)h * a.max_pages;
   uint32_t* bits = a.init_bits + (size_t)h * nwmax;
   const float* scores = a.scores ? a.scores + (size_t)h * a.max_pages : nullptr;
-  const int nround = (n + NT - 1) / NT;
-  for (int r = 0; r < nround; ++r) {
-    const int p = r * NT + t;  // a wave covers 64 consecutive pages = two bit words
+  // all loads first (clamped addresses; a wave covers 64 consecutive pages = two bit words per j)
+  float lv[J], tv[J], sc[J];
+  uint32_t bw[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int p = min(sel_page(j, J), n - 1);
+    lv[j] = level[p];
+    tv[j] = trend[p];
+    sc[j] = scores ? scores[p] : 0.0f;
+    bw[j] = bits[p >> 5];
+  }
+  uint32_t key[J];
+  uint64_t cand = 0;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int p = sel_page(j, J);
     const bool inr = p < n;
-    bool has = false;
-    float pred = 0.0f;
-    if (inr) {
-      has = (bits[p >> 5] >> (p & 31)) & 1u;
-      float lv = level[p], tv = trend[p];
-      if (scores) {
-        const float s = scores[p];
-        if (has) {
-          tv = a.beta * (s - lv) + (1.0f - a.beta) * tv;  // Eq. (3): the trend reads the previous level
-          lv = a.alpha * s + (1.0f - a.alpha) * lv;
-        } else {
-          lv = s;
-          tv = 0.0f;
-          has = true;
-        }
-        level[p] = lv;
-        trend[p] = tv;
+    bool has = inr && ((bw[j] >> (p & 31)) & 1u);
+    float l = lv[j], v = tv[j];
+    if (inr && scores) {
+      const float s = sc[j];
+      if (has) {
+        v = a.beta * (s - l) + (1.0f - a.beta) * v;  // Eq. (3): the trend reads the previous level
+        l = a.alpha * s + (1.0f - a.alpha) * l;
+      } else {
+        l = s;
+        v = 0.0f;
+        has = true;
       }
-      pred = lv + a.gamma * tv;  // Eq. (2)
-      L.keys[p] = score_key(pred);
+      level[p] = l;
+      trend[p] = v;
     }
+    key[j] = score_key(l + a.gamma * v);  // Eq. (2)
+    if (has) cand |= 1ull << j;
     const uint64_t hm = __ballot(has);
     const uint64_t vm = __ballot(inr);
-    if (lane == 0 || lane == 32) {
-      const int wd = (r * NT + (t & ~63) + lane) >> 5;
+    if (scores && (lane == 0 || lane == 32)) {
       const uint32_t hbits = (uint32_t)(lane == 0 ? hm : (hm >> 32));
       const uint32_t vbits = (uint32_t)(lane == 0 ? vm : (vm >> 32));
-      if (vbits) {
-        L.candb[wd] = hbits;
-        L.forceb[wd] = 0u;
-        if (scores) bits[wd] = (bits[wd] & ~vbits) | hbits;
-      }
+      if (vbits) bits[p >> 5] = (bw[j] & ~vbits) | hbits;
     }
   }
-  __syncthreads();
-  if (t < a.n_forced) {
-    const int p = a.forced[t];
-    atomicOr(&L.forceb[p >> 5], 1u << (p & 31));
-    atomicAnd(&L.candb[p >> 5], ~(1u << (p & 31)));
+  const uint64_t force = forced_mask<J>(a.forced, a.n_forced, n, ss.forceb);
+  cand &= ~force;
+  select_topk_regs<J>(key, cand, force, n, a.kextra, a.predicted + (size_t)h * a.cap, a.cap,
+                      a.predicted_count + h, ss);
+}
+
+__global__ __launch_bounds__(256) void predict_kernel(const PredictLaunch a) {
+  __shared__ SelectScratch ss;
+  const int h = blockIdx.x;
+  switch (select_j(a.num_pages)) {
+    case 1: predict_head<1>(a, h, ss); break;
+    case 2: predict_head<2>(a, h, ss); break;
+    case 4: predict_head<4>(a, h, ss); break;
+    case 8: predict_head<8>(a, h, ss); break;
+    case 16: predict_head<16>(a, h, ss); break;
+    case 32: predict_head<32>(a, h, ss); break;
+    default: predict_head<64>(a, h, ss); break;
   }
-  __syncthreads();
-  select_topk_block<NT>(L.keys, L.candb, L.forceb, n, a.kextra, a.predicted + (size_t)h * a.cap, a.cap,
-                        a.predicted_count + h, *L.ss);
 }
 
 // =====================================================================================
@@ -620,30 +660,35 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
     for (int s = 0; s < 4; ++s) qf[s] = u32x4_t{0, 0, 0, 0};
   }
 
+  // list entries w, w+4, w+8, w+12 of this wave: ids first, then page-table entries, each
+  // group issued together (wave-uniform values)
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  int pg[4], ph[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const int i = wu + 4 * kk;
+    pg[kk] = i < cnt ? pages[i] : -1;
+  }
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    pg[kk] = __builtin_amdgcn_readfirstlane(pg[kk]);
+    const bool in_list = (wu + 4 * kk) < cnt;
+    const bool valid = pg[kk] >= 0 && pg[kk] < c.num_pages;
+    if (in_list && !valid && flags && lane == 0) atomicOr(flags, kFlagBadListEntry);
+    if (!valid) pg[kk] = -1;
+  }
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) ph[kk] = (pg[kk] >= 0 && c.ptab) ? c.ptab[pg[kk]] : pg[kk];
   size_t off[4];
   int tok0[4];
   bool ok[4];
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) {
-    const int i = w + 4 * kk;
-    ok[kk] = false;
-    off[kk] = 0;
-    tok0[kk] = 0;
-    if (i < cnt) {
-      const int pg = pages[i];
-      if (pg >= 0 && pg < c.num_pages) {
-        const int phys = c.ptab ? c.ptab[pg] : pg;
-        if (phys >= 0 && phys < c.max_pages) {
-          ok[kk] = true;
-          off[kk] = (size_t)phys * PS * kHeadDim;
-          tok0[kk] = pg * PS;
-        } else if (flags && lane == 0) {
-          atomicOr(flags, kFlagBadListEntry);
-        }
-      } else if (flags && lane == 0) {
-        atomicOr(flags, kFlagBadListEntry);
-      }
-    }
+    const int phys = __builtin_amdgcn_readfirstlane(ph[kk]);
+    ok[kk] = pg[kk] >= 0 && phys >= 0 && phys < c.max_pages;
+    if (pg[kk] >= 0 && !ok[kk] && flags && lane == 0) atomicOr(flags, kFlagBadListEntry);
+    off[kk] = ok[kk] ? (size_t)phys * PS * kHeadDim : 0;
+    tok0[kk] = ok[kk] ? pg[kk] * PS : 0;
   }
 
   f32x4_t acc[8];
@@ -829,8 +874,15 @@ struct RepairLds {
   int32_t xpages[16];
   int32_t xslots[16];
   int red[64];
+  float fred[2][8];
   int nM, nW, nCont, nWp, nXp, bad;
-  UnitLds unit;
+  union {
+    UnitLds unit;  // work workgroups
+    struct {       // merge workgroups: (m, l) then weight of every state, for two query heads
+      float m[2][2 * PRR_MAX_CAP_DEV];
+      float w[2][2 * PRR_MAX_CAP_DEV];
+    } merge;
+  };
 };
 
 template <bool BF16, int PS>
@@ -1015,27 +1067,28 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
       if (recompute) attend_unit<BF16, PS>(ctx, S.xpages, nxp, nullptr, S.unit, a.flags, r);
       have = true;
     }
+    // publish the unit state to the merge workgroups (device-coherent stores, completed
+    // before the counter is bumped)
     if (have && hh < G) {
       const size_t row = ((size_t)h * a.nwork + u) * G + hh;
-      float4* dst = reinterpret_cast<float4*>(a.ws_o + row * kHeadDim + c0);
-      dst[0] = make_float4(r.o[0], r.o[1], r.o[2], r.o[3]);
-      dst[1] = make_float4(r.o[4], r.o[5], r.o[6], r.o[7]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) st_dev(a.ws_o + row * kHeadDim + c0 + e, r.o[e]);
       if ((t & 15) == 0) {
-        a.ws_ml[row * 2] = r.m;
-        a.ws_ml[row * 2 + 1] = r.l;
+        st_dev(a.ws_ml + row * 2, r.m);
+        st_dev(a.ws_ml + row * 2 + 1, r.l);
       }
     }
-    __threadfence();
+    stores_complete();
     __syncthreads();
-    if (t == 0) atomicAdd(&a.ws_cnt[h], 1u);
+    if (t == 0) counter_add(&a.ws_cnt[h], 1u);
     return;
   }
 
   // ---- merge
   if (t == 0) {
     int it = 0;
-    while (__hip_atomic_load(&a.ws_cnt[h], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)a.nwork) {
-      __builtin_amdgcn_s_sleep(2);
+    while (ld_dev(&a.ws_cnt[h]) < (uint32_t)a.nwork) {
+      __builtin_amdgcn_s_sleep(1);
       if (++it > kSpinLimit) {
         atomicOr(a.flags, kFlagSpinTimeout);
         break;
@@ -1043,42 +1096,91 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
     }
   }
   __syncthreads();
-  __threadfence();
-  const int g = pair * 2 + (t >> 7);
-  const int ch = t & 127;
   const int nchP = (nP + C - 1) / C;
   const int nUnits = nMU + (exact ? nCont : 0);
+  const int ns = nchP + nUnits;
+  const float kNegInf = -__builtin_inff();
+  // stage (m, l) of every state; chunks replaced by a unit state get weight zero
+  for (int i = t; i < ns; i += 256) {
+#pragma unroll
+    for (int gi = 0; gi < 2; ++gi) {
+      const int g = pair * 2 + gi;
+      float m = kNegInf, l = 0.f;
+      if (g < G) {
+        if (i < nchP) {
+          if (!(exact && ((S.contam_bits[i >> 5] >> (i & 31)) & 1u))) {
+            const size_t row = ((size_t)h * a.nchunks + i) * G + g;
+            m = a.part_m[row];
+            l = a.part_l[row];
+          }
+        } else {
+          const size_t row = ((size_t)h * a.nwork + (i - nchP)) * G + g;
+          m = ld_dev(a.ws_ml + row * 2);
+          l = ld_dev(a.ws_ml + row * 2 + 1);
+        }
+      }
+      S.merge.m[gi][i] = l > 0.f ? m : kNegInf;
+      S.merge.w[gi][i] = l;
+    }
+  }
+  __syncthreads();
+  const int lane = lane_id(), wv = t / kWave;
+  float mx0 = kNegInf, mx1 = kNegInf;
+  for (int i = t; i < ns; i += 256) {
+    mx0 = fmaxf(mx0, S.merge.m[0][i]);
+    mx1 = fmaxf(mx1, S.merge.m[1][i]);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    mx0 = fmaxf(mx0, __shfl_xor(mx0, o));
+    mx1 = fmaxf(mx1, __shfl_xor(mx1, o));
+  }
+  if (lane == 0) {
+    S.fred[0][wv] = mx0;
+    S.fred[1][wv] = mx1;
+  }
+  __syncthreads();
+  const float ms0 = fmaxf(fmaxf(S.fred[0][0], S.fred[0][1]), fmaxf(S.fred[0][2], S.fred[0][3]));
+  const float ms1 = fmaxf(fmaxf(S.fred[1][0], S.fred[1][1]), fmaxf(S.fred[1][2], S.fred[1][3]));
+  __syncthreads();
+  float l0 = 0.f, l1 = 0.f;
+  for (int i = t; i < ns; i += 256) {
+    const float w0 = S.merge.w[0][i] > 0.f ? S.merge.w[0][i] * exp2f((S.merge.m[0][i] - ms0) * kLog2e) : 0.f;
+    const float w1 = S.merge.w[1][i] > 0.f ? S.merge.w[1][i] * exp2f((S.merge.m[1][i] - ms1) * kLog2e) : 0.f;
+    S.merge.w[0][i] = w0;
+    S.merge.w[1][i] = w1;
+    l0 += w0;
+    l1 += w1;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    l0 += __shfl_xor(l0, o);
+    l1 += __shfl_xor(l1, o);
+  }
+  if (lane == 0) {
+    S.fred[0][4 + wv] = l0;
+    S.fred[1][4 + wv] = l1;
+  }
+  __syncthreads();
+  const int gi = t >> 7, g = pair * 2 + gi, ch = t & 127;
   if (g < G) {
-    const float kNegInf = -__builtin_inff();
-    float ms = kNegInf;
+    const float L = (S.fred[gi][4] + S.fred[gi][5]) + (S.fred[gi][6] + S.fred[gi][7]);
+    const float ms = gi == 0 ? ms0 : ms1;
+    const float* wts = S.merge.w[gi];
+    float O = 0.f;
+    const float* po = a.part_o + ((size_t)h * a.nchunks * G + g) * kHeadDim + ch;
+#pragma unroll 8
     for (int c = 0; c < nchP; ++c) {
-      if (exact && ((S.contam_bits[c >> 5] >> (c & 31)) & 1u)) continue;
-      const size_t row = ((size_t)h * a.nchunks + c) * G + g;
-      if (a.part_l[row] > 0.f) ms = fmaxf(ms, a.part_m[row]);
+      const float v = po[(size_t)c * G * kHeadDim];
+      const float w = wts[c];
+      O += w != 0.f ? w * v : 0.f;
     }
+    const float* wo = a.ws_o + ((size_t)h * a.nwork * G + g) * kHeadDim + ch;
+#pragma unroll 8
     for (int uu = 0; uu < nUnits; ++uu) {
-      const size_t row = ((size_t)h * a.nwork + uu) * G + g;
-      if (a.ws_ml[row * 2 + 1] > 0.f) ms = fmaxf(ms, a.ws_ml[row * 2]);
-    }
-    float L = 0.f, O = 0.f;
-    for (int c = 0; c < nchP; ++c) {
-      if (exact && ((S.contam_bits[c >> 5] >> (c & 31)) & 1u)) continue;
-      const size_t row = ((size_t)h * a.nchunks + c) * G + g;
-      const float l = a.part_l[row];
-      if (l > 0.f) {
-        const float wgt = l * exp2f((a.part_m[row] - ms) * kLog2e);
-        L += wgt;
-        O += wgt * a.part_o[row * kHeadDim + ch];
-      }
-    }
-    for (int uu = 0; uu < nUnits; ++uu) {
-      const size_t row = ((size_t)h * a.nwork + uu) * G + g;
-      const float l = a.ws_ml[row * 2 + 1];
-      if (l > 0.f) {
-        const float wgt = l * exp2f((a.ws_ml[row * 2] - ms) * kLog2e);
-        L += wgt;
-        O += wgt * a.ws_o[row * kHeadDim + ch];
-      }
+      const float v = ld_dev(wo + (size_t)uu * G * kHeadDim);
+      const float w = wts[nchP + uu];
+      O += w != 0.f ? w * v : 0.f;
     }
     const float o = L > 0.f ? O / L : 0.f;
     const size_t orow = (size_t)h * G + g;
@@ -1167,15 +1269,13 @@ static hipError_t launch1(const void* f, dim3 grid, dim3 block, size_t lds, hipS
 
 hipError_t launch_score_topk(const ScoreLaunch& a, hipStream_t stream) {
   dim3 grid((a.num_pages + kScorePagesPerWg - 1) / kScorePagesPerWg, a.num_kv_heads);
-  const size_t lds = select_lds_bytes(a.num_pages);
   const void* f = a.bf16 ? (a.meta_mean ? (const void*)score_topk_kernel<true, true> : (const void*)score_topk_kernel<true, false>)
                          : (a.meta_mean ? (const void*)score_topk_kernel<false, true> : (const void*)score_topk_kernel<false, false>);
-  return launch1(f, grid, dim3(256), lds, stream, a);
+  return launch1(f, grid, dim3(256), 0, stream, a);
 }
 
 hipError_t launch_predict(const PredictLaunch& a, hipStream_t stream) {
-  const size_t lds = select_lds_bytes(a.num_pages);
-  return launch1((const void*)predict_kernel<256>, dim3(a.num_kv_heads), dim3(256), lds, stream, a);
+  return launch1((const void*)predict_kernel, dim3(a.num_kv_heads), dim3(256), 0, stream, a);
 }
 
 hipError_t launch_spec_attn(const SpecLaunch& a, hipStream_t stream) {
