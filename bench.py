@@ -133,6 +133,9 @@ def main():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--kernel-reps", type=int, default=4, help="tokens per kernel-timing pass")
+    ap.add_argument("--workers", type=int, default=16, help="input-generation processes (0 = in-process)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run a plain device copy of this size (calibrates HBM byte counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -155,13 +158,21 @@ def main():
     total_tokens = 1 + 2 * args.warmup + 3 * args.steps + args.kernel_reps + 8
     t0 = time.time()
     layers = [None] * n_layers
-    with mp.get_context("fork").Pool(min(16, os.cpu_count() or 1)) as pool:
-        for layer, kb, vb in pool.imap_unordered(_gen_layer, [(cfg.name, l) for l in range(n_layers)]):
-            st = R.LayerState(pc, dev, k=R.bits_tensor(kb, pc.torch_dtype, dev),
-                              v=R.bits_tensor(vb, pc.torch_dtype, dev))
-            st.build_meta()
-            layers[layer] = st
-            print(f"[bench] layer {layer} ready ({time.time() - t0:.1f}s)", file=sys.stderr, flush=True)
+
+    def add_layer(layer, kb, vb):
+        st = R.LayerState(pc, dev, k=R.bits_tensor(kb, pc.torch_dtype, dev), v=R.bits_tensor(vb, pc.torch_dtype, dev))
+        st.build_meta()
+        layers[layer] = st
+        print(f"[bench] layer {layer} ready ({time.time() - t0:.1f}s)", file=sys.stderr, flush=True)
+
+    jobs = [(cfg.name, l) for l in range(n_layers)]
+    if args.workers > 0:
+        with mp.get_context("fork").Pool(min(args.workers, os.cpu_count() or 1)) as pool:
+            for layer, kb, vb in pool.imap_unordered(_gen_layer, jobs):
+                add_layer(layer, kb, vb)
+    else:
+        for job in jobs:
+            add_layer(*_gen_layer(job))
     qs = []
     for l in range(n_layers):
         _, qb = W.query_trajectory(cfg, l, steps=total_tokens)
@@ -378,6 +389,14 @@ def main():
         "kernel_us": {k: round(v, 2) for k, v in ktimes.items()},
         "roofline": roofline,
     }
+    if args.copy_calibration_mib > 0:
+        nbytes = args.copy_calibration_mib << 20
+        src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = {"read": nbytes, "write": nbytes}
     out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds) if args.cpu_seconds > 0 else None
     print(json.dumps(out), flush=True)
 

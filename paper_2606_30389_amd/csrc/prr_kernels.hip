@@ -161,16 +161,16 @@ hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream) {
 // =====================================================================================
 // block top-K select (shared by score_topk and predict)
 // =====================================================================================
-// 256 threads; thread (wave w, lane) owns pages p_j = w*J*64 + j*64 + lane, j < J, with
+// 1024 threads; thread (wave w, lane) owns pages p_j = w*J*64 + j*64 + lane, j < J, with
 // their keys in registers.  Candidates have their bit set in `cand`, pages in `force`
 // are always selected.  The threshold key T (the kextra-th largest candidate key) is
-// found by radix passes over the key range [lo, hi] with 4096 LDS bins: each pass keeps
-// only the bin that holds the wanted rank, so at most three passes are needed and
-// usually two.  Every candidate above T and the lowest-indexed candidates equal to T
+// found by radix passes over the key range [lo, hi] with 8192 LDS bins: each pass keeps
+// only the bin that holds the wanted rank, so at most three passes are needed and two
+// whenever the candidate scores span less than a factor of eight.  Every candidate above T and the lowest-indexed candidates equal to T
 // are then emitted in ascending page order by ballot compaction.
 
-constexpr int kSelThreads = 256;
-constexpr int kSelLog2Bins = 12;
+constexpr int kSelThreads = 1024;
+constexpr int kSelLog2Bins = 13;
 constexpr int kSelBins = 1 << kSelLog2Bins;
 
 struct SelectScratch {
@@ -350,6 +350,7 @@ __device__ __forceinline__ void select_topk_regs(const uint32_t (&key)[J], uint6
 // Forced pages as a bitmap in LDS; returns this thread's J-bit mask.
 template <int J>
 __device__ __forceinline__ uint64_t forced_mask(const int32_t* forced, int n_forced, int n, uint32_t* forceb) {
+  if (n_forced == 0) return 0;
   const int nw = (n + 31) / 32;
   for (int i = threadIdx.x; i < nw; i += kSelThreads) forceb[i] = 0u;
   __syncthreads();
@@ -370,9 +371,8 @@ __device__ __forceinline__ uint64_t forced_mask(const int32_t* forced, int n_for
 // =====================================================================================
 // score + top-K
 // =====================================================================================
-// grid (ceil(num_pages / 64), Hkv), 256 threads.  Wave w of a workgroup scores pages
-// base + it*16 + w*4 + (lane/16) for it = 0..3; lane%16 covers channels 8*(lane%16)..+8.
-
+// grid (ceil(num_pages / 64), Hkv), 1024 threads.  Wave w of a workgroup scores pages
+// base + w*4 + (lane/16); lane%16 covers channels 8*(lane%16)..+8.
 constexpr int kScorePagesPerWg = 64;
 
 // The selecting workgroup: this KV head's scores (published by every workgroup with
@@ -395,7 +395,7 @@ __device__ __forceinline__ void select_scores(const float* scores, int n, const 
 }
 
 template <bool BF16, bool MEAN>
-__global__ __launch_bounds__(256) void score_topk_kernel(const ScoreLaunch a) {
+__global__ __launch_bounds__(1024) void score_topk_kernel(const ScoreLaunch a) {
   __shared__ uint32_t dyn_lds[sizeof(SelectScratch) / 4];
   __shared__ float qbar[kHeadDim];
   __shared__ float qpart[16][kHeadDim];
@@ -406,7 +406,7 @@ __global__ __launch_bounds__(256) void score_topk_kernel(const ScoreLaunch a) {
   const uint16_t* q = static_cast<const uint16_t*>(a.q);
 
   {
-    // thread t loads 8 channels of query head t/16 of this group (one 16-byte load);
+    // thread t < 16G loads 8 channels of query head t/16 of this group (one 16-byte load);
     // the group mean is then summed in head order from LDS
     const int g = t >> 4, c8 = (t & 15) * 8;
     if (g < G) {
@@ -428,61 +428,34 @@ __global__ __launch_bounds__(256) void score_topk_kernel(const ScoreLaunch a) {
 #pragma unroll
   for (int e = 0; e < 8; ++e) qb[e] = qbar[cg * 8 + e];
 
-  const int base = blockIdx.x * kScorePagesPerWg;
+  const int page = blockIdx.x * kScorePagesPerWg + w * 4 + pi;
   float* scores = a.scores + (size_t)h * a.max_pages;
+  float s = 0.0f;
   if constexpr (!MEAN) {
-    const uint16_t* meta = static_cast<const uint16_t*>(a.meta);
-    uint4 mn[4], mx[4];
+    if (page < a.num_pages) {
+      const uint16_t* row = static_cast<const uint16_t*>(a.meta) + ((size_t)h * a.max_pages + page) * 2 * kHeadDim + cg * 8;
+      const uint4 mn = *reinterpret_cast<const uint4*>(row);
+      const uint4 mx = *reinterpret_cast<const uint4*>(row + kHeadDim);
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int page = base + it * 16 + w * 4 + pi;
-      if (page < a.num_pages) {
-        const uint16_t* row = meta + ((size_t)h * a.max_pages + page) * 2 * kHeadDim + cg * 8;
-        mn[it] = *reinterpret_cast<const uint4*>(row);
-        mx[it] = *reinterpret_cast<const uint4*>(row + kHeadDim);
-      }
-    }
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int page = base + it * 16 + w * 4 + pi;
-      float s = 0.0f;
-      if (page < a.num_pages) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s += fmaxf(qb[e] * u4_elem<BF16>(mn[it], e), qb[e] * u4_elem<BF16>(mx[it], e));
-      }
-      s = sum16(s);
-      if (cg == 0 && page < a.num_pages) st_dev(&scores[page], s);
+      for (int e = 0; e < 8; ++e) s += fmaxf(qb[e] * u4_elem<BF16>(mn, e), qb[e] * u4_elem<BF16>(mx, e));
     }
   } else {
-    const float* meta = static_cast<const float*>(a.meta);
-    float4 m0[4], m1[4];
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int page = base + it * 16 + w * 4 + pi;
-      if (page < a.num_pages) {
-        const float4* row = reinterpret_cast<const float4*>(meta + ((size_t)h * a.max_pages + page) * kHeadDim + cg * 8);
-        m0[it] = row[0];
-        m1[it] = row[1];
-      }
-    }
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int page = base + it * 16 + w * 4 + pi;
-      float s = 0.0f;
-      if (page < a.num_pages) {
-        s = qb[0] * m0[it].x;
-        s += qb[1] * m0[it].y;
-        s += qb[2] * m0[it].z;
-        s += qb[3] * m0[it].w;
-        s += qb[4] * m1[it].x;
-        s += qb[5] * m1[it].y;
-        s += qb[6] * m1[it].z;
-        s += qb[7] * m1[it].w;
-      }
-      s = sum16(s);
-      if (cg == 0 && page < a.num_pages) st_dev(&scores[page], s);
+    if (page < a.num_pages) {
+      const float4* row = reinterpret_cast<const float4*>(static_cast<const float*>(a.meta) +
+                                                          ((size_t)h * a.max_pages + page) * kHeadDim + cg * 8);
+      const float4 m0 = row[0], m1 = row[1];
+      s = qb[0] * m0.x;
+      s += qb[1] * m0.y;
+      s += qb[2] * m0.z;
+      s += qb[3] * m0.w;
+      s += qb[4] * m1.x;
+      s += qb[5] * m1.y;
+      s += qb[6] * m1.z;
+      s += qb[7] * m1.w;
     }
   }
+  s = sum16(s);
+  if (cg == 0 && page < a.num_pages) st_dev(&scores[page], s);
 
   // the last workgroup of this KV head selects: scores are published with device-coherent
   // stores, completed before the counter is bumped, and read back the same way
@@ -502,9 +475,7 @@ __global__ __launch_bounds__(256) void score_topk_kernel(const ScoreLaunch a) {
     case 2: select_scores<2>(scores, n, a, h, ss); break;
     case 4: select_scores<4>(scores, n, a, h, ss); break;
     case 8: select_scores<8>(scores, n, a, h, ss); break;
-    case 16: select_scores<16>(scores, n, a, h, ss); break;
-    case 32: select_scores<32>(scores, n, a, h, ss); break;
-    default: select_scores<64>(scores, n, a, h, ss); break;
+    default: select_scores<16>(scores, n, a, h, ss); break;
   }
   if (t == 0) atomicExch(&a.counters[h], 0u);
 }
@@ -570,7 +541,7 @@ __device__ __forceinline__ void predict_head(const PredictLaunch& a, int h, Sele
                       a.predicted_count + h, ss);
 }
 
-__global__ __launch_bounds__(256) void predict_kernel(const PredictLaunch a) {
+__global__ __launch_bounds__(1024) void predict_kernel(const PredictLaunch a) {
   __shared__ SelectScratch ss;
   const int h = blockIdx.x;
   switch (select_j(a.num_pages)) {
@@ -578,9 +549,7 @@ __global__ __launch_bounds__(256) void predict_kernel(const PredictLaunch a) {
     case 2: predict_head<2>(a, h, ss); break;
     case 4: predict_head<4>(a, h, ss); break;
     case 8: predict_head<8>(a, h, ss); break;
-    case 16: predict_head<16>(a, h, ss); break;
-    case 32: predict_head<32>(a, h, ss); break;
-    default: predict_head<64>(a, h, ss); break;
+    default: predict_head<16>(a, h, ss); break;
   }
 }
 
@@ -865,30 +834,77 @@ constexpr int kSpinLimit = 1 << 24;
 struct RepairLds {
   uint32_t bitA[PRR_MAX_PAGES_DEV / 32];
   uint32_t bitP[PRR_MAX_PAGES_DEV / 32];
-  int32_t listA[PRR_MAX_CAP_DEV];
   int32_t listP[PRR_MAX_CAP_DEV];
   int32_t missed[PRR_MAX_CAP_DEV];
   int32_t contam[PRR_MAX_CAP_DEV];
   uint32_t contam_bits[PRR_MAX_CAP_DEV / 32];
+  uint8_t wflag[PRR_MAX_CAP_DEV];
+  int cnt_m[4][4], cnt_w[4][4], cnt_c[4][4];
   int32_t wpages[16];
   int32_t xpages[16];
   int32_t xslots[16];
-  int red[64];
-  float fred[2][8];
-  int nM, nW, nCont, nWp, nXp, bad;
+  float fred[2][16];
+  int nWp, nXp;
   union {
     UnitLds unit;  // work workgroups
-    struct {       // merge workgroups: (m, l) then weight of every state, for two query heads
+    struct {       // merge workgroups: (m, l) then weight of each state, for two query heads
       float m[2][2 * PRR_MAX_CAP_DEV];
       float w[2][2 * PRR_MAX_CAP_DEV];
     } merge;
   };
 };
 
+// Merge-workgroup helper: for the two query heads of this workgroup, states
+// [0, count) with (m, l) staged in S.merge; returns the max and turns l into weights
+// relative to it; the sum of the weights goes to `lsum`.
+__device__ __forceinline__ void merge_weights(RepairLds& S, int count, float (&ms)[2], float (&lsum)[2]) {
+  const int t = threadIdx.x, lane = lane_id(), wv = t / kWave;
+  const float kNegInf = -__builtin_inff();
+  float mx0 = kNegInf, mx1 = kNegInf;
+  for (int i = t; i < count; i += 256) {
+    mx0 = fmaxf(mx0, S.merge.m[0][i]);
+    mx1 = fmaxf(mx1, S.merge.m[1][i]);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    mx0 = fmaxf(mx0, __shfl_xor(mx0, o));
+    mx1 = fmaxf(mx1, __shfl_xor(mx1, o));
+  }
+  if (lane == 0) {
+    S.fred[0][wv] = mx0;
+    S.fred[1][wv] = mx1;
+  }
+  __syncthreads();
+  ms[0] = fmaxf(fmaxf(S.fred[0][0], S.fred[0][1]), fmaxf(S.fred[0][2], S.fred[0][3]));
+  ms[1] = fmaxf(fmaxf(S.fred[1][0], S.fred[1][1]), fmaxf(S.fred[1][2], S.fred[1][3]));
+  __syncthreads();
+  float l0 = 0.f, l1 = 0.f;
+  for (int i = t; i < count; i += 256) {
+    const float w0 = S.merge.w[0][i] > 0.f ? S.merge.w[0][i] * exp2f((S.merge.m[0][i] - ms[0]) * kLog2e) : 0.f;
+    const float w1 = S.merge.w[1][i] > 0.f ? S.merge.w[1][i] * exp2f((S.merge.m[1][i] - ms[1]) * kLog2e) : 0.f;
+    S.merge.w[0][i] = w0;
+    S.merge.w[1][i] = w1;
+    l0 += w0;
+    l1 += w1;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    l0 += __shfl_xor(l0, o);
+    l1 += __shfl_xor(l1, o);
+  }
+  if (lane == 0) {
+    S.fred[0][4 + wv] = l0;
+    S.fred[1][4 + wv] = l1;
+  }
+  __syncthreads();
+  lsum[0] = (S.fred[0][4] + S.fred[0][5]) + (S.fred[0][6] + S.fred[0][7]);
+  lsum[1] = (S.fred[1][4] + S.fred[1][5]) + (S.fred[1][6] + S.fred[1][7]);
+}
+
 template <bool BF16, int PS>
 __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
   __shared__ RepairLds S;
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int G = a.group, C = a.chunk;
   const int work_wgs = a.num_kv_heads * a.nwork;
   const int bid = blockIdx.x;
@@ -907,91 +923,117 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
   const int nwords = (n + 31) / 32;
   const int nA = min(max(a.selected_count[h], 0), a.cap);
   const int nP = a.predicted ? min(max(a.predicted_count[h], 0), a.cap) : 0;
+  const float kNegInf = -__builtin_inff();
 
-  // ---- plan
+  // ---- plan.  List entry i is handled by thread i % 256 in round i / 256, so a wave
+  // covers 64 consecutive entries and every compaction is a ballot.
   for (int i = t; i < nwords; i += 256) {
     S.bitA[i] = 0u;
     S.bitP[i] = 0u;
   }
-  for (int i = t; i < nA; i += 256) S.listA[i] = a.selected[(size_t)h * a.cap + i];
-  for (int i = t; i < nP; i += 256) S.listP[i] = a.predicted[(size_t)h * a.cap + i];
+  int ea[4], ep[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int i = r * 256 + t;
+    ea[r] = i < nA ? a.selected[(size_t)h * a.cap + i] : -1;
+    ep[r] = i < nP ? a.predicted[(size_t)h * a.cap + i] : -1;
+  }
   __syncthreads();
   bool bad_entry = false;
-  for (int i = t; i < nA; i += 256) {
-    const int p = S.listA[i];
-    if (p >= 0 && p < n) atomicOr(&S.bitA[p >> 5], 1u << (p & 31));
-    else bad_entry = true;
-  }
-  for (int i = t; i < nP; i += 256) {
-    const int p = S.listP[i];
-    if (p >= 0 && p < n) atomicOr(&S.bitP[p >> 5], 1u << (p & 31));
-    else bad_entry = true;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int i = r * 256 + t;
+    if (i < nA) {
+      if (ea[r] >= 0 && ea[r] < n) atomicOr(&S.bitA[ea[r] >> 5], 1u << (ea[r] & 31));
+      else bad_entry = true;
+    }
+    if (i < nP) {
+      S.listP[i] = ep[r];
+      if (ep[r] >= 0 && ep[r] < n) atomicOr(&S.bitP[ep[r] >> 5], 1u << (ep[r] & 31));
+      else bad_entry = true;
+    }
   }
   if (bad_entry && bid == 0) atomicOr(a.flags, kFlagBadListEntry);
   __syncthreads();
-  {
-    // missed = A \ P in A's order: thread t owns entries [4t, 4t+4)
-    int flags = 0, cntm = 0;
+  uint64_t bm[4], bw[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int i = 4 * t + e;
-      if (i < nA) {
-        const int p = S.listA[i];
-        if (p >= 0 && p < n && !((S.bitP[p >> 5] >> (p & 31)) & 1u)) {
-          flags |= 1 << e;
-          ++cntm;
-        }
-      }
+  for (int r = 0; r < 4; ++r) {
+    const int i = r * 256 + t;
+    const int pa = ea[r], pp = ep[r];
+    const bool missed = i < nA && pa >= 0 && pa < n && !((S.bitP[pa >> 5] >> (pa & 31)) & 1u);
+    const bool wasted = i < nP && pp >= 0 && pp < n && !((S.bitA[pp >> 5] >> (pp & 31)) & 1u);
+    if (i < nP) S.wflag[i] = wasted ? 1 : 0;
+    bm[r] = __ballot(missed);
+    bw[r] = __ballot(wasted);
+    if (lane == 0) {
+      S.cnt_m[r][w] = __popcll(bm[r]);
+      S.cnt_w[r][w] = __popcll(bw[r]);
     }
-    int tot;
-    int pos = block_exclusive_scan<256>(cntm, S.red, tot);
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (flags & (1 << e)) S.missed[pos++] = S.listA[4 * t + e];
-    if (t == 0) S.nM = tot;
-    // wasted = P \ A
-    int cw = 0;
-    for (int i = t; i < nP; i += 256) {
-      const int p = S.listP[i];
-      if (p >= 0 && p < n && !((S.bitA[p >> 5] >> (p & 31)) & 1u)) ++cw;
-    }
-    cw = block_sum<256>(cw, S.red);
-    if (t == 0) S.nW = cw;
-    // contaminated chunks (exact mode), in chunk order: thread t owns chunks [4t, 4t+4)
-    const int nch = (nP + C - 1) / C;
-    int cf = 0, cc = 0;
-    if (exact) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int ch = 4 * t + e;
-        if (ch < nch) {
-          bool dirty = false;
-          for (int i = ch * C; i < min(nP, ch * C + C); ++i) {
-            const int p = S.listP[i];
-            if (p >= 0 && p < n && !((S.bitA[p >> 5] >> (p & 31)) & 1u)) dirty = true;
-          }
-          if (dirty) {
-            cf |= 1 << e;
-            ++cc;
-          }
-        }
-      }
-    }
-    pos = block_exclusive_scan<256>(cc, S.red, tot);
-    for (int i = t; i < PRR_MAX_CAP_DEV / 32; i += 256) S.contam_bits[i] = 0u;
-    __syncthreads();
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (cf & (1 << e)) {
-        const int ch = 4 * t + e;
-        S.contam[pos++] = ch;
-        atomicOr(&S.contam_bits[ch >> 5], 1u << (ch & 31));
-      }
-    }
-    if (t == 0) S.nCont = tot;
   }
   __syncthreads();
-  const int nM = S.nM, nCont = S.nCont;
+  int nM = 0, nW = 0;
+  {
+    int base[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+#pragma unroll
+      for (int ww = 0; ww < 4; ++ww) {
+        if (r < 0 || ww < 0) continue;
+        const int c = S.cnt_m[r][ww];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+          if (r < rr || (r == rr && ww < w)) base[rr] += c;
+        nM += c;
+        nW += S.cnt_w[r][ww];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if ((bm[r] >> lane) & 1ull) S.missed[base[r] + lanes_below(bm[r])] = ea[r];
+  }
+  const int nch = (nP + C - 1) / C;
+  int nCont = 0;
+  if (exact) {
+    // chunk c (of C consecutive entries of P) holds a wasted page: thread c % 256, round c / 256
+    uint64_t bc[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int c = r * 256 + t;
+      bool dirty = false;
+      if (c < nch) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int i = c * C + e;
+          if (e < C && i < nP) dirty |= S.wflag[i] != 0;
+        }
+      }
+      bc[r] = __ballot(dirty);
+      if (lane == 0) S.cnt_c[r][w] = __popcll(bc[r]);
+    }
+    for (int i = t; i < PRR_MAX_CAP_DEV / 32; i += 256) S.contam_bits[i] = 0u;
+    __syncthreads();
+    int base[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+#pragma unroll
+      for (int ww = 0; ww < 4; ++ww) {
+        const int c = S.cnt_c[r][ww];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+          if (r < rr || (r == rr && ww < w)) base[rr] += c;
+        nCont += c;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      if ((bc[r] >> lane) & 1ull) {
+        const int c = r * 256 + t;
+        S.contam[base[r] + lanes_below(bc[r])] = c;
+        atomicOr(&S.contam_bits[c >> 5], 1u << (c & 31));
+      }
+    }
+  }
+  __syncthreads();
   const int nMU = (nM + C - 1) / C;
 
   AttnCtx ctx;
@@ -1038,7 +1080,7 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
         attend_unit<BF16, PS>(ctx, S.wpages, nwp, nullptr, S.unit, a.flags, r);
         const size_t crow = ((size_t)h * a.nchunks + ch) * G;
         bool bad = false;
-        float mx = -__builtin_inff(), mc = 0.f, lc = 0.f;
+        float mx = kNegInf, mc = 0.f, lc = 0.f;
         if (hh < G) {
           mc = a.part_m[crow + hh];
           lc = a.part_l[crow + hh];
@@ -1084,7 +1126,40 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
     return;
   }
 
-  // ---- merge
+  // ---- merge.  The clean speculative chunks are ready at launch: merge them while the
+  // work workgroups run, then wait and fold in the unit states.
+  const int nUnits = nMU + (exact ? nCont : 0);
+  const int gi = t >> 7, g = pair * 2 + gi, ch = t & 127;
+  for (int i = t; i < nch; i += 256) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int gk = pair * 2 + k;
+      float m = kNegInf, l = 0.f;
+      if (gk < G && !(exact && ((S.contam_bits[i >> 5] >> (i & 31)) & 1u))) {
+        const size_t row = ((size_t)h * a.nchunks + i) * G + gk;
+        m = a.part_m[row];
+        l = a.part_l[row];
+      }
+      S.merge.m[k][i] = l > 0.f ? m : kNegInf;
+      S.merge.w[k][i] = l;
+    }
+  }
+  __syncthreads();
+  float ms_s[2], ls_s[2];
+  merge_weights(S, nch, ms_s, ls_s);
+  float Os = 0.f;
+  if (g < G) {
+    const float* wts = S.merge.w[gi];
+    const float* po = a.part_o + ((size_t)h * a.nchunks * G + g) * kHeadDim + ch;
+#pragma unroll 8
+    for (int c = 0; c < nch; ++c) {
+      const float v = po[(size_t)c * G * kHeadDim];
+      const float wgt = wts[c];
+      Os += wgt != 0.f ? wgt * v : 0.f;
+    }
+  }
+  __syncthreads();
+
   if (t == 0) {
     int it = 0;
     while (ld_dev(&a.ws_cnt[h]) < (uint32_t)a.nwork) {
@@ -1096,92 +1171,40 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
     }
   }
   __syncthreads();
-  const int nchP = (nP + C - 1) / C;
-  const int nUnits = nMU + (exact ? nCont : 0);
-  const int ns = nchP + nUnits;
-  const float kNegInf = -__builtin_inff();
-  // stage (m, l) of every state; chunks replaced by a unit state get weight zero
-  for (int i = t; i < ns; i += 256) {
+  for (int i = t; i < nUnits; i += 256) {
 #pragma unroll
-    for (int gi = 0; gi < 2; ++gi) {
-      const int g = pair * 2 + gi;
+    for (int k = 0; k < 2; ++k) {
+      const int gk = pair * 2 + k;
       float m = kNegInf, l = 0.f;
-      if (g < G) {
-        if (i < nchP) {
-          if (!(exact && ((S.contam_bits[i >> 5] >> (i & 31)) & 1u))) {
-            const size_t row = ((size_t)h * a.nchunks + i) * G + g;
-            m = a.part_m[row];
-            l = a.part_l[row];
-          }
-        } else {
-          const size_t row = ((size_t)h * a.nwork + (i - nchP)) * G + g;
-          m = ld_dev(a.ws_ml + row * 2);
-          l = ld_dev(a.ws_ml + row * 2 + 1);
-        }
+      if (gk < G) {
+        const size_t row = ((size_t)h * a.nwork + i) * G + gk;
+        m = ld_dev(a.ws_ml + row * 2);
+        l = ld_dev(a.ws_ml + row * 2 + 1);
       }
-      S.merge.m[gi][i] = l > 0.f ? m : kNegInf;
-      S.merge.w[gi][i] = l;
+      S.merge.m[k][i] = l > 0.f ? m : kNegInf;
+      S.merge.w[k][i] = l;
     }
   }
   __syncthreads();
-  const int lane = lane_id(), wv = t / kWave;
-  float mx0 = kNegInf, mx1 = kNegInf;
-  for (int i = t; i < ns; i += 256) {
-    mx0 = fmaxf(mx0, S.merge.m[0][i]);
-    mx1 = fmaxf(mx1, S.merge.m[1][i]);
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    mx0 = fmaxf(mx0, __shfl_xor(mx0, o));
-    mx1 = fmaxf(mx1, __shfl_xor(mx1, o));
-  }
-  if (lane == 0) {
-    S.fred[0][wv] = mx0;
-    S.fred[1][wv] = mx1;
-  }
-  __syncthreads();
-  const float ms0 = fmaxf(fmaxf(S.fred[0][0], S.fred[0][1]), fmaxf(S.fred[0][2], S.fred[0][3]));
-  const float ms1 = fmaxf(fmaxf(S.fred[1][0], S.fred[1][1]), fmaxf(S.fred[1][2], S.fred[1][3]));
-  __syncthreads();
-  float l0 = 0.f, l1 = 0.f;
-  for (int i = t; i < ns; i += 256) {
-    const float w0 = S.merge.w[0][i] > 0.f ? S.merge.w[0][i] * exp2f((S.merge.m[0][i] - ms0) * kLog2e) : 0.f;
-    const float w1 = S.merge.w[1][i] > 0.f ? S.merge.w[1][i] * exp2f((S.merge.m[1][i] - ms1) * kLog2e) : 0.f;
-    S.merge.w[0][i] = w0;
-    S.merge.w[1][i] = w1;
-    l0 += w0;
-    l1 += w1;
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    l0 += __shfl_xor(l0, o);
-    l1 += __shfl_xor(l1, o);
-  }
-  if (lane == 0) {
-    S.fred[0][4 + wv] = l0;
-    S.fred[1][4 + wv] = l1;
-  }
-  __syncthreads();
-  const int gi = t >> 7, g = pair * 2 + gi, ch = t & 127;
+  float ms_u[2], ls_u[2];
+  merge_weights(S, nUnits, ms_u, ls_u);
   if (g < G) {
-    const float L = (S.fred[gi][4] + S.fred[gi][5]) + (S.fred[gi][6] + S.fred[gi][7]);
-    const float ms = gi == 0 ? ms0 : ms1;
     const float* wts = S.merge.w[gi];
-    float O = 0.f;
-    const float* po = a.part_o + ((size_t)h * a.nchunks * G + g) * kHeadDim + ch;
-#pragma unroll 8
-    for (int c = 0; c < nchP; ++c) {
-      const float v = po[(size_t)c * G * kHeadDim];
-      const float w = wts[c];
-      O += w != 0.f ? w * v : 0.f;
-    }
     const float* wo = a.ws_o + ((size_t)h * a.nwork * G + g) * kHeadDim + ch;
+    float Ou = 0.f;
 #pragma unroll 8
     for (int uu = 0; uu < nUnits; ++uu) {
       const float v = ld_dev(wo + (size_t)uu * G * kHeadDim);
-      const float w = wts[nchP + uu];
-      O += w != 0.f ? w * v : 0.f;
+      const float wgt = wts[uu];
+      Ou += wgt != 0.f ? wgt * v : 0.f;
     }
+    // combine the two partial merges (each relative to its own maximum)
+    const float m1 = ms_s[gi], m2 = ms_u[gi];
+    const float ms = fmaxf(m1, m2);
+    const float f1 = ls_s[gi] > 0.f ? exp2f((m1 - ms) * kLog2e) : 0.f;
+    const float f2 = ls_u[gi] > 0.f ? exp2f((m2 - ms) * kLog2e) : 0.f;
+    const float L = ls_s[gi] * f1 + ls_u[gi] * f2;
+    const float O = Os * f1 + Ou * f2;
     const float o = L > 0.f ? O / L : 0.f;
     const size_t orow = (size_t)h * G + g;
     a.out_o32[orow * kHeadDim + ch] = o;
@@ -1193,7 +1216,7 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
   }
   if (pair == 0 && t == 0) {
     if (a.missed_count) a.missed_count[h] = nM;
-    if (a.wasted_count) a.wasted_count[h] = S.nW;
+    if (a.wasted_count) a.wasted_count[h] = nW;
   }
   __syncthreads();
   if (t == 0) {
@@ -1271,11 +1294,11 @@ hipError_t launch_score_topk(const ScoreLaunch& a, hipStream_t stream) {
   dim3 grid((a.num_pages + kScorePagesPerWg - 1) / kScorePagesPerWg, a.num_kv_heads);
   const void* f = a.bf16 ? (a.meta_mean ? (const void*)score_topk_kernel<true, true> : (const void*)score_topk_kernel<true, false>)
                          : (a.meta_mean ? (const void*)score_topk_kernel<false, true> : (const void*)score_topk_kernel<false, false>);
-  return launch1(f, grid, dim3(256), 0, stream, a);
+  return launch1(f, grid, dim3(kSelThreads), 0, stream, a);
 }
 
 hipError_t launch_predict(const PredictLaunch& a, hipStream_t stream) {
-  return launch1((const void*)predict_kernel, dim3(a.num_kv_heads), dim3(256), 0, stream, a);
+  return launch1((const void*)predict_kernel, dim3(a.num_kv_heads), dim3(kSelThreads), 0, stream, a);
 }
 
 hipError_t launch_spec_attn(const SpecLaunch& a, hipStream_t stream) {
