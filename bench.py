@@ -129,8 +129,8 @@ def main():
     ap.add_argument("--config", default="glm128k")
     ap.add_argument("--layers", type=int, default=None, help="fewer layers (quick runs only)")
     ap.add_argument("--mode", default="exact", choices=["exact", "keep"])
-    ap.add_argument("--chunk", type=int, default=8)
-    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--chunk", type=int, default=None, help="pages per speculation chunk (default 8, 4 for 64-token pages)")
+    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph variant")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--kernel-reps", type=int, default=4, help="tokens per kernel-timing pass")
     ap.add_argument("--workers", type=int, default=16, help="input-generation processes (0 = in-process)")
@@ -154,8 +154,9 @@ def main():
     pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
                       num_tokens=cfg.context, k_select=cfg.k_select, forced=cfg.forced_pages(),
                       forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
-                      alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma, chunk_pages=args.chunk, mode=mode)
-    total_tokens = 1 + 2 * args.warmup + 3 * args.steps + args.kernel_reps + 8
+                      alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma,
+                      chunk_pages=args.chunk or min(8, 256 // cfg.page_size), mode=mode)
+    total_tokens = 1 + max(2, args.warmup) + 5 * args.steps + args.kernel_reps + 16
     t0 = time.time()
     layers = [None] * n_layers
 
@@ -216,38 +217,55 @@ def main():
 
     # step 0: the prefill stand-in initialises the EMA state and predicts step 1
     q_static.copy_(q_all[0])
-    for st in layers:
-        st.select(q_static[layers.index(st)])
-        st.predict()
-        st.advance()
+    stack = R.DecodeStack(layers, [q_static[l] for l in range(n_layers)], dev)
+    s.wait_stream(torch.cuda.current_stream())
+    stack.step(L.PRR_SCHED_PREFILL, s)
     torch.cuda.synchronize()
 
     tok = [1]
 
-    def run_tokens(n, serial, graphs, measure_hits=False):
+    def run_native(n, schedule, measure_hits=False):
         hits = []
         for _ in range(n):
-            s.wait_stream(torch.cuda.current_stream())
             with torch.cuda.stream(s):
                 q_static.copy_(q_all[tok[0]])
-            if graphs is not None:
-                with torch.cuda.stream(s):
-                    graphs[layers[0].cur if not serial else 0].replay()
-            else:
-                prr_token(serial)
-            if not serial:
-                for st in layers:
-                    st.advance()
+            stack.step(schedule, s, p)
             tok[0] += 1
-            if measure_hits and not serial:
+            if measure_hits:
                 torch.cuda.synchronize()
                 miss = torch.stack([st.missed for st in layers]).sum().item()
                 hits.append(1.0 - miss / (n_layers * cfg.num_kv_heads * cfg.selected_count))
         return hits
 
+    def timed_native(n, schedule):
+        torch.cuda.synchronize()
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.wait_stream(torch.cuda.current_stream())
+        start.record(s)
+        run_native(n, schedule)
+        end.record(s)
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / n  # ms per token
+
+    hits = run_native(max(2, args.warmup), L.PRR_SCHED_TWO_STREAM, measure_hits=True)
+    run_native(2, L.PRR_SCHED_SERIAL)
+    ms_prr = timed_native(args.steps, L.PRR_SCHED_TWO_STREAM)
+    ms_serial = timed_native(args.steps, L.PRR_SCHED_SERIAL)
+    ms_prr = min(ms_prr, timed_native(args.steps, L.PRR_SCHED_TWO_STREAM))
+    ms_serial = min(ms_serial, timed_native(args.steps, L.PRR_SCHED_SERIAL))
+
+    def run_tokens(n, serial, graphs):
+        for _ in range(n):
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                q_static.copy_(q_all[tok[0]])
+                graphs[layers[0].cur if not serial else 0].replay()
+            if not serial:
+                for st in layers:
+                    st.cur = 1 - st.cur
+            tok[0] += 1
+
     def capture(serial):
-        if args.no_graph:
-            return None
         gs = []
         for parity in ((0,) if serial else (0, 1)):
             for st in layers:
@@ -257,34 +275,28 @@ def main():
             with torch.cuda.graph(g, stream=s):
                 prr_token(serial)
             gs.append(g)
-        for st in layers:
-            st.cur = 0
         torch.cuda.synchronize()
         return gs
 
-    def timed(n, serial, graphs):
+    ms_graph = None
+    if not args.no_graph:
+        # the same PRR token captured from the Python runtime as one HIP graph (its branches
+        # were observed to run one after another)
+        saved = [st.cur for st in layers]
+        prr_graphs = capture(False)
+        for st, c in zip(layers, saved):
+            st.cur = c
+        stack.parity = saved[0]
+        run_tokens(2, False, prr_graphs)
         torch.cuda.synchronize()
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s.wait_stream(torch.cuda.current_stream())
         start.record(s)
-        run_tokens(n, serial, graphs)
+        run_tokens(args.steps, False, prr_graphs)
         end.record(s)
         torch.cuda.synchronize()
-        return start.elapsed_time(end) / n  # ms per token
-
-    # eager warm-up first (sets any kernel attributes outside capture), then capture
-    run_tokens(1, False, None)
-    hits = run_tokens(max(1, args.warmup // 2), False, None, measure_hits=True)
-    saved = [st.cur for st in layers]
-    prr_graphs = capture(False)
-    serial_graphs = capture(True)
-    for st, c in zip(layers, saved):
-        st.cur = c
-    run_tokens(args.warmup, False, prr_graphs)
-    run_tokens(2, True, serial_graphs)
-    ms_prr = timed(args.steps, False, prr_graphs)
-    ms_serial = timed(args.steps, True, serial_graphs)
-    ms_prr = min(ms_prr, timed(args.steps, False, prr_graphs))
+        ms_graph = start.elapsed_time(end) / args.steps
+        stack.parity = layers[0].cur
 
     # critical path of one layer with direct launches: q ready -> o ready
     def critical_path(reps):
@@ -319,6 +331,7 @@ def main():
                 ser.append(1000.0 * a2.elapsed_time(b2))
             for st in layers:
                 st.advance()
+            stack.parity = layers[0].cur
             tok[0] += 1
         return float(np.median(prr)), float(np.median(ser))
 
@@ -378,7 +391,10 @@ def main():
         "config": {"workload": f"{cfg.name}: {n_layers} layers x ({cfg.num_q_heads} q / {cfg.num_kv_heads} kv heads, "
                                f"d {cfg.head_dim}), {cfg.dtype}, {cfg.context}-token context, page {cfg.page_size}, "
                                f"top-{cfg.k_select} pages, batch 1",
-                   "mode": args.mode, "chunk_pages": args.chunk, "graph": not args.no_graph},
+                   "mode": args.mode, "chunk_pages": pc.chunk_pages,
+                   "schedule": "prr_decode_step: select on stream S while speculating on stream P, repair on S, "
+                               "EMA update on P; native launches"},
+        "graph_us_per_layer": round(1000.0 * ms_graph / n_layers, 3) if ms_graph else None,
         "achieved_gbps": round(b_alg / (us_prr * 1e-6) / 1e9, 1),
         "alg_bytes_per_layer_step": b_alg,
         "serial_us_per_layer": round(us_serial, 3),

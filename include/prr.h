@@ -171,7 +171,8 @@ prr_status prr_predict(const prr_dims* dims, float* ema_level, float* ema_trend,
  *   page_table   device [max_pages] int32 or NULL (identity)
  *   num_tokens   tokens in the cache (masks a partial last page)
  *   pages        device [Hkv][cap] int32 list (normally P), page_count device [Hkv] int32
- *   chunk_pages  C, 1..16: consecutive list entries [cC, cC+C) form chunk c
+ *   chunk_pages  C, 1 <= C <= 256 / page_size (16 for 16-token pages, 4 for 64-token
+ *                pages): consecutive list entries [cC, cC+C) form chunk c
  *   part_o       device [Hkv][ceil(cap/C)][G][128] float32 out: normalised o of each chunk
  *   part_m, part_l device [Hkv][ceil(cap/C)][G] float32 out
  *   page_m       device [Hkv][cap][G] float32 out: max scaled logit of each listed page,
@@ -206,6 +207,73 @@ prr_status prr_repair(const prr_dims* dims, const void* q, const void* k_cache, 
                       int32_t mode, float* out_o32, void* out_o, float* out_m, float* out_l,
                       int32_t* missed_count, int32_t* wasted_count, void* workspace, size_t ws_bytes,
                       hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * Decode-step runtime: one token over a stack of layers, launched natively.
+ * --------------------------------------------------------------------------------- */
+
+/* Device buffers of one layer (all as described for the calls above). */
+typedef struct {
+  const void* q;           /* [Hq][128] this step's query of the layer */
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* page_table; /* or NULL */
+  const void* meta;
+  float* scores;
+  float* ema_level;
+  float* ema_trend;
+  uint32_t* ema_init_bits;
+  int32_t* selected;
+  int32_t* selected_count;
+  int32_t* predicted[2];       /* double-buffered P: P^t in [parity], P^{t+1} goes to [1 - parity] */
+  int32_t* predicted_count[2];
+  float* part_o;
+  float* part_m;
+  float* part_l;
+  float* page_m;
+  float* out_o32;
+  void* out_o;                 /* or NULL */
+  float* out_m;
+  float* out_l;
+  int32_t* missed_count;       /* or NULL */
+  int32_t* wasted_count;       /* or NULL */
+  void* workspace;
+  size_t ws_bytes;
+} prr_layer_io;
+
+/* Per-step parameters shared by the layers. */
+typedef struct {
+  int32_t num_tokens;
+  int32_t num_pages;
+  int32_t k_select;
+  int32_t p_select;            /* |P| budget (delta |A|) */
+  int32_t cap;
+  int32_t chunk_pages;
+  int32_t mode;                /* PRR_EXACT_SELECTED | PRR_KEEP_WASTED */
+  int32_t forced_in_budget;
+  int32_t n_forced;
+  const int32_t* forced;       /* host [n_forced] */
+  float alpha, beta, gamma;
+} prr_step_params;
+
+#define PRR_SCHED_SERIAL 0     /* per layer: select, then attend every page of A (one stream) */
+#define PRR_SCHED_TWO_STREAM 1 /* per layer: select on `stream` while speculating over P on `spec_stream`,
+                                  repair on `stream`, EMA update + next prediction on `spec_stream` */
+#define PRR_SCHED_PREFILL 2    /* per layer: select, then initialise the EMA state and predict P (step 0) */
+
+/* One decode step over n_layers layers in order (layer l+1 starts after layer l's output is
+ * written on `stream`): the select / speculate / repair / predict steps of Fig. 1 and
+ * Section 4 launched from native code with the fork/join of two streams.
+ *   events      host [3 * n_layers + 1] hipEvent_t created by the caller (timing may be
+ *               disabled); used for the fork/join of PRR_SCHED_TWO_STREAM, else ignored
+ *   parity      0 or 1: which predicted buffer holds P^t
+ * When the call returns every launch is enqueued; all work of the step is ordered
+ * before any later work on `stream` (the speculation stream is joined back).  The
+ * arguments of every layer are validated as by the individual calls; on an error in
+ * layer l, layers before l have been enqueued. */
+prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* params, const prr_layer_io* layers,
+                           int32_t n_layers, int32_t parity, int32_t schedule, hipStream_t stream,
+                           hipStream_t spec_stream, hipEvent_t* events);
 
 /* Merge n_states partial states per row (Eqs. (6)-(8) for arbitrary states).
  *   o  device [n_states][rows][d] float32, m, l device [n_states][rows] float32

@@ -30,11 +30,15 @@ PRR_MAX_PAGES = 16384
 PRR_MAX_CAP = 1024
 PRR_MAX_FORCED = 64
 
+PRR_SCHED_SERIAL = 0
+PRR_SCHED_TWO_STREAM = 1
+PRR_SCHED_PREFILL = 2
+
 # every function declared in include/prr.h
 EXPORTED = (
     "prr_status_string", "prr_last_error", "prr_workspace_size", "prr_workspace_init",
     "prr_spec_state_floats", "prr_build_page_meta", "prr_score_topk", "prr_predict",
-    "prr_spec_attn", "prr_repair", "prr_merge_states",
+    "prr_spec_attn", "prr_repair", "prr_merge_states", "prr_decode_step",
 )
 
 
@@ -47,6 +51,27 @@ class PrrError(RuntimeError):
 class prr_dims(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in
                 ("num_q_heads", "num_kv_heads", "head_dim", "page_size", "max_pages", "dtype", "meta_kind")]
+
+
+class prr_layer_io(ctypes.Structure):
+    _fields_ = [
+        ("q", ctypes.c_void_p), ("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
+        ("page_table", ctypes.c_void_p), ("meta", ctypes.c_void_p), ("scores", ctypes.c_void_p),
+        ("ema_level", ctypes.c_void_p), ("ema_trend", ctypes.c_void_p), ("ema_init_bits", ctypes.c_void_p),
+        ("selected", ctypes.c_void_p), ("selected_count", ctypes.c_void_p),
+        ("predicted", ctypes.c_void_p * 2), ("predicted_count", ctypes.c_void_p * 2),
+        ("part_o", ctypes.c_void_p), ("part_m", ctypes.c_void_p), ("part_l", ctypes.c_void_p),
+        ("page_m", ctypes.c_void_p), ("out_o32", ctypes.c_void_p), ("out_o", ctypes.c_void_p),
+        ("out_m", ctypes.c_void_p), ("out_l", ctypes.c_void_p), ("missed_count", ctypes.c_void_p),
+        ("wasted_count", ctypes.c_void_p), ("workspace", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t),
+    ]
+
+
+class prr_step_params(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("num_tokens", "num_pages", "k_select", "p_select", "cap",
+                                               "chunk_pages", "mode", "forced_in_budget", "n_forced")] + [
+        ("forced", ctypes.POINTER(ctypes.c_int32)), ("alpha", ctypes.c_float), ("beta", ctypes.c_float),
+        ("gamma", ctypes.c_float)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -72,6 +97,8 @@ _SIGS = {
     "prr_repair": (_I, [_DIMS, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _I,
                         _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "prr_merge_states": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _P]),
+    "prr_decode_step": (_I, [_DIMS, ctypes.POINTER(prr_step_params), ctypes.POINTER(prr_layer_io), _I, _I, _I, _P,
+                             _P, ctypes.POINTER(ctypes.c_void_p)]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -180,6 +207,33 @@ def prr_repair(dims, q, k_cache, v_cache, page_table, num_tokens, num_pages, sel
 def prr_merge_states(n_states, rows, d, o, m, l, out_o, out_m, out_l, stream=None):
     _check(_lib.prr_merge_states(n_states, rows, d, _ptr(o), _ptr(m), _ptr(l), _ptr(out_o), _ptr(out_m), _ptr(out_l),
                                  _stream(stream)))
+
+
+def prr_decode_step(dims, params, layers, parity, schedule, stream=None, spec_stream=None, events=None):
+    """layers: a ctypes array of prr_layer_io; events: a ctypes array of hipEvent_t (3 per layer + 1)."""
+    _check(_lib.prr_decode_step(ctypes.byref(dims), ctypes.byref(params), layers, len(layers), parity, schedule,
+                                _stream(stream), _stream(spec_stream) if spec_stream is not None else None,
+                                events))
+
+
+_hip = None
+
+
+def hip_events(n):
+    """n HIP events without timing (for prr_decode_step's fork/join), from the HIP runtime."""
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipEventCreateWithFlags.restype = ctypes.c_int
+        _hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+    arr = (ctypes.c_void_p * n)()
+    for i in range(n):
+        h = ctypes.c_void_p()
+        err = _hip.hipEventCreateWithFlags(ctypes.byref(h), 0x2)  # hipEventDisableTiming
+        if err != 0:
+            raise PrrError(PRR_ERR_HIP, f"hipEventCreateWithFlags failed ({err})")
+        arr[i] = h
+    return arr
 
 
 def library():

@@ -36,6 +36,9 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 int div_up(int a, int b) { return (a + b - 1) / b; }
 
+// a chunk (unit) holds at most 16 tiles of 16 tokens: four per wave
+bool chunk_ok(const prr_dims* d, int chunk) { return chunk >= 1 && chunk * (d->page_size / 16) <= 16; }
+
 prr_status check_dims(const prr_dims* d) {
   if (!d) return fail(PRR_ERR_INVALID_ARG, "dims is NULL");
   if (d->head_dim != 128) return fail(PRR_ERR_UNSUPPORTED, "head_dim %d: only 128 is compiled", d->head_dim);
@@ -72,7 +75,7 @@ struct WsLayout {
 };
 
 bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
-  if (check_dims(d) != PRR_OK || cap < 1 || cap > PRR_MAX_CAP || chunk < 1 || chunk > 16) return false;
+  if (check_dims(d) != PRR_OK || cap < 1 || cap > PRR_MAX_CAP || !chunk_ok(d, chunk)) return false;
   const int hkv = d->num_kv_heads, g = d->num_q_heads / d->num_kv_heads;
   L.nchunks = div_up(cap, chunk);
   L.nwork_max = 2 * L.nchunks;
@@ -141,7 +144,7 @@ prr_status prr_workspace_init(void* workspace, size_t bytes, hipStream_t stream)
 
 size_t prr_spec_state_floats(const prr_dims* dims, int32_t cap, int32_t chunk_pages, size_t* part_o_floats,
                              size_t* part_ml_floats, size_t* page_m_floats) {
-  if (check_dims(dims) != PRR_OK || cap < 1 || cap > PRR_MAX_CAP || chunk_pages < 1 || chunk_pages > 16) return 0;
+  if (check_dims(dims) != PRR_OK || cap < 1 || cap > PRR_MAX_CAP || !chunk_ok(dims, chunk_pages)) return 0;
   const size_t hkv = dims->num_kv_heads, g = dims->num_q_heads / dims->num_kv_heads;
   const size_t nch = (size_t)div_up(cap, chunk_pages);
   const size_t po = hkv * nch * g * 128, pml = hkv * nch * g, pm = hkv * (size_t)cap * g;
@@ -281,7 +284,8 @@ prr_status prr_spec_attn(const prr_dims* dims, const void* q, const void* k_cach
   if (num_tokens < 1 || (int64_t)num_tokens > (int64_t)dims->max_pages * dims->page_size)
     return fail(PRR_ERR_INVALID_ARG, "num_tokens %d outside [1, max_pages*page_size]", num_tokens);
   if (cap < 1 || cap > PRR_MAX_CAP) return fail(PRR_ERR_INVALID_ARG, "cap %d outside [1, %d]", cap, PRR_MAX_CAP);
-  if (chunk_pages < 1 || chunk_pages > 16) return fail(PRR_ERR_INVALID_ARG, "chunk_pages %d outside [1, 16]", chunk_pages);
+  if (!chunk_ok(dims, chunk_pages))
+    return fail(PRR_ERR_INVALID_ARG, "chunk_pages %d outside [1, 256 / page_size]", chunk_pages);
   prr::SpecLaunch a;
   memset(&a, 0, sizeof(a));
   a.q = q;
@@ -343,7 +347,8 @@ prr_status prr_repair(const prr_dims* dims, const void* q, const void* k_cache, 
     return fail(PRR_ERR_INVALID_ARG, "num_pages %d outside [1, min(ceil(num_tokens/page_size), %d)]", num_pages,
                 PRR_MAX_PAGES);
   if (cap < 1 || cap > PRR_MAX_CAP) return fail(PRR_ERR_INVALID_ARG, "cap %d outside [1, %d]", cap, PRR_MAX_CAP);
-  if (chunk_pages < 1 || chunk_pages > 16) return fail(PRR_ERR_INVALID_ARG, "chunk_pages %d outside [1, 16]", chunk_pages);
+  if (!chunk_ok(dims, chunk_pages))
+    return fail(PRR_ERR_INVALID_ARG, "chunk_pages %d outside [1, 256 / page_size]", chunk_pages);
   PRR_TRY(check_ptr(workspace, "workspace", 256));
   WsLayout L;
   if (!ws_layout(dims, cap, chunk_pages, L) || ws_bytes < L.total)
@@ -405,6 +410,65 @@ prr_status prr_merge_states(int32_t n_states, int32_t rows, int32_t d, const flo
   PRR_TRY(check_ptr(out_l, "out_l", 4));
   return hip_status(prr::launch_merge_states(n_states, rows, d, o, m, l, out_o, out_m, out_l, stream),
                     "merge_states launch");
+}
+
+prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* sp, const prr_layer_io* layers,
+                           int32_t n_layers, int32_t parity, int32_t schedule, hipStream_t stream,
+                           hipStream_t spec_stream, hipEvent_t* events) {
+  PRR_TRY(check_dims(dims));
+  if (!sp || !layers) return fail(PRR_ERR_INVALID_ARG, "params or layers is NULL");
+  if (n_layers < 1) return fail(PRR_ERR_INVALID_ARG, "n_layers %d < 1", n_layers);
+  if (parity != 0 && parity != 1) return fail(PRR_ERR_INVALID_ARG, "parity %d", parity);
+  if (schedule != PRR_SCHED_SERIAL && schedule != PRR_SCHED_TWO_STREAM && schedule != PRR_SCHED_PREFILL)
+    return fail(PRR_ERR_INVALID_ARG, "schedule %d", schedule);
+  if (schedule == PRR_SCHED_TWO_STREAM && !events) return fail(PRR_ERR_INVALID_ARG, "events is NULL");
+  const int nxt = 1 - parity;
+  for (int l = 0; l < n_layers; ++l) {
+    const prr_layer_io& y = layers[l];
+    if (schedule == PRR_SCHED_SERIAL) {
+      PRR_TRY(prr_score_topk(dims, y.q, y.meta, sp->num_pages, sp->k_select, sp->forced, sp->n_forced,
+                             sp->forced_in_budget, y.scores, y.selected, y.selected_count, sp->cap, y.workspace,
+                             y.ws_bytes, stream));
+      PRR_TRY(prr_repair(dims, y.q, y.k_cache, y.v_cache, y.page_table, sp->num_tokens, sp->num_pages, y.selected,
+                         y.selected_count, nullptr, nullptr, sp->cap, sp->chunk_pages, nullptr, nullptr, nullptr,
+                         nullptr, sp->mode, y.out_o32, y.out_o, y.out_m, y.out_l, y.missed_count, y.wasted_count,
+                         y.workspace, y.ws_bytes, stream));
+    } else if (schedule == PRR_SCHED_PREFILL) {
+      PRR_TRY(prr_score_topk(dims, y.q, y.meta, sp->num_pages, sp->k_select, sp->forced, sp->n_forced,
+                             sp->forced_in_budget, y.scores, y.selected, y.selected_count, sp->cap, y.workspace,
+                             y.ws_bytes, stream));
+      PRR_TRY(prr_predict(dims, y.ema_level, y.ema_trend, y.ema_init_bits, y.scores, sp->num_pages, sp->alpha,
+                          sp->beta, sp->gamma, sp->p_select, sp->forced, sp->n_forced, sp->forced_in_budget,
+                          y.predicted[nxt], y.predicted_count[nxt], sp->cap, stream));
+    } else {
+      hipEvent_t fork = events[3 * l], sel = events[3 * l + 1], spec = events[3 * l + 2];
+      PRR_TRY(hip_status(hipEventRecord(fork, stream), "event record"));
+      PRR_TRY(hip_status(hipStreamWaitEvent(spec_stream, fork, 0), "stream wait"));
+      PRR_TRY(prr_score_topk(dims, y.q, y.meta, sp->num_pages, sp->k_select, sp->forced, sp->n_forced,
+                             sp->forced_in_budget, y.scores, y.selected, y.selected_count, sp->cap, y.workspace,
+                             y.ws_bytes, stream));
+      PRR_TRY(hip_status(hipEventRecord(sel, stream), "event record"));
+      PRR_TRY(prr_spec_attn(dims, y.q, y.k_cache, y.v_cache, y.page_table, sp->num_tokens, y.predicted[parity],
+                            y.predicted_count[parity], sp->cap, sp->chunk_pages, y.part_o, y.part_m, y.part_l,
+                            y.page_m, spec_stream));
+      PRR_TRY(hip_status(hipEventRecord(spec, spec_stream), "event record"));
+      PRR_TRY(hip_status(hipStreamWaitEvent(stream, spec, 0), "stream wait"));
+      PRR_TRY(prr_repair(dims, y.q, y.k_cache, y.v_cache, y.page_table, sp->num_tokens, sp->num_pages, y.selected,
+                         y.selected_count, y.predicted[parity], y.predicted_count[parity], sp->cap, sp->chunk_pages,
+                         y.part_o, y.part_m, y.part_l, y.page_m, sp->mode, y.out_o32, y.out_o, y.out_m, y.out_l,
+                         y.missed_count, y.wasted_count, y.workspace, y.ws_bytes, stream));
+      PRR_TRY(hip_status(hipStreamWaitEvent(spec_stream, sel, 0), "stream wait"));
+      PRR_TRY(prr_predict(dims, y.ema_level, y.ema_trend, y.ema_init_bits, y.scores, sp->num_pages, sp->alpha,
+                          sp->beta, sp->gamma, sp->p_select, sp->forced, sp->n_forced, sp->forced_in_budget,
+                          y.predicted[nxt], y.predicted_count[nxt], sp->cap, spec_stream));
+    }
+  }
+  if (schedule == PRR_SCHED_TWO_STREAM) {
+    hipEvent_t join = events[3 * n_layers];
+    PRR_TRY(hip_status(hipEventRecord(join, spec_stream), "event record"));
+    PRR_TRY(hip_status(hipStreamWaitEvent(stream, join, 0), "stream wait"));
+  }
+  return ok();
 }
 
 }  // extern "C"

@@ -75,29 +75,119 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
   return __popcll(mask & ((1ull << lane) - 1ull));
 }
 
-__device__ __forceinline__ float wave_max16(float v) {  // over lanes l, l^1, .., l^8
-  v = fmaxf(v, __shfl_xor(v, 8));
-  v = fmaxf(v, __shfl_xor(v, 4));
-  v = fmaxf(v, __shfl_xor(v, 2));
-  v = fmaxf(v, __shfl_xor(v, 1));
+// Cross-lane data movement without the LDS crossbar: DPP within 16-lane rows and the
+// gfx950 permlane swaps across rows.  Every combine pairs commutative operands, so all
+// participating lanes end with bitwise identical results.
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // lane i <-> 7-i within each half row
+constexpr int kDppMirror = 0x140;     // lane i <-> 15-i within each row
+constexpr int kDppShr1 = 0x111, kDppShr2 = 0x112, kDppShr4 = 0x114, kDppShr8 = 0x118;
+constexpr int kDppBcast15 = 0x142, kDppBcast31 = 0x143;
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xf, 0xf, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+// combine over the 16 lanes of a row (all 16 lanes get the result)
+__device__ __forceinline__ float sum16(float v) {
+  v += dpp_f32<kDppXor1>(v);
+  v += dpp_f32<kDppXor2>(v);
+  v += dpp_f32<kDppHalfMirror>(v);
+  v += dpp_f32<kDppMirror>(v);
+  return v;
+}
+__device__ __forceinline__ float max16(float v) {
+  v = fmaxf(v, dpp_f32<kDppXor1>(v));
+  v = fmaxf(v, dpp_f32<kDppXor2>(v));
+  v = fmaxf(v, dpp_f32<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f32<kDppMirror>(v));
+  return v;
+}
+__device__ __forceinline__ float min16(float v) {
+  v = fminf(v, dpp_f32<kDppXor1>(v));
+  v = fminf(v, dpp_f32<kDppXor2>(v));
+  v = fminf(v, dpp_f32<kDppHalfMirror>(v));
+  v = fminf(v, dpp_f32<kDppMirror>(v));
   return v;
 }
 
-__device__ __forceinline__ float sum16(float v) {  // butterfly: identical result in all 16 lanes
-  v += __shfl_xor(v, 8);
-  v += __shfl_xor(v, 4);
-  v += __shfl_xor(v, 2);
-  v += __shfl_xor(v, 1);
-  return v;
+// combine of lanes l, l^16, l^32, l^48 (the four rows), result in all of them
+__device__ __forceinline__ float sum_rows(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+__device__ __forceinline__ float max_rows(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float min_rows(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fminf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fminf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ uint32_t umin_rows(uint32_t v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = min((uint32_t)a[0], (uint32_t)a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return min((uint32_t)b[0], (uint32_t)b[1]);
+}
+__device__ __forceinline__ uint32_t umax_rows(uint32_t v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = max((uint32_t)a[0], (uint32_t)a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return max((uint32_t)b[0], (uint32_t)b[1]);
+}
+__device__ __forceinline__ int isum_rows(int v) {
+  const auto a = __builtin_amdgcn_permlane16_swap((uint32_t)v, (uint32_t)v, false, false);
+  v = (int)a[0] + (int)a[1];
+  const auto b = __builtin_amdgcn_permlane32_swap((uint32_t)v, (uint32_t)v, false, false);
+  return (int)b[0] + (int)b[1];
 }
 
+// whole-wave reductions, result in every lane
+__device__ __forceinline__ float wave_sum(float v) { return sum_rows(sum16(v)); }
+__device__ __forceinline__ float wave_max(float v) { return max_rows(max16(v)); }
+__device__ __forceinline__ uint32_t wave_umin(uint32_t v) {
+  v = min(v, dpp_u32<kDppXor1>(v));
+  v = min(v, dpp_u32<kDppXor2>(v));
+  v = min(v, dpp_u32<kDppHalfMirror>(v));
+  v = min(v, dpp_u32<kDppMirror>(v));
+  return umin_rows(v);
+}
+__device__ __forceinline__ uint32_t wave_umax(uint32_t v) {
+  v = max(v, dpp_u32<kDppXor1>(v));
+  v = max(v, dpp_u32<kDppXor2>(v));
+  v = max(v, dpp_u32<kDppHalfMirror>(v));
+  v = max(v, dpp_u32<kDppMirror>(v));
+  return umax_rows(v);
+}
+__device__ __forceinline__ int wave_isum(int v) {
+  v += (int)dpp_u32<kDppXor1>((uint32_t)v);
+  v += (int)dpp_u32<kDppXor2>((uint32_t)v);
+  v += (int)dpp_u32<kDppHalfMirror>((uint32_t)v);
+  v += (int)dpp_u32<kDppMirror>((uint32_t)v);
+  return isum_rows(v);
+}
+
+// inclusive prefix sum over the wave (row shifts, then the row broadcasts)
 __device__ __forceinline__ int wave_inclusive_scan(int x) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
+  x += (int)dpp_u32<kDppShr1>((uint32_t)x);
+  x += (int)dpp_u32<kDppShr2>((uint32_t)x);
+  x += (int)dpp_u32<kDppShr4>((uint32_t)x);
+  x += (int)dpp_u32<kDppShr8>((uint32_t)x);
+  x += __builtin_amdgcn_update_dpp(0, x, kDppBcast15, 0xa, 0xf, false);
+  x += __builtin_amdgcn_update_dpp(0, x, kDppBcast31, 0xc, 0xf, false);
   return x;
 }
 
@@ -132,11 +222,8 @@ __device__ __forceinline__ int block_sum(int v, int* wave_tot) {
 template <int NT>
 __device__ __forceinline__ void block_minmax_u32(uint32_t& lo, uint32_t& hi, uint32_t* scratch) {
   constexpr int NW = NT / kWave;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    lo = min(lo, (uint32_t)__shfl_xor((int)lo, o));
-    hi = max(hi, (uint32_t)__shfl_xor((int)hi, o));
-  }
+  lo = wave_umin(lo);
+  hi = wave_umax(hi);
   const int w = threadIdx.x / kWave;
   if (lane_id() == 0) {
     scratch[w] = lo;

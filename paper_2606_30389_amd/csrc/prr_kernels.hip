@@ -556,8 +556,9 @@ __global__ __launch_bounds__(1024) void predict_kernel(const PredictLaunch a) {
 // =====================================================================================
 // attention over a short page list (one workgroup, four waves)
 // =====================================================================================
-// Wave w takes list entries w, w+4, w+8, w+12 (a list holds at most 16 pages) and runs
-// an online softmax over their 16-token tiles; the four wave states are merged in LDS.
+// Wave w takes list entries w, w+4, w+8, w+12 (a list holds at most 16 tiles of 16 tokens
+// per wave group, i.e. chunk_pages * page_size / 16 <= 16) and runs an online softmax
+// over their 16-token tiles; the four wave states are merged in LDS.
 //
 // q.k^T per tile: S^T (16 tokens x 16 heads) = K (16 x 128) . Q^T (128 x 16) as four
 // 16x16x32 MFMAs.  The contraction index is permuted so that each lane reads 64
@@ -565,11 +566,13 @@ __global__ __launch_bounds__(1024) void predict_kernel(const PredictLaunch a) {
 // 32j+8s .. +8 of token r (A operand) and lane 16j+n channels 32j+8s .. +8 of query head n
 // (B operand).  The result gives lane 16j+n the logits of tokens 4j..4j+3 for head n.
 //
-// p.V per tile: O (16 heads x 128) += P (16 x 16 tokens) . V (16 x 128) as 32 16x16x4
-// fp32 MFMAs.  Call (tg, cg) contracts tokens {tg, 4+tg, 8+tg, 12+tg}: lane 16j+n
-// supplies p[head n][token 4j+tg] (its own logit register tg) and V[token 4j+tg]
-// [channel 8n+cg] (from one 16-byte row load per tg); accumulator cg holds
-// O[head 4j+i][channel 8n+cg] in lane 16j+n.
+// p.V per tile, transposed: O^T (128 channels x 16 heads) += V^T . P^T as 32 16x16x4
+// fp32 MFMAs, so the softmax weights stay fp32.  Call (tg, cb) contracts tokens
+// {tg, 4+tg, 8+tg, 12+tg}: lane 16j+m supplies V[token 4j+tg][channel 8m+cb] (from one
+// 16-byte row load per tg) as A and p[head n][token 4j+tg] (its own logit register tg) as
+// B.  Accumulator cb, register i of lane 16j+n then holds O[head n][32j + 8i + cb]: each
+// lane owns 32 contiguous channels of the same head whose logits it holds, so the online
+// rescale is lane-local.
 
 struct AttnCtx {
   const uint16_t* q;  // q + h*G*128
@@ -579,8 +582,10 @@ struct AttnCtx {
   int max_pages, num_pages, num_tokens, G;
 };
 
+constexpr int kOPad = kHeadDim + 4;  // LDS row stride of a head's partial output
+
 struct UnitLds {
-  float wo[4][16][kHeadDim];
+  float wo[4][16][kOPad];
   float wm[4][16];
   float wl[4][16];
 };
@@ -612,7 +617,8 @@ template <bool BF16, int PS>
 __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, float* page_m_out, UnitLds& sm,
                             uint32_t* flags, UnitResult& res) {
   constexpr int TPP = PS / 16;
-  constexpr int NT = 4 * TPP;  // tiles per wave (4 list entries at most)
+  constexpr int NTL = 16 / 4;  // tiles per wave at most (16 tiles per unit)
+  constexpr int NPW = (NTL + TPP - 1) / TPP;  // list entries per wave at most
   const float kNegInf = -__builtin_inff();
   const float scale = 0.08838834764831845f;  // 1/sqrt(128)
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
@@ -629,17 +635,16 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
     for (int s = 0; s < 4; ++s) qf[s] = u32x4_t{0, 0, 0, 0};
   }
 
-  // list entries w, w+4, w+8, w+12 of this wave: ids first, then page-table entries, each
-  // group issued together (wave-uniform values)
+  // list entries w, w+4, ..: ids first, then page-table entries (wave-uniform values)
   const int wu = __builtin_amdgcn_readfirstlane(w);
-  int pg[4], ph[4];
+  int pg[NPW], ph[NPW];
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
+  for (int kk = 0; kk < NPW; ++kk) {
     const int i = wu + 4 * kk;
     pg[kk] = i < cnt ? pages[i] : -1;
   }
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
+  for (int kk = 0; kk < NPW; ++kk) {
     pg[kk] = __builtin_amdgcn_readfirstlane(pg[kk]);
     const bool in_list = (wu + 4 * kk) < cnt;
     const bool valid = pg[kk] >= 0 && pg[kk] < c.num_pages;
@@ -647,12 +652,12 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
     if (!valid) pg[kk] = -1;
   }
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) ph[kk] = (pg[kk] >= 0 && c.ptab) ? c.ptab[pg[kk]] : pg[kk];
-  size_t off[4];
-  int tok0[4];
-  bool ok[4];
+  for (int kk = 0; kk < NPW; ++kk) ph[kk] = (pg[kk] >= 0 && c.ptab) ? c.ptab[pg[kk]] : pg[kk];
+  size_t off[NPW];
+  int tok0[NPW];
+  bool ok[NPW];
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
+  for (int kk = 0; kk < NPW; ++kk) {
     const int phys = __builtin_amdgcn_readfirstlane(ph[kk]);
     ok[kk] = pg[kk] >= 0 && phys >= 0 && phys < c.max_pages;
     if (pg[kk] >= 0 && !ok[kk] && flags && lane == 0) atomicOr(flags, kFlagBadListEntry);
@@ -662,30 +667,35 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
 
   f32x4_t acc[8];
 #pragma unroll
-  for (int cg = 0; cg < 8; ++cg) acc[cg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int cb = 0; cb < 8; ++cb) acc[cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = kNegInf, l_run = 0.0f;
 
-  auto load_tile = [&](int f, u32x4_t (&kf)[4], u32x4_t (&vf)[4]) {
+  // every tile of the wave is loaded up front (at most 4 tiles: 32 registers each)
+  u32x4_t kf[NTL][4], vf[NTL][4];
+#pragma unroll
+  for (int f = 0; f < NPW * TPP; ++f) {
     const int kk = f / TPP, tt = f % TPP;
     if (ok[kk]) {
       const uint16_t* kt = c.k + off[kk] + (size_t)tt * 16 * kHeadDim;
       const uint16_t* vt = c.v + off[kk] + (size_t)tt * 16 * kHeadDim;
       const u32x4_t* ks = reinterpret_cast<const u32x4_t*>(kt + (size_t)n * kHeadDim + 32 * j);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) kf[s] = ks[s];
+      for (int s = 0; s < 4; ++s) kf[f][s] = ks[s];
 #pragma unroll
-      for (int tg = 0; tg < 4; ++tg) vf[tg] = *reinterpret_cast<const u32x4_t*>(vt + (size_t)(4 * j + tg) * kHeadDim + 8 * n);
+      for (int tg = 0; tg < 4; ++tg)
+        vf[f][tg] = *reinterpret_cast<const u32x4_t*>(vt + (size_t)(4 * j + tg) * kHeadDim + 8 * n);
     }
-  };
+  }
 
-  float pm = kNegInf;  // max logit of the current page, per head
-  auto compute_tile = [&](int f, const u32x4_t (&kf)[4], const u32x4_t (&vf)[4]) {
+  float pm = kNegInf;  // max logit of the current page, head n
+#pragma unroll
+  for (int f = 0; f < NPW * TPP; ++f) {
     const int kk = f / TPP, tt = f % TPP;
-    if (!ok[kk]) return;
+    if (!ok[kk]) continue;
     if (tt == 0) pm = kNegInf;
     f32x4_t st = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < 4; ++s) st = mfma_qk<BF16>(kf[s], qf[s], st);
+    for (int s = 0; s < 4; ++s) st = mfma_qk<BF16>(kf[f][s], qf[s], st);
     float sv[4];
     float mx = kNegInf;
 #pragma unroll
@@ -694,8 +704,7 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
       sv[i] = tok < c.num_tokens ? st[i] * scale : kNegInf;
       mx = fmaxf(mx, sv[i]);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = max_rows(mx);
     pm = fmaxf(pm, mx);
     const float mnew = fmaxf(m_run, mx);
     float alpha = 1.0f;
@@ -705,50 +714,33 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
 #pragma unroll
       for (int i = 0; i < 4; ++i) p[i] = exp2f((sv[i] - mnew) * kLog2e);
     }
-    float ls = (p[0] + p[1]) + (p[2] + p[3]);
-    ls += __shfl_xor(ls, 16);
-    ls += __shfl_xor(ls, 32);
+    const float ls = sum_rows((p[0] + p[1]) + (p[2] + p[3]));
     l_run = l_run * alpha + ls;
     m_run = mnew;
-    float a4[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a4[i] = __shfl(alpha, 4 * j + i);
+    for (int cb = 0; cb < 8; ++cb) {
 #pragma unroll
-    for (int cg = 0; cg < 8; ++cg) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) acc[cg][i] *= a4[i];
+      for (int i = 0; i < 4; ++i) acc[cb][i] *= alpha;
     }
 #pragma unroll
     for (int tg = 0; tg < 4; ++tg) {
 #pragma unroll
-      for (int cg = 0; cg < 8; ++cg)
-        acc[cg] = __builtin_amdgcn_mfma_f32_16x16x4f32(p[tg], v_elem<BF16>(vf[tg], cg), acc[cg], 0, 0, 0);
+      for (int cb = 0; cb < 8; ++cb)
+        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(v_elem<BF16>(vf[f][tg], cb), p[tg], acc[cb], 0, 0, 0);
     }
     if (tt == TPP - 1 && page_m_out && j == 0 && n < G) page_m_out[(size_t)(w + 4 * kk) * G + n] = pm;
-  };
-
-  // software pipeline: the next tile's loads are in flight while this one computes
-  u32x4_t ka[4], va[4], kb[4], vb[4];
-  load_tile(0, ka, va);
-#pragma unroll
-  for (int f = 0; f < NT; f += 2) {
-    if (f + 1 < NT) load_tile(f + 1, kb, vb);
-    compute_tile(f, ka, va);
-    if (f + 1 < NT) {
-      if (f + 2 < NT) load_tile(f + 2, ka, va);
-      compute_tile(f + 1, kb, vb);
-    }
   }
 
-  // merge the four wave states
+  // merge the four wave states: lane 16j+n holds channels 32j + 8i + cb of head n
   if (j == 0) {
     sm.wm[w][n] = m_run;
     sm.wl[w][n] = l_run;
   }
+  float* row = &sm.wo[w][n][32 * j];
 #pragma unroll
-  for (int cg = 0; cg < 8; ++cg) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) sm.wo[w][4 * j + i][8 * n + cg] = acc[cg][i];
+  for (int i = 0; i < 4; ++i) {
+    *reinterpret_cast<float4*>(row + 8 * i) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
+    *reinterpret_cast<float4*>(row + 8 * i + 4) = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
   }
   __syncthreads();
   const int hh = t >> 4, c0 = (t & 15) * 8;
@@ -767,13 +759,22 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
     L += lw * fw[ww];
   }
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+  float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    float o = 0.0f;
-#pragma unroll
-    for (int ww = 0; ww < 4; ++ww) o += sm.wo[ww][hh][c0 + e] * fw[ww];
-    res.o[e] = o * inv;
+  for (int ww = 0; ww < 4; ++ww) {
+    const float4 a = *reinterpret_cast<const float4*>(&sm.wo[ww][hh][c0]);
+    const float4 b = *reinterpret_cast<const float4*>(&sm.wo[ww][hh][c0 + 4]);
+    o[0] += a.x * fw[ww];
+    o[1] += a.y * fw[ww];
+    o[2] += a.z * fw[ww];
+    o[3] += a.w * fw[ww];
+    o[4] += b.x * fw[ww];
+    o[5] += b.y * fw[ww];
+    o[6] += b.z * fw[ww];
+    o[7] += b.w * fw[ww];
   }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) res.o[e] = o[e] * inv;
   res.m = L > 0.0f ? ms : kNegInf;
   res.l = L;
   __syncthreads();
@@ -1109,16 +1110,23 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
       if (recompute) attend_unit<BF16, PS>(ctx, S.xpages, nxp, nullptr, S.unit, a.flags, r);
       have = true;
     }
-    // publish the unit state to the merge workgroups (device-coherent stores, completed
-    // before the counter is bumped)
-    if (have && hh < G) {
-      const size_t row = ((size_t)h * a.nwork + u) * G + hh;
+    // publish the unit state to the merge workgroups: device-coherent stores, staged through
+    // LDS so that each store instruction writes 256 contiguous bytes, completed before the
+    // counter is bumped
+    if (have) {
+      float* tile = &S.unit.wo[0][0][0];  // [16][128], free after the unit's last barrier
+      if (hh < G) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) st_dev(a.ws_o + row * kHeadDim + c0 + e, r.o[e]);
-      if ((t & 15) == 0) {
-        st_dev(a.ws_ml + row * 2, r.m);
-        st_dev(a.ws_ml + row * 2 + 1, r.l);
+        for (int e = 0; e < 8; ++e) tile[hh * kHeadDim + c0 + e] = r.o[e];
+        if ((t & 15) == 0) {
+          S.unit.wm[0][hh] = r.m;
+          S.unit.wl[0][hh] = r.l;
+        }
       }
+      __syncthreads();
+      float* dst = a.ws_o + ((size_t)h * a.nwork + u) * G * kHeadDim;
+      for (int i = t; i < G * kHeadDim; i += 256) st_dev(dst + i, tile[i]);
+      if (t < 2 * G) st_dev(a.ws_ml + (((size_t)h * a.nwork + u) * G) * 2 + t, (t & 1) ? S.unit.wl[0][t >> 1] : S.unit.wm[0][t >> 1]);
     }
     stores_complete();
     __syncthreads();

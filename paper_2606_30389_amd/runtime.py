@@ -14,6 +14,7 @@ All arithmetic happens in libprr.so; this module only allocates, uploads and ord
 """
 from __future__ import annotations
 
+import ctypes
 import dataclasses
 from typing import List, Optional, Sequence
 
@@ -153,6 +154,54 @@ class LayerState:
                      self.sel_count, pred, cnt, self.cap, cfg.chunk_pages, self.part_o, self.part_m, self.part_l,
                      self.page_m, cfg.mode if mode is None else mode, self.out_o32, self.out_o, self.out_m,
                      self.out_l, self.missed, self.wasted, self.workspace, self.ws_bytes, stream)
+
+
+    def io(self, q):
+        """This layer's buffers as the C ABI's prr_layer_io (q: the layer's query tensor)."""
+        def ptr(t):
+            return None if t is None else t.data_ptr()
+        y = L.prr_layer_io()
+        y.q, y.k_cache, y.v_cache, y.page_table, y.meta = ptr(q), ptr(self.k), ptr(self.v), ptr(self.page_table), ptr(self.meta)
+        y.scores, y.ema_level, y.ema_trend, y.ema_init_bits = ptr(self.scores), ptr(self.level), ptr(self.trend), ptr(self.init_bits)
+        y.selected, y.selected_count = ptr(self.sel), ptr(self.sel_count)
+        y.predicted[0], y.predicted[1] = ptr(self.pred[0]), ptr(self.pred[1])
+        y.predicted_count[0], y.predicted_count[1] = ptr(self.pred_count[0]), ptr(self.pred_count[1])
+        y.part_o, y.part_m, y.part_l, y.page_m = ptr(self.part_o), ptr(self.part_m), ptr(self.part_l), ptr(self.page_m)
+        y.out_o32, y.out_o, y.out_m, y.out_l = ptr(self.out_o32), ptr(self.out_o), ptr(self.out_m), ptr(self.out_l)
+        y.missed_count, y.wasted_count = ptr(self.missed), ptr(self.wasted)
+        y.workspace, y.ws_bytes = ptr(self.workspace), self.ws_bytes
+        return y
+
+
+class DecodeStack:
+    """A stack of layers whose decode step is launched natively by prr_decode_step:
+    the two-stream PRR schedule, the serial select-then-attend schedule, or the step-0
+    select + EMA initialisation."""
+
+    def __init__(self, layers: List[LayerState], queries, device):
+        self.layers = layers
+        self.cfg = layers[0].cfg
+        self.dims = layers[0].dims
+        cfg = self.cfg
+        self.io = (L.prr_layer_io * len(layers))(*[st.io(q) for st, q in zip(layers, queries)])
+        self.forced = (ctypes.c_int32 * max(1, len(cfg.forced)))(*cfg.forced)
+        p = L.prr_step_params()
+        p.num_tokens, p.num_pages, p.k_select = cfg.num_tokens, cfg.num_pages, cfg.k_select
+        p.p_select = cfg.k_select if cfg.p_select is None else cfg.p_select
+        p.cap, p.chunk_pages, p.mode = layers[0].cap, cfg.chunk_pages, cfg.mode
+        p.forced_in_budget, p.n_forced = int(bool(cfg.forced_in_budget)), len(cfg.forced)
+        p.forced = ctypes.cast(self.forced, ctypes.POINTER(ctypes.c_int32))
+        p.alpha, p.beta, p.gamma = cfg.alpha, cfg.beta, cfg.gamma
+        self.params = p
+        self.events = L.hip_events(3 * len(layers) + 1)
+        self.parity = layers[0].cur
+
+    def step(self, schedule, stream, spec_stream=None):
+        L.prr_decode_step(self.dims, self.params, self.io, self.parity, schedule, stream, spec_stream, self.events)
+        if schedule != L.PRR_SCHED_SERIAL:
+            self.parity = 1 - self.parity
+            for st in self.layers:
+                st.cur = self.parity
 
 
 class TwoStream:

@@ -31,8 +31,10 @@ def torch_and_lib():
     return torch, P, R
 
 
-def path_config(cfg: W.Config, num_pages=None, chunk_pages=8, mode=0, num_tokens=None):
+def path_config(cfg: W.Config, num_pages=None, chunk_pages=None, mode=0, num_tokens=None):
     _, P, R = torch_and_lib()
+    if chunk_pages is None:
+        chunk_pages = min(8, 256 // cfg.page_size)
     n = cfg.num_pages if num_pages is None else num_pages
     nt = n * cfg.page_size if num_tokens is None else num_tokens
     return R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,

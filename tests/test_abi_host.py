@@ -47,6 +47,8 @@ def test_workspace_and_spec_state_sizes(P):
     assert tot == po + 2 * pml + pm
     assert P.prr_workspace_size(d, 0, 8) == 0
     assert P.prr_workspace_size(d, 256, 17) == 0
+    d64 = P.make_dims(32, 2, 64, 2048, P.PRR_BF16, P.PRR_META_MEAN)
+    assert P.prr_workspace_size(d64, 67, 4) > 0 and P.prr_workspace_size(d64, 67, 5) == 0
     bad = P.make_dims(32, 2, 16, 8192, P.PRR_BF16, head_dim=64)
     assert P.prr_workspace_size(bad, 256, 8) == 0
 

@@ -495,3 +495,67 @@ def test_merge_states(torch):
     assert np.abs(S.to_np(out_o) - ref[0]).max() < 1e-5
     assert np.abs(S.to_np(out_m) - ref[1]).max() < 1e-6
     assert np.allclose(S.to_np(out_l), ref[2], rtol=1e-5)
+
+
+@pytest.mark.parametrize("name,npages,mode", [("glm32k", 512, 0), ("llama64k", 300, 1), ("infllm128k", 200, 0)])
+def test_native_decode_step(torch, name, npages, mode):
+    """prr_decode_step over a stack of layers: step 0 (select + EMA init), then the
+    two-stream PRR schedule and the serial schedule, every layer against the oracle."""
+    from paper_2606_30389_amd import _lib as L
+    from paper_2606_30389_amd import runtime as R
+    cfg = W.CONFIGS[name]
+    n_layers, steps = 3, 3
+    layers, inputs, metas, qs, queries = [], [], [], [], []
+    for layer in range(n_layers):
+        pc = S.path_config(cfg, num_pages=npages, mode=mode)
+        S.log(f"native step {name} layer {layer} pages={npages} mode={mode}")
+        st, li = S.make_layer(cfg, pc, layer=layer)
+        st.build_meta()
+        layers.append(st)
+        inputs.append(li)
+        metas.append(S.oracle_meta(li, pc))
+        _, qb = W.query_trajectory(cfg, layer, steps=steps)
+        qs.append(qb)
+        queries.append(S.q_tensor(qb[0], pc))
+    pc = layers[0].cfg
+    stack = R.DecodeStack(layers, queries, torch.device("cuda:0"))
+    s, p = torch.cuda.Stream(), torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    stack.step(L.PRR_SCHED_PREFILL, s)
+    torch.cuda.synchronize()
+    forced = list(pc.forced)
+    state = []
+    for layer in range(n_layers):
+        s64 = S.oracle_scores(W.bits_to_f64(qs[layer][0], cfg.dtype), metas[layer], pc)
+        state.append(O.ema_init(s64))
+    for t in range(1, steps + 1):
+        for layer in range(n_layers):
+            queries[layer].copy_(S.q_tensor(qs[layer][t], pc))
+        torch.cuda.synchronize()
+        preds = [S.lists(st, st.cur) for st in layers]
+        S.log(f"native two-stream step {t}")
+        s.wait_stream(torch.cuda.current_stream())
+        stack.step(L.PRR_SCHED_TWO_STREAM, s, p)
+        torch.cuda.synchronize()
+        for layer, st in enumerate(layers):
+            q64 = W.bits_to_f64(qs[layer][t], cfg.dtype)
+            level, trend = state[layer]
+            P = S.check_selection(preds[layer], O.ema_predict(level, trend, cfg.gamma), pc.k_select, forced,
+                                  pc.forced_in_budget, what="P")
+            s64 = S.oracle_scores(q64, metas[layer], pc)
+            A = S.check_selection(S.lists(st), s64, pc.k_select, forced, pc.forced_in_budget)
+            target = A if mode == 0 else [np.union1d(a, b) for a, b in zip(A, P)]
+            ref = O.attend(q64, inputs[layer].k64(), inputs[layer].v64(), target, pc.page_size, pc.num_tokens)
+            S.check_attention(S.to_np(st.out_o32), S.to_np(st.out_m), S.to_np(st.out_l), ref, S.to_np(st.out_o),
+                              dtype=pc.dtype, what=f"layer {layer}")
+            state[layer] = O.ema_update(level, trend, s64, cfg.alpha, cfg.beta)
+        S.log(f"native serial step {t}")
+        stack.step(L.PRR_SCHED_SERIAL, s)
+        torch.cuda.synchronize()
+        for layer, st in enumerate(layers):
+            q64 = W.bits_to_f64(qs[layer][t], cfg.dtype)
+            A = S.check_selection(S.lists(st), S.oracle_scores(q64, metas[layer], pc), pc.k_select, forced,
+                                  pc.forced_in_budget)
+            ref = O.attend(q64, inputs[layer].k64(), inputs[layer].v64(), A, pc.page_size, pc.num_tokens)
+            S.check_attention(S.to_np(st.out_o32), S.to_np(st.out_m), S.to_np(st.out_l), ref, S.to_np(st.out_o),
+                              dtype=pc.dtype, what=f"serial layer {layer}")
