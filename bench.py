@@ -3,16 +3,21 @@
     python bench.py [--steps K] [--warmup W] [--config glm128k] [--gpus 1]
 
 A step is one decode token: every layer of the workload runs its per-layer hot path
-(select + speculate + repair, with the EMA update and next prediction).  Inputs are
-seeded synthetic K/V/queries with the workload's shapes (see workloads/synth.py),
-resident in HBM before timing starts; every layer has its own K/V, so a token touches
-far more than the 256 MB last-level cache.  The token step is captured once per
-prediction-buffer parity as a HIP graph and replayed.
+(select + speculate + repair, with the EMA update and next prediction), layer after
+layer on one stream.  Inputs are seeded synthetic K/V/queries with the workload's
+shapes (see workloads/synth.py), resident in HBM before timing starts; every layer has
+its own K/V, so a token touches far more than the 256 MB last-level cache.
 
-Prints one JSON line.  `value` is microseconds per decode step per layer (lower is
-better).  Also reported: the serial select-then-attend latency measured the same way,
-per-kernel HIP-event durations, the roofline of the dominant kernel, and the oracle's
-CPU time per layer-step on a bounded sample (rank 0 only).
+Schedules timed (all launched natively by prr_decode_step):
+  fused_prr     one launch per layer: select while speculating over P, repair, EMA update
+  fused_serial  one launch per layer: select, then attend every page of A
+  two_stream    separate kernels, selection and speculation on two streams
+  serial        separate kernels on one stream: select, then attend A
+
+Prints one JSON line.  `value` is microseconds per decode step per layer of fused_prr
+(lower is better).  Also reported: the other schedules, per-kernel HIP-event durations
+of the separate kernels, the roofline of the fused kernel, and the oracle's CPU time per
+layer-step on a bounded sample (rank 0 only).
 """
 from __future__ import annotations
 
@@ -65,7 +70,8 @@ def score_kernel_bytes(cfg, n_pages):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("paper_2606_30389_amd/csrc/prr_kernels.hip", "paper_2606_30389_amd/csrc/prr_device.h"):
+    for f in ("paper_2606_30389_amd/csrc/prr_kernels.hip", "paper_2606_30389_amd/csrc/prr_fused.hip",
+              "paper_2606_30389_amd/csrc/prr_select.h", "paper_2606_30389_amd/csrc/prr_device.h"):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -130,9 +136,10 @@ def main():
     ap.add_argument("--layers", type=int, default=None, help="fewer layers (quick runs only)")
     ap.add_argument("--mode", default="exact", choices=["exact", "keep"])
     ap.add_argument("--chunk", type=int, default=None, help="pages per speculation chunk (default 8, 4 for 64-token pages)")
-    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph variant")
+    ap.add_argument("--delta", type=float, default=1.0, help="|P| / |A| (speculation budget)")
+    ap.add_argument("--schedules", default="fused_prr,fused_serial,two_stream,serial")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--kernel-reps", type=int, default=4, help="tokens per kernel-timing pass")
+    ap.add_argument("--kernel-reps", type=int, default=2, help="tokens per kernel-timing pass (separate kernels)")
     ap.add_argument("--workers", type=int, default=16, help="input-generation processes (0 = in-process)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device copy of this size (calibrates HBM byte counters)")
@@ -151,12 +158,16 @@ def main():
     n_layers = args.layers or cfg.layers
     dev = torch.device("cuda:0")
     mode = L.PRR_EXACT_SELECTED if args.mode == "exact" else L.PRR_KEEP_WASTED
+    p_select = int(round(args.delta * cfg.k_select))
     pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
                       num_tokens=cfg.context, k_select=cfg.k_select, forced=cfg.forced_pages(),
                       forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
                       alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma,
-                      chunk_pages=args.chunk or min(8, 256 // cfg.page_size), mode=mode)
-    total_tokens = 1 + max(2, args.warmup) + 5 * args.steps + args.kernel_reps + 16
+                      chunk_pages=args.chunk or min(8, 256 // cfg.page_size), mode=mode, p_select=p_select)
+    schedules = [x for x in args.schedules.split(",") if x]
+    sched_id = {"fused_prr": L.PRR_SCHED_FUSED_PRR, "fused_serial": L.PRR_SCHED_FUSED_SERIAL,
+                "two_stream": L.PRR_SCHED_TWO_STREAM, "serial": L.PRR_SCHED_SERIAL}
+    total_tokens = 2 + max(2, args.warmup) + 2 * len(schedules) * (args.steps + 2) + args.kernel_reps + 8
     t0 = time.time()
     layers = [None] * n_layers
 
@@ -184,47 +195,10 @@ def main():
 
     s = torch.cuda.Stream(device=dev)
     p = torch.cuda.Stream(device=dev)
-    e = torch.cuda.Stream(device=dev)
-
-    def prr_token(serial=False):
-        """One token over all layers: the fork/join pattern of each layer step."""
-        joins = []
-        for l, st in enumerate(layers):
-            q = q_static[l]
-            if serial:
-                st.select(q, stream=s)
-                st.repair(q, stream=s, serial=True)
-                continue
-            fork = torch.cuda.Event()
-            fork.record(s)
-            p.wait_event(fork)
-            st.select(q, stream=s)
-            sel = torch.cuda.Event()
-            sel.record(s)
-            st.speculate(q, stream=p)
-            spec = torch.cuda.Event()
-            spec.record(p)
-            s.wait_event(spec)
-            st.repair(q, stream=s)
-            e.wait_event(sel)
-            st.predict(stream=e)
-        if not serial:
-            for strm in (p, e):
-                ev = torch.cuda.Event()
-                ev.record(strm)
-                s.wait_event(ev)
-        return joins
-
-    # step 0: the prefill stand-in initialises the EMA state and predicts step 1
-    q_static.copy_(q_all[0])
     stack = R.DecodeStack(layers, [q_static[l] for l in range(n_layers)], dev)
-    s.wait_stream(torch.cuda.current_stream())
-    stack.step(L.PRR_SCHED_PREFILL, s)
-    torch.cuda.synchronize()
+    tok = [0]
 
-    tok = [1]
-
-    def run_native(n, schedule, measure_hits=False):
+    def run(n, schedule, measure_hits=False):
         hits = []
         for _ in range(n):
             with torch.cuda.stream(s):
@@ -237,107 +211,31 @@ def main():
                 hits.append(1.0 - miss / (n_layers * cfg.num_kv_heads * cfg.selected_count))
         return hits
 
-    def timed_native(n, schedule):
+    def timed(n, schedule):
         torch.cuda.synchronize()
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s.wait_stream(torch.cuda.current_stream())
         start.record(s)
-        run_native(n, schedule)
+        run(n, schedule)
         end.record(s)
         torch.cuda.synchronize()
         return start.elapsed_time(end) / n  # ms per token
 
-    hits = run_native(max(2, args.warmup), L.PRR_SCHED_TWO_STREAM, measure_hits=True)
-    run_native(2, L.PRR_SCHED_SERIAL)
-    ms_prr = timed_native(args.steps, L.PRR_SCHED_TWO_STREAM)
-    ms_serial = timed_native(args.steps, L.PRR_SCHED_SERIAL)
-    ms_prr = min(ms_prr, timed_native(args.steps, L.PRR_SCHED_TWO_STREAM))
-    ms_serial = min(ms_serial, timed_native(args.steps, L.PRR_SCHED_SERIAL))
+    # step 0: the prefill stand-in selects and initialises the EMA state (predicts step 1)
+    s.wait_stream(torch.cuda.current_stream())
+    run(1, L.PRR_SCHED_FUSED_PREFILL)
+    torch.cuda.synchronize()
+    hits = run(max(2, args.warmup), L.PRR_SCHED_FUSED_PRR, measure_hits=True)
+    ms = {}
+    for name in schedules:  # warm each schedule, then two timed passes (the better one counts)
+        run(2, sched_id[name])
+        ms[name] = min(timed(args.steps, sched_id[name]), timed(args.steps, sched_id[name]))
+    flags = [int(st.workspace[:1].cpu()[0]) for st in layers]
+    if any(flags):
+        print(json.dumps({"error": f"device error flags {flags}"}), flush=True)
+        sys.exit(3)
 
-    def run_tokens(n, serial, graphs):
-        for _ in range(n):
-            s.wait_stream(torch.cuda.current_stream())
-            with torch.cuda.stream(s):
-                q_static.copy_(q_all[tok[0]])
-                graphs[layers[0].cur if not serial else 0].replay()
-            if not serial:
-                for st in layers:
-                    st.cur = 1 - st.cur
-            tok[0] += 1
-
-    def capture(serial):
-        gs = []
-        for parity in ((0,) if serial else (0, 1)):
-            for st in layers:
-                st.cur = parity
-            g = torch.cuda.CUDAGraph()
-            s.wait_stream(torch.cuda.current_stream())
-            with torch.cuda.graph(g, stream=s):
-                prr_token(serial)
-            gs.append(g)
-        torch.cuda.synchronize()
-        return gs
-
-    ms_graph = None
-    if not args.no_graph:
-        # the same PRR token captured from the Python runtime as one HIP graph (its branches
-        # were observed to run one after another)
-        saved = [st.cur for st in layers]
-        prr_graphs = capture(False)
-        for st, c in zip(layers, saved):
-            st.cur = c
-        stack.parity = saved[0]
-        run_tokens(2, False, prr_graphs)
-        torch.cuda.synchronize()
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        s.wait_stream(torch.cuda.current_stream())
-        start.record(s)
-        run_tokens(args.steps, False, prr_graphs)
-        end.record(s)
-        torch.cuda.synchronize()
-        ms_graph = start.elapsed_time(end) / args.steps
-        stack.parity = layers[0].cur
-
-    # critical path of one layer with direct launches: q ready -> o ready
-    def critical_path(reps):
-        prr, ser = [], []
-        for _ in range(reps):
-            q_static.copy_(q_all[tok[0]])
-            torch.cuda.synchronize()
-            for l, st in enumerate(layers):
-                q = q_static[l]
-                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a.record(s)
-                p.wait_event(a)
-                st.select(q, stream=s)
-                sel = torch.cuda.Event()
-                sel.record(s)
-                st.speculate(q, stream=p)
-                spec = torch.cuda.Event()
-                spec.record(p)
-                s.wait_event(spec)
-                st.repair(q, stream=s)
-                b.record(s)
-                e.wait_event(sel)
-                st.predict(stream=e)
-                torch.cuda.synchronize()
-                prr.append(1000.0 * a.elapsed_time(b))
-                a2, b2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a2.record(s)
-                st.select(q, stream=s)
-                st.repair(q, stream=s, serial=True)
-                b2.record(s)
-                torch.cuda.synchronize()
-                ser.append(1000.0 * a2.elapsed_time(b2))
-            for st in layers:
-                st.advance()
-            stack.parity = layers[0].cur
-            tok[0] += 1
-        return float(np.median(prr)), float(np.median(ser))
-
-    crit_prr, crit_serial = critical_path(2)
-
-    # per-kernel durations: HIP events around each launch on the stream it runs on
+    # per-kernel durations of the separate-kernel path: HIP events around each launch
     def kernel_times(reps):
         names = ("score_topk", "spec_attn", "repair", "predict", "repair_serial")
         acc = {k: [] for k in names}
@@ -370,38 +268,37 @@ def main():
             tok[0] += 1
         return {k: float(np.mean(v)) for k, v in acc.items()}
 
-    ktimes = kernel_times(args.kernel_reps)
+    ktimes = kernel_times(args.kernel_reps) if args.kernel_reps > 0 else {}
 
     b_alg = algorithmic_bytes(cfg, cfg.num_pages)
-    us_prr = 1000.0 * ms_prr / n_layers
-    us_serial = 1000.0 * ms_serial / n_layers
-    dominant = max(("score_topk", "spec_attn", "repair", "predict"), key=lambda k: ktimes[k])
-    sb = score_kernel_bytes(cfg, cfg.num_pages)
-    achieved = (sb / (ktimes["score_topk"] * 1e-6)) / 1e9
-    roofline = {"bound": "hbm", "kernel": "score_topk", "dominant_kernel": dominant,
-                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": load_traffic("score_topk"),
-                "alg_bytes_per_launch": sb, "avg_launch_us": round(ktimes["score_topk"], 2)}
-
+    us = {k: 1000.0 * v / n_layers for k, v in ms.items()}
+    main_sched = "fused_prr" if "fused_prr" in us else schedules[0]
+    us_prr = us[main_sched]
+    # the fused PRR step is one kernel per layer: its average launch duration is the
+    # timed region divided by the launches in it
+    achieved = b_alg / (us_prr * 1e-6) / 1e9
+    roofline = {"bound": "hbm", "kernel": "fused_step_kernel (PRR schedule)", "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic": load_traffic("fused_step_prr"), "alg_bytes_per_launch": b_alg,
+                "avg_launch_us": round(us_prr, 3)}
+    best_serial = min(us[k] for k in ("fused_serial", "serial") if k in us) if any(
+        k in us for k in ("fused_serial", "serial")) else None
     out = {
         "metric": METRIC, "value": round(us_prr, 3), "unit": "us/layer-step", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_prr, 4),
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms[main_sched], 4),
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
         "data": "synthetic (seeded N(0,1) K/V with hot pages, AR(1) queries; no model weights)",
         "config": {"workload": f"{cfg.name}: {n_layers} layers x ({cfg.num_q_heads} q / {cfg.num_kv_heads} kv heads, "
                                f"d {cfg.head_dim}), {cfg.dtype}, {cfg.context}-token context, page {cfg.page_size}, "
                                f"top-{cfg.k_select} pages, batch 1",
-                   "mode": args.mode, "chunk_pages": pc.chunk_pages,
-                   "schedule": "prr_decode_step: select on stream S while speculating on stream P, repair on S, "
-                               "EMA update on P; native launches"},
-        "graph_us_per_layer": round(1000.0 * ms_graph / n_layers, 3) if ms_graph else None,
-        "achieved_gbps": round(b_alg / (us_prr * 1e-6) / 1e9, 1),
+                   "mode": args.mode, "chunk_pages": pc.chunk_pages, "p_select": p_select,
+                   "schedule": main_sched},
+        "us_per_layer": {k: round(v, 3) for k, v in us.items()},
+        "achieved_gbps": round(achieved, 1),
         "alg_bytes_per_layer_step": b_alg,
-        "serial_us_per_layer": round(us_serial, 3),
-        "speedup_vs_serial": round(us_serial / us_prr, 3),
+        "serial_us_per_layer": round(best_serial, 3) if best_serial else None,
+        "speedup_vs_serial": round(best_serial / us_prr, 3) if best_serial else None,
         "hit_rate": round(float(np.mean(hits)), 4) if hits else None,
-        "critical_path_us": {"prr": round(crit_prr, 2), "serial": round(crit_serial, 2),
-                             "note": "one layer, direct launches, q ready -> o ready, median"},
         "kernel_us": {k: round(v, 2) for k, v in ktimes.items()},
         "roofline": roofline,
     }

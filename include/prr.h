@@ -94,12 +94,12 @@ typedef struct {
 const char* prr_status_string(prr_status status);
 const char* prr_last_error(void);
 
-/* Bytes of workspace used by prr_score_topk and prr_repair for lists of at most
- * `cap` pages and speculation chunks of `chunk_pages` pages.  The workspace holds
- * three disjoint regions (selection counters, repair counters, repair partial
- * states); one prr_score_topk and one prr_repair may use the same workspace at the
- * same time, two calls of the same entry point may not.  Returns 0 if the
- * arguments are invalid. */
+/* Bytes of workspace used by prr_score_topk, prr_repair and the fused schedules of
+ * prr_decode_step for lists of at most `cap` pages and speculation chunks of
+ * `chunk_pages` pages.  The workspace holds disjoint regions (selection counters,
+ * repair counters, repair partial states, the fused step's tagged hand-off buffers);
+ * one prr_score_topk and one prr_repair may use the same workspace at the same time,
+ * two calls of the same entry point may not.  Returns 0 if the arguments are invalid. */
 size_t prr_workspace_size(const prr_dims* dims, int32_t cap, int32_t chunk_pages);
 
 /* Zero a workspace (device, `bytes` long, 256-byte aligned) with a fill kernel on
@@ -254,12 +254,24 @@ typedef struct {
   int32_t n_forced;
   const int32_t* forced;       /* host [n_forced] */
   float alpha, beta, gamma;
+  uint32_t epoch;              /* fused schedules: >= 1 and different from every earlier call's
+                                  value on the same workspaces (e.g. the token index + 1) */
 } prr_step_params;
 
 #define PRR_SCHED_SERIAL 0     /* per layer: select, then attend every page of A (one stream) */
 #define PRR_SCHED_TWO_STREAM 1 /* per layer: select on `stream` while speculating over P on `spec_stream`,
                                   repair on `stream`, EMA update + next prediction on `spec_stream` */
 #define PRR_SCHED_PREFILL 2    /* per layer: select, then initialise the EMA state and predict P (step 0) */
+/* The same three steps, each layer as ONE launch on `stream` whose workgroups take the
+ * roles of the separate kernels (score, select, predict, speculate, attend missed pages,
+ * merge) and hand results to each other inside the launch, so selection and speculation
+ * overlap without a second stream.  In the fused PRR step the speculation keeps one
+ * softmax state per page of P and folds only the pages that turn out to be in A, so
+ * PRR_EXACT_SELECTED needs no recomputation.  Fused schedules need num_pages <= 8192,
+ * p_select <= cap, and use the fused region of the workspace (prr_workspace_size). */
+#define PRR_SCHED_FUSED_SERIAL 3
+#define PRR_SCHED_FUSED_PRR 4
+#define PRR_SCHED_FUSED_PREFILL 5
 
 /* One decode step over n_layers layers in order (layer l+1 starts after layer l's output is
  * written on `stream`): the select / speculate / repair / predict steps of Fig. 1 and

@@ -33,6 +33,9 @@ PRR_MAX_FORCED = 64
 PRR_SCHED_SERIAL = 0
 PRR_SCHED_TWO_STREAM = 1
 PRR_SCHED_PREFILL = 2
+PRR_SCHED_FUSED_SERIAL = 3
+PRR_SCHED_FUSED_PRR = 4
+PRR_SCHED_FUSED_PREFILL = 5
 
 # every function declared in include/prr.h
 EXPORTED = (
@@ -71,7 +74,7 @@ class prr_step_params(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("num_tokens", "num_pages", "k_select", "p_select", "cap",
                                                "chunk_pages", "mode", "forced_in_budget", "n_forced")] + [
         ("forced", ctypes.POINTER(ctypes.c_int32)), ("alpha", ctypes.c_float), ("beta", ctypes.c_float),
-        ("gamma", ctypes.c_float)]
+        ("gamma", ctypes.c_float), ("epoch", ctypes.c_uint32)]
 
 
 if not os.path.exists(LIB_PATH):

@@ -70,8 +70,8 @@ prr_status check_ptr(const void* p, const char* name, size_t align) {
   } while (0)
 
 struct WsLayout {
-  size_t flags, sel_cnt, rep_cnt, rep_o, rep_ml, total;
-  int nchunks, nwork_max;
+  size_t flags, sel_cnt, rep_cnt, rep_o, rep_ml, f_score, f_thr, f_mcnt, f_mlist, f_part, total;
+  int nchunks, nwork_max, nparts;
 };
 
 bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
@@ -90,6 +90,18 @@ bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
   off = align_up(off + (size_t)hkv * L.nwork_max * g * 128 * 4, 256);
   L.rep_ml = off;
   off = align_up(off + (size_t)hkv * L.nwork_max * g * 2 * 4, 256);
+  // fused step: tagged scores, threshold, missed count and list, partial states
+  L.nparts = 2 * L.nchunks;
+  L.f_score = off;
+  off = align_up(off + (size_t)hkv * d->max_pages * 8, 256);
+  L.f_thr = off;
+  off = align_up(off + (size_t)hkv * 2 * 8, 256);
+  L.f_mcnt = off;
+  off = align_up(off + (size_t)hkv * 8, 256);
+  L.f_mlist = off;
+  off = align_up(off + (size_t)hkv * cap * 8, 256);
+  L.f_part = off;
+  off = align_up(off + (size_t)hkv * L.nparts * g * 130 * 8, 256);
   L.total = off;
   return true;
 }
@@ -412,6 +424,126 @@ prr_status prr_merge_states(int32_t n_states, int32_t rows, int32_t d, const flo
                     "merge_states launch");
 }
 
+// One layer of a fused schedule: every argument checked as by the individual entry
+// points, then one launch.
+static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, const prr_layer_io& y, int parity,
+                              int schedule, hipStream_t stream) {
+  const bool prr = schedule == PRR_SCHED_FUSED_PRR, prefill = schedule == PRR_SCHED_FUSED_PREFILL;
+  PRR_TRY(check_ptr(y.q, "q", 16));
+  PRR_TRY(check_ptr(y.meta, "meta", 16));
+  PRR_TRY(check_ptr(y.scores, "scores", 4));
+  PRR_TRY(check_ptr(y.selected, "selected", 4));
+  PRR_TRY(check_ptr(y.selected_count, "selected_count", 4));
+  if (y.page_table && !aligned(y.page_table, 4)) return fail(PRR_ERR_INVALID_ARG, "page_table misaligned");
+  if (!prefill) {
+    PRR_TRY(check_ptr(y.k_cache, "k_cache", 16));
+    PRR_TRY(check_ptr(y.v_cache, "v_cache", 16));
+    PRR_TRY(check_ptr(y.out_o32, "out_o32", 4));
+    if (y.out_o && !aligned(y.out_o, 2)) return fail(PRR_ERR_INVALID_ARG, "out_o misaligned");
+    PRR_TRY(check_ptr(y.out_m, "out_m", 4));
+    PRR_TRY(check_ptr(y.out_l, "out_l", 4));
+    if (y.missed_count && !aligned(y.missed_count, 4)) return fail(PRR_ERR_INVALID_ARG, "missed_count misaligned");
+    if (y.wasted_count && !aligned(y.wasted_count, 4)) return fail(PRR_ERR_INVALID_ARG, "wasted_count misaligned");
+  }
+  if (prr || prefill) {
+    PRR_TRY(check_ptr(y.ema_level, "ema_level", 4));
+    PRR_TRY(check_ptr(y.ema_trend, "ema_trend", 4));
+    PRR_TRY(check_ptr(y.ema_init_bits, "ema_init_bits", 4));
+    PRR_TRY(check_ptr(y.predicted[1 - parity], "predicted[next]", 4));
+    PRR_TRY(check_ptr(y.predicted_count[1 - parity], "predicted_count[next]", 4));
+  }
+  if (prr) {
+    PRR_TRY(check_ptr(y.predicted[parity], "predicted[current]", 4));
+    PRR_TRY(check_ptr(y.predicted_count[parity], "predicted_count[current]", 4));
+  }
+  if (sp->num_tokens < 1 || (int64_t)sp->num_tokens > (int64_t)dims->max_pages * dims->page_size)
+    return fail(PRR_ERR_INVALID_ARG, "num_tokens %d outside [1, max_pages*page_size]", sp->num_tokens);
+  const int npages_tok = div_up(sp->num_tokens, dims->page_size);
+  if (sp->num_pages < 1 || sp->num_pages > npages_tok || sp->num_pages > PRR_MAX_PAGES)
+    return fail(PRR_ERR_INVALID_ARG, "num_pages %d outside [1, min(ceil(num_tokens/page_size), %d)]", sp->num_pages,
+                PRR_MAX_PAGES);
+  if (sp->num_pages > prr::kFusedMaxPages)
+    return fail(PRR_ERR_UNSUPPORTED, "fused schedules take at most %d pages (num_pages %d)", prr::kFusedMaxPages,
+                sp->num_pages);
+  if (sp->k_select < 0 || sp->p_select < 0)
+    return fail(PRR_ERR_INVALID_ARG, "k_select %d / p_select %d < 0", sp->k_select, sp->p_select);
+  PRR_TRY(check_forced(sp->forced, sp->n_forced, sp->num_pages));
+  if (sp->cap < 1 || sp->cap > PRR_MAX_CAP) return fail(PRR_ERR_INVALID_ARG, "cap %d outside [1, %d]", sp->cap, PRR_MAX_CAP);
+  if (!chunk_ok(dims, sp->chunk_pages))
+    return fail(PRR_ERR_INVALID_ARG, "chunk_pages %d outside [1, 256 / page_size]", sp->chunk_pages);
+  if (sp->mode != PRR_EXACT_SELECTED && sp->mode != PRR_KEEP_WASTED) return fail(PRR_ERR_INVALID_ARG, "mode %d", sp->mode);
+  if (sp->epoch == 0) return fail(PRR_ERR_INVALID_ARG, "epoch 0 is reserved (a zeroed workspace carries it)");
+  if (prr || prefill) {
+    if (!(sp->alpha > 0.f && sp->alpha <= 1.f) || !(sp->beta > 0.f && sp->beta <= 1.f) ||
+        !(sp->gamma >= 0.f && sp->gamma <= 1.f))
+      return fail(PRR_ERR_INVALID_ARG, "alpha %g, beta %g, gamma %g outside (0,1], (0,1], [0,1]", sp->alpha, sp->beta,
+                  sp->gamma);
+  }
+  int total_a, kextra_a, total_p, kextra_p;
+  budget(sp->k_select, sp->n_forced, sp->forced_in_budget, sp->num_pages, total_a, kextra_a);
+  budget(sp->p_select, sp->n_forced, sp->forced_in_budget, sp->num_pages, total_p, kextra_p);
+  if (total_a > sp->cap) return fail(PRR_ERR_INVALID_ARG, "|A| = %d exceeds cap %d", total_a, sp->cap);
+  if ((prr || prefill) && total_p > sp->cap) return fail(PRR_ERR_INVALID_ARG, "|P| = %d exceeds cap %d", total_p, sp->cap);
+  PRR_TRY(check_ptr(y.workspace, "workspace", 256));
+  WsLayout L;
+  if (!ws_layout(dims, sp->cap, sp->chunk_pages, L) || y.ws_bytes < L.total)
+    return fail(PRR_ERR_WORKSPACE, "workspace of %zu bytes too small (need %zu)", y.ws_bytes,
+                ws_layout(dims, sp->cap, sp->chunk_pages, L) ? L.total : (size_t)0);
+  prr::FusedLaunch a;
+  memset(&a, 0, sizeof(a));
+  a.q = y.q;
+  a.meta = y.meta;
+  a.k_cache = y.k_cache;
+  a.v_cache = y.v_cache;
+  a.page_table = y.page_table;
+  a.level = y.ema_level;
+  a.trend = y.ema_trend;
+  a.init_bits = y.ema_init_bits;
+  a.pred_cur = prr ? y.predicted[parity] : nullptr;
+  a.pred_cur_count = prr ? y.predicted_count[parity] : nullptr;
+  a.pred_nxt = y.predicted[1 - parity];
+  a.pred_nxt_count = y.predicted_count[1 - parity];
+  a.scores = y.scores;
+  a.selected = y.selected;
+  a.selected_count = y.selected_count;
+  a.out_o32 = y.out_o32;
+  a.out_o = y.out_o;
+  a.out_m = y.out_m;
+  a.out_l = y.out_l;
+  a.missed_count = y.missed_count;
+  a.wasted_count = y.wasted_count;
+  char* ws = static_cast<char*>(y.workspace);
+  a.t_score = reinterpret_cast<uint64_t*>(ws + L.f_score);
+  a.t_thr = reinterpret_cast<uint64_t*>(ws + L.f_thr);
+  a.t_mcnt = reinterpret_cast<uint64_t*>(ws + L.f_mcnt);
+  a.t_mlist = reinterpret_cast<uint64_t*>(ws + L.f_mlist);
+  a.t_part = reinterpret_cast<uint64_t*>(ws + L.f_part);
+  a.flags = reinterpret_cast<uint32_t*>(ws + L.flags);
+  a.alpha = sp->alpha;
+  a.beta = sp->beta;
+  a.gamma = sp->gamma;
+  a.epoch = sp->epoch;
+  a.schedule = prr ? 1 : (prefill ? 2 : 0);
+  a.mode = sp->mode;
+  a.num_kv_heads = dims->num_kv_heads;
+  a.group = dims->num_q_heads / dims->num_kv_heads;
+  a.max_pages = dims->max_pages;
+  a.num_pages = sp->num_pages;
+  a.num_tokens = sp->num_tokens;
+  a.kextra_a = kextra_a;
+  a.kextra_p = kextra_p;
+  a.cap = sp->cap;
+  a.chunk = sp->chunk_pages;
+  a.n_score = div_up(sp->num_pages, 128);
+  a.n_spec = L.nchunks;
+  a.n_miss = L.nchunks;
+  a.nparts = L.nparts;
+  a.n_forced = sp->n_forced;
+  a.meta_mean = dims->meta_kind == PRR_META_MEAN;
+  for (int i = 0; i < sp->n_forced; ++i) a.forced[i] = sp->forced[i];
+  return hip_status(prr::launch_fused(a, dims->dtype == PRR_BF16, dims->page_size, stream), "fused step launch");
+}
+
 prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* sp, const prr_layer_io* layers,
                            int32_t n_layers, int32_t parity, int32_t schedule, hipStream_t stream,
                            hipStream_t spec_stream, hipEvent_t* events) {
@@ -419,8 +551,12 @@ prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* sp, cons
   if (!sp || !layers) return fail(PRR_ERR_INVALID_ARG, "params or layers is NULL");
   if (n_layers < 1) return fail(PRR_ERR_INVALID_ARG, "n_layers %d < 1", n_layers);
   if (parity != 0 && parity != 1) return fail(PRR_ERR_INVALID_ARG, "parity %d", parity);
-  if (schedule != PRR_SCHED_SERIAL && schedule != PRR_SCHED_TWO_STREAM && schedule != PRR_SCHED_PREFILL)
+  if (schedule < PRR_SCHED_SERIAL || schedule > PRR_SCHED_FUSED_PREFILL)
     return fail(PRR_ERR_INVALID_ARG, "schedule %d", schedule);
+  if (schedule >= PRR_SCHED_FUSED_SERIAL) {
+    for (int l = 0; l < n_layers; ++l) PRR_TRY(fused_layer(dims, sp, layers[l], parity, schedule, stream));
+    return ok();
+  }
   if (schedule == PRR_SCHED_TWO_STREAM && !events) return fail(PRR_ERR_INVALID_ARG, "events is NULL");
   const int nxt = 1 - parity;
   for (int l = 0; l < n_layers; ++l) {

@@ -87,6 +87,51 @@ struct RepairLaunch {
   bool bf16;
 };
 
+// One layer's whole decode step in one launch (the fused schedules of prr_decode_step).
+struct FusedLaunch {
+  const void* q;
+  const void* meta;
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* page_table;
+  float* level;
+  float* trend;
+  uint32_t* init_bits;
+  const int32_t* pred_cur;        // P^t [Hkv][cap] (PRR)
+  const int32_t* pred_cur_count;
+  int32_t* pred_nxt;              // P^{t+1} (PRR, prefill)
+  int32_t* pred_nxt_count;
+  float* scores;
+  int32_t* selected;
+  int32_t* selected_count;
+  float* out_o32;
+  void* out_o;
+  float* out_m;
+  float* out_l;
+  int32_t* missed_count;
+  int32_t* wasted_count;
+  uint64_t* t_score;  // [Hkv][max_pages] tagged score bits
+  uint64_t* t_thr;    // [Hkv][2] tagged threshold of A
+  uint64_t* t_mcnt;   // [Hkv] tagged count of the missed list (bit 31: attended by the select workgroup)
+  uint64_t* t_mlist;  // [Hkv][cap] tagged missed pages
+  uint64_t* t_part;   // [Hkv][nparts][G][130] tagged partial states
+  uint32_t* flags;
+  float alpha, beta, gamma;
+  uint32_t epoch;
+  int schedule;  // 0 serial, 1 PRR, 2 prefill
+  int mode;
+  int num_kv_heads, group, max_pages, num_pages, num_tokens;
+  int kextra_a, kextra_p, cap, chunk;
+  int n_score, n_spec, n_miss, nparts;  // workgroups per KV head; partial slots per KV head
+  int n_forced;
+  bool meta_mean;
+  int32_t forced[PRR_MAX_FORCED];
+};
+
+constexpr int kFusedMaxPages = 8192;  // 16 keys per thread of a 512-thread select
+hipError_t launch_fused(const FusedLaunch& a, bool bf16, int page_size, hipStream_t stream);
+int fused_grid(const FusedLaunch& a);
+
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream);
 hipError_t launch_score_topk(const ScoreLaunch& a, hipStream_t stream);

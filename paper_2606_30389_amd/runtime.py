@@ -173,6 +173,16 @@ class LayerState:
         return y
 
 
+_epoch = [0]
+
+
+def next_epoch():
+    """A process-wide increasing value: the fused schedules need a new one for every call
+    on a workspace (the device-side hand-offs of a call are tagged with it)."""
+    _epoch[0] += 1
+    return _epoch[0]
+
+
 class DecodeStack:
     """A stack of layers whose decode step is launched natively by prr_decode_step:
     the two-stream PRR schedule, the serial select-then-attend schedule, or the step-0
@@ -194,14 +204,16 @@ class DecodeStack:
         p.alpha, p.beta, p.gamma = cfg.alpha, cfg.beta, cfg.gamma
         self.params = p
         self.events = L.hip_events(3 * len(layers) + 1)
-        self.parity = layers[0].cur
 
     def step(self, schedule, stream, spec_stream=None):
-        L.prr_decode_step(self.dims, self.params, self.io, self.parity, schedule, stream, spec_stream, self.events)
-        if schedule != L.PRR_SCHED_SERIAL:
-            self.parity = 1 - self.parity
+        """One decode step of every layer; P^t is in each layer's predicted[cur]."""
+        parity = self.layers[0].cur
+        assert all(st.cur == parity for st in self.layers), "layers disagree on the current prediction buffer"
+        self.params.epoch = next_epoch()
+        L.prr_decode_step(self.dims, self.params, self.io, parity, schedule, stream, spec_stream, self.events)
+        if schedule not in (L.PRR_SCHED_SERIAL, L.PRR_SCHED_FUSED_SERIAL):
             for st in self.layers:
-                st.cur = self.parity
+                st.cur = 1 - parity
 
 
 class TwoStream:

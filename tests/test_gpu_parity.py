@@ -559,3 +559,93 @@ def test_native_decode_step(torch, name, npages, mode):
             ref = O.attend(q64, inputs[layer].k64(), inputs[layer].v64(), A, pc.page_size, pc.num_tokens)
             S.check_attention(S.to_np(st.out_o32), S.to_np(st.out_m), S.to_np(st.out_l), ref, S.to_np(st.out_o),
                               dtype=pc.dtype, what=f"serial layer {layer}")
+
+
+FUSED_CASES = [
+    # name, pages, mode, chunk, |P|/|A|, k_select override, layers, steps
+    ("tiny", None, 0, None, 1, None, 2, 4),
+    ("tiny", None, 1, None, 1, None, 1, 3),
+    ("tiny", None, 0, 3, 1, 6, 1, 4),        # |A| <= 8: the select workgroup attends itself
+    ("glm32k", 512, 0, 16, 1, None, 2, 3),   # two pages per wave
+    ("glm32k", 512, 0, 8, 2, None, 1, 3),    # |P| = 2|A|
+    ("llama64k", 300, 1, None, 1, None, 2, 3),
+    ("infllm128k", 200, 0, None, 1, None, 1, 3),
+    ("glm128k", None, 0, None, 1, None, 1, 2),  # full size: 8192 pages, top-256
+]
+
+
+@pytest.mark.parametrize("case", FUSED_CASES, ids=lambda c: f"{c[0]}-p{c[1]}-m{c[2]}-c{c[3]}-d{c[4]}-k{c[5]}")
+def test_fused_decode_step(torch, case):
+    """The fused schedules of prr_decode_step (one launch per layer): step-0 select + EMA
+    initialisation, then per step the PRR launch and the serial launch, every layer
+    against the oracle (A, P, output, missed and wasted counts)."""
+    from paper_2606_30389_amd import _lib as L
+    from paper_2606_30389_amd import runtime as R
+    name, npages, mode, chunk, delta, kover, n_layers, steps = case
+    cfg = W.CONFIGS[name]
+    layers, inputs, metas, qs, queries = [], [], [], [], []
+    for layer in range(n_layers):
+        pc = S.path_config(cfg, num_pages=npages, mode=mode, chunk_pages=chunk)
+        if kover is not None:
+            pc.k_select = kover
+        pc.p_select = delta * pc.k_select
+        S.log(f"fused {name} layer {layer} pages={pc.num_pages} mode={mode} chunk={pc.chunk_pages} "
+              f"K={pc.k_select} |P|={pc.p_select}")
+        st, li = S.make_layer(cfg, pc, layer=layer)
+        st.build_meta()
+        layers.append(st)
+        inputs.append(li)
+        metas.append(S.oracle_meta(li, pc))
+        _, qb = W.query_trajectory(cfg, layer, steps=steps)
+        qs.append(qb)
+        queries.append(S.q_tensor(qb[0], pc))
+    pc = layers[0].cfg
+    forced = list(pc.forced)
+    stack = R.DecodeStack(layers, queries, torch.device("cuda:0"))
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    stack.step(L.PRR_SCHED_FUSED_PREFILL, s)
+    torch.cuda.synchronize()
+    state = []
+    for layer, st in enumerate(layers):
+        s64 = S.oracle_scores(W.bits_to_f64(qs[layer][0], cfg.dtype), metas[layer], pc)
+        S.check_selection(S.lists(st), s64, pc.k_select, forced, pc.forced_in_budget, what="A0")
+        state.append(O.ema_init(s64))
+    for t in range(1, steps + 1):
+        for layer in range(n_layers):
+            queries[layer].copy_(S.q_tensor(qs[layer][t], pc))
+        torch.cuda.synchronize()
+        preds = [S.lists(st, st.cur) for st in layers]
+        S.log(f"fused PRR step {t}")
+        s.wait_stream(torch.cuda.current_stream())
+        stack.step(L.PRR_SCHED_FUSED_PRR, s)
+        torch.cuda.synchronize()
+        for layer, st in enumerate(layers):
+            q64 = W.bits_to_f64(qs[layer][t], cfg.dtype)
+            level, trend = state[layer]
+            P = S.check_selection(preds[layer], O.ema_predict(level, trend, cfg.gamma), pc.p_select, forced,
+                                  pc.forced_in_budget, what="P")
+            s64 = S.oracle_scores(q64, metas[layer], pc)
+            A = S.check_selection(S.lists(st), s64, pc.k_select, forced, pc.forced_in_budget)
+            target = A if mode == 0 else [np.union1d(x, y) for x, y in zip(A, P)]
+            ref = O.attend(q64, inputs[layer].k64(), inputs[layer].v64(), target, pc.page_size, pc.num_tokens)
+            S.check_attention(S.to_np(st.out_o32), S.to_np(st.out_m), S.to_np(st.out_l), ref, S.to_np(st.out_o),
+                              dtype=pc.dtype, what=f"PRR layer {layer} step {t}")
+            mc, wc = S.to_np(st.missed), S.to_np(st.wasted)
+            for h in range(pc.num_kv_heads):
+                mm, ww = O.missed_and_wasted(A[h], P[h])
+                assert (mc[h], wc[h]) == (len(mm), len(ww)), f"layer {layer} head {h}: missed/wasted counts"
+            state[layer] = O.ema_update(level, trend, s64, cfg.alpha, cfg.beta)
+        S.log(f"fused serial step {t}")
+        stack.step(L.PRR_SCHED_FUSED_SERIAL, s)
+        torch.cuda.synchronize()
+        for layer, st in enumerate(layers):
+            q64 = W.bits_to_f64(qs[layer][t], cfg.dtype)
+            A = S.check_selection(S.lists(st), S.oracle_scores(q64, metas[layer], pc), pc.k_select, forced,
+                                  pc.forced_in_budget)
+            ref = O.attend(q64, inputs[layer].k64(), inputs[layer].v64(), A, pc.page_size, pc.num_tokens)
+            S.check_attention(S.to_np(st.out_o32), S.to_np(st.out_m), S.to_np(st.out_l), ref, S.to_np(st.out_o),
+                              dtype=pc.dtype, what=f"serial layer {layer} step {t}")
+    for st in layers:
+        fl = int(st.workspace[:4].view(torch.int32).cpu()[0])
+        assert fl == 0, f"workspace error flags {fl:#x}"
