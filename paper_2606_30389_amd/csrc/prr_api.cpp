@@ -70,7 +70,8 @@ prr_status check_ptr(const void* p, const char* name, size_t align) {
   } while (0)
 
 struct WsLayout {
-  size_t flags, sel_cnt, rep_cnt, rep_o, rep_ml, f_score, f_thr, f_mcnt, f_mlist, f_part, total;
+  size_t flags, sel_cnt, rep_cnt, rep_o, rep_ml, f_score, f_thr, f_mcnt, f_mlist, f_part, f_cnt, f_candk, f_candp,
+      f_pkey, f_win, total;
   int nchunks, nwork_max, nparts;
 };
 
@@ -102,6 +103,17 @@ bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
   off = align_up(off + (size_t)hkv * cap * 8, 256);
   L.f_part = off;
   off = align_up(off + (size_t)hkv * L.nparts * g * 130 * 8, 256);
+  const size_t nsc = (size_t)div_up(d->max_pages, 128);
+  L.f_cnt = off;
+  off = align_up(off + 2 * (size_t)hkv * nsc * 8, 256);
+  L.f_candk = off;
+  off = align_up(off + 2 * (size_t)hkv * nsc * 128 * 8, 256);
+  L.f_candp = off;
+  off = align_up(off + 2 * (size_t)hkv * nsc * 128 * 8, 256);
+  L.f_pkey = off;
+  off = align_up(off + (size_t)hkv * d->max_pages * 8, 256);
+  L.f_win = off;
+  off = align_up(off + (size_t)hkv * 2 * 4, 256);
   L.total = off;
   return true;
 }
@@ -518,6 +530,11 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.t_mcnt = reinterpret_cast<uint64_t*>(ws + L.f_mcnt);
   a.t_mlist = reinterpret_cast<uint64_t*>(ws + L.f_mlist);
   a.t_part = reinterpret_cast<uint64_t*>(ws + L.f_part);
+  a.t_cnt = reinterpret_cast<uint64_t*>(ws + L.f_cnt);
+  a.t_candk = reinterpret_cast<uint64_t*>(ws + L.f_candk);
+  a.t_candp = reinterpret_cast<uint64_t*>(ws + L.f_candp);
+  a.t_pkey = reinterpret_cast<uint64_t*>(ws + L.f_pkey);
+  a.win = reinterpret_cast<uint32_t*>(ws + L.f_win);
   a.flags = reinterpret_cast<uint32_t*>(ws + L.flags);
   a.alpha = sp->alpha;
   a.beta = sp->beta;

@@ -38,6 +38,7 @@ constexpr int kFPart = kHeadDim + 2;  // o[128], m, l of one query head
 constexpr uint32_t kSelfMiss = 0x80000000u;
 constexpr int kFOPad = kHeadDim + 4;
 constexpr int kEqAll = 16383;  // eq_cut meaning "every key equal to T is taken"
+constexpr int kCandMax = 8 * kFT;  // candidates ranked by one workgroup (8 per thread)
 
 __device__ __forceinline__ void put_tag(uint64_t* p, uint32_t v, uint32_t epoch) {
   __hip_atomic_store(p, ((uint64_t)epoch << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -51,7 +52,7 @@ __device__ __forceinline__ bool tag_is(uint64_t v, uint32_t epoch) { return (uin
 // of *p once it is (bounded wait; a timeout sets a flag and yields garbage).
 __device__ __forceinline__ uint32_t tagged(uint64_t v, const uint64_t* p, uint32_t epoch, uint32_t* flags) {
   for (int it = 0; !tag_is(v, epoch) && it < kFSpin; ++it) {
-    __builtin_amdgcn_s_sleep(1);
+    __builtin_amdgcn_s_sleep(4);
     v = get_tag(p);
   }
   if (!tag_is(v, epoch)) atomicOr(flags, kFlagSpinTimeout);
@@ -66,6 +67,8 @@ __device__ __forceinline__ uint32_t wait_tag(const uint64_t* p, uint32_t epoch, 
 struct FScoreLds {
   float qpart[16][kHeadDim];
   float qbar[kHeadDim];
+  float sc[kFScorePages];
+  uint32_t fbits[kFScorePages / 32];
 };
 
 struct FSelLds {
@@ -74,7 +77,13 @@ struct FSelLds {
   uint32_t forceb[PRR_MAX_PAGES_DEV / 32];
   int32_t mlist[PRR_MAX_CAP_DEV];
   int cnt[2][16];
+  int off[3 * kWave];  // exclusive offsets, counts and forced counts of the score workgroups
+  int tot[2];
+  float qb[kHeadDim];
+  uint32_t ck[kCandMax];
+  uint32_t cpg[kCandMax];
   int eq_cut;
+  int npv;
 };
 
 struct FAttnLds {
@@ -98,12 +107,28 @@ union FLds {
 };
 
 // ------------------------------------------------------------------------ score
+//
+// Besides the scores, a score workgroup filters its pages for the select workgroup: a
+// page is a candidate of A when its key reaches the lower bound win[h][0] kept from the
+// previous step (or it is forced).  When at least k candidates exist the top-k of all
+// pages are among them, so the select workgroup only ranks the candidates; otherwise it
+// falls back to all scores.  In the PRR and prefill schedules the workgroup also applies
+// the EMA update of Eq. (3) to its pages and filters the next prediction's keys
+// (Eq. (2)) the same way, for the predict workgroup.
+
 
 template <bool BF16>
 __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk, FScoreLds& S) {
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int G = a.group;
+  const int n = a.num_pages;
+  const int pbase = blk * kFScorePages;
+  const bool ema = a.schedule != 0;
   const uint16_t* q = static_cast<const uint16_t*>(a.q);
+  // wave 0 owns the filtering: EMA state of pages pbase + lane and pbase + 64 + lane
+  float lv[2] = {0.f, 0.f}, tv[2] = {0.f, 0.f};
+  uint32_t bw[2] = {0u, 0u};
+  const int nwmax = (a.max_pages + 31) / 32;
   {
     const int g = t >> 4, c8 = (t & 15) * 8;
     if (g < G) {
@@ -111,11 +136,22 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
 #pragma unroll
       for (int e = 0; e < 8; ++e) S.qpart[g][c8 + e] = u4_elem<BF16>(v, e);
     }
+    if (t < 4) S.fbits[t] = 0u;
     __syncthreads();
     if (t < kHeadDim) {
       float s = 0.0f;
       for (int gg = 0; gg < G; ++gg) s += S.qpart[gg][t];
       S.qbar[t] = s / (float)G;
+    }
+    if (t == 0 && a.n_forced > 0) {
+      // forced pages of this workgroup's range (the list lives in the kernel arguments:
+      // constant indices only)
+#pragma unroll
+      for (int i = 0; i < PRR_MAX_FORCED; ++i) {
+        if (i >= a.n_forced) break;
+        const int p = a.forced[i] - pbase;
+        if (p >= 0 && p < kFScorePages) S.fbits[p >> 5] |= 1u << (p & 31);
+      }
     }
     __syncthreads();
   }
@@ -123,8 +159,24 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
   float qb[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) qb[e] = S.qbar[cg * 8 + e];
-  const int base = blk * kFScorePages + w * 16 + pi;
-  const int n = a.num_pages;
+  // wave 0 filters: EMA state of pages pbase + lane and pbase + 64 + lane, and the
+  // candidate bounds, kept from the previous step as ratios to |q-bar|_1 (scores scale
+  // with q-bar); loaded together with the metadata
+  float r_a = 0.f, r_p = 0.f;
+  if (w == 0) {
+    r_a = __uint_as_float(a.win[2 * h]);
+    r_p = __uint_as_float(a.win[2 * h + 1]);
+    if (ema) {
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int p = min(pbase + 64 * half + lane, n - 1);
+        lv[half] = a.level[(size_t)h * a.max_pages + p];
+        tv[half] = a.trend[(size_t)h * a.max_pages + p];
+        bw[half] = a.init_bits[(size_t)h * nwmax + (p >> 5)];
+      }
+    }
+  }
+  const int base = pbase + w * 16 + pi;
   float* scores = a.scores + (size_t)h * a.max_pages;
   uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
   float s[4];
@@ -171,55 +223,84 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
   for (int it = 0; it < 4; ++it) {
     const float v = sum16(s[it]);
     const int p = base + 4 * it;
-    if (cg == 0 && p < n) {
-      scores[p] = v;
-      put_tag(&ts[p], __float_as_uint(v), a.epoch);
+    if (cg == 0) {
+      S.sc[p - pbase] = v;
+      if (p < n) {
+        scores[p] = v;
+        put_tag(&ts[p], __float_as_uint(v), a.epoch);
+      }
     }
+  }
+  __syncthreads();
+  if (w != 0) return;
+  const float qn = wave_sum(fabsf(S.qbar[lane]) + fabsf(S.qbar[lane + 64]));
+  const uint32_t lo_a = score_key(r_a * qn), lo_p = score_key(r_p * qn);
+
+  const size_t rec_a = (size_t)h * a.n_score + blk;
+  const size_t rec_p = ((size_t)a.num_kv_heads + h) * a.n_score + blk;
+  uint64_t* ck_a = a.t_candk + rec_a * kFScorePages;
+  uint64_t* cp_a = a.t_candp + rec_a * kFScorePages;
+  uint64_t* ck_p = a.t_candk + rec_p * kFScorePages;
+  uint64_t* cp_p = a.t_candp + rec_p * kFScorePages;
+  int na = 0, nfa = 0, np = 0, nfp = 0;
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    const int lp = 64 * half + lane;
+    const int p = pbase + lp;
+    const bool inr = p < n;
+    const float sv = S.sc[lp];
+    const bool f = inr && ((S.fbits[lp >> 5] >> (lp & 31)) & 1u);
+    const uint32_t ka = score_key(sv);
+    const bool ca = inr && (f || ka >= lo_a);
+    const uint64_t ma = __ballot(ca), mfa = __ballot(ca && f);
+    if (ca) {
+      const int pos = na + lanes_below(ma);
+      put_tag(&ck_a[pos], ka, a.epoch);
+      put_tag(&cp_a[pos], (uint32_t)p | (f ? 0x80000000u : 0u), a.epoch);
+    }
+    na += __popcll(ma);
+    nfa += __popcll(mfa);
+    if (ema) {
+      bool has = inr && ((bw[half] >> (p & 31)) & 1u);
+      float l = lv[half], v = tv[half];
+      if (inr) {
+        if (has) {
+          v = a.beta * (sv - l) + (1.0f - a.beta) * v;  // Eq. (3): the trend reads the previous level
+          l = a.alpha * sv + (1.0f - a.alpha) * l;
+        } else {
+          l = sv;
+          v = 0.0f;
+          has = true;
+        }
+        a.level[(size_t)h * a.max_pages + p] = l;
+        a.trend[(size_t)h * a.max_pages + p] = v;
+      }
+      const uint64_t hm = __ballot(has), vm = __ballot(inr);
+      if (lane == 0 || lane == 32) {
+        const uint32_t hbits = (uint32_t)(lane == 0 ? hm : (hm >> 32));
+        const uint32_t vbits = (uint32_t)(lane == 0 ? vm : (vm >> 32));
+        if (vbits) a.init_bits[(size_t)h * nwmax + (p >> 5)] = (bw[half] & ~vbits) | hbits;
+      }
+      const uint32_t kp = score_key(l + a.gamma * v);  // Eq. (2)
+      if (inr) put_tag(&a.t_pkey[(size_t)h * a.max_pages + p], kp, a.epoch);
+      const bool cpred = inr && (f || kp >= lo_p);
+      const uint64_t mp = __ballot(cpred), mfp = __ballot(cpred && f);
+      if (cpred) {
+        const int pos = np + lanes_below(mp);
+        put_tag(&ck_p[pos], kp, a.epoch);
+        put_tag(&cp_p[pos], (uint32_t)p | (f ? 0x80000000u : 0u), a.epoch);
+      }
+      np += __popcll(mp);
+      nfp += __popcll(mfp);
+    }
+  }
+  if (lane == 0) {
+    put_tag(&a.t_cnt[rec_a], (uint32_t)na | ((uint32_t)nfa << 16), a.epoch);
+    if (ema) put_tag(&a.t_cnt[rec_p], (uint32_t)np | ((uint32_t)nfp << 16), a.epoch);
   }
 }
 
 // ------------------------------------------------------------------------ shared select pieces
-
-// This thread's J scores of KV head h, polled until every one carries this epoch.
-template <int J>
-__device__ __forceinline__ void poll_scores(const FusedLaunch& a, int h, uint32_t (&sb)[J]) {
-  const int n = a.num_pages;
-  const uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
-  uint64_t pending = 0;
-#pragma unroll
-  for (int j = 0; j < J; ++j) {
-    sb[j] = 0u;
-    if (sel2_page<J>(j) < n) pending |= 1ull << j;
-  }
-  for (int it = 0; pending && it < kFSpin; ++it) {
-    uint64_t v[J];
-#pragma unroll
-    for (int j = 0; j < J; ++j) v[j] = get_tag(&ts[min(sel2_page<J>(j), n - 1)]);
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-      if (((pending >> j) & 1ull) && tag_is(v[j], a.epoch)) {
-        sb[j] = (uint32_t)v[j];
-        pending &= ~(1ull << j);
-      }
-    }
-    if (pending) __builtin_amdgcn_s_sleep(1);
-  }
-  if (pending) atomicOr(a.flags, kFlagSpinTimeout);
-}
-
-__device__ __forceinline__ void forced_bitmap(const FusedLaunch& a, uint32_t* forceb) {
-  const int t = threadIdx.x;
-  const int nw = (a.num_pages + 31) >> 5;
-  for (int i = t; i < nw; i += kFT) forceb[i] = 0u;
-  __syncthreads();
-  // the forced list lives in the kernel arguments: read it with constant indices only
-  if (t == 0) {
-#pragma unroll
-    for (int i = 0; i < PRR_MAX_FORCED; ++i)
-      if (i < a.n_forced) atomicOr(&forceb[a.forced[i] >> 5], 1u << (a.forced[i] & 31));
-  }
-  __syncthreads();
-}
 
 __device__ __forceinline__ bool bit_of(const uint32_t* bits, int p) { return (bits[p >> 5] >> (p & 31)) & 1u; }
 
@@ -258,19 +339,12 @@ __device__ __forceinline__ float v_elem(const u32x4_t& v, int e) {
 // transposed, O^T += V^T P^T, as 32 fp32 16x16x4 MFMAs (weights stay fp32): call
 // (tg, cb) contracts tokens {tg, 4+tg, 8+tg, 12+tg}, lane 16j+m supplying
 // V[4j+tg][8m+cb] and p[head n][4j+tg].
-template <bool BF16, int PS, int NPW>
-__device__ __forceinline__ void wave_attend(const FusedLaunch& a, int h, const int (&pg)[NPW], WaveStates<NPW>& st) {
-  constexpr int TPP = PS / 16;
-  constexpr int NTW = NPW * TPP;
-  const float kNegInf = -__builtin_inff();
-  const float scale = 0.08838834764831845f;  // 1/sqrt(128)
+// Query fragments of KV head h for the MFMA layout below (lane 16j+n: head n, channels
+// 32j..32j+31), loaded before a workgroup waits for its page list.
+__device__ __forceinline__ void load_q(const FusedLaunch& a, int h, u32x4_t (&qf)[4]) {
   const int lane = lane_id(), j = lane >> 4, n = lane & 15;
   const int G = a.group;
   const uint16_t* qh = static_cast<const uint16_t*>(a.q) + (size_t)h * G * kHeadDim;
-  const uint16_t* kh = static_cast<const uint16_t*>(a.k_cache) + (size_t)h * a.max_pages * PS * kHeadDim;
-  const uint16_t* vh = static_cast<const uint16_t*>(a.v_cache) + (size_t)h * a.max_pages * PS * kHeadDim;
-
-  u32x4_t qf[4];
   if (n < G) {
     const u32x4_t* src = reinterpret_cast<const u32x4_t*>(qh + (size_t)n * kHeadDim + 32 * j);
 #pragma unroll
@@ -279,6 +353,18 @@ __device__ __forceinline__ void wave_attend(const FusedLaunch& a, int h, const i
 #pragma unroll
     for (int s = 0; s < 4; ++s) qf[s] = u32x4_t{0, 0, 0, 0};
   }
+}
+
+template <bool BF16, int PS, int NPW>
+__device__ __forceinline__ void wave_attend(const FusedLaunch& a, int h, const u32x4_t (&qf)[4], const int (&pg)[NPW],
+                                            WaveStates<NPW>& st) {
+  constexpr int TPP = PS / 16;
+  constexpr int NTW = NPW * TPP;
+  const float kNegInf = -__builtin_inff();
+  const float scale = 0.08838834764831845f;  // 1/sqrt(128)
+  const int lane = lane_id(), j = lane >> 4, n = lane & 15;
+  const uint16_t* kh = static_cast<const uint16_t*>(a.k_cache) + (size_t)h * a.max_pages * PS * kHeadDim;
+  const uint16_t* vh = static_cast<const uint16_t*>(a.v_cache) + (size_t)h * a.max_pages * PS * kHeadDim;
   int phys[NPW];
 #pragma unroll
   for (int k = 0; k < NPW; ++k) phys[k] = (pg[k] >= 0 && a.page_table) ? a.page_table[pg[k]] : pg[k];
@@ -435,182 +521,347 @@ __device__ __forceinline__ void fold_publish(const FusedLaunch& a, int h, int sl
 __device__ __forceinline__ bool page_forced(const FusedLaunch& a, int p) {
   bool f = false;
 #pragma unroll
-  for (int i = 0; i < PRR_MAX_FORCED; ++i) f |= i < a.n_forced && a.forced[i] == p;
+  for (int i = 0; i < PRR_MAX_FORCED; ++i) {
+    if (i >= a.n_forced) break;
+    f |= a.forced[i] == p;
+  }
   return f;
 }
 
 // ------------------------------------------------------------------------ select
 
-template <bool BF16, int PS, int J>
-__device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U) {
-  FSelLds& L = U.sel;
+// Candidates of list `which` (0: A, 1: the next P) of KV head h.  Thread t serves score
+// workgroup t / 8: it loads that workgroup's count together with the workgroup's
+// entries t % 8 and t % 8 + 8 (most workgroups have fewer than 16 candidates, so one
+// round trip usually brings everything), then the list is laid out in LDS in page
+// order (exclusive offsets of the workgroups by a wave prefix sum).
+struct FCand {
+  int total, nforced;
+};
+
+__device__ __forceinline__ FCand cand_load(const FusedLaunch& a, int h, int which, int* off, int* tot, uint32_t* lk,
+                                           uint32_t* lp) {
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
-  const int n = a.num_pages, nw = (n + 31) >> 5;
-  const bool prr = a.schedule == 1;
-  // bitmaps of the forced pages and of P^t
-  for (int i = t; i < nw; i += kFT) {
-    L.forceb[i] = 0u;
-    L.bitP[i] = 0u;
+  const int nS = a.n_score;
+  const int wg = t >> 3, sub = t & 7;
+  const bool mine = wg < nS;
+  const size_t rec = ((size_t)which * a.num_kv_heads + h) * nS + min(wg, nS - 1);
+  const uint64_t* ck = a.t_candk + rec * kFScorePages;
+  const uint64_t* cp = a.t_candp + rec * kFScorePages;
+  // the count and the first two entries are polled together until all needed are there
+  uint64_t vc = 0, k0 = 0, p0 = 0, k1 = 0, p1 = 0;
+  uint32_t c = 0u;
+  for (int it = 0; mine && it < kFSpin; ++it) {
+    vc = get_tag(&a.t_cnt[rec]);
+    k0 = get_tag(&ck[sub]);
+    p0 = get_tag(&cp[sub]);
+    k1 = get_tag(&ck[sub + 8]);
+    p1 = get_tag(&cp[sub + 8]);
+    if (tag_is(vc, a.epoch)) {
+      c = (uint32_t)vc;
+      const int n0 = (int)(c & 0xffffu);
+      const bool ok0 = sub >= n0 || (tag_is(k0, a.epoch) && tag_is(p0, a.epoch));
+      const bool ok1 = sub + 8 >= n0 || (tag_is(k1, a.epoch) && tag_is(p1, a.epoch));
+      if (ok0 && ok1) break;
+    }
+    __builtin_amdgcn_s_sleep(2);
+    if (it == kFSpin - 1) atomicOr(a.flags, kFlagSpinTimeout);
   }
-  if (t == 0) L.eq_cut = kEqAll;
+  const int nc = (int)(c & 0xffffu);
+  if (mine && sub == 0) {
+    off[kWave + wg] = nc;
+    off[2 * kWave + wg] = (int)(c >> 16);
+  }
   __syncthreads();
-  if (t == 0) {
-#pragma unroll
-    for (int i = 0; i < PRR_MAX_FORCED; ++i)
-      if (i < a.n_forced) atomicOr(&L.forceb[a.forced[i] >> 5], 1u << (a.forced[i] & 31));
-  }
-  if (prr) {
-    const int pc = min(max(a.pred_cur_count[h], 0), a.cap);
-    for (int i = t; i < pc; i += kFT) {
-      const int p = a.pred_cur[(size_t)h * a.cap + i];
-      if (p >= 0 && p < n) atomicOr(&L.bitP[p >> 5], 1u << (p & 31));
+  if (w == 0) {
+    const int cw = lane < nS ? off[kWave + lane] : 0;
+    const int fw = lane < nS ? off[2 * kWave + lane] : 0;
+    const int incl = wave_inclusive_scan(cw);
+    if (lane < nS) off[lane] = incl - cw;
+    const int ft = wave_isum(fw);
+    if (lane == kWave - 1) {
+      tot[0] = incl;
+      tot[1] = ft;
     }
   }
   __syncthreads();
+  FCand r;
+  r.total = tot[0];
+  r.nforced = tot[1];
+  if (mine && r.total <= kCandMax) {
+    const int o = off[wg];
+    if (sub < nc) {
+      lk[o + sub] = tagged(k0, &ck[sub], a.epoch, a.flags);
+      lp[o + sub] = tagged(p0, &cp[sub], a.epoch, a.flags);
+    }
+    if (sub + 8 < nc) {
+      lk[o + sub + 8] = tagged(k1, &ck[sub + 8], a.epoch, a.flags);
+      lp[o + sub + 8] = tagged(p1, &cp[sub + 8], a.epoch, a.flags);
+    }
+    for (int slot = sub + 16; slot < nc; slot += 8) {
+      lk[o + slot] = wait_tag(&ck[slot], a.epoch, a.flags);
+      lp[o + slot] = wait_tag(&cp[slot], a.epoch, a.flags);
+    }
+  }
+  __syncthreads();
+  return r;
+}
 
-  uint32_t sb[J];
-  poll_scores<J>(a, h, sb);
-  uint32_t key[J];
-  uint64_t cand = 0, force = 0, inP = 0;
+// The candidate list (LDS, page order) into this thread's slots i = (w, j, lane).
+template <int J>
+__device__ __forceinline__ void cand_slots(int total, const uint32_t* lk, const uint32_t* lp, uint32_t (&key)[J],
+                                           int (&page)[J], uint64_t& cand, uint64_t& force) {
+  cand = 0;
+  force = 0;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
-    const int p = sel2_page<J>(j);
-    const int pc = min(p, n - 1);
-    key[j] = score_key(__uint_as_float(sb[j]));
-    const bool f = p < n && bit_of(L.forceb, pc);
-    if (p < n && !f) cand |= 1ull << j;
-    if (f) force |= 1ull << j;
-    if (p < n && bit_of(L.bitP, pc)) inP |= 1ull << j;
+    const int i = sel2_page<J>(j);
+    key[j] = 0u;
+    page[j] = 0;
+    if (i < total) {
+      key[j] = lk[i];
+      const uint32_t pv = lp[i];
+      page[j] = (int)(pv & 0x7fffffffu);
+      if (pv >> 31) force |= 1ull << j;
+      else cand |= 1ull << j;
+    }
+  }
+}
+
+// All pages of KV head h as slots (the fallback): keys polled from `tk`.
+template <int J>
+__device__ __forceinline__ void full_gather(const FusedLaunch& a, const uint64_t* tk, const uint32_t* forceb,
+                                            uint32_t (&key)[J], int (&page)[J], uint64_t& cand, uint64_t& force) {
+  const int n = a.num_pages;
+  uint64_t pending = 0;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    key[j] = 0u;
+    page[j] = sel2_page<J>(j);
+    if (page[j] < n) pending |= 1ull << j;
+  }
+  for (int it = 0; pending && it < kFSpin; ++it) {
+    uint64_t v[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) v[j] = get_tag(&tk[min(page[j], n - 1)]);
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      if (((pending >> j) & 1ull) && tag_is(v[j], a.epoch)) {
+        key[j] = (uint32_t)v[j];
+        pending &= ~(1ull << j);
+      }
+    }
+    if (pending) __builtin_amdgcn_s_sleep(4);
+  }
+  if (pending) atomicOr(a.flags, kFlagSpinTimeout);
+  cand = 0;
+  force = 0;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    if (page[j] >= n) continue;
+    if (bit_of(forceb, page[j])) force |= 1ull << j;
+    else cand |= 1ull << j;
+  }
+}
+
+// Lower bound of the next step's candidates: the score of rank 3k among this step's
+// candidates, kept as a ratio to |q-bar|_1 (kept unchanged when fewer than 3k
+// candidates exist and `keep` is set; -inf, i.e. every page, after a fallback that
+// found fewer than 3k pages).
+__device__ __forceinline__ float key_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+template <int J>
+__device__ __forceinline__ void update_window(const FusedLaunch& a, uint32_t* win, float qn, const uint32_t (&key)[J],
+                                              uint64_t cand, int k, bool keep, Sel2Lds& S) {
+  __syncthreads();  // the LDS may still be read by the previous step of this workgroup
+  const SelThreshold th = sel2_threshold<kFT, J>(key, cand, 3 * max(k, 1), S);
+  if (threadIdx.x == 0) {
+    if (th.mode == 2 && qn > 0.0f) *win = __float_as_uint(key_value(th.T) / qn);
+    else if (!keep) *win = __float_as_uint(-__builtin_inff());
+  }
+}
+
+// |q-bar_h|_1 (every thread), with q-bar as the score workgroups compute it.
+template <bool BF16>
+__device__ __forceinline__ float qbar_l1(const FusedLaunch& a, int h, float* qb) {
+  const int t = threadIdx.x;
+  const int G = a.group;
+  const uint16_t* q = static_cast<const uint16_t*>(a.q) + (size_t)h * G * kHeadDim;
+  if (t < kHeadDim) {
+    float s = 0.0f;
+    for (int g = 0; g < G; ++g) s += h2f<BF16>(q[(size_t)g * kHeadDim + t]);
+    qb[t] = fabsf(s / (float)G);
+  }
+  __syncthreads();
+  return wave_sum(qb[lane_id()] + qb[lane_id() + 64]);
+}
+
+template <bool BF16, int PS, int J>
+__device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const uint32_t (&key)[J],
+                                              const int (&page)[J], uint64_t cand, uint64_t force, bool keep_window,
+                                              float qn, FLds& U) {
+  FSelLds& L = U.sel;
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  const bool prr = a.schedule == 1;
+  uint64_t inP = 0;
+  if (prr) {
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+      if ((((cand | force) >> j) & 1ull) && bit_of(L.bitP, page[j])) inP |= 1ull << j;
   }
   const SelThreshold th = sel2_threshold<kFT, J>(key, cand, a.kextra_a, L.sel);
-  const bool early = th.mode != 2 || th.need_eq == th.eq_total;
+  const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
   uint64_t* thr = a.t_thr + 2 * (size_t)h;
   if (prr && early && t == 0) {
     put_tag(thr, th.T, a.epoch);
     put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), a.epoch);
   }
-  const uint64_t inA = sel2_compact<kFT, J>(key, cand, force, th, a.selected + (size_t)h * a.cap, a.cap,
-                                            a.selected_count + h, &L.eq_cut, L.sel);
-  __syncthreads();
-  if (prr && !early && t == 0) {
-    put_tag(thr, th.T, a.epoch);
-    put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)L.eq_cut << 2), a.epoch);
+  const uint64_t inA = sel2_membership<kFT, J>(key, page, cand, force, th, &L.eq_cut, L.sel);
+  if (prr && !early) {
+    __syncthreads();
+    if (t == 0) {
+      put_tag(thr, th.T, a.epoch);
+      put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)L.eq_cut << 2), a.epoch);
+    }
   }
 
-  // the list to attend after selection: A \ P (PRR) or A (serial), in page order
+  // the list to attend after selection, in page order: A \ P (PRR) or A (serial)
   const uint64_t inM = prr ? (inA & ~inP) : inA;
-  const uint64_t inW = prr ? (inP & ~inA) : 0ull;
-  const int mc = wave_isum(__popcll(inM)), wc = wave_isum(__popcll(inW));
-  if (lane == 0) {
-    L.cnt[0][w] = mc;
-    L.cnt[1][w] = wc;
-  }
-  __syncthreads();
-  int mbase = 0, nM = 0, nW = 0;
-#pragma unroll
-  for (int i = 0; i < kFW; ++i) {
-    mbase += i < w ? L.cnt[0][i] : 0;
-    nM += L.cnt[0][i];
-    nW += L.cnt[1][i];
-  }
-#pragma unroll
-  for (int j = 0; j < J; ++j) {
-    const bool in = (inM >> j) & 1ull;
-    const uint64_t bm = __ballot(in);
-    if (in) {
-      const int pos = mbase + lanes_below(bm);
-      if (pos < a.cap) L.mlist[pos] = sel2_page<J>(j);
-    }
-    mbase += __popcll(bm);
-  }
-  nM = min(nM, a.cap);
-  if (t == 0) {
-    if (a.missed_count) a.missed_count[h] = nM;
-    if (a.wasted_count) a.wasted_count[h] = nW;
-  }
+  const int nM = min(sel2_list<kFT, J>(inM, page, L.mlist, a.cap, L.sel), a.cap);
   __syncthreads();
   if (nM == 0) {
     if (t == 0) put_tag(&a.t_mcnt[h], 0u, a.epoch);
-  } else if (nM <= kFW) {
+  } else if (nM > kFW) {
+    uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
+    for (int i = t; i < nM; i += kFT) put_tag(&ml[i], (uint32_t)L.mlist[i], a.epoch);
+    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM, a.epoch);
+  }
+  // the selected list (an output) and the counts
+  int32_t* sel = a.selected + (size_t)h * a.cap;
+  int nA;
+  if (prr) {
+    nA = min(sel2_list<kFT, J>(inA, page, sel, a.cap, L.sel), a.cap);
+  } else {
+    nA = nM;
+    for (int i = t; i < nM; i += kFT) sel[i] = L.mlist[i];
+  }
+  const int nPA = prr ? block_sum<kFT>(__popcll(inP & inA), L.sel.red[2]) : 0;
+  if (t == 0) {
+    a.selected_count[h] = nA;
+    if (a.missed_count) a.missed_count[h] = nM;
+    if (a.wasted_count) a.wasted_count[h] = prr ? L.npv - nPA : 0;
+  }
+  if (nM > 0 && nM <= kFW) {
     // few enough to attend here: one page per wave, published as the first miss slot
     if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM | kSelfMiss, a.epoch);
     int pg[1];
     pg[0] = __builtin_amdgcn_readfirstlane(w < nM ? L.mlist[w] : -1);
     __syncthreads();  // the list is read before the attention reuses the LDS
+    u32x4_t qf[4];
+    load_q(a, h, qf);
     WaveStates<1> st;
-    wave_attend<BF16, PS, 1>(a, h, pg, st);
+    wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
     fold_publish<1>(a, h, a.n_spec, st, 1u, U.attn);
+  }
+  update_window<J>(a, a.win + 2 * h, qn, key, cand, a.kextra_a, keep_window, U.sel.sel);
+}
+
+template <bool BF16, int PS>
+__device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U) {
+  FSelLds& L = U.sel;
+  const int t = threadIdx.x;
+  const int n = a.num_pages, nw = (n + 31) >> 5;
+  // bitmaps of the forced pages (fallback) and of P^t (PRR), |P^t| in npv
+  for (int i = t; i < nw; i += kFT) {
+    L.forceb[i] = 0u;
+    L.bitP[i] = 0u;
+  }
+  if (t == 0) {
+    L.eq_cut = kEqAll;
+    L.npv = 0;
+  }
+  __syncthreads();
+  if (t == 0 && a.n_forced > 0) {
+#pragma unroll
+    for (int i = 0; i < PRR_MAX_FORCED; ++i) {
+      if (i >= a.n_forced) break;
+      atomicOr(&L.forceb[a.forced[i] >> 5], 1u << (a.forced[i] & 31));
+    }
+  }
+  if (a.schedule == 1) {
+    const int pc = min(max(a.pred_cur_count[h], 0), a.cap);
+    for (int i = t; i < pc; i += kFT) {
+      const int p = a.pred_cur[(size_t)h * a.cap + i];
+      if (p >= 0 && p < n) {
+        const uint32_t old = atomicOr(&L.bitP[p >> 5], 1u << (p & 31));
+        if (!((old >> (p & 31)) & 1u)) atomicAdd(&L.npv, 1);
+      }
+    }
+  }
+  const float qn = qbar_l1<BF16>(a, h, L.qb);
+  const FCand c = cand_load(a, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  if (a.kextra_a <= c.total - c.nforced && c.total <= kCandMax) {
+    // one instantiation per path keeps the kernel's code (and its instruction-cache
+    // footprint) small: 8 candidate slots per thread, 16 page slots in the fallback
+    uint32_t key[8];
+    int page[8];
+    uint64_t cand, force;
+    cand_slots<8>(c.total, L.ck, L.cpg, key, page, cand, force);
+    select_finish<BF16, PS, 8>(a, h, key, page, cand, force, true, qn, U);
   } else {
-    uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
-    for (int i = t; i < nM; i += kFT) put_tag(&ml[i], (uint32_t)L.mlist[i], a.epoch);
-    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM, a.epoch);
+    uint32_t key[16];
+    int page[16];
+    uint64_t cand, force;
+    full_gather<16>(a, a.t_score + (size_t)h * a.max_pages, L.forceb, key, page, cand, force);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) key[j] = score_key(__uint_as_float(key[j]));
+    select_finish<BF16, PS, 16>(a, h, key, page, cand, force, false, qn, U);
   }
 }
 
 // ------------------------------------------------------------------------ predict
 
 template <int J>
+__device__ __forceinline__ void predict_finish(const FusedLaunch& a, int h, const uint32_t (&key)[J],
+                                               const int (&page)[J], uint64_t cand, uint64_t force, bool keep_window,
+                                               float qn, FSelLds& L) {
+  const SelThreshold th = sel2_threshold<kFT, J>(key, cand, a.kextra_p, L.sel);
+  sel2_compact<kFT, J>(key, page, cand, force, th, a.pred_nxt + (size_t)h * a.cap, a.cap, a.pred_nxt_count + h,
+                       &L.eq_cut, L.sel);
+  update_window<J>(a, a.win + 2 * h + 1, qn, key, cand, a.kextra_p, keep_window, L.sel);
+}
+
+template <bool BF16>
 __device__ __forceinline__ void role_predict(const FusedLaunch& a, int h, FLds& U) {
   FSelLds& L = U.sel;
-  const int lane = lane_id();
-  const int n = a.num_pages;
-  forced_bitmap(a, L.forceb);
-  uint32_t sb[J];
-  poll_scores<J>(a, h, sb);
-  const int nwmax = (a.max_pages + 31) / 32;
-  float* level = a.level + (size_t)h * a.max_pages;
-  float* trend = a.trend + (size_t)h * a.max_pages;
-  uint32_t* bits = a.init_bits + (size_t)h * nwmax;
-  uint32_t key[J];
-  uint64_t cand = 0, force = 0;
-  constexpr int JB = J < 16 ? J : 16;  // EMA state is loaded in batches of 16 keys per thread
+  const int t = threadIdx.x;
+  const int n = a.num_pages, nw = (n + 31) >> 5;
+  for (int i = t; i < nw; i += kFT) L.forceb[i] = 0u;
+  __syncthreads();
+  if (t == 0 && a.n_forced > 0) {
 #pragma unroll
-  for (int j0 = 0; j0 < J; j0 += JB) {
-    float lv[JB], tv[JB];
-    uint32_t bw[JB];
-#pragma unroll
-    for (int jj = 0; jj < JB; ++jj) {
-      const int p = min(sel2_page<J>(j0 + jj), n - 1);
-      lv[jj] = level[p];
-      tv[jj] = trend[p];
-      bw[jj] = bits[p >> 5];
-    }
-#pragma unroll
-    for (int jj = 0; jj < JB; ++jj) {
-      const int j = j0 + jj;
-      const int p = sel2_page<J>(j);
-      const bool inr = p < n;
-      bool has = inr && ((bw[jj] >> (p & 31)) & 1u);
-      float l = lv[jj], v = tv[jj];
-      if (inr) {
-        const float s = __uint_as_float(sb[j]);
-        if (has) {
-          v = a.beta * (s - l) + (1.0f - a.beta) * v;  // Eq. (3): the trend reads the previous level
-          l = a.alpha * s + (1.0f - a.alpha) * l;
-        } else {
-          l = s;
-          v = 0.0f;
-          has = true;
-        }
-        level[p] = l;
-        trend[p] = v;
-      }
-      key[j] = score_key(l + a.gamma * v);  // Eq. (2)
-      const bool f = inr && bit_of(L.forceb, p);
-      if (has && !f) cand |= 1ull << j;
-      if (f) force |= 1ull << j;
-      const uint64_t hm = __ballot(has);
-      const uint64_t vm = __ballot(inr);
-      if (lane == 0 || lane == 32) {
-        const uint32_t hbits = (uint32_t)(lane == 0 ? hm : (hm >> 32));
-        const uint32_t vbits = (uint32_t)(lane == 0 ? vm : (vm >> 32));
-        if (vbits) bits[p >> 5] = (bw[jj] & ~vbits) | hbits;
-      }
+    for (int i = 0; i < PRR_MAX_FORCED; ++i) {
+      if (i >= a.n_forced) break;
+      atomicOr(&L.forceb[a.forced[i] >> 5], 1u << (a.forced[i] & 31));
     }
   }
-  const SelThreshold th = sel2_threshold<kFT, J>(key, cand, a.kextra_p, L.sel);
-  sel2_compact<kFT, J>(key, cand, force, th, a.pred_nxt + (size_t)h * a.cap, a.cap, a.pred_nxt_count + h,
-                       &L.eq_cut, L.sel);
+  const float qn = qbar_l1<BF16>(a, h, L.qb);
+  const FCand c = cand_load(a, h, 1, L.off, L.tot, L.ck, L.cpg);
+  if (a.kextra_p <= c.total - c.nforced && c.total <= kCandMax) {
+    uint32_t key[8];
+    int page[8];
+    uint64_t cand, force;
+    cand_slots<8>(c.total, L.ck, L.cpg, key, page, cand, force);
+    predict_finish<8>(a, h, key, page, cand, force, true, qn, L);
+  } else {
+    uint32_t key[16];
+    int page[16];
+    uint64_t cand, force;
+    full_gather<16>(a, a.t_pkey + (size_t)h * a.max_pages, L.forceb, key, page, cand, force);
+    predict_finish<16>(a, h, key, page, cand, force, false, qn, L);
+  }
 }
 
 // ------------------------------------------------------------------------ spec / miss
@@ -622,6 +873,8 @@ __device__ __forceinline__ void role_spec(const FusedLaunch& a, int h, int c, FL
   if (start >= count) return;
   const int cnt = min(a.chunk, count - start);
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  u32x4_t qf[4];
+  load_q(a, h, qf);
   int pg[NPW];
   uint32_t keep = 0;
 #pragma unroll
@@ -637,7 +890,7 @@ __device__ __forceinline__ void role_spec(const FusedLaunch& a, int h, int c, FL
     if (p >= 0) keep |= 1u << k;
   }
   WaveStates<NPW> st;
-  wave_attend<BF16, PS, NPW>(a, h, pg, st);
+  wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
   if (a.mode == PRR_EXACT_SELECTED && keep) {
     // membership of this wave's pages in A, from their scores and the published
     // threshold (all loads issued together, then waited for)
@@ -670,11 +923,26 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, int h, int u, FL
   // published before the count, so they are usually valid when the count is
   const int start = u * a.chunk;
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  u32x4_t qf[4];
+  load_q(a, h, qf);
   const uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
   uint64_t ve[NPW];
+  uint32_t mv = 0u;
+  for (int it = 0; it < kFSpin; ++it) {
+    const uint64_t vm = get_tag(a.t_mcnt + h);
 #pragma unroll
-  for (int k = 0; k < NPW; ++k) ve[k] = get_tag(&ml[min(start + w + kFW * k, a.cap - 1)]);
-  const uint32_t mv = wait_tag(a.t_mcnt + h, a.epoch, a.flags);
+    for (int k = 0; k < NPW; ++k) ve[k] = get_tag(&ml[min(start + w + kFW * k, a.cap - 1)]);
+    if (tag_is(vm, a.epoch)) {
+      mv = (uint32_t)vm;
+      const int nm = (mv & kSelfMiss) ? 0 : (int)(mv & ~kSelfMiss);
+      bool ok = true;
+#pragma unroll
+      for (int k = 0; k < NPW; ++k) ok = ok && (start + w + kFW * k >= nm || tag_is(ve[k], a.epoch));
+      if (ok) break;
+    }
+    __builtin_amdgcn_s_sleep(2);
+    if (it == kFSpin - 1 && lane_id() == 0) atomicOr(a.flags, kFlagSpinTimeout);
+  }
   if (mv & kSelfMiss) return;
   const int nM = (int)(mv & ~kSelfMiss);
   if (start >= nM) return;
@@ -694,7 +962,7 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, int h, int u, FL
     if (p >= 0) keep |= 1u << k;
   }
   WaveStates<NPW> st;
-  wave_attend<BF16, PS, NPW>(a, h, pg, st);
+  wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
   fold_publish<NPW>(a, h, a.n_spec + u, st, keep, U.attn);
 }
 
@@ -717,34 +985,25 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, 
   const int slot_gap = a.n_spec - nspec;
 #define PRR_ELEM(i, idx) (part + (size_t)((i) < nspec ? (i) : (i) + slot_gap) * sstride + (idx))
 
-  // This thread's output values of states g, g+4, .. (batches of 16) and the (m, l) of
-  // states t, t+512, ..: the first batch and every (m, l) are polled in one loop, so the
-  // merge starts one round trip after the last state is published.
+  // Only the (m, l) of every state are polled (threads t, t+512, ..): polling the output
+  // values themselves from every thread of every merge workgroup would flood the memory
+  // system while the states are being computed.  The output values are loaded once
+  // every (m, l) is there.
   const int c = t & (kHeadDim - 1), g = t >> 7;
   constexpr int kB = 16;
   uint64_t ov[kB];
-  uint32_t pend = 0;
-#pragma unroll
-  for (int r = 0; r < kB; ++r)
-    if (g + 4 * r < total) pend |= 1u << r;
   float mt = kNegInf;
-  for (int it = 0; it < kFSpin; ++it) {
-#pragma unroll
-    for (int r = 0; r < kB; ++r)
-      if ((pend >> r) & 1u) ov[r] = get_tag(PRR_ELEM(g + 4 * r, c));
-    bool ml_ok = true;
-    for (int i = t; i < total; i += kFT) {
-      const uint64_t vm = get_tag(PRR_ELEM(i, kHeadDim)), vl = get_tag(PRR_ELEM(i, kHeadDim + 1));
-      ml_ok = ml_ok && tag_is(vm, a.epoch) && tag_is(vl, a.epoch);
-      L.m[i] = __uint_as_float((uint32_t)vm);
-      L.w[i] = __uint_as_float((uint32_t)vl);
+  for (int i = t; i < total; i += kFT) {
+    uint64_t vm = 0, vl = 0;
+    for (int it = 0; it < kFSpin; ++it) {
+      vm = get_tag(PRR_ELEM(i, kHeadDim));
+      vl = get_tag(PRR_ELEM(i, kHeadDim + 1));
+      if (tag_is(vm, a.epoch) && tag_is(vl, a.epoch)) break;
+      __builtin_amdgcn_s_sleep(2);
+      if (it == kFSpin - 1) atomicOr(a.flags, kFlagSpinTimeout);
     }
-#pragma unroll
-    for (int r = 0; r < kB; ++r)
-      if (((pend >> r) & 1u) && tag_is(ov[r], a.epoch)) pend &= ~(1u << r);
-    if (!pend && ml_ok) break;
-    __builtin_amdgcn_s_sleep(1);
-    if (it == kFSpin - 1) atomicOr(a.flags, kFlagSpinTimeout);
+    L.m[i] = __uint_as_float((uint32_t)vm);
+    L.w[i] = __uint_as_float((uint32_t)vl);
   }
   for (int i = t; i < total; i += kFT)
     if (L.w[i] > 0.0f) mt = fmaxf(mt, L.m[i]);
@@ -773,7 +1032,7 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, 
 #pragma unroll
     for (int r = 0; r < kB; ++r) {
       const int i = b0 + g + 4 * r;
-      if (b0 > 0 && i < total) ov[r] = get_tag(PRR_ELEM(i, c));
+      ov[r] = i < total ? get_tag(PRR_ELEM(i, c)) : 0ull;
     }
 #pragma unroll
     for (int r = 0; r < kB; ++r) {
@@ -810,25 +1069,13 @@ __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
   }
   b -= H * a.n_score;
   if (b < H) {
-    switch (sel2_j(a.num_pages, kFT)) {
-      case 1: role_select<BF16, PS, 1>(a, b, U); break;
-      case 2: role_select<BF16, PS, 2>(a, b, U); break;
-      case 4: role_select<BF16, PS, 4>(a, b, U); break;
-      case 8: role_select<BF16, PS, 8>(a, b, U); break;
-      default: role_select<BF16, PS, 16>(a, b, U); break;
-    }
+    role_select<BF16, PS>(a, b, U);
     return;
   }
   b -= H;
   if (a.schedule != 0) {
     if (b < H) {
-      switch (sel2_j(a.num_pages, kFT)) {
-        case 1: role_predict<1>(a, b, U); break;
-        case 2: role_predict<2>(a, b, U); break;
-        case 4: role_predict<4>(a, b, U); break;
-        case 8: role_predict<8>(a, b, U); break;
-        default: role_predict<16>(a, b, U); break;
-      }
+      role_predict<BF16>(a, b, U);
       return;
     }
     b -= H;

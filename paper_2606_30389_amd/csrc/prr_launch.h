@@ -115,6 +115,11 @@ struct FusedLaunch {
   uint64_t* t_mcnt;   // [Hkv] tagged count of the missed list (bit 31: attended by the select workgroup)
   uint64_t* t_mlist;  // [Hkv][cap] tagged missed pages
   uint64_t* t_part;   // [Hkv][nparts][G][130] tagged partial states
+  uint64_t* t_cnt;    // [2][Hkv][n_score] tagged candidate counts of A and of P^{t+1}
+  uint64_t* t_candk;  // [2][Hkv][n_score][128] tagged candidate keys
+  uint64_t* t_candp;  // [2][Hkv][n_score][128] tagged candidate pages (bit 31: forced)
+  uint64_t* t_pkey;   // [Hkv][max_pages] tagged keys of the next prediction (EMA)
+  uint32_t* win;      // [Hkv][2] candidate lower bounds (keys) for A and P, kept across steps
   uint32_t* flags;
   float alpha, beta, gamma;
   uint32_t epoch;

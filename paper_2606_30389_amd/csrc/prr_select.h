@@ -117,37 +117,32 @@ __device__ __forceinline__ SelThreshold sel2_threshold(const uint32_t (&key)[J],
     }
     __syncthreads();
     if (w == 0) {
-      // lane l owns bins [2048 - 32(l+1), 2048 - 32l); c[i] is bin base + i
+      // lane l owns bins [2048 - 32(l+1), 2048 - 32l), summed, then a prefix over lanes
+      // (lane 0 holds the top bins) finds the lane holding rank `rank`; its 32 bins are
+      // then spread over lanes 0..31 and a second prefix finds the bin
       const int base = kSel2Bins - 32 * (lane + 1);
-      uint32_t c[32];
       const uint4* hb = reinterpret_cast<const uint4*>(hist + base);
+      int s = 0;
 #pragma unroll
       for (int v = 0; v < 8; ++v) {
         const uint4 x = hb[v];
-        c[4 * v] = x.x;
-        c[4 * v + 1] = x.y;
-        c[4 * v + 2] = x.z;
-        c[4 * v + 3] = x.w;
+        s += (int)(x.x + x.y + x.z + x.w);
       }
-      int s = 0;
-#pragma unroll
-      for (int i = 0; i < 32; ++i) s += (int)c[i];
       const int incl = wave_inclusive_scan(s);
       const int excl = incl - s;
-      if (excl < rank && rank <= incl) {
-        int run = excl;
-        bool found = false;
-#pragma unroll
-        for (int i = 31; i >= 0; --i) {
-          const int ci = (int)c[i];
-          if (!found && run + ci >= rank) {
-            S.res[0] = base + i;
-            S.res[1] = run;
-            S.res[2] = ci;
-            found = true;
-          }
-          run += ci;
-        }
+      const uint64_t hit = __ballot(excl < rank && rank <= incl);
+      const int ls = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit) - 1);
+      const int ex = __builtin_amdgcn_readlane(excl, ls);
+      const int lbase = kSel2Bins - 32 * (ls + 1);
+      // lane j < 32 takes bin lbase + 31 - j (descending)
+      const int cj = lane < 32 ? (int)hist[lbase + 31 - lane] : 0;
+      const int cinc = wave_inclusive_scan(cj);
+      const uint64_t hit2 = __ballot(lane < 32 && ex + cinc >= rank);
+      const int js = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit2) - 1);
+      if (lane == js) {
+        S.res[0] = lbase + 31 - js;
+        S.res[1] = ex + cinc - cj;
+        S.res[2] = cj;
       }
     } else {
       // clear the other histogram for the next pass while wave 0 scans this one
@@ -168,28 +163,29 @@ __device__ __forceinline__ SelThreshold sel2_threshold(const uint32_t (&key)[J],
       break;
     }
     if (cbin <= kSel2Small) {
-      // rank the few keys of this bin directly
+      // rank the few keys of this bin directly (one slot reservation per thread)
+      int mine_n = 0;
 #pragma unroll
-      for (int j = 0; j < J; ++j) {
-        if (((cand >> j) & 1ull) && key[j] >= lo && key[j] <= hi) S.small[atomicAdd(&S.nsmall, 1)] = key[j];
+      for (int j = 0; j < J; ++j) mine_n += (((cand >> j) & 1ull) && key[j] >= lo && key[j] <= hi) ? 1 : 0;
+      if (mine_n) {
+        int slot = atomicAdd(&S.nsmall, mine_n);
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+          if (((cand >> j) & 1ull) && key[j] >= lo && key[j] <= hi) S.small[slot++] = key[j];
+        }
       }
       __syncthreads();
       if (w == 0) {
         const uint32_t mine = S.small[lane < cbin ? lane : 0];
         int gt = 0, ge = 0;
-        const uint4* sv = reinterpret_cast<const uint4*>(S.small);
-#pragma unroll
-        for (int v = 0; v < kSel2Small / 4; ++v) {
-          const uint4 x = sv[v];
-          const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const bool live = 4 * v + e < cbin;
-            gt += (live && xs[e] > mine) ? 1 : 0;
-            ge += (live && xs[e] >= mine) ? 1 : 0;
-          }
+        for (int x = 0; x < cbin; ++x) {
+          const uint32_t kx = (uint32_t)__builtin_amdgcn_readlane((int)mine, x);
+          gt += kx > mine ? 1 : 0;
+          ge += kx >= mine ? 1 : 0;
         }
-        if (lane < cbin && gt < rank && rank <= ge) {
+        const uint64_t hit = __ballot(lane < cbin && gt < rank && rank <= ge);
+        const int ls = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit) - 1);
+        if (lane == ls) {
           S.res[3] = (int)mine;
           S.res[4] = rank - gt;
           S.res[5] = ge - gt;
@@ -206,18 +202,16 @@ __device__ __forceinline__ SelThreshold sel2_threshold(const uint32_t (&key)[J],
   return r;
 }
 
-// Membership of the candidates in the selection, given the threshold: every key above
-// T, and keys equal to T up to need_eq of them in page order.  `force` pages are added.
-// Writes the selected pages in ascending order to out[0, min(total, cap)), the count
-// to *out_count (thread 0), and returns this thread's membership mask.  *eq_cut
-// receives the page of the last key equal to T that is taken (or is left unchanged
-// when no tie is cut).
+// Membership of the slots in the selection, given the threshold: every candidate key
+// above T, the first need_eq candidate keys equal to T in slot order, and the `force`
+// slots.  Slot (w, j, lane) holds page page[j]; slot order must be ascending page
+// order.  *eq_cut receives the page of the last key equal to T that is taken when a tie
+// is cut (it is left unchanged otherwise).  Returns this thread's membership mask.
 template <int NT, int J>
-__device__ __forceinline__ uint64_t sel2_compact(const uint32_t (&key)[J], uint64_t cand, uint64_t force, const SelThreshold& th,
-                                 int32_t* __restrict__ out, int cap, int32_t* __restrict__ out_count, int* eq_cut,
-                                 Sel2Lds& S) {
+__device__ __forceinline__ uint64_t sel2_membership(const uint32_t (&key)[J], const int (&page)[J], uint64_t cand,
+                                                    uint64_t force, const SelThreshold& th, int* eq_cut, Sel2Lds& S) {
   constexpr int NW = NT / kWave;
-  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  const int lane = lane_id(), w = threadIdx.x / kWave;
   uint64_t gt = 0, eq = 0;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
@@ -227,48 +221,70 @@ __device__ __forceinline__ uint64_t sel2_compact(const uint32_t (&key)[J], uint6
     }
   }
   gt |= force;
-  const int gtc = wave_isum(__popcll(gt)), eqc = wave_isum(__popcll(eq));
+  if (th.mode != 2 || th.need_eq >= th.eq_total) return gt | eq;  // no tie is cut
+  // the first need_eq keys equal to T in slot order
+  const int eqc = wave_isum(__popcll(eq));
   __syncthreads();  // S.red may still be read by a previous step
-  if (lane == 0) {
-    S.red[0][w] = gtc;
-    S.red[1][w] = eqc;
-  }
+  if (lane == 0) S.red[1][w] = eqc;
   __syncthreads();
-  int eq_run = 0, sel_run = 0, total = 0;
-  {
-    int eb = 0, sb = 0;
+  int eq_run = 0;
 #pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const int gi = S.red[0][i], ei = S.red[1][i];
-      const int take = max(0, min(ei, th.need_eq - eb));
-      if (i == w) {
-        eq_run = eb;
-        sel_run = sb;
-      }
-      eb += ei;
-      sb += gi + take;
-    }
-    total = sb;
-  }
-  uint64_t in = 0;
+  for (int i = 0; i < NW; ++i) eq_run += i < w ? S.red[1][i] : 0;
+  uint64_t in = gt;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     const bool e = (eq >> j) & 1ull;
     const uint64_t em = __ballot(e);
     const int erank = eq_run + lanes_below(em);
-    const bool take_eq = e && erank < th.need_eq;
-    const bool sel = ((gt >> j) & 1ull) || take_eq;
-    const uint64_t sm = __ballot(sel);
-    if (sel) {
-      const int pos = sel_run + lanes_below(sm);
-      if (out && pos < cap) out[pos] = sel2_page<J>(j);
+    if (e && erank < th.need_eq) {
       in |= 1ull << j;
+      if (erank == th.need_eq - 1) *eq_cut = page[j];
     }
-    if (take_eq && erank == th.need_eq - 1 && th.need_eq < th.eq_total) *eq_cut = sel2_page<J>(j);
     eq_run += __popcll(em);
-    sel_run += __popcll(sm);
   }
-  if (t == 0 && out_count) *out_count = min(total, cap);
+  return in;
+}
+
+// The pages of the slots in `mask`, in slot order, to out[0, min(total, cap)) (global or
+// LDS); returns the total to every thread.  `wbase`, if not NULL, receives per thread
+// the number of masked slots of the waves before this one.
+template <int NT, int J>
+__device__ __forceinline__ int sel2_list(uint64_t mask, const int (&page)[J], int32_t* __restrict__ out, int cap,
+                                         Sel2Lds& S) {
+  constexpr int NW = NT / kWave;
+  const int lane = lane_id(), w = threadIdx.x / kWave;
+  const int c = wave_isum(__popcll(mask));
+  __syncthreads();  // S.red may still be read by a previous step
+  if (lane == 0) S.red[0][w] = c;
+  __syncthreads();
+  int run = 0, total = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const int ci = S.red[0][i];
+    run += i < w ? ci : 0;
+    total += ci;
+  }
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const bool in = (mask >> j) & 1ull;
+    const uint64_t bm = __ballot(in);
+    if (in) {
+      const int pos = run + lanes_below(bm);
+      if (pos < cap) out[pos] = page[j];
+    }
+    run += __popcll(bm);
+  }
+  return total;
+}
+
+// Membership and the list of the selection (ascending pages); the count to *out_count.
+template <int NT, int J>
+__device__ __forceinline__ uint64_t sel2_compact(const uint32_t (&key)[J], const int (&page)[J], uint64_t cand,
+                                                 uint64_t force, const SelThreshold& th, int32_t* __restrict__ out,
+                                                 int cap, int32_t* __restrict__ out_count, int* eq_cut, Sel2Lds& S) {
+  const uint64_t in = sel2_membership<NT, J>(key, page, cand, force, th, eq_cut, S);
+  const int total = sel2_list<NT, J>(in, page, out, cap, S);
+  if (threadIdx.x == 0 && out_count) *out_count = min(total, cap);
   return in;
 }
 
