@@ -134,7 +134,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--config", default="glm128k")
     ap.add_argument("--layers", type=int, default=None, help="fewer layers (quick runs only)")
-    ap.add_argument("--mode", default="exact", choices=["exact", "keep"])
+    ap.add_argument("--mode", default="exact", choices=["exact", "keep", "recompute"])
+    ap.add_argument("--theta", default=None, help="EMA alpha,beta,gamma (default: the workload's)")
+    ap.add_argument("--ablation", action="store_true",
+                    help="also time the ablation stages S1 (reuse the previous top-K, recompute on a miss), "
+                         "S2 (reuse + repair) and S3 (EMA + repair) with the fused PRR schedule")
     ap.add_argument("--chunk", type=int, default=None, help="pages per speculation chunk (default 8, 4 for 64-token pages)")
     ap.add_argument("--delta", type=float, default=1.0, help="|P| / |A| (speculation budget)")
     ap.add_argument("--schedules", default="fused_prr,fused_serial,two_stream,serial")
@@ -157,17 +161,20 @@ def main():
     cfg = W.CONFIGS[args.config]
     n_layers = args.layers or cfg.layers
     dev = torch.device("cuda:0")
-    mode = L.PRR_EXACT_SELECTED if args.mode == "exact" else L.PRR_KEEP_WASTED
+    mode = {"exact": L.PRR_EXACT_SELECTED, "keep": L.PRR_KEEP_WASTED, "recompute": L.PRR_RECOMPUTE_ON_MISS}[args.mode]
+    theta = tuple(float(x) for x in args.theta.split(",")) if args.theta else (cfg.alpha, cfg.beta, cfg.gamma)
     p_select = int(round(args.delta * cfg.k_select))
     pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
                       num_tokens=cfg.context, k_select=cfg.k_select, forced=cfg.forced_pages(),
                       forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
-                      alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma,
+                      alpha=theta[0], beta=theta[1], gamma=theta[2],
                       chunk_pages=args.chunk or min(8, 256 // cfg.page_size), mode=mode, p_select=p_select)
     schedules = [x for x in args.schedules.split(",") if x]
     sched_id = {"fused_prr": L.PRR_SCHED_FUSED_PRR, "fused_serial": L.PRR_SCHED_FUSED_SERIAL,
                 "two_stream": L.PRR_SCHED_TWO_STREAM, "serial": L.PRR_SCHED_SERIAL}
-    total_tokens = 2 + max(2, args.warmup) + 2 * len(schedules) * (args.steps + 2) + args.kernel_reps + 8
+    n_abl = 3 if args.ablation else 0
+    total_tokens = 2 + max(2, args.warmup) + 2 * (len(schedules) + n_abl) * (args.steps + 2) + \
+        n_abl * (1 + max(2, args.warmup)) + args.kernel_reps + 8
     t0 = time.time()
     layers = [None] * n_layers
 
@@ -230,6 +237,31 @@ def main():
     for name in schedules:  # warm each schedule, then two timed passes (the better one counts)
         run(2, sched_id[name])
         ms[name] = min(timed(args.steps, sched_id[name]), timed(args.steps, sched_id[name]))
+    ablation = None
+    if args.ablation:
+        # Section 6.3: S1 reuses the previous step's top-K (theta = (1, .5, 0)) and
+        # recomputes attention over A on any miss; S2 repairs instead; S3 is the EMA
+        # predictor with repair.  Every stage restarts from a fresh prefill.
+        ablation = {}
+        stages = {"S1": ((1.0, 0.5, 0.0), L.PRR_RECOMPUTE_ON_MISS), "S2": ((1.0, 0.5, 0.0), L.PRR_EXACT_SELECTED),
+                  "S3": ((cfg.alpha, cfg.beta, cfg.gamma), L.PRR_EXACT_SELECTED)}
+        saved = (stack.params.alpha, stack.params.beta, stack.params.gamma, stack.params.mode)
+        for name, (th, md) in stages.items():
+            stack.params.alpha, stack.params.beta, stack.params.gamma = th
+            stack.params.mode = md
+            for st in layers:
+                st.init_bits.zero_()
+            torch.cuda.synchronize()
+            run(1, L.PRR_SCHED_FUSED_PREFILL)
+            h = run(max(2, args.warmup), L.PRR_SCHED_FUSED_PRR, measure_hits=True)
+            t_ms = min(timed(args.steps, L.PRR_SCHED_FUSED_PRR), timed(args.steps, L.PRR_SCHED_FUSED_PRR))
+            ablation[name] = {"theta": list(th), "mode": {0: "repair", 2: "recompute on miss"}[md],
+                              "us_per_layer": round(1000.0 * t_ms / n_layers, 3),
+                              "hit_rate": round(float(np.mean(h)), 4)}
+        stack.params.alpha, stack.params.beta, stack.params.gamma, stack.params.mode = saved
+        for st in layers:
+            st.init_bits.zero_()
+        run(1, L.PRR_SCHED_FUSED_PREFILL)
     flags = [int(st.workspace[:1].cpu()[0]) for st in layers]
     if any(flags):
         print(json.dumps({"error": f"device error flags {flags}"}), flush=True)
@@ -291,7 +323,7 @@ def main():
         "config": {"workload": f"{cfg.name}: {n_layers} layers x ({cfg.num_q_heads} q / {cfg.num_kv_heads} kv heads, "
                                f"d {cfg.head_dim}), {cfg.dtype}, {cfg.context}-token context, page {cfg.page_size}, "
                                f"top-{cfg.k_select} pages, batch 1",
-                   "mode": args.mode, "chunk_pages": pc.chunk_pages, "p_select": p_select,
+                   "mode": args.mode, "chunk_pages": pc.chunk_pages, "p_select": p_select, "theta": list(theta),
                    "schedule": main_sched},
         "us_per_layer": {k: round(v, 3) for k, v in us.items()},
         "achieved_gbps": round(achieved, 1),
@@ -300,6 +332,7 @@ def main():
         "speedup_vs_serial": round(best_serial / us_prr, 3) if best_serial else None,
         "hit_rate": round(float(np.mean(hits)), 4) if hits else None,
         "kernel_us": {k: round(v, 2) for k, v in ktimes.items()},
+        "ablation": ablation,
         "roofline": roofline,
     }
     if args.copy_calibration_mib > 0:

@@ -68,6 +68,10 @@ typedef int32_t prr_status;
 
 #define PRR_EXACT_SELECTED 0 /* output = attention over exactly A */
 #define PRR_KEEP_WASTED 1    /* output = attention over P u A (wasted pages kept as context, Section 1) */
+#define PRR_RECOMPUTE_ON_MISS 2 /* fused schedules only: output = attention over exactly A, but when
+                                   any page of A was not predicted the speculation is discarded and
+                                   all of A is attended afresh (the ablation stage without repair,
+                                   Section 6.3) */
 
 /* Shape of one layer's paged KV cache.
  *   head_dim   128 (the only compiled value)

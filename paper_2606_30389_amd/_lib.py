@@ -26,6 +26,7 @@ PRR_META_MINMAX = 0
 PRR_META_MEAN = 1
 PRR_EXACT_SELECTED = 0
 PRR_KEEP_WASTED = 1
+PRR_RECOMPUTE_ON_MISS = 2
 PRR_MAX_PAGES = 16384
 PRR_MAX_CAP = 1024
 PRR_MAX_FORCED = 64

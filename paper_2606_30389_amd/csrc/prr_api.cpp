@@ -483,7 +483,8 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   if (sp->cap < 1 || sp->cap > PRR_MAX_CAP) return fail(PRR_ERR_INVALID_ARG, "cap %d outside [1, %d]", sp->cap, PRR_MAX_CAP);
   if (!chunk_ok(dims, sp->chunk_pages))
     return fail(PRR_ERR_INVALID_ARG, "chunk_pages %d outside [1, 256 / page_size]", sp->chunk_pages);
-  if (sp->mode != PRR_EXACT_SELECTED && sp->mode != PRR_KEEP_WASTED) return fail(PRR_ERR_INVALID_ARG, "mode %d", sp->mode);
+  if (sp->mode != PRR_EXACT_SELECTED && sp->mode != PRR_KEEP_WASTED && sp->mode != PRR_RECOMPUTE_ON_MISS)
+    return fail(PRR_ERR_INVALID_ARG, "mode %d", sp->mode);
   if (sp->epoch == 0) return fail(PRR_ERR_INVALID_ARG, "epoch 0 is reserved (a zeroed workspace carries it)");
   if (prr || prefill) {
     if (!(sp->alpha > 0.f && sp->alpha <= 1.f) || !(sp->beta > 0.f && sp->beta <= 1.f) ||

@@ -35,7 +35,9 @@ constexpr int kFW = kFT / kWave;
 constexpr int kFScorePages = 128;
 constexpr int kFSpin = 1 << 20;
 constexpr int kFPart = kHeadDim + 2;  // o[128], m, l of one query head
-constexpr uint32_t kSelfMiss = 0x80000000u;
+constexpr uint32_t kSelfMiss = 0x80000000u;  // missed-list count flags: attended by the select workgroup
+constexpr uint32_t kDropSpec = 0x40000000u;  //   the speculation is discarded (recompute on a miss)
+constexpr uint32_t kCountMask = 0x3fffffffu;
 constexpr int kFOPad = kHeadDim + 4;
 constexpr int kEqAll = 16383;  // eq_cut meaning "every key equal to T is taken"
 constexpr int kCandMax = 8 * kFT;  // candidates ranked by one workgroup (8 per thread)
@@ -243,14 +245,14 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
   uint64_t* ck_p = a.t_candk + rec_p * kFScorePages;
   uint64_t* cp_p = a.t_candp + rec_p * kFScorePages;
   int na = 0, nfa = 0, np = 0, nfp = 0;
+  // candidates of A first (the select workgroup waits for them) ...
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
     const int lp = 64 * half + lane;
     const int p = pbase + lp;
     const bool inr = p < n;
-    const float sv = S.sc[lp];
     const bool f = inr && ((S.fbits[lp >> 5] >> (lp & 31)) & 1u);
-    const uint32_t ka = score_key(sv);
+    const uint32_t ka = score_key(S.sc[lp]);
     const bool ca = inr && (f || ka >= lo_a);
     const uint64_t ma = __ballot(ca), mfa = __ballot(ca && f);
     if (ca) {
@@ -260,44 +262,50 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
     }
     na += __popcll(ma);
     nfa += __popcll(mfa);
-    if (ema) {
-      bool has = inr && ((bw[half] >> (p & 31)) & 1u);
-      float l = lv[half], v = tv[half];
-      if (inr) {
-        if (has) {
-          v = a.beta * (sv - l) + (1.0f - a.beta) * v;  // Eq. (3): the trend reads the previous level
-          l = a.alpha * sv + (1.0f - a.alpha) * l;
-        } else {
-          l = sv;
-          v = 0.0f;
-          has = true;
-        }
-        a.level[(size_t)h * a.max_pages + p] = l;
-        a.trend[(size_t)h * a.max_pages + p] = v;
+  }
+  if (lane == 0) put_tag(&a.t_cnt[rec_a], (uint32_t)na | ((uint32_t)nfa << 16), a.epoch);
+  if (!ema) return;
+  // ... then the EMA update of Eq. (3) and the candidates of the next prediction
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    const int lp = 64 * half + lane;
+    const int p = pbase + lp;
+    const bool inr = p < n;
+    const float sv = S.sc[lp];
+    const bool f = inr && ((S.fbits[lp >> 5] >> (lp & 31)) & 1u);
+    bool has = inr && ((bw[half] >> (p & 31)) & 1u);
+    float l = lv[half], v = tv[half];
+    if (inr) {
+      if (has) {
+        v = a.beta * (sv - l) + (1.0f - a.beta) * v;  // Eq. (3): the trend reads the previous level
+        l = a.alpha * sv + (1.0f - a.alpha) * l;
+      } else {
+        l = sv;
+        v = 0.0f;
+        has = true;
       }
-      const uint64_t hm = __ballot(has), vm = __ballot(inr);
-      if (lane == 0 || lane == 32) {
-        const uint32_t hbits = (uint32_t)(lane == 0 ? hm : (hm >> 32));
-        const uint32_t vbits = (uint32_t)(lane == 0 ? vm : (vm >> 32));
-        if (vbits) a.init_bits[(size_t)h * nwmax + (p >> 5)] = (bw[half] & ~vbits) | hbits;
-      }
-      const uint32_t kp = score_key(l + a.gamma * v);  // Eq. (2)
-      if (inr) put_tag(&a.t_pkey[(size_t)h * a.max_pages + p], kp, a.epoch);
-      const bool cpred = inr && (f || kp >= lo_p);
-      const uint64_t mp = __ballot(cpred), mfp = __ballot(cpred && f);
-      if (cpred) {
-        const int pos = np + lanes_below(mp);
-        put_tag(&ck_p[pos], kp, a.epoch);
-        put_tag(&cp_p[pos], (uint32_t)p | (f ? 0x80000000u : 0u), a.epoch);
-      }
-      np += __popcll(mp);
-      nfp += __popcll(mfp);
+      a.level[(size_t)h * a.max_pages + p] = l;
+      a.trend[(size_t)h * a.max_pages + p] = v;
     }
+    const uint64_t hm = __ballot(has), vm = __ballot(inr);
+    if (lane == 0 || lane == 32) {
+      const uint32_t hbits = (uint32_t)(lane == 0 ? hm : (hm >> 32));
+      const uint32_t vbits = (uint32_t)(lane == 0 ? vm : (vm >> 32));
+      if (vbits) a.init_bits[(size_t)h * nwmax + (p >> 5)] = (bw[half] & ~vbits) | hbits;
+    }
+    const uint32_t kp = score_key(l + a.gamma * v);  // Eq. (2)
+    if (inr) put_tag(&a.t_pkey[(size_t)h * a.max_pages + p], kp, a.epoch);
+    const bool cpred = inr && (f || kp >= lo_p);
+    const uint64_t mp = __ballot(cpred), mfp = __ballot(cpred && f);
+    if (cpred) {
+      const int pos = np + lanes_below(mp);
+      put_tag(&ck_p[pos], kp, a.epoch);
+      put_tag(&cp_p[pos], (uint32_t)p | (f ? 0x80000000u : 0u), a.epoch);
+    }
+    np += __popcll(mp);
+    nfp += __popcll(mfp);
   }
-  if (lane == 0) {
-    put_tag(&a.t_cnt[rec_a], (uint32_t)na | ((uint32_t)nfa << 16), a.epoch);
-    if (ema) put_tag(&a.t_cnt[rec_p], (uint32_t)np | ((uint32_t)nfp << 16), a.epoch);
-  }
+  if (lane == 0) put_tag(&a.t_cnt[rec_p], (uint32_t)np | ((uint32_t)nfp << 16), a.epoch);
 }
 
 // ------------------------------------------------------------------------ shared select pieces
@@ -683,16 +691,24 @@ __device__ __forceinline__ void update_window(const FusedLaunch& a, uint32_t* wi
   }
 }
 
-// |q-bar_h|_1 (every thread), with q-bar as the score workgroups compute it.
+// |q-bar_h|_1 (every thread), with q-bar as the score workgroups compute it: channel t
+// of the G query heads loaded by thread t < 128, summed in head order.
 template <bool BF16>
-__device__ __forceinline__ float qbar_l1(const FusedLaunch& a, int h, float* qb) {
+__device__ __forceinline__ void qbar_load(const FusedLaunch& a, int h, float (&qv)[16]) {
   const int t = threadIdx.x;
   const int G = a.group;
   const uint16_t* q = static_cast<const uint16_t*>(a.q) + (size_t)h * G * kHeadDim;
+#pragma unroll
+  for (int g = 0; g < 16; ++g) qv[g] = (t < kHeadDim && g < G) ? h2f<BF16>(q[(size_t)g * kHeadDim + t]) : 0.0f;
+}
+__device__ __forceinline__ float qbar_finish(const FusedLaunch& a, const float (&qv)[16], float* qb) {
+  const int t = threadIdx.x;
   if (t < kHeadDim) {
     float s = 0.0f;
-    for (int g = 0; g < G; ++g) s += h2f<BF16>(q[(size_t)g * kHeadDim + t]);
-    qb[t] = fabsf(s / (float)G);
+#pragma unroll
+    for (int g = 0; g < 16; ++g)
+      if (g < a.group) s += qv[g];
+    qb[t] = fabsf(s / (float)a.group);
   }
   __syncthreads();
   return wave_sum(qb[lane_id()] + qb[lane_id() + 64]);
@@ -727,21 +743,25 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
     }
   }
 
-  // the list to attend after selection, in page order: A \ P (PRR) or A (serial)
-  const uint64_t inM = prr ? (inA & ~inP) : inA;
+  // the list to attend after selection, in page order: A \ P (PRR) or A (serial, or a
+  // PRR step whose speculation is discarded because a page was missed)
+  const int nMiss = prr ? block_sum<kFT>(__popcll(inA & ~inP), L.sel.red[2]) : 0;
+  const bool drop = prr && a.mode == PRR_RECOMPUTE_ON_MISS && nMiss > 0;
+  const uint64_t inM = (prr && !drop) ? (inA & ~inP) : inA;
+  const uint32_t mflags = drop ? kDropSpec : 0u;
   const int nM = min(sel2_list<kFT, J>(inM, page, L.mlist, a.cap, L.sel), a.cap);
   __syncthreads();
   if (nM == 0) {
-    if (t == 0) put_tag(&a.t_mcnt[h], 0u, a.epoch);
+    if (t == 0) put_tag(&a.t_mcnt[h], mflags, a.epoch);
   } else if (nM > kFW) {
     uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
     for (int i = t; i < nM; i += kFT) put_tag(&ml[i], (uint32_t)L.mlist[i], a.epoch);
-    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM, a.epoch);
+    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM | mflags, a.epoch);
   }
   // the selected list (an output) and the counts
   int32_t* sel = a.selected + (size_t)h * a.cap;
   int nA;
-  if (prr) {
+  if (prr && !drop) {
     nA = min(sel2_list<kFT, J>(inA, page, sel, a.cap, L.sel), a.cap);
   } else {
     nA = nM;
@@ -750,12 +770,12 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
   const int nPA = prr ? block_sum<kFT>(__popcll(inP & inA), L.sel.red[2]) : 0;
   if (t == 0) {
     a.selected_count[h] = nA;
-    if (a.missed_count) a.missed_count[h] = nM;
+    if (a.missed_count) a.missed_count[h] = prr ? nMiss : nM;
     if (a.wasted_count) a.wasted_count[h] = prr ? L.npv - nPA : 0;
   }
   if (nM > 0 && nM <= kFW) {
     // few enough to attend here: one page per wave, published as the first miss slot
-    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM | kSelfMiss, a.epoch);
+    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM | kSelfMiss | mflags, a.epoch);
     int pg[1];
     pg[0] = __builtin_amdgcn_readfirstlane(w < nM ? L.mlist[w] : -1);
     __syncthreads();  // the list is read before the attention reuses the LDS
@@ -790,18 +810,26 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U
       atomicOr(&L.forceb[a.forced[i] >> 5], 1u << (a.forced[i] & 31));
     }
   }
-  if (a.schedule == 1) {
-    const int pc = min(max(a.pred_cur_count[h], 0), a.cap);
-    for (int i = t; i < pc; i += kFT) {
-      const int p = a.pred_cur[(size_t)h * a.cap + i];
-      if (p >= 0 && p < n) {
-        const uint32_t old = atomicOr(&L.bitP[p >> 5], 1u << (p & 31));
-        if (!((old >> (p & 31)) & 1u)) atomicAdd(&L.npv, 1);
-      }
+  // P^t and q are loaded while the candidates are polled
+  int pe[PRR_MAX_CAP_DEV / kFT];
+  const int pc = a.schedule == 1 ? min(max(a.pred_cur_count[h], 0), a.cap) : 0;
+#pragma unroll
+  for (int r = 0; r < PRR_MAX_CAP_DEV / kFT; ++r) {
+    const int i = t + r * kFT;
+    pe[r] = i < pc ? a.pred_cur[(size_t)h * a.cap + i] : -1;
+  }
+  float qv[16];
+  qbar_load<BF16>(a, h, qv);
+  const FCand c = cand_load(a, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+#pragma unroll
+  for (int r = 0; r < PRR_MAX_CAP_DEV / kFT; ++r) {
+    const int p = pe[r];
+    if (p >= 0 && p < n) {
+      const uint32_t old = atomicOr(&L.bitP[p >> 5], 1u << (p & 31));
+      if (!((old >> (p & 31)) & 1u)) atomicAdd(&L.npv, 1);
     }
   }
-  const float qn = qbar_l1<BF16>(a, h, L.qb);
-  const FCand c = cand_load(a, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  const float qn = qbar_finish(a, qv, L.qb);
   if (a.kextra_a <= c.total - c.nforced && c.total <= kCandMax) {
     // one instantiation per path keeps the kernel's code (and its instruction-cache
     // footprint) small: 8 candidate slots per thread, 16 page slots in the fallback
@@ -847,8 +875,10 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, int h, FLds& 
       atomicOr(&L.forceb[a.forced[i] >> 5], 1u << (a.forced[i] & 31));
     }
   }
-  const float qn = qbar_l1<BF16>(a, h, L.qb);
+  float qv[16];
+  qbar_load<BF16>(a, h, qv);
   const FCand c = cand_load(a, h, 1, L.off, L.tot, L.ck, L.cpg);
+  const float qn = qbar_finish(a, qv, L.qb);
   if (a.kextra_p <= c.total - c.nforced && c.total <= kCandMax) {
     uint32_t key[8];
     int page[8];
@@ -891,7 +921,7 @@ __device__ __forceinline__ void role_spec(const FusedLaunch& a, int h, int c, FL
   }
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
-  if (a.mode == PRR_EXACT_SELECTED && keep) {
+  if (a.mode != PRR_KEEP_WASTED && keep) {
     // membership of this wave's pages in A, from their scores and the published
     // threshold (all loads issued together, then waited for)
     const uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
@@ -934,7 +964,7 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, int h, int u, FL
     for (int k = 0; k < NPW; ++k) ve[k] = get_tag(&ml[min(start + w + kFW * k, a.cap - 1)]);
     if (tag_is(vm, a.epoch)) {
       mv = (uint32_t)vm;
-      const int nm = (mv & kSelfMiss) ? 0 : (int)(mv & ~kSelfMiss);
+      const int nm = (mv & kSelfMiss) ? 0 : (int)(mv & kCountMask);
       bool ok = true;
 #pragma unroll
       for (int k = 0; k < NPW; ++k) ok = ok && (start + w + kFW * k >= nm || tag_is(ve[k], a.epoch));
@@ -944,7 +974,7 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, int h, int u, FL
     if (it == kFSpin - 1 && lane_id() == 0) atomicOr(a.flags, kFlagSpinTimeout);
   }
   if (mv & kSelfMiss) return;
-  const int nM = (int)(mv & ~kSelfMiss);
+  const int nM = (int)(mv & kCountMask);
   if (start >= nM) return;
   const int cnt = min(a.chunk, nM - start);
   int pg[NPW];
@@ -976,8 +1006,9 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, 
   int nspec = 0;
   if (a.schedule == 1) nspec = (min(max(a.pred_cur_count[h], 0), a.cap) + C - 1) / C;
   const uint32_t mv = wait_tag(a.t_mcnt + h, a.epoch, a.flags);
-  const int nM = (int)(mv & ~kSelfMiss);
+  const int nM = (int)(mv & kCountMask);
   const int nmiss = (mv & kSelfMiss) ? 1 : (nM + C - 1) / C;
+  if (mv & kDropSpec) nspec = 0;
   const int total = nspec + nmiss;
   // state i lives in slot i (speculation chunks) or n_spec + (i - nspec) (missed chunks)
   const uint64_t* part = a.t_part + ((size_t)h * a.nparts * G + qn) * kFPart;

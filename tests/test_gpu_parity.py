@@ -571,24 +571,32 @@ FUSED_CASES = [
     ("llama64k", 300, 1, None, 1, None, 2, 3),
     ("infllm128k", 200, 0, None, 1, None, 1, 3),
     ("glm128k", None, 0, None, 1, None, 1, 2),  # full size: 8192 pages, top-256
+    # ablation stages: theta = (1, 0.5, 0) predicts the previous step's top-K; with a
+    # recompute on any miss (S1) and with repair (S2)
+    ("glm32k", 512, 2, None, 1, None, 1, 3, (1.0, 0.5, 0.0)),
+    ("glm32k", 512, 0, None, 1, None, 1, 3, (1.0, 0.5, 0.0)),
+    ("tiny", None, 2, None, 1, 6, 1, 4, (1.0, 0.5, 0.0)),
 ]
 
 
-@pytest.mark.parametrize("case", FUSED_CASES, ids=lambda c: f"{c[0]}-p{c[1]}-m{c[2]}-c{c[3]}-d{c[4]}-k{c[5]}")
+@pytest.mark.parametrize("case", FUSED_CASES,
+                         ids=lambda c: f"{c[0]}-p{c[1]}-m{c[2]}-c{c[3]}-d{c[4]}-k{c[5]}" + ("-reuse" if len(c) > 8 else ""))
 def test_fused_decode_step(torch, case):
     """The fused schedules of prr_decode_step (one launch per layer): step-0 select + EMA
     initialisation, then per step the PRR launch and the serial launch, every layer
     against the oracle (A, P, output, missed and wasted counts)."""
     from paper_2606_30389_amd import _lib as L
     from paper_2606_30389_amd import runtime as R
-    name, npages, mode, chunk, delta, kover, n_layers, steps = case
+    name, npages, mode, chunk, delta, kover, n_layers, steps = case[:8]
     cfg = W.CONFIGS[name]
+    theta = case[8] if len(case) > 8 else (cfg.alpha, cfg.beta, cfg.gamma)
     layers, inputs, metas, qs, queries = [], [], [], [], []
     for layer in range(n_layers):
         pc = S.path_config(cfg, num_pages=npages, mode=mode, chunk_pages=chunk)
         if kover is not None:
             pc.k_select = kover
         pc.p_select = delta * pc.k_select
+        pc.alpha, pc.beta, pc.gamma = theta
         S.log(f"fused {name} layer {layer} pages={pc.num_pages} mode={mode} chunk={pc.chunk_pages} "
               f"K={pc.k_select} |P|={pc.p_select}")
         st, li = S.make_layer(cfg, pc, layer=layer)
@@ -623,11 +631,11 @@ def test_fused_decode_step(torch, case):
         for layer, st in enumerate(layers):
             q64 = W.bits_to_f64(qs[layer][t], cfg.dtype)
             level, trend = state[layer]
-            P = S.check_selection(preds[layer], O.ema_predict(level, trend, cfg.gamma), pc.p_select, forced,
+            P = S.check_selection(preds[layer], O.ema_predict(level, trend, theta[2]), pc.p_select, forced,
                                   pc.forced_in_budget, what="P")
             s64 = S.oracle_scores(q64, metas[layer], pc)
             A = S.check_selection(S.lists(st), s64, pc.k_select, forced, pc.forced_in_budget)
-            target = A if mode == 0 else [np.union1d(x, y) for x, y in zip(A, P)]
+            target = A if mode != 1 else [np.union1d(x, y) for x, y in zip(A, P)]
             ref = O.attend(q64, inputs[layer].k64(), inputs[layer].v64(), target, pc.page_size, pc.num_tokens)
             S.check_attention(S.to_np(st.out_o32), S.to_np(st.out_m), S.to_np(st.out_l), ref, S.to_np(st.out_o),
                               dtype=pc.dtype, what=f"PRR layer {layer} step {t}")
@@ -635,7 +643,7 @@ def test_fused_decode_step(torch, case):
             for h in range(pc.num_kv_heads):
                 mm, ww = O.missed_and_wasted(A[h], P[h])
                 assert (mc[h], wc[h]) == (len(mm), len(ww)), f"layer {layer} head {h}: missed/wasted counts"
-            state[layer] = O.ema_update(level, trend, s64, cfg.alpha, cfg.beta)
+            state[layer] = O.ema_update(level, trend, s64, theta[0], theta[1])
         S.log(f"fused serial step {t}")
         stack.step(L.PRR_SCHED_FUSED_SERIAL, s)
         torch.cuda.synchronize()
