@@ -127,6 +127,115 @@ def cpu_baseline(cfg, budget_s):
             "sample": f"{len(times)} decode steps of layer 0 of {cfg.name} (float64 NumPy, 1 thread), median"}
 
 
+def kernel_sweep(args):
+    """Attention over a given selected set (the serial repair call: attend every page of A,
+    merge) on the kernel-comparison shape of Section 6.4: 32 query / 8 KV heads, head_dim
+    128, a 131072-token fp16 cache, pages of 16 and 64 tokens, budgets of 1K to 8K tokens
+    drawn uniformly per KV head.  Reports microseconds per call and GB/s of selected K/V."""
+    import torch
+    from paper_2606_30389_amd import _lib as L
+    from paper_2606_30389_amd import runtime as R
+    dev = torch.device("cuda:0")
+    hq, hkv, d, ctx = 32, 8, 128, 131072
+    gen = torch.Generator(device="cpu").manual_seed(2606)
+    k = torch.randn(hkv * ctx * d, generator=gen, dtype=torch.float32).to(torch.float16).to(dev)
+    v = torch.randn(hkv * ctx * d, generator=gen, dtype=torch.float32).to(torch.float16).to(dev)
+    q = torch.randn(hq * d, generator=gen, dtype=torch.float32).to(torch.float16).to(dev)
+    s = torch.cuda.Stream(device=dev)
+    rows = []
+    for ps in (16, 64):
+        npg = ctx // ps
+        for budget in (1024, 2048, 4096, 6144, 8192):
+            kk = budget // ps
+            pc = R.PathConfig(num_q_heads=hq, num_kv_heads=hkv, page_size=ps, num_tokens=ctx, k_select=kk,
+                              forced=[], forced_in_budget=True, dtype="f16", meta_kind="minmax",
+                              chunk_pages=min(8, 256 // ps))
+            st = R.LayerState(pc, dev, k=k.view(hkv, npg, ps, d), v=v.view(hkv, npg, ps, d))
+            sel = np.stack([np.sort(np.random.default_rng(7 + h).choice(npg, kk, replace=False)) for h in range(hkv)])
+            st.sel[:, :kk].copy_(torch.from_numpy(sel.astype(np.int32)))
+            st.sel_count.fill_(kk)
+            for _ in range(3):
+                st.repair(q, stream=s, serial=True)
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            n = 50
+            a.record(s)
+            for _ in range(n):
+                st.repair(q, stream=s, serial=True)
+            b.record(s)
+            torch.cuda.synchronize()
+            us = 1000.0 * a.elapsed_time(b) / n
+            kv_bytes = hkv * budget * d * 2 * 2
+            rows.append({"page": ps, "budget_tokens": budget, "us": round(us, 2),
+                         "gbps": round(kv_bytes / (us * 1e-6) / 1e9, 1)})
+            print(f"[kernel-sweep] {rows[-1]}", file=sys.stderr, flush=True)
+            del st
+    print(json.dumps({"sweep": "sparse attention over a selected set (Section 6.4 shape)", "table": rows}), flush=True)
+
+
+def delta_sweep(args, cfg):
+    """Section 4.4's offline profiling: for each context length (a prefix of layer 0's
+    cache) and budget delta, the latency of the selection kernel, of the speculation
+    kernel over delta*|A| predicted pages, and of the fused PRR step with that budget."""
+    import torch
+    from paper_2606_30389_amd import _lib as L
+    from paper_2606_30389_amd import runtime as R
+    dev = torch.device("cuda:0")
+    li = W.layer_inputs(cfg, 0)
+    k = R.bits_tensor(li.k_bits, {"bf16": torch.bfloat16, "f16": torch.float16}[cfg.dtype], dev)
+    v = R.bits_tensor(li.v_bits, k.dtype, dev)
+    _, qb = W.query_trajectory(cfg, 0, steps=64)
+    rows = []
+    s = torch.cuda.Stream(device=dev)
+    reps = 20
+
+    def timed(fn, n):
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(n):
+            fn()
+        b.record(s)
+        torch.cuda.synchronize()
+        return 1000.0 * a.elapsed_time(b) / n
+
+    contexts = [c for c in (4096, 8192, 16384, 32768, 65536, 131072) if c <= cfg.context]
+    for ctx in contexts:
+        for delta in (1.0, 1.25, 1.5, 2.0):
+            npg = ctx // cfg.page_size
+            p_sel = int(round(delta * cfg.k_select))
+            pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
+                              num_tokens=ctx, k_select=cfg.k_select, forced=cfg.forced_pages(npg),
+                              forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
+                              alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma,
+                              chunk_pages=min(8, 256 // cfg.page_size), p_select=p_sel)
+            pc.max_pages = cfg.num_pages
+            st = R.LayerState(pc, dev, k=k, v=v)
+            st.build_meta()
+            q = R.bits_tensor(qb[0], pc.torch_dtype, dev)
+            stack = R.DecodeStack([st], [q], dev)
+            stack.step(L.PRR_SCHED_FUSED_PREFILL, s)
+            for t in range(1, 5):
+                q.copy_(R.bits_tensor(qb[t], pc.torch_dtype, dev))
+                stack.step(L.PRR_SCHED_FUSED_PRR, s)
+            torch.cuda.synchronize()
+            sel_us = timed(lambda: st.select(q, stream=s), reps)
+            spec_us = timed(lambda: st.speculate(q, stream=s), reps)
+            fused_us = timed(lambda: stack.step(L.PRR_SCHED_FUSED_PRR, s), reps)
+            rows.append({"context": ctx, "delta": delta, "select_us": round(sel_us, 2), "spec_us": round(spec_us, 2),
+                         "fused_prr_us": round(fused_us, 2)})
+            print(f"[sweep] {rows[-1]}", file=sys.stderr, flush=True)
+            del stack, st
+    pick = {c: R.pick_delta(rows, c) for c in contexts}
+    out = {"sweep": "speculation budget (Section 4.4)", "workload": f"{cfg.name} layer 0, context prefixes",
+           "table": rows, "picked_delta": pick}
+    if args.write_lut:
+        os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+        with open(os.path.join(ROOT, "gpurun_out", "delta_lut.json"), "w") as f:
+            json.dump({"workload": out["workload"], "table": rows}, f, indent=1)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -136,6 +245,16 @@ def main():
     ap.add_argument("--layers", type=int, default=None, help="fewer layers (quick runs only)")
     ap.add_argument("--mode", default="exact", choices=["exact", "keep", "recompute"])
     ap.add_argument("--theta", default=None, help="EMA alpha,beta,gamma (default: the workload's)")
+    ap.add_argument("--delta-sweep", action="store_true",
+                    help="only the offline speculation-budget sweep (Section 4.4): selection and speculation "
+                         "latency per context length and delta, and the fused PRR step; prints the table")
+    ap.add_argument("--write-lut", action="store_true", help="with --delta-sweep: store the table in the package")
+    ap.add_argument("--kernel-sweep", action="store_true",
+                    help="only the sparse-attention kernel sweep (Table 3 shape: 32 q / 8 kv heads, d 128, 128K "
+                         "context, page 16 and 64, budget 1K-8K tokens): microseconds and GB/s")
+    ap.add_argument("--calibrate", type=int, default=0, metavar="ROWS",
+                    help="calibrate theta (Section 4.2) on ROWS prefill score rows of the first 4 layers, then "
+                         "time the fused PRR step with it")
     ap.add_argument("--ablation", action="store_true",
                     help="also time the ablation stages S1 (reuse the previous top-K, recompute on a miss), "
                          "S2 (reuse + repair) and S3 (EMA + repair) with the fused PRR schedule")
@@ -159,6 +278,12 @@ def main():
     from paper_2606_30389_amd import runtime as R
 
     cfg = W.CONFIGS[args.config]
+    if args.delta_sweep:
+        delta_sweep(args, cfg)
+        return
+    if args.kernel_sweep:
+        kernel_sweep(args)
+        return
     n_layers = args.layers or cfg.layers
     dev = torch.device("cuda:0")
     mode = {"exact": L.PRR_EXACT_SELECTED, "keep": L.PRR_KEEP_WASTED, "recompute": L.PRR_RECOMPUTE_ON_MISS}[args.mode]
@@ -172,7 +297,7 @@ def main():
     schedules = [x for x in args.schedules.split(",") if x]
     sched_id = {"fused_prr": L.PRR_SCHED_FUSED_PRR, "fused_serial": L.PRR_SCHED_FUSED_SERIAL,
                 "two_stream": L.PRR_SCHED_TWO_STREAM, "serial": L.PRR_SCHED_SERIAL}
-    n_abl = 3 if args.ablation else 0
+    n_abl = (3 if args.ablation else 0) + (2 if args.calibrate > 1 else 0)
     total_tokens = 2 + max(2, args.warmup) + 2 * (len(schedules) + n_abl) * (args.steps + 2) + \
         n_abl * (1 + max(2, args.warmup)) + args.kernel_reps + 8
     t0 = time.time()
@@ -262,6 +387,44 @@ def main():
         for st in layers:
             st.init_bits.zero_()
         run(1, L.PRR_SCHED_FUSED_PREFILL)
+    calibration = None
+    if args.calibrate > 1:
+        # prefill trajectories: scores of the last ROWS prefill queries (the block of the
+        # current position forms as the prompt grows), scored by the select kernel
+        rows, n_cal = args.calibrate, min(4, n_layers)
+        nb = cfg.num_pages
+        traj = np.zeros((n_cal, cfg.num_kv_heads, rows, nb), dtype=np.float32)
+        for l in range(n_cal):
+            qb = R.bits_tensor(W.prefill_trajectory(cfg, l, rows), pc.torch_dtype, dev)
+            st = layers[l]
+            for r in range(rows):
+                st.select(qb[r], stream=s)
+                torch.cuda.synchronize()
+                pos = cfg.context - (rows - 1 - r)  # tokens up to and including this position
+                formed = min(nb, pos // cfg.page_size)
+                traj[l, :, r, :formed] = st.scores[:, :formed].float().cpu().numpy()
+        t_cal = time.perf_counter()
+        grid = np.asarray(R.THETA_GRID, dtype=np.float32)
+        best, obj = L.prr_calibrate(traj.reshape(-1, rows, nb), cfg.k_select, grid, p_select=p_select)
+        host_ms = 1000.0 * (time.perf_counter() - t_cal)
+        default_theta = (stack.params.alpha, stack.params.beta, stack.params.gamma)
+        calibration = {"rows": rows, "layers": n_cal, "theta": [round(x, 3) for x in best],
+                       "objective": round(float(obj.max()), 5), "host_ms": round(host_ms, 1),
+                       "host_threads": os.cpu_count()}
+        for name, th in (("default", default_theta), ("calibrated", best)):
+            stack.params.alpha, stack.params.beta, stack.params.gamma = th
+            for st in layers:
+                st.init_bits.zero_()
+            torch.cuda.synchronize()
+            run(1, L.PRR_SCHED_FUSED_PREFILL)
+            h = run(max(4, args.warmup), L.PRR_SCHED_FUSED_PRR, measure_hits=True)
+            calibration[f"hit_rate_{name}"] = round(float(np.mean(h)), 4)
+            calibration[f"us_per_layer_{name}"] = round(
+                1000.0 * timed(args.steps, L.PRR_SCHED_FUSED_PRR) / n_layers, 3)
+        stack.params.alpha, stack.params.beta, stack.params.gamma = default_theta
+        for st in layers:
+            st.init_bits.zero_()
+        run(1, L.PRR_SCHED_FUSED_PREFILL)
     flags = [int(st.workspace[:1].cpu()[0]) for st in layers]
     if any(flags):
         print(json.dumps({"error": f"device error flags {flags}"}), flush=True)
@@ -333,6 +496,7 @@ def main():
         "hit_rate": round(float(np.mean(hits)), 4) if hits else None,
         "kernel_us": {k: round(v, 2) for k, v in ktimes.items()},
         "ablation": ablation,
+        "calibration": calibration,
         "roofline": roofline,
     }
     if args.copy_calibration_mib > 0:

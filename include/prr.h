@@ -291,6 +291,27 @@ prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* params, 
                            int32_t n_layers, int32_t parity, int32_t schedule, hipStream_t stream,
                            hipStream_t spec_stream, hipEvent_t* events);
 
+/* Online calibration of the EMA predictor (Section 4.2): for each candidate theta =
+ * (alpha, beta, gamma) of `grid`, the score-weighted hit rate of Eq. (4) -- the EMA of
+ * Eqs. (2)-(3) simulated over each trajectory, P_phi = top-p_select of the prediction,
+ * A_phi = top-k_select of row phi (ties: lower block index; keys rounded to float32 as on
+ * the device), averaged over rows 1..n_rows-1 and then over the trajectories -- and the
+ * argmax of Eq. (5) (the first grid point on ties).  Host code, run on the CPU while the
+ * device finishes the prefill; no device memory is touched.
+ *   scores         host [n_traj][n_rows][n_blocks] float32 prefill score trajectories
+ *                  (a block not formed yet at a row carries a score below every formed
+ *                  block's, e.g. 0 when scores are positive; the EMA of a -inf score is NaN)
+ *   k_select       |A_phi|; p_select: |P_phi| (0 = k_select)
+ *   grid           host [n_grid][3] float32, alpha, beta in (0, 1], gamma in [0, 1]
+ *   n_threads      host threads (0 = all hardware threads)
+ *   best_theta     host [3] out: the argmax
+ *   objective_out  host [n_grid] out (may be NULL): Eq. (4) per grid point
+ * Errors: PRR_ERR_INVALID_ARG for NULL pointers, sizes < 1 (n_rows < 2), a grid point out
+ * of range. */
+prr_status prr_calibrate(const float* scores, int32_t n_traj, int32_t n_rows, int32_t n_blocks, int32_t k_select,
+                         int32_t p_select, const float* grid, int32_t n_grid, int32_t n_threads, float* best_theta,
+                         double* objective_out);
+
 /* Merge n_states partial states per row (Eqs. (6)-(8) for arbitrary states).
  *   o  device [n_states][rows][d] float32, m, l device [n_states][rows] float32
  *   out_o device [rows][d], out_m, out_l device [rows]; d <= 1024; states with l = 0 are empty. */

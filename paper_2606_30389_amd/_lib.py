@@ -42,7 +42,7 @@ PRR_SCHED_FUSED_PREFILL = 5
 EXPORTED = (
     "prr_status_string", "prr_last_error", "prr_workspace_size", "prr_workspace_init",
     "prr_spec_state_floats", "prr_build_page_meta", "prr_score_topk", "prr_predict",
-    "prr_spec_attn", "prr_repair", "prr_merge_states", "prr_decode_step",
+    "prr_spec_attn", "prr_repair", "prr_merge_states", "prr_decode_step", "prr_calibrate",
 )
 
 
@@ -103,6 +103,7 @@ _SIGS = {
     "prr_merge_states": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _P]),
     "prr_decode_step": (_I, [_DIMS, ctypes.POINTER(prr_step_params), ctypes.POINTER(prr_layer_io), _I, _I, _I, _P,
                              _P, ctypes.POINTER(ctypes.c_void_p)]),
+    "prr_calibrate": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _P, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -211,6 +212,21 @@ def prr_repair(dims, q, k_cache, v_cache, page_table, num_tokens, num_pages, sel
 def prr_merge_states(n_states, rows, d, o, m, l, out_o, out_m, out_l, stream=None):
     _check(_lib.prr_merge_states(n_states, rows, d, _ptr(o), _ptr(m), _ptr(l), _ptr(out_o), _ptr(out_m), _ptr(out_l),
                                  _stream(stream)))
+
+
+def prr_calibrate(scores, k_select, grid, p_select=0, n_threads=0):
+    """scores: host float32 array [n_traj][n_rows][n_blocks]; grid: host float32 [n_grid][3].
+    Returns (best theta as a tuple, objective per grid point as a float64 array)."""
+    import numpy as np
+    sc = np.ascontiguousarray(scores, dtype=np.float32)
+    if sc.ndim == 2:
+        sc = sc[None]
+    g = np.ascontiguousarray(grid, dtype=np.float32).reshape(-1, 3)
+    best = np.zeros(3, dtype=np.float32)
+    obj = np.zeros(len(g), dtype=np.float64)
+    _check(_lib.prr_calibrate(sc.ctypes.data, sc.shape[0], sc.shape[1], sc.shape[2], k_select, p_select,
+                              g.ctypes.data, len(g), n_threads, best.ctypes.data, obj.ctypes.data))
+    return tuple(float(x) for x in best), obj
 
 
 def prr_decode_step(dims, params, layers, parity, schedule, stream=None, spec_stream=None, events=None):

@@ -7,7 +7,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = ["csrc/prr_kernels.hip", "csrc/prr_fused.hip", "csrc/prr_api.cpp"]
+SOURCES = ["csrc/prr_kernels.hip", "csrc/prr_fused.hip", "csrc/prr_api.cpp", "csrc/prr_calibrate.cpp"]
 OUT = os.path.join(HERE, "libprr.so")
 
 HIPCC_FLAGS = [

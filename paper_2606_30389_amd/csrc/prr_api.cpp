@@ -420,6 +420,24 @@ prr_status prr_repair(const prr_dims* dims, const void* q, const void* k_cache, 
   return hip_status(prr::launch_repair(a, stream), "repair launch");
 }
 
+prr_status prr_calibrate(const float* scores, int32_t n_traj, int32_t n_rows, int32_t n_blocks, int32_t k_select,
+                         int32_t p_select, const float* grid, int32_t n_grid, int32_t n_threads, float* best_theta,
+                         double* objective_out) {
+  if (!scores || !grid || !best_theta) return fail(PRR_ERR_INVALID_ARG, "scores, grid or best_theta is NULL");
+  if (n_traj < 1 || n_rows < 2 || n_blocks < 1 || n_grid < 1)
+    return fail(PRR_ERR_INVALID_ARG, "n_traj %d, n_rows %d (>= 2), n_blocks %d, n_grid %d", n_traj, n_rows, n_blocks,
+                n_grid);
+  if (k_select < 0 || p_select < 0) return fail(PRR_ERR_INVALID_ARG, "k_select %d / p_select %d < 0", k_select, p_select);
+  for (int g = 0; g < n_grid; ++g) {
+    const float a = grid[3 * g], b = grid[3 * g + 1], c = grid[3 * g + 2];
+    if (!(a > 0.f && a <= 1.f) || !(b > 0.f && b <= 1.f) || !(c >= 0.f && c <= 1.f))
+      return fail(PRR_ERR_INVALID_ARG, "grid point %d (%g, %g, %g) outside (0,1] x (0,1] x [0,1]", g, a, b, c);
+  }
+  prr::calibrate_grid(scores, n_traj, n_rows, n_blocks, k_select, p_select, grid, n_grid, n_threads, best_theta,
+                      objective_out);
+  return ok();
+}
+
 prr_status prr_merge_states(int32_t n_states, int32_t rows, int32_t d, const float* o, const float* m, const float* l,
                             float* out_o, float* out_m, float* out_l, hipStream_t stream) {
   if (n_states < 0 || rows < 1 || d < 1 || d > 1024)

@@ -138,6 +138,8 @@ hipError_t launch_fused(const FusedLaunch& a, bool bf16, int page_size, hipStrea
 int fused_grid(const FusedLaunch& a);
 
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
+void calibrate_grid(const float* scores, int n_traj, int n_rows, int n_blocks, int k_select, int p_select,
+                    const float* grid, int n_grid, int n_threads, float* best_theta, double* objective_out);
 hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream);
 hipError_t launch_score_topk(const ScoreLaunch& a, hipStream_t stream);
 hipError_t launch_predict(const PredictLaunch& a, hipStream_t stream);

@@ -15,5 +15,6 @@ from .synth import (  # noqa: F401
     layer_inputs,
     page_table_permutation,
     query_trajectory,
+    prefill_trajectory,
     to_physical,
 )

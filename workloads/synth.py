@@ -32,7 +32,7 @@ from typing import Dict, List, Optional
 import numpy as np
 
 SEED_ROOT = 2606
-STREAM_K, STREAM_V, STREAM_HOT, STREAM_Q, STREAM_DRIFT = 0, 1, 2, 3, 4
+STREAM_K, STREAM_V, STREAM_HOT, STREAM_Q, STREAM_DRIFT, STREAM_PREFILL = 0, 1, 2, 3, 4, 5
 HOT_SHIFT = 2.0
 
 
@@ -225,6 +225,21 @@ def query_trajectory(cfg: Config, layer: int = 0, steps: Optional[int] = None):
     for t in range(1, t_total):
         lat[t] = rho * lat[t - 1] + sig * rng.standard_normal(shape, dtype=np.float32)
     return lat, f32_to_dtype_bits(lat, cfg.dtype)
+
+
+def prefill_trajectory(cfg: Config, layer: int = 0, rows: int = 16):
+    """The queries of the last `rows` prefill tokens, ending with the step-0 query: the
+    stationary AR(1) process run backwards from q_0 (it is time-reversible), drawn from
+    its own stream.  Returns stored bits uint16 [rows][Hq][d] in time order."""
+    lat0, _ = query_trajectory(cfg, layer, steps=0)
+    rng = _rng(cfg.cfg_id, layer, STREAM_PREFILL)
+    shape = (cfg.num_q_heads, cfg.head_dim)
+    lat = np.empty((rows,) + shape, dtype=np.float32)
+    lat[rows - 1] = lat0[0]
+    rho, sig = np.float32(cfg.rho), np.float32(cfg.sigma)
+    for r in range(rows - 2, -1, -1):
+        lat[r] = rho * lat[r + 1] + sig * rng.standard_normal(shape, dtype=np.float32)
+    return f32_to_dtype_bits(lat, cfg.dtype)
 
 
 def page_table_permutation(num_logical: int, num_physical: int, seed: int) -> np.ndarray:
