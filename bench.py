@@ -230,8 +230,7 @@ def delta_sweep(args, cfg):
     out = {"sweep": "speculation budget (Section 4.4)", "workload": f"{cfg.name} layer 0, context prefixes",
            "table": rows, "picked_delta": pick}
     if args.write_lut:
-        os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
-        with open(os.path.join(ROOT, "gpurun_out", "delta_lut.json"), "w") as f:
+        with open(args.write_lut, "w") as f:
             json.dump({"workload": out["workload"], "table": rows}, f, indent=1)
     print(json.dumps(out), flush=True)
 
@@ -248,7 +247,7 @@ def main():
     ap.add_argument("--delta-sweep", action="store_true",
                     help="only the offline speculation-budget sweep (Section 4.4): selection and speculation "
                          "latency per context length and delta, and the fused PRR step; prints the table")
-    ap.add_argument("--write-lut", action="store_true", help="with --delta-sweep: store the table in the package")
+    ap.add_argument("--write-lut", default=None, metavar="PATH", help="with --delta-sweep: also write the table as JSON")
     ap.add_argument("--kernel-sweep", action="store_true",
                     help="only the sparse-attention kernel sweep (Table 3 shape: 32 q / 8 kv heads, d 128, 128K "
                          "context, page 16 and 64, budget 1K-8K tokens): microseconds and GB/s")
