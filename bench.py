@@ -259,7 +259,7 @@ def main():
                          "S2 (reuse + repair) and S3 (EMA + repair) with the fused PRR schedule")
     ap.add_argument("--chunk", type=int, default=None, help="pages per speculation chunk (default 8, 4 for 64-token pages)")
     ap.add_argument("--delta", type=float, default=1.0, help="|P| / |A| (speculation budget)")
-    ap.add_argument("--schedules", default="fused_prr,fused_serial,two_stream,serial")
+    ap.add_argument("--schedules", default="fused_prr,fused_prr_late,fused_serial,two_stream,serial")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--kernel-reps", type=int, default=2, help="tokens per kernel-timing pass (separate kernels)")
     ap.add_argument("--workers", type=int, default=16, help="input-generation processes (0 = in-process)")
@@ -294,8 +294,9 @@ def main():
                       alpha=theta[0], beta=theta[1], gamma=theta[2],
                       chunk_pages=args.chunk or min(8, 256 // cfg.page_size), mode=mode, p_select=p_select)
     schedules = [x for x in args.schedules.split(",") if x]
-    sched_id = {"fused_prr": L.PRR_SCHED_FUSED_PRR, "fused_serial": L.PRR_SCHED_FUSED_SERIAL,
-                "two_stream": L.PRR_SCHED_TWO_STREAM, "serial": L.PRR_SCHED_SERIAL}
+    sched_id = {"fused_prr": L.PRR_SCHED_FUSED_PRR, "fused_prr_late": L.PRR_SCHED_FUSED_PRR,
+                "fused_serial": L.PRR_SCHED_FUSED_SERIAL, "two_stream": L.PRR_SCHED_TWO_STREAM,
+                "serial": L.PRR_SCHED_SERIAL}
     n_abl = (3 if args.ablation else 0) + (2 if args.calibrate > 1 else 0)
     total_tokens = 2 + max(2, args.warmup) + 2 * (len(schedules) + n_abl) * (args.steps + 2) + \
         n_abl * (1 + max(2, args.warmup)) + args.kernel_reps + 8
@@ -359,8 +360,10 @@ def main():
     hits = run(max(2, args.warmup), L.PRR_SCHED_FUSED_PRR, measure_hits=True)
     ms = {}
     for name in schedules:  # warm each schedule, then two timed passes (the better one counts)
+        stack.params.late_spec = int(name == "fused_prr_late")
         run(2, sched_id[name])
         ms[name] = min(timed(args.steps, sched_id[name]), timed(args.steps, sched_id[name]))
+    stack.params.late_spec = 0
     ablation = None
     if args.ablation:
         # Section 6.3: S1 reuses the previous step's top-K (theta = (1, .5, 0)) and

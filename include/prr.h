@@ -260,6 +260,10 @@ typedef struct {
   float alpha, beta, gamma;
   uint32_t epoch;              /* fused schedules: >= 1 and different from every earlier call's
                                   value on the same workspaces (e.g. the token index + 1) */
+  int32_t late_spec;           /* PRR_SCHED_FUSED_PRR: 1 = also speculate, as soon as this step's
+                                  scores exist, over the pages just above the selection threshold
+                                  that P missed (the threshold is learned across steps); the result
+                                  is still attention over exactly A (or P u A) */
 } prr_step_params;
 
 #define PRR_SCHED_SERIAL 0     /* per layer: select, then attend every page of A (one stream) */

@@ -75,7 +75,7 @@ class prr_step_params(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("num_tokens", "num_pages", "k_select", "p_select", "cap",
                                                "chunk_pages", "mode", "forced_in_budget", "n_forced")] + [
         ("forced", ctypes.POINTER(ctypes.c_int32)), ("alpha", ctypes.c_float), ("beta", ctypes.c_float),
-        ("gamma", ctypes.c_float), ("epoch", ctypes.c_uint32)]
+        ("gamma", ctypes.c_float), ("epoch", ctypes.c_uint32), ("late_spec", ctypes.c_int32)]
 
 
 if not os.path.exists(LIB_PATH):

@@ -71,7 +71,7 @@ prr_status check_ptr(const void* p, const char* name, size_t align) {
 
 struct WsLayout {
   size_t flags, sel_cnt, rep_cnt, rep_o, rep_ml, f_score, f_thr, f_mcnt, f_mlist, f_part, f_cnt, f_candk, f_candp,
-      f_pkey, f_win, total;
+      f_pkey, f_win, f_lcnt, f_pbits, total;
   int nchunks, nwork_max, nparts;
 };
 
@@ -92,7 +92,7 @@ bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
   L.rep_ml = off;
   off = align_up(off + (size_t)hkv * L.nwork_max * g * 2 * 4, 256);
   // fused step: tagged scores, threshold, missed count and list, partial states
-  L.nparts = 2 * L.nchunks;
+  L.nparts = 3 * L.nchunks;
   L.f_score = off;
   off = align_up(off + (size_t)hkv * d->max_pages * 8, 256);
   L.f_thr = off;
@@ -105,15 +105,19 @@ bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
   off = align_up(off + (size_t)hkv * L.nparts * g * 130 * 8, 256);
   const size_t nsc = (size_t)div_up(d->max_pages, 128);
   L.f_cnt = off;
-  off = align_up(off + 2 * (size_t)hkv * nsc * 8, 256);
+  off = align_up(off + 3 * (size_t)hkv * nsc * 8, 256);
   L.f_candk = off;
-  off = align_up(off + 2 * (size_t)hkv * nsc * 128 * 8, 256);
+  off = align_up(off + 3 * (size_t)hkv * nsc * 128 * 8, 256);
   L.f_candp = off;
-  off = align_up(off + 2 * (size_t)hkv * nsc * 128 * 8, 256);
+  off = align_up(off + 3 * (size_t)hkv * nsc * 128 * 8, 256);
   L.f_pkey = off;
   off = align_up(off + (size_t)hkv * d->max_pages * 8, 256);
   L.f_win = off;
-  off = align_up(off + (size_t)hkv * 2 * 4, 256);
+  off = align_up(off + (size_t)hkv * 4 * 4, 256);
+  L.f_lcnt = off;
+  off = align_up(off + (size_t)hkv * 8, 256);
+  L.f_pbits = off;
+  off = align_up(off + 2 * (size_t)hkv * ((d->max_pages + 31) / 32) * 4, 256);
   L.total = off;
   return true;
 }
@@ -554,6 +558,13 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.t_candp = reinterpret_cast<uint64_t*>(ws + L.f_candp);
   a.t_pkey = reinterpret_cast<uint64_t*>(ws + L.f_pkey);
   a.win = reinterpret_cast<uint32_t*>(ws + L.f_win);
+  a.t_lcnt = reinterpret_cast<uint64_t*>(ws + L.f_lcnt);
+  {
+    uint32_t* pb = reinterpret_cast<uint32_t*>(ws + L.f_pbits);
+    const size_t nwp = (size_t)dims->num_kv_heads * ((dims->max_pages + 31) / 32);
+    a.pbits_cur = pb + (size_t)parity * nwp;
+    a.pbits_nxt = pb + (size_t)(1 - parity) * nwp;
+  }
   a.flags = reinterpret_cast<uint32_t*>(ws + L.flags);
   a.alpha = sp->alpha;
   a.beta = sp->beta;
@@ -573,6 +584,8 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.n_score = div_up(sp->num_pages, 128);
   a.n_spec = L.nchunks;
   a.n_miss = L.nchunks;
+  a.late = prr && sp->late_spec && sp->mode != PRR_RECOMPUTE_ON_MISS;
+  a.n_late = a.late ? L.nchunks : 0;
   a.nparts = L.nparts;
   a.n_forced = sp->n_forced;
   a.meta_mean = dims->meta_kind == PRR_META_MEAN;

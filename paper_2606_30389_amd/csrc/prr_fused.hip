@@ -164,10 +164,17 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
   // wave 0 filters: EMA state of pages pbase + lane and pbase + 64 + lane, and the
   // candidate bounds, kept from the previous step as ratios to |q-bar|_1 (scores scale
   // with q-bar); loaded together with the metadata
-  float r_a = 0.f, r_p = 0.f;
+  float r_a = 0.f, r_p = 0.f, r_l = 0.f;
+  uint32_t pw[2] = {0u, 0u};
   if (w == 0) {
-    r_a = __uint_as_float(a.win[2 * h]);
-    r_p = __uint_as_float(a.win[2 * h + 1]);
+    r_a = __uint_as_float(a.win[4 * h]);
+    r_p = __uint_as_float(a.win[4 * h + 1]);
+    r_l = __uint_as_float(a.win[4 * h + 2]);
+    if (a.late) {
+#pragma unroll
+      for (int half = 0; half < 2; ++half)
+        pw[half] = a.pbits_cur[(size_t)h * nwmax + (min(pbase + 64 * half + (lane & 32), n - 1) >> 5)];
+    }
     if (ema) {
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
@@ -237,6 +244,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
   if (w != 0) return;
   const float qn = wave_sum(fabsf(S.qbar[lane]) + fabsf(S.qbar[lane + 64]));
   const uint32_t lo_a = score_key(r_a * qn), lo_p = score_key(r_p * qn);
+  const uint32_t lo_l = max(score_key(r_l * qn), lo_a);  // late pages are candidates of A
 
   const size_t rec_a = (size_t)h * a.n_score + blk;
   const size_t rec_p = ((size_t)a.num_kv_heads + h) * a.n_score + blk;
@@ -244,8 +252,12 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
   uint64_t* cp_a = a.t_candp + rec_a * kFScorePages;
   uint64_t* ck_p = a.t_candk + rec_p * kFScorePages;
   uint64_t* cp_p = a.t_candp + rec_p * kFScorePages;
-  int na = 0, nfa = 0, np = 0, nfp = 0;
-  // candidates of A first (the select workgroup waits for them) ...
+  int na = 0, nfa = 0, np = 0, nfp = 0, nl = 0;
+  // candidates of A first (the select workgroup waits for them), each flagged when it is
+  // also a page for late speculation: not forced, not in P^t, key at least lo_l ...
+  const size_t rec_l = (2 * (size_t)a.num_kv_heads + h) * a.n_score + blk;
+  uint64_t* ck_l = a.t_candk + rec_l * kFScorePages;
+  uint64_t* cp_l = a.t_candp + rec_l * kFScorePages;
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
     const int lp = 64 * half + lane;
@@ -254,16 +266,26 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
     const bool f = inr && ((S.fbits[lp >> 5] >> (lp & 31)) & 1u);
     const uint32_t ka = score_key(S.sc[lp]);
     const bool ca = inr && (f || ka >= lo_a);
-    const uint64_t ma = __ballot(ca), mfa = __ballot(ca && f);
+    const bool late = a.late && ca && !f && ka >= lo_l && !((pw[half] >> (p & 31)) & 1u);
+    const uint64_t ma = __ballot(ca), mfa = __ballot(ca && f), ml = __ballot(late);
     if (ca) {
       const int pos = na + lanes_below(ma);
       put_tag(&ck_a[pos], ka, a.epoch);
-      put_tag(&cp_a[pos], (uint32_t)p | (f ? 0x80000000u : 0u), a.epoch);
+      put_tag(&cp_a[pos], (uint32_t)p | (f ? 0x80000000u : 0u) | (late ? 0x40000000u : 0u), a.epoch);
+    }
+    if (late) {
+      const int pos = nl + lanes_below(ml);
+      put_tag(&ck_l[pos], ka, a.epoch);
+      put_tag(&cp_l[pos], (uint32_t)p, a.epoch);
     }
     na += __popcll(ma);
     nfa += __popcll(mfa);
+    nl += __popcll(ml);
   }
-  if (lane == 0) put_tag(&a.t_cnt[rec_a], (uint32_t)na | ((uint32_t)nfa << 16), a.epoch);
+  if (lane == 0) {
+    put_tag(&a.t_cnt[rec_a], (uint32_t)na | ((uint32_t)nfa << 16), a.epoch);
+    if (a.late) put_tag(&a.t_cnt[rec_l], (uint32_t)nl, a.epoch);
+  }
   if (!ema) return;
   // ... then the EMA update of Eq. (3) and the candidates of the next prediction
 #pragma unroll
@@ -618,9 +640,10 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, int h, int whic
 // The candidate list (LDS, page order) into this thread's slots i = (w, j, lane).
 template <int J>
 __device__ __forceinline__ void cand_slots(int total, const uint32_t* lk, const uint32_t* lp, uint32_t (&key)[J],
-                                           int (&page)[J], uint64_t& cand, uint64_t& force) {
+                                           int (&page)[J], uint64_t& cand, uint64_t& force, uint64_t* late) {
   cand = 0;
   force = 0;
+  uint64_t lb = 0;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     const int i = sel2_page<J>(j);
@@ -629,11 +652,13 @@ __device__ __forceinline__ void cand_slots(int total, const uint32_t* lk, const 
     if (i < total) {
       key[j] = lk[i];
       const uint32_t pv = lp[i];
-      page[j] = (int)(pv & 0x7fffffffu);
+      page[j] = (int)(pv & 0x3fffffffu);
       if (pv >> 31) force |= 1ull << j;
       else cand |= 1ull << j;
+      if ((pv >> 30) & 1u) lb |= 1ull << j;
     }
   }
+  if (late) *late = lb;
 }
 
 // All pages of KV head h as slots (the fallback): keys polled from `tk`.
@@ -672,10 +697,10 @@ __device__ __forceinline__ void full_gather(const FusedLaunch& a, const uint64_t
   }
 }
 
-// Lower bound of the next step's candidates: the score of rank 3k among this step's
-// candidates, kept as a ratio to |q-bar|_1 (kept unchanged when fewer than 3k
-// candidates exist and `keep` is set; -inf, i.e. every page, after a fallback that
-// found fewer than 3k pages).
+// Lower bound of the next step's candidates: the score of rank `k` (3 |A| for the
+// candidates, 1.5 |A| for late speculation) among this step's candidates, kept as a
+// ratio to |q-bar|_1 (unchanged when fewer candidates exist and `keep` is set; -inf,
+// i.e. every page, after a fallback that found fewer).
 __device__ __forceinline__ float key_value(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
 }
@@ -684,7 +709,7 @@ template <int J>
 __device__ __forceinline__ void update_window(const FusedLaunch& a, uint32_t* win, float qn, const uint32_t (&key)[J],
                                               uint64_t cand, int k, bool keep, Sel2Lds& S) {
   __syncthreads();  // the LDS may still be read by the previous step of this workgroup
-  const SelThreshold th = sel2_threshold<kFT, J>(key, cand, 3 * max(k, 1), S);
+  const SelThreshold th = sel2_threshold<kFT, J>(key, cand, max(k, 1), S);
   if (threadIdx.x == 0) {
     if (th.mode == 2 && qn > 0.0f) *win = __float_as_uint(key_value(th.T) / qn);
     else if (!keep) *win = __float_as_uint(-__builtin_inff());
@@ -716,8 +741,8 @@ __device__ __forceinline__ float qbar_finish(const FusedLaunch& a, const float (
 
 template <bool BF16, int PS, int J>
 __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const uint32_t (&key)[J],
-                                              const int (&page)[J], uint64_t cand, uint64_t force, bool keep_window,
-                                              float qn, FLds& U) {
+                                              const int (&page)[J], uint64_t cand, uint64_t force, uint64_t late_bits,
+                                              bool keep_window, float qn, FLds& U) {
   FSelLds& L = U.sel;
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const bool prr = a.schedule == 1;
@@ -743,11 +768,40 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
     }
   }
 
-  // the list to attend after selection, in page order: A \ P (PRR) or A (serial, or a
-  // PRR step whose speculation is discarded because a page was missed)
+  // pages attended by late speculation: flagged candidates within the late capacity
+  // (rank among the flagged pages in page order), never a page of P^t
+  uint64_t inLate = 0;
+  if (a.late) {
+    uint64_t flagged = 0;
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+      if ((((cand | force) >> j) & 1ull) && (late_bits >> j) & 1ull) flagged |= 1ull << j;
+    const int lc = wave_isum(__popcll(flagged));
+    __syncthreads();
+    if (lane == 0) L.cnt[0][w] = lc;
+    __syncthreads();
+    int run = 0, ltot = 0;
+#pragma unroll
+    for (int i = 0; i < kFW; ++i) {
+      run += i < w ? L.cnt[0][i] : 0;
+      ltot += L.cnt[0][i];
+    }
+    const int capl = a.n_late * a.chunk;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const bool f = (flagged >> j) & 1ull;
+      const uint64_t bm = __ballot(f);
+      if (f && run + lanes_below(bm) < capl && !((inP >> j) & 1ull)) inLate |= 1ull << j;
+      run += __popcll(bm);
+    }
+    if (t == 0) put_tag(&a.t_lcnt[h], (uint32_t)min(ltot, capl), a.epoch);
+  }
+  // the list to attend after selection, in page order: A \ P (PRR; also without the
+  // late-speculated pages) or A (serial, or a PRR step whose speculation is discarded
+  // because a page was missed)
   const int nMiss = prr ? block_sum<kFT>(__popcll(inA & ~inP), L.sel.red[2]) : 0;
   const bool drop = prr && a.mode == PRR_RECOMPUTE_ON_MISS && nMiss > 0;
-  const uint64_t inM = (prr && !drop) ? (inA & ~inP) : inA;
+  const uint64_t inM = (prr && !drop) ? (inA & ~inP & ~inLate) : inA;
   const uint32_t mflags = drop ? kDropSpec : 0u;
   const int nM = min(sel2_list<kFT, J>(inM, page, L.mlist, a.cap, L.sel), a.cap);
   __syncthreads();
@@ -785,7 +839,8 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
     fold_publish<1>(a, h, a.n_spec, st, 1u, U.attn);
   }
-  update_window<J>(a, a.win + 2 * h, qn, key, cand, a.kextra_a, keep_window, U.sel.sel);
+  update_window<J>(a, a.win + 4 * h, qn, key, cand, 3 * a.kextra_a, keep_window, U.sel.sel);
+  if (a.late) update_window<J>(a, a.win + 4 * h + 2, qn, key, cand, (3 * a.kextra_a) / 2, true, U.sel.sel);
 }
 
 template <bool BF16, int PS>
@@ -836,8 +891,9 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U
     uint32_t key[8];
     int page[8];
     uint64_t cand, force;
-    cand_slots<8>(c.total, L.ck, L.cpg, key, page, cand, force);
-    select_finish<BF16, PS, 8>(a, h, key, page, cand, force, true, qn, U);
+    uint64_t late_bits;
+    cand_slots<8>(c.total, L.ck, L.cpg, key, page, cand, force, &late_bits);
+    select_finish<BF16, PS, 8>(a, h, key, page, cand, force, late_bits, true, qn, U);
   } else {
     uint32_t key[16];
     int page[16];
@@ -845,7 +901,7 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U
     full_gather<16>(a, a.t_score + (size_t)h * a.max_pages, L.forceb, key, page, cand, force);
 #pragma unroll
     for (int j = 0; j < 16; ++j) key[j] = score_key(__uint_as_float(key[j]));
-    select_finish<BF16, PS, 16>(a, h, key, page, cand, force, false, qn, U);
+    select_finish<BF16, PS, 16>(a, h, key, page, cand, force, 0ull, false, qn, U);
   }
 }
 
@@ -856,9 +912,18 @@ __device__ __forceinline__ void predict_finish(const FusedLaunch& a, int h, cons
                                                const int (&page)[J], uint64_t cand, uint64_t force, bool keep_window,
                                                float qn, FSelLds& L) {
   const SelThreshold th = sel2_threshold<kFT, J>(key, cand, a.kextra_p, L.sel);
-  sel2_compact<kFT, J>(key, page, cand, force, th, a.pred_nxt + (size_t)h * a.cap, a.cap, a.pred_nxt_count + h,
-                       &L.eq_cut, L.sel);
-  update_window<J>(a, a.win + 2 * h + 1, qn, key, cand, a.kextra_p, keep_window, L.sel);
+  const uint64_t in = sel2_compact<kFT, J>(key, page, cand, force, th, a.pred_nxt + (size_t)h * a.cap, a.cap,
+                                           a.pred_nxt_count + h, &L.eq_cut, L.sel);
+  // P^{t+1} as a bitmap too (the late-speculation filter of the next step)
+  const int nw = (a.num_pages + 31) >> 5, nwmax = (a.max_pages + 31) >> 5;
+  for (int i = threadIdx.x; i < nw; i += kFT) L.bitP[i] = 0u;
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < J; ++j)
+    if ((in >> j) & 1ull) atomicOr(&L.bitP[page[j] >> 5], 1u << (page[j] & 31));
+  __syncthreads();
+  for (int i = threadIdx.x; i < nw; i += kFT) a.pbits_nxt[(size_t)h * nwmax + i] = L.bitP[i];
+  update_window<J>(a, a.win + 4 * h + 1, qn, key, cand, 3 * a.kextra_p, keep_window, L.sel);
 }
 
 template <bool BF16>
@@ -883,7 +948,7 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, int h, FLds& 
     uint32_t key[8];
     int page[8];
     uint64_t cand, force;
-    cand_slots<8>(c.total, L.ck, L.cpg, key, page, cand, force);
+    cand_slots<8>(c.total, L.ck, L.cpg, key, page, cand, force, nullptr);
     predict_finish<8>(a, h, key, page, cand, force, true, qn, L);
   } else {
     uint32_t key[16];
@@ -895,6 +960,33 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, int h, FLds& 
 }
 
 // ------------------------------------------------------------------------ spec / miss
+
+// Membership of this wave's pages in A, from their scores and the published threshold
+// (all loads issued together, then waited for); returns `keep` without the pages not in A.
+template <int NPW>
+__device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, int h, const int (&pg)[NPW], uint32_t keep) {
+  if (!keep) return keep;
+  const uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
+  const uint64_t* thr = a.t_thr + 2 * (size_t)h;
+  uint64_t vs[NPW];
+#pragma unroll
+  for (int k = 0; k < NPW; ++k) vs[k] = get_tag(&ts[max(pg[k], 0)]);
+  const uint64_t v0 = get_tag(thr), v1 = get_tag(thr + 1);
+  uint32_t sc[NPW];
+#pragma unroll
+  for (int k = 0; k < NPW; ++k) sc[k] = pg[k] >= 0 ? tagged(vs[k], &ts[pg[k]], a.epoch, a.flags) : 0u;
+  const uint32_t T = tagged(v0, thr, a.epoch, a.flags);
+  const uint32_t me = tagged(v1, thr + 1, a.epoch, a.flags);
+  const int mode = (int)(me & 3u), eq_cut = (int)(me >> 2);
+#pragma unroll
+  for (int k = 0; k < NPW; ++k) {
+    if (pg[k] < 0 || page_forced(a, pg[k])) continue;
+    const uint32_t key = score_key(__uint_as_float(sc[k]));
+    const bool in = mode == 1 || (mode == 2 && (key > T || (key == T && pg[k] <= eq_cut)));
+    if (!in) keep &= ~(1u << k);
+  }
+  return keep;
+}
 
 template <bool BF16, int PS, int NPW>
 __device__ __forceinline__ void role_spec(const FusedLaunch& a, int h, int c, FLds& U) {
@@ -921,30 +1013,58 @@ __device__ __forceinline__ void role_spec(const FusedLaunch& a, int h, int c, FL
   }
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
-  if (a.mode != PRR_KEEP_WASTED && keep) {
-    // membership of this wave's pages in A, from their scores and the published
-    // threshold (all loads issued together, then waited for)
-    const uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
-    const uint64_t* thr = a.t_thr + 2 * (size_t)h;
-    uint64_t vs[NPW];
-#pragma unroll
-    for (int k = 0; k < NPW; ++k) vs[k] = get_tag(&ts[max(pg[k], 0)]);
-    const uint64_t v0 = get_tag(thr), v1 = get_tag(thr + 1);
-    uint32_t sc[NPW];
-#pragma unroll
-    for (int k = 0; k < NPW; ++k) sc[k] = pg[k] >= 0 ? tagged(vs[k], &ts[pg[k]], a.epoch, a.flags) : 0u;
-    const uint32_t T = tagged(v0, thr, a.epoch, a.flags);
-    const uint32_t me = tagged(v1, thr + 1, a.epoch, a.flags);
-    const int mode = (int)(me & 3u), eq_cut = (int)(me >> 2);
-#pragma unroll
-    for (int k = 0; k < NPW; ++k) {
-      if (pg[k] < 0 || page_forced(a, pg[k])) continue;
-      const uint32_t key = score_key(__uint_as_float(sc[k]));
-      const bool in = mode == 1 || (mode == 2 && (key > T || (key == T && pg[k] <= eq_cut)));
-      if (!in) keep &= ~(1u << k);
-    }
-  }
+  if (a.mode != PRR_KEEP_WASTED) keep = keep_in_A<NPW>(a, h, pg, keep);
   fold_publish<NPW>(a, h, c, st, keep, U.attn);
+}
+
+// Late speculation (PRR schedule): as soon as this step's scores exist, the pages just
+// above the selection threshold that P^t missed (listed by the score workgroups) are
+// attended, one state per page; once A is known the states of pages in A are folded.
+template <bool BF16, int PS, int NPW>
+__device__ __forceinline__ void role_late(const FusedLaunch& a, int h, int u, FLds& U) {
+  FSelLds& L = U.sel;
+  const int t = threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane((int)(t / kWave));
+  u32x4_t qf[4];
+  load_q(a, h, qf);
+  // P^t as an LDS bitmap: a page of P^t is never attended here (the hint bitmap the
+  // score workgroups filtered with may be stale)
+  const int n = a.num_pages, nw = (n + 31) >> 5;
+  for (int i = t; i < nw; i += kFT) L.bitP[i] = 0u;
+  int pe[PRR_MAX_CAP_DEV / kFT];
+  const int pc = min(max(a.pred_cur_count[h], 0), a.cap);
+#pragma unroll
+  for (int r = 0; r < PRR_MAX_CAP_DEV / kFT; ++r) {
+    const int i = t + r * kFT;
+    pe[r] = i < pc ? a.pred_cur[(size_t)h * a.cap + i] : -1;
+  }
+  const FCand c = cand_load(a, h, 2, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+#pragma unroll
+  for (int r = 0; r < PRR_MAX_CAP_DEV / kFT; ++r)
+    if (pe[r] >= 0 && pe[r] < n) atomicOr(&L.bitP[pe[r] >> 5], 1u << (pe[r] & 31));
+  __syncthreads();
+  const int cover = min(c.total, a.n_late * a.chunk);
+  const int start = u * a.chunk;
+  if (start >= cover) return;
+  const int cnt = min(a.chunk, cover - start);
+  int pg[NPW];
+  uint32_t keep = 0;
+#pragma unroll
+  for (int k = 0; k < NPW; ++k) {
+    const int i = w + kFW * k;
+    int p = -1;
+    if (i < cnt) {
+      p = (int)(L.cpg[start + i] & 0x3fffffffu);
+      if (p >= n || bit_of(L.bitP, p)) p = -1;
+    }
+    pg[k] = __builtin_amdgcn_readfirstlane(p);
+    if (pg[k] >= 0) keep |= 1u << k;
+  }
+  __syncthreads();  // the list is read before the attention reuses the LDS
+  WaveStates<NPW> st;
+  wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
+  keep = keep_in_A<NPW>(a, h, pg, keep);
+  fold_publish<NPW>(a, h, a.n_spec + a.n_miss + u, st, keep, U.attn);
 }
 
 template <bool BF16, int PS, int NPW>
@@ -1009,12 +1129,15 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, 
   const int nM = (int)(mv & kCountMask);
   const int nmiss = (mv & kSelfMiss) ? 1 : (nM + C - 1) / C;
   if (mv & kDropSpec) nspec = 0;
-  const int total = nspec + nmiss;
-  // state i lives in slot i (speculation chunks) or n_spec + (i - nspec) (missed chunks)
+  const int nlate = a.late ? ((int)wait_tag(a.t_lcnt + h, a.epoch, a.flags) + C - 1) / C : 0;
+  const int total = nspec + nmiss + nlate;
+  // state i lives in slot i (speculation chunks), n_spec + (i - nspec) (missed chunks) or
+  // n_spec + n_miss + (i - nspec - nmiss) (late-speculation chunks)
   const uint64_t* part = a.t_part + ((size_t)h * a.nparts * G + qn) * kFPart;
   const size_t sstride = (size_t)G * kFPart;
-  const int slot_gap = a.n_spec - nspec;
-#define PRR_ELEM(i, idx) (part + (size_t)((i) < nspec ? (i) : (i) + slot_gap) * sstride + (idx))
+  const int gap1 = a.n_spec - nspec, gap2 = a.n_spec + a.n_miss - nspec - nmiss;
+#define PRR_ELEM(i, idx) \
+  (part + (size_t)((i) < nspec ? (i) : ((i) < nspec + nmiss ? (i) + gap1 : (i) + gap2)) * sstride + (idx))
 
   // Only the (m, l) of every state are polled (threads t, t+512, ..): polling the output
   // values themselves from every thread of every merge workgroup would flood the memory
@@ -1118,6 +1241,11 @@ __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
       return;
     }
     b -= H * a.n_spec;
+    if (b < H * a.n_late) {
+      role_late<BF16, PS, NPW>(a, b / a.n_late, b % a.n_late, U);
+      return;
+    }
+    b -= H * a.n_late;
   }
   if (b < H * a.n_miss) {
     role_miss<BF16, PS, NPW>(a, b / a.n_miss, b % a.n_miss, U);
@@ -1139,7 +1267,7 @@ int fused_grid(const FusedLaunch& a) {
   const int H = a.num_kv_heads;
   int per = a.n_score + 1;
   if (a.schedule != 0) per += 1;
-  if (a.schedule == 1) per += a.n_spec;
+  if (a.schedule == 1) per += a.n_spec + a.n_late;
   if (a.schedule != 2) per += a.n_miss + a.group;
   return H * per;
 }

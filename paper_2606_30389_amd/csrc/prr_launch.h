@@ -115,11 +115,14 @@ struct FusedLaunch {
   uint64_t* t_mcnt;   // [Hkv] tagged count of the missed list (bit 31: attended by the select workgroup)
   uint64_t* t_mlist;  // [Hkv][cap] tagged missed pages
   uint64_t* t_part;   // [Hkv][nparts][G][130] tagged partial states
-  uint64_t* t_cnt;    // [2][Hkv][n_score] tagged candidate counts of A and of P^{t+1}
-  uint64_t* t_candk;  // [2][Hkv][n_score][128] tagged candidate keys
-  uint64_t* t_candp;  // [2][Hkv][n_score][128] tagged candidate pages (bit 31: forced)
+  uint64_t* t_cnt;    // [3][Hkv][n_score] tagged candidate counts: A, P^{t+1}, late speculation
+  uint64_t* t_candk;  // [3][Hkv][n_score][128] tagged candidate keys
+  uint64_t* t_candp;  // [3][Hkv][n_score][128] tagged candidate pages (bit 31: forced, bit 30: late)
   uint64_t* t_pkey;   // [Hkv][max_pages] tagged keys of the next prediction (EMA)
-  uint32_t* win;      // [Hkv][2] candidate lower bounds (keys) for A and P, kept across steps
+  uint64_t* t_lcnt;   // [Hkv] tagged number of late-speculated pages
+  uint32_t* win;      // [Hkv][4] candidate bounds (ratios to |q-bar|_1) for A, P, late, kept across steps
+  const uint32_t* pbits_cur;  // [Hkv][ceil(max_pages/32)] bitmap of P^t (a hint for the late filter)
+  uint32_t* pbits_nxt;        // bitmap of P^{t+1}
   uint32_t* flags;
   float alpha, beta, gamma;
   uint32_t epoch;
@@ -127,7 +130,8 @@ struct FusedLaunch {
   int mode;
   int num_kv_heads, group, max_pages, num_pages, num_tokens;
   int kextra_a, kextra_p, cap, chunk;
-  int n_score, n_spec, n_miss, nparts;  // workgroups per KV head; partial slots per KV head
+  int n_score, n_spec, n_miss, n_late, nparts;  // workgroups per KV head; partial slots per KV head
+  int late;  // late speculation on (PRR schedule)
   int n_forced;
   bool meta_mean;
   int32_t forced[PRR_MAX_FORCED];

@@ -576,11 +576,19 @@ FUSED_CASES = [
     ("glm32k", 512, 2, None, 1, None, 1, 3, (1.0, 0.5, 0.0)),
     ("glm32k", 512, 0, None, 1, None, 1, 3, (1.0, 0.5, 0.0)),
     ("tiny", None, 2, None, 1, 6, 1, 4, (1.0, 0.5, 0.0)),
+    # late speculation over the pages just above the threshold that P missed
+    ("glm32k", 512, 0, None, 1, None, 2, 4, None, True),
+    ("glm128k", None, 0, None, 1, None, 1, 4, None, True),
+    ("llama64k", 300, 1, None, 1, None, 1, 3, None, True),
+    ("infllm128k", 200, 0, None, 1, None, 1, 3, None, True),
+    ("tiny", None, 0, 3, 1, 6, 1, 4, None, True),
 ]
 
 
 @pytest.mark.parametrize("case", FUSED_CASES,
-                         ids=lambda c: f"{c[0]}-p{c[1]}-m{c[2]}-c{c[3]}-d{c[4]}-k{c[5]}" + ("-reuse" if len(c) > 8 else ""))
+                         ids=lambda c: f"{c[0]}-p{c[1]}-m{c[2]}-c{c[3]}-d{c[4]}-k{c[5]}"
+                         + ("-reuse" if len(c) > 8 and c[8] is not None else "")
+                         + ("-late" if len(c) > 9 and c[9] else ""))
 def test_fused_decode_step(torch, case):
     """The fused schedules of prr_decode_step (one launch per layer): step-0 select + EMA
     initialisation, then per step the PRR launch and the serial launch, every layer
@@ -589,7 +597,8 @@ def test_fused_decode_step(torch, case):
     from paper_2606_30389_amd import runtime as R
     name, npages, mode, chunk, delta, kover, n_layers, steps = case[:8]
     cfg = W.CONFIGS[name]
-    theta = case[8] if len(case) > 8 else (cfg.alpha, cfg.beta, cfg.gamma)
+    theta = case[8] if len(case) > 8 and case[8] is not None else (cfg.alpha, cfg.beta, cfg.gamma)
+    late = bool(case[9]) if len(case) > 9 else False
     layers, inputs, metas, qs, queries = [], [], [], [], []
     for layer in range(n_layers):
         pc = S.path_config(cfg, num_pages=npages, mode=mode, chunk_pages=chunk)
@@ -610,6 +619,7 @@ def test_fused_decode_step(torch, case):
     pc = layers[0].cfg
     forced = list(pc.forced)
     stack = R.DecodeStack(layers, queries, torch.device("cuda:0"))
+    stack.params.late_spec = int(late)
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     stack.step(L.PRR_SCHED_FUSED_PREFILL, s)
