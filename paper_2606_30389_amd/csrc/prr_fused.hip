@@ -40,7 +40,8 @@ constexpr uint32_t kDropSpec = 0x40000000u;  //   the speculation is discarded (
 constexpr uint32_t kCountMask = 0x3fffffffu;
 constexpr int kFOPad = kHeadDim + 4;
 constexpr int kEqAll = 16383;  // eq_cut meaning "every key equal to T is taken"
-constexpr int kCandMax = 8 * kFT;  // candidates ranked by one workgroup (8 per thread)
+constexpr int kCandMax = 4 * kFT;     // candidates ranked by one workgroup (4 per thread)
+constexpr int kCandWave = 16 * kWave;  // candidates ranked by one wave (16 per lane)
 
 __device__ __forceinline__ void put_tag(uint64_t* p, uint32_t v, uint32_t epoch) {
   __hip_atomic_store(p, ((uint64_t)epoch << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -74,7 +75,10 @@ struct FScoreLds {
 };
 
 struct FSelLds {
-  Sel2Lds sel;
+  union {
+    Sel2Lds sel;       // block-wide select
+    WSelLds ws[3];     // one-wave selects: A, and the next step's bounds of A and of late pages
+  };
   uint32_t bitP[PRR_MAX_PAGES_DEV / 32];
   uint32_t forceb[PRR_MAX_PAGES_DEV / 32];
   int32_t mlist[PRR_MAX_CAP_DEV];
@@ -843,6 +847,125 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
   if (a.late) update_window<J>(a, a.win + 4 * h + 2, qn, key, cand, (3 * a.kextra_a) / 2, true, U.sel.sel);
 }
 
+// Short candidate lists (at most 1024): wave 0 selects A, publishes the threshold and
+// the list to attend, and writes the outputs, with no barrier; waves 1 and 2 meanwhile
+// derive the next step's candidate bounds from the same list.
+template <bool BF16, int PS>
+__device__ __forceinline__ void select_wave(const FusedLaunch& a, int h, int total, float qn, FLds& U) {
+  FSelLds& L = U.sel;
+  constexpr int NK = kCandWave / kWave;
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  const bool prr = a.schedule == 1;
+  uint32_t key[NK];
+  int page[NK];
+  uint64_t cand = 0, force = 0, lateb = 0, inP = 0;
+#pragma unroll
+  for (int j = 0; j < NK; ++j) {
+    const int i = j * kWave + lane;
+    key[j] = 0u;
+    page[j] = 0;
+    if (i < total) {
+      key[j] = L.ck[i];
+      const uint32_t pv = L.cpg[i];
+      page[j] = (int)(pv & 0x3fffffffu);
+      if (pv >> 31) force |= 1ull << j;
+      else cand |= 1ull << j;
+      if ((pv >> 30) & 1u) lateb |= 1ull << j;
+      if (prr && bit_of(L.bitP, page[j])) inP |= 1ull << j;
+    }
+  }
+  if (w == 0) {
+    const SelThreshold th = wsel_threshold<NK>(key, cand, a.kextra_a, L.ws[0]);
+    const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
+    uint64_t* thr = a.t_thr + 2 * (size_t)h;
+    if (prr && early && lane == 0) {
+      put_tag(thr, th.T, a.epoch);
+      put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), a.epoch);
+    }
+    int eq_cut = kEqAll;
+    const uint64_t inA = wsel_membership<NK>(key, page, cand, force, th, &eq_cut);
+    if (prr && !early) {
+      eq_cut = __builtin_amdgcn_readfirstlane(wave_umin((uint32_t)eq_cut));
+      if (lane == 0) {
+        put_tag(thr, th.T, a.epoch);
+        put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)eq_cut << 2), a.epoch);
+      }
+    }
+    // pages of late speculation: flagged, within the late capacity, never in P^t
+    uint64_t inLate = 0;
+    int ltot = 0;
+    if (a.late) {
+      const int capl = a.n_late * a.chunk;
+#pragma unroll
+      for (int j = 0; j < NK; ++j) {
+        const bool f = (lateb >> j) & 1ull;
+        const uint64_t bm = __ballot(f);
+        if (f && ltot + lanes_below(bm) < capl && !((inP >> j) & 1ull)) inLate |= 1ull << j;
+        ltot += __popcll(bm);
+      }
+      if (lane == 0) put_tag(&a.t_lcnt[h], (uint32_t)min(ltot, capl), a.epoch);
+    }
+    const int nMiss = prr ? wave_isum(__popcll(inA & ~inP)) : 0;
+    const bool drop = prr && a.mode == PRR_RECOMPUTE_ON_MISS && nMiss > 0;
+    const uint64_t inM = (prr && !drop) ? (inA & ~inP & ~inLate) : inA;
+    const uint32_t mflags = drop ? kDropSpec : 0u;
+    const int nM = min(wave_isum(__popcll(inM)), a.cap);
+    uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
+    int pos = 0;
+#pragma unroll
+    for (int j = 0; j < NK; ++j) {
+      const bool in = (inM >> j) & 1ull;
+      const uint64_t bm = __ballot(in);
+      const int q = pos + lanes_below(bm);
+      if (in && q < a.cap) {
+        L.mlist[q] = page[j];
+        if (nM > kFW) put_tag(&ml[q], (uint32_t)page[j], a.epoch);
+      }
+      pos += __popcll(bm);
+    }
+    if (lane == 0) {
+      const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
+      put_tag(&a.t_mcnt[h], (uint32_t)nM | mflags | self, a.epoch);
+      L.cnt[0][0] = nM;
+    }
+    // the selected list (an output) and the counts
+    int32_t* sel = a.selected + (size_t)h * a.cap;
+    int na = 0;
+#pragma unroll
+    for (int j = 0; j < NK; ++j) {
+      const bool in = (inA >> j) & 1ull;
+      const uint64_t bm = __ballot(in);
+      const int q = na + lanes_below(bm);
+      if (in && q < a.cap) sel[q] = page[j];
+      na += __popcll(bm);
+    }
+    const int nPA = prr ? wave_isum(__popcll(inP & inA)) : 0;
+    if (lane == 0) {
+      a.selected_count[h] = min(na, a.cap);
+      if (a.missed_count) a.missed_count[h] = prr ? nMiss : nM;
+      if (a.wasted_count) a.wasted_count[h] = prr ? L.npv - nPA : 0;
+    }
+  } else if (w == 1 || (w == 2 && a.late)) {
+    // the next step's lower bounds: rank 3|A| (candidates of A) and 1.5|A| (late pages)
+    const int k = w == 1 ? 3 * a.kextra_a : (3 * a.kextra_a) / 2;
+    const SelThreshold th = wsel_threshold<NK>(key, cand, max(k, 1), L.ws[w]);
+    if (lane == 0 && th.mode == 2 && qn > 0.0f) a.win[4 * h + (w == 1 ? 0 : 2)] = __float_as_uint(key_value(th.T) / qn);
+  }
+  __syncthreads();
+  const int nM = L.cnt[0][0];
+  if (nM > 0 && nM <= kFW) {
+    // few enough to attend here: one page per wave, published as the first miss slot
+    int pg[1];
+    pg[0] = __builtin_amdgcn_readfirstlane(w < nM ? L.mlist[w] : -1);
+    __syncthreads();  // the list is read before the attention reuses the LDS
+    u32x4_t qf[4];
+    load_q(a, h, qf);
+    WaveStates<1> st;
+    wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
+    fold_publish<1>(a, h, a.n_spec, st, 1u, U.attn);
+  }
+}
+
 template <bool BF16, int PS>
 __device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U) {
   FSelLds& L = U.sel;
@@ -875,25 +998,31 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U
   }
   float qv[16];
   qbar_load<BF16>(a, h, qv);
-  const FCand c = cand_load(a, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  // both are ready long before the candidates: built first
+  int nv = 0;
 #pragma unroll
   for (int r = 0; r < PRR_MAX_CAP_DEV / kFT; ++r) {
     const int p = pe[r];
     if (p >= 0 && p < n) {
-      const uint32_t old = atomicOr(&L.bitP[p >> 5], 1u << (p & 31));
-      if (!((old >> (p & 31)) & 1u)) atomicAdd(&L.npv, 1);
+      atomicOr(&L.bitP[p >> 5], 1u << (p & 31));
+      ++nv;
     }
   }
+  nv = block_sum<kFT>(nv, L.cnt[1]);  // P^t holds no duplicates
+  if (t == 0) L.npv = nv;
   const float qn = qbar_finish(a, qv, L.qb);
-  if (a.kextra_a <= c.total - c.nforced && c.total <= kCandMax) {
+  const FCand c = cand_load(a, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  if (a.kextra_a <= c.total - c.nforced && c.total <= kCandWave) {
+    select_wave<BF16, PS>(a, h, c.total, qn, U);
+  } else if (a.kextra_a <= c.total - c.nforced && c.total <= kCandMax) {
     // one instantiation per path keeps the kernel's code (and its instruction-cache
-    // footprint) small: 8 candidate slots per thread, 16 page slots in the fallback
-    uint32_t key[8];
-    int page[8];
+    // footprint) small: 4 candidate slots per thread, 16 page slots in the fallback
+    uint32_t key[4];
+    int page[4];
     uint64_t cand, force;
     uint64_t late_bits;
-    cand_slots<8>(c.total, L.ck, L.cpg, key, page, cand, force, &late_bits);
-    select_finish<BF16, PS, 8>(a, h, key, page, cand, force, late_bits, true, qn, U);
+    cand_slots<4>(c.total, L.ck, L.cpg, key, page, cand, force, &late_bits);
+    select_finish<BF16, PS, 4>(a, h, key, page, cand, force, late_bits, true, qn, U);
   } else {
     uint32_t key[16];
     int page[16];
@@ -942,14 +1071,14 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, int h, FLds& 
   }
   float qv[16];
   qbar_load<BF16>(a, h, qv);
-  const FCand c = cand_load(a, h, 1, L.off, L.tot, L.ck, L.cpg);
   const float qn = qbar_finish(a, qv, L.qb);
+  const FCand c = cand_load(a, h, 1, L.off, L.tot, L.ck, L.cpg);
   if (a.kextra_p <= c.total - c.nforced && c.total <= kCandMax) {
-    uint32_t key[8];
-    int page[8];
+    uint32_t key[4];
+    int page[4];
     uint64_t cand, force;
-    cand_slots<8>(c.total, L.ck, L.cpg, key, page, cand, force, nullptr);
-    predict_finish<8>(a, h, key, page, cand, force, true, qn, L);
+    cand_slots<4>(c.total, L.ck, L.cpg, key, page, cand, force, nullptr);
+    predict_finish<4>(a, h, key, page, cand, force, true, qn, L);
   } else {
     uint32_t key[16];
     int page[16];
@@ -1038,11 +1167,11 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, int h, int u, FL
     const int i = t + r * kFT;
     pe[r] = i < pc ? a.pred_cur[(size_t)h * a.cap + i] : -1;
   }
-  const FCand c = cand_load(a, h, 2, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  __syncthreads();
 #pragma unroll
   for (int r = 0; r < PRR_MAX_CAP_DEV / kFT; ++r)
     if (pe[r] >= 0 && pe[r] < n) atomicOr(&L.bitP[pe[r] >> 5], 1u << (pe[r] & 31));
-  __syncthreads();
+  const FCand c = cand_load(a, h, 2, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
   const int cover = min(c.total, a.n_late * a.chunk);
   const int start = u * a.chunk;
   if (start >= cover) return;

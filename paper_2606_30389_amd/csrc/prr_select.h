@@ -289,3 +289,159 @@ __device__ __forceinline__ uint64_t sel2_compact(const uint32_t (&key)[J], const
 }
 
 }  // namespace prr
+
+namespace prr {
+
+// ------------------------------------------------------------------ one-wave select
+// The same exact top-K for at most 64 * NK keys held by ONE wave (slot (j, lane) holds
+// page page[j]; slot order j * 64 + lane must be ascending page order).  Used when the
+// candidate list is short: a single wave needs no barrier between the radix passes, so
+// the threshold is known after a few LDS round trips.  Each wave using it needs its own
+// WSelLds.
+
+struct WSelLds {
+  uint32_t hist[kSel2Bins];
+  uint32_t small[kSel2Small];
+};
+
+template <int NK>
+__device__ __forceinline__ SelThreshold wsel_threshold(const uint32_t (&key)[NK], uint64_t cand, int kextra,
+                                                       WSelLds& S) {
+  const int lane = lane_id();
+  int cnt = __popcll(cand);
+  uint32_t lo = 0xffffffffu, hi = 0u;
+#pragma unroll
+  for (int j = 0; j < NK; ++j) {
+    if ((cand >> j) & 1ull) {
+      lo = min(lo, key[j]);
+      hi = max(hi, key[j]);
+    }
+  }
+  cnt = wave_isum(cnt);
+  lo = wave_umin(lo);
+  hi = wave_umax(hi);
+  SelThreshold r;
+  r.mode = 0;
+  r.T = 0;
+  r.need_eq = 0;
+  r.eq_total = 0;
+  if (kextra <= 0 || cnt == 0) return r;
+  if (kextra >= cnt) {
+    r.mode = 1;
+    return r;
+  }
+  r.mode = 2;
+  int rank = kextra, inrange = cnt;
+  for (int pass = 0; pass < 3; ++pass) {
+    const uint32_t range = hi - lo;
+    if (range == 0) {
+      r.T = lo;
+      r.need_eq = rank;
+      r.eq_total = inrange;
+      return r;
+    }
+    const int bits = 32 - __clz(range);
+    const int shift = bits > kSel2Log2Bins ? bits - kSel2Log2Bins : 0;
+    // this lane's 32 bins [2048 - 32(lane+1), 2048 - 32 lane) are cleared, then counted
+    const int base = kSel2Bins - 32 * (lane + 1);
+    uint4* hb = reinterpret_cast<uint4*>(S.hist + base);
+#pragma unroll
+    for (int v = 0; v < 8; ++v) hb[v] = make_uint4(0, 0, 0, 0);
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int j = 0; j < NK; ++j)
+      if (((cand >> j) & 1ull) && key[j] >= lo && key[j] <= hi) atomicAdd(&S.hist[(key[j] - lo) >> shift], 1u);
+    __builtin_amdgcn_wave_barrier();
+    int s = 0;
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      const uint4 x = hb[v];
+      s += (int)(x.x + x.y + x.z + x.w);
+    }
+    const int incl = wave_inclusive_scan(s);
+    const uint64_t hit = __ballot(incl - s < rank && rank <= incl);
+    const int ls = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit) - 1);
+    const int ex = __builtin_amdgcn_readlane(incl - s, ls);
+    const int lbase = kSel2Bins - 32 * (ls + 1);
+    const int cj = lane < 32 ? (int)S.hist[lbase + 31 - lane] : 0;  // descending bins
+    const int cinc = wave_inclusive_scan(cj);
+    const uint64_t hit2 = __ballot(lane < 32 && ex + cinc >= rank);
+    const int js = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit2) - 1);
+    const int bstar = lbase + 31 - js;
+    const int cbin = __builtin_amdgcn_readlane(cj, js);
+    rank -= __builtin_amdgcn_readlane(ex + cinc - cj, js);
+    inrange = cbin;
+    const uint32_t nlo = lo + ((uint32_t)bstar << shift);
+    hi = (uint32_t)min((uint64_t)hi, (uint64_t)nlo + ((1ull << shift) - 1ull));
+    lo = nlo;
+    if (shift == 0) {
+      r.T = lo;
+      r.need_eq = rank;
+      r.eq_total = cbin;
+      return r;
+    }
+    if (cbin <= kSel2Small) {
+      // the keys of this bin, compacted in slot order, ranked by broadcast
+      int pos = 0;
+#pragma unroll
+      for (int j = 0; j < NK; ++j) {
+        const bool in = ((cand >> j) & 1ull) && key[j] >= lo && key[j] <= hi;
+        const uint64_t m = __ballot(in);
+        if (in) S.small[pos + lanes_below(m)] = key[j];
+        pos += __popcll(m);
+      }
+      __builtin_amdgcn_wave_barrier();
+      const uint32_t mine = S.small[lane < cbin ? lane : 0];
+      int gt = 0, ge = 0;
+      for (int x = 0; x < cbin; ++x) {
+        const uint32_t kx = (uint32_t)__builtin_amdgcn_readlane((int)mine, x);
+        gt += kx > mine ? 1 : 0;
+        ge += kx >= mine ? 1 : 0;
+      }
+      const uint64_t hit3 = __ballot(lane < cbin && gt < rank && rank <= ge);
+      const int l3 = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit3) - 1);
+      r.T = (uint32_t)__builtin_amdgcn_readlane((int)mine, l3);
+      r.need_eq = rank - __builtin_amdgcn_readlane(gt, l3);
+      r.eq_total = __builtin_amdgcn_readlane(ge - gt, l3);
+      return r;
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  r.T = lo;
+  r.need_eq = rank;
+  r.eq_total = inrange;
+  return r;
+}
+
+// Membership given the threshold (one wave; ties cut in slot order).  *eq_cut (written by
+// one lane) receives the page of the last key equal to T that is taken when a tie is cut.
+template <int NK>
+__device__ __forceinline__ uint64_t wsel_membership(const uint32_t (&key)[NK], const int (&page)[NK], uint64_t cand,
+                                                    uint64_t force, const SelThreshold& th, int* eq_cut) {
+  uint64_t gt = 0, eq = 0;
+#pragma unroll
+  for (int j = 0; j < NK; ++j) {
+    if ((cand >> j) & 1ull) {
+      if (th.mode == 1 || (th.mode == 2 && key[j] > th.T)) gt |= 1ull << j;
+      if (th.mode == 2 && key[j] == th.T) eq |= 1ull << j;
+    }
+  }
+  gt |= force;
+  if (th.mode != 2 || th.need_eq >= th.eq_total) return gt | eq;
+  uint64_t in = gt;
+  int run = 0;
+#pragma unroll
+  for (int j = 0; j < NK; ++j) {
+    const bool e = (eq >> j) & 1ull;
+    const uint64_t em = __ballot(e);
+    const int er = run + lanes_below(em);
+    if (e && er < th.need_eq) {
+      in |= 1ull << j;
+      if (er == th.need_eq - 1) *eq_cut = page[j];
+    }
+    run += __popcll(em);
+  }
+  return in;
+}
+
+}  // namespace prr
