@@ -105,11 +105,16 @@ struct FMergeLds {
   float acc[4][kHeadDim];
 };
 
-union FLds {
-  FScoreLds score;
-  FSelLds sel;
-  FAttnLds attn;
-  FMergeLds merge;
+struct FLds {
+  union {
+    FScoreLds score;
+    FSelLds sel;
+    FAttnLds attn;
+    FMergeLds merge;
+  };
+  // Values polled by one wave and read by the whole workgroup: hundreds of waves
+  // polling the same word would queue at its memory channel and slow every hand-off.
+  uint32_t bc[2 + 2 * kFW];
 };
 
 // ------------------------------------------------------------------------ score
@@ -573,19 +578,39 @@ struct FCand {
   int total, nforced;
 };
 
+// POLL_ALL: every thread polls (the count and the first entries of one score workgroup
+// per eight threads, the fastest hand-off); otherwise one wave polls the counts and the
+// entries are loaded afterwards (for workgroups that are not on the critical path, so
+// that they do not slow the others' polls down).
+template <bool POLL_ALL>
 __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, int h, int which, int* off, int* tot, uint32_t* lk,
                                            uint32_t* lp) {
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int nS = a.n_score;
   const int wg = t >> 3, sub = t & 7;
   const bool mine = wg < nS;
-  const size_t rec = ((size_t)which * a.num_kv_heads + h) * nS + min(wg, nS - 1);
+  const size_t rec0 = ((size_t)which * a.num_kv_heads + h) * nS;
+  const size_t rec = rec0 + min(wg, nS - 1);
   const uint64_t* ck = a.t_candk + rec * kFScorePages;
   const uint64_t* cp = a.t_candp + rec * kFScorePages;
   // the count and the first two entries are polled together until all needed are there
   uint64_t vc = 0, k0 = 0, p0 = 0, k1 = 0, p1 = 0;
   uint32_t c = 0u;
-  for (int it = 0; mine && it < kFSpin; ++it) {
+  if (!POLL_ALL && w == 0) {
+    const bool m1 = lane < nS;
+    const uint64_t* pc = &a.t_cnt[rec0 + min(lane, nS - 1)];
+    for (int it = 0; it < kFSpin; ++it) {
+      vc = get_tag(pc);
+      if (__ballot(m1 && !tag_is(vc, a.epoch)) == 0ull) break;
+      __builtin_amdgcn_s_sleep(2);
+      if (it == kFSpin - 1 && lane == 0) atomicOr(a.flags, kFlagSpinTimeout);
+    }
+    if (m1) {
+      off[kWave + lane] = (int)((uint32_t)vc & 0xffffu);
+      off[2 * kWave + lane] = (int)((uint32_t)vc >> 16);
+    }
+  }
+  for (int it = 0; POLL_ALL && mine && it < kFSpin; ++it) {
     vc = get_tag(&a.t_cnt[rec]);
     k0 = get_tag(&ck[sub]);
     p0 = get_tag(&cp[sub]);
@@ -601,12 +626,12 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, int h, int whic
     __builtin_amdgcn_s_sleep(2);
     if (it == kFSpin - 1) atomicOr(a.flags, kFlagSpinTimeout);
   }
-  const int nc = (int)(c & 0xffffu);
-  if (mine && sub == 0) {
-    off[kWave + wg] = nc;
+  if (POLL_ALL && mine && sub == 0) {
+    off[kWave + wg] = (int)(c & 0xffffu);
     off[2 * kWave + wg] = (int)(c >> 16);
   }
   __syncthreads();
+  const int nc = mine ? off[kWave + wg] : 0;
   if (w == 0) {
     const int cw = lane < nS ? off[kWave + lane] : 0;
     const int fw = lane < nS ? off[2 * kWave + lane] : 0;
@@ -624,15 +649,17 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, int h, int whic
   r.nforced = tot[1];
   if (mine && r.total <= kCandMax) {
     const int o = off[wg];
-    if (sub < nc) {
-      lk[o + sub] = tagged(k0, &ck[sub], a.epoch, a.flags);
-      lp[o + sub] = tagged(p0, &cp[sub], a.epoch, a.flags);
+    if (POLL_ALL) {
+      if (sub < nc) {
+        lk[o + sub] = tagged(k0, &ck[sub], a.epoch, a.flags);
+        lp[o + sub] = tagged(p0, &cp[sub], a.epoch, a.flags);
+      }
+      if (sub + 8 < nc) {
+        lk[o + sub + 8] = tagged(k1, &ck[sub + 8], a.epoch, a.flags);
+        lp[o + sub + 8] = tagged(p1, &cp[sub + 8], a.epoch, a.flags);
+      }
     }
-    if (sub + 8 < nc) {
-      lk[o + sub + 8] = tagged(k1, &ck[sub + 8], a.epoch, a.flags);
-      lp[o + sub + 8] = tagged(p1, &cp[sub + 8], a.epoch, a.flags);
-    }
-    for (int slot = sub + 16; slot < nc; slot += 8) {
+    for (int slot = sub + (POLL_ALL ? 16 : 0); slot < nc; slot += 8) {
       lk[o + slot] = wait_tag(&ck[slot], a.epoch, a.flags);
       lp[o + slot] = wait_tag(&cp[slot], a.epoch, a.flags);
     }
@@ -859,23 +886,34 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, int h, int tot
   uint32_t key[NK];
   int page[NK];
   uint64_t cand = 0, force = 0, lateb = 0, inP = 0;
+  // unconditional LDS loads (slots past the list read stale words and are masked), so
+  // that they issue back to back instead of one branch at a time
+  static_assert(kCandWave <= kCandMax, "one-wave slots lie inside the LDS list");
+  uint32_t pv[NK];
 #pragma unroll
   for (int j = 0; j < NK; ++j) {
-    const int i = j * kWave + lane;
-    key[j] = 0u;
-    page[j] = 0;
-    if (i < total) {
-      key[j] = L.ck[i];
-      const uint32_t pv = L.cpg[i];
-      page[j] = (int)(pv & 0x3fffffffu);
-      if (pv >> 31) force |= 1ull << j;
-      else cand |= 1ull << j;
-      if ((pv >> 30) & 1u) lateb |= 1ull << j;
-      if (prr && bit_of(L.bitP, page[j])) inP |= 1ull << j;
-    }
+    key[j] = L.ck[j * kWave + lane];
+    pv[j] = L.cpg[j * kWave + lane];
+  }
+  uint32_t pw[NK];
+#pragma unroll
+  for (int j = 0; j < NK; ++j) {
+    const bool v = j * kWave + lane < total;
+    key[j] = v ? key[j] : 0u;
+    pv[j] = v ? pv[j] : 0u;
+    page[j] = (int)(pv[j] & 0x3fffffffu);
+    pw[j] = prr ? L.bitP[(page[j] >> 5) & (PRR_MAX_PAGES_DEV / 32 - 1)] : 0u;
+  }
+#pragma unroll
+  for (int j = 0; j < NK; ++j) {
+    const bool v = j * kWave + lane < total;
+    if (v && (pv[j] >> 31)) force |= 1ull << j;
+    if (v && !(pv[j] >> 31)) cand |= 1ull << j;
+    if (v && ((pv[j] >> 30) & 1u)) lateb |= 1ull << j;
+    if (v && ((pw[j] >> (page[j] & 31)) & 1u)) inP |= 1ull << j;
   }
   if (w == 0) {
-    const SelThreshold th = wsel_threshold<NK>(key, cand, a.kextra_a, L.ws[0]);
+    const SelThreshold th = wsel_threshold<NK>(key, cand, a.kextra_a, L.ws[0], true);
     const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
     uint64_t* thr = a.t_thr + 2 * (size_t)h;
     if (prr && early && lane == 0) {
@@ -948,7 +986,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, int h, int tot
   } else if (w == 1 || (w == 2 && a.late)) {
     // the next step's lower bounds: rank 3|A| (candidates of A) and 1.5|A| (late pages)
     const int k = w == 1 ? 3 * a.kextra_a : (3 * a.kextra_a) / 2;
-    const SelThreshold th = wsel_threshold<NK>(key, cand, max(k, 1), L.ws[w]);
+    const SelThreshold th = wsel_threshold<NK>(key, cand, max(k, 1), L.ws[w], true);
     if (lane == 0 && th.mode == 2 && qn > 0.0f) a.win[4 * h + (w == 1 ? 0 : 2)] = __float_as_uint(key_value(th.T) / qn);
   }
   __syncthreads();
@@ -980,6 +1018,8 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U
     L.eq_cut = kEqAll;
     L.npv = 0;
   }
+  // the bins of the one-wave selects, cleared while the candidates are awaited
+  if (t < 3 * kWave) wsel_clear(L.ws[t / kWave]);
   __syncthreads();
   if (t == 0 && a.n_forced > 0) {
 #pragma unroll
@@ -1011,7 +1051,7 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U
   nv = block_sum<kFT>(nv, L.cnt[1]);  // P^t holds no duplicates
   if (t == 0) L.npv = nv;
   const float qn = qbar_finish(a, qv, L.qb);
-  const FCand c = cand_load(a, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  const FCand c = cand_load<true>(a, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
   if (a.kextra_a <= c.total - c.nforced && c.total <= kCandWave) {
     select_wave<BF16, PS>(a, h, c.total, qn, U);
   } else if (a.kextra_a <= c.total - c.nforced && c.total <= kCandMax) {
@@ -1072,7 +1112,7 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, int h, FLds& 
   float qv[16];
   qbar_load<BF16>(a, h, qv);
   const float qn = qbar_finish(a, qv, L.qb);
-  const FCand c = cand_load(a, h, 1, L.off, L.tot, L.ck, L.cpg);
+  const FCand c = cand_load<true>(a, h, 1, L.off, L.tot, L.ck, L.cpg);
   if (a.kextra_p <= c.total - c.nforced && c.total <= kCandMax) {
     uint32_t key[4];
     int page[4];
@@ -1092,20 +1132,36 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, int h, FLds& 
 
 // Membership of this wave's pages in A, from their scores and the published threshold
 // (all loads issued together, then waited for); returns `keep` without the pages not in A.
+// Called by every wave of the workgroup (it holds a barrier).
 template <int NPW>
-__device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, int h, const int (&pg)[NPW], uint32_t keep) {
-  if (!keep) return keep;
+__device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, int h, const int (&pg)[NPW], uint32_t keep,
+                                              uint32_t* bc) {
   const uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
-  const uint64_t* thr = a.t_thr + 2 * (size_t)h;
   uint64_t vs[NPW];
 #pragma unroll
-  for (int k = 0; k < NPW; ++k) vs[k] = get_tag(&ts[max(pg[k], 0)]);
-  const uint64_t v0 = get_tag(thr), v1 = get_tag(thr + 1);
+  for (int k = 0; k < NPW; ++k) vs[k] = keep ? get_tag(&ts[max(pg[k], 0)]) : 0ull;
+  if (threadIdx.x < kWave) {
+    const uint64_t* thr = a.t_thr + 2 * (size_t)h;
+    uint64_t v0 = 0, v1 = 0;
+    for (int it = 0; it < kFSpin; ++it) {
+      v0 = get_tag(thr);
+      v1 = get_tag(thr + 1);
+      if (tag_is(v0, a.epoch) && tag_is(v1, a.epoch)) break;
+      __builtin_amdgcn_s_sleep(2);
+      if (it == kFSpin - 1 && threadIdx.x == 0) atomicOr(a.flags, kFlagSpinTimeout);
+    }
+    if (threadIdx.x == 0) {
+      bc[0] = (uint32_t)v0;
+      bc[1] = (uint32_t)v1;
+    }
+  }
+  __syncthreads();
+  if (!keep) return keep;
   uint32_t sc[NPW];
 #pragma unroll
   for (int k = 0; k < NPW; ++k) sc[k] = pg[k] >= 0 ? tagged(vs[k], &ts[pg[k]], a.epoch, a.flags) : 0u;
-  const uint32_t T = tagged(v0, thr, a.epoch, a.flags);
-  const uint32_t me = tagged(v1, thr + 1, a.epoch, a.flags);
+  const uint32_t T = bc[0];
+  const uint32_t me = bc[1];
   const int mode = (int)(me & 3u), eq_cut = (int)(me >> 2);
 #pragma unroll
   for (int k = 0; k < NPW; ++k) {
@@ -1142,7 +1198,7 @@ __device__ __forceinline__ void role_spec(const FusedLaunch& a, int h, int c, FL
   }
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
-  if (a.mode != PRR_KEEP_WASTED) keep = keep_in_A<NPW>(a, h, pg, keep);
+  if (a.mode != PRR_KEEP_WASTED) keep = keep_in_A<NPW>(a, h, pg, keep, U.bc);
   fold_publish<NPW>(a, h, c, st, keep, U.attn);
 }
 
@@ -1171,7 +1227,7 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, int h, int u, FL
 #pragma unroll
   for (int r = 0; r < PRR_MAX_CAP_DEV / kFT; ++r)
     if (pe[r] >= 0 && pe[r] < n) atomicOr(&L.bitP[pe[r] >> 5], 1u << (pe[r] & 31));
-  const FCand c = cand_load(a, h, 2, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  const FCand c = cand_load<false>(a, h, 2, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
   const int cover = min(c.total, a.n_late * a.chunk);
   const int start = u * a.chunk;
   if (start >= cover) return;
@@ -1192,7 +1248,7 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, int h, int u, FL
   __syncthreads();  // the list is read before the attention reuses the LDS
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
-  keep = keep_in_A<NPW>(a, h, pg, keep);
+  keep = keep_in_A<NPW>(a, h, pg, keep, U.bc);
   fold_publish<NPW>(a, h, a.n_spec + a.n_miss + u, st, keep, U.attn);
 }
 
@@ -1204,24 +1260,29 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, int h, int u, FL
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   u32x4_t qf[4];
   load_q(a, h, qf);
+  static_assert(1 + kFW * NPW <= 2 + 2 * kFW, "broadcast area");
   const uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
-  uint64_t ve[NPW];
-  uint32_t mv = 0u;
-  for (int it = 0; it < kFSpin; ++it) {
-    const uint64_t vm = get_tag(a.t_mcnt + h);
-#pragma unroll
-    for (int k = 0; k < NPW; ++k) ve[k] = get_tag(&ml[min(start + w + kFW * k, a.cap - 1)]);
-    if (tag_is(vm, a.epoch)) {
-      mv = (uint32_t)vm;
-      const int nm = (mv & kSelfMiss) ? 0 : (int)(mv & kCountMask);
-      bool ok = true;
-#pragma unroll
-      for (int k = 0; k < NPW; ++k) ok = ok && (start + w + kFW * k >= nm || tag_is(ve[k], a.epoch));
-      if (ok) break;
+  if (w == 0) {
+    // lane l < kFW * NPW polls entry start + l (page k of wave w is entry w + kFW k)
+    const int lane = lane_id();
+    const int i = start + lane;
+    uint64_t vm = 0, ve = 0;
+    for (int it = 0; it < kFSpin; ++it) {
+      vm = get_tag(a.t_mcnt + h);
+      ve = get_tag(&ml[min(i, a.cap - 1)]);
+      if (tag_is(vm, a.epoch)) {
+        const uint32_t mv = (uint32_t)vm;
+        const int nm = (mv & kSelfMiss) ? 0 : (int)(mv & kCountMask);
+        if (__ballot(lane < kFW * NPW && i < nm && !tag_is(ve, a.epoch)) == 0ull) break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+      if (it == kFSpin - 1 && lane == 0) atomicOr(a.flags, kFlagSpinTimeout);
     }
-    __builtin_amdgcn_s_sleep(2);
-    if (it == kFSpin - 1 && lane_id() == 0) atomicOr(a.flags, kFlagSpinTimeout);
+    if (lane == 0) U.bc[0] = (uint32_t)vm;
+    if (lane < kFW * NPW) U.bc[1 + lane] = (uint32_t)ve;
   }
+  __syncthreads();
+  const uint32_t mv = U.bc[0];
   if (mv & kSelfMiss) return;
   const int nM = (int)(mv & kCountMask);
   if (start >= nM) return;
@@ -1231,7 +1292,7 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, int h, int u, FL
 #pragma unroll
   for (int k = 0; k < NPW; ++k) {
     const int i = w + kFW * k;
-    int p = i < cnt ? (int)tagged(ve[k], &ml[start + i], a.epoch, a.flags) : -1;
+    int p = i < cnt ? (int)U.bc[1 + i] : -1;
     p = __builtin_amdgcn_readfirstlane(p);
     if (i < cnt && (p < 0 || p >= a.num_pages)) {  // only after a timed-out wait
       if (lane_id() == 0) atomicOr(a.flags, kFlagBadListEntry);
@@ -1248,17 +1309,32 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, int h, int u, FL
 // ------------------------------------------------------------------------ merge
 
 template <bool BF16>
-__device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, FMergeLds& L) {
+__device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, FMergeLds& L, uint32_t* bc) {
   const float kNegInf = -__builtin_inff();
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int G = a.group, C = a.chunk;
   int nspec = 0;
   if (a.schedule == 1) nspec = (min(max(a.pred_cur_count[h], 0), a.cap) + C - 1) / C;
-  const uint32_t mv = wait_tag(a.t_mcnt + h, a.epoch, a.flags);
+  if (t < kWave) {
+    uint64_t v0 = 0, v1 = 0;
+    for (int it = 0; it < kFSpin; ++it) {
+      v0 = get_tag(a.t_mcnt + h);
+      v1 = a.late ? get_tag(a.t_lcnt + h) : ((uint64_t)a.epoch << 32);
+      if (tag_is(v0, a.epoch) && tag_is(v1, a.epoch)) break;
+      __builtin_amdgcn_s_sleep(2);
+      if (it == kFSpin - 1 && t == 0) atomicOr(a.flags, kFlagSpinTimeout);
+    }
+    if (t == 0) {
+      bc[0] = (uint32_t)v0;
+      bc[1] = (uint32_t)v1;
+    }
+  }
+  __syncthreads();
+  const uint32_t mv = bc[0];
   const int nM = (int)(mv & kCountMask);
   const int nmiss = (mv & kSelfMiss) ? 1 : (nM + C - 1) / C;
   if (mv & kDropSpec) nspec = 0;
-  const int nlate = a.late ? ((int)wait_tag(a.t_lcnt + h, a.epoch, a.flags) + C - 1) / C : 0;
+  const int nlate = a.late ? ((int)bc[1] + C - 1) / C : 0;
   const int total = nspec + nmiss + nlate;
   // state i lives in slot i (speculation chunks), n_spec + (i - nspec) (missed chunks) or
   // n_spec + n_miss + (i - nspec - nmiss) (late-speculation chunks)
@@ -1381,7 +1457,7 @@ __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
     return;
   }
   b -= H * a.n_miss;
-  if (b < H * a.group) role_merge<BF16>(a, b / a.group, b % a.group, U.merge);
+  if (b < H * a.group) role_merge<BF16>(a, b / a.group, b % a.group, U.merge, U.bc);
 }
 
 template <typename K>

@@ -304,9 +304,18 @@ struct WSelLds {
   uint32_t small[kSel2Small];
 };
 
+// The 2048 bins of S, cleared by one wave with contiguous stores.
+__device__ __forceinline__ void wsel_clear(WSelLds& S) {
+  uint4* hb = reinterpret_cast<uint4*>(S.hist);
+#pragma unroll
+  for (int v = 0; v < kSel2Bins / 4 / kWave; ++v) hb[v * kWave + lane_id()] = make_uint4(0, 0, 0, 0);
+}
+
+// precleared: the bins of S are zero on entry (cleared while the caller waited for the
+// keys), so the first pass starts with the atomics.
 template <int NK>
 __device__ __forceinline__ SelThreshold wsel_threshold(const uint32_t (&key)[NK], uint64_t cand, int kextra,
-                                                       WSelLds& S) {
+                                                       WSelLds& S, bool precleared = false) {
   const int lane = lane_id();
   int cnt = __popcll(cand);
   uint32_t lo = 0xffffffffu, hi = 0u;
@@ -342,12 +351,13 @@ __device__ __forceinline__ SelThreshold wsel_threshold(const uint32_t (&key)[NK]
     }
     const int bits = 32 - __clz(range);
     const int shift = bits > kSel2Log2Bins ? bits - kSel2Log2Bins : 0;
-    // this lane's 32 bins [2048 - 32(lane+1), 2048 - 32 lane) are cleared, then counted
+    if (pass > 0 || !precleared) {
+      wsel_clear(S);
+      __builtin_amdgcn_wave_barrier();
+    }
+    // lane l sums its 32 bins [2048 - 32(l+1), 2048 - 32 l) after the counting
     const int base = kSel2Bins - 32 * (lane + 1);
-    uint4* hb = reinterpret_cast<uint4*>(S.hist + base);
-#pragma unroll
-    for (int v = 0; v < 8; ++v) hb[v] = make_uint4(0, 0, 0, 0);
-    __builtin_amdgcn_wave_barrier();
+    const uint4* hb = reinterpret_cast<const uint4*>(S.hist + base);
 #pragma unroll
     for (int j = 0; j < NK; ++j)
       if (((cand >> j) & 1ull) && key[j] >= lo && key[j] <= hi) atomicAdd(&S.hist[(key[j] - lo) >> shift], 1u);
@@ -379,6 +389,34 @@ __device__ __forceinline__ SelThreshold wsel_threshold(const uint32_t (&key)[NK]
       r.need_eq = rank;
       r.eq_total = cbin;
       return r;
+    }
+    if (cbin <= 4) {
+      // the rank-th largest key of the bin by repeated maxima (cheaper than a compaction
+      // for the usual bin of one or two keys); each round takes every key equal to the
+      // maximum, so at most cbin rounds
+      uint32_t ub = hi;
+      for (int round = 0; round < cbin; ++round) {
+        uint32_t m = 0u;
+#pragma unroll
+        for (int j = 0; j < NK; ++j) {
+          const bool in = ((cand >> j) & 1ull) && key[j] >= lo && key[j] <= ub;
+          m = in ? max(m, key[j] - lo + 1u) : m;
+        }
+        m = wave_umax(m);  // 1 + (maximum - lo); nonzero while keys remain below ub
+        const uint32_t km = lo + m - 1u;
+        int c = 0;
+#pragma unroll
+        for (int j = 0; j < NK; ++j) c += (((cand >> j) & 1ull) && key[j] == km) ? 1 : 0;
+        c = wave_isum(c);
+        if (rank <= c || m == 0u || km == lo) {
+          r.T = km;
+          r.need_eq = rank;
+          r.eq_total = c;
+          return r;
+        }
+        rank -= c;
+        ub = km - 1u;
+      }
     }
     if (cbin <= kSel2Small) {
       // the keys of this bin, compacted in slot order, ranked by broadcast
