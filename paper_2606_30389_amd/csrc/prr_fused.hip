@@ -34,14 +34,14 @@ constexpr int kFT = 512;
 constexpr int kFW = kFT / kWave;
 constexpr int kFScorePages = 128;
 constexpr int kFSpin = 1 << 20;
-constexpr int kFPart = kHeadDim + 2;  // o[128], m, l of one query head
+constexpr int kMaxParts = 3 * PRR_MAX_CAP_DEV;  // partial states per KV head (chunk 1)
 constexpr uint32_t kSelfMiss = 0x80000000u;  // missed-list count flags: attended by the select workgroup
 constexpr uint32_t kDropSpec = 0x40000000u;  //   the speculation is discarded (recompute on a miss)
 constexpr uint32_t kCountMask = 0x3fffffffu;
 constexpr int kFOPad = kHeadDim + 4;
 constexpr int kEqAll = 16383;  // eq_cut meaning "every key equal to T is taken"
 constexpr int kCandMax = 4 * kFT;     // candidates ranked by one workgroup (4 per thread)
-constexpr int kCandWave = 16 * kWave;  // candidates ranked by one wave (16 per lane)
+constexpr int kCandWave = 12 * kWave;  // candidates ranked by one wave (12 per lane)
 
 __device__ __forceinline__ void put_tag(uint64_t* p, uint32_t v, uint32_t epoch) {
   __hip_atomic_store(p, ((uint64_t)epoch << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -99,10 +99,10 @@ struct FAttnLds {
 };
 
 struct FMergeLds {
-  float w[2 * PRR_MAX_CAP_DEV];  // l, then the weight, of each state
-  float m[2 * PRR_MAX_CAP_DEV];
+  float w[kMaxParts];  // l, then the weight, of each state
+  float m[kMaxParts];
   float red[2][kFW];
-  float acc[4][kHeadDim];
+  float acc[kFW][kHeadDim];
 };
 
 struct FLds {
@@ -522,6 +522,7 @@ __device__ __forceinline__ void fold_publish(const FusedLaunch& a, int h, int sl
   __syncthreads();
   const int hh = t >> 5, c0 = (t & 31) * 4;
   const int G = a.group;
+  float mrow = kNegInf, lrow = 0.0f;
   if (hh < G) {
     float mw[kFW], fw[kFW];
     float ms = kNegInf;
@@ -547,13 +548,24 @@ __device__ __forceinline__ void fold_publish(const FusedLaunch& a, int h, int sl
       o[2] += x.z * fw[ww];
       o[3] += x.w * fw[ww];
     }
-    uint64_t* dst = a.t_part + (((size_t)h * a.nparts + slot) * G + hh) * kFPart;
+    uint64_t* dst = reinterpret_cast<uint64_t*>(a.part_o + (((size_t)h * a.nparts + slot) * G + hh) * kHeadDim + c0);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) put_tag(dst + c0 + e, __float_as_uint(o[e] * inv), a.epoch);
-    if ((t & 31) == 0) {
-      put_tag(dst + kHeadDim, __float_as_uint(lsum > 0.0f ? ms : kNegInf), a.epoch);
-      put_tag(dst + kHeadDim + 1, __float_as_uint(lsum), a.epoch);
+    for (int e = 0; e < 2; ++e) {
+      const uint64_t v = (uint64_t)__float_as_uint(o[2 * e] * inv) | ((uint64_t)__float_as_uint(o[2 * e + 1] * inv) << 32);
+      __hip_atomic_store(dst + e, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    mrow = lsum > 0.0f ? ms : kNegInf;
+    lrow = lsum;
+  }
+  // The tagged (m, l) of a state are stored only after every output value of it has
+  // completed (device-coherent stores are acknowledged once visible to the whole
+  // device), so a reader that sees them current reads a complete, untagged output.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (hh < G && (t & 31) == 0) {
+    uint64_t* ml = a.t_part + (((size_t)h * a.nparts + slot) * G + hh) * 2;
+    put_tag(ml, __float_as_uint(mrow), a.epoch);
+    put_tag(ml + 1, __float_as_uint(lrow), a.epoch);
   }
 }
 
@@ -728,7 +740,7 @@ __device__ __forceinline__ void full_gather(const FusedLaunch& a, const uint64_t
   }
 }
 
-// Lower bound of the next step's candidates: the score of rank `k` (3 |A| for the
+// Lower bound of the next step's candidates: the score of rank `k` (2.5 |A| for the
 // candidates, 1.5 |A| for late speculation) among this step's candidates, kept as a
 // ratio to |q-bar|_1 (unchanged when fewer candidates exist and `keep` is set; -inf,
 // i.e. every page, after a fallback that found fewer).
@@ -870,7 +882,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
     fold_publish<1>(a, h, a.n_spec, st, 1u, U.attn);
   }
-  update_window<J>(a, a.win + 4 * h, qn, key, cand, 3 * a.kextra_a, keep_window, U.sel.sel);
+  update_window<J>(a, a.win + 4 * h, qn, key, cand, (5 * a.kextra_a) / 2, keep_window, U.sel.sel);
   if (a.late) update_window<J>(a, a.win + 4 * h + 2, qn, key, cand, (3 * a.kextra_a) / 2, true, U.sel.sel);
 }
 
@@ -984,8 +996,8 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, int h, int tot
       if (a.wasted_count) a.wasted_count[h] = prr ? L.npv - nPA : 0;
     }
   } else if (w == 1 || (w == 2 && a.late)) {
-    // the next step's lower bounds: rank 3|A| (candidates of A) and 1.5|A| (late pages)
-    const int k = w == 1 ? 3 * a.kextra_a : (3 * a.kextra_a) / 2;
+    // the next step's lower bounds: rank 2.5|A| (candidates of A) and 1.5|A| (late pages)
+    const int k = w == 1 ? (5 * a.kextra_a) / 2 : (3 * a.kextra_a) / 2;
     const SelThreshold th = wsel_threshold<NK>(key, cand, max(k, 1), L.ws[w], true);
     if (lane == 0 && th.mode == 2 && qn > 0.0f) a.win[4 * h + (w == 1 ? 0 : 2)] = __float_as_uint(key_value(th.T) / qn);
   }
@@ -1338,25 +1350,20 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, 
   const int total = nspec + nmiss + nlate;
   // state i lives in slot i (speculation chunks), n_spec + (i - nspec) (missed chunks) or
   // n_spec + n_miss + (i - nspec - nmiss) (late-speculation chunks)
-  const uint64_t* part = a.t_part + ((size_t)h * a.nparts * G + qn) * kFPart;
-  const size_t sstride = (size_t)G * kFPart;
+  const uint64_t* pml = a.t_part + ((size_t)h * a.nparts * G + qn) * 2;
+  const float* po = a.part_o + ((size_t)h * a.nparts * G + qn) * kHeadDim;
   const int gap1 = a.n_spec - nspec, gap2 = a.n_spec + a.n_miss - nspec - nmiss;
-#define PRR_ELEM(i, idx) \
-  (part + (size_t)((i) < nspec ? (i) : ((i) < nspec + nmiss ? (i) + gap1 : (i) + gap2)) * sstride + (idx))
+#define PRR_SLOT(i) ((size_t)((i) < nspec ? (i) : ((i) < nspec + nmiss ? (i) + gap1 : (i) + gap2)) * G)
 
-  // Only the (m, l) of every state are polled (threads t, t+512, ..): polling the output
-  // values themselves from every thread of every merge workgroup would flood the memory
-  // system while the states are being computed.  The output values are loaded once
-  // every (m, l) is there.
-  const int c = t & (kHeadDim - 1), g = t >> 7;
-  constexpr int kB = 16;
-  uint64_t ov[kB];
+  // Only the (m, l) of every state are polled (threads t, t+512, ..); the output values
+  // of a state are complete once its (m, l) are current.
   float mt = kNegInf;
   for (int i = t; i < total; i += kFT) {
     uint64_t vm = 0, vl = 0;
+    const uint64_t* p = pml + PRR_SLOT(i) * 2;
     for (int it = 0; it < kFSpin; ++it) {
-      vm = get_tag(PRR_ELEM(i, kHeadDim));
-      vl = get_tag(PRR_ELEM(i, kHeadDim + 1));
+      vm = get_tag(p);
+      vl = get_tag(p + 1);
       if (tag_is(vm, a.epoch) && tag_is(vl, a.epoch)) break;
       __builtin_amdgcn_s_sleep(2);
       if (it == kFSpin - 1) atomicOr(a.flags, kFlagSpinTimeout);
@@ -1386,23 +1393,33 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, 
 #pragma unroll
   for (int i = 0; i < kFW; ++i) Lsum += L.red[1][i];
 
-  float acc = 0.0f;
-  for (int b0 = 0; b0 < total; b0 += 4 * kB) {
+  // wave w sums states w, w + 8, ..; lane l columns 2l and 2l + 1 (all loads of a batch
+  // are issued before any is used; indices past the last state repeat it with weight 0)
+  constexpr int kB = 8;
+  float ax = 0.0f, ay = 0.0f;
+  for (int b0 = 0; b0 < total; b0 += kFW * kB) {
+    uint64_t ov[kB];
 #pragma unroll
     for (int r = 0; r < kB; ++r) {
-      const int i = b0 + g + 4 * r;
-      ov[r] = i < total ? get_tag(PRR_ELEM(i, c)) : 0ull;
+      const int i = min(b0 + w + kFW * r, total - 1);
+      ov[r] = __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<float*>(po + PRR_SLOT(i) * kHeadDim)) + lane,
+                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 #pragma unroll
     for (int r = 0; r < kB; ++r) {
-      const int i = b0 + g + 4 * r;
-      if (i < total) acc += L.w[i] * __uint_as_float(tagged(ov[r], PRR_ELEM(i, c), a.epoch, a.flags));
+      const int i = b0 + w + kFW * r;
+      const float wi = i < total ? L.w[i] : 0.0f;
+      ax += wi * __uint_as_float((uint32_t)ov[r]);
+      ay += wi * __uint_as_float((uint32_t)(ov[r] >> 32));
     }
   }
-  L.acc[g][c] = acc;
+  *reinterpret_cast<float2*>(&L.acc[w][2 * lane]) = make_float2(ax, ay);
   __syncthreads();
-  if (g == 0) {
-    const float sum = (L.acc[0][c] + L.acc[1][c]) + (L.acc[2][c] + L.acc[3][c]);
+  if (t < kHeadDim) {
+    const int c = t;
+    float sum = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < kFW; ++ww) sum += L.acc[ww][c];
     const float o = Lsum > 0.0f ? sum / Lsum : 0.0f;
     const size_t row = (size_t)h * G + qn;
     a.out_o32[row * kHeadDim + c] = o;
@@ -1412,7 +1429,7 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, 
       a.out_l[row] = Lsum;
     }
   }
-#undef PRR_ELEM
+#undef PRR_SLOT
 }
 
 // ------------------------------------------------------------------------ kernel

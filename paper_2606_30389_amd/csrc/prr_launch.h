@@ -114,7 +114,8 @@ struct FusedLaunch {
   uint64_t* t_thr;    // [Hkv][2] tagged threshold of A
   uint64_t* t_mcnt;   // [Hkv] tagged count of the missed list (bit 31: attended by the select workgroup)
   uint64_t* t_mlist;  // [Hkv][cap] tagged missed pages
-  uint64_t* t_part;   // [Hkv][nparts][G][130] tagged partial states
+  uint64_t* t_part;   // [Hkv][nparts][G][2] tagged (m, l) of the partial states
+  float* part_o;      // [Hkv][nparts][G][128] their outputs (complete before (m, l) are stored)
   uint64_t* t_cnt;    // [3][Hkv][n_score] tagged candidate counts: A, P^{t+1}, late speculation
   uint64_t* t_candk;  // [3][Hkv][n_score][128] tagged candidate keys
   uint64_t* t_candp;  // [3][Hkv][n_score][128] tagged candidate pages (bit 31: forced, bit 30: late)
