@@ -253,7 +253,7 @@ typedef struct {
   int32_t p_select;            /* |P| budget (delta |A|) */
   int32_t cap;
   int32_t chunk_pages;
-  int32_t mode;                /* PRR_EXACT_SELECTED | PRR_KEEP_WASTED */
+  int32_t mode;                /* PRR_EXACT_SELECTED | PRR_KEEP_WASTED | PRR_RECOMPUTE_ON_MISS (fused) */
   int32_t forced_in_budget;
   int32_t n_forced;
   const int32_t* forced;       /* host [n_forced] */
