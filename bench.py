@@ -259,7 +259,7 @@ def main():
                          "S2 (reuse + repair) and S3 (EMA + repair) with the fused PRR schedule")
     ap.add_argument("--chunk", type=int, default=None, help="pages per speculation chunk (default 8, 4 for 64-token pages)")
     ap.add_argument("--delta", type=float, default=1.0, help="|P| / |A| (speculation budget)")
-    ap.add_argument("--schedules", default="fused_prr,fused_prr_late,fused_serial,two_stream,serial")
+    ap.add_argument("--schedules", default="fused_prr,fused_prr_late,fused_serial,fused_prr_late_graph,two_stream,serial")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--kernel-reps", type=int, default=2, help="tokens per kernel-timing pass (separate kernels)")
     ap.add_argument("--workers", type=int, default=16, help="input-generation processes (0 = in-process)")
@@ -296,7 +296,7 @@ def main():
     schedules = [x for x in args.schedules.split(",") if x]
     sched_id = {"fused_prr": L.PRR_SCHED_FUSED_PRR, "fused_prr_late": L.PRR_SCHED_FUSED_PRR,
                 "fused_serial": L.PRR_SCHED_FUSED_SERIAL, "two_stream": L.PRR_SCHED_TWO_STREAM,
-                "serial": L.PRR_SCHED_SERIAL}
+                "serial": L.PRR_SCHED_SERIAL, "fused_prr_late_graph": L.PRR_SCHED_FUSED_PRR}
     n_abl = (3 if args.ablation else 0) + (2 if args.calibrate > 1 else 0)
     total_tokens = 2 + max(2, args.warmup) + 2 * (len(schedules) + n_abl) * (args.steps + 2) + \
         n_abl * (1 + max(2, args.warmup)) + args.kernel_reps + 8
@@ -330,12 +330,15 @@ def main():
     stack = R.DecodeStack(layers, [q_static[l] for l in range(n_layers)], dev)
     tok = [0]
 
-    def run(n, schedule, measure_hits=False):
+    def run(n, schedule, measure_hits=False, tag=None):
         hits = []
         for _ in range(n):
             with torch.cuda.stream(s):
                 q_static.copy_(q_all[tok[0]])
-            stack.step(schedule, s, p)
+            if tag is None:
+                stack.step(schedule, s, p)
+            else:
+                stack.replay(schedule, s, tag)
             tok[0] += 1
             if measure_hits:
                 torch.cuda.synchronize()
@@ -343,12 +346,12 @@ def main():
                 hits.append(1.0 - miss / (n_layers * cfg.num_kv_heads * cfg.selected_count))
         return hits
 
-    def timed(n, schedule):
+    def timed(n, schedule, tag=None):
         torch.cuda.synchronize()
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s.wait_stream(torch.cuda.current_stream())
         start.record(s)
-        run(n, schedule)
+        run(n, schedule, tag=tag)
         end.record(s)
         torch.cuda.synchronize()
         return start.elapsed_time(end) / n  # ms per token
@@ -360,9 +363,17 @@ def main():
     hits = run(max(2, args.warmup), L.PRR_SCHED_FUSED_PRR, measure_hits=True)
     ms = {}
     for name in schedules:  # warm each schedule, then two timed passes (the better one counts)
-        stack.params.late_spec = int(name == "fused_prr_late")
+        stack.params.late_spec = int(name.startswith("fused_prr_late"))
         run(2, sched_id[name])
-        ms[name] = min(timed(args.steps, sched_id[name]), timed(args.steps, sched_id[name]))
+        # *_graph: the token's launches are captured as HIP graphs (one per parity of the
+        # prediction buffers) and replayed; otherwise launched directly
+        tag = None
+        if name.endswith("_graph"):
+            torch.cuda.synchronize()
+            stack.capture(sched_id[name], s, tag=name)
+            tag = name
+            run(2, sched_id[name], tag=tag)
+        ms[name] = min(timed(args.steps, sched_id[name], tag), timed(args.steps, sched_id[name], tag))
     stack.params.late_spec = 0
     ablation = None
     if args.ablation:

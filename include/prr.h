@@ -260,6 +260,10 @@ typedef struct {
   float alpha, beta, gamma;
   uint32_t epoch;              /* fused schedules: >= 1 and different from every earlier call's
                                   value on the same workspaces (e.g. the token index + 1) */
+  const uint32_t* epoch_dev;   /* fused schedules, or NULL: device word read by each launch
+                                  instead of `epoch`, for launches captured once and replayed
+                                  (HIP graphs); the caller advances it between replays with
+                                  prr_epoch_advance, under the same uniqueness rule */
   int32_t late_spec;           /* PRR_SCHED_FUSED_PRR: 1 = also speculate, as soon as this step's
                                   scores exist, over the pages just above the selection threshold
                                   that P missed (the threshold is learned across steps); the result
@@ -294,6 +298,11 @@ typedef struct {
 prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* params, const prr_layer_io* layers,
                            int32_t n_layers, int32_t parity, int32_t schedule, hipStream_t stream,
                            hipStream_t spec_stream, hipEvent_t* events);
+
+/* Advance the device epoch word of captured fused steps (prr_step_params.epoch_dev)
+ * by one, skipping 0: one single-thread launch on `stream`, so it can be captured with
+ * the steps it precedes.  Errors: PRR_ERR_INVALID_ARG for a NULL or misaligned pointer. */
+prr_status prr_epoch_advance(uint32_t* epoch_dev, hipStream_t stream);
 
 /* Online calibration of the EMA predictor (Section 4.2): for each candidate theta =
  * (alpha, beta, gamma) of `grid`, the score-weighted hit rate of Eq. (4) -- the EMA of

@@ -43,6 +43,7 @@ EXPORTED = (
     "prr_status_string", "prr_last_error", "prr_workspace_size", "prr_workspace_init",
     "prr_spec_state_floats", "prr_build_page_meta", "prr_score_topk", "prr_predict",
     "prr_spec_attn", "prr_repair", "prr_merge_states", "prr_decode_step", "prr_calibrate",
+    "prr_epoch_advance",
 )
 
 
@@ -75,7 +76,8 @@ class prr_step_params(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("num_tokens", "num_pages", "k_select", "p_select", "cap",
                                                "chunk_pages", "mode", "forced_in_budget", "n_forced")] + [
         ("forced", ctypes.POINTER(ctypes.c_int32)), ("alpha", ctypes.c_float), ("beta", ctypes.c_float),
-        ("gamma", ctypes.c_float), ("epoch", ctypes.c_uint32), ("late_spec", ctypes.c_int32)]
+        ("gamma", ctypes.c_float), ("epoch", ctypes.c_uint32), ("epoch_dev", ctypes.c_void_p),
+        ("late_spec", ctypes.c_int32)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -104,6 +106,7 @@ _SIGS = {
     "prr_decode_step": (_I, [_DIMS, ctypes.POINTER(prr_step_params), ctypes.POINTER(prr_layer_io), _I, _I, _I, _P,
                              _P, ctypes.POINTER(ctypes.c_void_p)]),
     "prr_calibrate": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _P, _P]),
+    "prr_epoch_advance": (_I, [_P, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -212,6 +215,10 @@ def prr_repair(dims, q, k_cache, v_cache, page_table, num_tokens, num_pages, sel
 def prr_merge_states(n_states, rows, d, o, m, l, out_o, out_m, out_l, stream=None):
     _check(_lib.prr_merge_states(n_states, rows, d, _ptr(o), _ptr(m), _ptr(l), _ptr(out_o), _ptr(out_m), _ptr(out_l),
                                  _stream(stream)))
+
+
+def prr_epoch_advance(epoch_dev, stream=None):
+    _check(_lib.prr_epoch_advance(_ptr(epoch_dev), _stream(stream)))
 
 
 def prr_calibrate(scores, k_select, grid, p_select=0, n_threads=0):

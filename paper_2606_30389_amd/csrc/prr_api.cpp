@@ -172,6 +172,11 @@ prr_status prr_workspace_init(void* workspace, size_t bytes, hipStream_t stream)
   return hip_status(prr::launch_fill_zero(workspace, bytes, stream), "workspace fill");
 }
 
+prr_status prr_epoch_advance(uint32_t* epoch_dev, hipStream_t stream) {
+  PRR_TRY(check_ptr(epoch_dev, "epoch_dev", 4));
+  return hip_status(prr::launch_epoch_advance(epoch_dev, stream), "epoch advance");
+}
+
 size_t prr_spec_state_floats(const prr_dims* dims, int32_t cap, int32_t chunk_pages, size_t* part_o_floats,
                              size_t* part_ml_floats, size_t* page_m_floats) {
   if (check_dims(dims) != PRR_OK || cap < 1 || cap > PRR_MAX_CAP || !chunk_ok(dims, chunk_pages)) return 0;
@@ -509,7 +514,11 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
     return fail(PRR_ERR_INVALID_ARG, "chunk_pages %d outside [1, 256 / page_size]", sp->chunk_pages);
   if (sp->mode != PRR_EXACT_SELECTED && sp->mode != PRR_KEEP_WASTED && sp->mode != PRR_RECOMPUTE_ON_MISS)
     return fail(PRR_ERR_INVALID_ARG, "mode %d", sp->mode);
-  if (sp->epoch == 0) return fail(PRR_ERR_INVALID_ARG, "epoch 0 is reserved (a zeroed workspace carries it)");
+  if (sp->epoch_dev) {
+    PRR_TRY(check_ptr(sp->epoch_dev, "epoch_dev", 4));
+  } else if (sp->epoch == 0) {
+    return fail(PRR_ERR_INVALID_ARG, "epoch 0 is reserved (a zeroed workspace carries it)");
+  }
   if (prr || prefill) {
     if (!(sp->alpha > 0.f && sp->alpha <= 1.f) || !(sp->beta > 0.f && sp->beta <= 1.f) ||
         !(sp->gamma >= 0.f && sp->gamma <= 1.f))
@@ -573,6 +582,7 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.beta = sp->beta;
   a.gamma = sp->gamma;
   a.epoch = sp->epoch;
+  a.epoch_dev = sp->epoch_dev;
   a.schedule = prr ? 1 : (prefill ? 2 : 0);
   a.mode = sp->mode;
   a.num_kv_heads = dims->num_kv_heads;

@@ -129,7 +129,7 @@ struct FLds {
 
 
 template <bool BF16>
-__device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk, FScoreLds& S) {
+__device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, int h, int blk, FScoreLds& S) {
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int G = a.group;
   const int n = a.num_pages;
@@ -245,7 +245,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
       S.sc[p - pbase] = v;
       if (p < n) {
         scores[p] = v;
-        put_tag(&ts[p], __float_as_uint(v), a.epoch);
+        put_tag(&ts[p], __float_as_uint(v), ep);
       }
     }
   }
@@ -279,21 +279,21 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
     const uint64_t ma = __ballot(ca), mfa = __ballot(ca && f), ml = __ballot(late);
     if (ca) {
       const int pos = na + lanes_below(ma);
-      put_tag(&ck_a[pos], ka, a.epoch);
-      put_tag(&cp_a[pos], (uint32_t)p | (f ? 0x80000000u : 0u) | (late ? 0x40000000u : 0u), a.epoch);
+      put_tag(&ck_a[pos], ka, ep);
+      put_tag(&cp_a[pos], (uint32_t)p | (f ? 0x80000000u : 0u) | (late ? 0x40000000u : 0u), ep);
     }
     if (late) {
       const int pos = nl + lanes_below(ml);
-      put_tag(&ck_l[pos], ka, a.epoch);
-      put_tag(&cp_l[pos], (uint32_t)p, a.epoch);
+      put_tag(&ck_l[pos], ka, ep);
+      put_tag(&cp_l[pos], (uint32_t)p, ep);
     }
     na += __popcll(ma);
     nfa += __popcll(mfa);
     nl += __popcll(ml);
   }
   if (lane == 0) {
-    put_tag(&a.t_cnt[rec_a], (uint32_t)na | ((uint32_t)nfa << 16), a.epoch);
-    if (a.late) put_tag(&a.t_cnt[rec_l], (uint32_t)nl, a.epoch);
+    put_tag(&a.t_cnt[rec_a], (uint32_t)na | ((uint32_t)nfa << 16), ep);
+    if (a.late) put_tag(&a.t_cnt[rec_l], (uint32_t)nl, ep);
   }
   if (!ema) return;
   // ... then the EMA update of Eq. (3) and the candidates of the next prediction
@@ -325,18 +325,18 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, int h, int blk,
       if (vbits) a.init_bits[(size_t)h * nwmax + (p >> 5)] = (bw[half] & ~vbits) | hbits;
     }
     const uint32_t kp = score_key(l + a.gamma * v);  // Eq. (2)
-    if (inr) put_tag(&a.t_pkey[(size_t)h * a.max_pages + p], kp, a.epoch);
+    if (inr) put_tag(&a.t_pkey[(size_t)h * a.max_pages + p], kp, ep);
     const bool cpred = inr && (f || kp >= lo_p);
     const uint64_t mp = __ballot(cpred), mfp = __ballot(cpred && f);
     if (cpred) {
       const int pos = np + lanes_below(mp);
-      put_tag(&ck_p[pos], kp, a.epoch);
-      put_tag(&cp_p[pos], (uint32_t)p | (f ? 0x80000000u : 0u), a.epoch);
+      put_tag(&ck_p[pos], kp, ep);
+      put_tag(&cp_p[pos], (uint32_t)p | (f ? 0x80000000u : 0u), ep);
     }
     np += __popcll(mp);
     nfp += __popcll(mfp);
   }
-  if (lane == 0) put_tag(&a.t_cnt[rec_p], (uint32_t)np | ((uint32_t)nfp << 16), a.epoch);
+  if (lane == 0) put_tag(&a.t_cnt[rec_p], (uint32_t)np | ((uint32_t)nfp << 16), ep);
 }
 
 // ------------------------------------------------------------------------ shared select pieces
@@ -484,7 +484,7 @@ __device__ __forceinline__ void wave_attend(const FusedLaunch& a, int h, const u
 // Fold the kept page states of every wave (keep: wave-uniform bit mask) and publish the
 // workgroup's state into partial slot `slot` of KV head h.
 template <int NPW>
-__device__ __forceinline__ void fold_publish(const FusedLaunch& a, int h, int slot, WaveStates<NPW>& st, uint32_t keep,
+__device__ __forceinline__ void fold_publish(const FusedLaunch& a, uint32_t ep, int h, int slot, WaveStates<NPW>& st, uint32_t keep,
                              FAttnLds& L) {
   const float kNegInf = -__builtin_inff();
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
@@ -564,8 +564,8 @@ __device__ __forceinline__ void fold_publish(const FusedLaunch& a, int h, int sl
   __syncthreads();
   if (hh < G && (t & 31) == 0) {
     uint64_t* ml = a.t_part + (((size_t)h * a.nparts + slot) * G + hh) * 2;
-    put_tag(ml, __float_as_uint(mrow), a.epoch);
-    put_tag(ml + 1, __float_as_uint(lrow), a.epoch);
+    put_tag(ml, __float_as_uint(mrow), ep);
+    put_tag(ml + 1, __float_as_uint(lrow), ep);
   }
 }
 
@@ -595,7 +595,7 @@ struct FCand {
 // entries are loaded afterwards (for workgroups that are not on the critical path, so
 // that they do not slow the others' polls down).
 template <bool POLL_ALL>
-__device__ __forceinline__ FCand cand_load(const FusedLaunch& a, int h, int which, int* off, int* tot, uint32_t* lk,
+__device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, int h, int which, int* off, int* tot, uint32_t* lk,
                                            uint32_t* lp) {
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int nS = a.n_score;
@@ -605,15 +605,19 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, int h, int whic
   const size_t rec = rec0 + min(wg, nS - 1);
   const uint64_t* ck = a.t_candk + rec * kFScorePages;
   const uint64_t* cp = a.t_candp + rec * kFScorePages;
-  // the count and the first two entries are polled together until all needed are there
-  uint64_t vc = 0, k0 = 0, p0 = 0, k1 = 0, p1 = 0;
+  // the count and the first four entries are polled together until all needed are there
+  // (32 per score workgroup, more than almost any list holds)
+  constexpr int kPollE = 4;
+  uint64_t vc = 0, ke[kPollE], pe[kPollE];
+#pragma unroll
+  for (int u = 0; u < kPollE; ++u) ke[u] = pe[u] = 0ull;
   uint32_t c = 0u;
   if (!POLL_ALL && w == 0) {
     const bool m1 = lane < nS;
     const uint64_t* pc = &a.t_cnt[rec0 + min(lane, nS - 1)];
     for (int it = 0; it < kFSpin; ++it) {
       vc = get_tag(pc);
-      if (__ballot(m1 && !tag_is(vc, a.epoch)) == 0ull) break;
+      if (__ballot(m1 && !tag_is(vc, ep)) == 0ull) break;
       __builtin_amdgcn_s_sleep(2);
       if (it == kFSpin - 1 && lane == 0) atomicOr(a.flags, kFlagSpinTimeout);
     }
@@ -624,16 +628,19 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, int h, int whic
   }
   for (int it = 0; POLL_ALL && mine && it < kFSpin; ++it) {
     vc = get_tag(&a.t_cnt[rec]);
-    k0 = get_tag(&ck[sub]);
-    p0 = get_tag(&cp[sub]);
-    k1 = get_tag(&ck[sub + 8]);
-    p1 = get_tag(&cp[sub + 8]);
-    if (tag_is(vc, a.epoch)) {
+#pragma unroll
+    for (int u = 0; u < kPollE; ++u) {
+      ke[u] = get_tag(&ck[sub + 8 * u]);
+      pe[u] = get_tag(&cp[sub + 8 * u]);
+    }
+    if (tag_is(vc, ep)) {
       c = (uint32_t)vc;
       const int n0 = (int)(c & 0xffffu);
-      const bool ok0 = sub >= n0 || (tag_is(k0, a.epoch) && tag_is(p0, a.epoch));
-      const bool ok1 = sub + 8 >= n0 || (tag_is(k1, a.epoch) && tag_is(p1, a.epoch));
-      if (ok0 && ok1) break;
+      bool ok = true;
+#pragma unroll
+      for (int u = 0; u < kPollE; ++u)
+        ok = ok && (sub + 8 * u >= n0 || (tag_is(ke[u], ep) && tag_is(pe[u], ep)));
+      if (ok) break;
     }
     __builtin_amdgcn_s_sleep(2);
     if (it == kFSpin - 1) atomicOr(a.flags, kFlagSpinTimeout);
@@ -662,18 +669,32 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, int h, int whic
   if (mine && r.total <= kCandMax) {
     const int o = off[wg];
     if (POLL_ALL) {
-      if (sub < nc) {
-        lk[o + sub] = tagged(k0, &ck[sub], a.epoch, a.flags);
-        lp[o + sub] = tagged(p0, &cp[sub], a.epoch, a.flags);
-      }
-      if (sub + 8 < nc) {
-        lk[o + sub + 8] = tagged(k1, &ck[sub + 8], a.epoch, a.flags);
-        lp[o + sub + 8] = tagged(p1, &cp[sub + 8], a.epoch, a.flags);
+#pragma unroll
+      for (int u = 0; u < kPollE; ++u) {
+        const int slot = sub + 8 * u;
+        if (slot < nc) {
+          lk[o + slot] = tagged(ke[u], &ck[slot], ep, a.flags);
+          lp[o + slot] = tagged(pe[u], &cp[slot], ep, a.flags);
+        }
       }
     }
-    for (int slot = sub + (POLL_ALL ? 16 : 0); slot < nc; slot += 8) {
-      lk[o + slot] = wait_tag(&ck[slot], a.epoch, a.flags);
-      lp[o + slot] = wait_tag(&cp[slot], a.epoch, a.flags);
+    // the rest in batches of four per thread, all loads of a batch issued before any wait
+    for (int s0 = sub + (POLL_ALL ? 8 * kPollE : 0); s0 < nc; s0 += 32) {
+      uint64_t kv[4], pv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int slot = min(s0 + 8 * u, kFScorePages - 1);
+        kv[u] = get_tag(&ck[slot]);
+        pv[u] = get_tag(&cp[slot]);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int slot = s0 + 8 * u;
+        if (slot < nc) {
+          lk[o + slot] = tagged(kv[u], &ck[slot], ep, a.flags);
+          lp[o + slot] = tagged(pv[u], &cp[slot], ep, a.flags);
+        }
+      }
     }
   }
   __syncthreads();
@@ -706,7 +727,7 @@ __device__ __forceinline__ void cand_slots(int total, const uint32_t* lk, const 
 
 // All pages of KV head h as slots (the fallback): keys polled from `tk`.
 template <int J>
-__device__ __forceinline__ void full_gather(const FusedLaunch& a, const uint64_t* tk, const uint32_t* forceb,
+__device__ __forceinline__ void full_gather(const FusedLaunch& a, uint32_t ep, const uint64_t* tk, const uint32_t* forceb,
                                             uint32_t (&key)[J], int (&page)[J], uint64_t& cand, uint64_t& force) {
   const int n = a.num_pages;
   uint64_t pending = 0;
@@ -722,7 +743,7 @@ __device__ __forceinline__ void full_gather(const FusedLaunch& a, const uint64_t
     for (int j = 0; j < J; ++j) v[j] = get_tag(&tk[min(page[j], n - 1)]);
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-      if (((pending >> j) & 1ull) && tag_is(v[j], a.epoch)) {
+      if (((pending >> j) & 1ull) && tag_is(v[j], ep)) {
         key[j] = (uint32_t)v[j];
         pending &= ~(1ull << j);
       }
@@ -783,7 +804,7 @@ __device__ __forceinline__ float qbar_finish(const FusedLaunch& a, const float (
 }
 
 template <bool BF16, int PS, int J>
-__device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const uint32_t (&key)[J],
+__device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep, int h, const uint32_t (&key)[J],
                                               const int (&page)[J], uint64_t cand, uint64_t force, uint64_t late_bits,
                                               bool keep_window, float qn, FLds& U) {
   FSelLds& L = U.sel;
@@ -799,15 +820,15 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
   const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
   uint64_t* thr = a.t_thr + 2 * (size_t)h;
   if (prr && early && t == 0) {
-    put_tag(thr, th.T, a.epoch);
-    put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), a.epoch);
+    put_tag(thr, th.T, ep);
+    put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
   }
   const uint64_t inA = sel2_membership<kFT, J>(key, page, cand, force, th, &L.eq_cut, L.sel);
   if (prr && !early) {
     __syncthreads();
     if (t == 0) {
-      put_tag(thr, th.T, a.epoch);
-      put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)L.eq_cut << 2), a.epoch);
+      put_tag(thr, th.T, ep);
+      put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)L.eq_cut << 2), ep);
     }
   }
 
@@ -837,7 +858,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
       if (f && run + lanes_below(bm) < capl && !((inP >> j) & 1ull)) inLate |= 1ull << j;
       run += __popcll(bm);
     }
-    if (t == 0) put_tag(&a.t_lcnt[h], (uint32_t)min(ltot, capl), a.epoch);
+    if (t == 0) put_tag(&a.t_lcnt[h], (uint32_t)min(ltot, capl), ep);
   }
   // the list to attend after selection, in page order: A \ P (PRR; also without the
   // late-speculated pages) or A (serial, or a PRR step whose speculation is discarded
@@ -849,11 +870,11 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
   const int nM = min(sel2_list<kFT, J>(inM, page, L.mlist, a.cap, L.sel), a.cap);
   __syncthreads();
   if (nM == 0) {
-    if (t == 0) put_tag(&a.t_mcnt[h], mflags, a.epoch);
+    if (t == 0) put_tag(&a.t_mcnt[h], mflags, ep);
   } else if (nM > kFW) {
     uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
-    for (int i = t; i < nM; i += kFT) put_tag(&ml[i], (uint32_t)L.mlist[i], a.epoch);
-    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM | mflags, a.epoch);
+    for (int i = t; i < nM; i += kFT) put_tag(&ml[i], (uint32_t)L.mlist[i], ep);
+    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM | mflags, ep);
   }
   // the selected list (an output) and the counts
   int32_t* sel = a.selected + (size_t)h * a.cap;
@@ -872,7 +893,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
   }
   if (nM > 0 && nM <= kFW) {
     // few enough to attend here: one page per wave, published as the first miss slot
-    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM | kSelfMiss | mflags, a.epoch);
+    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM | kSelfMiss | mflags, ep);
     int pg[1];
     pg[0] = __builtin_amdgcn_readfirstlane(w < nM ? L.mlist[w] : -1);
     __syncthreads();  // the list is read before the attention reuses the LDS
@@ -880,7 +901,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
     load_q(a, h, qf);
     WaveStates<1> st;
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
-    fold_publish<1>(a, h, a.n_spec, st, 1u, U.attn);
+    fold_publish<1>(a, ep, h, a.n_spec, st, 1u, U.attn);
   }
   update_window<J>(a, a.win + 4 * h, qn, key, cand, (5 * a.kextra_a) / 2, keep_window, U.sel.sel);
   if (a.late) update_window<J>(a, a.win + 4 * h + 2, qn, key, cand, (3 * a.kextra_a) / 2, true, U.sel.sel);
@@ -890,7 +911,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, int h, const
 // the list to attend, and writes the outputs, with no barrier; waves 1 and 2 meanwhile
 // derive the next step's candidate bounds from the same list.
 template <bool BF16, int PS>
-__device__ __forceinline__ void select_wave(const FusedLaunch& a, int h, int total, float qn, FLds& U) {
+__device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, int h, int total, float qn, FLds& U) {
   FSelLds& L = U.sel;
   constexpr int NK = kCandWave / kWave;
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
@@ -929,16 +950,16 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, int h, int tot
     const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
     uint64_t* thr = a.t_thr + 2 * (size_t)h;
     if (prr && early && lane == 0) {
-      put_tag(thr, th.T, a.epoch);
-      put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), a.epoch);
+      put_tag(thr, th.T, ep);
+      put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
     }
     int eq_cut = kEqAll;
     const uint64_t inA = wsel_membership<NK>(key, page, cand, force, th, &eq_cut);
     if (prr && !early) {
       eq_cut = __builtin_amdgcn_readfirstlane(wave_umin((uint32_t)eq_cut));
       if (lane == 0) {
-        put_tag(thr, th.T, a.epoch);
-        put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)eq_cut << 2), a.epoch);
+        put_tag(thr, th.T, ep);
+        put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)eq_cut << 2), ep);
       }
     }
     // pages of late speculation: flagged, within the late capacity, never in P^t
@@ -953,7 +974,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, int h, int tot
         if (f && ltot + lanes_below(bm) < capl && !((inP >> j) & 1ull)) inLate |= 1ull << j;
         ltot += __popcll(bm);
       }
-      if (lane == 0) put_tag(&a.t_lcnt[h], (uint32_t)min(ltot, capl), a.epoch);
+      if (lane == 0) put_tag(&a.t_lcnt[h], (uint32_t)min(ltot, capl), ep);
     }
     const int nMiss = prr ? wave_isum(__popcll(inA & ~inP)) : 0;
     const bool drop = prr && a.mode == PRR_RECOMPUTE_ON_MISS && nMiss > 0;
@@ -969,13 +990,13 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, int h, int tot
       const int q = pos + lanes_below(bm);
       if (in && q < a.cap) {
         L.mlist[q] = page[j];
-        if (nM > kFW) put_tag(&ml[q], (uint32_t)page[j], a.epoch);
+        if (nM > kFW) put_tag(&ml[q], (uint32_t)page[j], ep);
       }
       pos += __popcll(bm);
     }
     if (lane == 0) {
       const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
-      put_tag(&a.t_mcnt[h], (uint32_t)nM | mflags | self, a.epoch);
+      put_tag(&a.t_mcnt[h], (uint32_t)nM | mflags | self, ep);
       L.cnt[0][0] = nM;
     }
     // the selected list (an output) and the counts
@@ -1012,12 +1033,12 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, int h, int tot
     load_q(a, h, qf);
     WaveStates<1> st;
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
-    fold_publish<1>(a, h, a.n_spec, st, 1u, U.attn);
+    fold_publish<1>(a, ep, h, a.n_spec, st, 1u, U.attn);
   }
 }
 
 template <bool BF16, int PS>
-__device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U) {
+__device__ __forceinline__ void role_select(const FusedLaunch& a, uint32_t ep, int h, FLds& U) {
   FSelLds& L = U.sel;
   const int t = threadIdx.x;
   const int n = a.num_pages, nw = (n + 31) >> 5;
@@ -1063,9 +1084,9 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U
   nv = block_sum<kFT>(nv, L.cnt[1]);  // P^t holds no duplicates
   if (t == 0) L.npv = nv;
   const float qn = qbar_finish(a, qv, L.qb);
-  const FCand c = cand_load<true>(a, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  const FCand c = cand_load<true>(a, ep, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
   if (a.kextra_a <= c.total - c.nforced && c.total <= kCandWave) {
-    select_wave<BF16, PS>(a, h, c.total, qn, U);
+    select_wave<BF16, PS>(a, ep, h, c.total, qn, U);
   } else if (a.kextra_a <= c.total - c.nforced && c.total <= kCandMax) {
     // one instantiation per path keeps the kernel's code (and its instruction-cache
     // footprint) small: 4 candidate slots per thread, 16 page slots in the fallback
@@ -1074,22 +1095,22 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, int h, FLds& U
     uint64_t cand, force;
     uint64_t late_bits;
     cand_slots<4>(c.total, L.ck, L.cpg, key, page, cand, force, &late_bits);
-    select_finish<BF16, PS, 4>(a, h, key, page, cand, force, late_bits, true, qn, U);
+    select_finish<BF16, PS, 4>(a, ep, h, key, page, cand, force, late_bits, true, qn, U);
   } else {
     uint32_t key[16];
     int page[16];
     uint64_t cand, force;
-    full_gather<16>(a, a.t_score + (size_t)h * a.max_pages, L.forceb, key, page, cand, force);
+    full_gather<16>(a, ep, a.t_score + (size_t)h * a.max_pages, L.forceb, key, page, cand, force);
 #pragma unroll
     for (int j = 0; j < 16; ++j) key[j] = score_key(__uint_as_float(key[j]));
-    select_finish<BF16, PS, 16>(a, h, key, page, cand, force, 0ull, false, qn, U);
+    select_finish<BF16, PS, 16>(a, ep, h, key, page, cand, force, 0ull, false, qn, U);
   }
 }
 
 // ------------------------------------------------------------------------ predict
 
 template <int J>
-__device__ __forceinline__ void predict_finish(const FusedLaunch& a, int h, const uint32_t (&key)[J],
+__device__ __forceinline__ void predict_finish(const FusedLaunch& a, uint32_t ep, int h, const uint32_t (&key)[J],
                                                const int (&page)[J], uint64_t cand, uint64_t force, bool keep_window,
                                                float qn, FSelLds& L) {
   const SelThreshold th = sel2_threshold<kFT, J>(key, cand, a.kextra_p, L.sel);
@@ -1108,7 +1129,7 @@ __device__ __forceinline__ void predict_finish(const FusedLaunch& a, int h, cons
 }
 
 template <bool BF16>
-__device__ __forceinline__ void role_predict(const FusedLaunch& a, int h, FLds& U) {
+__device__ __forceinline__ void role_predict(const FusedLaunch& a, uint32_t ep, int h, FLds& U) {
   FSelLds& L = U.sel;
   const int t = threadIdx.x;
   const int n = a.num_pages, nw = (n + 31) >> 5;
@@ -1124,19 +1145,19 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, int h, FLds& 
   float qv[16];
   qbar_load<BF16>(a, h, qv);
   const float qn = qbar_finish(a, qv, L.qb);
-  const FCand c = cand_load<true>(a, h, 1, L.off, L.tot, L.ck, L.cpg);
+  const FCand c = cand_load<true>(a, ep, h, 1, L.off, L.tot, L.ck, L.cpg);
   if (a.kextra_p <= c.total - c.nforced && c.total <= kCandMax) {
     uint32_t key[4];
     int page[4];
     uint64_t cand, force;
     cand_slots<4>(c.total, L.ck, L.cpg, key, page, cand, force, nullptr);
-    predict_finish<4>(a, h, key, page, cand, force, true, qn, L);
+    predict_finish<4>(a, ep, h, key, page, cand, force, true, qn, L);
   } else {
     uint32_t key[16];
     int page[16];
     uint64_t cand, force;
-    full_gather<16>(a, a.t_pkey + (size_t)h * a.max_pages, L.forceb, key, page, cand, force);
-    predict_finish<16>(a, h, key, page, cand, force, false, qn, L);
+    full_gather<16>(a, ep, a.t_pkey + (size_t)h * a.max_pages, L.forceb, key, page, cand, force);
+    predict_finish<16>(a, ep, h, key, page, cand, force, false, qn, L);
   }
 }
 
@@ -1146,7 +1167,7 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, int h, FLds& 
 // (all loads issued together, then waited for); returns `keep` without the pages not in A.
 // Called by every wave of the workgroup (it holds a barrier).
 template <int NPW>
-__device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, int h, const int (&pg)[NPW], uint32_t keep,
+__device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, uint32_t ep, int h, const int (&pg)[NPW], uint32_t keep,
                                               uint32_t* bc) {
   const uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
   uint64_t vs[NPW];
@@ -1158,7 +1179,7 @@ __device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, int h, const
     for (int it = 0; it < kFSpin; ++it) {
       v0 = get_tag(thr);
       v1 = get_tag(thr + 1);
-      if (tag_is(v0, a.epoch) && tag_is(v1, a.epoch)) break;
+      if (tag_is(v0, ep) && tag_is(v1, ep)) break;
       __builtin_amdgcn_s_sleep(2);
       if (it == kFSpin - 1 && threadIdx.x == 0) atomicOr(a.flags, kFlagSpinTimeout);
     }
@@ -1171,7 +1192,7 @@ __device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, int h, const
   if (!keep) return keep;
   uint32_t sc[NPW];
 #pragma unroll
-  for (int k = 0; k < NPW; ++k) sc[k] = pg[k] >= 0 ? tagged(vs[k], &ts[pg[k]], a.epoch, a.flags) : 0u;
+  for (int k = 0; k < NPW; ++k) sc[k] = pg[k] >= 0 ? tagged(vs[k], &ts[pg[k]], ep, a.flags) : 0u;
   const uint32_t T = bc[0];
   const uint32_t me = bc[1];
   const int mode = (int)(me & 3u), eq_cut = (int)(me >> 2);
@@ -1186,7 +1207,7 @@ __device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, int h, const
 }
 
 template <bool BF16, int PS, int NPW>
-__device__ __forceinline__ void role_spec(const FusedLaunch& a, int h, int c, FLds& U) {
+__device__ __forceinline__ void role_spec(const FusedLaunch& a, uint32_t ep, int h, int c, FLds& U) {
   const int count = min(max(a.pred_cur_count[h], 0), a.cap);
   const int start = c * a.chunk;
   if (start >= count) return;
@@ -1210,15 +1231,15 @@ __device__ __forceinline__ void role_spec(const FusedLaunch& a, int h, int c, FL
   }
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
-  if (a.mode != PRR_KEEP_WASTED) keep = keep_in_A<NPW>(a, h, pg, keep, U.bc);
-  fold_publish<NPW>(a, h, c, st, keep, U.attn);
+  if (a.mode != PRR_KEEP_WASTED) keep = keep_in_A<NPW>(a, ep, h, pg, keep, U.bc);
+  fold_publish<NPW>(a, ep, h, c, st, keep, U.attn);
 }
 
 // Late speculation (PRR schedule): as soon as this step's scores exist, the pages just
 // above the selection threshold that P^t missed (listed by the score workgroups) are
 // attended, one state per page; once A is known the states of pages in A are folded.
 template <bool BF16, int PS, int NPW>
-__device__ __forceinline__ void role_late(const FusedLaunch& a, int h, int u, FLds& U) {
+__device__ __forceinline__ void role_late(const FusedLaunch& a, uint32_t ep, int h, int u, FLds& U) {
   FSelLds& L = U.sel;
   const int t = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane((int)(t / kWave));
@@ -1239,7 +1260,7 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, int h, int u, FL
 #pragma unroll
   for (int r = 0; r < PRR_MAX_CAP_DEV / kFT; ++r)
     if (pe[r] >= 0 && pe[r] < n) atomicOr(&L.bitP[pe[r] >> 5], 1u << (pe[r] & 31));
-  const FCand c = cand_load<false>(a, h, 2, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  const FCand c = cand_load<false>(a, ep, h, 2, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
   const int cover = min(c.total, a.n_late * a.chunk);
   const int start = u * a.chunk;
   if (start >= cover) return;
@@ -1260,12 +1281,12 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, int h, int u, FL
   __syncthreads();  // the list is read before the attention reuses the LDS
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
-  keep = keep_in_A<NPW>(a, h, pg, keep, U.bc);
-  fold_publish<NPW>(a, h, a.n_spec + a.n_miss + u, st, keep, U.attn);
+  keep = keep_in_A<NPW>(a, ep, h, pg, keep, U.bc);
+  fold_publish<NPW>(a, ep, h, a.n_spec + a.n_miss + u, st, keep, U.attn);
 }
 
 template <bool BF16, int PS, int NPW>
-__device__ __forceinline__ void role_miss(const FusedLaunch& a, int h, int u, FLds& U) {
+__device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int h, int u, FLds& U) {
   // the count and this wave's list entries are loaded together; the entries are
   // published before the count, so they are usually valid when the count is
   const int start = u * a.chunk;
@@ -1282,10 +1303,10 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, int h, int u, FL
     for (int it = 0; it < kFSpin; ++it) {
       vm = get_tag(a.t_mcnt + h);
       ve = get_tag(&ml[min(i, a.cap - 1)]);
-      if (tag_is(vm, a.epoch)) {
+      if (tag_is(vm, ep)) {
         const uint32_t mv = (uint32_t)vm;
         const int nm = (mv & kSelfMiss) ? 0 : (int)(mv & kCountMask);
-        if (__ballot(lane < kFW * NPW && i < nm && !tag_is(ve, a.epoch)) == 0ull) break;
+        if (__ballot(lane < kFW * NPW && i < nm && !tag_is(ve, ep)) == 0ull) break;
       }
       __builtin_amdgcn_s_sleep(2);
       if (it == kFSpin - 1 && lane == 0) atomicOr(a.flags, kFlagSpinTimeout);
@@ -1315,13 +1336,13 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, int h, int u, FL
   }
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
-  fold_publish<NPW>(a, h, a.n_spec + u, st, keep, U.attn);
+  fold_publish<NPW>(a, ep, h, a.n_spec + u, st, keep, U.attn);
 }
 
 // ------------------------------------------------------------------------ merge
 
 template <bool BF16>
-__device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, FMergeLds& L, uint32_t* bc) {
+__device__ __forceinline__ void role_merge(const FusedLaunch& a, uint32_t ep, int h, int qn, FMergeLds& L, uint32_t* bc) {
   const float kNegInf = -__builtin_inff();
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int G = a.group, C = a.chunk;
@@ -1331,8 +1352,8 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, 
     uint64_t v0 = 0, v1 = 0;
     for (int it = 0; it < kFSpin; ++it) {
       v0 = get_tag(a.t_mcnt + h);
-      v1 = a.late ? get_tag(a.t_lcnt + h) : ((uint64_t)a.epoch << 32);
-      if (tag_is(v0, a.epoch) && tag_is(v1, a.epoch)) break;
+      v1 = a.late ? get_tag(a.t_lcnt + h) : ((uint64_t)ep << 32);
+      if (tag_is(v0, ep) && tag_is(v1, ep)) break;
       __builtin_amdgcn_s_sleep(2);
       if (it == kFSpin - 1 && t == 0) atomicOr(a.flags, kFlagSpinTimeout);
     }
@@ -1364,7 +1385,7 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, 
     for (int it = 0; it < kFSpin; ++it) {
       vm = get_tag(p);
       vl = get_tag(p + 1);
-      if (tag_is(vm, a.epoch) && tag_is(vl, a.epoch)) break;
+      if (tag_is(vm, ep) && tag_is(vl, ep)) break;
       __builtin_amdgcn_s_sleep(2);
       if (it == kFSpin - 1) atomicOr(a.flags, kFlagSpinTimeout);
     }
@@ -1437,21 +1458,25 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, int h, int qn, 
 template <bool BF16, int PS, int NPW>
 __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
   __shared__ FLds U;
+  // the epoch of this call: the kernel argument, or a device word that the caller
+  // advances between replays of a captured launch (written by an earlier launch, so
+  // visible at this launch's start)
+  const uint32_t ep = a.epoch_dev ? *a.epoch_dev : a.epoch;
   int b = blockIdx.x;
   const int H = a.num_kv_heads;
   if (b < H * a.n_score) {
-    role_score<BF16>(a, b / a.n_score, b % a.n_score, U.score);
+    role_score<BF16>(a, ep, b / a.n_score, b % a.n_score, U.score);
     return;
   }
   b -= H * a.n_score;
   if (b < H) {
-    role_select<BF16, PS>(a, b, U);
+    role_select<BF16, PS>(a, ep, b, U);
     return;
   }
   b -= H;
   if (a.schedule != 0) {
     if (b < H) {
-      role_predict<BF16>(a, b, U);
+      role_predict<BF16>(a, ep, b, U);
       return;
     }
     b -= H;
@@ -1459,22 +1484,22 @@ __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
   if (a.schedule == 2) return;
   if (a.schedule == 1) {
     if (b < H * a.n_spec) {
-      role_spec<BF16, PS, NPW>(a, b / a.n_spec, b % a.n_spec, U);
+      role_spec<BF16, PS, NPW>(a, ep, b / a.n_spec, b % a.n_spec, U);
       return;
     }
     b -= H * a.n_spec;
     if (b < H * a.n_late) {
-      role_late<BF16, PS, NPW>(a, b / a.n_late, b % a.n_late, U);
+      role_late<BF16, PS, NPW>(a, ep, b / a.n_late, b % a.n_late, U);
       return;
     }
     b -= H * a.n_late;
   }
   if (b < H * a.n_miss) {
-    role_miss<BF16, PS, NPW>(a, b / a.n_miss, b % a.n_miss, U);
+    role_miss<BF16, PS, NPW>(a, ep, b / a.n_miss, b % a.n_miss, U);
     return;
   }
   b -= H * a.n_miss;
-  if (b < H * a.group) role_merge<BF16>(a, b / a.group, b % a.group, U.merge, U.bc);
+  if (b < H * a.group) role_merge<BF16>(a, ep, b / a.group, b % a.group, U.merge, U.bc);
 }
 
 template <typename K>

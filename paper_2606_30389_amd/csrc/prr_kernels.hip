@@ -24,6 +24,22 @@ namespace prr {
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 
 // =====================================================================================
+// epoch of captured fused steps: one thread advances the word (skipping 0)
+// =====================================================================================
+
+__global__ void epoch_advance_kernel(uint32_t* p) {
+  if (threadIdx.x == 0) {
+    const uint32_t v = *p + 1u;
+    *p = v == 0u ? 1u : v;
+  }
+}
+
+hipError_t launch_epoch_advance(uint32_t* epoch_dev, hipStream_t stream) {
+  void* args[] = {&epoch_dev};
+  return hipLaunchKernel((const void*)epoch_advance_kernel, dim3(1), dim3(64), args, 0, stream);
+}
+
+// =====================================================================================
 // workspace fill
 // =====================================================================================
 

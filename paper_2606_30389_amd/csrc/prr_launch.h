@@ -127,6 +127,7 @@ struct FusedLaunch {
   uint32_t* flags;
   float alpha, beta, gamma;
   uint32_t epoch;
+  const uint32_t* epoch_dev;  // if set, the epoch is read from here (graph replays)
   int schedule;  // 0 serial, 1 PRR, 2 prefill
   int mode;
   int num_kv_heads, group, max_pages, num_pages, num_tokens;
@@ -143,6 +144,7 @@ hipError_t launch_fused(const FusedLaunch& a, bool bf16, int page_size, hipStrea
 int fused_grid(const FusedLaunch& a);
 
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
+hipError_t launch_epoch_advance(uint32_t* epoch_dev, hipStream_t stream);
 void calibrate_grid(const float* scores, int n_traj, int n_rows, int n_blocks, int k_select, int p_select,
                     const float* grid, int n_grid, int n_threads, float* best_theta, double* objective_out);
 hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream);

@@ -212,7 +212,22 @@ def next_epoch():
     """A process-wide increasing value: the fused schedules need a new one for every call
     on a workspace (the device-side hand-offs of a call are tagged with it)."""
     _epoch[0] += 1
+    assert _epoch[0] < GRAPH_EPOCH_BASE
     return _epoch[0]
+
+
+# Captured fused steps read their epoch from one device word per device, advanced by
+# every replay; it counts up from 2^30, above every epoch the host hands out.
+GRAPH_EPOCH_BASE = 1 << 30
+_device_epoch = {}
+
+
+def device_epoch(device) -> torch.Tensor:
+    dev = torch.device(device)
+    key = (dev.type, dev.index if dev.index is not None else torch.cuda.current_device())
+    if key not in _device_epoch:
+        _device_epoch[key] = torch.full((1,), GRAPH_EPOCH_BASE, dtype=torch.int32, device=dev)
+    return _device_epoch[key]
 
 
 class DecodeStack:
@@ -237,15 +252,49 @@ class DecodeStack:
         self.params = p
         self.events = L.hip_events(3 * len(layers) + 1)
 
-    def step(self, schedule, stream, spec_stream=None):
-        """One decode step of every layer; P^t is in each layer's predicted[cur]."""
+    def _parity(self):
         parity = self.layers[0].cur
         assert all(st.cur == parity for st in self.layers), "layers disagree on the current prediction buffer"
-        self.params.epoch = next_epoch()
-        L.prr_decode_step(self.dims, self.params, self.io, parity, schedule, stream, spec_stream, self.events)
+        return parity
+
+    def _advance(self, schedule, parity):
         if schedule not in (L.PRR_SCHED_SERIAL, L.PRR_SCHED_FUSED_SERIAL):
             for st in self.layers:
                 st.cur = 1 - parity
+
+    def step(self, schedule, stream, spec_stream=None):
+        """One decode step of every layer; P^t is in each layer's predicted[cur]."""
+        parity = self._parity()
+        self.params.epoch = next_epoch()
+        self.params.epoch_dev = None
+        L.prr_decode_step(self.dims, self.params, self.io, parity, schedule, stream, spec_stream, self.events)
+        self._advance(schedule, parity)
+
+    def capture(self, schedule, stream, tag=None):
+        """Capture one fused decode step of every layer as a HIP graph per parity of the
+        prediction buffers: an advance of the device epoch word, then the layers' launches
+        (which read it).  The step parameters are those of this moment; `tag` names the
+        capture when several are kept for one schedule."""
+        assert schedule in (L.PRR_SCHED_FUSED_SERIAL, L.PRR_SCHED_FUSED_PRR), "fused steps only"
+        if not hasattr(self, "graphs"):
+            self.graphs = {}
+        ep = device_epoch(self.layers[0].k.device)
+        self.params.epoch = 0
+        self.params.epoch_dev = ep.data_ptr()
+        for parity in (0, 1):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                L.prr_epoch_advance(ep, stream)
+                L.prr_decode_step(self.dims, self.params, self.io, parity, schedule, stream, None, self.events)
+            self.graphs[(schedule, tag, parity)] = g
+        self.params.epoch_dev = None
+
+    def replay(self, schedule, stream, tag=None):
+        """One decode step of every layer by replaying the captured graph (see capture)."""
+        parity = self._parity()
+        with torch.cuda.stream(stream):
+            self.graphs[(schedule, tag, parity)].replay()
+        self._advance(schedule, parity)
 
 
 class TwoStream:

@@ -667,3 +667,73 @@ def test_fused_decode_step(torch, case):
     for st in layers:
         fl = int(st.workspace[:4].view(torch.int32).cpu()[0])
         assert fl == 0, f"workspace error flags {fl:#x}"
+
+
+@pytest.mark.parametrize("late", [False, True], ids=["spec", "late"])
+def test_fused_graph_replay(torch, late):
+    """Fused PRR steps captured once as HIP graphs (the launches read a device epoch word
+    that each replay advances) and replayed with eager work and synchronisations in
+    between: every replay equals the eager launch of the same step on a twin stack bit for
+    bit, and the oracle."""
+    from paper_2606_30389_amd import _lib as L
+    from paper_2606_30389_amd import runtime as R
+    cfg = W.CONFIGS["glm32k"]
+    n_layers, steps = 2, 5
+    stacks, inputs, metas, qs, queries = [], [], [[], []], [], [[], []]
+    for twin in range(2):
+        layers = []
+        for layer in range(n_layers):
+            pc = S.path_config(cfg, num_pages=512, mode=0)
+            st, li = S.make_layer(cfg, pc, layer=layer)
+            st.build_meta()
+            layers.append(st)
+            if twin == 0:
+                inputs.append(li)
+                metas[0].append(S.oracle_meta(li, pc))
+                _, qb = W.query_trajectory(cfg, layer, steps=steps)
+                qs.append(qb)
+            queries[twin].append(S.q_tensor(qs[layer][0], pc))
+        stack = R.DecodeStack(layers, queries[twin], torch.device("cuda:0"))
+        stack.params.late_spec = int(late)
+        stacks.append(stack)
+    pc = stacks[0].layers[0].cfg
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    for stack in stacks:
+        stack.step(L.PRR_SCHED_FUSED_PREFILL, s)
+    torch.cuda.synchronize()
+    S.log(f"capturing fused PRR graphs (late={late})")
+    stacks[1].capture(L.PRR_SCHED_FUSED_PRR, s)
+    torch.cuda.synchronize()
+    for t in range(1, steps + 1):
+        for twin in range(2):
+            for layer in range(n_layers):
+                queries[twin][layer].copy_(S.q_tensor(qs[layer][t], pc))
+        torch.cuda.synchronize()
+        S.log(f"graph replay step {t}")
+        s.wait_stream(torch.cuda.current_stream())
+        stacks[0].step(L.PRR_SCHED_FUSED_PRR, s)
+        torch.cuda.synchronize()
+        junk = torch.randn(1 << 16, device="cuda:0").sum().item()  # eager work between replays
+        assert junk == junk
+        s.wait_stream(torch.cuda.current_stream())
+        stacks[1].replay(L.PRR_SCHED_FUSED_PRR, s)
+        torch.cuda.synchronize()
+        for layer in range(n_layers):
+            a, b = stacks[0].layers[layer], stacks[1].layers[layer]
+            for name in ("out_o32", "out_m", "out_l", "out_o", "sel", "sel_count", "missed", "wasted"):
+                x, y = getattr(a, name), getattr(b, name)
+                assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)) if x.dtype.is_floating_point else \
+                    torch.equal(x, y), f"step {t} layer {layer}: {name} differs between eager and graph replay"
+            assert torch.equal(a.pred[a.cur], b.pred[b.cur]) and torch.equal(a.pred_count[a.cur], b.pred_count[b.cur]), \
+                f"step {t} layer {layer}: next prediction"
+            q64 = W.bits_to_f64(qs[layer][t], cfg.dtype)
+            A = S.check_selection(S.lists(b), S.oracle_scores(q64, metas[0][layer], pc), pc.k_select, list(pc.forced),
+                                  pc.forced_in_budget)
+            ref = O.attend(q64, inputs[layer].k64(), inputs[layer].v64(), A, pc.page_size, pc.num_tokens)
+            S.check_attention(S.to_np(b.out_o32), S.to_np(b.out_m), S.to_np(b.out_l), ref, S.to_np(b.out_o),
+                              dtype=pc.dtype, what=f"graph layer {layer} step {t}")
+    for stack in stacks:
+        for st in stack.layers:
+            fl = int(st.workspace[:4].view(torch.int32).cpu()[0])
+            assert fl == 0, f"workspace error flags {fl:#x}"
