@@ -70,7 +70,7 @@ prr_status check_ptr(const void* p, const char* name, size_t align) {
   } while (0)
 
 struct WsLayout {
-  size_t flags, sel_cnt, rep_cnt, rep_o, rep_ml, f_score, f_thr, f_mcnt, f_mlist, f_part, f_parto, f_cnt, f_candk,
+  size_t flags, sel_cnt, rep_cnt, rep_o, rep_ml, f_score, f_thr, f_mcnt, f_mlist, f_part, f_parto, f_candk,
       f_candp, f_pkey, f_win, f_lcnt, f_pbits, total;
   int nchunks, nwork_max, nparts;
 };
@@ -106,10 +106,8 @@ bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
   L.f_parto = off;
   off = align_up(off + (size_t)hkv * L.nparts * g * 128 * 4, 256);
   const size_t nsc = (size_t)div_up(d->max_pages, 128);
-  L.f_cnt = off;
-  off = align_up(off + 3 * (size_t)hkv * nsc * 8, 256);
-  L.f_candk = off;
-  off = align_up(off + 3 * (size_t)hkv * nsc * 128 * 8, 256);
+  L.f_candk = off;  // per list: the count, then the keys (stride 132)
+  off = align_up(off + 3 * (size_t)hkv * nsc * 132 * 8, 256);
   L.f_candp = off;
   off = align_up(off + 3 * (size_t)hkv * nsc * 128 * 8, 256);
   L.f_pkey = off;
@@ -565,7 +563,6 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.t_mlist = reinterpret_cast<uint64_t*>(ws + L.f_mlist);
   a.t_part = reinterpret_cast<uint64_t*>(ws + L.f_part);
   a.part_o = reinterpret_cast<float*>(ws + L.f_parto);
-  a.t_cnt = reinterpret_cast<uint64_t*>(ws + L.f_cnt);
   a.t_candk = reinterpret_cast<uint64_t*>(ws + L.f_candk);
   a.t_candp = reinterpret_cast<uint64_t*>(ws + L.f_candp);
   a.t_pkey = reinterpret_cast<uint64_t*>(ws + L.f_pkey);

@@ -42,6 +42,10 @@ constexpr int kFOPad = kHeadDim + 4;
 constexpr int kEqAll = 16383;  // eq_cut meaning "every key equal to T is taken"
 constexpr int kCandMax = 4 * kFT;     // candidates ranked by one workgroup (4 per thread)
 constexpr int kCandWave = 12 * kWave;  // candidates ranked by one wave (12 per lane)
+// A candidate list of one score workgroup: its tagged count, then up to 128 tagged keys;
+// the count shares lines with the first keys, and the lists of different workgroups lie
+// in different memory channels, so polls of many lists do not queue on one channel.
+constexpr int kCandStride = 132;
 
 __device__ __forceinline__ void put_tag(uint64_t* p, uint32_t v, uint32_t epoch) {
   __hip_atomic_store(p, ((uint64_t)epoch << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -257,15 +261,15 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
 
   const size_t rec_a = (size_t)h * a.n_score + blk;
   const size_t rec_p = ((size_t)a.num_kv_heads + h) * a.n_score + blk;
-  uint64_t* ck_a = a.t_candk + rec_a * kFScorePages;
+  uint64_t* ck_a = a.t_candk + rec_a * kCandStride + 1;
   uint64_t* cp_a = a.t_candp + rec_a * kFScorePages;
-  uint64_t* ck_p = a.t_candk + rec_p * kFScorePages;
+  uint64_t* ck_p = a.t_candk + rec_p * kCandStride + 1;
   uint64_t* cp_p = a.t_candp + rec_p * kFScorePages;
   int na = 0, nfa = 0, np = 0, nfp = 0, nl = 0;
   // candidates of A first (the select workgroup waits for them), each flagged when it is
   // also a page for late speculation: not forced, not in P^t, key at least lo_l ...
   const size_t rec_l = (2 * (size_t)a.num_kv_heads + h) * a.n_score + blk;
-  uint64_t* ck_l = a.t_candk + rec_l * kFScorePages;
+  uint64_t* ck_l = a.t_candk + rec_l * kCandStride + 1;
   uint64_t* cp_l = a.t_candp + rec_l * kFScorePages;
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
@@ -292,8 +296,8 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     nl += __popcll(ml);
   }
   if (lane == 0) {
-    put_tag(&a.t_cnt[rec_a], (uint32_t)na | ((uint32_t)nfa << 16), ep);
-    if (a.late) put_tag(&a.t_cnt[rec_l], (uint32_t)nl, ep);
+    put_tag(ck_a - 1, (uint32_t)na | ((uint32_t)nfa << 16), ep);
+    if (a.late) put_tag(ck_l - 1, (uint32_t)nl, ep);
   }
   if (!ema) return;
   // ... then the EMA update of Eq. (3) and the candidates of the next prediction
@@ -336,7 +340,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     np += __popcll(mp);
     nfp += __popcll(mfp);
   }
-  if (lane == 0) put_tag(&a.t_cnt[rec_p], (uint32_t)np | ((uint32_t)nfp << 16), ep);
+  if (lane == 0) put_tag(ck_p - 1, (uint32_t)np | ((uint32_t)nfp << 16), ep);
 }
 
 // ------------------------------------------------------------------------ shared select pieces
@@ -603,7 +607,7 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, in
   const bool mine = wg < nS;
   const size_t rec0 = ((size_t)which * a.num_kv_heads + h) * nS;
   const size_t rec = rec0 + min(wg, nS - 1);
-  const uint64_t* ck = a.t_candk + rec * kFScorePages;
+  const uint64_t* ck = a.t_candk + rec * kCandStride + 1;
   const uint64_t* cp = a.t_candp + rec * kFScorePages;
   // the count and the first four entries are polled together until all needed are there
   // (32 per score workgroup, more than almost any list holds)
@@ -614,11 +618,11 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, in
   uint32_t c = 0u;
   if (!POLL_ALL && w == 0) {
     const bool m1 = lane < nS;
-    const uint64_t* pc = &a.t_cnt[rec0 + min(lane, nS - 1)];
+    const uint64_t* pc = &a.t_candk[(rec0 + min(lane, nS - 1)) * kCandStride];
     for (int it = 0; it < kFSpin; ++it) {
       vc = get_tag(pc);
       if (__ballot(m1 && !tag_is(vc, ep)) == 0ull) break;
-      __builtin_amdgcn_s_sleep(2);
+      __builtin_amdgcn_s_sleep(24);  // slow polling: these workgroups have slack
       if (it == kFSpin - 1 && lane == 0) atomicOr(a.flags, kFlagSpinTimeout);
     }
     if (m1) {
@@ -627,7 +631,7 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, in
     }
   }
   for (int it = 0; POLL_ALL && mine && it < kFSpin; ++it) {
-    vc = get_tag(&a.t_cnt[rec]);
+    vc = get_tag(ck - 1);
 #pragma unroll
     for (int u = 0; u < kPollE; ++u) {
       ke[u] = get_tag(&ck[sub + 8 * u]);
