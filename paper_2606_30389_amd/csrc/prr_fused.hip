@@ -132,6 +132,12 @@ struct FLds {
 // (Eq. (2)) the same way, for the predict workgroup.
 
 
+// EMA of |q-bar|_1 at the rate of the score EMA (the scale of the prediction keys);
+// prev = 0: none yet
+__device__ __forceinline__ float qn_ema(const FusedLaunch& a, float qn, float prev) {
+  return prev > 0.0f ? a.alpha * qn + (1.0f - a.alpha) * prev : qn;
+}
+
 template <bool BF16>
 __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, int h, int blk, FScoreLds& S) {
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
@@ -175,14 +181,16 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
 #pragma unroll
   for (int e = 0; e < 8; ++e) qb[e] = S.qbar[cg * 8 + e];
   // wave 0 filters: EMA state of pages pbase + lane and pbase + 64 + lane, and the
-  // candidate bounds, kept from the previous step as ratios to |q-bar|_1 (scores scale
-  // with q-bar); loaded together with the metadata
-  float r_a = 0.f, r_p = 0.f, r_l = 0.f;
+  // candidate bounds kept from the previous step as ratios: of A and of late pages to
+  // |q-bar|_1 (scores scale with q-bar), of the next prediction to the EMA of |q-bar|_1
+  // (the EMA keys scale with it); loaded together with the metadata
+  float r_a = 0.f, r_p = 0.f, r_l = 0.f, qe0 = 0.f;
   uint32_t pw[2] = {0u, 0u};
   if (w == 0) {
     r_a = __uint_as_float(a.win[4 * h]);
     r_p = __uint_as_float(a.win[4 * h + 1]);
     r_l = __uint_as_float(a.win[4 * h + 2]);
+    qe0 = __uint_as_float(a.win[4 * h + 3]);
     if (a.late) {
 #pragma unroll
       for (int half = 0; half < 2; ++half)
@@ -256,7 +264,8 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   __syncthreads();
   if (w != 0) return;
   const float qn = wave_sum(fabsf(S.qbar[lane]) + fabsf(S.qbar[lane + 64]));
-  const uint32_t lo_a = score_key(r_a * qn), lo_p = score_key(r_p * qn);
+  const float qe = qn_ema(a, qn, qe0);
+  const uint32_t lo_a = score_key(r_a * qn), lo_p = score_key(r_p * qe);
   const uint32_t lo_l = max(score_key(r_l * qn), lo_a);  // late pages are candidates of A
 
   const size_t rec_a = (size_t)h * a.n_score + blk;
@@ -1116,7 +1125,7 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, uint32_t ep, i
 template <int J>
 __device__ __forceinline__ void predict_finish(const FusedLaunch& a, uint32_t ep, int h, const uint32_t (&key)[J],
                                                const int (&page)[J], uint64_t cand, uint64_t force, bool keep_window,
-                                               float qn, FSelLds& L) {
+                                               float qe, FSelLds& L) {
   const SelThreshold th = sel2_threshold<kFT, J>(key, cand, a.kextra_p, L.sel);
   const uint64_t in = sel2_compact<kFT, J>(key, page, cand, force, th, a.pred_nxt + (size_t)h * a.cap, a.cap,
                                            a.pred_nxt_count + h, &L.eq_cut, L.sel);
@@ -1129,7 +1138,64 @@ __device__ __forceinline__ void predict_finish(const FusedLaunch& a, uint32_t ep
     if ((in >> j) & 1ull) atomicOr(&L.bitP[page[j] >> 5], 1u << (page[j] & 31));
   __syncthreads();
   for (int i = threadIdx.x; i < nw; i += kFT) a.pbits_nxt[(size_t)h * nwmax + i] = L.bitP[i];
-  update_window<J>(a, a.win + 4 * h + 1, qn, key, cand, 3 * a.kextra_p, keep_window, L.sel);
+  update_window<J>(a, a.win + 4 * h + 1, qe, key, cand, (5 * a.kextra_p) / 2, keep_window, L.sel);
+}
+
+// The next prediction from a short candidate list, as select_wave does for A: wave 0
+// ranks the keys (12 per lane) and writes P^{t+1} in page order, wave 1 the next step's
+// bound of the candidates (rank 2.5 |P|), the other waves clear the bitmap meanwhile.
+__device__ __forceinline__ void predict_wave(const FusedLaunch& a, int h, int total, float qe, FSelLds& L) {
+  constexpr int NK = kCandWave / kWave;
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  const int nw = (a.num_pages + 31) >> 5, nwmax = (a.max_pages + 31) >> 5;
+  uint32_t key[NK], pv[NK];
+  int page[NK];
+  uint64_t cand = 0, force = 0, in = 0;
+  if (w < 2) {
+#pragma unroll
+    for (int j = 0; j < NK; ++j) {
+      key[j] = L.ck[j * kWave + lane];
+      pv[j] = L.cpg[j * kWave + lane];
+    }
+#pragma unroll
+    for (int j = 0; j < NK; ++j) {
+      const bool v = j * kWave + lane < total;
+      key[j] = v ? key[j] : 0u;
+      page[j] = v ? (int)(pv[j] & 0x3fffffffu) : 0;
+      if (v && (pv[j] >> 31)) force |= 1ull << j;
+      if (v && !(pv[j] >> 31)) cand |= 1ull << j;
+    }
+  }
+  if (w == 0) {
+    const SelThreshold th = wsel_threshold<NK>(key, cand, a.kextra_p, L.ws[0], true);
+    int eq_cut = kEqAll;
+    in = wsel_membership<NK>(key, page, cand, force, th, &eq_cut);
+    int32_t* out = a.pred_nxt + (size_t)h * a.cap;
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < NK; ++j) {
+      const bool m = (in >> j) & 1ull;
+      const uint64_t bm = __ballot(m);
+      const int q = n + lanes_below(bm);
+      if (m && q < a.cap) out[q] = page[j];
+      n += __popcll(bm);
+    }
+    if (lane == 0) a.pred_nxt_count[h] = min(n, a.cap);
+  } else if (w == 1) {
+    const SelThreshold th = wsel_threshold<NK>(key, cand, max((5 * a.kextra_p) / 2, 1), L.ws[1], true);
+    if (lane == 0 && th.mode == 2 && qe > 0.0f) a.win[4 * h + 1] = __float_as_uint(key_value(th.T) / qe);
+  } else {
+    for (int i = t - 2 * kWave; i < nw; i += kFT - 2 * kWave) L.bitP[i] = 0u;
+  }
+  __syncthreads();
+  // P^{t+1} as a bitmap too (the late-speculation filter of the next step)
+  if (w == 0) {
+#pragma unroll
+    for (int j = 0; j < NK; ++j)
+      if ((in >> j) & 1ull) atomicOr(&L.bitP[page[j] >> 5], 1u << (page[j] & 31));
+  }
+  __syncthreads();
+  for (int i = t; i < nw; i += kFT) a.pbits_nxt[(size_t)h * nwmax + i] = L.bitP[i];
 }
 
 template <bool BF16>
@@ -1138,6 +1204,8 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, uint32_t ep, 
   const int t = threadIdx.x;
   const int n = a.num_pages, nw = (n + 31) >> 5;
   for (int i = t; i < nw; i += kFT) L.forceb[i] = 0u;
+  // the bins of the one-wave selects, cleared while the candidates are awaited
+  if (t < 2 * kWave) wsel_clear(L.ws[t / kWave]);
   __syncthreads();
   if (t == 0 && a.n_forced > 0) {
 #pragma unroll
@@ -1146,22 +1214,27 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, uint32_t ep, 
       atomicOr(&L.forceb[a.forced[i] >> 5], 1u << (a.forced[i] & 31));
     }
   }
+  const float qe0 = __uint_as_float(a.win[4 * h + 3]);  // read before any score workgroup ends
   float qv[16];
   qbar_load<BF16>(a, h, qv);
-  const float qn = qbar_finish(a, qv, L.qb);
+  const float qe = qn_ema(a, qbar_finish(a, qv, L.qb), qe0);
   const FCand c = cand_load<true>(a, ep, h, 1, L.off, L.tot, L.ck, L.cpg);
-  if (a.kextra_p <= c.total - c.nforced && c.total <= kCandMax) {
+  // every score workgroup has read the bounds: the scale of the next step's keys
+  if (t == 0) a.win[4 * h + 3] = __float_as_uint(qe);
+  if (a.kextra_p <= c.total - c.nforced && c.total <= kCandWave) {
+    predict_wave(a, h, c.total, qe, L);
+  } else if (a.kextra_p <= c.total - c.nforced && c.total <= kCandMax) {
     uint32_t key[4];
     int page[4];
     uint64_t cand, force;
     cand_slots<4>(c.total, L.ck, L.cpg, key, page, cand, force, nullptr);
-    predict_finish<4>(a, ep, h, key, page, cand, force, true, qn, L);
+    predict_finish<4>(a, ep, h, key, page, cand, force, true, qe, L);
   } else {
     uint32_t key[16];
     int page[16];
     uint64_t cand, force;
     full_gather<16>(a, ep, a.t_pkey + (size_t)h * a.max_pages, L.forceb, key, page, cand, force);
-    predict_finish<16>(a, ep, h, key, page, cand, force, false, qn, L);
+    predict_finish<16>(a, ep, h, key, page, cand, force, false, qe, L);
   }
 }
 
