@@ -34,7 +34,6 @@ constexpr int kFT = 512;
 constexpr int kFW = kFT / kWave;
 constexpr int kFScorePages = 128;
 constexpr int kFSpin = 1 << 20;
-constexpr int kMaxParts = 3 * PRR_MAX_CAP_DEV;  // partial states per KV head (chunk 1)
 constexpr uint32_t kSelfMiss = 0x80000000u;  // missed-list count flags: attended by the select workgroup
 constexpr uint32_t kDropSpec = 0x40000000u;  //   the speculation is discarded (recompute on a miss)
 constexpr uint32_t kCountMask = 0x3fffffffu;
@@ -82,6 +81,7 @@ struct FSelLds {
   union {
     Sel2Lds sel;       // block-wide select
     WSelLds ws[3];     // one-wave selects: A, and the next step's bounds of A and of late pages
+    BSelLds bsel;      // threshold of A by the whole workgroup (in place of ws[0])
   };
   uint32_t bitP[PRR_MAX_PAGES_DEV / 32];
   uint32_t forceb[PRR_MAX_PAGES_DEV / 32];
@@ -96,6 +96,8 @@ struct FSelLds {
   int npv;
 };
 
+static_assert(sizeof(BSelLds) <= sizeof(WSelLds), "bsel lies inside ws[0]");
+
 struct FAttnLds {
   float wo[kFW][16][kFOPad];
   float wm[kFW][16];
@@ -103,9 +105,7 @@ struct FAttnLds {
 };
 
 struct FMergeLds {
-  float w[kMaxParts];  // l, then the weight, of each state
-  float m[kMaxParts];
-  float red[2][kFW];
+  float red[2][kFW];  // running max and sum of each wave
   float acc[kFW][kHeadDim];
 };
 
@@ -150,36 +150,33 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   float lv[2] = {0.f, 0.f}, tv[2] = {0.f, 0.f};
   uint32_t bw[2] = {0u, 0u};
   const int nwmax = (a.max_pages + 31) / 32;
-  {
-    const int g = t >> 4, c8 = (t & 15) * 8;
-    if (g < G) {
-      const uint4 v = *reinterpret_cast<const uint4*>(q + (size_t)(h * G + g) * kHeadDim + c8);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) S.qpart[g][c8 + e] = u4_elem<BF16>(v, e);
-    }
-    if (t < 4) S.fbits[t] = 0u;
-    __syncthreads();
-    if (t < kHeadDim) {
-      float s = 0.0f;
-      for (int gg = 0; gg < G; ++gg) s += S.qpart[gg][t];
-      S.qbar[t] = s / (float)G;
-    }
-    if (t == 0 && a.n_forced > 0) {
-      // forced pages of this workgroup's range (the list lives in the kernel arguments:
-      // constant indices only)
-#pragma unroll
-      for (int i = 0; i < PRR_MAX_FORCED; ++i) {
-        if (i >= a.n_forced) break;
-        const int p = a.forced[i] - pbase;
-        if (p >= 0 && p < kFScorePages) S.fbits[p >> 5] |= 1u << (p & 31);
-      }
-    }
-    __syncthreads();
-  }
+  // the query first, then this thread's metadata, so that q-bar is formed while the
+  // metadata is still in flight (loads complete in issue order)
+  const int g16 = t >> 4, c8 = (t & 15) * 8;
+  uint4 qv = make_uint4(0, 0, 0, 0);
+  if (g16 < G) qv = *reinterpret_cast<const uint4*>(q + (size_t)(h * G + g16) * kHeadDim + c8);
   const int cg = lane & 15, pi = lane >> 4;
-  float qb[8];
+  const int base = pbase + w * 16 + pi;
+  uint4 mn[4], mx[4];
+  float4 m0[4], m1[4];
+  if (!a.meta_mean) {
 #pragma unroll
-  for (int e = 0; e < 8; ++e) qb[e] = S.qbar[cg * 8 + e];
+    for (int it = 0; it < 4; ++it) {
+      const int p = min(base + 4 * it, n - 1);
+      const uint16_t* row = static_cast<const uint16_t*>(a.meta) + ((size_t)h * a.max_pages + p) * 2 * kHeadDim + cg * 8;
+      mn[it] = *reinterpret_cast<const uint4*>(row);
+      mx[it] = *reinterpret_cast<const uint4*>(row + kHeadDim);
+    }
+  } else {
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int p = min(base + 4 * it, n - 1);
+      const float4* row = reinterpret_cast<const float4*>(static_cast<const float*>(a.meta) +
+                                                          ((size_t)h * a.max_pages + p) * kHeadDim + cg * 8);
+      m0[it] = row[0];
+      m1[it] = row[1];
+    }
+  }
   // wave 0 filters: EMA state of pages pbase + lane and pbase + 64 + lane, and the
   // candidate bounds kept from the previous step as ratios: of A and of late pages to
   // |q-bar|_1 (scores scale with q-bar), of the next prediction to the EMA of |q-bar|_1
@@ -206,19 +203,38 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
       }
     }
   }
-  const int base = pbase + w * 16 + pi;
+  {
+    const int g = g16;
+    if (g < G) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) S.qpart[g][c8 + e] = u4_elem<BF16>(qv, e);
+    }
+    if (t < 4) S.fbits[t] = 0u;
+    __syncthreads();
+    if (t < kHeadDim) {
+      float s = 0.0f;
+      for (int gg = 0; gg < G; ++gg) s += S.qpart[gg][t];
+      S.qbar[t] = s / (float)G;
+    }
+    if (t == 0 && a.n_forced > 0) {
+      // forced pages of this workgroup's range (the list lives in the kernel arguments:
+      // constant indices only)
+#pragma unroll
+      for (int i = 0; i < PRR_MAX_FORCED; ++i) {
+        if (i >= a.n_forced) break;
+        const int p = a.forced[i] - pbase;
+        if (p >= 0 && p < kFScorePages) S.fbits[p >> 5] |= 1u << (p & 31);
+      }
+    }
+    __syncthreads();
+  }
+  float qb[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) qb[e] = S.qbar[cg * 8 + e];
   float* scores = a.scores + (size_t)h * a.max_pages;
   uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
   float s[4];
   if (!a.meta_mean) {
-    uint4 mn[4], mx[4];
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int p = min(base + 4 * it, n - 1);
-      const uint16_t* row = static_cast<const uint16_t*>(a.meta) + ((size_t)h * a.max_pages + p) * 2 * kHeadDim + cg * 8;
-      mn[it] = *reinterpret_cast<const uint4*>(row);
-      mx[it] = *reinterpret_cast<const uint4*>(row + kHeadDim);
-    }
 #pragma unroll
     for (int it = 0; it < 4; ++it) {
       float v = 0.0f;
@@ -227,15 +243,6 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
       s[it] = v;
     }
   } else {
-    float4 m0[4], m1[4];
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int p = min(base + 4 * it, n - 1);
-      const float4* row = reinterpret_cast<const float4*>(static_cast<const float*>(a.meta) +
-                                                          ((size_t)h * a.max_pages + p) * kHeadDim + cg * 8);
-      m0[it] = row[0];
-      m1[it] = row[1];
-    }
 #pragma unroll
     for (int it = 0; it < 4; ++it) {
       float v = qb[0] * m0[it].x;
@@ -924,7 +931,8 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
 // the list to attend, and writes the outputs, with no barrier; waves 1 and 2 meanwhile
 // derive the next step's candidate bounds from the same list.
 template <bool BF16, int PS>
-__device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, int h, int total, float qn, FLds& U) {
+__device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, int h, int total, float qn,
+                                            const SelThreshold& th, FLds& U) {
   FSelLds& L = U.sel;
   constexpr int NK = kCandWave / kWave;
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
@@ -959,13 +967,9 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
     if (v && ((pw[j] >> (page[j] & 31)) & 1u)) inP |= 1ull << j;
   }
   if (w == 0) {
-    const SelThreshold th = wsel_threshold<NK>(key, cand, a.kextra_a, L.ws[0], true);
+    // the threshold was published already unless a tie at T is cut by page order
     const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
     uint64_t* thr = a.t_thr + 2 * (size_t)h;
-    if (prr && early && lane == 0) {
-      put_tag(thr, th.T, ep);
-      put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
-    }
     int eq_cut = kEqAll;
     const uint64_t inA = wsel_membership<NK>(key, page, cand, force, th, &eq_cut);
     if (prr && !early) {
@@ -1099,7 +1103,23 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, uint32_t ep, i
   const float qn = qbar_finish(a, qv, L.qb);
   const FCand c = cand_load<true>(a, ep, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
   if (a.kextra_a <= c.total - c.nforced && c.total <= kCandWave) {
-    select_wave<BF16, PS>(a, ep, h, c.total, qn, U);
+    // the threshold by the whole workgroup straight from the list (two keys per thread),
+    // published at once when no tie at T needs cutting; the one-wave pass that follows
+    // derives the sets and lists from it
+    uint32_t k2[2];
+    bool c2[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int i = t + kFT * j;  // < kCandWave <= 2 kFT
+      k2[j] = L.ck[i];
+      c2[j] = i < c.total && !(L.cpg[i] >> 31);
+    }
+    const SelThreshold th = bsel_threshold<kFT>(k2, c2, a.kextra_a, L.bsel);
+    if (a.schedule == 1 && t == 0 && (th.mode != 2 || th.need_eq >= th.eq_total)) {
+      put_tag(a.t_thr + 2 * (size_t)h, th.T, ep);
+      put_tag(a.t_thr + 2 * (size_t)h + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
+    }
+    select_wave<BF16, PS>(a, ep, h, c.total, qn, th, U);
   } else if (a.kextra_a <= c.total - c.nforced && c.total <= kCandMax) {
     // one instantiation per path keeps the kernel's code (and its instruction-cache
     // footprint) small: 4 candidate slots per thread, 16 page slots in the fallback
@@ -1453,71 +1473,73 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, uint32_t ep, in
   const int gap1 = a.n_spec - nspec, gap2 = a.n_spec + a.n_miss - nspec - nmiss;
 #define PRR_SLOT(i) ((size_t)((i) < nspec ? (i) : ((i) < nspec + nmiss ? (i) + gap1 : (i) + gap2)) * G)
 
-  // Only the (m, l) of every state are polled (threads t, t+512, ..); the output values
-  // of a state are complete once its (m, l) are current.
-  float mt = kNegInf;
-  for (int i = t; i < total; i += kFT) {
+  // Wave w merges states w, w + 8, .. on its own (no barrier until the end): lane k polls
+  // the (m, l) of state w + 8k (the outputs of a state are complete once its (m, l) are
+  // current), then the wave loads the outputs of its states, lane l columns 2l and 2l + 1,
+  // and folds them in state order into a running (max, sum, output).
+  float Mw = kNegInf, Lw = 0.0f, ax = 0.0f, ay = 0.0f;
+  const int nk = total > w ? (total - w + kFW - 1) / kFW : 0;
+  for (int k0 = 0; k0 < nk; k0 += kWave) {
+    const int k = k0 + lane;
+    const bool mine = k < nk;
+    const uint64_t* p = pml + PRR_SLOT(w + kFW * min(k, nk - 1)) * 2;
     uint64_t vm = 0, vl = 0;
-    const uint64_t* p = pml + PRR_SLOT(i) * 2;
     for (int it = 0; it < kFSpin; ++it) {
       vm = get_tag(p);
       vl = get_tag(p + 1);
-      if (tag_is(vm, ep) && tag_is(vl, ep)) break;
+      if (__ballot(mine && !(tag_is(vm, ep) && tag_is(vl, ep))) == 0ull) break;
       __builtin_amdgcn_s_sleep(2);
-      if (it == kFSpin - 1) atomicOr(a.flags, kFlagSpinTimeout);
+      if (it == kFSpin - 1 && lane == 0) atomicOr(a.flags, kFlagSpinTimeout);
     }
-    L.m[i] = __uint_as_float((uint32_t)vm);
-    L.w[i] = __uint_as_float((uint32_t)vl);
-  }
-  for (int i = t; i < total; i += kFT)
-    if (L.w[i] > 0.0f) mt = fmaxf(mt, L.m[i]);
-  mt = wave_max(mt);
-  if (lane == 0) L.red[0][w] = mt;
-  __syncthreads();
-  float M = kNegInf;
+    const float li = mine ? __uint_as_float((uint32_t)vl) : 0.0f;
+    const float mi = li > 0.0f ? __uint_as_float((uint32_t)vm) : kNegInf;
+    const float Mn = fmaxf(Mw, wave_max(mi));
+    if (Mn == kNegInf) continue;  // no state of this batch holds anything
+    const float sc = Lw > 0.0f ? exp2f((Mw - Mn) * kLog2e) : 0.0f;
+    ax *= sc;
+    ay *= sc;
+    const float wi = li > 0.0f ? li * exp2f((mi - Mn) * kLog2e) : 0.0f;
+    Lw = Lw * sc + wave_sum(wi);
+    Mw = Mn;
+    const int nb = min(kWave, nk - k0);
+    constexpr int kB = 8;
+    for (int b0 = 0; b0 < nb; b0 += kB) {
+      uint64_t ov[kB];
 #pragma unroll
-  for (int i = 0; i < kFW; ++i) M = fmaxf(M, L.red[0][i]);
-  float lsum_part = 0.0f;
-  for (int i = t; i < total; i += kFT) {
-    const float li = L.w[i];
-    const float wi = li > 0.0f ? li * exp2f((L.m[i] - M) * kLog2e) : 0.0f;
-    lsum_part += wi;
-    L.w[i] = wi;
-  }
-  lsum_part = wave_sum(lsum_part);
-  if (lane == 0) L.red[1][w] = lsum_part;
-  __syncthreads();
-  float Lsum = 0.0f;
+      for (int r = 0; r < kB; ++r) {
+        const int i = w + kFW * (k0 + min(b0 + r, nb - 1));
+        ov[r] = __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<float*>(po + PRR_SLOT(i) * kHeadDim)) + lane,
+                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
 #pragma unroll
-  for (int i = 0; i < kFW; ++i) Lsum += L.red[1][i];
-
-  // wave w sums states w, w + 8, ..; lane l columns 2l and 2l + 1 (all loads of a batch
-  // are issued before any is used; indices past the last state repeat it with weight 0)
-  constexpr int kB = 8;
-  float ax = 0.0f, ay = 0.0f;
-  for (int b0 = 0; b0 < total; b0 += kFW * kB) {
-    uint64_t ov[kB];
-#pragma unroll
-    for (int r = 0; r < kB; ++r) {
-      const int i = min(b0 + w + kFW * r, total - 1);
-      ov[r] = __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<float*>(po + PRR_SLOT(i) * kHeadDim)) + lane,
-                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-#pragma unroll
-    for (int r = 0; r < kB; ++r) {
-      const int i = b0 + w + kFW * r;
-      const float wi = i < total ? L.w[i] : 0.0f;
-      ax += wi * __uint_as_float((uint32_t)ov[r]);
-      ay += wi * __uint_as_float((uint32_t)(ov[r] >> 32));
+      for (int r = 0; r < kB; ++r) {
+        const float wr = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wi), min(b0 + r, kWave - 1)));
+        const float wgt = b0 + r < nb ? wr : 0.0f;
+        ax += wgt * __uint_as_float((uint32_t)ov[r]);
+        ay += wgt * __uint_as_float((uint32_t)(ov[r] >> 32));
+      }
     }
   }
   *reinterpret_cast<float2*>(&L.acc[w][2 * lane]) = make_float2(ax, ay);
+  if (lane == 0) {
+    L.red[0][w] = Mw;
+    L.red[1][w] = Lw;
+  }
   __syncthreads();
   if (t < kHeadDim) {
     const int c = t;
-    float sum = 0.0f;
+    float M = kNegInf;
 #pragma unroll
-    for (int ww = 0; ww < kFW; ++ww) sum += L.acc[ww][c];
+    for (int ww = 0; ww < kFW; ++ww)
+      if (L.red[1][ww] > 0.0f) M = fmaxf(M, L.red[0][ww]);
+    float Lsum = 0.0f, sum = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < kFW; ++ww) {
+      const float lw = L.red[1][ww];
+      const float f = lw > 0.0f ? exp2f((L.red[0][ww] - M) * kLog2e) : 0.0f;
+      Lsum += lw * f;
+      sum += L.acc[ww][c] * f;
+    }
     const float o = Lsum > 0.0f ? sum / Lsum : 0.0f;
     const size_t row = (size_t)h * G + qn;
     a.out_o32[row * kHeadDim + c] = o;

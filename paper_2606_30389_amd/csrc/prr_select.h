@@ -483,3 +483,136 @@ __device__ __forceinline__ uint64_t wsel_membership(const uint32_t (&key)[NK], c
 }
 
 }  // namespace prr
+
+namespace prr {
+
+// ------------------------------------------------------------ block select of <= 1024 keys
+// The threshold of the same exact top-K for at most 2 * NT keys, two per thread, without
+// gathering them into one wave: every pass builds the histogram of the current key range
+// with LDS atomics, scans it (four bins per thread, DPP prefix within the wave, wave
+// totals through LDS) and keeps the bin holding the wanted rank, until that bin holds a
+// single key or a single value.  The bins of `hist` must be zero on entry (they are left
+// nonzero).
+
+struct BSelLds {
+  uint32_t hist[kSel2Bins];
+  uint32_t red[2][16];
+  int res[4];
+};
+
+template <int NT>
+__device__ __forceinline__ SelThreshold bsel_threshold(const uint32_t (&key)[2], const bool (&cand)[2], int kextra,
+                                                       BSelLds& S) {
+  static_assert(NT == 512, "four bins per thread");
+  constexpr int NW = NT / kWave;
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  uint32_t lo = 0xffffffffu, hi = 0u;
+  int cnt = 0;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (cand[j]) {
+      lo = min(lo, key[j]);
+      hi = max(hi, key[j]);
+      ++cnt;
+    }
+  }
+  lo = wave_umin(lo);
+  hi = wave_umax(hi);
+  cnt = wave_isum(cnt);
+  if (lane == 0) {
+    S.red[0][w] = lo;
+    S.red[1][w] = hi;
+    S.red[0][NW + w] = (uint32_t)cnt;
+  }
+  __syncthreads();
+  cnt = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    lo = min(lo, S.red[0][i]);
+    hi = max(hi, S.red[1][i]);
+    cnt += (int)S.red[0][NW + i];
+  }
+  SelThreshold r;
+  r.mode = 0;
+  r.T = 0;
+  r.need_eq = 0;
+  r.eq_total = 0;
+  if (kextra <= 0 || cnt == 0) return r;
+  if (kextra >= cnt) {
+    r.mode = 1;
+    return r;
+  }
+  r.mode = 2;
+  int rank = kextra, inrange = cnt;
+  // thread t owns bins [2048 - 4(t+1), 2048 - 4t) (bins in descending key order)
+  const int b0 = kSel2Bins - 4 * (t + 1);
+  for (int pass = 0; pass < 3; ++pass) {
+    const uint32_t range = hi - lo;
+    if (range == 0) break;
+    const int bits = 32 - __clz(range);
+    const int shift = bits > kSel2Log2Bins ? bits - kSel2Log2Bins : 0;
+    if (pass > 0) {
+      reinterpret_cast<uint4*>(S.hist)[t] = make_uint4(0, 0, 0, 0);
+      __syncthreads();
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      if (cand[j] && key[j] >= lo && key[j] <= hi) atomicAdd(&S.hist[(key[j] - lo) >> shift], 1u);
+    __syncthreads();
+    const uint4 hv = reinterpret_cast<const uint4*>(S.hist)[b0 / 4];
+    const int s = (int)(hv.x + hv.y + hv.z + hv.w);
+    const int incl = wave_inclusive_scan(s);
+    if (lane == kWave - 1) S.red[1][w] = (uint32_t)incl;
+    __syncthreads();
+    int before = incl - s;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) before += i < w ? (int)S.red[1][i] : 0;
+    if (before < rank && rank <= before + s) {
+      // descending: bins b0+3, b0+2, b0+1, b0
+      const int c3 = (int)hv.w, c2 = (int)hv.z, c1 = (int)hv.y;
+      int bstar, above;
+      if (rank <= before + c3) {
+        bstar = b0 + 3;
+        above = before;
+      } else if (rank <= before + c3 + c2) {
+        bstar = b0 + 2;
+        above = before + c3;
+      } else if (rank <= before + c3 + c2 + c1) {
+        bstar = b0 + 1;
+        above = before + c3 + c2;
+      } else {
+        bstar = b0;
+        above = before + c3 + c2 + c1;
+      }
+      S.res[0] = bstar;
+      S.res[1] = above;
+      S.res[2] = (int)S.hist[bstar];
+    }
+    __syncthreads();
+    const int bstar = S.res[0], cbin = S.res[2];
+    rank -= S.res[1];
+    inrange = cbin;
+    const uint32_t nlo = lo + ((uint32_t)bstar << shift);
+    hi = (uint32_t)min((uint64_t)hi, (uint64_t)nlo + ((1ull << shift) - 1ull));
+    lo = nlo;
+    if (shift == 0) break;
+    if (cbin == 1) {
+      // the single key of the bin is T: its holder publishes it
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        if (cand[j] && key[j] >= lo && key[j] <= hi) S.res[3] = (int)key[j];
+      __syncthreads();
+      r.T = (uint32_t)S.res[3];
+      r.need_eq = rank;
+      r.eq_total = 1;
+      return r;
+    }
+  }
+  // a bin of one value (or three passes): every key in [lo, hi] equals lo
+  r.T = lo;
+  r.need_eq = rank;
+  r.eq_total = inrange;
+  return r;
+}
+
+}  // namespace prr
