@@ -932,7 +932,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
 // derive the next step's candidate bounds from the same list.
 template <bool BF16, int PS>
 __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, int h, int total, float qn,
-                                            const SelThreshold& th, FLds& U) {
+                                            const SelThreshold& th, int nM_done, FLds& U) {
   FSelLds& L = U.sel;
   constexpr int NK = kCandWave / kWave;
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
@@ -980,9 +980,10 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
       }
     }
     // pages of late speculation: flagged, within the late capacity, never in P^t
+    // (nM_done >= 0: the missed list was published by the whole workgroup already)
     uint64_t inLate = 0;
     int ltot = 0;
-    if (a.late) {
+    if (a.late && nM_done < 0) {
       const int capl = a.n_late * a.chunk;
 #pragma unroll
       for (int j = 0; j < NK; ++j) {
@@ -994,27 +995,30 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
       if (lane == 0) put_tag(&a.t_lcnt[h], (uint32_t)min(ltot, capl), ep);
     }
     const int nMiss = prr ? wave_isum(__popcll(inA & ~inP)) : 0;
-    const bool drop = prr && a.mode == PRR_RECOMPUTE_ON_MISS && nMiss > 0;
-    const uint64_t inM = (prr && !drop) ? (inA & ~inP & ~inLate) : inA;
-    const uint32_t mflags = drop ? kDropSpec : 0u;
-    const int nM = min(wave_isum(__popcll(inM)), a.cap);
-    uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
-    int pos = 0;
+    int nM = nM_done;
+    if (nM_done < 0) {
+      const bool drop = prr && a.mode == PRR_RECOMPUTE_ON_MISS && nMiss > 0;
+      const uint64_t inM = (prr && !drop) ? (inA & ~inP & ~inLate) : inA;
+      const uint32_t mflags = drop ? kDropSpec : 0u;
+      nM = min(wave_isum(__popcll(inM)), a.cap);
+      uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
+      int pos = 0;
 #pragma unroll
-    for (int j = 0; j < NK; ++j) {
-      const bool in = (inM >> j) & 1ull;
-      const uint64_t bm = __ballot(in);
-      const int q = pos + lanes_below(bm);
-      if (in && q < a.cap) {
-        L.mlist[q] = page[j];
-        if (nM > kFW) put_tag(&ml[q], (uint32_t)page[j], ep);
+      for (int j = 0; j < NK; ++j) {
+        const bool in = (inM >> j) & 1ull;
+        const uint64_t bm = __ballot(in);
+        const int q = pos + lanes_below(bm);
+        if (in && q < a.cap) {
+          L.mlist[q] = page[j];
+          if (nM > kFW) put_tag(&ml[q], (uint32_t)page[j], ep);
+        }
+        pos += __popcll(bm);
       }
-      pos += __popcll(bm);
-    }
-    if (lane == 0) {
-      const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
-      put_tag(&a.t_mcnt[h], (uint32_t)nM | mflags | self, ep);
-      L.cnt[0][0] = nM;
+      if (lane == 0) {
+        const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
+        put_tag(&a.t_mcnt[h], (uint32_t)nM | mflags | self, ep);
+        L.cnt[0][0] = nM;
+      }
     }
     // the selected list (an output) and the counts
     int32_t* sel = a.selected + (size_t)h * a.cap;
@@ -1052,6 +1056,74 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
     fold_publish<1>(a, ep, h, a.n_spec, st, 1u, U.attn);
   }
+}
+
+// The missed list M = A \ P \ (late-covered pages) (serial schedule: A) by the whole
+// workgroup right after the threshold, when no tie at T is cut (membership is then
+// key >= T); slot i = t + 512 j of the candidate list, two per thread.  Publishes M,
+// its count and the number of late-covered pages; returns |M|.
+__device__ __forceinline__ int miss_block(const FusedLaunch& a, uint32_t ep, int h, int total, const SelThreshold& th,
+                                          const uint32_t (&k2)[2], FSelLds& L) {
+  const int t = threadIdx.x;
+  const bool prr = a.schedule == 1;
+  const int capl = a.late ? a.n_late * a.chunk : 0;
+  bool inA[2], late[2], inP[2];
+  int pg[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int i = t + kFT * j;
+    const uint32_t pv = L.cpg[i];
+    const bool v = i < total;
+    pg[j] = v ? (int)(pv & 0x3fffffffu) : 0;
+    const bool forced = v && (pv >> 31);
+    inA[j] = forced || (v && (th.mode == 1 || (th.mode == 2 && k2[j] >= th.T)));
+    late[j] = v && a.late && ((pv >> 30) & 1u);
+    inP[j] = prr && v && bit_of(L.bitP, pg[j]);
+  }
+  // late-covered: flagged, among the first capl flagged slots, not in P^t
+  int tot_l;
+  const int el = block_exclusive_scan<kFT>((int)late[0] | ((int)late[1] << 16), L.cnt[1], tot_l);
+  const int l0 = tot_l & 0xffff;
+  const int pl[2] = {el & 0xffff, l0 + (el >> 16)};
+  bool mM[2], mA[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const bool cov = late[j] && pl[j] < capl && !inP[j];
+    mA[j] = inA[j] && !inP[j];
+    mM[j] = prr ? (mA[j] && !cov) : inA[j];
+  }
+  int tot_m;
+  const int em = block_exclusive_scan<kFT>((int)mM[0] | ((int)mM[1] << 10) | (((int)mA[0] + (int)mA[1]) << 20),
+                                          L.cnt[1], tot_m);
+  const int nMiss = tot_m >> 20;
+  const bool drop = prr && a.mode == PRR_RECOMPUTE_ON_MISS && nMiss > 0;
+  int q[2] = {em & 0x3ff, (tot_m & 0x3ff) + ((em >> 10) & 0x3ff)};
+  int nM = (tot_m & 0x3ff) + ((tot_m >> 10) & 0x3ff);
+  if (drop) {  // the speculation is discarded: M = A
+    int tot_a;
+    const int ea = block_exclusive_scan<kFT>((int)inA[0] | ((int)inA[1] << 16), L.cnt[1], tot_a);
+    mM[0] = inA[0];
+    mM[1] = inA[1];
+    q[0] = ea & 0xffff;
+    q[1] = (tot_a & 0xffff) + (ea >> 16);
+    nM = (tot_a & 0xffff) + (tot_a >> 16);
+  }
+  nM = min(nM, a.cap);
+  uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (mM[j] && q[j] < a.cap) {
+      L.mlist[q[j]] = pg[j];
+      if (nM > kFW) put_tag(&ml[q[j]], (uint32_t)pg[j], ep);
+    }
+  }
+  if (t == 0) {
+    const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
+    put_tag(&a.t_mcnt[h], (uint32_t)nM | (drop ? kDropSpec : 0u) | self, ep);
+    if (a.late) put_tag(&a.t_lcnt[h], (uint32_t)min(l0 + (tot_l >> 16), capl), ep);
+    L.cnt[0][0] = nM;
+  }
+  return nM;
 }
 
 template <bool BF16, int PS>
@@ -1115,11 +1187,13 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, uint32_t ep, i
       c2[j] = i < c.total && !(L.cpg[i] >> 31);
     }
     const SelThreshold th = bsel_threshold<kFT>(k2, c2, a.kextra_a, L.bsel);
-    if (a.schedule == 1 && t == 0 && (th.mode != 2 || th.need_eq >= th.eq_total)) {
+    const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
+    if (a.schedule == 1 && t == 0 && early) {
       put_tag(a.t_thr + 2 * (size_t)h, th.T, ep);
       put_tag(a.t_thr + 2 * (size_t)h + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
     }
-    select_wave<BF16, PS>(a, ep, h, c.total, qn, th, U);
+    const int nM = early ? miss_block(a, ep, h, c.total, th, k2, L) : -1;
+    select_wave<BF16, PS>(a, ep, h, c.total, qn, th, nM, U);
   } else if (a.kextra_a <= c.total - c.nforced && c.total <= kCandMax) {
     // one instantiation per path keeps the kernel's code (and its instruction-cache
     // footprint) small: 4 candidate slots per thread, 16 page slots in the fallback
