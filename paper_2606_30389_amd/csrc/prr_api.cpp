@@ -95,10 +95,11 @@ bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
   L.nparts = 3 * L.nchunks;
   L.f_score = off;
   off = align_up(off + (size_t)hkv * d->max_pages * 8, 256);
+  // the threshold, missed and late counts: 8 copies of 256 bytes per KV head
   L.f_thr = off;
-  off = align_up(off + (size_t)hkv * 2 * 8, 256);
+  off = align_up(off + (size_t)hkv * 8 * 256, 256);
   L.f_mcnt = off;
-  off = align_up(off + (size_t)hkv * 8, 256);
+  off = align_up(off + (size_t)hkv * 8 * 256, 256);
   L.f_mlist = off;
   off = align_up(off + (size_t)hkv * cap * 8, 256);
   L.f_part = off;
@@ -115,7 +116,7 @@ bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
   L.f_win = off;
   off = align_up(off + (size_t)hkv * 4 * 4, 256);
   L.f_lcnt = off;
-  off = align_up(off + (size_t)hkv * 8, 256);
+  off = align_up(off + (size_t)hkv * 8 * 256, 256);
   L.f_pbits = off;
   off = align_up(off + 2 * (size_t)hkv * ((d->max_pages + 31) / 32) * 4, 256);
   L.total = off;

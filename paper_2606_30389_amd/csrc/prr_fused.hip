@@ -68,6 +68,21 @@ __device__ __forceinline__ uint32_t wait_tag(const uint64_t* p, uint32_t epoch, 
   return tagged(get_tag(p), p, epoch, flags);
 }
 
+// A value that many workgroups wait for (the threshold, the missed and late counts) is
+// stored in kRep copies 256 bytes apart, and each waiting workgroup polls one of them, so
+// that the polls spread over memory channels instead of queueing on one line.  Record of
+// KV head h: kRep copies of kRepStride words; word k of copy c.
+constexpr int kRep = 8;
+constexpr int kRepStride = 32;
+__device__ __forceinline__ uint64_t* rep_at(uint64_t* base, int h, int c) {
+  return base + ((size_t)h * kRep + (c & (kRep - 1))) * kRepStride;
+}
+// stores word k of every copy (one thread)
+__device__ __forceinline__ void put_rep(uint64_t* base, int h, int k, uint32_t v, uint32_t epoch) {
+#pragma unroll
+  for (int c = 0; c < kRep; ++c) put_tag(rep_at(base, h, c) + k, v, epoch);
+}
+
 // ------------------------------------------------------------------------ LDS
 
 struct FScoreLds {
@@ -838,17 +853,16 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
   }
   const SelThreshold th = sel2_threshold<kFT, J>(key, cand, a.kextra_a, L.sel);
   const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
-  uint64_t* thr = a.t_thr + 2 * (size_t)h;
   if (prr && early && t == 0) {
-    put_tag(thr, th.T, ep);
-    put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
+    put_rep(a.t_thr, h, 0, th.T, ep);
+    put_rep(a.t_thr, h, 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
   }
   const uint64_t inA = sel2_membership<kFT, J>(key, page, cand, force, th, &L.eq_cut, L.sel);
   if (prr && !early) {
     __syncthreads();
     if (t == 0) {
-      put_tag(thr, th.T, ep);
-      put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)L.eq_cut << 2), ep);
+      put_rep(a.t_thr, h, 0, th.T, ep);
+      put_rep(a.t_thr, h, 1, (uint32_t)th.mode | ((uint32_t)L.eq_cut << 2), ep);
     }
   }
 
@@ -878,7 +892,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
       if (f && run + lanes_below(bm) < capl && !((inP >> j) & 1ull)) inLate |= 1ull << j;
       run += __popcll(bm);
     }
-    if (t == 0) put_tag(&a.t_lcnt[h], (uint32_t)min(ltot, capl), ep);
+    if (t == 0) put_rep(a.t_lcnt, h, 0, (uint32_t)min(ltot, capl), ep);
   }
   // the list to attend after selection, in page order: A \ P (PRR; also without the
   // late-speculated pages) or A (serial, or a PRR step whose speculation is discarded
@@ -890,11 +904,11 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
   const int nM = min(sel2_list<kFT, J>(inM, page, L.mlist, a.cap, L.sel), a.cap);
   __syncthreads();
   if (nM == 0) {
-    if (t == 0) put_tag(&a.t_mcnt[h], mflags, ep);
+    if (t == 0) put_rep(a.t_mcnt, h, 0, mflags, ep);
   } else if (nM > kFW) {
     uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
     for (int i = t; i < nM; i += kFT) put_tag(&ml[i], (uint32_t)L.mlist[i], ep);
-    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM | mflags, ep);
+    if (t == 0) put_rep(a.t_mcnt, h, 0, (uint32_t)nM | mflags, ep);
   }
   // the selected list (an output) and the counts
   int32_t* sel = a.selected + (size_t)h * a.cap;
@@ -913,7 +927,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
   }
   if (nM > 0 && nM <= kFW) {
     // few enough to attend here: one page per wave, published as the first miss slot
-    if (t == 0) put_tag(&a.t_mcnt[h], (uint32_t)nM | kSelfMiss | mflags, ep);
+    if (t == 0) put_rep(a.t_mcnt, h, 0, (uint32_t)nM | kSelfMiss | mflags, ep);
     int pg[1];
     pg[0] = __builtin_amdgcn_readfirstlane(w < nM ? L.mlist[w] : -1);
     __syncthreads();  // the list is read before the attention reuses the LDS
@@ -969,14 +983,13 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
   if (w == 0) {
     // the threshold was published already unless a tie at T is cut by page order
     const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
-    uint64_t* thr = a.t_thr + 2 * (size_t)h;
     int eq_cut = kEqAll;
     const uint64_t inA = wsel_membership<NK>(key, page, cand, force, th, &eq_cut);
     if (prr && !early) {
       eq_cut = __builtin_amdgcn_readfirstlane(wave_umin((uint32_t)eq_cut));
       if (lane == 0) {
-        put_tag(thr, th.T, ep);
-        put_tag(thr + 1, (uint32_t)th.mode | ((uint32_t)eq_cut << 2), ep);
+        put_rep(a.t_thr, h, 0, th.T, ep);
+        put_rep(a.t_thr, h, 1, (uint32_t)th.mode | ((uint32_t)eq_cut << 2), ep);
       }
     }
     // pages of late speculation: flagged, within the late capacity, never in P^t
@@ -992,7 +1005,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
         if (f && ltot + lanes_below(bm) < capl && !((inP >> j) & 1ull)) inLate |= 1ull << j;
         ltot += __popcll(bm);
       }
-      if (lane == 0) put_tag(&a.t_lcnt[h], (uint32_t)min(ltot, capl), ep);
+      if (lane == 0) put_rep(a.t_lcnt, h, 0, (uint32_t)min(ltot, capl), ep);
     }
     const int nMiss = prr ? wave_isum(__popcll(inA & ~inP)) : 0;
     int nM = nM_done;
@@ -1016,7 +1029,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
       }
       if (lane == 0) {
         const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
-        put_tag(&a.t_mcnt[h], (uint32_t)nM | mflags | self, ep);
+        put_rep(a.t_mcnt, h, 0, (uint32_t)nM | mflags | self, ep);
         L.cnt[0][0] = nM;
       }
     }
@@ -1119,8 +1132,8 @@ __device__ __forceinline__ int miss_block(const FusedLaunch& a, uint32_t ep, int
   }
   if (t == 0) {
     const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
-    put_tag(&a.t_mcnt[h], (uint32_t)nM | (drop ? kDropSpec : 0u) | self, ep);
-    if (a.late) put_tag(&a.t_lcnt[h], (uint32_t)min(l0 + (tot_l >> 16), capl), ep);
+    put_rep(a.t_mcnt, h, 0, (uint32_t)nM | (drop ? kDropSpec : 0u) | self, ep);
+    if (a.late) put_rep(a.t_lcnt, h, 0, (uint32_t)min(l0 + (tot_l >> 16), capl), ep);
     L.cnt[0][0] = nM;
   }
   return nM;
@@ -1189,8 +1202,8 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, uint32_t ep, i
     const SelThreshold th = bsel_threshold<kFT>(k2, c2, a.kextra_a, L.bsel);
     const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
     if (a.schedule == 1 && t == 0 && early) {
-      put_tag(a.t_thr + 2 * (size_t)h, th.T, ep);
-      put_tag(a.t_thr + 2 * (size_t)h + 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
+      put_rep(a.t_thr, h, 0, th.T, ep);
+      put_rep(a.t_thr, h, 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
     }
     const int nM = early ? miss_block(a, ep, h, c.total, th, k2, L) : -1;
     select_wave<BF16, PS>(a, ep, h, c.total, qn, th, nM, U);
@@ -1345,7 +1358,7 @@ __device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, uint32_t ep,
 #pragma unroll
   for (int k = 0; k < NPW; ++k) vs[k] = keep ? get_tag(&ts[max(pg[k], 0)]) : 0ull;
   if (threadIdx.x < kWave) {
-    const uint64_t* thr = a.t_thr + 2 * (size_t)h;
+    const uint64_t* thr = rep_at(a.t_thr, h, blockIdx.x);
     uint64_t v0 = 0, v1 = 0;
     for (int it = 0; it < kFSpin; ++it) {
       v0 = get_tag(thr);
@@ -1472,7 +1485,7 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int
     const int i = start + lane;
     uint64_t vm = 0, ve = 0;
     for (int it = 0; it < kFSpin; ++it) {
-      vm = get_tag(a.t_mcnt + h);
+      vm = get_tag(rep_at(a.t_mcnt, h, u));
       ve = get_tag(&ml[min(i, a.cap - 1)]);
       if (tag_is(vm, ep)) {
         const uint32_t mv = (uint32_t)vm;
@@ -1522,8 +1535,8 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, uint32_t ep, in
   if (t < kWave) {
     uint64_t v0 = 0, v1 = 0;
     for (int it = 0; it < kFSpin; ++it) {
-      v0 = get_tag(a.t_mcnt + h);
-      v1 = a.late ? get_tag(a.t_lcnt + h) : ((uint64_t)ep << 32);
+      v0 = get_tag(rep_at(a.t_mcnt, h, qn));
+      v1 = a.late ? get_tag(rep_at(a.t_lcnt, h, qn)) : ((uint64_t)ep << 32);
       if (tag_is(v0, ep) && tag_is(v1, ep)) break;
       __builtin_amdgcn_s_sleep(2);
       if (it == kFSpin - 1 && t == 0) atomicOr(a.flags, kFlagSpinTimeout);

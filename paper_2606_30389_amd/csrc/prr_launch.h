@@ -111,15 +111,15 @@ struct FusedLaunch {
   int32_t* missed_count;
   int32_t* wasted_count;
   uint64_t* t_score;  // [Hkv][max_pages] tagged score bits
-  uint64_t* t_thr;    // [Hkv][2] tagged threshold of A
-  uint64_t* t_mcnt;   // [Hkv] tagged count of the missed list (bit 31: attended by the select workgroup)
+  uint64_t* t_thr;    // [Hkv][8 copies][32] tagged threshold of A (words 0, 1 of each copy)
+  uint64_t* t_mcnt;   // [Hkv][8][32] tagged count of the missed list (bit 31: attended by the select workgroup)
   uint64_t* t_mlist;  // [Hkv][cap] tagged missed pages
   uint64_t* t_part;   // [Hkv][nparts][G][2] tagged (m, l) of the partial states
   float* part_o;      // [Hkv][nparts][G][128] their outputs (complete before (m, l) are stored)
   uint64_t* t_candk;  // [3][Hkv][n_score][132] tagged candidate count, then keys: A, P^{t+1}, late
   uint64_t* t_candp;  // [3][Hkv][n_score][128] tagged candidate pages (bit 31: forced, bit 30: late)
   uint64_t* t_pkey;   // [Hkv][max_pages] tagged keys of the next prediction (EMA)
-  uint64_t* t_lcnt;   // [Hkv] tagged number of late-speculated pages
+  uint64_t* t_lcnt;   // [Hkv][8][32] tagged number of late-speculated pages
   uint32_t* win;      // [Hkv][4] candidate bounds (ratios to |q-bar|_1) for A, P, late, kept across steps
   const uint32_t* pbits_cur;  // [Hkv][ceil(max_pages/32)] bitmap of P^t (a hint for the late filter)
   uint32_t* pbits_nxt;        // bitmap of P^{t+1}
