@@ -516,11 +516,35 @@ __device__ __forceinline__ void wave_attend(const FusedLaunch& a, int h, const u
   }
 }
 
+// Where a workgroup publishes its partial state (slot `slot` of KV head h), computed
+// before a long wait and kept in scalar registers: the kernel arguments it derives
+// from would otherwise be loaded again after the wait, on the critical path.
+struct PubDst {
+  float* po;      // [G][128] outputs of the slot
+  uint64_t* pml;  // [G][2] tagged (m, l) of the slot
+  int G;
+};
+__device__ __forceinline__ PubDst pub_dst(const FusedLaunch& a, int h, int slot) {
+  const size_t row0 = ((size_t)h * a.nparts + slot) * a.group;
+  const uint64_t po = (uint64_t)(a.part_o + row0 * kHeadDim), pml = (uint64_t)(a.t_part + row0 * 2);
+  uint32_t w[5] = {(uint32_t)po, (uint32_t)(po >> 32), (uint32_t)pml, (uint32_t)(pml >> 32), (uint32_t)a.group};
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
+    w[i] = (uint32_t)__builtin_amdgcn_readfirstlane((int)w[i]);
+    asm volatile("" : "+s"(w[i]));
+  }
+  PubDst d;
+  d.po = reinterpret_cast<float*>((uint64_t)w[0] | ((uint64_t)w[1] << 32));
+  d.pml = reinterpret_cast<uint64_t*>((uint64_t)w[2] | ((uint64_t)w[3] << 32));
+  d.G = (int)w[4];
+  return d;
+}
+
 // Fold the kept page states of every wave (keep: wave-uniform bit mask) and publish the
 // workgroup's state into partial slot `slot` of KV head h.
 template <int NPW>
-__device__ __forceinline__ void fold_publish(const FusedLaunch& a, uint32_t ep, int h, int slot, WaveStates<NPW>& st, uint32_t keep,
-                             FAttnLds& L) {
+__device__ __forceinline__ void fold_publish(const PubDst& d, uint32_t ep, WaveStates<NPW>& st, uint32_t keep,
+                                             FAttnLds& L) {
   const float kNegInf = -__builtin_inff();
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int j = lane >> 4, n = lane & 15;
@@ -556,7 +580,7 @@ __device__ __forceinline__ void fold_publish(const FusedLaunch& a, uint32_t ep, 
   }
   __syncthreads();
   const int hh = t >> 5, c0 = (t & 31) * 4;
-  const int G = a.group;
+  const int G = d.G;
   float mrow = kNegInf, lrow = 0.0f;
   if (hh < G) {
     float mw[kFW], fw[kFW];
@@ -583,7 +607,7 @@ __device__ __forceinline__ void fold_publish(const FusedLaunch& a, uint32_t ep, 
       o[2] += x.z * fw[ww];
       o[3] += x.w * fw[ww];
     }
-    uint64_t* dst = reinterpret_cast<uint64_t*>(a.part_o + (((size_t)h * a.nparts + slot) * G + hh) * kHeadDim + c0);
+    uint64_t* dst = reinterpret_cast<uint64_t*>(d.po + (size_t)hh * kHeadDim + c0);
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const uint64_t v = (uint64_t)__float_as_uint(o[2 * e] * inv) | ((uint64_t)__float_as_uint(o[2 * e + 1] * inv) << 32);
@@ -598,7 +622,7 @@ __device__ __forceinline__ void fold_publish(const FusedLaunch& a, uint32_t ep, 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (hh < G && (t & 31) == 0) {
-    uint64_t* ml = a.t_part + (((size_t)h * a.nparts + slot) * G + hh) * 2;
+    uint64_t* ml = d.pml + (size_t)hh * 2;
     put_tag(ml, __float_as_uint(mrow), ep);
     put_tag(ml + 1, __float_as_uint(lrow), ep);
   }
@@ -935,7 +959,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
     load_q(a, h, qf);
     WaveStates<1> st;
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
-    fold_publish<1>(a, ep, h, a.n_spec, st, 1u, U.attn);
+    fold_publish<1>(pub_dst(a, h, a.n_spec), ep, st, 1u, U.attn);
   }
   update_window<J>(a, a.win + 4 * h, qn, key, cand, (5 * a.kextra_a) / 2, keep_window, U.sel.sel);
   if (a.late) update_window<J>(a, a.win + 4 * h + 2, qn, key, cand, (3 * a.kextra_a) / 2, true, U.sel.sel);
@@ -1067,7 +1091,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
     load_q(a, h, qf);
     WaveStates<1> st;
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
-    fold_publish<1>(a, ep, h, a.n_spec, st, 1u, U.attn);
+    fold_publish<1>(pub_dst(a, h, a.n_spec), ep, st, 1u, U.attn);
   }
 }
 
@@ -1415,8 +1439,9 @@ __device__ __forceinline__ void role_spec(const FusedLaunch& a, uint32_t ep, int
   }
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
+  const PubDst pd = pub_dst(a, h, c);
   if (a.mode != PRR_KEEP_WASTED) keep = keep_in_A<NPW>(a, ep, h, pg, keep, U.bc);
-  fold_publish<NPW>(a, ep, h, c, st, keep, U.attn);
+  fold_publish<NPW>(pd, ep, st, keep, U.attn);
 }
 
 // Late speculation (PRR schedule): as soon as this step's scores exist, the pages just
@@ -1465,8 +1490,9 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, uint32_t ep, int
   __syncthreads();  // the list is read before the attention reuses the LDS
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
+  const PubDst pd = pub_dst(a, h, a.n_spec + a.n_miss + u);
   keep = keep_in_A<NPW>(a, ep, h, pg, keep, U.bc);
-  fold_publish<NPW>(a, ep, h, a.n_spec + a.n_miss + u, st, keep, U.attn);
+  fold_publish<NPW>(pd, ep, st, keep, U.attn);
 }
 
 template <bool BF16, int PS, int NPW>
@@ -1520,7 +1546,7 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int
   }
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
-  fold_publish<NPW>(a, ep, h, a.n_spec + u, st, keep, U.attn);
+  fold_publish<NPW>(pub_dst(a, h, a.n_spec + u), ep, st, keep, U.attn);
 }
 
 // ------------------------------------------------------------------------ merge
