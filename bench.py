@@ -222,8 +222,11 @@ def delta_sweep(args, cfg):
             sel_us = timed(lambda: st.select(q, stream=s), reps)
             spec_us = timed(lambda: st.speculate(q, stream=s), reps)
             fused_us = timed(lambda: stack.step(L.PRR_SCHED_FUSED_PRR, s), reps)
+            stack.params.late_spec = 1
+            stack.step(L.PRR_SCHED_FUSED_PRR, s)
+            late_us = timed(lambda: stack.step(L.PRR_SCHED_FUSED_PRR, s), reps)
             rows.append({"context": ctx, "delta": delta, "select_us": round(sel_us, 2), "spec_us": round(spec_us, 2),
-                         "fused_prr_us": round(fused_us, 2)})
+                         "fused_prr_us": round(fused_us, 2), "fused_prr_late_us": round(late_us, 2)})
             print(f"[sweep] {rows[-1]}", file=sys.stderr, flush=True)
             del stack, st
     pick = {c: R.pick_delta(rows, c) for c in contexts}
