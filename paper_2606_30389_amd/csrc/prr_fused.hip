@@ -582,30 +582,36 @@ __device__ __forceinline__ void fold_publish(const PubDst& d, uint32_t ep, WaveS
   const int hh = t >> 5, c0 = (t & 31) * 4;
   const int G = d.G;
   float mrow = kNegInf, lrow = 0.0f;
+  static_assert(kFW == 8, "the weights of a row are spread over 8 lanes");
+  // The weight of wave ww's state for this row is computed once, by lane ww of the row's
+  // 32-lane group (lanes repeat it every 8), and read from there: the fold's arithmetic
+  // runs on every wave of the CU at once, so its instruction count is its latency.
+  const int ww8 = lane & 7;
+  const float mv = hh < G ? L.wm[ww8][hh] : kNegInf;
+  const float lv = hh < G ? L.wl[ww8][hh] : 0.0f;
+  float ms = lv > 0.0f ? mv : kNegInf;
+  ms = fmaxf(ms, dpp_f32<kDppXor1>(ms));
+  ms = fmaxf(ms, dpp_f32<kDppXor2>(ms));
+  ms = fmaxf(ms, dpp_f32<kDppHalfMirror>(ms));
+  const float fwl = lv > 0.0f ? exp2f((mv - ms) * kLog2e) : 0.0f;
+  float lsum = lv * fwl;
+  lsum += dpp_f32<kDppXor1>(lsum);
+  lsum += dpp_f32<kDppXor2>(lsum);
+  lsum += dpp_f32<kDppHalfMirror>(lsum);
   if (hh < G) {
-    float mw[kFW], fw[kFW];
-    float ms = kNegInf;
-#pragma unroll
-    for (int ww = 0; ww < kFW; ++ww) {
-      mw[ww] = L.wm[ww][hh];
-      if (L.wl[ww][hh] > 0.0f) ms = fmaxf(ms, mw[ww]);
-    }
-    float lsum = 0.0f;
-#pragma unroll
-    for (int ww = 0; ww < kFW; ++ww) {
-      const float lw = L.wl[ww][hh];
-      fw[ww] = lw > 0.0f ? exp2f((mw[ww] - ms) * kLog2e) : 0.0f;
-      lsum += lw * fw[ww];
-    }
     const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+    const int hi = lane & 32;
     float o[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ww = 0; ww < kFW; ++ww) {
+      const float f0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fwl), ww));
+      const float f1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fwl), 32 + ww));
+      const float f = hi ? f1 : f0;
       const float4 x = *reinterpret_cast<const float4*>(&L.wo[ww][hh][c0]);
-      o[0] += x.x * fw[ww];
-      o[1] += x.y * fw[ww];
-      o[2] += x.z * fw[ww];
-      o[3] += x.w * fw[ww];
+      o[0] += x.x * f;
+      o[1] += x.y * f;
+      o[2] += x.z * f;
+      o[3] += x.w * f;
     }
     uint64_t* dst = reinterpret_cast<uint64_t*>(d.po + (size_t)hh * kHeadDim + c0);
 #pragma unroll
