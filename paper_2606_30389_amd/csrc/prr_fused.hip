@@ -117,6 +117,8 @@ struct FAttnLds {
   float wo[kFW][16][kFOPad];
   float wm[kFW][16];
   float wl[kFW][16];
+  int kpg[kFW];     // page of each wave (keep decided after the state is in LDS)
+  uint32_t kmask;   // waves whose page is kept
 };
 
 struct FMergeLds {
@@ -540,13 +542,12 @@ __device__ __forceinline__ PubDst pub_dst(const FusedLaunch& a, int h, int slot)
   return d;
 }
 
-// Fold the kept page states of every wave (keep: wave-uniform bit mask) and publish the
-// workgroup's state into partial slot `slot` of KV head h.
+// Fold the kept page states of this wave (keep: wave-uniform bit mask) and write the
+// result to the wave's LDS slot.
 template <int NPW>
-__device__ __forceinline__ void fold_publish(const PubDst& d, uint32_t ep, WaveStates<NPW>& st, uint32_t keep,
-                                             FAttnLds& L) {
+__device__ __forceinline__ void fold_write(WaveStates<NPW>& st, uint32_t keep, FAttnLds& L) {
   const float kNegInf = -__builtin_inff();
-  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  const int lane = lane_id(), w = threadIdx.x / kWave;
   const int j = lane >> 4, n = lane & 15;
   float mf = kNegInf;
 #pragma unroll
@@ -578,7 +579,13 @@ __device__ __forceinline__ void fold_publish(const PubDst& d, uint32_t ep, WaveS
     *reinterpret_cast<float4*>(row + 8 * i) = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
     *reinterpret_cast<float4*>(row + 8 * i + 4) = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
   }
-  __syncthreads();
+}
+
+// The states of the waves in `wmask` (uniform) combined per row and published (the
+// states are in LDS, behind a barrier).
+__device__ __forceinline__ void combine_publish(const PubDst& d, uint32_t ep, uint32_t wmask, FAttnLds& L) {
+  const float kNegInf = -__builtin_inff();
+  const int t = threadIdx.x, lane = lane_id();
   const int hh = t >> 5, c0 = (t & 31) * 4;
   const int G = d.G;
   float mrow = kNegInf, lrow = 0.0f;
@@ -588,7 +595,7 @@ __device__ __forceinline__ void fold_publish(const PubDst& d, uint32_t ep, WaveS
   // runs on every wave of the CU at once, so its instruction count is its latency.
   const int ww8 = lane & 7;
   const float mv = hh < G ? L.wm[ww8][hh] : kNegInf;
-  const float lv = hh < G ? L.wl[ww8][hh] : 0.0f;
+  const float lv = (hh < G && ((wmask >> ww8) & 1u)) ? L.wl[ww8][hh] : 0.0f;
   float ms = lv > 0.0f ? mv : kNegInf;
   ms = fmaxf(ms, dpp_f32<kDppXor1>(ms));
   ms = fmaxf(ms, dpp_f32<kDppXor2>(ms));
@@ -632,6 +639,16 @@ __device__ __forceinline__ void fold_publish(const PubDst& d, uint32_t ep, WaveS
     put_tag(ml, __float_as_uint(mrow), ep);
     put_tag(ml + 1, __float_as_uint(lrow), ep);
   }
+}
+
+// Fold the kept page states of every wave (keep: wave-uniform bit mask) and publish the
+// workgroup's state.
+template <int NPW>
+__device__ __forceinline__ void fold_publish(const PubDst& d, uint32_t ep, WaveStates<NPW>& st, uint32_t keep,
+                                             FAttnLds& L) {
+  fold_write<NPW>(st, keep, L);
+  __syncthreads();
+  combine_publish(d, ep, 0xffu, L);
 }
 
 __device__ __forceinline__ bool page_forced(const FusedLaunch& a, int p) {
@@ -1420,6 +1437,40 @@ __device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, uint32_t ep,
   return keep;
 }
 
+// One page per wave: the page states go to LDS before A is known; once the threshold is
+// published, wave 0 decides for the eight pages which are in A (so one barrier follows
+// the threshold instead of two), and the kept states are combined and published.
+__device__ __forceinline__ void keep_fold_publish(const FusedLaunch& a, uint32_t ep, int h, int pg, WaveStates<1>& st,
+                                                  const PubDst& pd, FAttnLds& L) {
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  fold_write<1>(st, 1u, L);
+  if (lane == 0) L.kpg[w] = pg;
+  __syncthreads();
+  if (w == 0) {
+    const int p = lane < kFW ? L.kpg[lane] : -1;
+    const uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
+    const uint64_t vs = get_tag(&ts[max(p, 0)]);
+    const uint64_t* thr = rep_at(a.t_thr, h, blockIdx.x);
+    uint64_t v0 = 0, v1 = 0;
+    for (int it = 0; it < kFSpin; ++it) {
+      v0 = get_tag(thr);
+      v1 = get_tag(thr + 1);
+      if (tag_is(v0, ep) && tag_is(v1, ep)) break;
+      __builtin_amdgcn_s_sleep(2);
+      if (it == kFSpin - 1 && lane == 0) atomicOr(a.flags, kFlagSpinTimeout);
+    }
+    const uint32_t sc = p >= 0 ? tagged(vs, &ts[p], ep, a.flags) : 0u;
+    const uint32_t T = (uint32_t)v0, me = (uint32_t)v1;
+    const int mode = (int)(me & 3u), eq_cut = (int)(me >> 2);
+    const uint32_t key = score_key(__uint_as_float(sc));
+    const bool in = p >= 0 && (page_forced(a, p) || mode == 1 || (mode == 2 && (key > T || (key == T && p <= eq_cut))));
+    const uint32_t m = (uint32_t)__ballot(in) & ((1u << kFW) - 1u);
+    if (lane == 0) L.kmask = m;
+  }
+  __syncthreads();
+  combine_publish(pd, ep, L.kmask, L);
+}
+
 template <bool BF16, int PS, int NPW>
 __device__ __forceinline__ void role_spec(const FusedLaunch& a, uint32_t ep, int h, int c, FLds& U) {
   const int count = min(max(a.pred_cur_count[h], 0), a.cap);
@@ -1446,7 +1497,14 @@ __device__ __forceinline__ void role_spec(const FusedLaunch& a, uint32_t ep, int
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
   const PubDst pd = pub_dst(a, h, c);
-  if (a.mode != PRR_KEEP_WASTED) keep = keep_in_A<NPW>(a, ep, h, pg, keep, U.bc);
+  if constexpr (NPW == 1) {
+    if (a.mode != PRR_KEEP_WASTED) {
+      keep_fold_publish(a, ep, h, pg[0], st, pd, U.attn);
+      return;
+    }
+  } else {
+    if (a.mode != PRR_KEEP_WASTED) keep = keep_in_A<NPW>(a, ep, h, pg, keep, U.bc);
+  }
   fold_publish<NPW>(pd, ep, st, keep, U.attn);
 }
 
@@ -1497,8 +1555,12 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, uint32_t ep, int
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
   const PubDst pd = pub_dst(a, h, a.n_spec + a.n_miss + u);
-  keep = keep_in_A<NPW>(a, ep, h, pg, keep, U.bc);
-  fold_publish<NPW>(pd, ep, st, keep, U.attn);
+  if constexpr (NPW == 1) {
+    keep_fold_publish(a, ep, h, pg[0], st, pd, U.attn);
+  } else {
+    keep = keep_in_A<NPW>(a, ep, h, pg, keep, U.bc);
+    fold_publish<NPW>(pd, ep, st, keep, U.attn);
+  }
 }
 
 template <bool BF16, int PS, int NPW>
