@@ -106,11 +106,11 @@ bool ws_layout(const prr_dims* d, int cap, int chunk, WsLayout& L) {
   off = align_up(off + (size_t)hkv * L.nparts * g * 2 * 8, 256);
   L.f_parto = off;
   off = align_up(off + (size_t)hkv * L.nparts * g * 128 * 4, 256);
-  const size_t nsc = (size_t)div_up(d->max_pages, 128);
-  L.f_candk = off;  // per list: the count, then the keys (stride 132)
-  off = align_up(off + 3 * (size_t)hkv * nsc * 132 * 8, 256);
+  const size_t nsc = (size_t)div_up(d->max_pages, prr::kFusedScorePages);
+  L.f_candk = off;  // per list: the count, then the keys
+  off = align_up(off + 3 * (size_t)hkv * nsc * (prr::kFusedScorePages + 4) * 8, 256);
   L.f_candp = off;
-  off = align_up(off + 3 * (size_t)hkv * nsc * 128 * 8, 256);
+  off = align_up(off + 3 * (size_t)hkv * nsc * prr::kFusedScorePages * 8, 256);
   L.f_pkey = off;
   off = align_up(off + (size_t)hkv * d->max_pages * 8, 256);
   L.f_win = off;
@@ -592,7 +592,7 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.kextra_p = kextra_p;
   a.cap = sp->cap;
   a.chunk = sp->chunk_pages;
-  a.n_score = div_up(sp->num_pages, 128);
+  a.n_score = div_up(sp->num_pages, prr::kFusedScorePages);
   a.n_spec = L.nchunks;
   a.n_miss = L.nchunks;
   a.late = prr && sp->late_spec && sp->mode != PRR_RECOMPUTE_ON_MISS;

@@ -32,7 +32,11 @@ namespace {
 
 constexpr int kFT = 512;
 constexpr int kFW = kFT / kWave;
-constexpr int kFScorePages = 128;
+constexpr int kFScorePages = kFusedScorePages;  // pages of one score workgroup
+constexpr int kFPagesPerWave = kFScorePages / 8;  // scored by each of its 8 waves
+constexpr int kFScoreIt = kFPagesPerWave / 4;     // 4 pages per 16-lane row group at a time
+constexpr int kFMaxLists = kFusedMaxPages / kFScorePages;  // score workgroups per KV head
+constexpr int kFThreadsPerList = 512 / kFMaxLists;
 constexpr int kFSpin = 1 << 20;
 constexpr uint32_t kSelfMiss = 0x80000000u;  // missed-list count flags: attended by the select workgroup
 constexpr uint32_t kDropSpec = 0x40000000u;  //   the speculation is discarded (recompute on a miss)
@@ -41,10 +45,10 @@ constexpr int kFOPad = kHeadDim + 4;
 constexpr int kEqAll = 16383;  // eq_cut meaning "every key equal to T is taken"
 constexpr int kCandMax = 4 * kFT;     // candidates ranked by one workgroup (4 per thread)
 constexpr int kCandWave = 12 * kWave;  // candidates ranked by one wave (12 per lane)
-// A candidate list of one score workgroup: its tagged count, then up to 128 tagged keys;
-// the count shares lines with the first keys, and the lists of different workgroups lie
-// in different memory channels, so polls of many lists do not queue on one channel.
-constexpr int kCandStride = 132;
+// A candidate list of one score workgroup: its tagged count, then its tagged keys; the
+// count shares lines with the first keys, and the lists of different workgroups lie in
+// different memory channels, so polls of many lists do not queue on one channel.
+constexpr int kCandStride = kFScorePages + 4;
 
 __device__ __forceinline__ void put_tag(uint64_t* p, uint32_t v, uint32_t epoch) {
   __hip_atomic_store(p, ((uint64_t)epoch << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -102,7 +106,7 @@ struct FSelLds {
   uint32_t forceb[PRR_MAX_PAGES_DEV / 32];
   int32_t mlist[PRR_MAX_CAP_DEV];
   int cnt[2][16];
-  int off[3 * kWave];  // exclusive offsets, counts and forced counts of the score workgroups
+  int off[3 * kFMaxLists];  // exclusive offsets, counts and forced counts of the score workgroups
   int tot[2];
   float qb[kHeadDim];
   uint32_t ck[kCandMax];
@@ -163,9 +167,15 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   const int pbase = blk * kFScorePages;
   const bool ema = a.schedule != 0;
   const uint16_t* q = static_cast<const uint16_t*>(a.q);
-  // wave 0 owns the filtering: EMA state of pages pbase + lane and pbase + 64 + lane
-  float lv[2] = {0.f, 0.f}, tv[2] = {0.f, 0.f};
-  uint32_t bw[2] = {0u, 0u};
+  // wave 0 owns the filtering: EMA state of pages pbase + lane (+ 64 ...)
+  constexpr int kHalves = (kFScorePages + kWave - 1) / kWave;
+  float lv[kHalves], tv[kHalves];
+  uint32_t bw[kHalves];
+#pragma unroll
+  for (int i = 0; i < kHalves; ++i) {
+    lv[i] = tv[i] = 0.f;
+    bw[i] = 0u;
+  }
   const int nwmax = (a.max_pages + 31) / 32;
   // the query first, then this thread's metadata, so that q-bar is formed while the
   // metadata is still in flight (loads complete in issue order)
@@ -173,12 +183,12 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   uint4 qv = make_uint4(0, 0, 0, 0);
   if (g16 < G) qv = *reinterpret_cast<const uint4*>(q + (size_t)(h * G + g16) * kHeadDim + c8);
   const int cg = lane & 15, pi = lane >> 4;
-  const int base = pbase + w * 16 + pi;
-  uint4 mn[4], mx[4];
-  float4 m0[4], m1[4];
+  const int base = pbase + w * kFPagesPerWave + pi;
+  uint4 mn[kFScoreIt], mx[kFScoreIt];
+  float4 m0[kFScoreIt], m1[kFScoreIt];
   if (!a.meta_mean) {
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < kFScoreIt; ++it) {
       const int p = min(base + 4 * it, n - 1);
       const uint16_t* row = static_cast<const uint16_t*>(a.meta) + ((size_t)h * a.max_pages + p) * 2 * kHeadDim + cg * 8;
       mn[it] = *reinterpret_cast<const uint4*>(row);
@@ -186,7 +196,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     }
   } else {
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < kFScoreIt; ++it) {
       const int p = min(base + 4 * it, n - 1);
       const float4* row = reinterpret_cast<const float4*>(static_cast<const float*>(a.meta) +
                                                           ((size_t)h * a.max_pages + p) * kHeadDim + cg * 8);
@@ -194,12 +204,14 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
       m1[it] = row[1];
     }
   }
-  // wave 0 filters: EMA state of pages pbase + lane and pbase + 64 + lane, and the
+  // wave 0 filters: EMA state of pages pbase + lane (+ 64 ...), and the
   // candidate bounds kept from the previous step as ratios: of A and of late pages to
   // |q-bar|_1 (scores scale with q-bar), of the next prediction to the EMA of |q-bar|_1
   // (the EMA keys scale with it); loaded together with the metadata
   float r_a = 0.f, r_p = 0.f, r_l = 0.f, qe0 = 0.f;
-  uint32_t pw[2] = {0u, 0u};
+  uint32_t pw[kHalves];
+#pragma unroll
+  for (int i = 0; i < kHalves; ++i) pw[i] = 0u;
   if (w == 0) {
     r_a = __uint_as_float(a.win[4 * h]);
     r_p = __uint_as_float(a.win[4 * h + 1]);
@@ -207,12 +219,12 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     qe0 = __uint_as_float(a.win[4 * h + 3]);
     if (a.late) {
 #pragma unroll
-      for (int half = 0; half < 2; ++half)
+      for (int half = 0; half < kHalves; ++half)
         pw[half] = a.pbits_cur[(size_t)h * nwmax + (min(pbase + 64 * half + (lane & 32), n - 1) >> 5)];
     }
     if (ema) {
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
+      for (int half = 0; half < kHalves; ++half) {
         const int p = min(pbase + 64 * half + lane, n - 1);
         lv[half] = a.level[(size_t)h * a.max_pages + p];
         tv[half] = a.trend[(size_t)h * a.max_pages + p];
@@ -226,7 +238,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
 #pragma unroll
       for (int e = 0; e < 8; ++e) S.qpart[g][c8 + e] = u4_elem<BF16>(qv, e);
     }
-    if (t < 4) S.fbits[t] = 0u;
+    if (t < kFScorePages / 32) S.fbits[t] = 0u;
     __syncthreads();
     if (t < kHeadDim) {
       float s = 0.0f;
@@ -250,10 +262,10 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   for (int e = 0; e < 8; ++e) qb[e] = S.qbar[cg * 8 + e];
   float* scores = a.scores + (size_t)h * a.max_pages;
   uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
-  float s[4];
+  float s[kFScoreIt];
   if (!a.meta_mean) {
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < kFScoreIt; ++it) {
       float v = 0.0f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) v += fmaxf(qb[e] * u4_elem<BF16>(mn[it], e), qb[e] * u4_elem<BF16>(mx[it], e));
@@ -261,7 +273,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     }
   } else {
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < kFScoreIt; ++it) {
       float v = qb[0] * m0[it].x;
       v += qb[1] * m0[it].y;
       v += qb[2] * m0[it].z;
@@ -274,7 +286,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     }
   }
 #pragma unroll
-  for (int it = 0; it < 4; ++it) {
+  for (int it = 0; it < kFScoreIt; ++it) {
     const float v = sum16(s[it]);
     const int p = base + 4 * it;
     if (cg == 0) {
@@ -305,12 +317,12 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   uint64_t* ck_l = a.t_candk + rec_l * kCandStride + 1;
   uint64_t* cp_l = a.t_candp + rec_l * kFScorePages;
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
+  for (int half = 0; half < kHalves; ++half) {
     const int lp = 64 * half + lane;
     const int p = pbase + lp;
-    const bool inr = p < n;
+    const bool inr = p < n && lp < kFScorePages;
     const bool f = inr && ((S.fbits[lp >> 5] >> (lp & 31)) & 1u);
-    const uint32_t ka = score_key(S.sc[lp]);
+    const uint32_t ka = score_key(S.sc[min(lp, kFScorePages - 1)]);
     const bool ca = inr && (f || ka >= lo_a);
     const bool late = a.late && ca && !f && ka >= lo_l && !((pw[half] >> (p & 31)) & 1u);
     const uint64_t ma = __ballot(ca), mfa = __ballot(ca && f), ml = __ballot(late);
@@ -335,11 +347,11 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   if (!ema) return;
   // ... then the EMA update of Eq. (3) and the candidates of the next prediction
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
+  for (int half = 0; half < kHalves; ++half) {
     const int lp = 64 * half + lane;
     const int p = pbase + lp;
-    const bool inr = p < n;
-    const float sv = S.sc[lp];
+    const bool inr = p < n && lp < kFScorePages;
+    const float sv = S.sc[min(lp, kFScorePages - 1)];
     const bool f = inr && ((S.fbits[lp >> 5] >> (lp & 31)) & 1u);
     bool has = inr && ((bw[half] >> (p & 31)) & 1u);
     float l = lv[half], v = tv[half];
@@ -679,41 +691,56 @@ struct FCand {
 template <bool POLL_ALL>
 __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, int h, int which, int* off, int* tot, uint32_t* lk,
                                            uint32_t* lp) {
+  constexpr int TPL = kFThreadsPerList;  // threads per list
+  constexpr int L2 = kFMaxLists / kWave; // lists per lane in the one-wave paths
+  static_assert(TPL * kFMaxLists == 512 && L2 * kWave == kFMaxLists, "list layout");
+  int* cnt = off + kFMaxLists;
+  int* fcnt = off + 2 * kFMaxLists;
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int nS = a.n_score;
-  const int wg = t >> 3, sub = t & 7;
+  const int wg = t / TPL, sub = t % TPL;
   const bool mine = wg < nS;
   const size_t rec0 = ((size_t)which * a.num_kv_heads + h) * nS;
   const size_t rec = rec0 + min(wg, nS - 1);
   const uint64_t* ck = a.t_candk + rec * kCandStride + 1;
   const uint64_t* cp = a.t_candp + rec * kFScorePages;
-  // the count and the first four entries are polled together until all needed are there
-  // (32 per score workgroup, more than almost any list holds)
-  constexpr int kPollE = 4;
+  // the count and the first eight entries per thread are polled together until all
+  // needed are there (32 per list, more than almost any list holds)
+  constexpr int kPollE = 32 / TPL;
   uint64_t vc = 0, ke[kPollE], pe[kPollE];
 #pragma unroll
   for (int u = 0; u < kPollE; ++u) ke[u] = pe[u] = 0ull;
   uint32_t c = 0u;
   if (!POLL_ALL && w == 0) {
-    const bool m1 = lane < nS;
-    const uint64_t* pc = &a.t_candk[(rec0 + min(lane, nS - 1)) * kCandStride];
+    // lane l polls the counts of lists l, l + 64, ..
+    uint64_t v[L2];
     for (int it = 0; it < kFSpin; ++it) {
-      vc = get_tag(pc);
-      if (__ballot(m1 && !tag_is(vc, ep)) == 0ull) break;
+      bool missing = false;
+#pragma unroll
+      for (int k = 0; k < L2; ++k) {
+        const int li = lane + kWave * k;
+        v[k] = get_tag(&a.t_candk[(rec0 + min(li, nS - 1)) * kCandStride]);
+        missing = missing || (li < nS && !tag_is(v[k], ep));
+      }
+      if (__ballot(missing) == 0ull) break;
       __builtin_amdgcn_s_sleep(24);  // slow polling: these workgroups have slack
       if (it == kFSpin - 1 && lane == 0) atomicOr(a.flags, kFlagSpinTimeout);
     }
-    if (m1) {
-      off[kWave + lane] = (int)((uint32_t)vc & 0xffffu);
-      off[2 * kWave + lane] = (int)((uint32_t)vc >> 16);
+#pragma unroll
+    for (int k = 0; k < L2; ++k) {
+      const int li = lane + kWave * k;
+      if (li < nS) {
+        cnt[li] = (int)((uint32_t)v[k] & 0xffffu);
+        fcnt[li] = (int)((uint32_t)v[k] >> 16);
+      }
     }
   }
   for (int it = 0; POLL_ALL && mine && it < kFSpin; ++it) {
     vc = get_tag(ck - 1);
 #pragma unroll
     for (int u = 0; u < kPollE; ++u) {
-      ke[u] = get_tag(&ck[sub + 8 * u]);
-      pe[u] = get_tag(&cp[sub + 8 * u]);
+      ke[u] = get_tag(&ck[sub + TPL * u]);
+      pe[u] = get_tag(&cp[sub + TPL * u]);
     }
     if (tag_is(vc, ep)) {
       c = (uint32_t)vc;
@@ -721,24 +748,37 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, in
       bool ok = true;
 #pragma unroll
       for (int u = 0; u < kPollE; ++u)
-        ok = ok && (sub + 8 * u >= n0 || (tag_is(ke[u], ep) && tag_is(pe[u], ep)));
+        ok = ok && (sub + TPL * u >= n0 || (tag_is(ke[u], ep) && tag_is(pe[u], ep)));
       if (ok) break;
     }
     __builtin_amdgcn_s_sleep(2);
     if (it == kFSpin - 1) atomicOr(a.flags, kFlagSpinTimeout);
   }
   if (POLL_ALL && mine && sub == 0) {
-    off[kWave + wg] = (int)(c & 0xffffu);
-    off[2 * kWave + wg] = (int)(c >> 16);
+    cnt[wg] = (int)(c & 0xffffu);
+    fcnt[wg] = (int)(c >> 16);
   }
   __syncthreads();
-  const int nc = mine ? off[kWave + wg] : 0;
+  const int nc = mine ? cnt[wg] : 0;
   if (w == 0) {
-    const int cw = lane < nS ? off[kWave + lane] : 0;
-    const int fw = lane < nS ? off[2 * kWave + lane] : 0;
-    const int incl = wave_inclusive_scan(cw);
-    if (lane < nS) off[lane] = incl - cw;
-    const int ft = wave_isum(fw);
+    // lane l holds lists L2 l .. L2 l + L2 - 1 (consecutive, so the offsets follow a scan)
+    int cw[L2], sum = 0, fs = 0;
+#pragma unroll
+    for (int k = 0; k < L2; ++k) {
+      const int li = L2 * lane + k;
+      cw[k] = li < nS ? cnt[li] : 0;
+      sum += cw[k];
+      fs += li < nS ? fcnt[li] : 0;
+    }
+    const int incl = wave_inclusive_scan(sum);
+    int o = incl - sum;
+#pragma unroll
+    for (int k = 0; k < L2; ++k) {
+      const int li = L2 * lane + k;
+      if (li < nS) off[li] = o;
+      o += cw[k];
+    }
+    const int ft = wave_isum(fs);
     if (lane == kWave - 1) {
       tot[0] = incl;
       tot[1] = ft;
@@ -753,7 +793,7 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, in
     if (POLL_ALL) {
 #pragma unroll
       for (int u = 0; u < kPollE; ++u) {
-        const int slot = sub + 8 * u;
+        const int slot = sub + TPL * u;
         if (slot < nc) {
           lk[o + slot] = tagged(ke[u], &ck[slot], ep, a.flags);
           lp[o + slot] = tagged(pe[u], &cp[slot], ep, a.flags);
@@ -761,17 +801,17 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, in
       }
     }
     // the rest in batches of four per thread, all loads of a batch issued before any wait
-    for (int s0 = sub + (POLL_ALL ? 8 * kPollE : 0); s0 < nc; s0 += 32) {
+    for (int s0 = sub + (POLL_ALL ? TPL * kPollE : 0); s0 < nc; s0 += 4 * TPL) {
       uint64_t kv[4], pv[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int slot = min(s0 + 8 * u, kFScorePages - 1);
+        const int slot = min(s0 + TPL * u, kFScorePages - 1);
         kv[u] = get_tag(&ck[slot]);
         pv[u] = get_tag(&cp[slot]);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int slot = s0 + 8 * u;
+        const int slot = s0 + TPL * u;
         if (slot < nc) {
           lk[o + slot] = tagged(kv[u], &ck[slot], ep, a.flags);
           lp[o + slot] = tagged(pv[u], &cp[slot], ep, a.flags);

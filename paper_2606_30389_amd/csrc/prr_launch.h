@@ -138,7 +138,8 @@ struct FusedLaunch {
   int32_t forced[PRR_MAX_FORCED];
 };
 
-constexpr int kFusedMaxPages = 8192;  // 16 keys per thread of a 512-thread select
+constexpr int kFusedMaxPages = 8192;   // 16 keys per thread of a 512-thread select
+constexpr int kFusedScorePages = 128;   // pages per score workgroup of the fused step
 hipError_t launch_fused(const FusedLaunch& a, bool bf16, int page_size, hipStream_t stream);
 int fused_grid(const FusedLaunch& a);
 
