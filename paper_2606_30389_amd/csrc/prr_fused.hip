@@ -598,7 +598,7 @@ __device__ __forceinline__ void fold_write(WaveStates<NPW>& st, uint32_t keep, F
 __device__ __forceinline__ void combine_publish(const PubDst& d, uint32_t ep, uint32_t wmask, FAttnLds& L) {
   const float kNegInf = -__builtin_inff();
   const int t = threadIdx.x, lane = lane_id();
-  const int hh = t >> 5, c0 = (t & 31) * 4;
+  const int hh = t >> 5, ci = t & 31;  // row; columns 2ci, 2ci + 1, 64 + 2ci, 65 + 2ci
   const int G = d.G;
   float mrow = kNegInf, lrow = 0.0f;
   static_assert(kFW == 8, "the weights of a row are spread over 8 lanes");
@@ -626,18 +626,20 @@ __device__ __forceinline__ void combine_publish(const PubDst& d, uint32_t ep, ui
       const float f0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fwl), ww));
       const float f1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fwl), 32 + ww));
       const float f = hi ? f1 : f0;
-      const float4 x = *reinterpret_cast<const float4*>(&L.wo[ww][hh][c0]);
-      o[0] += x.x * f;
-      o[1] += x.y * f;
-      o[2] += x.z * f;
-      o[3] += x.w * f;
+      const float2 xa = *reinterpret_cast<const float2*>(&L.wo[ww][hh][2 * ci]);
+      const float2 xb = *reinterpret_cast<const float2*>(&L.wo[ww][hh][64 + 2 * ci]);
+      o[0] += xa.x * f;
+      o[1] += xa.y * f;
+      o[2] += xb.x * f;
+      o[3] += xb.y * f;
     }
-    uint64_t* dst = reinterpret_cast<uint64_t*>(d.po + (size_t)hh * kHeadDim + c0);
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const uint64_t v = (uint64_t)__float_as_uint(o[2 * e] * inv) | ((uint64_t)__float_as_uint(o[2 * e + 1] * inv) << 32);
-      __hip_atomic_store(dst + e, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    // each store instruction of a wave covers whole lines (partial lines written
+    // through to memory cost a read-modify-write each)
+    uint64_t* dst = reinterpret_cast<uint64_t*>(d.po + (size_t)hh * kHeadDim);
+    const uint64_t va = (uint64_t)__float_as_uint(o[0] * inv) | ((uint64_t)__float_as_uint(o[1] * inv) << 32);
+    const uint64_t vb = (uint64_t)__float_as_uint(o[2] * inv) | ((uint64_t)__float_as_uint(o[3] * inv) << 32);
+    __hip_atomic_store(dst + ci, va, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(dst + 32 + ci, vb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     mrow = lsum > 0.0f ? ms : kNegInf;
     lrow = lsum;
   }
