@@ -123,6 +123,7 @@ struct FAttnLds {
   float wl[kFW][16];
   int kpg[kFW];     // page of each wave (keep decided after the state is in LDS)
   uint32_t kmask;   // waves whose page is kept
+  uint32_t ml[32];  // (m, l) of each row of the combined state
 };
 
 struct FMergeLds {
@@ -289,13 +290,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   for (int it = 0; it < kFScoreIt; ++it) {
     const float v = sum16(s[it]);
     const int p = base + 4 * it;
-    if (cg == 0) {
-      S.sc[p - pbase] = v;
-      if (p < n) {
-        scores[p] = v;
-        put_tag(&ts[p], __float_as_uint(v), ep);
-      }
-    }
+    if (cg == 0) S.sc[p - pbase] = v;
   }
   __syncthreads();
   if (w != 0) return;
@@ -322,7 +317,13 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     const int p = pbase + lp;
     const bool inr = p < n && lp < kFScorePages;
     const bool f = inr && ((S.fbits[lp >> 5] >> (lp & 31)) & 1u);
-    const uint32_t ka = score_key(S.sc[min(lp, kFScorePages - 1)]);
+    const float sv = S.sc[min(lp, kFScorePages - 1)];
+    if (inr) {
+      // the scores, 64 pages per store instruction (whole lines)
+      scores[p] = sv;
+      put_tag(&ts[p], __float_as_uint(sv), ep);
+    }
+    const uint32_t ka = score_key(sv);
     const bool ca = inr && (f || ka >= lo_a);
     const bool late = a.late && ca && !f && ka >= lo_l && !((pw[half] >> (p & 31)) & 1u);
     const uint64_t ma = __ballot(ca), mfa = __ballot(ca && f), ml = __ballot(late);
@@ -600,7 +601,6 @@ __device__ __forceinline__ void combine_publish(const PubDst& d, uint32_t ep, ui
   const int t = threadIdx.x, lane = lane_id();
   const int hh = t >> 5, ci = t & 31;  // row; columns 2ci, 2ci + 1, 64 + 2ci, 65 + 2ci
   const int G = d.G;
-  float mrow = kNegInf, lrow = 0.0f;
   static_assert(kFW == 8, "the weights of a row are spread over 8 lanes");
   // The weight of wave ww's state for this row is computed once, by lane ww of the row's
   // 32-lane group (lanes repeat it every 8), and read from there: the fold's arithmetic
@@ -640,19 +640,18 @@ __device__ __forceinline__ void combine_publish(const PubDst& d, uint32_t ep, ui
     const uint64_t vb = (uint64_t)__float_as_uint(o[2] * inv) | ((uint64_t)__float_as_uint(o[3] * inv) << 32);
     __hip_atomic_store(dst + ci, va, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(dst + 32 + ci, vb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    mrow = lsum > 0.0f ? ms : kNegInf;
-    lrow = lsum;
+    if ((t & 31) == 0) {
+      L.ml[2 * hh] = __float_as_uint(lsum > 0.0f ? ms : kNegInf);
+      L.ml[2 * hh + 1] = __float_as_uint(lsum);
+    }
   }
   // The tagged (m, l) of a state are stored only after every output value of it has
   // completed (device-coherent stores are acknowledged once visible to the whole
-  // device), so a reader that sees them current reads a complete, untagged output.
+  // device), so a reader that sees them current reads a complete, untagged output;
+  // all rows' (m, l) go out in one store instruction.
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  if (hh < G && (t & 31) == 0) {
-    uint64_t* ml = d.pml + (size_t)hh * 2;
-    put_tag(ml, __float_as_uint(mrow), ep);
-    put_tag(ml + 1, __float_as_uint(lrow), ep);
-  }
+  if (t < 2 * G) put_tag(d.pml + t, L.ml[t], ep);
 }
 
 // Fold the kept page states of every wave (keep: wave-uniform bit mask) and publish the
