@@ -792,12 +792,14 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, in
   if (mine && r.total <= kCandMax) {
     const int o = off[wg];
     if (POLL_ALL) {
+      // the poll above only ended once every one of these slots below the count was
+      // from this epoch
 #pragma unroll
       for (int u = 0; u < kPollE; ++u) {
         const int slot = sub + TPL * u;
         if (slot < nc) {
-          lk[o + slot] = tagged(ke[u], &ck[slot], ep, a.flags);
-          lp[o + slot] = tagged(pe[u], &cp[slot], ep, a.flags);
+          lk[o + slot] = (uint32_t)ke[u];
+          lp[o + slot] = (uint32_t)pe[u];
         }
       }
     }
@@ -1462,9 +1464,19 @@ __device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, uint32_t ep,
   }
   __syncthreads();
   if (!keep) return keep;
+  // the scores were published before the threshold; one that is not visible yet is
+  // awaited (the rare case, kept out of the common path's instruction stream)
+  bool stale = false;
+#pragma unroll
+  for (int k = 0; k < NPW; ++k) stale = stale || (pg[k] >= 0 && !tag_is(vs[k], ep));
+  if (__builtin_expect(stale, 0)) {
+#pragma unroll
+    for (int k = 0; k < NPW; ++k)
+      if (pg[k] >= 0) vs[k] = tagged(vs[k], &ts[pg[k]], ep, a.flags);
+  }
   uint32_t sc[NPW];
 #pragma unroll
-  for (int k = 0; k < NPW; ++k) sc[k] = pg[k] >= 0 ? tagged(vs[k], &ts[pg[k]], ep, a.flags) : 0u;
+  for (int k = 0; k < NPW; ++k) sc[k] = (uint32_t)vs[k];
   const uint32_t T = bc[0];
   const uint32_t me = bc[1];
   const int mode = (int)(me & 3u), eq_cut = (int)(me >> 2);
@@ -1490,17 +1502,19 @@ __device__ __forceinline__ void keep_fold_publish(const FusedLaunch& a, uint32_t
   if (w == 0) {
     const int p = lane < kFW ? L.kpg[lane] : -1;
     const uint64_t* ts = a.t_score + (size_t)h * a.max_pages;
-    const uint64_t vs = get_tag(&ts[max(p, 0)]);
+    // the page's score is polled with the threshold (it was published before it)
+    const uint64_t* sp = &ts[max(p, 0)];
     const uint64_t* thr = rep_at(a.t_thr, h, blockIdx.x);
-    uint64_t v0 = 0, v1 = 0;
+    uint64_t v0 = 0, v1 = 0, vs = 0;
     for (int it = 0; it < kFSpin; ++it) {
       v0 = get_tag(thr);
       v1 = get_tag(thr + 1);
-      if (tag_is(v0, ep) && tag_is(v1, ep)) break;
+      vs = get_tag(sp);
+      if (__ballot(!tag_is(v0, ep) || !tag_is(v1, ep) || (p >= 0 && !tag_is(vs, ep))) == 0ull) break;
       __builtin_amdgcn_s_sleep(2);
       if (it == kFSpin - 1 && lane == 0) atomicOr(a.flags, kFlagSpinTimeout);
     }
-    const uint32_t sc = p >= 0 ? tagged(vs, &ts[p], ep, a.flags) : 0u;
+    const uint32_t sc = p >= 0 ? (uint32_t)vs : 0u;
     const uint32_t T = (uint32_t)v0, me = (uint32_t)v1;
     const int mode = (int)(me & 3u), eq_cut = (int)(me >> 2);
     const uint32_t key = score_key(__uint_as_float(sc));
