@@ -211,8 +211,12 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   // (the EMA keys scale with it); loaded together with the metadata
   float r_a = 0.f, r_p = 0.f, r_l = 0.f, qe0 = 0.f;
   uint32_t pw[kHalves];
+  int ph[kHalves];  // physical pages (late pages are listed with them)
 #pragma unroll
-  for (int i = 0; i < kHalves; ++i) pw[i] = 0u;
+  for (int i = 0; i < kHalves; ++i) {
+    pw[i] = 0u;
+    ph[i] = 0;
+  }
   if (w == 0) {
     r_a = __uint_as_float(a.win[4 * h]);
     r_p = __uint_as_float(a.win[4 * h + 1]);
@@ -220,8 +224,11 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     qe0 = __uint_as_float(a.win[4 * h + 3]);
     if (a.late) {
 #pragma unroll
-      for (int half = 0; half < kHalves; ++half)
+      for (int half = 0; half < kHalves; ++half) {
         pw[half] = a.pbits_cur[(size_t)h * nwmax + (min(pbase + 64 * half + (lane & 32), n - 1) >> 5)];
+        const int p = min(pbase + 64 * half + lane, n - 1);
+        ph[half] = a.page_table ? a.page_table[p] : p;
+      }
     }
     if (ema) {
 #pragma unroll
@@ -333,8 +340,10 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
       put_tag(&cp_a[pos], (uint32_t)p | (f ? 0x80000000u : 0u) | (late ? 0x40000000u : 0u), ep);
     }
     if (late) {
+      // a late page is listed with its physical page in place of its key (the late
+      // workgroups only attend it; the select ranks the candidates of A)
       const int pos = nl + lanes_below(ml);
-      put_tag(&ck_l[pos], ka, ep);
+      put_tag(&ck_l[pos], (uint32_t)ph[half], ep);
       put_tag(&cp_l[pos], (uint32_t)p, ep);
     }
     na += __popcll(ma);
@@ -446,7 +455,7 @@ __device__ __forceinline__ void load_q(const FusedLaunch& a, int h, u32x4_t (&qf
 
 template <bool BF16, int PS, int NPW>
 __device__ __forceinline__ void wave_attend(const FusedLaunch& a, int h, const u32x4_t (&qf)[4], const int (&pg)[NPW],
-                                            WaveStates<NPW>& st) {
+                                            WaveStates<NPW>& st, const int* phys_in = nullptr) {
   constexpr int TPP = PS / 16;
   constexpr int NTW = NPW * TPP;
   const float kNegInf = -__builtin_inff();
@@ -456,7 +465,8 @@ __device__ __forceinline__ void wave_attend(const FusedLaunch& a, int h, const u
   const uint16_t* vh = static_cast<const uint16_t*>(a.v_cache) + (size_t)h * a.max_pages * PS * kHeadDim;
   int phys[NPW];
 #pragma unroll
-  for (int k = 0; k < NPW; ++k) phys[k] = (pg[k] >= 0 && a.page_table) ? a.page_table[pg[k]] : pg[k];
+  for (int k = 0; k < NPW; ++k)
+    phys[k] = phys_in ? phys_in[k] : ((pg[k] >= 0 && a.page_table) ? a.page_table[pg[k]] : pg[k]);
   bool ok[NPW];
   size_t off[NPW];
 #pragma unroll
@@ -724,7 +734,7 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, in
         missing = missing || (li < nS && !tag_is(v[k], ep));
       }
       if (__ballot(missing) == 0ull) break;
-      __builtin_amdgcn_s_sleep(24);  // slow polling: these workgroups have slack
+      __builtin_amdgcn_s_sleep(2);
       if (it == kFSpin - 1 && lane == 0) atomicOr(a.flags, kFlagSpinTimeout);
     }
 #pragma unroll
@@ -1593,22 +1603,24 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, uint32_t ep, int
   const int start = u * a.chunk;
   if (start >= cover) return;
   const int cnt = min(a.chunk, cover - start);
-  int pg[NPW];
+  int pg[NPW], ph[NPW];
   uint32_t keep = 0;
 #pragma unroll
   for (int k = 0; k < NPW; ++k) {
     const int i = w + kFW * k;
-    int p = -1;
+    int p = -1, q = -1;
     if (i < cnt) {
       p = (int)(L.cpg[start + i] & 0x3fffffffu);
+      q = (int)L.ck[start + i];  // its physical page
       if (p >= n || bit_of(L.bitP, p)) p = -1;
     }
     pg[k] = __builtin_amdgcn_readfirstlane(p);
+    ph[k] = __builtin_amdgcn_readfirstlane(p >= 0 ? q : -1);
     if (pg[k] >= 0) keep |= 1u << k;
   }
   __syncthreads();  // the list is read before the attention reuses the LDS
   WaveStates<NPW> st;
-  wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
+  wave_attend<BF16, PS, NPW>(a, h, qf, pg, st, ph);
   const PubDst pd = pub_dst(a, h, a.n_spec + a.n_miss + u);
   if constexpr (NPW == 1) {
     keep_fold_publish(a, ep, h, pg[0], st, pd, U.attn);

@@ -116,7 +116,8 @@ struct FusedLaunch {
   uint64_t* t_mlist;  // [Hkv][cap] tagged missed pages
   uint64_t* t_part;   // [Hkv][nparts][G][2] tagged (m, l) of the partial states
   float* part_o;      // [Hkv][nparts][G][128] their outputs (complete before (m, l) are stored)
-  uint64_t* t_candk;  // [3][Hkv][n_score][132] tagged candidate count, then keys: A, P^{t+1}, late
+  uint64_t* t_candk;  // [3][Hkv][n_score][132] tagged candidate count, then keys (A, P^{t+1}) or
+                      //   physical pages (late)
   uint64_t* t_candp;  // [3][Hkv][n_score][128] tagged candidate pages (bit 31: forced, bit 30: late)
   uint64_t* t_pkey;   // [Hkv][max_pages] tagged keys of the next prediction (EMA)
   uint64_t* t_lcnt;   // [Hkv][8][32] tagged number of late-speculated pages
