@@ -1425,7 +1425,7 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, uint32_t ep, 
   float qv[16];
   qbar_load<BF16>(a, h, qv);
   const float qe = qn_ema(a, qbar_finish(a, qv, L.qb), qe0);
-  const FCand c = cand_load<true>(a, ep, h, 1, L.off, L.tot, L.ck, L.cpg);
+  const FCand c = cand_load<false>(a, ep, h, 1, L.off, L.tot, L.ck, L.cpg);  // (no hurry: the next step's set)
   // every score workgroup has read the bounds: the scale of the next step's keys
   if (t == 0) a.win[4 * h + 3] = __float_as_uint(qe);
   if (a.kextra_p <= c.total - c.nforced && c.total <= kCandWave) {
