@@ -1647,7 +1647,7 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int
     uint64_t vm = 0, ve = 0;
     for (int it = 0; it < kFSpin; ++it) {
       vm = get_tag(rep_at(a.t_mcnt, h, u));
-      ve = get_tag(&ml[min(i, a.cap - 1)]);
+      if (lane < kFW * NPW) ve = get_tag(&ml[min(i, a.cap - 1)]);  // (only the entries of this chunk)
       if (tag_is(vm, ep)) {
         const uint32_t mv = (uint32_t)vm;
         const int nm = (mv & kSelfMiss) ? 0 : (int)(mv & kCountMask);
