@@ -160,7 +160,7 @@ __device__ __forceinline__ float qn_ema(const FusedLaunch& a, float qn, float pr
   return prev > 0.0f ? a.alpha * qn + (1.0f - a.alpha) * prev : qn;
 }
 
-template <bool BF16>
+template <bool BF16, int PS>
 __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, int h, int blk, FScoreLds& S) {
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int G = a.group;
@@ -313,6 +313,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   uint64_t* ck_p = a.t_candk + rec_p * kCandStride + 1;
   uint64_t* cp_p = a.t_candp + rec_p * kFScorePages;
   int na = 0, nfa = 0, np = 0, nfp = 0, nl = 0;
+  uint64_t lmask[kHalves];  // late pages of each half
   // candidates of A first (the select workgroup waits for them), each flagged when it is
   // also a page for late speculation: not forced, not in P^t, key at least lo_l ...
   const size_t rec_l = (2 * (size_t)a.num_kv_heads + h) * a.n_score + blk;
@@ -334,6 +335,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     const bool ca = inr && (f || ka >= lo_a);
     const bool late = a.late && ca && !f && ka >= lo_l && !((pw[half] >> (p & 31)) & 1u);
     const uint64_t ma = __ballot(ca), mfa = __ballot(ca && f), ml = __ballot(late);
+    lmask[half] = ml;
     if (ca) {
       const int pos = na + lanes_below(ma);
       put_tag(&ck_a[pos], ka, ep);
@@ -353,6 +355,44 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   if (lane == 0) {
     put_tag(ck_a - 1, (uint32_t)na | ((uint32_t)nfa << 16), ep);
     if (a.late) put_tag(ck_l - 1, (uint32_t)nl, ep);
+  }
+  // The K and V of the first late pages, one word per 64-byte line, read now: the late
+  // workgroups load them about two microseconds later and then find them in the
+  // memory-side cache.  The words only feed a check at the end of this role.
+  constexpr int kPfLoads = PS * kHeadDim * 2 / (64 * kWave);  // instructions per K (or V) of a page
+  constexpr int kPfPages = 8;
+  uint32_t pf[kPfPages][2 * kPfLoads];
+#pragma unroll
+  for (int k = 0; k < kPfPages; ++k) {
+#pragma unroll
+    for (int j = 0; j < 2 * kPfLoads; ++j) pf[k][j] = 0u;
+  }
+  if (a.late) {
+    const char* kh = static_cast<const char*>(a.k_cache) + (size_t)h * a.max_pages * PS * kHeadDim * 2;
+    const char* vh = static_cast<const char*>(a.v_cache) + (size_t)h * a.max_pages * PS * kHeadDim * 2;
+    uint64_t m0 = lmask[0], m1 = kHalves > 1 ? lmask[kHalves - 1] : 0ull;
+#pragma unroll
+    for (int k = 0; k < kPfPages; ++k) {
+      int q = -1;
+      if (m0) {
+        const int l = __builtin_ctzll(m0);
+        m0 &= m0 - 1;
+        q = __builtin_amdgcn_readlane(ph[0], l);
+      } else if (m1) {
+        const int l = __builtin_ctzll(m1);
+        m1 &= m1 - 1;
+        q = __builtin_amdgcn_readlane(ph[kHalves - 1], l);
+      }
+      if (q >= 0 && q < a.max_pages) {
+        const size_t page = (size_t)q * PS * kHeadDim * 2;
+#pragma unroll
+        for (int j = 0; j < kPfLoads; ++j) {
+          const size_t o = page + ((size_t)j * kWave + lane) * 64;
+          pf[k][j] = *reinterpret_cast<const uint32_t*>(kh + o);
+          pf[k][kPfLoads + j] = *reinterpret_cast<const uint32_t*>(vh + o);
+        }
+      }
+    }
   }
   if (!ema) return;
   // ... then the EMA update of Eq. (3) and the candidates of the next prediction
@@ -396,6 +436,13 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     nfp += __popcll(mfp);
   }
   if (lane == 0) put_tag(ck_p - 1, (uint32_t)np | ((uint32_t)nfp << 16), ep);
+  uint32_t px = 0u;
+#pragma unroll
+  for (int k = 0; k < kPfPages; ++k) {
+#pragma unroll
+    for (int j = 0; j < 2 * kPfLoads; ++j) px ^= pf[k][j];
+  }
+  if (px == ep * 2654435761u + 0x9e3779b9u) atomicOr(a.flags, 0u);  // (no effect when it holds)
 }
 
 // ------------------------------------------------------------------------ shared select pieces
@@ -1812,7 +1859,7 @@ __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
   int b = blockIdx.x;
   const int H = a.num_kv_heads;
   if (b < H * a.n_score) {
-    role_score<BF16>(a, ep, b / a.n_score, b % a.n_score, U.score);
+    role_score<BF16, PS>(a, ep, b / a.n_score, b % a.n_score, U.score);
     return;
   }
   b -= H * a.n_score;
