@@ -319,6 +319,34 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   const size_t rec_l = (2 * (size_t)a.num_kv_heads + h) * a.n_score + blk;
   uint64_t* ck_l = a.t_candk + rec_l * kCandStride + 1;
   uint64_t* cp_l = a.t_candp + rec_l * kFScorePages;
+  // the late list first (late speculation is the longer chain after the scores)
+  bool lt[kHalves];
+#pragma unroll
+  for (int half = 0; half < kHalves; ++half) {
+    lt[half] = false;
+    lmask[half] = 0ull;
+  }
+#pragma unroll
+  for (int half = 0; half < kHalves && a.late; ++half) {
+    const int lp = 64 * half + lane;
+    const int p = pbase + lp;
+    const bool inr = p < n && lp < kFScorePages;
+    const bool f = inr && ((S.fbits[lp >> 5] >> (lp & 31)) & 1u);
+    const uint32_t ka = score_key(S.sc[min(lp, kFScorePages - 1)]);
+    const bool late = a.late && inr && !f && ka >= lo_l && !((pw[half] >> (p & 31)) & 1u);
+    const uint64_t ml = __ballot(late);
+    lt[half] = late;
+    lmask[half] = ml;
+    if (late) {
+      // a late page is listed with its physical page in place of its key (the late
+      // workgroups only attend it; the select ranks the candidates of A)
+      const int pos = nl + lanes_below(ml);
+      put_tag(&ck_l[pos], (uint32_t)ph[half], ep);
+      put_tag(&cp_l[pos], (uint32_t)p, ep);
+    }
+    nl += __popcll(ml);
+  }
+  if (a.late && lane == 0) put_tag(ck_l - 1, (uint32_t)nl, ep);
 #pragma unroll
   for (int half = 0; half < kHalves; ++half) {
     const int lp = 64 * half + lane;
@@ -333,29 +361,17 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     }
     const uint32_t ka = score_key(sv);
     const bool ca = inr && (f || ka >= lo_a);
-    const bool late = a.late && ca && !f && ka >= lo_l && !((pw[half] >> (p & 31)) & 1u);
-    const uint64_t ma = __ballot(ca), mfa = __ballot(ca && f), ml = __ballot(late);
-    lmask[half] = ml;
+    const bool late = lt[half];
+    const uint64_t ma = __ballot(ca), mfa = __ballot(ca && f);
     if (ca) {
       const int pos = na + lanes_below(ma);
       put_tag(&ck_a[pos], ka, ep);
       put_tag(&cp_a[pos], (uint32_t)p | (f ? 0x80000000u : 0u) | (late ? 0x40000000u : 0u), ep);
     }
-    if (late) {
-      // a late page is listed with its physical page in place of its key (the late
-      // workgroups only attend it; the select ranks the candidates of A)
-      const int pos = nl + lanes_below(ml);
-      put_tag(&ck_l[pos], (uint32_t)ph[half], ep);
-      put_tag(&cp_l[pos], (uint32_t)p, ep);
-    }
     na += __popcll(ma);
     nfa += __popcll(mfa);
-    nl += __popcll(ml);
   }
-  if (lane == 0) {
-    put_tag(ck_a - 1, (uint32_t)na | ((uint32_t)nfa << 16), ep);
-    if (a.late) put_tag(ck_l - 1, (uint32_t)nl, ep);
-  }
+  if (lane == 0) put_tag(ck_a - 1, (uint32_t)na | ((uint32_t)nfa << 16), ep);
   // The K and V of the first late pages, one word per 64-byte line, read now: the late
   // workgroups load them about two microseconds later and then find them in the
   // memory-side cache.  The words only feed a check at the end of this role.
