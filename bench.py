@@ -69,11 +69,16 @@ def score_kernel_bytes(cfg, n_pages):
 
 
 def kernel_source_hash():
+    """Hash of the device sources' code (comments, blank lines and trailing blanks left out,
+    so that only a change of the code itself invalidates the recorded counters)."""
+    import re
     h = hashlib.sha256()
     for f in ("paper_2606_30389_amd/csrc/prr_kernels.hip", "paper_2606_30389_amd/csrc/prr_fused.hip",
               "paper_2606_30389_amd/csrc/prr_select.h", "paper_2606_30389_amd/csrc/prr_device.h"):
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
+            text = re.sub(r"/\*.*?\*/", "", fh.read(), flags=re.S)
+        lines = (re.sub(r"//.*$", "", ln).rstrip() for ln in text.splitlines())
+        h.update("\n".join(ln for ln in lines if ln).encode())
     return h.hexdigest()[:16]
 
 

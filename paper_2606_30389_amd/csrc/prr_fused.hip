@@ -759,9 +759,10 @@ struct FCand {
 };
 
 // POLL_ALL: every thread polls (the count and the first entries of one score workgroup
-// per eight threads, the fastest hand-off); otherwise one wave polls the counts and the
-// entries are loaded afterwards (for workgroups that are not on the critical path, so
-// that they do not slow the others' polls down).
+// per kFThreadsPerList threads: one round trip after the last list, used by the select
+// workgroup); otherwise one wave polls the counts and the entries are loaded afterwards,
+// a light poll for the many late-speculation workgroups and for the predict workgroup
+// (polling every list's entries from all of them measured slower).
 template <bool POLL_ALL>
 __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, int h, int which, int* off, int* tot, uint32_t* lk,
                                            uint32_t* lp) {
