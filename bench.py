@@ -22,6 +22,7 @@ layer-step on a bounded sample (rank 0 only).
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import math
@@ -336,6 +337,22 @@ def main():
     s = torch.cuda.Stream(device=dev)
     p = torch.cuda.Stream(device=dev)
     stack = R.DecodeStack(layers, [q_static[l] for l in range(n_layers)], dev)
+    # The serial baseline runs at its own best chunk (4 pages: twice the attending
+    # workgroups, measured faster for it; speculation is fastest at 8), on layer states of
+    # its own that share the K/V cache and metadata.
+    serial_chunk = pc.chunk_pages
+    stack_serial = stack
+    if "fused_serial" in args.schedules.split(",") and args.chunk is None:
+        serial_chunk = min(4, 256 // cfg.page_size)
+        if serial_chunk != pc.chunk_pages:
+            pc_s = dataclasses.replace(pc, chunk_pages=serial_chunk)
+            layers_s = []
+            for st in layers:
+                st2 = R.LayerState(pc_s, dev, k=st.k, v=st.v, page_table=st.page_table)
+                st2.meta.copy_(st.meta)
+                layers_s.append(st2)
+            stack_serial = R.DecodeStack(layers_s, [q_static[l] for l in range(n_layers)], dev)
+    cur = [stack]
     tok = [0]
 
     def run(n, schedule, measure_hits=False, tag=None):
@@ -344,9 +361,9 @@ def main():
             with torch.cuda.stream(s):
                 q_static.copy_(q_all[tok[0]])
             if tag is None:
-                stack.step(schedule, s, p)
+                cur[0].step(schedule, s, p)
             else:
-                stack.replay(schedule, s, tag)
+                cur[0].replay(schedule, s, tag)
             tok[0] += 1
             if measure_hits:
                 torch.cuda.synchronize()
@@ -371,6 +388,7 @@ def main():
     hits = run(max(2, args.warmup), L.PRR_SCHED_FUSED_PRR, measure_hits=True)
     ms = {}
     for name in schedules:  # warm each schedule, then two timed passes (the better one counts)
+        cur[0] = stack_serial if name == "fused_serial" else stack
         stack.params.late_spec = int(name.startswith("fused_prr_late"))
         run(2, sched_id[name])
         # *_graph: the token's launches are captured as HIP graphs (one per parity of the
@@ -382,6 +400,7 @@ def main():
             tag = name
             run(2, sched_id[name], tag=tag)
         ms[name] = min(timed(args.steps, sched_id[name], tag), timed(args.steps, sched_id[name], tag))
+    cur[0] = stack
     stack.params.late_spec = 0
     ablation = None
     if args.ablation:
@@ -507,7 +526,7 @@ def main():
         "config": {"workload": f"{cfg.name}: {n_layers} layers x ({cfg.num_q_heads} q / {cfg.num_kv_heads} kv heads, "
                                f"d {cfg.head_dim}), {cfg.dtype}, {cfg.context}-token context, page {cfg.page_size}, "
                                f"top-{cfg.k_select} pages, batch 1",
-                   "mode": args.mode, "chunk_pages": pc.chunk_pages, "p_select": p_select, "theta": list(theta),
+                   "mode": args.mode, "chunk_pages": pc.chunk_pages, "serial_chunk_pages": serial_chunk, "p_select": p_select, "theta": list(theta),
                    "schedule": main_sched},
         "us_per_layer": {k: round(v, 3) for k, v in us.items()},
         "achieved_gbps": round(achieved, 1),
