@@ -571,6 +571,7 @@ FUSED_CASES = [
     ("llama64k", 300, 1, None, 1, None, 2, 3),
     ("infllm128k", 200, 0, None, 1, None, 1, 3),
     ("glm128k", None, 0, None, 1, None, 1, 2),  # full size: 8192 pages, top-256
+    ("glm128k", None, 0, 4, 1, None, 1, 2),     # full size at chunk 4 (the serial baseline's)
     # ablation stages: theta = (1, 0.5, 0) predicts the previous step's top-K; with a
     # recompute on any miss (S1) and with repair (S2)
     ("glm32k", 512, 2, None, 1, None, 1, 3, (1.0, 0.5, 0.0)),
