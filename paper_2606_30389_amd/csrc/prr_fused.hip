@@ -318,12 +318,13 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
   uint64_t* cp_p = a.t_candp + rec_p * kFScorePages;
   int na = 0, nfa = 0, np = 0, nfp = 0, nl = 0;
   uint64_t lmask[kHalves];  // late pages of each half
-  // candidates of A first (the select workgroup waits for them), each flagged when it is
-  // also a page for late speculation: not forced, not in P^t, key at least lo_l ...
+  // Late pages (not forced, not in the bitmap of P^t, key at least lo_l) are listed first:
+  // late speculation is the longer chain after the scores.  Then the candidates of A (the
+  // select workgroup waits for them), each flagged when it is also a late page, then the
+  // EMA update and the candidates of the next prediction.
   const size_t rec_l = (2 * (size_t)a.num_kv_heads + h) * a.n_score + blk;
   uint64_t* ck_l = a.t_candk + rec_l * kCandStride + 1;
   uint64_t* cp_l = a.t_candp + rec_l * kFScorePages;
-  // the late list first (late speculation is the longer chain after the scores)
   bool lt[kHalves];
 #pragma unroll
   for (int half = 0; half < kHalves; ++half) {
