@@ -587,6 +587,7 @@ __device__ __forceinline__ SelThreshold bsel_threshold(const uint32_t (&key)[2],
       S.res[0] = bstar;
       S.res[1] = above;
       S.res[2] = (int)S.hist[bstar];
+      S.res[3] = 0;  // the compaction counter of a small bin
     }
     __syncthreads();
     const int bstar = S.res[0], cbin = S.res[2];
@@ -605,6 +606,35 @@ __device__ __forceinline__ SelThreshold bsel_threshold(const uint32_t (&key)[2],
       r.T = (uint32_t)S.res[3];
       r.need_eq = rank;
       r.eq_total = 1;
+      return r;
+    }
+    if (cbin <= kWave) {
+      // Few keys in the bin that holds rank K: they go to LDS (the histogram is read no
+      // more) and one wave ranks them, instead of another histogram pass.  T is the
+      // rank-th largest of them; the keys equal to T all lie in this bin.
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        if (cand[j] && key[j] >= lo && key[j] <= hi) S.hist[atomicAdd(&S.res[3], 1)] = key[j];
+      __syncthreads();
+      if (w == 0) {
+        const int nb = min(S.res[3], kWave);
+        const uint32_t mk = lane < nb ? S.hist[lane] : 0u;
+        int gt = 0, eq = 0;
+        for (int j = 0; j < nb; ++j) {
+          const uint32_t o = S.hist[j];
+          gt += o > mk ? 1 : 0;
+          eq += o == mk ? 1 : 0;
+        }
+        if (lane < nb && gt < rank && rank <= gt + eq) {  // (every lane holding T writes the same)
+          S.red[0][0] = mk;
+          S.red[0][1] = (uint32_t)(rank - gt);
+          S.red[0][2] = (uint32_t)eq;
+        }
+      }
+      __syncthreads();
+      r.T = S.red[0][0];
+      r.need_eq = (int)S.red[0][1];
+      r.eq_total = (int)S.red[0][2];
       return r;
     }
   }

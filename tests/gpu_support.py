@@ -43,10 +43,13 @@ def path_config(cfg: W.Config, num_pages=None, chunk_pages=None, mode=0, num_tok
                         alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma, chunk_pages=chunk_pages, mode=mode)
 
 
-def make_layer(cfg: W.Config, pc, layer=0, epoch=0, page_table=None, num_physical=None):
-    """Upload one layer's keys and values; returns (LayerState, LayerInputs)."""
+def make_layer(cfg: W.Config, pc, layer=0, epoch=0, page_table=None, num_physical=None, levels=None):
+    """Upload one layer's keys and values; returns (LayerState, LayerInputs).  levels: page p
+    takes the keys of page p mod levels, so that scores come in `levels` tied groups."""
     torch, P, R = torch_and_lib()
     li = W.layer_inputs(cfg, layer, epoch, num_pages=pc.num_pages)
+    if levels:
+        li.k_bits[:] = li.k_bits[:, np.arange(li.k_bits.shape[1]) % levels]
     dev = torch.device("cuda:0")
     if page_table is not None:
         kb = W.to_physical(li.k_bits, page_table, num_physical)

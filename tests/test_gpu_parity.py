@@ -583,13 +583,18 @@ FUSED_CASES = [
     ("llama64k", 300, 1, None, 1, None, 1, 3, None, True),
     ("infllm128k", 200, 0, None, 1, None, 1, 3, None, True),
     ("tiny", None, 0, 3, 1, 6, 1, 4, None, True),
+    # scores in 12 tied groups of ~43 pages: the threshold falls inside a group, so the
+    # select ranks a small bin of equal keys and cuts the tie by page index
+    ("glm32k", 512, 0, None, 1, None, 1, 3, None, False, 12),
+    ("glm32k", 512, 0, None, 1, None, 1, 3, None, True, 12),
 ]
 
 
 @pytest.mark.parametrize("case", FUSED_CASES,
                          ids=lambda c: f"{c[0]}-p{c[1]}-m{c[2]}-c{c[3]}-d{c[4]}-k{c[5]}"
                          + ("-reuse" if len(c) > 8 and c[8] is not None else "")
-                         + ("-late" if len(c) > 9 and c[9] else ""))
+                         + ("-late" if len(c) > 9 and c[9] else "")
+                         + (f"-lv{c[10]}" if len(c) > 10 else ""))
 def test_fused_decode_step(torch, case):
     """The fused schedules of prr_decode_step (one launch per layer): step-0 select + EMA
     initialisation, then per step the PRR launch and the serial launch, every layer
@@ -600,6 +605,7 @@ def test_fused_decode_step(torch, case):
     cfg = W.CONFIGS[name]
     theta = case[8] if len(case) > 8 and case[8] is not None else (cfg.alpha, cfg.beta, cfg.gamma)
     late = bool(case[9]) if len(case) > 9 else False
+    levels = case[10] if len(case) > 10 else None
     layers, inputs, metas, qs, queries = [], [], [], [], []
     for layer in range(n_layers):
         pc = S.path_config(cfg, num_pages=npages, mode=mode, chunk_pages=chunk)
@@ -609,7 +615,7 @@ def test_fused_decode_step(torch, case):
         pc.alpha, pc.beta, pc.gamma = theta
         S.log(f"fused {name} layer {layer} pages={pc.num_pages} mode={mode} chunk={pc.chunk_pages} "
               f"K={pc.k_select} |P|={pc.p_select}")
-        st, li = S.make_layer(cfg, pc, layer=layer)
+        st, li = S.make_layer(cfg, pc, layer=layer, levels=levels)
         st.build_meta()
         layers.append(st)
         inputs.append(li)
