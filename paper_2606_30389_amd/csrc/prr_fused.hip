@@ -145,7 +145,10 @@ struct FLds {
   // Values polled by one wave and read by the whole workgroup: hundreds of waves
   // polling the same word would queue at its memory channel and slow every hand-off.
   uint32_t bc[2 + 2 * kFW];
+  // the G query rows of the KV head (attending roles; never reused within a role)
+  u32x4_t qs[16 * kHeadDim / 8];
 };
+static_assert(sizeof(FLds) <= 80 * 1024, "two workgroups per CU");
 
 // ------------------------------------------------------------------------ score
 //
@@ -507,14 +510,21 @@ __device__ __forceinline__ float v_elem(const u32x4_t& v, int e) {
 // V[4j+tg][8m+cb] and p[head n][4j+tg].
 // Query fragments of KV head h for the MFMA layout below (lane 16j+n: head n, channels
 // 32j..32j+31), loaded before a workgroup waits for its page list.
-__device__ __forceinline__ void load_q(const FusedLaunch& a, int h, u32x4_t (&qf)[4]) {
-  const int lane = lane_id(), j = lane >> 4, n = lane & 15;
+// The MFMA operand fragments of q (G rows of the KV head): the rows are read from memory
+// once per workgroup into LDS and the waves take their fragments from there.  Eight
+// waves each reading the whole of q put eight times the traffic through the CU's memory
+// pipeline at the launch's start, where the attending workgroups share CUs with score
+// workgroups that are still reading metadata.  Called by every thread (one barrier).
+__device__ __forceinline__ void load_q(const FusedLaunch& a, int h, u32x4_t (&qf)[4], u32x4_t* qs) {
+  const int t = threadIdx.x, lane = lane_id(), j = lane >> 4, n = lane & 15;
   const int G = a.group;
-  const uint16_t* qh = static_cast<const uint16_t*>(a.q) + (size_t)h * G * kHeadDim;
+  constexpr int kRow = kHeadDim / 8;  // 16-byte words per row
+  const u32x4_t* qh = reinterpret_cast<const u32x4_t*>(static_cast<const uint16_t*>(a.q) + (size_t)h * G * kHeadDim);
+  if (t < G * kRow) qs[t] = qh[t];
+  __syncthreads();
   if (n < G) {
-    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(qh + (size_t)n * kHeadDim + 32 * j);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) qf[s] = src[s];
+    for (int s = 0; s < 4; ++s) qf[s] = qs[n * kRow + 4 * j + s];
   } else {
 #pragma unroll
     for (int s = 0; s < 4; ++s) qf[s] = u32x4_t{0, 0, 0, 0};
@@ -1101,7 +1111,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
     pg[0] = __builtin_amdgcn_readfirstlane(w < nM ? L.mlist[w] : -1);
     __syncthreads();  // the list is read before the attention reuses the LDS
     u32x4_t qf[4];
-    load_q(a, h, qf);
+    load_q(a, h, qf, U.qs);
     WaveStates<1> st;
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
     fold_publish<1>(pub_dst(a, h, a.n_spec), ep, st, 1u, U.attn);
@@ -1233,7 +1243,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
     pg[0] = __builtin_amdgcn_readfirstlane(w < nM ? L.mlist[w] : -1);
     __syncthreads();  // the list is read before the attention reuses the LDS
     u32x4_t qf[4];
-    load_q(a, h, qf);
+    load_q(a, h, qf, U.qs);
     WaveStates<1> st;
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
     fold_publish<1>(pub_dst(a, h, a.n_spec), ep, st, 1u, U.attn);
@@ -1613,7 +1623,7 @@ __device__ __forceinline__ void role_spec(const FusedLaunch& a, uint32_t ep, int
   const int cnt = min(a.chunk, count - start);
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   u32x4_t qf[4];
-  load_q(a, h, qf);
+  load_q(a, h, qf, U.qs);
   int pg[NPW];
   uint32_t keep = 0;
 #pragma unroll
@@ -1651,7 +1661,7 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, uint32_t ep, int
   const int t = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane((int)(t / kWave));
   u32x4_t qf[4];
-  load_q(a, h, qf);
+  load_q(a, h, qf, U.qs);
   // P^t as an LDS bitmap: a page of P^t is never attended here (the hint bitmap the
   // score workgroups filtered with may be stale)
   const int n = a.num_pages, nw = (n + 31) >> 5;
@@ -1706,7 +1716,7 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int
   const int start = u * a.chunk;
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   u32x4_t qf[4];
-  load_q(a, h, qf);
+  load_q(a, h, qf, U.qs);
   static_assert(1 + kFW * NPW <= 2 + 2 * kFW, "broadcast area");
   const uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
   if (w == 0) {
