@@ -1427,10 +1427,11 @@ __device__ __forceinline__ void predict_finish(const FusedLaunch& a, uint32_t ep
   update_window<J>(a, a.win + 4 * h + 1, qe, key, cand, (5 * a.kextra_p) / 2, keep_window, L.sel);
 }
 
-// The next prediction from a short candidate list, as select_wave does for A: wave 0
-// ranks the keys (12 per lane) and writes P^{t+1} in page order, wave 1 the next step's
-// bound of the candidates (rank 2.5 |P|), the other waves clear the bitmap meanwhile.
-__device__ __forceinline__ void predict_wave(const FusedLaunch& a, int h, int total, float qe, FSelLds& L) {
+// The next prediction from a short candidate list and the workgroup's threshold, as
+// select_wave does for A: wave 0 writes P^{t+1} in page order, wave 1 finds the next
+// step's bound of the candidates (rank 2.5 |P|), the other waves clear the bitmap meanwhile.
+__device__ __forceinline__ void predict_wave(const FusedLaunch& a, int h, int total, float qe, const SelThreshold& th,
+                                             FSelLds& L) {
   constexpr int NK = kCandWave / kWave;
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   const int nw = (a.num_pages + 31) >> 5, nwmax = (a.max_pages + 31) >> 5;
@@ -1453,7 +1454,6 @@ __device__ __forceinline__ void predict_wave(const FusedLaunch& a, int h, int to
     }
   }
   if (w == 0) {
-    const SelThreshold th = wsel_threshold<NK>(key, cand, a.kextra_p, L.ws[0], true);
     int eq_cut = kEqAll;
     in = wsel_membership<NK>(key, page, cand, force, th, &eq_cut);
     int32_t* out = a.pred_nxt + (size_t)h * a.cap;
@@ -1508,7 +1508,18 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, uint32_t ep, 
   // every score workgroup has read the bounds: the scale of the next step's keys
   if (t == 0) a.win[4 * h + 3] = __float_as_uint(qe);
   if (a.kextra_p <= c.total - c.nforced && c.total <= kCandWave) {
-    predict_wave(a, h, c.total, qe, L);
+    // the threshold of P^{t+1} by the whole workgroup (two keys per thread); then one wave
+    // writes the list while another finds the next step's bound
+    uint32_t k2[2];
+    bool c2[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int i = t + kFT * j;  // < kCandWave <= 2 kFT
+      k2[j] = L.ck[i];
+      c2[j] = i < c.total && !(L.cpg[i] >> 31);
+    }
+    const SelThreshold th = bsel_threshold<kFT>(k2, c2, a.kextra_p, L.bsel);
+    predict_wave(a, h, c.total, qe, th, L);
   } else if (a.kextra_p <= c.total - c.nforced && c.total <= kCandMax) {
     uint32_t key[4];
     int page[4];
