@@ -318,31 +318,54 @@ THETA_GRID = [(a, b, c)
               for c in (0.0, 0.25, 0.5, 0.75)]
 
 
-def calibration_objective(is_matrix: np.ndarray, k: int, theta, p_select: Optional[int] = None) -> float:
-    """Eq. (4): the score-weighted hit rate of the predictor simulated over a
-    trajectory of score vectors (rows = steps, columns = blocks), averaged over the
-    steps that have a prediction (every row after the first)."""
+def calibration_objective(is_matrix: np.ndarray, k: int, theta, p_select: Optional[int] = None,
+                          form_row: Optional[Sequence[int]] = None) -> float:
+    """Eq. (4): the score-weighted hit rate of the predictor simulated over a prefill
+    trajectory of score vectors (rows = prefill tokens phi, columns = blocks b).
+
+    Blocks form as the prefill grows: block b exists from row form_row[b] on (default:
+    every block from row 0).  As Section 4.1 initialises a block when it enters the
+    cache, block b's state is (level = IS_{phi,b}, trend = 0) at phi = form_row[b], and
+    the EMA of Eqs. (2)-(3) runs from there.  At row phi, A_phi is the top-k of the
+    blocks that exist, P_phi the top-|P| predictions of the blocks that already had a
+    state before phi (a block cannot be predicted at the row it forms); entries of
+    blocks that do not exist yet are never read.  The mean runs over the rows that have
+    a prediction (phi >= 1); a row whose selected scores sum to 0 contributes 0.
+    """
     alpha, beta, gamma = theta
     p_select = k if p_select is None else p_select
-    level, trend = ema_init(is_matrix[0])
+    n_rows, n_blocks = is_matrix.shape
+    born = np.zeros(n_blocks, dtype=np.int64) if form_row is None else np.asarray(form_row, dtype=np.int64)
+    level = np.zeros(n_blocks)
+    trend = np.zeros(n_blocks)
+    has_state = np.zeros(n_blocks, dtype=bool)
     total, count = 0.0, 0
-    for phi in range(1, is_matrix.shape[0]):
+    for phi in range(n_rows):
         row = is_matrix[phi]
-        pred = ema_predict(level, trend, gamma)
-        a = select_topk(row, k)
-        p = predicted_set(pred, p_select)
-        inter = np.intersect1d(a, p)
-        total += row[inter].sum() / row[a].sum()
-        count += 1
-        level, trend = ema_update(level, trend, row, alpha, beta)
+        exists = born <= phi
+        if phi >= 1:
+            pred = ema_predict(level, trend, gamma)
+            live = np.flatnonzero(exists)
+            a = live[select_topk(row[live], k)]
+            old = np.flatnonzero(has_state)
+            p = old[predicted_set(pred[old], p_select)]
+            denom = row[a].sum()
+            total += row[np.intersect1d(a, p)].sum() / denom if denom != 0.0 else 0.0
+            count += 1
+            level[has_state], trend[has_state] = ema_update(level[has_state], trend[has_state], row[has_state],
+                                                            alpha, beta)
+        new = exists & ~has_state
+        level[new], trend[new] = ema_init(row[new])
+        has_state |= new
     return total / max(count, 1)
 
 
-def calibrate(is_matrix: np.ndarray, k: int, grid=THETA_GRID, p_select: Optional[int] = None):
+def calibrate(is_matrix: np.ndarray, k: int, grid=THETA_GRID, p_select: Optional[int] = None,
+              form_row: Optional[Sequence[int]] = None):
     """Eq. (5): the grid point with the largest objective (first one on ties)."""
     best, best_val = None, -np.inf
     for theta in grid:
-        val = calibration_objective(is_matrix, k, theta, p_select)
+        val = calibration_objective(is_matrix, k, theta, p_select, form_row)
         if val > best_val:
             best, best_val = theta, val
     return best, best_val

@@ -358,3 +358,69 @@ def check_speculate_repair(spec_repair_fn, attend_fn, seed=12):
         if not all(np.allclose(x, y, atol=1e-12) for x, y in zip(kw, ref_u)):
             return False
     return True
+
+
+# ----------------------------------------------------------------------------- calibration
+
+def check_calibrate_closed_form(objective_fn, calibrate_fn, grid):
+    """Three rows of two blocks, k = |P| = 1, scores s0 = (1, 3), s1 = (2, 1), s2 = (5, 1).
+    Worked by hand from Eqs. (2)-(3): the state after row 1 is v = beta (s1 - s0),
+    l = s0 + alpha (s1 - s0), so the prediction of row 2 is s0 + c (s1 - s0) with
+    c = alpha + gamma beta: block 0 is predicted iff 1 + c > 3 - 2c, i.e. c > 2/3.  Row 1's
+    prediction is s0 (block 1) while A_1 = {0}: no hit.  Row 2's A_2 = {0}.  So Eq. (4) is
+    1/2 where alpha + gamma beta > 2/3 and 0 elsewhere (no grid point has c = 2/3), and
+    Eq. (5)'s first maximiser in grid order (alpha outer, then beta, then gamma) is
+    (0.4, 0.4, 0.75), the first point with c > 2/3."""
+    traj = np.array([[1.0, 3.0], [2.0, 1.0], [5.0, 1.0]])
+    for a, b, g in grid:
+        want = 0.5 if a + g * b > 2.0 / 3.0 else 0.0
+        if abs(objective_fn(traj, 1, (a, b, g)) - want) > 1e-12:
+            return False
+    best, val = calibrate_fn(traj, 1, grid)
+    return tuple(best) == (0.4, 0.4, 0.75) and abs(val - 0.5) <= 1e-12
+
+
+def check_calibrate_all_tied(calibrate_fn, grid, seed=13):
+    """A constant trajectory is predicted exactly by every theta (Eq. (4) = 1 for all), so
+    Eq. (5) returns the first grid point."""
+    row = np.abs(_rng(seed).standard_normal(10)) + 0.1
+    best, val = calibrate_fn(np.tile(row, (5, 1)), 3, grid)
+    return tuple(best) == tuple(grid[0]) and abs(val - 1.0) <= 1e-12
+
+
+def check_calibration_formation(objective_fn, grid):
+    """Block 1 forms at row 1 (its row-0 entry is junk that must never be read).  By hand,
+    k = |P| = 1, rows (2, junk), (2, 3), (2, 3): at row 1 only block 0 has a state, so
+    P_1 = {0} while A_1 = {1} (no hit); block 1's state starts at row 1 as (3, 0) and block
+    0 stays at (2, 0), so P_2 = {1} = A_2.  Eq. (4) is 1/2 for every theta.  A state begun at
+    row 0 -- from the junk, or from a placeholder 0 -- predicts row 1 or row 2 differently
+    for some theta."""
+    for junk in (100.0, 0.0):
+        traj = np.array([[2.0, junk], [2.0, 3.0], [2.0, 3.0]])
+        for theta in grid:
+            if abs(objective_fn(traj, 1, theta, None, [0, 1]) - 0.5) > 1e-12:
+                return False
+    return True
+
+
+def check_criticality_mean_bounds(meta_mean_fn, qbar_fn, score_fn, seed=14):
+    """The block-mean score lies between the smallest and the largest token score of the
+    block (a mean of the tokens' q-bar . k), equals it for a block of identical tokens, and
+    ignores tokens at or past num_tokens."""
+    r = _rng(seed)
+    k = r.standard_normal((2, 4, 16, 8))
+    q = r.standard_normal((6, 8))
+    nt = 3 * 16 + 5
+    kk = k.copy()
+    kk[:, 3, 5:] = 1e6
+    s = score_fn(qbar_fn(q, 2), meta_mean_fn(kk, 16, nt))
+    qb = qbar_fn(q, 2)
+    for h in range(2):
+        for p in range(4):
+            valid = 16 if p < 3 else 5
+            tok = k[h, p, :valid] @ qb[h]
+            if not (tok.min() - 1e-12 <= s[h, p] <= tok.max() + 1e-12):
+                return False
+    same = np.broadcast_to(k[0, 0, :1], (1, 1, 16, 8)).copy()
+    s1 = score_fn(qbar_fn(q[:3], 1), meta_mean_fn(same, 16, 16))
+    return abs(s1[0, 0] - float(same[0, 0, 0] @ qbar_fn(q[:3], 1)[0])) <= 1e-12

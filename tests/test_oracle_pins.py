@@ -159,6 +159,22 @@ def test_calibration_picks_trend_on_ramps():
     assert best[2] > 0.0 and val >= O.calibration_objective(traj, 3, (best[0], best[1], 0.0))
 
 
+def test_calibrate_closed_form_argmax():
+    assert pins.check_calibrate_closed_form(O.calibration_objective, O.calibrate, O.THETA_GRID)
+
+
+def test_calibrate_ties_take_first_grid_point():
+    assert pins.check_calibrate_all_tied(O.calibrate, O.THETA_GRID)
+
+
+def test_calibration_blocks_form_during_prefill():
+    assert pins.check_calibration_formation(O.calibration_objective, O.THETA_GRID)
+
+
+def test_criticality_mean_bounds():
+    assert pins.check_criticality_mean_bounds(O.page_metadata_mean, O.representative_query, O.criticality_mean)
+
+
 def test_dropped_page_changes_output():
     """On the tiny workload, removing any one selected page moves the output by more
     than the internal tolerance (1e-4), so a missed page is visible to the parity tests."""
@@ -267,6 +283,41 @@ def _merge_forgets_l(a, b):
     return (wa[:, None] * oa + wb[:, None] * ob) / (wa + wb)[:, None], mo, lo
 
 
+def _calibrate_argmin(traj, k, grid=O.THETA_GRID, p_select=None, form_row=None):
+    vals = [O.calibration_objective(traj, k, th, p_select, form_row) for th in grid]
+    i = int(np.argmin(vals))
+    return grid[i], vals[i]
+
+
+def _calibrate_last_on_ties(traj, k, grid=O.THETA_GRID, p_select=None, form_row=None):
+    vals = [O.calibration_objective(traj, k, th, p_select, form_row) for th in grid]
+    i = len(vals) - 1 - int(np.argmax(vals[::-1]))
+    return grid[i], vals[i]
+
+
+def _objective_state_from_row0(traj, k, theta, p_select=None, form_row=None):
+    return O.calibration_objective(traj, k, theta, p_select)
+
+
+def _objective_placeholder_zero(traj, k, theta, p_select=None, form_row=None):
+    t = np.array(traj, dtype=np.float64, copy=True)
+    if form_row is not None:
+        for b, r in enumerate(form_row):
+            t[:r, b] = 0.0
+    return O.calibration_objective(t, k, theta, p_select)
+
+
+def _objective_level_first(traj, k, theta, p_select=None, form_row=None):
+    import unittest.mock as um
+    from oracle import prr_oracle
+    with um.patch.object(prr_oracle, "ema_update", _ema_update_level_first):
+        return O.calibration_objective(traj, k, theta, p_select, form_row)
+
+
+def _criticality_mean_sum(qbar, means):
+    return O.criticality_mean(qbar, means) * 16
+
+
 def _spec_repair_skips_missed(q, k, v, sel, pred, ps, nt, keep_wasted=False):
     hq, hkv = q.shape[0], k.shape[0]
     spec = [(set(p) if keep_wasted else set(p) & set(a)) for a, p in zip(sel, pred)]
@@ -304,6 +355,19 @@ MUTANTS = [
     ("repair skips missed pages", lambda: pins.check_speculate_repair(_spec_repair_skips_missed, O.attend)),
     ("repair keeps wasted in exact mode", lambda: pins.check_speculate_repair(
         _spec_repair_keeps_wasted_always, O.attend)),
+    ("calibrate takes the argmin", lambda: pins.check_calibrate_closed_form(
+        O.calibration_objective, _calibrate_argmin, O.THETA_GRID)),
+    ("calibrate takes the last maximiser", lambda: pins.check_calibrate_closed_form(
+        O.calibration_objective, _calibrate_last_on_ties, O.THETA_GRID)),
+    ("calibrate last on all-tied grid", lambda: pins.check_calibrate_all_tied(_calibrate_last_on_ties, O.THETA_GRID)),
+    ("calibration objective with the level updated first", lambda: pins.check_calibrate_closed_form(
+        _objective_level_first, O.calibrate, O.THETA_GRID)),
+    ("calibration state from row 0 (junk)", lambda: pins.check_calibration_formation(
+        _objective_state_from_row0, O.THETA_GRID)),
+    ("calibration state from a placeholder 0", lambda: pins.check_calibration_formation(
+        _objective_placeholder_zero, O.THETA_GRID)),
+    ("block-mean score as a sum", lambda: pins.check_criticality_mean_bounds(
+        O.page_metadata_mean, O.representative_query, _criticality_mean_sum)),
 ]
 
 
