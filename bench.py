@@ -74,7 +74,7 @@ def kernel_source_hash():
     so that only a change of the code itself invalidates the recorded counters)."""
     import re
     h = hashlib.sha256()
-    for f in ("paper_2606_30389_amd/csrc/prr_kernels.hip", "paper_2606_30389_amd/csrc/prr_fused.hip",
+    for f in ("paper_2606_30389_amd/csrc/prr_kernels.hip", "paper_2606_30389_amd/csrc/prr_fused_impl.h",
               "paper_2606_30389_amd/csrc/prr_select.h", "paper_2606_30389_amd/csrc/prr_device.h"):
         with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
             text = re.sub(r"/\*.*?\*/", "", fh.read(), flags=re.S)
@@ -135,7 +135,7 @@ def cpu_baseline(cfg, budget_s):
 
 def kernel_sweep(args):
     """Attention over a given selected set (the serial repair call: attend every page of A,
-    merge) on the kernel-comparison shape of Section 6.4: 32 query / 8 KV heads, head_dim
+    merge) on the kernel-comparison shape of Section 5.4: 32 query / 8 KV heads, head_dim
     128, a 131072-token fp16 cache, pages of 16 and 64 tokens, budgets of 1K to 8K tokens
     drawn uniformly per KV head.  Reports microseconds per call and GB/s of selected K/V."""
     import torch
@@ -176,7 +176,7 @@ def kernel_sweep(args):
                          "gbps": round(kv_bytes / (us * 1e-6) / 1e9, 1)})
             print(f"[kernel-sweep] {rows[-1]}", file=sys.stderr, flush=True)
             del st
-    print(json.dumps({"sweep": "sparse attention over a selected set (Section 6.4 shape)", "table": rows}), flush=True)
+    print(json.dumps({"sweep": "sparse attention over a selected set (Section 5.4 shape)", "table": rows}), flush=True)
 
 
 def delta_sweep(args, cfg):
@@ -258,7 +258,7 @@ def main():
                          "latency per context length and delta, and the fused PRR step; prints the table")
     ap.add_argument("--write-lut", default=None, metavar="PATH", help="with --delta-sweep: also write the table as JSON")
     ap.add_argument("--kernel-sweep", action="store_true",
-                    help="only the sparse-attention kernel sweep (Table 3 shape: 32 q / 8 kv heads, d 128, 128K "
+                    help="only the sparse-attention kernel sweep (Section 5.4, Table tab:kernel_table shape: 32 q / 8 kv heads, d 128, 128K "
                          "context, page 16 and 64, budget 1K-8K tokens): microseconds and GB/s")
     ap.add_argument("--calibrate", type=int, default=0, metavar="ROWS",
                     help="calibrate theta (Section 4.2) on ROWS prefill score rows of the first 4 layers, then "
@@ -404,7 +404,7 @@ def main():
     stack.params.late_spec = 0
     ablation = None
     if args.ablation:
-        # Section 6.3: S1 reuses the previous step's top-K (theta = (1, .5, 0)) and
+        # Section 5.3: S1 reuses the previous step's top-K (theta = (1, .5, 0)) and
         # recomputes attention over A on any miss; S2 repairs instead; S3 is the EMA
         # predictor with repair.  Every stage restarts from a fresh prefill.
         ablation = {}

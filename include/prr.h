@@ -71,7 +71,7 @@ typedef int32_t prr_status;
 #define PRR_RECOMPUTE_ON_MISS 2 /* fused schedules only: output = attention over exactly A, but when
                                    any page of A was not predicted the speculation is discarded and
                                    all of A is attended afresh (the ablation stage without repair,
-                                   Section 6.3) */
+                                   Section 5.3) */
 
 /* Shape of one layer's paged KV cache.
  *   head_dim   128 (the only compiled value)
@@ -196,9 +196,11 @@ prr_status prr_spec_attn(const prr_dims* dims, const void* q, const void* k_cach
  *   part_o, part_m, part_l, page_m   the speculation output of prr_spec_attn over P
  *                with the same cap and chunk_pages (ignored when P is NULL)
  *   mode         PRR_EXACT_SELECTED: chunks of P that hold a wasted page (P \ A) have
- *                the wasted pages' contribution removed (re-attended and subtracted when
- *                they carry at most half of the chunk's softmax mass, otherwise the
- *                chunk's pages of A are re-attended); PRR_KEEP_WASTED: P u A is attended
+ *                the wasted pages' contribution removed: re-attended and subtracted when
+ *                they carry at most 7/8 of the chunk's softmax mass for every query head
+ *                (the remaining part then holds at least 1/8 of it, so the subtraction
+ *                amplifies float32 rounding at most 8-fold), otherwise the chunk's pages
+ *                of A are re-attended; PRR_KEEP_WASTED: P u A is attended
  *   out_o32      device [Hq][128] float32 out, out_o device [Hq][128] dtype out or NULL
  *   out_m, out_l device [Hq] float32 out
  *   missed_count, wasted_count  device [Hkv] int32 out: |A \ P|, |P \ A|
@@ -306,24 +308,49 @@ prr_status prr_epoch_advance(uint32_t* epoch_dev, hipStream_t stream);
 
 /* Online calibration of the EMA predictor (Section 4.2): for each candidate theta =
  * (alpha, beta, gamma) of `grid`, the score-weighted hit rate of Eq. (4) -- the EMA of
- * Eqs. (2)-(3) simulated over each trajectory, P_phi = top-p_select of the prediction,
- * A_phi = top-k_select of row phi (ties: lower block index; keys rounded to float32 as on
- * the device), averaged over rows 1..n_rows-1 and then over the trajectories -- and the
- * argmax of Eq. (5) (the first grid point on ties).  Host code, run on the CPU while the
- * device finishes the prefill; no device memory is touched.
- *   scores         host [n_traj][n_rows][n_blocks] float32 prefill score trajectories
- *                  (a block not formed yet at a row carries a score below every formed
- *                  block's, e.g. 0 when scores are positive; the EMA of a -inf score is NaN)
+ * Eqs. (2)-(3) simulated over each prefill trajectory, P_phi = top-p_select of the
+ * prediction, A_phi = top-k_select of row phi (ties: lower block index; keys rounded to
+ * float32 as on the device) -- and the argmax of Eq. (5) (the first grid point on ties).
+ * Blocks form as the prefill grows: block b exists from row form_row[b] on; its state
+ * starts there as (level = its score, trend = 0), as Section 4.1 initialises a block when
+ * it enters the cache.  A_phi ranks the blocks that exist at row phi, P_phi the blocks
+ * that had a state before row phi.  The hit rates of rows 1..n_rows-1 (the rows with a
+ * prediction) are averaged, then over the trajectories.  Host code, run on the CPU while
+ * the device finishes the prefill; no device memory is touched.
+ *   scores         host [n_traj][n_rows][n_blocks] float32 prefill score trajectories;
+ *                  entries of blocks that do not exist yet at a row are never read
+ *   form_row       host [n_blocks] int32 >= 0, the row at which each block forms (shared by
+ *                  the trajectories), or NULL = every block exists from row 0
  *   k_select       |A_phi|; p_select: |P_phi| (0 = k_select)
  *   grid           host [n_grid][3] float32, alpha, beta in (0, 1], gamma in [0, 1]
  *   n_threads      host threads (0 = all hardware threads)
  *   best_theta     host [3] out: the argmax
  *   objective_out  host [n_grid] out (may be NULL): Eq. (4) per grid point
- * Errors: PRR_ERR_INVALID_ARG for NULL pointers, sizes < 1 (n_rows < 2), a grid point out
- * of range. */
-prr_status prr_calibrate(const float* scores, int32_t n_traj, int32_t n_rows, int32_t n_blocks, int32_t k_select,
-                         int32_t p_select, const float* grid, int32_t n_grid, int32_t n_threads, float* best_theta,
-                         double* objective_out);
+ * Errors: PRR_ERR_INVALID_ARG for NULL pointers, sizes < 1 (n_rows < 2), a negative
+ * form_row entry, a grid point out of range. */
+prr_status prr_calibrate(const float* scores, int32_t n_traj, int32_t n_rows, int32_t n_blocks,
+                         const int32_t* form_row, int32_t k_select, int32_t p_select, const float* grid,
+                         int32_t n_grid, int32_t n_threads, float* best_theta, double* objective_out);
+
+/* Critical-path-aware speculation budget (Section 4.4): the largest delta = |P| / |A|
+ * whose speculation latency fits within the selection window at `query_context`, from a
+ * table profiled offline (one row per context length and delta).  At a profiled context
+ * the row's latencies are used as measured; at any other context each delta's selection
+ * and speculation latencies are estimated by least-squares polynomial regression in
+ * log2(context) over that delta's rows (appendix "Profiling Overheads"), of degree
+ * min(degree, distinct profiled contexts - 1).  Host code.
+ *   context, delta, select_us, spec_us  host [n_rows] table columns (context >= 1,
+ *                delta >= 1, latencies >= 0), or NULL when n_rows = 0
+ *   degree       0..3
+ *   delta_out    host out: the chosen delta; 1 when no delta fits or the table is empty
+ *   select_est, spec_est  host out or NULL: the latencies of the chosen delta (estimated
+ *                or measured) at query_context (of the smallest profiled delta when none
+ *                fits; NaN when the table is empty)
+ * Errors: PRR_ERR_INVALID_ARG for NULL pointers, n_rows < 0, query_context < 1, a
+ * degree outside [0, 3], a table row out of range. */
+prr_status prr_pick_delta(const int32_t* context, const float* delta, const float* select_us, const float* spec_us,
+                          int32_t n_rows, int32_t query_context, int32_t degree, float* delta_out, float* select_est,
+                          float* spec_est);
 
 /* Merge n_states partial states per row (Eqs. (6)-(8) for arbitrary states).
  *   o  device [n_states][rows][d] float32, m, l device [n_states][rows] float32

@@ -43,7 +43,7 @@ EXPORTED = (
     "prr_status_string", "prr_last_error", "prr_workspace_size", "prr_workspace_init",
     "prr_spec_state_floats", "prr_build_page_meta", "prr_score_topk", "prr_predict",
     "prr_spec_attn", "prr_repair", "prr_merge_states", "prr_decode_step", "prr_calibrate",
-    "prr_epoch_advance",
+    "prr_epoch_advance", "prr_pick_delta",
 )
 
 
@@ -105,8 +105,9 @@ _SIGS = {
     "prr_merge_states": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _P]),
     "prr_decode_step": (_I, [_DIMS, ctypes.POINTER(prr_step_params), ctypes.POINTER(prr_layer_io), _I, _I, _I, _P,
                              _P, ctypes.POINTER(ctypes.c_void_p)]),
-    "prr_calibrate": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _P, _P]),
+    "prr_calibrate": (_I, [_P, _I, _I, _I, _P, _I, _I, _P, _I, _I, _P, _P]),
     "prr_epoch_advance": (_I, [_P, _P]),
+    "prr_pick_delta": (_I, [_P, _P, _P, _P, _I, _I, _I, _P, _P, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -221,8 +222,9 @@ def prr_epoch_advance(epoch_dev, stream=None):
     _check(_lib.prr_epoch_advance(_ptr(epoch_dev), _stream(stream)))
 
 
-def prr_calibrate(scores, k_select, grid, p_select=0, n_threads=0):
-    """scores: host float32 array [n_traj][n_rows][n_blocks]; grid: host float32 [n_grid][3].
+def prr_calibrate(scores, k_select, grid, p_select=0, n_threads=0, form_row=None):
+    """scores: host float32 array [n_traj][n_rows][n_blocks]; grid: host float32 [n_grid][3];
+    form_row: host int32 [n_blocks] (the row at which each block forms) or None.
     Returns (best theta as a tuple, objective per grid point as a float64 array)."""
     import numpy as np
     sc = np.ascontiguousarray(scores, dtype=np.float32)
@@ -231,9 +233,30 @@ def prr_calibrate(scores, k_select, grid, p_select=0, n_threads=0):
     g = np.ascontiguousarray(grid, dtype=np.float32).reshape(-1, 3)
     best = np.zeros(3, dtype=np.float32)
     obj = np.zeros(len(g), dtype=np.float64)
-    _check(_lib.prr_calibrate(sc.ctypes.data, sc.shape[0], sc.shape[1], sc.shape[2], k_select, p_select,
+    fr = None if form_row is None else np.ascontiguousarray(form_row, dtype=np.int32)
+    if fr is not None and fr.shape != (sc.shape[2],):
+        raise ValueError(f"form_row has shape {fr.shape}, expected ({sc.shape[2]},)")
+    _check(_lib.prr_calibrate(sc.ctypes.data, sc.shape[0], sc.shape[1], sc.shape[2],
+                              None if fr is None else fr.ctypes.data, k_select, p_select,
                               g.ctypes.data, len(g), n_threads, best.ctypes.data, obj.ctypes.data))
     return tuple(float(x) for x in best), obj
+
+
+def prr_pick_delta(rows, query_context, degree=2):
+    """rows: the profiled table, dicts with "context", "delta", "select_us", "spec_us".
+    Returns (delta, select_us estimate, spec_us estimate) at query_context."""
+    import numpy as np
+    ctx = np.ascontiguousarray([int(r["context"]) for r in rows], dtype=np.int32)
+    dl = np.ascontiguousarray([float(r["delta"]) for r in rows], dtype=np.float32)
+    se = np.ascontiguousarray([float(r["select_us"]) for r in rows], dtype=np.float32)
+    sp = np.ascontiguousarray([float(r["spec_us"]) for r in rows], dtype=np.float32)
+    out = (ctypes.c_float * 3)()
+    n = len(rows)
+    _check(_lib.prr_pick_delta(ctx.ctypes.data if n else None, dl.ctypes.data if n else None,
+                               se.ctypes.data if n else None, sp.ctypes.data if n else None, n, int(query_context),
+                               int(degree), ctypes.addressof(out), ctypes.addressof(out) + 4,
+                               ctypes.addressof(out) + 8))
+    return float(out[0]), float(out[1]), float(out[2])
 
 
 def prr_decode_step(dims, params, layers, parity, schedule, stream=None, spec_stream=None, events=None):

@@ -1,4 +1,5 @@
 // C ABI of libprr: argument validation, workspace carving, dispatch to the launchers.
+#include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -430,21 +431,47 @@ prr_status prr_repair(const prr_dims* dims, const void* q, const void* k_cache, 
   return hip_status(prr::launch_repair(a, stream), "repair launch");
 }
 
-prr_status prr_calibrate(const float* scores, int32_t n_traj, int32_t n_rows, int32_t n_blocks, int32_t k_select,
-                         int32_t p_select, const float* grid, int32_t n_grid, int32_t n_threads, float* best_theta,
-                         double* objective_out) {
+prr_status prr_calibrate(const float* scores, int32_t n_traj, int32_t n_rows, int32_t n_blocks,
+                         const int32_t* form_row, int32_t k_select, int32_t p_select, const float* grid, int32_t n_grid,
+                         int32_t n_threads, float* best_theta, double* objective_out) {
   if (!scores || !grid || !best_theta) return fail(PRR_ERR_INVALID_ARG, "scores, grid or best_theta is NULL");
   if (n_traj < 1 || n_rows < 2 || n_blocks < 1 || n_grid < 1)
     return fail(PRR_ERR_INVALID_ARG, "n_traj %d, n_rows %d (>= 2), n_blocks %d, n_grid %d", n_traj, n_rows, n_blocks,
                 n_grid);
   if (k_select < 0 || p_select < 0) return fail(PRR_ERR_INVALID_ARG, "k_select %d / p_select %d < 0", k_select, p_select);
+  if (form_row) {
+    for (int b = 0; b < n_blocks; ++b)
+      if (form_row[b] < 0) return fail(PRR_ERR_INVALID_ARG, "form_row[%d] = %d < 0", b, form_row[b]);
+  }
   for (int g = 0; g < n_grid; ++g) {
     const float a = grid[3 * g], b = grid[3 * g + 1], c = grid[3 * g + 2];
     if (!(a > 0.f && a <= 1.f) || !(b > 0.f && b <= 1.f) || !(c >= 0.f && c <= 1.f))
       return fail(PRR_ERR_INVALID_ARG, "grid point %d (%g, %g, %g) outside (0,1] x (0,1] x [0,1]", g, a, b, c);
   }
-  prr::calibrate_grid(scores, n_traj, n_rows, n_blocks, k_select, p_select, grid, n_grid, n_threads, best_theta,
-                      objective_out);
+  prr::calibrate_grid(scores, n_traj, n_rows, n_blocks, form_row, k_select, p_select, grid, n_grid, n_threads,
+                      best_theta, objective_out);
+  return ok();
+}
+
+prr_status prr_pick_delta(const int32_t* context, const float* delta, const float* select_us, const float* spec_us,
+                          int32_t n_rows, int32_t query_context, int32_t degree, float* delta_out, float* select_est,
+                          float* spec_est) {
+  if (!delta_out) return fail(PRR_ERR_INVALID_ARG, "delta_out is NULL");
+  if (n_rows < 0) return fail(PRR_ERR_INVALID_ARG, "n_rows %d < 0", n_rows);
+  if (n_rows > 0 && (!context || !delta || !select_us || !spec_us))
+    return fail(PRR_ERR_INVALID_ARG, "a table column is NULL");
+  if (query_context < 1) return fail(PRR_ERR_INVALID_ARG, "query_context %d < 1", query_context);
+  if (degree < 0 || degree > 3) return fail(PRR_ERR_INVALID_ARG, "degree %d outside [0, 3]", degree);
+  for (int i = 0; i < n_rows; ++i) {
+    if (context[i] < 1 || !(delta[i] >= 1.0f) || !(select_us[i] >= 0.0f) || !(spec_us[i] >= 0.0f))
+      return fail(PRR_ERR_INVALID_ARG, "table row %d: context %d, delta %g, select %g us, spec %g us", i, context[i],
+                  delta[i], select_us[i], spec_us[i]);
+  }
+  if (select_est) *select_est = NAN;
+  if (spec_est) *spec_est = NAN;
+  *delta_out = n_rows > 0 ? prr::pick_delta(context, delta, select_us, spec_us, n_rows, query_context, degree,
+                                            select_est, spec_est)
+                          : 1.0f;
   return ok();
 }
 

@@ -24,55 +24,67 @@ inline uint32_t key_of(double v) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Indices of the k largest keys (ties: lower index first), as a 0/1 membership vector.
-void top_k(const std::vector<uint64_t>& packed, int k, std::vector<uint64_t>& work, std::vector<uint8_t>& in) {
-  const int n = (int)packed.size();
+// Membership (0/1 by block index) of the k largest of the packed candidates (ties:
+// lower index first); `cand` holds only the blocks that may be chosen.
+void top_k(std::vector<uint64_t>& cand, int k, std::vector<uint8_t>& in) {
   std::fill(in.begin(), in.end(), 0);
-  if (k <= 0) return;
-  if (k >= n) {
-    std::fill(in.begin(), in.end(), 1);
-    return;
-  }
-  work = packed;  // key in the high word, ~index in the low word: larger = better
-  std::nth_element(work.begin(), work.begin() + (k - 1), work.end(), std::greater<uint64_t>());
-  for (int i = 0; i < k; ++i) in[~(uint32_t)work[i] & 0xffffffffu] = 1;
+  const int n = (int)cand.size();
+  if (k <= 0 || n == 0) return;
+  if (k < n) std::nth_element(cand.begin(), cand.begin() + (k - 1), cand.end(), std::greater<uint64_t>());
+  for (int i = 0; i < std::min(k, n); ++i) in[~(uint32_t)cand[i] & 0xffffffffu] = 1;
 }
 
 inline uint64_t pack(uint32_t key, int index) { return ((uint64_t)key << 32) | (uint32_t)~(uint32_t)index; }
 
-// Eq. (4) for one theta over B trajectories of T rows of N scores, averaged over B.
-double objective(const float* scores, int B, int T, int N, int k, int p, const float theta[3]) {
+// Eq. (4) for one theta over B trajectories of T rows of N scores, averaged over B.  Block
+// i exists from row born[i] on (Section 4.1: its state starts there as level = its score,
+// trend = 0); A_phi ranks the blocks that exist at row phi, P_phi the predictions of the
+// blocks that had a state before it.  Rows phi >= 1 (those with a prediction) are averaged.
+double objective(const float* scores, int B, int T, int N, const int32_t* born, int k, int p,
+                 const float theta[3]) {
   const double alpha = theta[0], beta = theta[1], gamma = theta[2];
   std::vector<double> level(N), trend(N);
-  std::vector<uint64_t> pk(N), work;
-  std::vector<uint8_t> inA(N), inP(N);
+  std::vector<uint8_t> has(N), inA(N), inP(N);
+  std::vector<uint64_t> cand;
+  cand.reserve(N);
   double sum_b = 0.0;
   for (int b = 0; b < B; ++b) {
     const float* traj = scores + (size_t)b * T * N;
-    for (int i = 0; i < N; ++i) {  // step 0 initialises the state
-      level[i] = traj[i];
-      trend[i] = 0.0;
-    }
+    std::fill(has.begin(), has.end(), 0);
     double sum_t = 0.0;
     int rows = 0;
-    for (int phi = 1; phi < T; ++phi) {
+    for (int phi = 0; phi < T; ++phi) {
       const float* row = traj + (size_t)phi * N;
-      for (int i = 0; i < N; ++i) pk[i] = pack(key_of(level[i] + gamma * trend[i]), i);  // Eq. (2)
-      top_k(pk, p, work, inP);
-      for (int i = 0; i < N; ++i) pk[i] = pack(key_of(row[i]), i);
-      top_k(pk, k, work, inA);
-      double hit = 0.0, all = 0.0;
-      for (int i = 0; i < N; ++i) {
-        if (inA[i]) {
-          all += row[i];
-          if (inP[i]) hit += row[i];
+      if (phi >= 1) {
+        cand.clear();
+        for (int i = 0; i < N; ++i)
+          if (has[i]) cand.push_back(pack(key_of(level[i] + gamma * trend[i]), i));  // Eq. (2)
+        top_k(cand, p, inP);
+        cand.clear();
+        for (int i = 0; i < N; ++i)
+          if (born[i] <= phi) cand.push_back(pack(key_of(row[i]), i));
+        top_k(cand, k, inA);
+        double hit = 0.0, all = 0.0;
+        for (int i = 0; i < N; ++i) {
+          if (inA[i]) {
+            all += row[i];
+            if (inP[i]) hit += row[i];
+          }
+        }
+        sum_t += all != 0.0 ? hit / all : 0.0;
+        ++rows;
+        for (int i = 0; i < N; ++i) {  // Eq. (3): the trend reads the previous level
+          if (!has[i]) continue;
+          trend[i] = beta * (row[i] - level[i]) + (1.0 - beta) * trend[i];
+          level[i] = alpha * row[i] + (1.0 - alpha) * level[i];
         }
       }
-      sum_t += all != 0.0 ? hit / all : 0.0;
-      ++rows;
-      for (int i = 0; i < N; ++i) {  // Eq. (3): the trend reads the previous level
-        trend[i] = beta * (row[i] - level[i]) + (1.0 - beta) * trend[i];
-        level[i] = alpha * row[i] + (1.0 - alpha) * level[i];
+      for (int i = 0; i < N; ++i) {  // blocks that form at this row
+        if (!has[i] && born[i] <= phi) {
+          level[i] = row[i];
+          trend[i] = 0.0;
+          has[i] = 1;
+        }
       }
     }
     sum_b += rows ? sum_t / rows : 0.0;
@@ -85,9 +97,12 @@ double objective(const float* scores, int B, int T, int N, int k, int p, const f
 namespace prr {
 
 // Arguments were validated by the C ABI (prr_calibrate).
-void calibrate_grid(const float* scores, int n_traj, int n_rows, int n_blocks, int k_select, int p_select,
-                    const float* grid, int n_grid, int n_threads, float* best_theta, double* objective_out) {
+void calibrate_grid(const float* scores, int n_traj, int n_rows, int n_blocks, const int32_t* form_row, int k_select,
+                    int p_select, const float* grid, int n_grid, int n_threads, float* best_theta,
+                    double* objective_out) {
   const int p = p_select > 0 ? p_select : k_select;
+  std::vector<int32_t> born(n_blocks, 0);
+  if (form_row) born.assign(form_row, form_row + n_blocks);
   std::vector<double> obj(n_grid, 0.0);
   unsigned hw = std::thread::hardware_concurrency();
   int nt = n_threads > 0 ? n_threads : (int)(hw ? hw : 1);
@@ -95,7 +110,7 @@ void calibrate_grid(const float* scores, int n_traj, int n_rows, int n_blocks, i
   std::atomic<int> next(0);
   auto work = [&]() {
     for (int g = next++; g < n_grid; g = next++)
-      obj[g] = objective(scores, n_traj, n_rows, n_blocks, k_select, p, grid + 3 * g);
+      obj[g] = objective(scores, n_traj, n_rows, n_blocks, born.data(), k_select, p, grid + 3 * g);
   };
   std::vector<std::thread> pool;
   for (int i = 1; i < nt; ++i) pool.emplace_back(work);

@@ -20,6 +20,7 @@
 // the previous step's epoch or the whole new value, so no counter, flag or fence is
 // needed.  The caller passes a new epoch for every call on a workspace.  A select or
 // predict workgroup holds 16 keys per thread, so a fused step takes at most 8192 pages.
+#pragma once
 #include "prr_device.h"
 #include "prr_launch.h"
 #include "prr_select.h"
@@ -32,6 +33,7 @@ namespace {
 
 constexpr int kFT = 512;
 constexpr int kFW = kFT / kWave;
+static_assert(kFW == kFusedWaves, "waves per workgroup");
 constexpr int kFScorePages = kFusedScorePages;  // pages of one score workgroup
 constexpr int kFPagesPerWave = kFScorePages / 8;  // scored by each of its 8 waves
 constexpr int kFScoreIt = kFPagesPerWave / 4;     // 4 pages per 16-lane row group at a time
@@ -603,6 +605,13 @@ __device__ __forceinline__ void wave_attend(const FusedLaunch& a, int h, const u
     const float ls = sum_rows((p[0] + p[1]) + (p[2] + p[3]));
     st.l[k] = st.l[k] * alpha + ls;
     st.m[k] = mnew;
+    if (pg[k] * PS + PS > a.num_tokens) {
+      // a partial last page: the values of tokens at or past num_tokens are zeroed, not
+      // only weighted by 0 (0 x NaN or Inf from an unwritten cache tail would poison o)
+#pragma unroll
+      for (int tg = 0; tg < 4; ++tg)
+        if (tok0 + tg >= a.num_tokens) vf[f][tg] = u32x4_t{0, 0, 0, 0};
+    }
     if (tt > 0) {
 #pragma unroll
       for (int cb = 0; cb < 8; ++cb) {
@@ -1939,35 +1948,16 @@ __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
   if (b < H * a.group) role_merge<BF16>(a, ep, b / a.group, b % a.group, U.merge, U.bc);
 }
 
-template <typename K>
-hipError_t launch_k(K kernel, int grid, const FusedLaunch& a, hipStream_t stream) {
-  void* args[] = {const_cast<FusedLaunch*>(&a)};
-  return hipLaunchKernel(reinterpret_cast<const void*>(kernel), dim3(grid), dim3(kFT), args, 0, stream);
-}
-
 }  // namespace
 
-int fused_grid(const FusedLaunch& a) {
-  const int H = a.num_kv_heads;
-  int per = a.n_score + 1;
-  if (a.schedule != 0) per += 1;
-  if (a.schedule == 1) per += a.n_spec + a.n_late;
-  if (a.schedule != 2) per += a.n_miss + a.group;
-  return H * per;
-}
-
-hipError_t launch_fused(const FusedLaunch& a, bool bf16, int page_size, hipStream_t stream) {
-  const int grid = fused_grid(a);
-  const int npw = (a.chunk + kFW - 1) / kFW;
-  if (page_size == 16) {
-    if (npw <= 1)
-      return bf16 ? launch_k(fused_step_kernel<true, 16, 1>, grid, a, stream)
-                  : launch_k(fused_step_kernel<false, 16, 1>, grid, a, stream);
-    return bf16 ? launch_k(fused_step_kernel<true, 16, 2>, grid, a, stream)
-                : launch_k(fused_step_kernel<false, 16, 2>, grid, a, stream);
-  }
-  return bf16 ? launch_k(fused_step_kernel<true, 64, 1>, grid, a, stream)
-              : launch_k(fused_step_kernel<false, 64, 1>, grid, a, stream);
+// One instance of the fused kernel, launched on `grid` workgroups.  Instances are spread
+// over several translation units (explicit instantiations below each include of this
+// file), so that they compile in parallel.
+template <bool BF16, int PS, int NPW>
+hipError_t launch_fused_inst(int grid, const FusedLaunch& a, hipStream_t stream) {
+  void* args[] = {const_cast<FusedLaunch*>(&a)};
+  return hipLaunchKernel(reinterpret_cast<const void*>(fused_step_kernel<BF16, PS, NPW>), dim3(grid), dim3(kFT), args,
+                         0, stream);
 }
 
 }  // namespace prr

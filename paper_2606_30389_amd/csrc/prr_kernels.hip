@@ -733,6 +733,13 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
     const float ls = sum_rows((p[0] + p[1]) + (p[2] + p[3]));
     l_run = l_run * alpha + ls;
     m_run = mnew;
+    if (tok0[kk] + PS > c.num_tokens) {
+      // a partial last page: the values of tokens at or past num_tokens are zeroed, not
+      // only weighted by 0 (0 x NaN or Inf from an unwritten cache tail would poison o)
+#pragma unroll
+      for (int tg = 0; tg < 4; ++tg)
+        if (tok0[kk] + tt * 16 + 4 * j + tg >= c.num_tokens) vf[f][tg] = u32x4_t{0, 0, 0, 0};
+    }
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
 #pragma unroll

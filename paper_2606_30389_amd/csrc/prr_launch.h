@@ -141,13 +141,19 @@ struct FusedLaunch {
 
 constexpr int kFusedMaxPages = 8192;   // 16 keys per thread of a 512-thread select
 constexpr int kFusedScorePages = 128;   // pages per score workgroup of the fused step
+constexpr int kFusedWaves = 8;          // waves of a fused-step workgroup
+template <bool BF16, int PS, int NPW>
+hipError_t launch_fused_inst(int grid, const FusedLaunch& a, hipStream_t stream);
 hipError_t launch_fused(const FusedLaunch& a, bool bf16, int page_size, hipStream_t stream);
 int fused_grid(const FusedLaunch& a);
 
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 hipError_t launch_epoch_advance(uint32_t* epoch_dev, hipStream_t stream);
-void calibrate_grid(const float* scores, int n_traj, int n_rows, int n_blocks, int k_select, int p_select,
-                    const float* grid, int n_grid, int n_threads, float* best_theta, double* objective_out);
+void calibrate_grid(const float* scores, int n_traj, int n_rows, int n_blocks, const int32_t* form_row, int k_select,
+                    int p_select, const float* grid, int n_grid, int n_threads, float* best_theta,
+                    double* objective_out);
+float pick_delta(const int32_t* context, const float* delta, const float* select_us, const float* spec_us, int n_rows,
+                 int32_t query_context, int degree, float* select_est, float* spec_est);
 hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream);
 hipError_t launch_score_topk(const ScoreLaunch& a, hipStream_t stream);
 hipError_t launch_predict(const PredictLaunch& a, hipStream_t stream);

@@ -179,30 +179,11 @@ THETA_GRID = [(a, b, c) for a in (0.2, 0.4, 0.6, 0.8) for b in (0.1, 0.2, 0.3, 0
               for c in (0.0, 0.25, 0.5, 0.75)]
 
 
-def pick_delta(lut, context):
-    """Section 4.4: the largest speculation budget delta = |P| / |A| whose speculative
-    attention fits in the selection window at this context length.  `lut` rows are
-    {"context", "delta", "select_us", "spec_us"} from the offline sweep; latencies at an
-    unprofiled context are interpolated linearly in log2(context) between the two nearest
-    profiled contexts (clamped at the ends).  Returns 1.0 if no delta fits."""
-    import math
-    ctxs = sorted({r["context"] for r in lut})
-    if not ctxs:
-        return 1.0
-    x = math.log2(max(context, 1))
-    lo = max([c for c in ctxs if c <= context], default=ctxs[0])
-    hi = min([c for c in ctxs if c >= context], default=ctxs[-1])
-    w = 0.0 if hi == lo else (x - math.log2(lo)) / (math.log2(hi) - math.log2(lo))
-    best = 1.0
-    for d in sorted({r["delta"] for r in lut}):
-        rows = {r["context"]: r for r in lut if r["delta"] == d}
-        if lo not in rows or hi not in rows:
-            continue
-        sel = (1 - w) * rows[lo]["select_us"] + w * rows[hi]["select_us"]
-        spec = (1 - w) * rows[lo]["spec_us"] + w * rows[hi]["spec_us"]
-        if spec <= sel:
-            best = max(best, d)
-    return best
+def pick_delta(lut, context, degree=2):
+    """Section 4.4's speculation budget for this context length, decided by the library
+    (prr_pick_delta) from the profiled table `lut` (rows with "context", "delta",
+    "select_us", "spec_us").  Returns the chosen delta."""
+    return L.prr_pick_delta(lut, context, degree)[0]
 
 
 _epoch = [0]

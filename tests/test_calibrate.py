@@ -19,7 +19,7 @@ def _lib():
 
 def _trajectory(seed, rows, blocks, drift=0.15, growing=0):
     """Positive AR(1)-drifting scores; with `growing`, the last rows gain blocks one by one
-    (blocks not formed yet score 0)."""
+    (entries of blocks not formed yet hold junk that must never be read)."""
     rng = np.random.default_rng(seed)
     base = rng.gamma(2.0, 1.0, size=blocks)
     out = np.empty((rows, blocks), dtype=np.float32)
@@ -29,8 +29,14 @@ def _trajectory(seed, rows, blocks, drift=0.15, growing=0):
         out[r] = cur
         if growing:
             formed = blocks - growing + min(r, growing)
-            out[r, formed:] = 0.0
+            out[r, formed:] = 1e6
     return out
+
+
+def _form_rows(rows, blocks, growing):
+    """Row at which each block of a `growing` trajectory forms."""
+    return np.array([max(0, b - (blocks - growing)) if b >= blocks - growing else 0 for b in range(blocks)],
+                    dtype=np.int32)
 
 
 @pytest.mark.parametrize("seed,rows,blocks,k,p", [(1, 10, 96, 8, 0), (2, 14, 200, 16, 24), (3, 6, 40, 40, 0),
@@ -51,12 +57,34 @@ def test_calibrate_growing_blocks_and_threads():
     L = _lib()
     grid = np.asarray(O.THETA_GRID, dtype=np.float32)
     traj = _trajectory(7, 12, 150, growing=10)
-    b1, o1 = L.prr_calibrate(traj, 10, grid, n_threads=1)
-    b8, o8 = L.prr_calibrate(traj, 10, grid, n_threads=8)
+    fr = _form_rows(12, 150, 10)
+    b1, o1 = L.prr_calibrate(traj, 10, grid, n_threads=1, form_row=fr)
+    b8, o8 = L.prr_calibrate(traj, 10, grid, n_threads=8, form_row=fr)
     assert b1 == b8 and np.array_equal(o1, o8)
     t64 = traj.astype(np.float64)
-    ref = np.array([O.calibration_objective(t64, 10, tuple(float(x) for x in th)) for th in grid])
+    ref = np.array([O.calibration_objective(t64, 10, tuple(float(x) for x in th), None, fr) for th in grid])
     np.testing.assert_allclose(o1, ref, rtol=0, atol=1e-12)
+    assert int(np.argmax(ref)) == int(np.argmax(o1)) and b1 == tuple(float(x) for x in grid[int(np.argmax(ref))])
+
+
+def test_calibrate_formation_pins_natively():
+    """The library's calibration on the hand-worked trajectories that pin the oracle."""
+    from tests import oracle_pins as pins
+    L = _lib()
+    grid = [tuple(float(x) for x in t) for t in O.THETA_GRID]
+
+    def objective(traj, k, theta, p_select=None, form_row=None):
+        g = np.asarray([theta], dtype=np.float32)
+        return float(L.prr_calibrate(np.asarray(traj, np.float32), k, g, p_select=p_select or 0,
+                                     form_row=form_row)[1][0])
+
+    def calibrate(traj, k, grid_):
+        best, obj = L.prr_calibrate(np.asarray(traj, np.float32), k, np.asarray(grid_, np.float32))
+        return tuple(round(x, 6) for x in best), float(obj.max())
+
+    assert pins.check_calibrate_closed_form(objective, calibrate, grid)
+    assert pins.check_calibrate_all_tied(calibrate, grid)
+    assert pins.check_calibration_formation(objective, grid)
 
 
 def test_calibrate_invalid_arguments():
@@ -69,6 +97,8 @@ def test_calibrate_invalid_arguments():
         L.prr_calibrate(traj, 4, np.asarray([[0.0, 0.5, 0.0]], dtype=np.float32))  # alpha = 0
     with pytest.raises(L.PrrError):
         L.prr_calibrate(traj, -1, grid)
+    with pytest.raises(L.PrrError):
+        L.prr_calibrate(traj, 4, grid, form_row=np.full(16, -1, dtype=np.int32))
 
 
 def test_runtime_grid_is_the_papers():
@@ -81,20 +111,52 @@ def test_runtime_grid_is_the_papers():
 
 
 def test_pick_delta():
-    """The largest budget whose speculation fits in the selection window, interpolated in
-    log2(context) between profiled contexts."""
+    """Section 4.4 in the library: the largest delta whose speculation fits in the selection
+    window.  The profiled latencies are exact polynomials of x = log2(context) of degree
+    <= 2, so the degree-2 regression recovers them at unprofiled contexts and the pick
+    follows by hand: select(x) = 2 + x; delta 1 and 1.5 always fit (1 + x/2 and 1 + x);
+    delta 2 (0.25 (x - 14)^2 + 12) fits iff x^2 - 32 x + 236 <= 0, i.e. for x in
+    [16 - 2 sqrt(5), 16 + 2 sqrt(5)]."""
+    L = _lib()
+    rows = []
+    for ctx in (4096, 8192, 16384, 32768, 65536):
+        x = np.log2(ctx)
+        for d, spec in ((1.0, 1 + x / 2), (1.5, 1.0 + x), (2.0, 0.25 * (x - 14) ** 2 + 12)):
+            rows.append({"context": ctx, "delta": d, "select_us": 2 + x, "spec_us": spec})
+    lo, hi = 16 - 2 * np.sqrt(5), 16 + 2 * np.sqrt(5)
+    for ctx in (5000, 12000, 20000, 100000, 131072, 2 ** 20, 2 ** 22):
+        x = np.log2(ctx)
+        want = 2.0 if lo <= x <= hi else 1.5
+        d, se, sp = L.prr_pick_delta(rows, ctx, degree=2)
+        assert d == want, (ctx, d, want)
+        assert abs(se - (2 + x)) < 1e-3
+    # a profiled context uses its own row: make delta 2 fit only there
+    rows2 = [dict(r) for r in rows]
+    for r in rows2:
+        if r["delta"] == 2.0:
+            r["spec_us"] = 100.0 if r["context"] != 16384 else 1.0
+    assert L.prr_pick_delta(rows2, 16384)[0] == 2.0
+    assert L.prr_pick_delta(rows2, 16000)[0] == 1.5
+    # degree 0 averages: a constant fit
+    d0 = L.prr_pick_delta([{"context": 4096, "delta": 2.0, "select_us": 10.0, "spec_us": 9.0},
+                           {"context": 8192, "delta": 2.0, "select_us": 10.0, "spec_us": 12.0}], 6000, degree=0)
+    assert d0[0] == 1.0 and abs(d0[2] - 10.5) < 1e-5
+    # no table: delta 1; nothing fits: delta 1
+    assert L.prr_pick_delta([], 4096)[0] == 1.0
+    assert L.prr_pick_delta([{"context": 4096, "delta": 2.0, "select_us": 1.0, "spec_us": 5.0}], 4096)[0] == 1.0
+    with pytest.raises(L.PrrError):
+        L.prr_pick_delta(rows, 0)
+    with pytest.raises(L.PrrError):
+        L.prr_pick_delta(rows, 4096, degree=4)
+    with pytest.raises(L.PrrError):
+        L.prr_pick_delta([{"context": 4096, "delta": 0.5, "select_us": 1.0, "spec_us": 0.5}], 4096)
+
+
+def test_runtime_pick_delta_is_the_library_call():
     try:
         from paper_2606_30389_amd import runtime as R
     except ImportError as e:
         pytest.skip(f"libprr not built: {e}")
-    lut = []
-    for ctx, sel in ((4096, 10.0), (16384, 20.0)):
-        for d, spec in ((1.0, 5.0), (1.5, 9.0), (2.0, 12.0 if ctx == 4096 else 19.0)):
-            lut.append({"context": ctx, "delta": d, "select_us": sel, "spec_us": spec})
-    assert R.pick_delta(lut, 4096) == 1.5       # 12 > 10
-    assert R.pick_delta(lut, 16384) == 2.0      # 19 <= 20
-    assert R.pick_delta(lut, 8192) == 1.5       # midway: spec 15.5 > select 15
-    assert R.pick_delta(lut, 1024) == 1.5       # clamped to the smallest context
-    assert R.pick_delta([], 4096) == 1.0
-    lut_bad = [{"context": 4096, "delta": 2.0, "select_us": 1.0, "spec_us": 5.0}]
-    assert R.pick_delta(lut_bad, 4096) == 1.0
+    L = _lib()
+    lut = [{"context": c, "delta": d, "select_us": 10.0, "spec_us": 5.0 * d} for c in (4096, 65536) for d in (1.0, 2.0, 3.0)]
+    assert R.pick_delta(lut, 16384) == L.prr_pick_delta(lut, 16384)[0] == 2.0
