@@ -1698,6 +1698,11 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, uint32_t ep, int
   for (int r = 0; r < PRR_MAX_CAP_DEV / kFT; ++r)
     if (pe[r] >= 0 && pe[r] < n) atomicOr(&L.bitP[pe[r] >> 5], 1u << (pe[r] & 31));
   const FCand c = cand_load<false>(a, ep, h, 2, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  // More late pages than one list in LDS holds (after the candidate windows were reset):
+  // the list was not loaded.  The candidates of A are then at least as many, so the select
+  // workgroup takes its fallback over all scores and publishes a late count of 0, and the
+  // merge reads no late state.
+  if (c.total > kCandMax) return;
   const int cover = min(c.total, a.n_late * a.chunk);
   const int start = u * a.chunk;
   if (start >= cover) return;

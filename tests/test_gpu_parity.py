@@ -285,6 +285,53 @@ def test_speculate_repair_any_split(torch, name, npages, mode, split):
             assert mc[h] == len(mm) and wc[h] == len(ww)
 
 
+def _page_masses(q64, k64, pages, page_size, num_tokens, g):
+    """Per (query head, page): the page's softmax mass sum_t exp(q.k_t / sqrt(d)) (fp64)."""
+    out = np.zeros((q64.shape[0], len(pages)))
+    for i, p in enumerate(pages):
+        toks = O.page_tokens([p], page_size, num_tokens) - p * page_size
+        for j in range(q64.shape[0]):
+            out[j, i] = np.exp(k64[j // g, p, toks] @ q64[j] / np.sqrt(q64.shape[1])).sum()
+    return out
+
+
+@pytest.mark.parametrize("band", [(0.80, 0.875), (0.876, 0.95)], ids=["subtract", "reattend"])
+def test_repair_wasted_share_near_the_limit(torch, band):
+    """Exact-mode repair of a speculation chunk whose wasted pages carry a share of the
+    chunk's softmax mass just below the 7/8 limit for every query head (the wasted part is
+    subtracted, the largest cancellation allowed) and just above it for some head (the
+    chunk's pages of A are attended afresh).  The chunk is chosen on the CPU from the
+    oracle's per-page masses."""
+    cfg, pc, st, li = _setup("glm32k", 300)
+    _, qb = W.query_trajectory(cfg, 0, steps=1)
+    q64 = W.bits_to_f64(qb[1], cfg.dtype)
+    k64, v64 = li.k64(), li.v64()
+    g = pc.group
+    rng = np.random.default_rng(42)
+    pool = rng.choice(300, 120, replace=False)
+    masses = _page_masses(q64, k64, pool, 16, pc.num_tokens, g)
+    lo, hi = band
+    found = None
+    for _ in range(200000):
+        pick = rng.choice(len(pool), 8, replace=False)
+        wasted, clean = pick[:6], pick[6:]
+        tot = [masses[h * g:(h + 1) * g][:, pick].sum(axis=1) for h in range(2)]
+        share = [masses[h * g:(h + 1) * g][:, wasted].sum(axis=1) / tot[h] for h in range(2)]
+        top = max(float(share[0].max()), float(share[1].max()))
+        if lo <= top < hi:
+            found = (pool[wasted], pool[clean], top)
+            break
+    assert found is not None, "no chunk with the wanted wasted share"
+    wasted, clean, top = found
+    S.log(f"wasted share {top:.4f} in band {band}")
+    chunk = np.sort(np.concatenate([wasted, clean]))
+    extra = np.setdiff1d(pool, chunk)[:20]
+    A = [np.sort(np.concatenate([clean, extra])) for _ in range(2)]
+    P = [chunk for _ in range(2)]
+    o32, od, m, l = _run_spec_repair(torch, st, S.q_tensor(qb[1], pc), A, P, 0)
+    S.check_attention(o32, m, l, O.attend(q64, k64, v64, A, 16, pc.num_tokens), od, dtype=pc.dtype)
+
+
 @pytest.mark.parametrize("chunk", [1, 3, 8, 16])
 def test_chunk_sizes(torch, chunk):
     cfg, pc, st, li = _setup("glm32k", 500, chunk_pages=chunk)
@@ -316,14 +363,22 @@ def test_all_pages_is_dense_attention(torch):
     S.check_attention(S.to_np(st.out_o32), S.to_np(st.out_m), S.to_np(st.out_l), ref, S.to_np(st.out_o), dtype=pc.dtype)
 
 
+@pytest.mark.parametrize("poison", [False, True], ids=["clean-tail", "nan-tail"])
 @pytest.mark.parametrize("name", ["glm32k", "infllm128k"])
-def test_partial_last_page(torch, name):
+def test_partial_last_page(torch, name, poison):
+    """A partial last page; with `poison` the tokens past num_tokens hold NaN and Inf in K
+    and V (an unwritten cache tail), which must not reach the metadata or the output."""
     cfg = W.CONFIGS[name]
     npg = 100
     nt = npg * cfg.page_size - (5 if cfg.page_size == 16 else 37)
     pc = S.path_config(cfg, num_pages=npg, num_tokens=nt)
-    S.log(f"partial last page {name} tokens={nt}")
+    S.log(f"partial last page {name} tokens={nt} poison={poison}")
     st, li = S.make_layer(cfg, pc)
+    if poison:
+        valid = nt - (npg - 1) * cfg.page_size
+        st.v[:, npg - 1, valid:] = float("nan")
+        st.k[:, npg - 1, valid:] = float("inf")
+        st.k[:, npg - 1, valid::3] = float("nan")
     st.build_meta()
     _, qb = W.query_trajectory(cfg, 0, steps=1)
     q = S.q_tensor(qb[1], pc)
