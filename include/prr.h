@@ -150,6 +150,23 @@ prr_status prr_score_topk(const prr_dims* dims, const void* q, const void* meta,
                           float* scores, int32_t* selected, int32_t* selected_count, int32_t cap,
                           void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* prr_score_topk without a workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).
+ * The arguments and results are those of prr_score_topk.  Its only scratch, one arrival
+ * counter per KV head, is a static device array of PRR_STATIC_MAX_KV_HEADS words that
+ * each GPU holds until the process ends; the call uses the copy of the current device and
+ * clears it on `stream` (with a fill kernel) before the selection.  Every call on one GPU
+ * shares that array: calls that overlap on one GPU (on different streams, or from
+ * different threads) race and give undefined results.  No allocation, no
+ * synchronisation.  Errors: those of prr_score_topk; PRR_ERR_INVALID_ARG when
+ * num_kv_heads > PRR_STATIC_MAX_KV_HEADS; PRR_ERR_HIP when the array's device address
+ * cannot be looked up. */
+#define PRR_STATIC_MAX_KV_HEADS 256
+prr_status prr_score_topk_static(const prr_dims* dims, const void* q, const void* meta, int32_t num_pages,
+                                 int32_t k_select, const int32_t* forced, int32_t n_forced, int32_t forced_in_budget,
+                                 float* scores, int32_t* selected, int32_t* selected_count, int32_t cap,
+                                 hipStream_t stream);
+
 /* EMA predictor (Section 4.1, Eqs. (2)-(3)) and the predicted set P (Eq. (1)).
  *   ema_level, ema_trend  device [Hkv][max_pages] float32 in/out (level l and trend v)
  *   ema_init_bits         device [Hkv][ceil(max_pages/32)] uint32 in/out: bit p set once

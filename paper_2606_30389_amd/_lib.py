@@ -30,6 +30,7 @@ PRR_RECOMPUTE_ON_MISS = 2
 PRR_MAX_PAGES = 16384
 PRR_MAX_CAP = 1024
 PRR_MAX_FORCED = 64
+PRR_STATIC_MAX_KV_HEADS = 256
 
 PRR_SCHED_SERIAL = 0
 PRR_SCHED_TWO_STREAM = 1
@@ -43,7 +44,7 @@ EXPORTED = (
     "prr_status_string", "prr_last_error", "prr_workspace_size", "prr_workspace_init",
     "prr_spec_state_floats", "prr_build_page_meta", "prr_score_topk", "prr_predict",
     "prr_spec_attn", "prr_repair", "prr_merge_states", "prr_decode_step", "prr_calibrate",
-    "prr_epoch_advance", "prr_pick_delta",
+    "prr_epoch_advance", "prr_pick_delta", "prr_score_topk_static",
 )
 
 
@@ -98,6 +99,7 @@ _SIGS = {
     "prr_spec_state_floats": (_S, [_DIMS, _I, _I, ctypes.POINTER(_S), ctypes.POINTER(_S), ctypes.POINTER(_S)]),
     "prr_build_page_meta": (_I, [_DIMS, _P, _P, _I, _I, _I, _P, _P]),
     "prr_score_topk": (_I, [_DIMS, _P, _P, _I, _I, _P, _I, _I, _P, _P, _P, _I, _P, _S, _P]),
+    "prr_score_topk_static": (_I, [_DIMS, _P, _P, _I, _I, _P, _I, _I, _P, _P, _P, _I, _P]),
     "prr_predict": (_I, [_DIMS, _P, _P, _P, _P, _I, _F, _F, _F, _I, _P, _I, _I, _P, _P, _I, _P]),
     "prr_spec_attn": (_I, [_DIMS, _P, _P, _P, _P, _I, _P, _P, _I, _I, _P, _P, _P, _P, _P]),
     "prr_repair": (_I, [_DIMS, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _I, _I, _P, _P, _P, _P, _I,
@@ -185,6 +187,15 @@ def prr_score_topk(dims, q, meta, num_pages, k_select, forced, forced_in_budget,
                                ctypes.cast(farr, _P) if farr is not None else None, nf, int(bool(forced_in_budget)),
                                _ptr(scores), _ptr(selected), _ptr(selected_count), cap, _ptr(workspace), ws_bytes,
                                _stream(stream)))
+
+
+def prr_score_topk_static(dims, q, meta, num_pages, k_select, forced, forced_in_budget, scores, selected,
+                          selected_count, cap, stream=None):
+    farr, nf = _forced(forced)
+    _check(_lib.prr_score_topk_static(ctypes.byref(dims), _ptr(q), _ptr(meta), num_pages, k_select,
+                                      ctypes.cast(farr, _P) if farr is not None else None, nf,
+                                      int(bool(forced_in_budget)), _ptr(scores), _ptr(selected), _ptr(selected_count),
+                                      cap, _stream(stream)))
 
 
 def prr_predict(dims, ema_level, ema_trend, ema_init_bits, scores, num_pages, alpha, beta, gamma, p_select, forced,

@@ -145,6 +145,56 @@ void budget(int k_select, int n_forced, int forced_in_budget, int num_pages, int
 
 }  // namespace
 
+namespace prr {
+
+prr_status api_fail(prr_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+prr_status api_ok() { return ok(); }
+
+prr_status prepare_score(const prr_dims* dims, const void* q, const void* meta, int32_t num_pages, int32_t k_select,
+                         const int32_t* forced, int32_t n_forced, int32_t forced_in_budget, float* scores,
+                         int32_t* selected, int32_t* selected_count, int32_t cap, ScoreLaunch& a) {
+  PRR_TRY(check_dims(dims));
+  PRR_TRY(check_ptr(q, "q", 16));
+  PRR_TRY(check_ptr(meta, "meta", 16));
+  PRR_TRY(check_ptr(scores, "scores", 4));
+  PRR_TRY(check_ptr(selected, "selected", 4));
+  PRR_TRY(check_ptr(selected_count, "selected_count", 4));
+  if (num_pages < 1 || num_pages > PRR_MAX_PAGES || num_pages > dims->max_pages)
+    return fail(PRR_ERR_INVALID_ARG, "num_pages %d outside [1, min(max_pages, %d)]", num_pages, PRR_MAX_PAGES);
+  if (k_select < 0) return fail(PRR_ERR_INVALID_ARG, "k_select %d < 0", k_select);
+  PRR_TRY(check_forced(forced, n_forced, num_pages));
+  if (cap < 1 || cap > PRR_MAX_CAP) return fail(PRR_ERR_INVALID_ARG, "cap %d outside [1, %d]", cap, PRR_MAX_CAP);
+  int total, kextra;
+  budget(k_select, n_forced, forced_in_budget, num_pages, total, kextra);
+  if (total > cap) return fail(PRR_ERR_INVALID_ARG, "|A| = %d exceeds cap %d", total, cap);
+  memset(&a, 0, sizeof(a));
+  a.q = q;
+  a.meta = meta;
+  a.scores = scores;
+  a.selected = selected;
+  a.selected_count = selected_count;
+  a.num_kv_heads = dims->num_kv_heads;
+  a.group = dims->num_q_heads / dims->num_kv_heads;
+  a.max_pages = dims->max_pages;
+  a.num_pages = num_pages;
+  a.kextra = kextra;
+  a.cap = cap;
+  a.n_forced = n_forced;
+  a.bf16 = dims->dtype == PRR_BF16;
+  a.meta_mean = dims->meta_kind == PRR_META_MEAN;
+  for (int i = 0; i < n_forced; ++i) a.forced[i] = forced[i];
+  return ok();
+}
+
+}  // namespace prr
+
 extern "C" {
 
 const char* prr_status_string(prr_status s) {
@@ -220,42 +270,14 @@ prr_status prr_score_topk(const prr_dims* dims, const void* q, const void* meta,
                           const int32_t* forced, int32_t n_forced, int32_t forced_in_budget, float* scores,
                           int32_t* selected, int32_t* selected_count, int32_t cap, void* workspace, size_t ws_bytes,
                           hipStream_t stream) {
-  PRR_TRY(check_dims(dims));
-  PRR_TRY(check_ptr(q, "q", 16));
-  PRR_TRY(check_ptr(meta, "meta", 16));
-  PRR_TRY(check_ptr(scores, "scores", 4));
-  PRR_TRY(check_ptr(selected, "selected", 4));
-  PRR_TRY(check_ptr(selected_count, "selected_count", 4));
-  if (num_pages < 1 || num_pages > PRR_MAX_PAGES || num_pages > dims->max_pages)
-    return fail(PRR_ERR_INVALID_ARG, "num_pages %d outside [1, min(max_pages, %d)]", num_pages, PRR_MAX_PAGES);
-  if (k_select < 0) return fail(PRR_ERR_INVALID_ARG, "k_select %d < 0", k_select);
-  PRR_TRY(check_forced(forced, n_forced, num_pages));
-  if (cap < 1 || cap > PRR_MAX_CAP) return fail(PRR_ERR_INVALID_ARG, "cap %d outside [1, %d]", cap, PRR_MAX_CAP);
-  int total, kextra;
-  budget(k_select, n_forced, forced_in_budget, num_pages, total, kextra);
-  if (total > cap) return fail(PRR_ERR_INVALID_ARG, "|A| = %d exceeds cap %d", total, cap);
+  prr::ScoreLaunch a;
+  PRR_TRY(prr::prepare_score(dims, q, meta, num_pages, k_select, forced, n_forced, forced_in_budget, scores, selected,
+                             selected_count, cap, a));
   PRR_TRY(check_ptr(workspace, "workspace", 256));
   WsLayout L;
   if (!ws_layout(dims, cap, 1, L) || ws_bytes < L.rep_cnt)
     return fail(PRR_ERR_WORKSPACE, "workspace of %zu bytes too small", ws_bytes);
-  prr::ScoreLaunch a;
-  memset(&a, 0, sizeof(a));
-  a.q = q;
-  a.meta = meta;
-  a.scores = scores;
-  a.selected = selected;
-  a.selected_count = selected_count;
   a.counters = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + L.sel_cnt);
-  a.num_kv_heads = dims->num_kv_heads;
-  a.group = dims->num_q_heads / dims->num_kv_heads;
-  a.max_pages = dims->max_pages;
-  a.num_pages = num_pages;
-  a.kextra = kextra;
-  a.cap = cap;
-  a.n_forced = n_forced;
-  a.bf16 = dims->dtype == PRR_BF16;
-  a.meta_mean = dims->meta_kind == PRR_META_MEAN;
-  for (int i = 0; i < n_forced; ++i) a.forced[i] = forced[i];
   return hip_status(prr::launch_score_topk(a, stream), "score_topk launch");
 }
 

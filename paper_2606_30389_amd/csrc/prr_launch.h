@@ -147,6 +147,15 @@ hipError_t launch_fused_inst(int grid, const FusedLaunch& a, hipStream_t stream)
 hipError_t launch_fused(const FusedLaunch& a, bool bf16, int page_size, hipStream_t stream);
 int fused_grid(const FusedLaunch& a);
 
+// The argument checks of prr_score_topk (everything but the workspace), filling the launch
+// descriptor; shared with the entry point that allocates nothing.  Errors are recorded
+// for prr_last_error.
+prr_status prepare_score(const prr_dims* dims, const void* q, const void* meta, int32_t num_pages, int32_t k_select,
+                         const int32_t* forced, int32_t n_forced, int32_t forced_in_budget, float* scores,
+                         int32_t* selected, int32_t* selected_count, int32_t cap, ScoreLaunch& a);
+prr_status api_fail(prr_status st, const char* fmt, ...);
+prr_status api_ok();
+
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 hipError_t launch_epoch_advance(uint32_t* epoch_dev, hipStream_t stream);
 void calibrate_grid(const float* scores, int n_traj, int n_rows, int n_blocks, const int32_t* form_row, int k_select,
