@@ -266,6 +266,9 @@ def main():
     ap.add_argument("--ablation", action="store_true",
                     help="also time the ablation stages S1 (reuse the previous top-K, recompute on a miss), "
                          "S2 (reuse + repair) and S3 (EMA + repair) with the fused PRR schedule")
+    ap.add_argument("--phases", type=int, default=0, metavar="TOKENS",
+                    help="also record the fused launches' phase timestamps over TOKENS tokens (medians, us from start)")
+    ap.add_argument("--phases-raw", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--chunk", type=int, default=None, help="pages per speculation chunk (default 8, 4 for 64-token pages)")
     ap.add_argument("--delta", type=float, default=1.0, help="|P| / |A| (speculation budget)")
     ap.add_argument("--schedules", default="fused_prr,fused_prr_late,fused_serial,fused_prr_late_graph,two_stream,serial")
@@ -308,7 +311,7 @@ def main():
                 "serial": L.PRR_SCHED_SERIAL, "fused_prr_late_graph": L.PRR_SCHED_FUSED_PRR}
     n_abl = (3 if args.ablation else 0) + (2 if args.calibrate > 1 else 0)
     total_tokens = 2 + max(2, args.warmup) + 2 * (len(schedules) + n_abl) * (args.steps + 2) + \
-        n_abl * (1 + max(2, args.warmup)) + args.kernel_reps + 8
+        n_abl * (1 + max(2, args.warmup)) + args.kernel_reps + 2 * args.phases + 8
     t0 = time.time()
     layers = [None] * n_layers
 
@@ -465,6 +468,47 @@ def main():
         for st in layers:
             st.init_bits.zero_()
         run(1, L.PRR_SCHED_FUSED_PREFILL)
+    phases = None
+    if args.phases > 0:
+        # per-layer phase timestamps of the fused launches (device clock, 100 MHz), in us
+        # from the first workgroup's start; medians over the tokens and layers
+        names = ["scores", "candidates_stored", "candidates_gathered", "threshold", "missed_count", "spec_state",
+                 "late_state", "miss_state", "merge_done", "select_done", "predict_done", "end", "attended",
+                 "late_list"]
+        stamps = torch.zeros(n_layers, 16, 1024, dtype=torch.int64, device=dev)
+        phases = {}
+        for label, sched, late, stk in (("fused_prr_late", L.PRR_SCHED_FUSED_PRR, 1, stack),
+                                        ("fused_serial", L.PRR_SCHED_FUSED_SERIAL, 0, stack_serial)):
+            cur[0] = stk
+            stk.params.late_spec = late
+            stk.params.phase_stamps = stamps.data_ptr()
+            rows = []
+            for _ in range(args.phases):
+                stamps.zero_()
+                torch.cuda.synchronize()
+                run(1, sched)
+                torch.cuda.synchronize()
+                st_np = stamps.cpu().numpy()
+                for l in range(n_layers):
+                    started = st_np[l, 0][st_np[l, 0] > 0]
+                    t0 = started.min()
+                    row = []
+                    for i in range(len(names)):
+                        v = st_np[l, i + 1][st_np[l, i + 1] > 0]
+                        row.append(((np.median(v) - t0) / 100.0, (v.max() - t0) / 100.0) if v.size else (np.nan, np.nan))
+                    rows.append(row)
+            stk.params.phase_stamps = None
+            if args.phases_raw:
+                raw = stamps.cpu().numpy()[0]
+                t0 = raw[0][raw[0] > 0].min()
+                phases[label + "_raw_layer0"] = [[int((x - t0) // 10) if x > 0 else -1 for x in raw[k][:400]]
+                                                 for k in range(15)]
+            arr = np.asarray(rows, dtype=np.float64)  # [launch][phase][median over workgroups, last]
+            phases[label] = {n: ([round(float(np.nanmedian(arr[:, i, j])), 2) for j in range(2)]
+                                 if np.isfinite(arr[:, i, 1]).any() else None)
+                             for i, n in enumerate(names)}
+        cur[0] = stack
+        stack.params.late_spec = 0
     flags = [int(st.workspace[:1].cpu()[0]) for st in layers]
     if any(flags):
         print(json.dumps({"error": f"device error flags {flags}"}), flush=True)
@@ -537,6 +581,7 @@ def main():
         "kernel_us": {k: round(v, 2) for k, v in ktimes.items()},
         "ablation": ablation,
         "calibration": calibration,
+        "phases_us": phases,
         "roofline": roofline,
     }
     if args.copy_calibration_mib > 0:

@@ -287,6 +287,18 @@ typedef struct {
                                   scores exist, over the pages just above the selection threshold
                                   that P missed (the threshold is learned across steps); the result
                                   is still attention over exactly A (or P u A) */
+  uint64_t* phase_stamps;      /* fused schedules, or NULL: device [n_layers][16][1024] zeroed by the
+                                  caller; entry [l][k][w] receives the device real-time clock
+                                  (100 MHz, s_memrealtime) when workgroup w of layer l's launch
+                                  reached phase k (0 = never): 0 start; 1 scores computed; 2
+                                  candidate lists stored; 3 candidates gathered; 4 threshold
+                                  published; 5 missed count published; 6, 7, 8 a speculation,
+                                  late or missed-page state published; 9 an output row written;
+                                  10 select done; 11 next prediction written; 12 end; 13 an
+                                  attending workgroup's page states computed; 14 a late
+                                  workgroup holds its list.  One
+                                  plain store per entry.  Grids above 1024 workgroups give
+                                  PRR_ERR_UNSUPPORTED. */
 } prr_step_params;
 
 #define PRR_SCHED_SERIAL 0     /* per layer: select, then attend every page of A (one stream) */

@@ -78,7 +78,7 @@ class prr_step_params(ctypes.Structure):
                                                "chunk_pages", "mode", "forced_in_budget", "n_forced")] + [
         ("forced", ctypes.POINTER(ctypes.c_int32)), ("alpha", ctypes.c_float), ("beta", ctypes.c_float),
         ("gamma", ctypes.c_float), ("epoch", ctypes.c_uint32), ("epoch_dev", ctypes.c_void_p),
-        ("late_spec", ctypes.c_int32)]
+        ("late_spec", ctypes.c_int32), ("phase_stamps", ctypes.c_void_p)]
 
 
 if not os.path.exists(LIB_PATH):

@@ -516,7 +516,7 @@ prr_status prr_merge_states(int32_t n_states, int32_t rows, int32_t d, const flo
 // One layer of a fused schedule: every argument checked as by the individual entry
 // points, then one launch.
 static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, const prr_layer_io& y, int parity,
-                              int schedule, hipStream_t stream) {
+                              int schedule, hipStream_t stream, int layer) {
   const bool prr = schedule == PRR_SCHED_FUSED_PRR, prefill = schedule == PRR_SCHED_FUSED_PREFILL;
   PRR_TRY(check_ptr(y.q, "q", 16));
   PRR_TRY(check_ptr(y.meta, "meta", 16));
@@ -625,6 +625,9 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
     a.pbits_nxt = pb + (size_t)(1 - parity) * nwp;
   }
   a.flags = reinterpret_cast<uint32_t*>(ws + L.flags);
+  a.stamps = sp->phase_stamps ? reinterpret_cast<unsigned long long*>(sp->phase_stamps) +
+                                    (size_t)layer * prr::kStampSlots * prr::kStampMaxWorkgroups
+                              : nullptr;
   a.alpha = sp->alpha;
   a.beta = sp->beta;
   a.gamma = sp->gamma;
@@ -650,6 +653,9 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.n_forced = sp->n_forced;
   a.meta_mean = dims->meta_kind == PRR_META_MEAN;
   for (int i = 0; i < sp->n_forced; ++i) a.forced[i] = sp->forced[i];
+  if (a.stamps && prr::fused_grid(a) > prr::kStampMaxWorkgroups)
+    return fail(PRR_ERR_UNSUPPORTED, "phase_stamps record at most %d workgroups (grid %d)", prr::kStampMaxWorkgroups,
+                prr::fused_grid(a));
   return hip_status(prr::launch_fused(a, dims->dtype == PRR_BF16, dims->page_size, stream), "fused step launch");
 }
 
@@ -663,7 +669,8 @@ prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* sp, cons
   if (schedule < PRR_SCHED_SERIAL || schedule > PRR_SCHED_FUSED_PREFILL)
     return fail(PRR_ERR_INVALID_ARG, "schedule %d", schedule);
   if (schedule >= PRR_SCHED_FUSED_SERIAL) {
-    for (int l = 0; l < n_layers; ++l) PRR_TRY(fused_layer(dims, sp, layers[l], parity, schedule, stream));
+    if (sp->phase_stamps && !aligned(sp->phase_stamps, 8)) return fail(PRR_ERR_INVALID_ARG, "phase_stamps misaligned");
+    for (int l = 0; l < n_layers; ++l) PRR_TRY(fused_layer(dims, sp, layers[l], parity, schedule, stream, l));
     return ok();
   }
   if (schedule == PRR_SCHED_TWO_STREAM && !events) return fail(PRR_ERR_INVALID_ARG, "events is NULL");

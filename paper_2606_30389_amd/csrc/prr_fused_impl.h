@@ -78,6 +78,13 @@ __device__ __forceinline__ uint32_t wait_tag(const uint64_t* p, uint32_t epoch, 
   return tagged(get_tag(p), p, epoch, flags);
 }
 
+// Phase timestamp (called by one thread): the device clock when this workgroup reached
+// phase `slot`, one plain store to an entry of its own (only when the caller asked for
+// timestamps; workgroups never share an entry, so recording adds no contention).
+__device__ __forceinline__ void stamp(const FusedLaunch& a, int slot) {
+  if (a.stamps) a.stamps[(size_t)slot * kStampMaxWorkgroups + blockIdx.x] = __builtin_amdgcn_s_memrealtime();
+}
+
 // A value that many workgroups wait for (the threshold, the missed and late counts) is
 // stored in kRep copies 256 bytes apart, and each waiting workgroup polls one of them, so
 // that the polls spread over memory channels instead of queueing on one line.  Record of
@@ -91,6 +98,18 @@ __device__ __forceinline__ uint64_t* rep_at(uint64_t* base, int h, int c) {
 __device__ __forceinline__ void put_rep(uint64_t* base, int h, int k, uint32_t v, uint32_t epoch) {
 #pragma unroll
   for (int c = 0; c < kRep; ++c) put_tag(rep_at(base, h, c) + k, v, epoch);
+}
+
+// The threshold record of KV head h (words 0: T, 1: mode | tie cut << 2) and the missed
+// count, published in every copy (one thread).
+__device__ __forceinline__ void publish_thr(const FusedLaunch& a, int h, uint32_t T, uint32_t me, uint32_t epoch) {
+  put_rep(a.t_thr, h, 0, T, epoch);
+  put_rep(a.t_thr, h, 1, me, epoch);
+  stamp(a, kStampThreshold);
+}
+__device__ __forceinline__ void publish_mcnt(const FusedLaunch& a, int h, uint32_t v, uint32_t epoch) {
+  put_rep(a.t_mcnt, h, 0, v, epoch);
+  stamp(a, kStampMissed);
 }
 
 // ------------------------------------------------------------------------ LDS
@@ -309,6 +328,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     if (cg == 0) S.sc[p - pbase] = v;
   }
   __syncthreads();
+  if (t == 0) stamp(a, kStampScores);
   if (w != 0) return;
   const float qn = wave_sum(fabsf(S.qbar[lane]) + fabsf(S.qbar[lane + 64]));
   const float qe = qn_ema(a, qn, qe0);
@@ -382,6 +402,10 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
     nfa += __popcll(mfa);
   }
   if (lane == 0) put_tag(ck_a - 1, (uint32_t)na | ((uint32_t)nfa << 16), ep);
+  if (a.stamps) {
+    stores_complete();
+    if (lane == 0) stamp(a, kStampCandidates);
+  }
   // The K and V of the first late pages, one word per 64-byte line, read now: the late
   // workgroups load them about two microseconds later and then find them in the
   // memory-side cache.  The words only feed a check at the end of this role.
@@ -693,7 +717,8 @@ __device__ __forceinline__ void fold_write(WaveStates<NPW>& st, uint32_t keep, F
 
 // The states of the waves in `wmask` (uniform) combined per row and published (the
 // states are in LDS, behind a barrier).
-__device__ __forceinline__ void combine_publish(const PubDst& d, uint32_t ep, uint32_t wmask, FAttnLds& L) {
+__device__ __forceinline__ void combine_publish(const FusedLaunch& a, int slot, const PubDst& d, uint32_t ep,
+                                                uint32_t wmask, FAttnLds& L) {
   const float kNegInf = -__builtin_inff();
   const int t = threadIdx.x, lane = lane_id();
   const int hh = t >> 5, ci = t & 31;  // row; columns 2ci, 2ci + 1, 64 + 2ci, 65 + 2ci
@@ -749,16 +774,17 @@ __device__ __forceinline__ void combine_publish(const PubDst& d, uint32_t ep, ui
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (t < 2 * G) put_tag(d.pml + t, L.ml[t], ep);
+  if (t == 0) stamp(a, slot);
 }
 
 // Fold the kept page states of every wave (keep: wave-uniform bit mask) and publish the
 // workgroup's state.
 template <int NPW>
-__device__ __forceinline__ void fold_publish(const PubDst& d, uint32_t ep, WaveStates<NPW>& st, uint32_t keep,
-                                             FAttnLds& L) {
+__device__ __forceinline__ void fold_publish(const FusedLaunch& a, int slot, const PubDst& d, uint32_t ep,
+                                             WaveStates<NPW>& st, uint32_t keep, FAttnLds& L) {
   fold_write<NPW>(st, keep, L);
   __syncthreads();
-  combine_publish(d, ep, 0xffu, L);
+  combine_publish(a, slot, d, ep, 0xffu, L);
 }
 
 __device__ __forceinline__ bool page_forced(const FusedLaunch& a, int p) {
@@ -1042,15 +1068,13 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
   const SelThreshold th = sel2_threshold<kFT, J>(key, cand, a.kextra_a, L.sel);
   const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
   if (prr && early && t == 0) {
-    put_rep(a.t_thr, h, 0, th.T, ep);
-    put_rep(a.t_thr, h, 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
+    publish_thr(a, h, th.T, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
   }
   const uint64_t inA = sel2_membership<kFT, J>(key, page, cand, force, th, &L.eq_cut, L.sel);
   if (prr && !early) {
     __syncthreads();
     if (t == 0) {
-      put_rep(a.t_thr, h, 0, th.T, ep);
-      put_rep(a.t_thr, h, 1, (uint32_t)th.mode | ((uint32_t)L.eq_cut << 2), ep);
+      publish_thr(a, h, th.T, (uint32_t)th.mode | ((uint32_t)L.eq_cut << 2), ep);
     }
   }
 
@@ -1092,11 +1116,11 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
   const int nM = min(sel2_list<kFT, J>(inM, page, L.mlist, a.cap, L.sel), a.cap);
   __syncthreads();
   if (nM == 0) {
-    if (t == 0) put_rep(a.t_mcnt, h, 0, mflags, ep);
+    if (t == 0) publish_mcnt(a, h, mflags, ep);
   } else if (nM > kFW) {
     uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
     for (int i = t; i < nM; i += kFT) put_tag(&ml[i], (uint32_t)L.mlist[i], ep);
-    if (t == 0) put_rep(a.t_mcnt, h, 0, (uint32_t)nM | mflags, ep);
+    if (t == 0) publish_mcnt(a, h, (uint32_t)nM | mflags, ep);
   }
   // the selected list (an output) and the counts
   int32_t* sel = a.selected + (size_t)h * a.cap;
@@ -1115,7 +1139,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
   }
   if (nM > 0 && nM <= kFW) {
     // few enough to attend here: one page per wave, published as the first miss slot
-    if (t == 0) put_rep(a.t_mcnt, h, 0, (uint32_t)nM | kSelfMiss | mflags, ep);
+    if (t == 0) publish_mcnt(a, h, (uint32_t)nM | kSelfMiss | mflags, ep);
     int pg[1];
     pg[0] = __builtin_amdgcn_readfirstlane(w < nM ? L.mlist[w] : -1);
     __syncthreads();  // the list is read before the attention reuses the LDS
@@ -1123,7 +1147,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
     load_q(a, h, qf, U.qs);
     WaveStates<1> st;
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
-    fold_publish<1>(pub_dst(a, h, a.n_spec), ep, st, 1u, U.attn);
+    fold_publish<1>(a, kStampMiss, pub_dst(a, h, a.n_spec), ep, st, 1u, U.attn);
   }
   update_window<J>(a, a.win + 4 * h, qn, key, cand, (5 * a.kextra_a) / 2, keep_window, U.sel.sel);
   if (a.late) update_window<J>(a, a.win + 4 * h + 2, qn, key, cand, kLateRank(a.kextra_a), true, U.sel.sel);
@@ -1176,8 +1200,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
     if (prr && !early) {
       eq_cut = __builtin_amdgcn_readfirstlane(wave_umin((uint32_t)eq_cut));
       if (lane == 0) {
-        put_rep(a.t_thr, h, 0, th.T, ep);
-        put_rep(a.t_thr, h, 1, (uint32_t)th.mode | ((uint32_t)eq_cut << 2), ep);
+        publish_thr(a, h, th.T, (uint32_t)th.mode | ((uint32_t)eq_cut << 2), ep);
       }
     }
     // pages of late speculation: flagged, within the late capacity, never in P^t
@@ -1217,7 +1240,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
       }
       if (lane == 0) {
         const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
-        put_rep(a.t_mcnt, h, 0, (uint32_t)nM | mflags | self, ep);
+        publish_mcnt(a, h, (uint32_t)nM | mflags | self, ep);
         L.cnt[0][0] = nM;
       }
     }
@@ -1255,7 +1278,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
     load_q(a, h, qf, U.qs);
     WaveStates<1> st;
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
-    fold_publish<1>(pub_dst(a, h, a.n_spec), ep, st, 1u, U.attn);
+    fold_publish<1>(a, kStampMiss, pub_dst(a, h, a.n_spec), ep, st, 1u, U.attn);
   }
 }
 
@@ -1320,7 +1343,7 @@ __device__ __forceinline__ int miss_block(const FusedLaunch& a, uint32_t ep, int
   }
   if (t == 0) {
     const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
-    put_rep(a.t_mcnt, h, 0, (uint32_t)nM | (drop ? kDropSpec : 0u) | self, ep);
+    publish_mcnt(a, h, (uint32_t)nM | (drop ? kDropSpec : 0u) | self, ep);
     if (a.late) put_rep(a.t_lcnt, h, 0, (uint32_t)min(l0 + (tot_l >> 16), capl), ep);
     L.cnt[0][0] = nM;
   }
@@ -1375,6 +1398,7 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, uint32_t ep, i
   if (t == 0) L.npv = nv;
   const float qn = qbar_finish(a, qv, L.qb);
   const FCand c = cand_load<true>(a, ep, h, 0, L.off, L.tot, L.ck, L.cpg);  // (barriers inside)
+  if (t == 0) stamp(a, kStampGathered);
   if (a.kextra_a <= c.total - c.nforced && c.total <= kCandWave) {
     // the threshold by the whole workgroup straight from the list (two keys per thread),
     // published at once when no tie at T needs cutting; the one-wave pass that follows
@@ -1390,8 +1414,7 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, uint32_t ep, i
     const SelThreshold th = bsel_threshold<kFT>(k2, c2, a.kextra_a, L.bsel);
     const bool early = th.mode != 2 || th.need_eq >= th.eq_total;
     if (a.schedule == 1 && t == 0 && early) {
-      put_rep(a.t_thr, h, 0, th.T, ep);
-      put_rep(a.t_thr, h, 1, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
+      publish_thr(a, h, th.T, (uint32_t)th.mode | ((uint32_t)kEqAll << 2), ep);
     }
     const int nM = early ? miss_block(a, ep, h, c.total, th, k2, L) : -1;
     select_wave<BF16, PS>(a, ep, h, c.total, qn, th, nM, U);
@@ -1413,6 +1436,7 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, uint32_t ep, i
     for (int j = 0; j < 16; ++j) key[j] = score_key(__uint_as_float(key[j]));
     select_finish<BF16, PS, 16>(a, ep, h, key, page, cand, force, 0ull, false, qn, U);
   }
+  if (t == 0) stamp(a, kStampSelectDone);
 }
 
 // ------------------------------------------------------------------------ predict
@@ -1542,6 +1566,7 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, uint32_t ep, 
     full_gather<16>(a, ep, a.t_pkey + (size_t)h * a.max_pages, L.forceb, key, page, cand, force);
     predict_finish<16>(a, ep, h, key, page, cand, force, false, qe, L);
   }
+  if (t == 0) stamp(a, kStampPredictDone);
 }
 
 // ------------------------------------------------------------------------ spec / miss
@@ -1602,8 +1627,8 @@ __device__ __forceinline__ uint32_t keep_in_A(const FusedLaunch& a, uint32_t ep,
 // One page per wave: the page states go to LDS before A is known; once the threshold is
 // published, wave 0 decides for the eight pages which are in A (so one barrier follows
 // the threshold instead of two), and the kept states are combined and published.
-__device__ __forceinline__ void keep_fold_publish(const FusedLaunch& a, uint32_t ep, int h, int pg, WaveStates<1>& st,
-                                                  const PubDst& pd, FAttnLds& L) {
+__device__ __forceinline__ void keep_fold_publish(const FusedLaunch& a, int slot, uint32_t ep, int h, int pg,
+                                                  WaveStates<1>& st, const PubDst& pd, FAttnLds& L) {
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   fold_write<1>(st, 1u, L);
   if (lane == 0) L.kpg[w] = pg;
@@ -1632,7 +1657,7 @@ __device__ __forceinline__ void keep_fold_publish(const FusedLaunch& a, uint32_t
     if (lane == 0) L.kmask = m;
   }
   __syncthreads();
-  combine_publish(pd, ep, L.kmask, L);
+  combine_publish(a, slot, pd, ep, L.kmask, L);
 }
 
 template <bool BF16, int PS, int NPW>
@@ -1660,16 +1685,17 @@ __device__ __forceinline__ void role_spec(const FusedLaunch& a, uint32_t ep, int
   }
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
+  if (threadIdx.x == 0) stamp(a, kStampAttended);
   const PubDst pd = pub_dst(a, h, c);
   if constexpr (NPW == 1) {
     if (a.mode != PRR_KEEP_WASTED) {
-      keep_fold_publish(a, ep, h, pg[0], st, pd, U.attn);
+      keep_fold_publish(a, kStampSpec, ep, h, pg[0], st, pd, U.attn);
       return;
     }
   } else {
     if (a.mode != PRR_KEEP_WASTED) keep = keep_in_A<NPW>(a, ep, h, pg, keep, U.bc);
   }
-  fold_publish<NPW>(pd, ep, st, keep, U.attn);
+  fold_publish<NPW>(a, kStampSpec, pd, ep, st, keep, U.attn);
 }
 
 // Late speculation (PRR schedule): as soon as this step's scores exist, the pages just
@@ -1703,6 +1729,7 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, uint32_t ep, int
   // workgroup takes its fallback over all scores and publishes a late count of 0, and the
   // merge reads no late state.
   if (c.total > kCandMax) return;
+  if (t == 0) stamp(a, kStampLateList);
   const int cover = min(c.total, a.n_late * a.chunk);
   const int start = u * a.chunk;
   if (start >= cover) return;
@@ -1725,12 +1752,13 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, uint32_t ep, int
   __syncthreads();  // the list is read before the attention reuses the LDS
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st, ph);
+  if (t == 0) stamp(a, kStampAttended);
   const PubDst pd = pub_dst(a, h, a.n_spec + a.n_miss + u);
   if constexpr (NPW == 1) {
-    keep_fold_publish(a, ep, h, pg[0], st, pd, U.attn);
+    keep_fold_publish(a, kStampLate, ep, h, pg[0], st, pd, U.attn);
   } else {
     keep = keep_in_A<NPW>(a, ep, h, pg, keep, U.bc);
-    fold_publish<NPW>(pd, ep, st, keep, U.attn);
+    fold_publish<NPW>(a, kStampLate, pd, ep, st, keep, U.attn);
   }
 }
 
@@ -1785,7 +1813,7 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int
   }
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
-  fold_publish<NPW>(pub_dst(a, h, a.n_spec + u), ep, st, keep, U.attn);
+  fold_publish<NPW>(a, kStampMiss, pub_dst(a, h, a.n_spec + u), ep, st, keep, U.attn);
 }
 
 // ------------------------------------------------------------------------ merge
@@ -1899,6 +1927,7 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, uint32_t ep, in
     if (c == 0) {
       a.out_m[row] = Lsum > 0.0f ? M : kNegInf;
       a.out_l[row] = Lsum;
+      stamp(a, kStampMerge);
     }
   }
 #undef PRR_SLOT
@@ -1907,12 +1936,7 @@ __device__ __forceinline__ void role_merge(const FusedLaunch& a, uint32_t ep, in
 // ------------------------------------------------------------------------ kernel
 
 template <bool BF16, int PS, int NPW>
-__global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
-  __shared__ FLds U;
-  // the epoch of this call: the kernel argument, or a device word that the caller
-  // advances between replays of a captured launch (written by an earlier launch, so
-  // visible at this launch's start)
-  const uint32_t ep = a.epoch_dev ? *a.epoch_dev : a.epoch;
+__device__ __forceinline__ void fused_roles(const FusedLaunch& a, uint32_t ep, FLds& U) {
   int b = blockIdx.x;
   const int H = a.num_kv_heads;
   if (b < H * a.n_score) {
@@ -1951,6 +1975,18 @@ __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
   }
   b -= H * a.n_miss;
   if (b < H * a.group) role_merge<BF16>(a, ep, b / a.group, b % a.group, U.merge, U.bc);
+}
+
+template <bool BF16, int PS, int NPW>
+__global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
+  __shared__ FLds U;
+  if (threadIdx.x == 0) stamp(a, kStampStart);
+  // the epoch of this call: the kernel argument, or a device word that the caller
+  // advances between replays of a captured launch (written by an earlier launch, so
+  // visible at this launch's start)
+  const uint32_t ep = a.epoch_dev ? *a.epoch_dev : a.epoch;
+  fused_roles<BF16, PS, NPW>(a, ep, U);
+  if (threadIdx.x == 0) stamp(a, kStampEnd);
 }
 
 }  // namespace

@@ -125,6 +125,7 @@ struct FusedLaunch {
   const uint32_t* pbits_cur;  // [Hkv][ceil(max_pages/32)] bitmap of P^t (a hint for the late filter)
   uint32_t* pbits_nxt;        // bitmap of P^{t+1}
   uint32_t* flags;
+  unsigned long long* stamps;  // [kStampSlots][kStampMaxWorkgroups] phase timestamps (s_memrealtime), or NULL
   float alpha, beta, gamma;
   uint32_t epoch;
   const uint32_t* epoch_dev;  // if set, the epoch is read from here (graph replays)
@@ -138,6 +139,28 @@ struct FusedLaunch {
   bool meta_mean;
   int32_t forced[PRR_MAX_FORCED];
 };
+
+// Phase timestamps of a fused launch (prr_step_params.phase_stamps): entry
+// [slot][workgroup] holds the device clock when that workgroup reached the phase.
+enum StampSlot {
+  kStampStart = 0,
+  kStampScores,        // a score workgroup's scores computed
+  kStampCandidates,    // a score workgroup's candidate lists stored (complete)
+  kStampGathered,      // the select workgroup holds every candidate
+  kStampThreshold,     // T published
+  kStampMissed,        // missed count published
+  kStampSpec,          // a speculation state published
+  kStampLate,          // a late-speculation state published
+  kStampMiss,          // a missed-page state published
+  kStampMerge,         // a merge workgroup's output written
+  kStampSelectDone,    // the select workgroup's last work (next step's bounds) done
+  kStampPredictDone,   // P^{t+1} written
+  kStampEnd,           // a workgroup ends
+  kStampAttended,      // an attending workgroup's page states computed
+  kStampLateList,      // a late workgroup holds its list
+  kStampSlots = 16
+};
+constexpr int kStampMaxWorkgroups = 1024;
 
 constexpr int kFusedMaxPages = 8192;   // 16 keys per thread of a 512-thread select
 constexpr int kFusedScorePages = 128;   // pages per score workgroup of the fused step

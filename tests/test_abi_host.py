@@ -157,3 +157,33 @@ def test_last_error_is_thread_local(P):
     t.start()
     t.join()
     assert msg == [""] and "k_cache" in P.last_error()
+
+
+def test_fused_step_rejects_bad_stamps_and_epoch(P):
+    """Fused schedules: a misaligned phase-stamp buffer and the reserved epoch 0 are rejected
+    before any launch."""
+    d = P.make_dims(32, 2, 16, 100, P.PRR_BF16)
+    ws = P.prr_workspace_size(d, 16, 8)
+    y = P.prr_layer_io()
+    for name, _ in P.prr_layer_io._fields_:
+        if name in ("predicted", "predicted_count"):
+            getattr(y, name)[0] = FAKE
+            getattr(y, name)[1] = FAKE
+        elif name == "ws_bytes":
+            y.ws_bytes = ws
+        elif name in ("page_table", "out_o", "missed_count", "wasted_count"):
+            setattr(y, name, None)
+        else:
+            setattr(y, name, FAKE)
+    layers = (P.prr_layer_io * 1)(y)
+
+    def params(stamps=None, epoch=1):
+        p = P.prr_step_params()
+        p.num_tokens, p.num_pages, p.k_select, p.p_select, p.cap = 1600, 100, 16, 16, 16
+        p.chunk_pages, p.mode, p.forced_in_budget, p.n_forced = 8, 0, 1, 0
+        p.alpha, p.beta, p.gamma, p.epoch, p.late_spec = 0.5, 0.5, 0.0, epoch, 1
+        p.phase_stamps = stamps
+        return p
+
+    _expect(P, 1, P.prr_decode_step, d, params(stamps=FAKE + 4), layers, 0, P.PRR_SCHED_FUSED_PRR)
+    _expect(P, 1, P.prr_decode_step, d, params(epoch=0), layers, 0, P.PRR_SCHED_FUSED_PRR)
