@@ -620,8 +620,8 @@ __device__ __forceinline__ SelThreshold bsel_threshold(const uint32_t (&key)[2],
         const int nb = min(S.res[3], kWave);
         const uint32_t mk = lane < nb ? S.hist[lane] : 0u;
         int gt = 0, eq = 0;
-        for (int j = 0; j < nb; ++j) {
-          const uint32_t o = S.hist[j];
+        for (int j = 0; j < nb; ++j) {  // (the keys from registers: no LDS round trip per key)
+          const uint32_t o = (uint32_t)__builtin_amdgcn_readlane((int)mk, j);
           gt += o > mk ? 1 : 0;
           eq += o == mk ? 1 : 0;
         }
