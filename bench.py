@@ -96,10 +96,35 @@ def load_traffic(kernel):
     return t.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(cfg, budget_s):
+def host_info():
+    """The host the CPU baseline runs on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        affinity = os.cpu_count()
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [{"api": i.get("internal_api"), "threads": i.get("num_threads")} for i in threadpool_info()]
+    except ImportError:  # pragma: no cover
+        pass
+    return {"cpu_model": model, "cpu_count": os.cpu_count(), "affinity": affinity, "blas": blas}
+
+
+def cpu_baseline(cfg, budget_s, threads=1):
     """The oracle's serial select-then-attend step (scores, top-K, attention over the
     selected pages), timed on this host on a bounded sample of layer 0's decode steps;
-    metadata is prefill work and is built before timing."""
+    metadata is prefill work and is built before timing.  `threads`: BLAS / OpenMP threads
+    of the numpy oracle (the oracle itself is not changed)."""
     import oracle as O
     try:
         from threadpoolctl import threadpool_limits
@@ -114,23 +139,24 @@ def cpu_baseline(cfg, budget_s):
 
     def run():
         t_start = time.perf_counter()
-        t = 1
-        while time.perf_counter() - t_start < budget_s and t <= cfg.steps:
-            q = W.bits_to_f64(qb[t], cfg.dtype)
+        i = 0
+        while time.perf_counter() - t_start < budget_s:
+            q = W.bits_to_f64(qb[1 + i % cfg.steps], cfg.dtype)
             t0 = time.perf_counter()
             O.serial_step(q, k, v, cfg.page_size, cfg.context, cfg.k_select, cfg.forced_pages(),
                           cfg.forced_in_budget, cfg.meta_kind, meta=meta)
             times.append(time.perf_counter() - t0)
-            t += 1
+            i += 1
 
     if threadpool_limits is not None:
-        with threadpool_limits(limits=1):
+        with threadpool_limits(limits=threads):
             run()
     else:
         run()
     us = 1e6 * float(np.median(times))
-    return {"value": round(us, 1), "unit": "us/layer-step", "cores": 1, "kind": "oracle",
-            "sample": f"{len(times)} decode steps of layer 0 of {cfg.name} (float64 NumPy, 1 thread), median"}
+    return {"value": round(us, 1), "unit": "us/layer-step", "cores": threads, "kind": "oracle",
+            "sample": f"{len(times)} decode steps of layer 0 of {cfg.name} (float64 NumPy, {threads} BLAS "
+                      f"thread(s); the {cfg.steps}-step query trajectory repeats), median"}
 
 
 def kernel_sweep(args):
@@ -244,6 +270,110 @@ def delta_sweep(args, cfg):
     print(json.dumps(out), flush=True)
 
 
+def _timed_ms(torch, stream, fn, n):
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(n):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / n
+
+
+def extra_measurements(args, cfg, pc, layers, stack, s, dev, L, R, torch, n_layers):
+    """Launch floor of the fused grid, measured HBM peaks, and the metadata build (a
+    prefill step, not part of the decode step)."""
+    out = {}
+    grid = L.prr_fused_grid(stack.dims, stack.params, L.PRR_SCHED_FUSED_PRR)
+    stack.params.late_spec = 1
+    grid_late = L.prr_fused_grid(stack.dims, stack.params, L.PRR_SCHED_FUSED_PRR)
+    stack.params.late_spec = 0
+    floor = {"grid": grid_late, "threads": 512}
+    floor["direct_us"] = round(1000.0 * _timed_ms(torch, s, lambda: L.prr_empty_launch(grid_late, 512, s), 400), 3)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for _ in range(n_layers):
+            L.prr_empty_launch(grid_late, 512, s)
+    with torch.cuda.stream(s):
+        floor["graph_us"] = round(1000.0 * _timed_ms(torch, s, g.replay, 20) / n_layers, 3)
+    floor["fused_prr_grid_without_late"] = grid
+    out["launch_floor"] = floor
+    # HBM: a plain device copy (read + write) and a read-only reduction of 2 GiB
+    nbytes = 2 << 30
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    with torch.cuda.stream(s):
+        cp_ms = _timed_ms(torch, s, lambda: dst.copy_(src), 10)
+        rd_ms = _timed_ms(torch, s, lambda: src.sum(), 10)
+    del src, dst
+    torch.cuda.empty_cache()
+    out["hbm_measured"] = {"copy_gbps": round(2 * nbytes / (cp_ms * 1e-3) / 1e9, 1),
+                           "read_gbps": round(nbytes / (rd_ms * 1e-3) / 1e9, 1),
+                           "kind": "2 GiB float32: torch copy_ (read + write) and sum (read)"}
+    # page metadata (a1): every layer's K read once, metadata written
+    def build_all():
+        for st in layers:
+            st.build_meta(stream=s)
+    meta_ms = _timed_ms(torch, s, build_all, 3) / n_layers
+    kv_bytes = cfg.num_kv_heads * cfg.num_pages * cfg.page_size * cfg.head_dim * 2
+    meta_bytes = cfg.num_kv_heads * cfg.num_pages * ((2 * cfg.head_dim * 2) if cfg.meta_kind == "minmax" else cfg.head_dim * 4)
+    out["metadata_build"] = {"us_per_layer": round(1000.0 * meta_ms, 2), "bytes_per_layer": kv_bytes + meta_bytes,
+                             "gbps": round((kv_bytes + meta_bytes) / (meta_ms * 1e-3) / 1e9, 1)}
+    return out
+
+
+def other_workload(args, name, L, R, torch, dev, pool):
+    """The fused PRR step with late speculation and the fused serial step on another
+    workload: microseconds per layer-step and per token."""
+    cfg = W.CONFIGS[name]
+    pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
+                      num_tokens=cfg.context, k_select=cfg.k_select, forced=cfg.forced_pages(),
+                      forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
+                      alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma, chunk_pages=min(8, 256 // cfg.page_size))
+    layers = [None] * cfg.layers
+    t0 = time.time()
+    jobs = [(name, l) for l in range(cfg.layers)]
+    for layer, kb, vb in (pool.imap_unordered(_gen_layer, jobs) if pool is not None else map(_gen_layer, jobs)):
+        st = R.LayerState(pc, dev, k=R.bits_tensor(kb, pc.torch_dtype, dev), v=R.bits_tensor(vb, pc.torch_dtype, dev))
+        st.build_meta()
+        layers[layer] = st
+    print(f"[bench] {name}: {cfg.layers} layers ready ({time.time() - t0:.1f}s)", file=sys.stderr, flush=True)
+    steps = max(args.steps // 2, 8)
+    qs = torch.stack([R.bits_tensor(W.query_trajectory(cfg, l, steps=2 * steps + 16)[1], pc.torch_dtype, dev)
+                      for l in range(cfg.layers)], dim=1).contiguous()
+    q_static = torch.empty_like(qs[0])
+    stack = R.DecodeStack(layers, [q_static[l] for l in range(cfg.layers)], dev)
+    s = torch.cuda.Stream(device=dev)
+    tok = [0]
+
+    def step(schedule):
+        with torch.cuda.stream(s):
+            q_static.copy_(qs[tok[0]])
+        stack.step(schedule, s)
+        tok[0] += 1
+
+    s.wait_stream(torch.cuda.current_stream())
+    step(L.PRR_SCHED_FUSED_PREFILL)
+    res = {"layers": cfg.layers}
+    for label, sched, late in (("fused_prr_late", L.PRR_SCHED_FUSED_PRR, 1), ("fused_serial", L.PRR_SCHED_FUSED_SERIAL, 0)):
+        stack.params.late_spec = late
+        for _ in range(4):
+            step(sched)
+        ms = _timed_ms(torch, s, lambda: step(sched), steps)
+        res[label] = {"us_per_layer": round(1000.0 * ms / cfg.layers, 3), "us_per_token": round(1000.0 * ms, 1)}
+        flags = [int(st.workspace[:1].cpu()[0]) for st in layers]
+        if any(flags):
+            res[label]["error_flags"] = flags
+    b_alg = algorithmic_bytes(cfg, cfg.num_pages)
+    res["alg_bytes_per_layer_step"] = b_alg
+    res["roofline_frac"] = round(b_alg / (res["fused_prr_late"]["us_per_layer"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+    res["speedup_vs_serial"] = round(res["fused_serial"]["us_per_layer"] / res["fused_prr_late"]["us_per_layer"], 3)
+    del stack, layers
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -266,6 +396,10 @@ def main():
     ap.add_argument("--ablation", action="store_true",
                     help="also time the ablation stages S1 (reuse the previous top-K, recompute on a miss), "
                          "S2 (reuse + repair) and S3 (EMA + repair) with the fused PRR schedule")
+    ap.add_argument("--no-extras", dest="extras", action="store_false",
+                    help="skip the launch floor, HBM peak, metadata build and other-workload measurements")
+    ap.add_argument("--other-workloads", default="llama64k,infllm128k",
+                    help="workloads whose per-layer and per-token latency are also measured (comma list, '' = none)")
     ap.add_argument("--phases", type=int, default=0, metavar="TOKENS",
                     help="also record the fused launches' phase timestamps over TOKENS tokens (medians, us from start)")
     ap.add_argument("--phases-raw", action="store_true", help=argparse.SUPPRESS)
@@ -311,7 +445,7 @@ def main():
                 "serial": L.PRR_SCHED_SERIAL, "fused_prr_late_graph": L.PRR_SCHED_FUSED_PRR}
     n_abl = (3 if args.ablation else 0) + (2 if args.calibrate > 1 else 0)
     total_tokens = 2 + max(2, args.warmup) + 2 * (len(schedules) + n_abl) * (args.steps + 2) + \
-        n_abl * (1 + max(2, args.warmup)) + args.kernel_reps + 2 * args.phases + 8
+        n_abl * (1 + max(2, args.warmup)) + args.kernel_reps + 2 * args.phases + max(2, args.warmup) + 8
     t0 = time.time()
     layers = [None] * n_layers
 
@@ -322,10 +456,12 @@ def main():
         print(f"[bench] layer {layer} ready ({time.time() - t0:.1f}s)", file=sys.stderr, flush=True)
 
     jobs = [(cfg.name, l) for l in range(n_layers)]
-    if args.workers > 0:
-        with mp.get_context("fork").Pool(min(args.workers, os.cpu_count() or 1)) as pool:
-            for layer, kb, vb in pool.imap_unordered(_gen_layer, jobs):
-                add_layer(layer, kb, vb)
+    # input generators are forked before anything initialises the GPU, and kept for the
+    # other workloads measured at the end
+    pool = mp.get_context("fork").Pool(min(args.workers, os.cpu_count() or 1)) if args.workers > 0 else None
+    if pool is not None:
+        for layer, kb, vb in pool.imap_unordered(_gen_layer, jobs):
+            add_layer(layer, kb, vb)
     else:
         for job in jobs:
             add_layer(*_gen_layer(job))
@@ -389,6 +525,17 @@ def main():
     run(1, L.PRR_SCHED_FUSED_PREFILL)
     torch.cuda.synchronize()
     hits = run(max(2, args.warmup), L.PRR_SCHED_FUSED_PRR, measure_hits=True)
+    # how much of A the headline schedule attends before the threshold is known: P and the
+    # late pages (measured over warm-up tokens with late speculation)
+    coverage = []
+    stack.params.late_spec = 1
+    for _ in range(max(2, args.warmup)):
+        run(1, L.PRR_SCHED_FUSED_PRR)
+        torch.cuda.synchronize()
+        miss = torch.stack([st.missed for st in layers]).sum().item()
+        cov = torch.stack([st.covered for st in layers]).sum().item()
+        coverage.append(1.0 - (miss - cov) / (n_layers * cfg.num_kv_heads * cfg.selected_count))
+    stack.params.late_spec = 0
     ms = {}
     for name in schedules:  # warm each schedule, then two timed passes (the better one counts)
         cur[0] = stack_serial if name == "fused_serial" else stack
@@ -578,6 +725,7 @@ def main():
         "serial_us_per_layer": round(best_serial, 3) if best_serial else None,
         "speedup_vs_serial": round(best_serial / us_prr, 3) if best_serial else None,
         "hit_rate": round(float(np.mean(hits)), 4) if hits else None,
+        "coverage_before_threshold": round(float(np.mean(coverage)), 4) if coverage else None,
         "kernel_us": {k: round(v, 2) for k, v in ktimes.items()},
         "ablation": ablation,
         "calibration": calibration,
@@ -592,7 +740,23 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         out["copy_calibration_bytes"] = {"read": nbytes, "write": nbytes}
-    out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds) if args.cpu_seconds > 0 else None
+    if args.extras:
+        out.update(extra_measurements(args, cfg, pc, layers, stack, s, dev, L, R, torch, n_layers))
+        if args.other_workloads:
+            del stack, stack_serial, cur
+            layers.clear()
+            torch.cuda.empty_cache()
+            out["other_workloads"] = {name: other_workload(args, name, L, R, torch, dev, pool)
+                                      for name in args.other_workloads.split(",") if name}
+    if pool is not None:
+        pool.close()
+        pool.join()
+    if args.cpu_seconds > 0:
+        out["host"] = host_info()
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds, threads=out["host"]["affinity"] or 1)
+        out["cpu_baseline_1core"] = cpu_baseline(cfg, args.cpu_seconds, threads=1)
+    else:
+        out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)
 
 

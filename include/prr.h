@@ -262,6 +262,8 @@ typedef struct {
   int32_t* wasted_count;       /* or NULL */
   void* workspace;
   size_t ws_bytes;
+  int32_t* covered_count;      /* or NULL: [Hkv] pages of A \ P attended by late speculation
+                                  (fused PRR schedule; 0 otherwise) */
 } prr_layer_io;
 
 /* Per-step parameters shared by the layers. */
@@ -329,6 +331,16 @@ typedef struct {
 prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* params, const prr_layer_io* layers,
                            int32_t n_layers, int32_t parity, int32_t schedule, hipStream_t stream,
                            hipStream_t spec_stream, hipEvent_t* events);
+
+/* Workgroups of one layer's launch of a fused schedule with these parameters (the
+ * launch-floor measurement compares it with an empty launch of the same shape); 0 for
+ * invalid arguments or a schedule that is not fused. */
+int32_t prr_fused_grid(const prr_dims* dims, const prr_step_params* params, int32_t schedule);
+
+/* Measurement helper: an empty kernel of `grid` workgroups of `threads` threads on
+ * `stream` (the launch floor of a grid of that shape).  Errors: PRR_ERR_INVALID_ARG for a
+ * grid outside [1, 2^20] or threads outside [1, 1024]. */
+prr_status prr_empty_launch(int32_t grid, int32_t threads, hipStream_t stream);
 
 /* Advance the device epoch word of captured fused steps (prr_step_params.epoch_dev)
  * by one, skipping 0: one single-thread launch on `stream`, so it can be captured with

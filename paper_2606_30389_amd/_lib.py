@@ -44,7 +44,7 @@ EXPORTED = (
     "prr_status_string", "prr_last_error", "prr_workspace_size", "prr_workspace_init",
     "prr_spec_state_floats", "prr_build_page_meta", "prr_score_topk", "prr_predict",
     "prr_spec_attn", "prr_repair", "prr_merge_states", "prr_decode_step", "prr_calibrate",
-    "prr_epoch_advance", "prr_pick_delta", "prr_score_topk_static",
+    "prr_epoch_advance", "prr_pick_delta", "prr_score_topk_static", "prr_empty_launch", "prr_fused_grid",
 )
 
 
@@ -70,6 +70,7 @@ class prr_layer_io(ctypes.Structure):
         ("page_m", ctypes.c_void_p), ("out_o32", ctypes.c_void_p), ("out_o", ctypes.c_void_p),
         ("out_m", ctypes.c_void_p), ("out_l", ctypes.c_void_p), ("missed_count", ctypes.c_void_p),
         ("wasted_count", ctypes.c_void_p), ("workspace", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t),
+        ("covered_count", ctypes.c_void_p),
     ]
 
 
@@ -109,6 +110,8 @@ _SIGS = {
                              _P, ctypes.POINTER(ctypes.c_void_p)]),
     "prr_calibrate": (_I, [_P, _I, _I, _I, _P, _I, _I, _P, _I, _I, _P, _P]),
     "prr_epoch_advance": (_I, [_P, _P]),
+    "prr_empty_launch": (_I, [_I, _I, _P]),
+    "prr_fused_grid": (_I, [_DIMS, _P, _I]),
     "prr_pick_delta": (_I, [_P, _P, _P, _P, _I, _I, _I, _P, _P, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
@@ -268,6 +271,14 @@ def prr_pick_delta(rows, query_context, degree=2):
                                int(degree), ctypes.addressof(out), ctypes.addressof(out) + 4,
                                ctypes.addressof(out) + 8))
     return float(out[0]), float(out[1]), float(out[2])
+
+
+def prr_empty_launch(grid, threads, stream=None):
+    _check(_lib.prr_empty_launch(int(grid), int(threads), _stream(stream)))
+
+
+def prr_fused_grid(dims, params, schedule):
+    return int(_lib.prr_fused_grid(ctypes.byref(dims), ctypes.byref(params), int(schedule)))
 
 
 def prr_decode_step(dims, params, layers, parity, schedule, stream=None, spec_stream=None, events=None):

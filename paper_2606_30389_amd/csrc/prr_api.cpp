@@ -222,6 +222,30 @@ prr_status prr_workspace_init(void* workspace, size_t bytes, hipStream_t stream)
   return hip_status(prr::launch_fill_zero(workspace, bytes, stream), "workspace fill");
 }
 
+prr_status prr_empty_launch(int32_t grid, int32_t threads, hipStream_t stream) {
+  if (grid < 1 || grid > (1 << 20)) return fail(PRR_ERR_INVALID_ARG, "grid %d outside [1, 2^20]", grid);
+  if (threads < 1 || threads > 1024) return fail(PRR_ERR_INVALID_ARG, "threads %d outside [1, 1024]", threads);
+  return hip_status(prr::launch_empty(grid, threads, stream), "empty launch");
+}
+
+int32_t prr_fused_grid(const prr_dims* dims, const prr_step_params* sp, int32_t schedule) {
+  if (check_dims(dims) != PRR_OK || !sp || schedule < PRR_SCHED_FUSED_SERIAL || schedule > PRR_SCHED_FUSED_PREFILL)
+    return 0;
+  WsLayout L;
+  if (!ws_layout(dims, sp->cap, sp->chunk_pages, L) || sp->num_pages < 1) return 0;
+  prr::FusedLaunch a;
+  memset(&a, 0, sizeof(a));
+  a.schedule = schedule == PRR_SCHED_FUSED_PRR ? 1 : (schedule == PRR_SCHED_FUSED_PREFILL ? 2 : 0);
+  a.num_kv_heads = dims->num_kv_heads;
+  a.group = dims->num_q_heads / dims->num_kv_heads;
+  a.n_score = div_up(sp->num_pages, prr::kFusedScorePages);
+  a.n_spec = L.nchunks;
+  a.n_miss = L.nchunks;
+  a.late = a.schedule == 1 && sp->late_spec && sp->mode != PRR_RECOMPUTE_ON_MISS;
+  a.n_late = a.late ? L.nchunks : 0;
+  return prr::fused_grid(a);
+}
+
 prr_status prr_epoch_advance(uint32_t* epoch_dev, hipStream_t stream) {
   PRR_TRY(check_ptr(epoch_dev, "epoch_dev", 4));
   return hip_status(prr::launch_epoch_advance(epoch_dev, stream), "epoch advance");
@@ -533,6 +557,7 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
     PRR_TRY(check_ptr(y.out_l, "out_l", 4));
     if (y.missed_count && !aligned(y.missed_count, 4)) return fail(PRR_ERR_INVALID_ARG, "missed_count misaligned");
     if (y.wasted_count && !aligned(y.wasted_count, 4)) return fail(PRR_ERR_INVALID_ARG, "wasted_count misaligned");
+    if (y.covered_count && !aligned(y.covered_count, 4)) return fail(PRR_ERR_INVALID_ARG, "covered_count misaligned");
   }
   if (prr || prefill) {
     PRR_TRY(check_ptr(y.ema_level, "ema_level", 4));
@@ -606,6 +631,7 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.out_l = y.out_l;
   a.missed_count = y.missed_count;
   a.wasted_count = y.wasted_count;
+  a.covered_count = y.covered_count;
   char* ws = static_cast<char*>(y.workspace);
   a.t_score = reinterpret_cast<uint64_t*>(ws + L.f_score);
   a.t_thr = reinterpret_cast<uint64_t*>(ws + L.f_thr);

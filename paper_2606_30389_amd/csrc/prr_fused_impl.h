@@ -1136,6 +1136,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
     a.selected_count[h] = nA;
     if (a.missed_count) a.missed_count[h] = prr ? nMiss : nM;
     if (a.wasted_count) a.wasted_count[h] = prr ? L.npv - nPA : 0;
+    if (a.covered_count) a.covered_count[h] = prr ? max(nMiss - nM, 0) : 0;  // (0 when M = A)
   }
   if (nM > 0 && nM <= kFW) {
     // few enough to attend here: one page per wave, published as the first miss slot
@@ -1260,6 +1261,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
       a.selected_count[h] = min(na, a.cap);
       if (a.missed_count) a.missed_count[h] = prr ? nMiss : nM;
       if (a.wasted_count) a.wasted_count[h] = prr ? L.npv - nPA : 0;
+      if (a.covered_count) a.covered_count[h] = prr ? max(nMiss - nM, 0) : 0;  // (0 when M = A)
     }
   } else if (w == 1 || (w == 2 && a.late)) {
     // the next step's lower bounds: rank 2.5|A| (candidates of A) and 1.375|A| (late pages)

@@ -43,6 +43,13 @@ hipError_t launch_epoch_advance(uint32_t* epoch_dev, hipStream_t stream) {
 // workspace fill
 // =====================================================================================
 
+// An empty kernel: the launch floor of a grid of a given shape.
+__global__ void empty_kernel() {}
+
+hipError_t launch_empty(int grid, int threads, hipStream_t stream) {
+  return hipLaunchKernel((const void*)empty_kernel, dim3(grid), dim3(threads), nullptr, 0, stream);
+}
+
 __global__ void fill_zero_kernel(u32x4_t* __restrict__ p, size_t n16) {
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) p[i] = u32x4_t{0, 0, 0, 0};

@@ -110,6 +110,7 @@ struct FusedLaunch {
   float* out_l;
   int32_t* missed_count;
   int32_t* wasted_count;
+  int32_t* covered_count;  // pages of A \ P attended by late speculation, or NULL
   uint64_t* t_score;  // [Hkv][max_pages] tagged score bits
   uint64_t* t_thr;    // [Hkv][8 copies][32] tagged threshold of A (words 0, 1 of each copy)
   uint64_t* t_mcnt;   // [Hkv][8][32] tagged count of the missed list (bit 31: attended by the select workgroup)
@@ -180,6 +181,7 @@ prr_status api_fail(prr_status st, const char* fmt, ...);
 prr_status api_ok();
 
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
+hipError_t launch_empty(int grid, int threads, hipStream_t stream);
 hipError_t launch_epoch_advance(uint32_t* epoch_dev, hipStream_t stream);
 void calibrate_grid(const float* scores, int n_traj, int n_rows, int n_blocks, const int32_t* form_row, int k_select,
                     int p_select, const float* grid, int n_grid, int n_threads, float* best_theta,

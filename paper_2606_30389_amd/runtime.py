@@ -111,6 +111,7 @@ class LayerState:
         self.out_l = torch.zeros(cfg.num_q_heads, **f32)
         self.missed = torch.zeros(hkv, **i32)
         self.wasted = torch.zeros(hkv, **i32)
+        self.covered = torch.zeros(hkv, **i32)
         self.ws_bytes = L.prr_workspace_size(self.dims, self.cap, cfg.chunk_pages)
         self.workspace = torch.empty(self.ws_bytes // 4 + 64, dtype=torch.int32, device=dev)
         L.prr_workspace_init(self.workspace, self.ws_bytes)
@@ -169,6 +170,7 @@ class LayerState:
         y.part_o, y.part_m, y.part_l, y.page_m = ptr(self.part_o), ptr(self.part_m), ptr(self.part_l), ptr(self.page_m)
         y.out_o32, y.out_o, y.out_m, y.out_l = ptr(self.out_o32), ptr(self.out_o), ptr(self.out_m), ptr(self.out_l)
         y.missed_count, y.wasted_count = ptr(self.missed), ptr(self.wasted)
+        y.covered_count = ptr(self.covered)
         y.workspace, y.ws_bytes = ptr(self.workspace), self.ws_bytes
         return y
 

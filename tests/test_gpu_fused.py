@@ -197,10 +197,12 @@ def test_fused_full_size(torch, case):
             ref = O.attend(q64, *kv64[layer], target, pc.page_size, nt)
             S.check_attention(S.to_np(st.out_o32), S.to_np(st.out_m), S.to_np(st.out_l), ref, S.to_np(st.out_o),
                               dtype=pc.dtype, what=f"PRR layer {layer} step {t}")
-            mc, wc = S.to_np(st.missed), S.to_np(st.wasted)
+            mc, wc, cc = S.to_np(st.missed), S.to_np(st.wasted), S.to_np(st.covered)
             for h in range(pc.num_kv_heads):
                 mm, ww = O.missed_and_wasted(A[h], P[h])
                 assert (mc[h], wc[h]) == (len(mm), len(ww)), f"layer {layer} head {h} step {t}: missed/wasted"
+                # pages of A outside P that late speculation attended: none without it
+                assert 0 <= cc[h] <= (mc[h] if case.late else 0), f"layer {layer} head {h} step {t}: covered {cc[h]}"
             state[layer] = O.ema_update(level, trend, s64, pc.alpha, pc.beta)
             _check_state(st, *state[layer], pc, f"layer {layer} step {t}")
         if case.serial:
