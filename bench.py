@@ -648,7 +648,7 @@ def main():
             if args.phases_raw:
                 raw = stamps.cpu().numpy()[0]
                 t0 = raw[0][raw[0] > 0].min()
-                phases[label + "_raw_layer0"] = [[int((x - t0) // 10) if x > 0 else -1 for x in raw[k][:400]]
+                phases[label + "_raw_layer0"] = [[int((x - t0) // 10) if x > 0 else -1 for x in raw[k][:1024]]
                                                  for k in range(15)]
             arr = np.asarray(rows, dtype=np.float64)  # [launch][phase][median over workgroups, last]
             phases[label] = {n: ([round(float(np.nanmedian(arr[:, i, j])), 2) for j in range(2)]

@@ -417,7 +417,7 @@ __device__ __forceinline__ void role_score(const FusedLaunch& a, uint32_t ep, in
 #pragma unroll
     for (int j = 0; j < 2 * kPfLoads; ++j) pf[k][j] = 0u;
   }
-  if (a.late) {
+  if (a.readahead) {
     const char* kh = static_cast<const char*>(a.k_cache) + (size_t)h * a.max_pages * PS * kHeadDim * 2;
     const char* vh = static_cast<const char*>(a.v_cache) + (size_t)h * a.max_pages * PS * kHeadDim * 2;
     uint64_t m0 = lmask[0], m1 = kHalves > 1 ? lmask[kHalves - 1] : 0ull;
@@ -1233,17 +1233,12 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
         const bool in = (inM >> j) & 1ull;
         const uint64_t bm = __ballot(in);
         const int q = pos + lanes_below(bm);
-        if (in && q < a.cap) {
-          L.mlist[q] = page[j];
-          if (nM > kFW) put_tag(&ml[q], (uint32_t)page[j], ep);
-        }
+        if (in && q < a.cap) put_tag(&ml[q], (uint32_t)page[j], ep);
         pos += __popcll(bm);
       }
-      if (lane == 0) {
-        const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
-        publish_mcnt(a, h, (uint32_t)nM | mflags | self, ep);
-        L.cnt[0][0] = nM;
-      }
+      // (the missed-page workgroups attend M even when it is short: this workgroup's
+      // other waves are still deriving the next step's bounds)
+      if (lane == 0) publish_mcnt(a, h, (uint32_t)nM | mflags, ep);
     }
     // the selected list (an output) and the counts
     int32_t* sel = a.selected + (size_t)h * a.cap;
@@ -1268,19 +1263,6 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
     const int k = w == 1 ? (5 * a.kextra_a) / 2 : kLateRank(a.kextra_a);
     const SelThreshold th = wsel_threshold<NK>(key, cand, max(k, 1), L.ws[w], true);
     if (lane == 0 && th.mode == 2 && qn > 0.0f) a.win[4 * h + (w == 1 ? 0 : 2)] = __float_as_uint(key_value(th.T) / qn);
-  }
-  __syncthreads();
-  const int nM = L.cnt[0][0];
-  if (nM > 0 && nM <= kFW) {
-    // few enough to attend here: one page per wave, published as the first miss slot
-    int pg[1];
-    pg[0] = __builtin_amdgcn_readfirstlane(w < nM ? L.mlist[w] : -1);
-    __syncthreads();  // the list is read before the attention reuses the LDS
-    u32x4_t qf[4];
-    load_q(a, h, qf, U.qs);
-    WaveStates<1> st;
-    wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
-    fold_publish<1>(a, kStampMiss, pub_dst(a, h, a.n_spec), ep, st, 1u, U.attn);
   }
 }
 
@@ -1338,16 +1320,13 @@ __device__ __forceinline__ int miss_block(const FusedLaunch& a, uint32_t ep, int
   uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    if (mM[j] && q[j] < a.cap) {
-      L.mlist[q[j]] = pg[j];
-      if (nM > kFW) put_tag(&ml[q[j]], (uint32_t)pg[j], ep);
-    }
+    if (mM[j] && q[j] < a.cap) put_tag(&ml[q[j]], (uint32_t)pg[j], ep);
   }
+  // (the missed-page workgroups attend M even when it is short: this workgroup goes on
+  // to derive the next step's bounds)
   if (t == 0) {
-    const uint32_t self = (nM > 0 && nM <= kFW) ? kSelfMiss : 0u;
-    publish_mcnt(a, h, (uint32_t)nM | (drop ? kDropSpec : 0u) | self, ep);
+    publish_mcnt(a, h, (uint32_t)nM | (drop ? kDropSpec : 0u), ep);
     if (a.late) put_rep(a.t_lcnt, h, 0, (uint32_t)min(l0 + (tot_l >> 16), capl), ep);
-    L.cnt[0][0] = nM;
   }
   return nM;
 }
@@ -1996,9 +1975,31 @@ __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
 // One instance of the fused kernel, launched on `grid` workgroups.  Instances are spread
 // over several translation units (explicit instantiations below each include of this
 // file), so that they compile in parallel.
+//
+// The late read-ahead keeps a score workgroup resident until its loads return.  It is
+// used only when the whole grid is resident at once: otherwise the workgroups dispatched
+// last (late, missed-page and merge roles) wait for those slots.
 template <bool BF16, int PS, int NPW>
 hipError_t launch_fused_inst(int grid, const FusedLaunch& a, hipStream_t stream) {
-  void* args[] = {const_cast<FusedLaunch*>(&a)};
+  constexpr int kMaxDevices = 64;
+  static int resident[kMaxDevices];  // workgroups of this kernel resident at once (0 = not known yet)
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  int cap = dev >= 0 && dev < kMaxDevices ? resident[dev] : 0;
+  if (cap == 0) {
+    int per_cu = 0, cus = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fused_step_kernel<BF16, PS, NPW>),
+                                                     kFT, 0);
+    if (e != hipSuccess) return e;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    cap = per_cu * cus;
+    if (dev >= 0 && dev < kMaxDevices) resident[dev] = cap;
+  }
+  FusedLaunch b = a;
+  b.readahead = a.late && grid <= cap;
+  void* args[] = {&b};
   return hipLaunchKernel(reinterpret_cast<const void*>(fused_step_kernel<BF16, PS, NPW>), dim3(grid), dim3(kFT), args,
                          0, stream);
 }

@@ -136,6 +136,7 @@ struct FusedLaunch {
   int kextra_a, kextra_p, cap, chunk;
   int n_score, n_spec, n_miss, n_late, nparts;  // workgroups per KV head; partial slots per KV head
   int late;  // late speculation on (PRR schedule)
+  int readahead;  // score workgroups read the first late pages ahead (set at launch)
   int n_forced;
   bool meta_mean;
   int32_t forced[PRR_MAX_FORCED];
