@@ -23,7 +23,6 @@ from __future__ import annotations
 
 import argparse
 import dataclasses
-import hashlib
 import json
 import math
 import multiprocessing as mp
@@ -69,29 +68,16 @@ def score_kernel_bytes(cfg, n_pages):
         cfg.num_kv_heads * cfg.selected_count * 4
 
 
-def kernel_source_hash():
-    """Hash of the device sources' code (comments, blank lines and trailing blanks left out,
-    so that only a change of the code itself invalidates the recorded counters)."""
-    import re
-    h = hashlib.sha256()
-    for f in ("paper_2606_30389_amd/csrc/prr_kernels.hip", "paper_2606_30389_amd/csrc/prr_fused_impl.h",
-              "paper_2606_30389_amd/csrc/prr_select.h", "paper_2606_30389_amd/csrc/prr_device.h"):
-        with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
-            text = re.sub(r"/\*.*?\*/", "", fh.read(), flags=re.S)
-        lines = (re.sub(r"//.*$", "", ln).rstrip() for ln in text.splitlines())
-        h.update("\n".join(ln for ln in lines if ln).encode())
-    return h.hexdigest()[:16]
-
-
-def load_traffic(kernel):
+def load_traffic(kernel, config):
     """HBM bytes per launch from the committed rocprofv3 counter runs, if they were taken
-    on the current kernel source (otherwise null)."""
+    on the current kernel source and this workload (otherwise null)."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
-    if t.get("kernel_source") != kernel_source_hash():
+    from paper_2606_30389_amd.profile_summary import kernel_source_hash
+    if t.get("kernel_source") != kernel_source_hash() or t.get("config") != config:
         return None
     return t.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
 
@@ -270,6 +256,14 @@ def delta_sweep(args, cfg):
     print(json.dumps(out), flush=True)
 
 
+def late_spec_of(schedule):
+    """prr_step_params.late_spec of a schedule label: fused_prr_late* speculate late pages
+    (with the read-ahead; *_nora without it)."""
+    if not schedule.startswith("fused_prr_late"):
+        return 0
+    return 2 if "nora" in schedule else 1
+
+
 def _timed_ms(torch, stream, fn, n):
     torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -306,11 +300,20 @@ def extra_measurements(args, cfg, pc, layers, stack, s, dev, L, R, torch, n_laye
     with torch.cuda.stream(s):
         cp_ms = _timed_ms(torch, s, lambda: dst.copy_(src), 10)
         rd_ms = _timed_ms(torch, s, lambda: src.sum(), 10)
+        # the library's read-stream kernel (16-byte loads, eight in flight per thread):
+        # the best over a few grid sizes
+        sink = torch.empty(16384, dtype=torch.int32, device=dev)
+        rs = {}
+        for grid in (2048, 4096, 8192, 16384):
+            rs[grid] = _timed_ms(torch, s, lambda: L.prr_read_stream(src, nbytes, sink, grid, s), 10)
     del src, dst
     torch.cuda.empty_cache()
+    best_grid = min(rs, key=rs.get)
     out["hbm_measured"] = {"copy_gbps": round(2 * nbytes / (cp_ms * 1e-3) / 1e9, 1),
-                           "read_gbps": round(nbytes / (rd_ms * 1e-3) / 1e9, 1),
-                           "kind": "2 GiB float32: torch copy_ (read + write) and sum (read)"}
+                           "torch_sum_read_gbps": round(nbytes / (rd_ms * 1e-3) / 1e9, 1),
+                           "read_gbps": round(nbytes / (rs[best_grid] * 1e-3) / 1e9, 1),
+                           "read_grid": best_grid,
+                           "kind": "2 GiB buffer: torch copy_ (read + write), torch sum (read), prr_read_stream (read)"}
     # page metadata (a1): every layer's K read once, metadata written
     def build_all():
         for st in layers:
@@ -405,7 +408,8 @@ def main():
     ap.add_argument("--phases-raw", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--chunk", type=int, default=None, help="pages per speculation chunk (default 8, 4 for 64-token pages)")
     ap.add_argument("--delta", type=float, default=1.0, help="|P| / |A| (speculation budget)")
-    ap.add_argument("--schedules", default="fused_prr,fused_prr_late,fused_serial,fused_prr_late_graph,two_stream,serial")
+    ap.add_argument("--schedules", default="fused_prr,fused_prr_late,fused_prr_late_nora,fused_serial,fused_prr_late_graph,"
+                                           "two_stream,serial")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--kernel-reps", type=int, default=2, help="tokens per kernel-timing pass (separate kernels)")
     ap.add_argument("--workers", type=int, default=16, help="input-generation processes (0 = in-process)")
@@ -441,6 +445,7 @@ def main():
                       chunk_pages=args.chunk or min(8, 256 // cfg.page_size), mode=mode, p_select=p_select)
     schedules = [x for x in args.schedules.split(",") if x]
     sched_id = {"fused_prr": L.PRR_SCHED_FUSED_PRR, "fused_prr_late": L.PRR_SCHED_FUSED_PRR,
+                "fused_prr_late_nora": L.PRR_SCHED_FUSED_PRR,
                 "fused_serial": L.PRR_SCHED_FUSED_SERIAL, "two_stream": L.PRR_SCHED_TWO_STREAM,
                 "serial": L.PRR_SCHED_SERIAL, "fused_prr_late_graph": L.PRR_SCHED_FUSED_PRR}
     n_abl = (3 if args.ablation else 0) + (2 if args.calibrate > 1 else 0)
@@ -528,7 +533,7 @@ def main():
     # how much of A the headline schedule attends before the threshold is known: P and the
     # late pages (measured over warm-up tokens with late speculation)
     coverage = []
-    stack.params.late_spec = 1
+    stack.params.late_spec = next((late_spec_of(x) for x in schedules if late_spec_of(x)), 1)
     for _ in range(max(2, args.warmup)):
         run(1, L.PRR_SCHED_FUSED_PRR)
         torch.cuda.synchronize()
@@ -539,7 +544,7 @@ def main():
     ms = {}
     for name in schedules:  # warm each schedule, then two timed passes (the better one counts)
         cur[0] = stack_serial if name == "fused_serial" else stack
-        stack.params.late_spec = int(name.startswith("fused_prr_late"))
+        stack.params.late_spec = late_spec_of(name)
         run(2, sched_id[name])
         # *_graph: the token's launches are captured as HIP graphs (one per parity of the
         # prediction buffers) and replayed; otherwise launched directly
@@ -705,8 +710,11 @@ def main():
     achieved = b_alg / (us_prr * 1e-6) / 1e9
     roofline = {"bound": "hbm", "kernel": f"fused_step_kernel ({main_sched})", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                "traffic": load_traffic(main_sched), "alg_bytes_per_launch": b_alg,
+                "traffic": load_traffic(main_sched, cfg.name), "alg_bytes_per_launch": b_alg,
+                "traffic_over_alg": None,
                 "avg_launch_us": round(us_prr, 3)}
+    if roofline["traffic"]:
+        roofline["traffic_over_alg"] = round(roofline["traffic"] / b_alg, 3)
     best_serial = min(us[k] for k in ("fused_serial", "serial") if k in us) if any(
         k in us for k in ("fused_serial", "serial")) else None
     out = {
@@ -742,6 +750,9 @@ def main():
         out["copy_calibration_bytes"] = {"read": nbytes, "write": nbytes}
     if args.extras:
         out.update(extra_measurements(args, cfg, pc, layers, stack, s, dev, L, R, torch, n_layers))
+        # the same achieved rate against the read rate this chip reaches in practice
+        roofline["measured_read_peak"] = out["hbm_measured"]["read_gbps"]
+        roofline["frac_of_measured_read"] = round(achieved / out["hbm_measured"]["read_gbps"], 4)
         if args.other_workloads:
             del stack, stack_serial, cur
             layers.clear()

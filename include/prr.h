@@ -288,7 +288,12 @@ typedef struct {
   int32_t late_spec;           /* PRR_SCHED_FUSED_PRR: 1 = also speculate, as soon as this step's
                                   scores exist, over the pages just above the selection threshold
                                   that P missed (the threshold is learned across steps); the result
-                                  is still attention over exactly A (or P u A) */
+                                  is still attention over exactly A (or P u A).  With 1 the score
+                                  workgroups also read the first late pages ahead into the
+                                  memory-side cache when the launch's grid is resident at once
+                                  (those lines are then fetched twice); 2 = late speculation
+                                  without the read-ahead; 0 = none; other values give
+                                  PRR_ERR_INVALID_ARG */
   uint64_t* phase_stamps;      /* fused schedules, or NULL: device [n_layers][16][1024] zeroed by the
                                   caller; entry [l][k][w] receives the device real-time clock
                                   (100 MHz, s_memrealtime) when workgroup w of layer l's launch
@@ -341,6 +346,14 @@ int32_t prr_fused_grid(const prr_dims* dims, const prr_step_params* params, int3
  * `stream` (the launch floor of a grid of that shape).  Errors: PRR_ERR_INVALID_ARG for a
  * grid outside [1, 2^20] or threads outside [1, 1024]. */
 prr_status prr_empty_launch(int32_t grid, int32_t threads, hipStream_t stream);
+
+/* Measurement helper: reads each 16-byte word of the device buffer `buf` (`bytes` long)
+ * once, with `grid` workgroups of 256 threads on `stream`, and writes one word per
+ * workgroup to the device array `sink` (grid words; their values are meaningless): the
+ * chip's read-stream rate for a kernel of this library's access pattern.  Errors:
+ * PRR_ERR_INVALID_ARG for a NULL or misaligned pointer (buf 16 bytes, sink 4), `bytes`
+ * not a positive multiple of 16, or a grid outside [1, 2^20]. */
+prr_status prr_read_stream(const void* buf, size_t bytes, uint32_t* sink, int32_t grid, hipStream_t stream);
 
 /* Advance the device epoch word of captured fused steps (prr_step_params.epoch_dev)
  * by one, skipping 0: one single-thread launch on `stream`, so it can be captured with

@@ -45,6 +45,7 @@ EXPORTED = (
     "prr_spec_state_floats", "prr_build_page_meta", "prr_score_topk", "prr_predict",
     "prr_spec_attn", "prr_repair", "prr_merge_states", "prr_decode_step", "prr_calibrate",
     "prr_epoch_advance", "prr_pick_delta", "prr_score_topk_static", "prr_empty_launch", "prr_fused_grid",
+    "prr_read_stream",
 )
 
 
@@ -111,6 +112,7 @@ _SIGS = {
     "prr_calibrate": (_I, [_P, _I, _I, _I, _P, _I, _I, _P, _I, _I, _P, _P]),
     "prr_epoch_advance": (_I, [_P, _P]),
     "prr_empty_launch": (_I, [_I, _I, _P]),
+    "prr_read_stream": (_I, [_P, _S, _P, _I, _P]),
     "prr_fused_grid": (_I, [_DIMS, _P, _I]),
     "prr_pick_delta": (_I, [_P, _P, _P, _P, _I, _I, _I, _P, _P, _P]),
 }
@@ -275,6 +277,10 @@ def prr_pick_delta(rows, query_context, degree=2):
 
 def prr_empty_launch(grid, threads, stream=None):
     _check(_lib.prr_empty_launch(int(grid), int(threads), _stream(stream)))
+
+
+def prr_read_stream(buf, nbytes, sink, grid, stream=None):
+    _check(_lib.prr_read_stream(_ptr(buf), int(nbytes), _ptr(sink), int(grid), _stream(stream)))
 
 
 def prr_fused_grid(dims, params, schedule):

@@ -228,6 +228,14 @@ prr_status prr_empty_launch(int32_t grid, int32_t threads, hipStream_t stream) {
   return hip_status(prr::launch_empty(grid, threads, stream), "empty launch");
 }
 
+prr_status prr_read_stream(const void* buf, size_t bytes, uint32_t* sink, int32_t grid, hipStream_t stream) {
+  PRR_TRY(check_ptr(buf, "buf", 16));
+  PRR_TRY(check_ptr(sink, "sink", 4));
+  if (bytes == 0 || bytes % 16 != 0) return fail(PRR_ERR_INVALID_ARG, "bytes %zu is not a positive multiple of 16", bytes);
+  if (grid < 1 || grid > (1 << 20)) return fail(PRR_ERR_INVALID_ARG, "grid %d outside [1, 2^20]", grid);
+  return hip_status(prr::launch_read_stream(buf, bytes, sink, grid, stream), "read stream");
+}
+
 int32_t prr_fused_grid(const prr_dims* dims, const prr_step_params* sp, int32_t schedule) {
   if (check_dims(dims) != PRR_OK || !sp || schedule < PRR_SCHED_FUSED_SERIAL || schedule > PRR_SCHED_FUSED_PREFILL)
     return 0;
@@ -587,6 +595,7 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
     return fail(PRR_ERR_INVALID_ARG, "chunk_pages %d outside [1, 256 / page_size]", sp->chunk_pages);
   if (sp->mode != PRR_EXACT_SELECTED && sp->mode != PRR_KEEP_WASTED && sp->mode != PRR_RECOMPUTE_ON_MISS)
     return fail(PRR_ERR_INVALID_ARG, "mode %d", sp->mode);
+  if (sp->late_spec < 0 || sp->late_spec > 2) return fail(PRR_ERR_INVALID_ARG, "late_spec %d", sp->late_spec);
   if (sp->epoch_dev) {
     PRR_TRY(check_ptr(sp->epoch_dev, "epoch_dev", 4));
   } else if (sp->epoch == 0) {
@@ -674,6 +683,7 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.n_spec = L.nchunks;
   a.n_miss = L.nchunks;
   a.late = prr && sp->late_spec && sp->mode != PRR_RECOMPUTE_ON_MISS;
+  a.readahead = a.late && sp->late_spec == 1;  // (kept only if the grid is resident at once)
   a.n_late = a.late ? L.nchunks : 0;
   a.nparts = L.nparts;
   a.n_forced = sp->n_forced;

@@ -1998,7 +1998,7 @@ hipError_t launch_fused_inst(int grid, const FusedLaunch& a, hipStream_t stream)
     if (dev >= 0 && dev < kMaxDevices) resident[dev] = cap;
   }
   FusedLaunch b = a;
-  b.readahead = a.late && grid <= cap;
+  b.readahead = a.readahead && grid <= cap;
   void* args[] = {&b};
   return hipLaunchKernel(reinterpret_cast<const void*>(fused_step_kernel<BF16, PS, NPW>), dim3(grid), dim3(kFT), args,
                          0, stream);

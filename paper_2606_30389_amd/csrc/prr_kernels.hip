@@ -50,6 +50,38 @@ hipError_t launch_empty(int grid, int threads, hipStream_t stream) {
   return hipLaunchKernel((const void*)empty_kernel, dim3(grid), dim3(threads), nullptr, 0, stream);
 }
 
+// Read-stream rate: every 16-byte word of the buffer read once (eight loads in flight
+// per thread, consecutive lanes on consecutive words), folded into one word per
+// workgroup so that the loads stay live.
+__global__ void __launch_bounds__(256) read_stream_kernel(const u32x4_t* __restrict__ p, size_t n16,
+                                                          uint32_t* __restrict__ sink) {
+  constexpr int kU = 8;
+  const size_t stride = (size_t)gridDim.x * 256;
+  uint32_t acc = 0;
+  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  for (; i + (kU - 1) * stride < n16; i += kU * stride) {
+    u32x4_t v[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) v[u] = __builtin_nontemporal_load(p + i + u * stride);
+#pragma unroll
+    for (int u = 0; u < kU; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  for (; i < n16; i += stride) {
+    const u32x4_t v = p[i];
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  __shared__ uint32_t red[4];
+  for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
+}
+
+hipError_t launch_read_stream(const void* p, size_t bytes, uint32_t* sink, int grid, hipStream_t stream) {
+  read_stream_kernel<<<grid, 256, 0, stream>>>(static_cast<const u32x4_t*>(p), bytes / 16, sink);
+  return hipGetLastError();
+}
+
 __global__ void fill_zero_kernel(u32x4_t* __restrict__ p, size_t n16) {
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) p[i] = u32x4_t{0, 0, 0, 0};

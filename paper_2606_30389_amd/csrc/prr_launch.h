@@ -136,7 +136,7 @@ struct FusedLaunch {
   int kextra_a, kextra_p, cap, chunk;
   int n_score, n_spec, n_miss, n_late, nparts;  // workgroups per KV head; partial slots per KV head
   int late;  // late speculation on (PRR schedule)
-  int readahead;  // score workgroups read the first late pages ahead (set at launch)
+  int readahead;  // score workgroups read the first late pages ahead (allowed; decided at launch)
   int n_forced;
   bool meta_mean;
   int32_t forced[PRR_MAX_FORCED];
@@ -183,6 +183,7 @@ prr_status api_ok();
 
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 hipError_t launch_empty(int grid, int threads, hipStream_t stream);
+hipError_t launch_read_stream(const void* p, size_t bytes, uint32_t* sink, int grid, hipStream_t stream);
 hipError_t launch_epoch_advance(uint32_t* epoch_dev, hipStream_t stream);
 void calibrate_grid(const float* scores, int n_traj, int n_rows, int n_blocks, const int32_t* form_row, int k_select,
                     int p_select, const float* grid, int n_grid, int n_threads, float* best_theta,
