@@ -191,32 +191,29 @@ def kernel_sweep(args):
     print(json.dumps({"sweep": "sparse attention over a selected set (Section 5.4 shape)", "table": rows}), flush=True)
 
 
+LUT_PATH = os.path.join(ROOT, "paper_2606_30389_amd", "delta_lut.json")
+
+
 def delta_sweep(args, cfg):
-    """Section 4.4's offline profiling: for each context length (a prefix of layer 0's
-    cache) and budget delta, the latency of the selection kernel, of the speculation
-    kernel over delta*|A| predicted pages, and of the fused PRR step with that budget."""
+    """Section 4.4's offline profiling on the fused PRR step (with late speculation): for
+    each context length (a prefix of layer 0's cache) and budget delta = |P| / |A|, the
+    selection window (launch start to the threshold's publication, as the select
+    workgroup stamps it) and the speculation latency (launch start to the last
+    speculation workgroup holding its pages' states), both from the launch's phase
+    timestamps, medians over tokens; plus the step's latency from HIP events."""
     import torch
     from paper_2606_30389_amd import _lib as L
     from paper_2606_30389_amd import runtime as R
+    from paper_2606_30389_amd.profile_summary import kernel_source_hash
     dev = torch.device("cuda:0")
     li = W.layer_inputs(cfg, 0)
     k = R.bits_tensor(li.k_bits, {"bf16": torch.bfloat16, "f16": torch.float16}[cfg.dtype], dev)
     v = R.bits_tensor(li.v_bits, k.dtype, dev)
-    _, qb = W.query_trajectory(cfg, 0, steps=64)
+    n_tok = 24
+    _, qb = W.query_trajectory(cfg, 0, steps=8 + 2 * n_tok + 40)
     rows = []
     s = torch.cuda.Stream(device=dev)
-    reps = 20
-
-    def timed(fn, n):
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(s)
-        for _ in range(n):
-            fn()
-        b.record(s)
-        torch.cuda.synchronize()
-        return 1000.0 * a.elapsed_time(b) / n
-
+    stamps = torch.zeros(1, 16, 1024, dtype=torch.int64, device=dev)
     contexts = [c for c in (4096, 8192, 16384, 32768, 65536, 131072) if c <= cfg.context]
     for ctx in contexts:
         for delta in (1.0, 1.25, 1.5, 2.0):
@@ -230,30 +227,78 @@ def delta_sweep(args, cfg):
             pc.max_pages = cfg.num_pages
             st = R.LayerState(pc, dev, k=k, v=v)
             st.build_meta()
-            q = R.bits_tensor(qb[0], pc.torch_dtype, dev)
+            qs = R.bits_tensor(qb, pc.torch_dtype, dev)
+            q = qs[0].clone()
             stack = R.DecodeStack([st], [q], dev)
-            stack.step(L.PRR_SCHED_FUSED_PREFILL, s)
-            for t in range(1, 5):
-                q.copy_(R.bits_tensor(qb[t], pc.torch_dtype, dev))
-                stack.step(L.PRR_SCHED_FUSED_PRR, s)
-            torch.cuda.synchronize()
-            sel_us = timed(lambda: st.select(q, stream=s), reps)
-            spec_us = timed(lambda: st.speculate(q, stream=s), reps)
-            fused_us = timed(lambda: stack.step(L.PRR_SCHED_FUSED_PRR, s), reps)
             stack.params.late_spec = 1
-            stack.step(L.PRR_SCHED_FUSED_PRR, s)
-            late_us = timed(lambda: stack.step(L.PRR_SCHED_FUSED_PRR, s), reps)
-            rows.append({"context": ctx, "delta": delta, "select_us": round(sel_us, 2), "spec_us": round(spec_us, 2),
-                         "fused_prr_us": round(fused_us, 2), "fused_prr_late_us": round(late_us, 2)})
+            t = [0]
+
+            def step():
+                q.copy_(qs[t[0]])
+                stack.step(L.PRR_SCHED_FUSED_PRR if t[0] else L.PRR_SCHED_FUSED_PREFILL, s)
+                t[0] += 1
+
+            with torch.cuda.stream(s):
+                for _ in range(8):
+                    step()
+                # roles in grid order: score, select, predict, speculation, late, missed, merge
+                H, nsc = cfg.num_kv_heads, -(-npg // 128)
+                nspec = -(-st.cap // pc.chunk_pages)
+                sel0, spec0 = H * nsc, H * (nsc + 2)
+                win, spec, hits = [], [], []
+                stack.params.phase_stamps = stamps.data_ptr()
+                for _ in range(n_tok):
+                    stamps.zero_()
+                    step()
+                    torch.cuda.synchronize()
+                    a = stamps[0].cpu().numpy()
+                    t0 = a[0][a[0] > 0].min()
+                    thr = a[4, sel0:sel0 + H]
+                    att = a[13, spec0:spec0 + H * nspec]
+                    win.append((thr.max() - t0) / 100.0)
+                    spec.append((att[att > 0].max() - t0) / 100.0 if (att > 0).any() else 0.0)
+                    hits.append(1.0 - st.missed.sum().item() / (H * cfg.selected_count))
+                stack.params.phase_stamps = None
+                torch.cuda.synchronize()
+                a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a_ev.record(s)
+                for _ in range(n_tok):
+                    step()
+                b_ev.record(s)
+            torch.cuda.synchronize()
+            rows.append({"context": ctx, "delta": delta, "select_us": round(float(np.median(win)), 2),
+                         "spec_us": round(float(np.median(spec)), 2),
+                         "fused_prr_late_us": round(1000.0 * a_ev.elapsed_time(b_ev) / n_tok, 2),
+                         "hit_rate": round(float(np.mean(hits)), 4)})
             print(f"[sweep] {rows[-1]}", file=sys.stderr, flush=True)
             del stack, st
     pick = {c: R.pick_delta(rows, c) for c in contexts}
-    out = {"sweep": "speculation budget (Section 4.4)", "workload": f"{cfg.name} layer 0, context prefixes",
+    out = {"sweep": "speculation budget (Section 4.4) on the fused PRR step with late speculation",
+           "config": cfg.name, "workload": f"{cfg.name} layer 0, context prefixes", "kernel_source": kernel_source_hash(),
            "table": rows, "picked_delta": pick}
     if args.write_lut:
         with open(args.write_lut, "w") as f:
-            json.dump({"workload": out["workload"], "table": rows}, f, indent=1)
+            json.dump({k: out[k] for k in ("sweep", "config", "workload", "kernel_source", "table")}, f, indent=1)
+            f.write("\n")
     print(json.dumps(out), flush=True)
+
+
+def auto_delta(cfg, how):
+    """delta from the committed profile of this workload at its full context: "rule" is
+    Section 4.4's rule (the largest budget whose speculation fits the selection window),
+    "auto" the fitting budget with the shortest profiled step.  1 when there is no profile.
+    Returns (delta, source, the rule's choice or None)."""
+    from paper_2606_30389_amd import runtime as R
+    if os.path.exists(LUT_PATH):
+        with open(LUT_PATH) as f:
+            lut = json.load(f)
+        if lut.get("config") == cfg.name and lut.get("table"):
+            rule = R.pick_delta(lut["table"], cfg.context)
+            if how == "rule":
+                return rule, f"Section 4.4 rule over {os.path.basename(LUT_PATH)}", rule
+            d, _ = R.pick_delta_step(lut["table"], cfg.context)
+            return d, f"fitting budget with the shortest profiled step ({os.path.basename(LUT_PATH)})", rule
+    return 1.0, "default (no profile of this workload)", None
 
 
 def late_spec_of(schedule):
@@ -407,7 +452,9 @@ def main():
                     help="also record the fused launches' phase timestamps over TOKENS tokens (medians, us from start)")
     ap.add_argument("--phases-raw", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--chunk", type=int, default=None, help="pages per speculation chunk (default 8, 4 for 64-token pages)")
-    ap.add_argument("--delta", type=float, default=1.0, help="|P| / |A| (speculation budget)")
+    ap.add_argument("--delta", default="auto",
+                    help="|P| / |A| (speculation budget); 'rule': Section 4.4's rule over the profiled table; "
+                         "'auto': of the budgets that rule allows, the one with the shortest profiled step")
     ap.add_argument("--schedules", default="fused_prr,fused_prr_late,fused_prr_late_nora,fused_serial,fused_prr_late_graph,"
                                            "two_stream,serial")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -437,7 +484,11 @@ def main():
     dev = torch.device("cuda:0")
     mode = {"exact": L.PRR_EXACT_SELECTED, "keep": L.PRR_KEEP_WASTED, "recompute": L.PRR_RECOMPUTE_ON_MISS}[args.mode]
     theta = tuple(float(x) for x in args.theta.split(",")) if args.theta else (cfg.alpha, cfg.beta, cfg.gamma)
-    p_select = int(round(args.delta * cfg.k_select))
+    if args.delta in ("auto", "rule"):
+        delta, delta_source, delta_rule = auto_delta(cfg, args.delta)
+    else:
+        delta, delta_source, delta_rule = float(args.delta), "--delta", None
+    p_select = int(round(delta * cfg.k_select))
     pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
                       num_tokens=cfg.context, k_select=cfg.k_select, forced=cfg.forced_pages(),
                       forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
@@ -725,7 +776,8 @@ def main():
         "config": {"workload": f"{cfg.name}: {n_layers} layers x ({cfg.num_q_heads} q / {cfg.num_kv_heads} kv heads, "
                                f"d {cfg.head_dim}), {cfg.dtype}, {cfg.context}-token context, page {cfg.page_size}, "
                                f"top-{cfg.k_select} pages, batch 1",
-                   "mode": args.mode, "chunk_pages": pc.chunk_pages, "serial_chunk_pages": serial_chunk, "p_select": p_select, "theta": list(theta),
+                   "mode": args.mode, "chunk_pages": pc.chunk_pages, "serial_chunk_pages": serial_chunk, "p_select": p_select, "delta": delta,
+                   "delta_source": delta_source, "delta_rule": delta_rule, "theta": list(theta),
                    "schedule": main_sched},
         "us_per_layer": {k: round(v, 3) for k, v in us.items()},
         "achieved_gbps": round(achieved, 1),

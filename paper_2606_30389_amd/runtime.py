@@ -188,6 +188,20 @@ def pick_delta(lut, context, degree=2):
     return L.prr_pick_delta(lut, context, degree)[0]
 
 
+def pick_delta_step(lut, context, degree=2):
+    """The budget among those whose speculation fits the selection window (the test of
+    pick_delta, per delta) with the shortest profiled step ("fused_prr_late_us") at this
+    context; pick_delta's choice when the context was not profiled or the rows carry no
+    step latency.  Returns (delta, step latency or None)."""
+    rows = [r for r in lut if r["context"] == context and r.get("fused_prr_late_us") is not None]
+    if not rows:
+        return pick_delta(lut, context, degree), None
+    fits = [r for r in rows if r["delta"] == 1.0 or
+            L.prr_pick_delta([x for x in lut if x["delta"] == r["delta"]], context, degree)[0] == r["delta"]]
+    best = min(fits, key=lambda r: (r["fused_prr_late_us"], r["delta"]))
+    return best["delta"], best["fused_prr_late_us"]
+
+
 _epoch = [0]
 
 

@@ -160,3 +160,26 @@ def test_runtime_pick_delta_is_the_library_call():
     L = _lib()
     lut = [{"context": c, "delta": d, "select_us": 10.0, "spec_us": 5.0 * d} for c in (4096, 65536) for d in (1.0, 2.0, 3.0)]
     assert R.pick_delta(lut, 16384) == L.prr_pick_delta(lut, 16384)[0] == 2.0
+
+
+def test_pick_delta_step_takes_the_fastest_fitting_budget():
+    """Of the budgets whose speculation fits the selection window, the one with the
+    shortest profiled step; a budget that does not fit is never taken, however fast; an
+    unprofiled context falls back to the Section 4.4 rule."""
+    try:
+        from paper_2606_30389_amd import runtime as R
+    except ImportError as e:
+        pytest.skip(f"libprr not built: {e}")
+    rows = [
+        {"context": 4096, "delta": 1.0, "select_us": 8.0, "spec_us": 4.0, "fused_prr_late_us": 16.0},
+        {"context": 4096, "delta": 1.5, "select_us": 8.0, "spec_us": 5.0, "fused_prr_late_us": 15.0},
+        {"context": 4096, "delta": 2.0, "select_us": 8.0, "spec_us": 9.0, "fused_prr_late_us": 14.0},
+        {"context": 8192, "delta": 1.0, "select_us": 8.0, "spec_us": 4.0, "fused_prr_late_us": 16.0},
+        {"context": 8192, "delta": 1.5, "select_us": 8.0, "spec_us": 5.0, "fused_prr_late_us": 17.0},
+        {"context": 8192, "delta": 2.0, "select_us": 8.0, "spec_us": 6.0, "fused_prr_late_us": 18.0},
+    ]
+    assert R.pick_delta_step(rows, 4096) == (1.5, 15.0)  # delta 2 is faster but does not fit
+    assert R.pick_delta_step(rows, 8192) == (1.0, 16.0)  # the rule would take 2
+    assert R.pick_delta(rows, 8192) == 2.0
+    d, us = R.pick_delta_step(rows, 6000)
+    assert us is None and d == R.pick_delta(rows, 6000)
