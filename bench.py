@@ -146,12 +146,13 @@ def cpu_baseline(cfg, budget_s, threads=1):
 
 
 def kernel_sweep(args):
-    """Attention over a given selected set (the serial repair call: attend every page of A,
-    merge) on the kernel-comparison shape of Section 5.4: 32 query / 8 KV heads, head_dim
-    128, a 131072-token fp16 cache, pages of 16 and 64 tokens, budgets of 1K to 8K tokens
-    drawn uniformly per KV head.  Reports microseconds per call and GB/s of selected K/V."""
+    """Section 5.4's kernel comparison shape: 32 query / 8 KV heads, head_dim 128, a
+    131072-token fp16 cache, blocks (pages) of 16 to 256 tokens, budgets of 1K to 8K tokens
+    (a random sorted set of budget / page pages per KV head).  Times attention over the set
+    two ways -- the serial repair call (attend every page, merge: one launch) and the
+    speculation kernel alone (partial states per chunk) -- and reports microseconds per
+    call and GB/s of selected K/V."""
     import torch
-    from paper_2606_30389_amd import _lib as L
     from paper_2606_30389_amd import runtime as R
     dev = torch.device("cuda:0")
     hq, hkv, d, ctx = 32, 8, 128, 131072
@@ -161,33 +162,49 @@ def kernel_sweep(args):
     q = torch.randn(hq * d, generator=gen, dtype=torch.float32).to(torch.float16).to(dev)
     s = torch.cuda.Stream(device=dev)
     rows = []
-    for ps in (16, 64):
+
+    def timed(fn, n=50):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(n):
+            fn()
+        b.record(s)
+        torch.cuda.synchronize()
+        return 1000.0 * a.elapsed_time(b) / n
+
+    for ps in (16, 32, 64, 128, 256):
         npg = ctx // ps
         for budget in (1024, 2048, 4096, 6144, 8192):
             kk = budget // ps
-            pc = R.PathConfig(num_q_heads=hq, num_kv_heads=hkv, page_size=ps, num_tokens=ctx, k_select=kk,
-                              forced=[], forced_in_budget=True, dtype="f16", meta_kind="minmax",
-                              chunk_pages=min(8, 256 // ps))
-            st = R.LayerState(pc, dev, k=k.view(hkv, npg, ps, d), v=v.view(hkv, npg, ps, d))
             sel = np.stack([np.sort(np.random.default_rng(7 + h).choice(npg, kk, replace=False)) for h in range(hkv)])
-            st.sel[:, :kk].copy_(torch.from_numpy(sel.astype(np.int32)))
-            st.sel_count.fill_(kk)
-            for _ in range(3):
-                st.repair(q, stream=s, serial=True)
-            torch.cuda.synchronize()
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            n = 50
-            a.record(s)
-            for _ in range(n):
-                st.repair(q, stream=s, serial=True)
-            b.record(s)
-            torch.cuda.synchronize()
-            us = 1000.0 * a.elapsed_time(b) / n
+            best = None
+            # the pages per workgroup (chunk) is a launch parameter: every allowed value is
+            # timed and the fastest kept (small budgets want more, smaller chunks)
+            for chunk in (c for c in (1, 2, 4, 8, 16) if c * ps <= 256 and c <= kk):
+                pc = R.PathConfig(num_q_heads=hq, num_kv_heads=hkv, page_size=ps, num_tokens=ctx, k_select=kk,
+                                  forced=[], forced_in_budget=True, dtype="f16", meta_kind="minmax", chunk_pages=chunk)
+                st = R.LayerState(pc, dev, k=k.view(hkv, npg, ps, d), v=v.view(hkv, npg, ps, d))
+                st.sel[:, :kk].copy_(torch.from_numpy(sel.astype(np.int32)))
+                st.sel_count.fill_(kk)
+                us = timed(lambda: st.repair(q, stream=s, serial=True))
+                spec_us = timed(lambda: st.speculate(q, stream=s, pages=st.sel, counts=st.sel_count))
+                if best is None:
+                    best = dict(chunk_us=chunk, us=us, chunk_spec=chunk, spec_us=spec_us)
+                if us < best["us"]:
+                    best.update(chunk_us=chunk, us=us)
+                if spec_us < best["spec_us"]:
+                    best.update(chunk_spec=chunk, spec_us=spec_us)
+                del st
             kv_bytes = hkv * budget * d * 2 * 2
-            rows.append({"page": ps, "budget_tokens": budget, "us": round(us, 2),
-                         "gbps": round(kv_bytes / (us * 1e-6) / 1e9, 1)})
+            rows.append({"page": ps, "budget_tokens": budget, "us": round(best["us"], 2),
+                         "gbps": round(kv_bytes / (best["us"] * 1e-6) / 1e9, 1), "chunk": best["chunk_us"],
+                         "spec_us": round(best["spec_us"], 2),
+                         "spec_gbps": round(kv_bytes / (best["spec_us"] * 1e-6) / 1e9, 1),
+                         "spec_chunk": best["chunk_spec"]})
             print(f"[kernel-sweep] {rows[-1]}", file=sys.stderr, flush=True)
-            del st
     print(json.dumps({"sweep": "sparse attention over a selected set (Section 5.4 shape)", "table": rows}), flush=True)
 
 
@@ -436,8 +453,8 @@ def main():
                          "latency per context length and delta, and the fused PRR step; prints the table")
     ap.add_argument("--write-lut", default=None, metavar="PATH", help="with --delta-sweep: also write the table as JSON")
     ap.add_argument("--kernel-sweep", action="store_true",
-                    help="only the sparse-attention kernel sweep (Section 5.4, Table tab:kernel_table shape: 32 q / 8 kv heads, d 128, 128K "
-                         "context, page 16 and 64, budget 1K-8K tokens): microseconds and GB/s")
+                    help="only the sparse-attention kernel sweep (the shape of Section 5.4's kernel table: 32 q / 8 kv "
+                         "heads, d 128, 128K context, pages of 16-256 tokens, budget 1K-8K tokens): microseconds and GB/s")
     ap.add_argument("--calibrate", type=int, default=0, metavar="ROWS",
                     help="calibrate theta (Section 4.2) on ROWS prefill score rows of the first 4 layers, then "
                          "time the fused PRR step with it")

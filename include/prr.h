@@ -75,7 +75,8 @@ typedef int32_t prr_status;
 
 /* Shape of one layer's paged KV cache.
  *   head_dim   128 (the only compiled value)
- *   page_size  16 or 64 tokens
+ *   page_size  16, 32, 64, 128 or 256 tokens (the fused schedules of prr_decode_step: 16
+ *              or 64; other sizes give PRR_ERR_UNSUPPORTED there)
  *   max_pages  page slots per KV head in the cache; also the row stride of per-page arrays
  *   dtype      PRR_F16 or PRR_BF16, for q, keys, values, min/max metadata and out_o
  *   meta_kind  PRR_META_MINMAX or PRR_META_MEAN
@@ -193,7 +194,8 @@ prr_status prr_predict(const prr_dims* dims, float* ema_level, float* ema_trend,
  *   num_tokens   tokens in the cache (masks a partial last page)
  *   pages        device [Hkv][cap] int32 list (normally P), page_count device [Hkv] int32
  *   chunk_pages  C, 1 <= C <= 256 / page_size (16 for 16-token pages, 4 for 64-token
- *                pages): consecutive list entries [cC, cC+C) form chunk c
+ *                pages, 1 for 256-token pages): consecutive list entries [cC, cC+C)
+ *                form chunk c
  *   part_o       device [Hkv][ceil(cap/C)][G][128] float32 out: normalised o of each chunk
  *   part_m, part_l device [Hkv][ceil(cap/C)][G] float32 out
  *   page_m       device [Hkv][cap][G] float32 out: max scaled logit of each listed page,
@@ -317,8 +319,9 @@ typedef struct {
  * merge) and hand results to each other inside the launch, so selection and speculation
  * overlap without a second stream.  In the fused PRR step the speculation keeps one
  * softmax state per page of P and folds only the pages that turn out to be in A, so
- * PRR_EXACT_SELECTED needs no recomputation.  Fused schedules need num_pages <= 8192,
- * p_select <= cap, and use the fused region of the workspace (prr_workspace_size). */
+ * PRR_EXACT_SELECTED needs no recomputation.  Fused schedules need page_size 16 or 64,
+ * num_pages <= 8192, p_select <= cap, and use the fused region of the workspace
+ * (prr_workspace_size). */
 #define PRR_SCHED_FUSED_SERIAL 3
 #define PRR_SCHED_FUSED_PRR 4
 #define PRR_SCHED_FUSED_PREFILL 5

@@ -43,8 +43,8 @@ bool chunk_ok(const prr_dims* d, int chunk) { return chunk >= 1 && chunk * (d->p
 prr_status check_dims(const prr_dims* d) {
   if (!d) return fail(PRR_ERR_INVALID_ARG, "dims is NULL");
   if (d->head_dim != 128) return fail(PRR_ERR_UNSUPPORTED, "head_dim %d: only 128 is compiled", d->head_dim);
-  if (d->page_size != 16 && d->page_size != 64)
-    return fail(PRR_ERR_UNSUPPORTED, "page_size %d: only 16 and 64 are compiled", d->page_size);
+  if (d->page_size != 16 && d->page_size != 32 && d->page_size != 64 && d->page_size != 128 && d->page_size != 256)
+    return fail(PRR_ERR_UNSUPPORTED, "page_size %d: only 16, 32, 64, 128 and 256 are compiled", d->page_size);
   if (d->num_kv_heads < 1) return fail(PRR_ERR_INVALID_ARG, "num_kv_heads %d < 1", d->num_kv_heads);
   if (d->num_q_heads < 1 || d->num_q_heads % d->num_kv_heads != 0)
     return fail(PRR_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d", d->num_q_heads,
@@ -237,7 +237,8 @@ prr_status prr_read_stream(const void* buf, size_t bytes, uint32_t* sink, int32_
 }
 
 int32_t prr_fused_grid(const prr_dims* dims, const prr_step_params* sp, int32_t schedule) {
-  if (check_dims(dims) != PRR_OK || !sp || schedule < PRR_SCHED_FUSED_SERIAL || schedule > PRR_SCHED_FUSED_PREFILL)
+  if (check_dims(dims) != PRR_OK || !sp || schedule < PRR_SCHED_FUSED_SERIAL || schedule > PRR_SCHED_FUSED_PREFILL ||
+      (dims->page_size != 16 && dims->page_size != 64))
     return 0;
   WsLayout L;
   if (!ws_layout(dims, sp->cap, sp->chunk_pages, L) || sp->num_pages < 1) return 0;
@@ -705,6 +706,8 @@ prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* sp, cons
   if (schedule < PRR_SCHED_SERIAL || schedule > PRR_SCHED_FUSED_PREFILL)
     return fail(PRR_ERR_INVALID_ARG, "schedule %d", schedule);
   if (schedule >= PRR_SCHED_FUSED_SERIAL) {
+    if (dims->page_size != 16 && dims->page_size != 64)
+      return fail(PRR_ERR_UNSUPPORTED, "page_size %d: the fused schedules are compiled for 16 and 64", dims->page_size);
     if (sp->phase_stamps && !aligned(sp->phase_stamps, 8)) return fail(PRR_ERR_INVALID_ARG, "phase_stamps misaligned");
     for (int l = 0; l < n_layers; ++l) PRR_TRY(fused_layer(dims, sp, layers[l], parity, schedule, stream, l));
     return ok();

@@ -193,6 +193,31 @@ __global__ __launch_bounds__(256) void meta_mean_kernel(const uint16_t* __restri
   }
 }
 
+// The instance of a kernel template for a page size (16, 32, 64, 128 or 256 tokens), or
+// NULL for another size (the C ABI admits only these).
+template <typename K>
+const void* by_page_size(int ps) {
+  switch (ps) {
+    case 16: return K::template get<16>();
+    case 32: return K::template get<32>();
+    case 64: return K::template get<64>();
+    case 128: return K::template get<128>();
+    case 256: return K::template get<256>();
+    default: return nullptr;
+  }
+}
+
+template <bool BF16>
+struct MetaMeanK {
+  template <int PS>
+  static const void* get() { return (const void*)meta_mean_kernel<BF16, PS>; }
+};
+template <bool BF16>
+struct MetaMinmaxK {
+  template <int PS>
+  static const void* get() { return (const void*)meta_minmax_kernel<BF16, PS>; }
+};
+
 hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream) {
   const int np = a.page_end - a.page_begin;
   if (np <= 0) return hipSuccess;
@@ -202,14 +227,10 @@ hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream) {
   int nt = a.num_tokens, pb = a.page_begin, pe = a.page_end, mp = a.max_pages;
   void* meta = a.meta;
   void* args[] = {&k, &ptab, &nt, &pb, &pe, &mp, &meta};
-  const void* f;
-  if (a.meta_mean) {
-    f = a.bf16 ? (a.page_size == 16 ? (const void*)meta_mean_kernel<true, 16> : (const void*)meta_mean_kernel<true, 64>)
-               : (a.page_size == 16 ? (const void*)meta_mean_kernel<false, 16> : (const void*)meta_mean_kernel<false, 64>);
-  } else {
-    f = a.bf16 ? (a.page_size == 16 ? (const void*)meta_minmax_kernel<true, 16> : (const void*)meta_minmax_kernel<true, 64>)
-               : (a.page_size == 16 ? (const void*)meta_minmax_kernel<false, 16> : (const void*)meta_minmax_kernel<false, 64>);
-  }
+  const void* f = a.meta_mean ? (a.bf16 ? by_page_size<MetaMeanK<true>>(a.page_size) : by_page_size<MetaMeanK<false>>(a.page_size))
+                              : (a.bf16 ? by_page_size<MetaMinmaxK<true>>(a.page_size)
+                                        : by_page_size<MetaMinmaxK<false>>(a.page_size));
+  if (!f) return hipErrorInvalidValue;
   return hipLaunchKernel(f, grid, dim3(256), args, 0, stream);
 }
 
@@ -643,6 +664,7 @@ struct UnitLds {
   float wo[4][16][kOPad];
   float wm[4][16];
   float wl[4][16];
+  float wpm[4][16];  // per-wave page maxima (pages of 128 and 256 tokens span several waves)
 };
 
 template <bool BF16>
@@ -668,12 +690,18 @@ struct UnitResult {
   float m, l;
 };
 
+// A unit is at most 16 tiles of 16 tokens, four per wave.  Pages of up to 64 tokens are
+// whole to one wave (list entries w, w + 4, .. for wave w); a page of 128 or 256 tokens
+// spans WPP = 2 or 4 waves (entry w / WPP, tiles 4 (w % WPP) .. + 3).
 template <bool BF16, int PS>
 __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, float* page_m_out, UnitLds& sm,
                             uint32_t* flags, UnitResult& res) {
+  static_assert(PS == 16 || PS == 32 || PS == 64 || PS == 128 || PS == 256, "page size");
   constexpr int TPP = PS / 16;
   constexpr int NTL = 16 / 4;  // tiles per wave at most (16 tiles per unit)
-  constexpr int NPW = (NTL + TPP - 1) / TPP;  // list entries per wave at most
+  constexpr int NPW = TPP <= NTL ? NTL / TPP : 1;  // list entries per wave at most
+  constexpr int WPP = TPP <= NTL ? 1 : TPP / NTL;  // waves per page
+  constexpr int TW = TPP <= NTL ? NPW * TPP : NTL;  // tiles of one wave
   const float kNegInf = -__builtin_inff();
   const float scale = 0.08838834764831845f;  // 1/sqrt(128)
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
@@ -690,18 +718,19 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
     for (int s = 0; s < 4; ++s) qf[s] = u32x4_t{0, 0, 0, 0};
   }
 
-  // list entries w, w+4, ..: ids first, then page-table entries (wave-uniform values)
+  // list entries w, w+4, .. (or w / WPP): ids first, then page-table entries (wave-uniform values)
   const int wu = __builtin_amdgcn_readfirstlane(w);
+  const int e0 = wu / WPP, tt0 = (wu % WPP) * NTL;  // (0 when a page is whole to a wave)
   int pg[NPW], ph[NPW];
 #pragma unroll
   for (int kk = 0; kk < NPW; ++kk) {
-    const int i = wu + 4 * kk;
+    const int i = WPP == 1 ? wu + 4 * kk : e0;
     pg[kk] = i < cnt ? pages[i] : -1;
   }
 #pragma unroll
   for (int kk = 0; kk < NPW; ++kk) {
     pg[kk] = __builtin_amdgcn_readfirstlane(pg[kk]);
-    const bool in_list = (wu + 4 * kk) < cnt;
+    const bool in_list = (WPP == 1 ? wu + 4 * kk : e0) < cnt;
     const bool valid = pg[kk] >= 0 && pg[kk] < c.num_pages;
     if (in_list && !valid && flags && lane == 0) atomicOr(flags, kFlagBadListEntry);
     if (!valid) pg[kk] = -1;
@@ -728,8 +757,8 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
   // every tile of the wave is loaded up front (at most 4 tiles: 32 registers each)
   u32x4_t kf[NTL][4], vf[NTL][4];
 #pragma unroll
-  for (int f = 0; f < NPW * TPP; ++f) {
-    const int kk = f / TPP, tt = f % TPP;
+  for (int f = 0; f < TW; ++f) {
+    const int kk = WPP == 1 ? f / TPP : 0, tt = WPP == 1 ? f % TPP : tt0 + f;
     if (ok[kk]) {
       const uint16_t* kt = c.k + off[kk] + (size_t)tt * 16 * kHeadDim;
       const uint16_t* vt = c.v + off[kk] + (size_t)tt * 16 * kHeadDim;
@@ -742,12 +771,12 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
     }
   }
 
-  float pm = kNegInf;  // max logit of the current page, head n
+  float pm = kNegInf;  // max logit of the current page (this wave's tiles of it), head n
 #pragma unroll
-  for (int f = 0; f < NPW * TPP; ++f) {
-    const int kk = f / TPP, tt = f % TPP;
+  for (int f = 0; f < TW; ++f) {
+    const int kk = WPP == 1 ? f / TPP : 0, tt = WPP == 1 ? f % TPP : tt0 + f;
     if (!ok[kk]) continue;
-    if (tt == 0) pm = kNegInf;
+    if (WPP == 1 && tt == 0) pm = kNegInf;
     f32x4_t st = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 4; ++s) st = mfma_qk<BF16>(kf[f][s], qf[s], st);
@@ -790,7 +819,10 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
       for (int cb = 0; cb < 8; ++cb)
         acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(v_elem<BF16>(vf[f][tg], cb), p[tg], acc[cb], 0, 0, 0);
     }
-    if (tt == TPP - 1 && page_m_out && j == 0 && n < G) page_m_out[(size_t)(w + 4 * kk) * G + n] = pm;
+    if (WPP == 1 && tt == TPP - 1 && page_m_out && j == 0 && n < G) page_m_out[(size_t)(w + 4 * kk) * G + n] = pm;
+  }
+  if constexpr (WPP > 1) {
+    if (j == 0) sm.wpm[w][n] = pm;
   }
 
   // merge the four wave states: lane 16j+n holds channels 32j + 8i + cb of head n
@@ -805,6 +837,16 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
     *reinterpret_cast<float4*>(row + 8 * i + 4) = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
   }
   __syncthreads();
+  if constexpr (WPP > 1) {
+    // page e's maximum over its waves (thread e * 16 + head)
+    const int e = t >> 4, hd = t & 15;
+    if (page_m_out && e < 4 / WPP && e < cnt && hd < G) {
+      float m = kNegInf;
+#pragma unroll
+      for (int x = 0; x < WPP; ++x) m = fmaxf(m, sm.wpm[e * WPP + x][hd]);
+      page_m_out[(size_t)e * G + hd] = m;
+    }
+  }
   const int hh = t >> 4, c0 = (t & 15) * 8;
   float mw[4], fw[4];
   float ms = kNegInf;
@@ -1371,17 +1413,28 @@ hipError_t launch_predict(const PredictLaunch& a, hipStream_t stream) {
   return launch1((const void*)predict_kernel, dim3(a.num_kv_heads), dim3(kSelThreads), 0, stream, a);
 }
 
+template <bool BF16>
+struct SpecK {
+  template <int PS>
+  static const void* get() { return (const void*)spec_attn_kernel<BF16, PS>; }
+};
+template <bool BF16>
+struct RepairK {
+  template <int PS>
+  static const void* get() { return (const void*)repair_kernel<BF16, PS>; }
+};
+
 hipError_t launch_spec_attn(const SpecLaunch& a, hipStream_t stream) {
   dim3 grid(a.nchunks, a.num_kv_heads);
-  const void* f = a.bf16 ? (a.page_size == 16 ? (const void*)spec_attn_kernel<true, 16> : (const void*)spec_attn_kernel<true, 64>)
-                         : (a.page_size == 16 ? (const void*)spec_attn_kernel<false, 16> : (const void*)spec_attn_kernel<false, 64>);
+  const void* f = a.bf16 ? by_page_size<SpecK<true>>(a.page_size) : by_page_size<SpecK<false>>(a.page_size);
+  if (!f) return hipErrorInvalidValue;
   return launch1(f, grid, dim3(256), 0, stream, a);
 }
 
 hipError_t launch_repair(const RepairLaunch& a, hipStream_t stream) {
   const int grid = a.num_kv_heads * (a.nwork + a.nmerge_per_kv);
-  const void* f = a.bf16 ? (a.page_size == 16 ? (const void*)repair_kernel<true, 16> : (const void*)repair_kernel<true, 64>)
-                         : (a.page_size == 16 ? (const void*)repair_kernel<false, 16> : (const void*)repair_kernel<false, 64>);
+  const void* f = a.bf16 ? by_page_size<RepairK<true>>(a.page_size) : by_page_size<RepairK<false>>(a.page_size);
+  if (!f) return hipErrorInvalidValue;
   return launch1(f, dim3(grid), dim3(256), 0, stream, a);
 }
 

@@ -64,7 +64,7 @@ def _expect(P, status, fn, *args, **kwargs):
 
 
 @pytest.mark.parametrize("field,value,status", [
-    ("head_dim", 64, 2), ("page_size", 32, 2), ("num_kv_heads", 0, 1), ("num_q_heads", 33, 1),
+    ("head_dim", 64, 2), ("page_size", 48, 2), ("page_size", 512, 2), ("num_kv_heads", 0, 1), ("num_q_heads", 33, 1),
     ("num_q_heads", 34, 2), ("max_pages", 0, 1), ("dtype", 5, 1), ("meta_kind", 3, 1)])
 def test_bad_dims(P, field, value, status):
     kw = dict(num_q_heads=32, num_kv_heads=2, page_size=16, max_pages=100, dtype=P.PRR_BF16)
@@ -187,3 +187,21 @@ def test_fused_step_rejects_bad_stamps_and_epoch(P):
 
     _expect(P, 1, P.prr_decode_step, d, params(stamps=FAKE + 4), layers, 0, P.PRR_SCHED_FUSED_PRR)
     _expect(P, 1, P.prr_decode_step, d, params(epoch=0), layers, 0, P.PRR_SCHED_FUSED_PRR)
+    bad_late = params()
+    bad_late.late_spec = 3
+    _expect(P, 1, P.prr_decode_step, d, bad_late, layers, 0, P.PRR_SCHED_FUSED_PRR)
+    assert P.prr_fused_grid(d, params(), P.PRR_SCHED_FUSED_PRR) > 0
+
+
+@pytest.mark.parametrize("ps", [32, 128, 256])
+def test_fused_schedules_need_page_16_or_64(P, ps):
+    """The separate kernels take pages of 16 to 256 tokens; the fused schedules only 16
+    and 64 (PRR_ERR_UNSUPPORTED before any launch)."""
+    d = P.make_dims(32, 8, ps, 64, P.PRR_F16)
+    assert P.prr_workspace_size(d, 8, 1) > 0
+    p = P.prr_step_params()
+    p.num_tokens, p.num_pages, p.k_select, p.p_select, p.cap, p.chunk_pages, p.epoch = 64 * ps, 64, 8, 8, 8, 1, 1
+    layers = (P.prr_layer_io * 1)()
+    for sched in (P.PRR_SCHED_FUSED_SERIAL, P.PRR_SCHED_FUSED_PRR, P.PRR_SCHED_FUSED_PREFILL):
+        _expect(P, 2, P.prr_decode_step, d, p, layers, 0, sched)
+        assert P.prr_fused_grid(d, p, sched) == 0
