@@ -318,6 +318,88 @@ def auto_delta(cfg, how):
     return 1.0, "default (no profile of this workload)", None
 
 
+def causal_calibration(args, cfg, pc, layers, s, dev, L, R, torch):
+    """Section 4.2 on a causal prefill trajectory, per layer, overlapped with the GPU.
+
+    Rows are the last ROWS prefill tokens STRIDE tokens apart (args.calibrate_stride; 1 =
+    consecutive tokens, like decode steps; page_size = one block forms per row), each
+    scoring only the blocks formed by its position; the scores come
+    from the library's selection kernel on the GPU (the prefill stand-in), are copied to
+    pinned host memory, and each layer's grid search (prr_calibrate, all host threads)
+    starts as soon as that layer's rows are on the host, while the GPU scores the next
+    layers.  The search of the last layer cannot overlap with prefill: its time is the
+    non-overlapped tail (the appendix "Search and Prediction Cost")."""
+    import threading
+    rows, stride, nb, ps = args.calibrate, args.calibrate_stride, cfg.num_pages, cfg.page_size
+    hkv, n_layers = cfg.num_kv_heads, len(layers)
+    pos = [cfg.context - (rows - 1 - r) * stride for r in range(rows)]  # tokens up to and incl. row r
+    formed = [min(nb, p // ps) for p in pos]
+    # the row at which each block forms (rows: never, within the trajectory)
+    born = np.array([next(r for r in range(rows) if formed[r] > b) if b < formed[-1] else rows
+                     for b in range(nb)], dtype=np.int32)
+    grid = np.asarray(R.THETA_GRID, dtype=np.float32)
+    host = torch.zeros((n_layers, hkv, rows, nb), dtype=torch.float32, pin_memory=True)
+    dev_scores = torch.zeros((rows, hkv, layers[0].dims.max_pages), dtype=torch.float32, device=dev)
+    sel = torch.zeros((hkv, layers[0].cap), dtype=torch.int32, device=dev)
+    sel_n = torch.zeros(hkv, dtype=torch.int32, device=dev)
+    qs = [R.bits_tensor(W.prefill_trajectory(cfg, l, rows, stride), pc.torch_dtype, dev) for l in range(n_layers)]
+    events = [torch.cuda.Event() for _ in range(n_layers)]
+    ready, done, gpu_ms = [0.0] * n_layers, [0.0] * n_layers, []
+    thetas, objective = [None] * n_layers, [0.0] * n_layers
+    nthreads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+
+    def search():
+        for l in range(n_layers):
+            events[l].synchronize()
+            ready[l] = time.perf_counter()
+            traj = host[l].numpy()
+            best, obj = L.prr_calibrate(traj, cfg.k_select, grid, p_select=pc.p_select or cfg.k_select,
+                                        n_threads=nthreads, form_row=born)
+            thetas[l], objective[l] = tuple(float(x) for x in best), float(obj.max())
+            done[l] = time.perf_counter()
+
+    worker = threading.Thread(target=search)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    worker.start()
+    for l, st in enumerate(layers):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(s):
+            a.record(s)
+            for r in range(rows):
+                fc = cfg.forced_pages(formed[r])
+                L.prr_score_topk(st.dims, qs[l][r], st.meta, formed[r], cfg.k_select, fc, cfg.forced_in_budget,
+                                 dev_scores[r], sel, sel_n, st.cap, st.workspace, st.ws_bytes, s)
+            b.record(s)
+            host[l].copy_(dev_scores[:, :, :nb].transpose(0, 1), non_blocking=True)
+            events[l].record(s)
+        gpu_ms.append((a, b))
+    events[-1].synchronize()
+    t_gpu = time.perf_counter()
+    worker.join()
+    t_end = time.perf_counter()
+    per_layer_gpu = [a.elapsed_time(b) for a, b in gpu_ms]
+    search_ms = [1000.0 * (done[l] - max(ready[l], done[l - 1] if l else 0.0)) for l in range(n_layers)]
+    hist = {}
+    for th in thetas:
+        key = ",".join(f"{x:.2f}" for x in th)
+        hist[key] = hist.get(key, 0) + 1
+    return {
+        "rows": rows, "row_stride_tokens": stride, "layers": n_layers, "blocks_forming_in_trajectory": int(nb - formed[0]),
+        "host_threads": nthreads, "grid_points": len(grid),
+        "search_ms_per_layer": {"median": round(float(np.median(search_ms)), 2), "max": round(max(search_ms), 2)},
+        "gpu_prefill_standin_ms_per_layer": round(float(np.median(per_layer_gpu)), 3),
+        "non_overlapped_tail_ms": round(search_ms[-1], 2),
+        "search_total_ms": round(sum(search_ms), 1),
+        "wall_ms_after_gpu_done": round(1000.0 * (t_end - t_gpu), 1),
+        "wall_ms": round(1000.0 * (t_end - t0), 1),
+        "objective_median": round(float(np.median(objective)), 5),
+        "theta_histogram": dict(sorted(hist.items(), key=lambda kv: -kv[1])),
+        "_thetas": thetas,
+    }
+
+
 def late_spec_of(schedule):
     """prr_step_params.late_spec of a schedule label: fused_prr_late* speculate late pages
     (with the read-ahead; *_nora without it)."""
@@ -455,9 +537,12 @@ def main():
     ap.add_argument("--kernel-sweep", action="store_true",
                     help="only the sparse-attention kernel sweep (the shape of Section 5.4's kernel table: 32 q / 8 kv "
                          "heads, d 128, 128K context, pages of 16-256 tokens, budget 1K-8K tokens): microseconds and GB/s")
-    ap.add_argument("--calibrate", type=int, default=0, metavar="ROWS",
-                    help="calibrate theta (Section 4.2) on ROWS prefill score rows of the first 4 layers, then "
-                         "time the fused PRR step with it")
+    ap.add_argument("--calibrate", type=int, default=64, metavar="ROWS",
+                    help="calibrate theta per layer (Section 4.2) on a causal prefill trajectory of ROWS rows, "
+                         "overlapped with the GPU; then compare hit rate and step time with the default theta "
+                         "(0 = skip)")
+    ap.add_argument("--calibrate-stride", type=int, default=1, metavar="TOKENS",
+                    help="tokens between the calibration rows (1: consecutive, as decode steps are)")
     ap.add_argument("--ablation", action="store_true",
                     help="also time the ablation stages S1 (reuse the previous top-K, recompute on a miss), "
                          "S2 (reuse + repair) and S3 (EMA + repair) with the fused PRR schedule")
@@ -652,39 +737,23 @@ def main():
         run(1, L.PRR_SCHED_FUSED_PREFILL)
     calibration = None
     if args.calibrate > 1:
-        # prefill trajectories: scores of the last ROWS prefill queries (the block of the
-        # current position forms as the prompt grows), scored by the select kernel
-        rows, n_cal = args.calibrate, min(4, n_layers)
-        nb = cfg.num_pages
-        traj = np.zeros((n_cal, cfg.num_kv_heads, rows, nb), dtype=np.float32)
-        for l in range(n_cal):
-            qb = R.bits_tensor(W.prefill_trajectory(cfg, l, rows), pc.torch_dtype, dev)
-            st = layers[l]
-            for r in range(rows):
-                st.select(qb[r], stream=s)
-                torch.cuda.synchronize()
-                pos = cfg.context - (rows - 1 - r)  # tokens up to and including this position
-                formed = min(nb, pos // cfg.page_size)
-                traj[l, :, r, :formed] = st.scores[:, :formed].float().cpu().numpy()
-        t_cal = time.perf_counter()
-        grid = np.asarray(R.THETA_GRID, dtype=np.float32)
-        best, obj = L.prr_calibrate(traj.reshape(-1, rows, nb), cfg.k_select, grid, p_select=p_select)
-        host_ms = 1000.0 * (time.perf_counter() - t_cal)
+        calibration = causal_calibration(args, cfg, pc, layers, s, dev, L, R, torch)
+        thetas = calibration.pop("_thetas")
         default_theta = (stack.params.alpha, stack.params.beta, stack.params.gamma)
-        calibration = {"rows": rows, "layers": n_cal, "theta": [round(x, 3) for x in best],
-                       "objective": round(float(obj.max()), 5), "host_ms": round(host_ms, 1),
-                       "host_threads": os.cpu_count()}
-        for name, th in (("default", default_theta), ("calibrated", best)):
-            stack.params.alpha, stack.params.beta, stack.params.gamma = th
+        for name, th in (("default", None), ("calibrated", thetas)):
+            stack.set_layer_theta(th)
             for st in layers:
                 st.init_bits.zero_()
             torch.cuda.synchronize()
             run(1, L.PRR_SCHED_FUSED_PREFILL)
             h = run(max(4, args.warmup), L.PRR_SCHED_FUSED_PRR, measure_hits=True)
             calibration[f"hit_rate_{name}"] = round(float(np.mean(h)), 4)
+            stack.params.late_spec = 1
             calibration[f"us_per_layer_{name}"] = round(
                 1000.0 * timed(args.steps, L.PRR_SCHED_FUSED_PRR) / n_layers, 3)
-        stack.params.alpha, stack.params.beta, stack.params.gamma = default_theta
+            stack.params.late_spec = 0
+        calibration["default_theta"] = [round(float(x), 3) for x in default_theta]
+        stack.set_layer_theta(None)
         for st in layers:
             st.init_bits.zero_()
         run(1, L.PRR_SCHED_FUSED_PREFILL)

@@ -266,6 +266,10 @@ typedef struct {
   size_t ws_bytes;
   int32_t* covered_count;      /* or NULL: [Hkv] pages of A \ P attended by late speculation
                                   (fused PRR schedule; 0 otherwise) */
+  const float* theta;          /* or NULL: HOST [3] (alpha, beta, gamma) of this layer's EMA
+                                  predictor (Section 4.2 calibrates one per layer), in place of
+                                  the step's; read when the call is made (a captured graph keeps
+                                  the values of capture time); same ranges as the step's */
 } prr_layer_io;
 
 /* Per-step parameters shared by the layers. */
@@ -303,11 +307,11 @@ typedef struct {
                                   candidate lists stored; 3 candidates gathered; 4 threshold
                                   published; 5 missed count published; 6, 7, 8 a speculation,
                                   late or missed-page state published; 9 an output row written;
-                                  10 select done; 11 next prediction written; 12 end; 13 an
-                                  attending workgroup's page states computed; 14 a late
-                                  workgroup holds its list.  One
-                                  plain store per entry.  Grids above 1024 workgroups give
-                                  PRR_ERR_UNSUPPORTED. */
+                                  10 select done; 11 next prediction written; 12 the
+                                  workgroup's last wave ended; 13 an attending workgroup's page
+                                  states computed; 14 a late workgroup holds its list.  One
+                                  plain store per entry (12: an atomic maximum per wave).
+                                  Grids above 1024 workgroups give PRR_ERR_UNSUPPORTED. */
 } prr_step_params;
 
 #define PRR_SCHED_SERIAL 0     /* per layer: select, then attend every page of A (one stream) */

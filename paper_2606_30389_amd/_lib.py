@@ -72,6 +72,7 @@ class prr_layer_io(ctypes.Structure):
         ("out_m", ctypes.c_void_p), ("out_l", ctypes.c_void_p), ("missed_count", ctypes.c_void_p),
         ("wasted_count", ctypes.c_void_p), ("workspace", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t),
         ("covered_count", ctypes.c_void_p),
+        ("theta", ctypes.c_void_p),
     ]
 
 

@@ -4,10 +4,17 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <stddef.h>
+
 #include <algorithm>
 
 #include "prr.h"
 #include "prr_launch.h"
+
+// (alpha, beta, gamma) of the step parameters are read as one float[3]
+static_assert(offsetof(prr_step_params, beta) == offsetof(prr_step_params, alpha) + sizeof(float) &&
+                  offsetof(prr_step_params, gamma) == offsetof(prr_step_params, alpha) + 2 * sizeof(float),
+              "alpha, beta, gamma are consecutive");
 
 namespace {
 
@@ -134,6 +141,13 @@ prr_status check_forced(const int32_t* forced, int n_forced, int num_pages) {
     for (int j = 0; j < i; ++j)
       if (forced[j] == forced[i]) return fail(PRR_ERR_INVALID_ARG, "forced page %d listed twice", forced[i]);
   }
+  return ok();
+}
+
+// (alpha, beta, gamma) of the EMA predictor in (0, 1], (0, 1], [0, 1].
+prr_status check_theta(const float* th) {
+  if (!(th[0] > 0.f && th[0] <= 1.f) || !(th[1] > 0.f && th[1] <= 1.f) || !(th[2] >= 0.f && th[2] <= 1.f))
+    return fail(PRR_ERR_INVALID_ARG, "alpha %g, beta %g, gamma %g outside (0,1], (0,1], [0,1]", th[0], th[1], th[2]);
   return ok();
 }
 
@@ -602,12 +616,7 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   } else if (sp->epoch == 0) {
     return fail(PRR_ERR_INVALID_ARG, "epoch 0 is reserved (a zeroed workspace carries it)");
   }
-  if (prr || prefill) {
-    if (!(sp->alpha > 0.f && sp->alpha <= 1.f) || !(sp->beta > 0.f && sp->beta <= 1.f) ||
-        !(sp->gamma >= 0.f && sp->gamma <= 1.f))
-      return fail(PRR_ERR_INVALID_ARG, "alpha %g, beta %g, gamma %g outside (0,1], (0,1], [0,1]", sp->alpha, sp->beta,
-                  sp->gamma);
-  }
+  if (prr || prefill) PRR_TRY(check_theta(y.theta ? y.theta : &sp->alpha));
   int total_a, kextra_a, total_p, kextra_p;
   budget(sp->k_select, sp->n_forced, sp->forced_in_budget, sp->num_pages, total_a, kextra_a);
   budget(sp->p_select, sp->n_forced, sp->forced_in_budget, sp->num_pages, total_p, kextra_p);
@@ -664,9 +673,9 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.stamps = sp->phase_stamps ? reinterpret_cast<unsigned long long*>(sp->phase_stamps) +
                                     (size_t)layer * prr::kStampSlots * prr::kStampMaxWorkgroups
                               : nullptr;
-  a.alpha = sp->alpha;
-  a.beta = sp->beta;
-  a.gamma = sp->gamma;
+  a.alpha = y.theta ? y.theta[0] : sp->alpha;
+  a.beta = y.theta ? y.theta[1] : sp->beta;
+  a.gamma = y.theta ? y.theta[2] : sp->gamma;
   a.epoch = sp->epoch;
   a.epoch_dev = sp->epoch_dev;
   a.schedule = prr ? 1 : (prefill ? 2 : 0);
@@ -716,6 +725,8 @@ prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* sp, cons
   const int nxt = 1 - parity;
   for (int l = 0; l < n_layers; ++l) {
     const prr_layer_io& y = layers[l];
+    const float* th = y.theta ? y.theta : &sp->alpha;  // (alpha, beta, gamma are consecutive)
+    if (schedule != PRR_SCHED_SERIAL) PRR_TRY(check_theta(th));
     if (schedule == PRR_SCHED_SERIAL) {
       PRR_TRY(prr_score_topk(dims, y.q, y.meta, sp->num_pages, sp->k_select, sp->forced, sp->n_forced,
                              sp->forced_in_budget, y.scores, y.selected, y.selected_count, sp->cap, y.workspace,
@@ -728,8 +739,8 @@ prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* sp, cons
       PRR_TRY(prr_score_topk(dims, y.q, y.meta, sp->num_pages, sp->k_select, sp->forced, sp->n_forced,
                              sp->forced_in_budget, y.scores, y.selected, y.selected_count, sp->cap, y.workspace,
                              y.ws_bytes, stream));
-      PRR_TRY(prr_predict(dims, y.ema_level, y.ema_trend, y.ema_init_bits, y.scores, sp->num_pages, sp->alpha,
-                          sp->beta, sp->gamma, sp->p_select, sp->forced, sp->n_forced, sp->forced_in_budget,
+      PRR_TRY(prr_predict(dims, y.ema_level, y.ema_trend, y.ema_init_bits, y.scores, sp->num_pages, th[0], th[1],
+                          th[2], sp->p_select, sp->forced, sp->n_forced, sp->forced_in_budget,
                           y.predicted[nxt], y.predicted_count[nxt], sp->cap, stream));
     } else {
       hipEvent_t fork = events[3 * l], sel = events[3 * l + 1], spec = events[3 * l + 2];
@@ -749,8 +760,8 @@ prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* sp, cons
                          y.part_o, y.part_m, y.part_l, y.page_m, sp->mode, y.out_o32, y.out_o, y.out_m, y.out_l,
                          y.missed_count, y.wasted_count, y.workspace, y.ws_bytes, stream));
       PRR_TRY(hip_status(hipStreamWaitEvent(spec_stream, sel, 0), "stream wait"));
-      PRR_TRY(prr_predict(dims, y.ema_level, y.ema_trend, y.ema_init_bits, y.scores, sp->num_pages, sp->alpha,
-                          sp->beta, sp->gamma, sp->p_select, sp->forced, sp->n_forced, sp->forced_in_budget,
+      PRR_TRY(prr_predict(dims, y.ema_level, y.ema_trend, y.ema_init_bits, y.scores, sp->num_pages, th[0], th[1],
+                          th[2], sp->p_select, sp->forced, sp->n_forced, sp->forced_in_budget,
                           y.predicted[nxt], y.predicted_count[nxt], sp->cap, spec_stream));
     }
   }

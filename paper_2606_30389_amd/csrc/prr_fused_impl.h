@@ -1967,7 +1967,10 @@ __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
   // visible at this launch's start)
   const uint32_t ep = a.epoch_dev ? *a.epoch_dev : a.epoch;
   fused_roles<BF16, PS, NPW>(a, ep, U);
-  if (threadIdx.x == 0) stamp(a, kStampEnd);
+  // the end of the workgroup's last wave (waves of a role may finish at different times)
+  if (a.stamps && (threadIdx.x & (kWave - 1)) == 0)
+    atomicMax(&a.stamps[(size_t)kStampEnd * kStampMaxWorkgroups + blockIdx.x],
+              (unsigned long long)__builtin_amdgcn_s_memrealtime());
 }
 
 }  // namespace

@@ -116,6 +116,7 @@ class LayerState:
         self.workspace = torch.empty(self.ws_bytes // 4 + 64, dtype=torch.int32, device=dev)
         L.prr_workspace_init(self.workspace, self.ws_bytes)
         self.cur = 0  # which predicted-list buffer holds P^t
+        self.theta = None  # this layer's (alpha, beta, gamma), host float32 [3], or None (the step's)
 
     # --------------------------------------------------------------- steps
     def build_meta(self, stream=None, page_begin=0, page_end=None):
@@ -172,6 +173,7 @@ class LayerState:
         y.missed_count, y.wasted_count = ptr(self.missed), ptr(self.wasted)
         y.covered_count = ptr(self.covered)
         y.workspace, y.ws_bytes = ptr(self.workspace), self.ws_bytes
+        y.theta = None if self.theta is None else self.theta.ctypes.data
         return y
 
 
@@ -248,6 +250,13 @@ class DecodeStack:
         p.alpha, p.beta, p.gamma = cfg.alpha, cfg.beta, cfg.gamma
         self.params = p
         self.events = L.hip_events(3 * len(layers) + 1)
+
+    def set_layer_theta(self, thetas):
+        """Per-layer EMA parameters (Section 4.2 calibrates one per layer): a sequence of
+        (alpha, beta, gamma) per layer, or None to use the step's for every layer."""
+        for i, st in enumerate(self.layers):
+            st.theta = None if thetas is None else np.asarray(thetas[i], dtype=np.float32).copy()
+            self.io[i].theta = None if st.theta is None else st.theta.ctypes.data
 
     def _parity(self):
         parity = self.layers[0].cur

@@ -171,7 +171,7 @@ def test_fused_step_rejects_bad_stamps_and_epoch(P):
             getattr(y, name)[1] = FAKE
         elif name == "ws_bytes":
             y.ws_bytes = ws
-        elif name in ("page_table", "out_o", "missed_count", "wasted_count"):
+        elif name in ("page_table", "out_o", "missed_count", "wasted_count", "covered_count", "theta"):
             setattr(y, name, None)
         else:
             setattr(y, name, FAKE)
@@ -190,6 +190,15 @@ def test_fused_step_rejects_bad_stamps_and_epoch(P):
     bad_late = params()
     bad_late.late_spec = 3
     _expect(P, 1, P.prr_decode_step, d, bad_late, layers, 0, P.PRR_SCHED_FUSED_PRR)
+    # a layer's own (alpha, beta, gamma) out of range (host memory, read at the call)
+    import numpy as np
+    for bad in ((0.0, 0.5, 0.0), (0.5, 1.5, 0.0), (0.5, 0.5, -0.25)):
+        th = np.asarray(bad, dtype=np.float32)
+        layers[0].theta = th.ctypes.data
+        for sched in (P.PRR_SCHED_FUSED_PRR, P.PRR_SCHED_FUSED_PREFILL):
+            _expect(P, 1, P.prr_decode_step, d, params(), layers, 0, sched)
+            assert "alpha" in P.last_error()
+    layers[0].theta = None
     assert P.prr_fused_grid(d, params(), P.PRR_SCHED_FUSED_PRR) > 0
 
 

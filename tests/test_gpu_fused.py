@@ -44,6 +44,7 @@ class Case:
     reinit: tuple = ()          # steps before which the workspace is zeroed again
     drift: bool = False
     serial: bool = True         # also run the fused serial step after each PRR step
+    thetas: tuple = ()          # per-layer (alpha, beta, gamma) in place of the workload's
 
     def id(self):
         bits = [self.name, f"p{self.npages}" if self.npages else "full", f"m{self.mode}", f"s{self.steps}"]
@@ -58,6 +59,8 @@ class Case:
             bits.append(f"d{self.delta}")
         if self.reinit:
             bits.append("reinit" + "-".join(map(str, self.reinit)))
+        if self.thetas:
+            bits.append(f"theta{self.layers}l")
         return "_".join(bits)
 
 
@@ -82,6 +85,9 @@ CASES = [
     Case("glm32k", steps=24, delta=1.5, late=True, serial=False),
     # the Llama-shaped workload's hot set re-drawn every 16 steps
     Case("llama64k", steps=20, drift=True, late=True, serial=False),
+    # a calibrated (alpha, beta, gamma) per layer (Section 4.2), two layers that differ
+    # (values exact in float32, so that both sides rank the same predictions)
+    Case("glm32k", layers=2, steps=6, late=True, serial=False, thetas=((0.75, 0.375, 0.75), (0.25, 0.125, 0.5))),
 ]
 
 
@@ -146,6 +152,9 @@ def test_fused_full_size(torch, case):
     forced = list(pc.forced)
     stack = R.DecodeStack(layers, queries, torch.device("cuda:0"))
     stack.params.late_spec = int(case.late)
+    thetas = list(case.thetas) if case.thetas else [(pc.alpha, pc.beta, pc.gamma)] * case.layers
+    if case.thetas:
+        stack.set_layer_theta(case.thetas)
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     stack.step(L.PRR_SCHED_FUSED_PREFILL, s)
@@ -187,7 +196,8 @@ def test_fused_full_size(torch, case):
         for layer, st in enumerate(layers):
             q64 = W.bits_to_f64(qs[layer][t], cfg.dtype)
             level, trend = state[layer]
-            P = S.check_selection(preds[layer], O.ema_predict(level, trend, pc.gamma), pc.p_select, forced,
+            al, be, ga = thetas[layer]
+            P = S.check_selection(preds[layer], O.ema_predict(level, trend, ga), pc.p_select, forced,
                                   pc.forced_in_budget, what=f"P step {t}")
             s64 = S.oracle_scores(q64, metas[layer], pc)
             got_s = S.to_np(st.scores)[:, :n]
@@ -203,7 +213,7 @@ def test_fused_full_size(torch, case):
                 assert (mc[h], wc[h]) == (len(mm), len(ww)), f"layer {layer} head {h} step {t}: missed/wasted"
                 # pages of A outside P that late speculation attended: none without it
                 assert 0 <= cc[h] <= (mc[h] if case.late else 0), f"layer {layer} head {h} step {t}: covered {cc[h]}"
-            state[layer] = O.ema_update(level, trend, s64, pc.alpha, pc.beta)
+            state[layer] = O.ema_update(level, trend, s64, al, be)
             _check_state(st, *state[layer], pc, f"layer {layer} step {t}")
         if case.serial:
             S.log(f"fused serial step {t}")

@@ -227,16 +227,20 @@ def query_trajectory(cfg: Config, layer: int = 0, steps: Optional[int] = None):
     return lat, f32_to_dtype_bits(lat, cfg.dtype)
 
 
-def prefill_trajectory(cfg: Config, layer: int = 0, rows: int = 16):
-    """The queries of the last `rows` prefill tokens, ending with the step-0 query: the
-    stationary AR(1) process run backwards from q_0 (it is time-reversible), drawn from
-    its own stream.  Returns stored bits uint16 [rows][Hq][d] in time order."""
+def prefill_trajectory(cfg: Config, layer: int = 0, rows: int = 16, stride: int = 1):
+    """The queries of `rows` prefill tokens `stride` tokens apart, ending with the step-0
+    query: the AR(1) process run backwards from q_0 (it is time-reversible), drawn from its
+    own stream; `stride` steps of it at once are one step with coefficient rho^stride and
+    noise sigma * sqrt((1 - rho^(2 stride)) / (1 - rho^2)).  Returns stored bits uint16
+    [rows][Hq][d] in time order."""
     lat0, _ = query_trajectory(cfg, layer, steps=0)
-    rng = _rng(cfg.cfg_id, layer, STREAM_PREFILL)
+    rng = _rng(cfg.cfg_id, layer, STREAM_PREFILL) if stride == 1 else _rng(cfg.cfg_id, layer, STREAM_PREFILL, stride)
     shape = (cfg.num_q_heads, cfg.head_dim)
     lat = np.empty((rows,) + shape, dtype=np.float32)
     lat[rows - 1] = lat0[0]
-    rho, sig = np.float32(cfg.rho), np.float32(cfg.sigma)
+    rho_s = cfg.rho ** stride
+    sig_s = cfg.sigma * math.sqrt((1.0 - rho_s * rho_s) / (1.0 - cfg.rho * cfg.rho)) if stride > 1 else cfg.sigma
+    rho, sig = np.float32(rho_s), np.float32(sig_s)
     for r in range(rows - 2, -1, -1):
         lat[r] = rho * lat[r + 1] + sig * rng.standard_normal(shape, dtype=np.float32)
     return f32_to_dtype_bits(lat, cfg.dtype)
