@@ -304,8 +304,8 @@ typedef struct {
                                   caller; entry [l][k][w] receives the device real-time clock
                                   (100 MHz, s_memrealtime) when workgroup w of layer l's launch
                                   reached phase k (0 = never): 0 start; 1 scores computed; 2
-                                  candidate lists stored; 3 candidates gathered; 4 threshold
-                                  published; 5 missed count published; 6, 7, 8 a speculation,
+                                  candidate lists stored; 3 candidates gathered (select and
+                                  predict workgroups); 4 threshold published (predict: found); 5 missed count published; 6, 7, 8 a speculation,
                                   late or missed-page state published; 9 an output row written;
                                   10 select done; 11 next prediction written; 12 the
                                   workgroup's last wave ended; 13 an attending workgroup's page

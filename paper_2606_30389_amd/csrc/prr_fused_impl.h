@@ -1519,6 +1519,7 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, uint32_t ep, 
   qbar_load<BF16>(a, h, qv);
   const float qe = qn_ema(a, qbar_finish(a, qv, L.qb), qe0);
   const FCand c = cand_load<false>(a, ep, h, 1, L.off, L.tot, L.ck, L.cpg);  // (no hurry: the next step's set)
+  if (t == 0) stamp(a, kStampGathered);
   // every score workgroup has read the bounds: the scale of the next step's keys
   if (t == 0) a.win[4 * h + 3] = __float_as_uint(qe);
   if (a.kextra_p <= c.total - c.nforced && c.total <= kCandWave) {
@@ -1533,6 +1534,7 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, uint32_t ep, 
       c2[j] = i < c.total && !(L.cpg[i] >> 31);
     }
     const SelThreshold th = bsel_threshold<kFT>(k2, c2, a.kextra_p, L.bsel);
+    if (t == 0) stamp(a, kStampThreshold);
     predict_wave(a, h, c.total, qe, th, L);
   } else if (a.kextra_p <= c.total - c.nforced && c.total <= kCandMax) {
     uint32_t key[4];
