@@ -400,6 +400,90 @@ def causal_calibration(args, cfg, pc, layers, s, dev, L, R, torch):
     }
 
 
+# phase-stamp slots (prr_step_params.phase_stamps) read for each workgroup role
+STAMP_SLOTS = {"start": 0, "scores": 1, "candidates_stored": 2, "candidates_gathered": 3, "threshold": 4,
+               "missed_count": 5, "spec_state": 6, "late_state": 7, "miss_state": 8, "merge_done": 9,
+               "select_done": 10, "predict_done": 11, "end": 12, "attended": 13, "late_list": 14}
+ROLE_PHASES = {
+    "score": ["scores", "candidates_stored", "end"],
+    "select": ["candidates_gathered", "threshold", "missed_count", "miss_state", "select_done", "end"],
+    "predict": ["candidates_gathered", "threshold", "predict_done", "end"],
+    "spec": ["attended", "spec_state", "end"],
+    "late": ["late_list", "attended", "late_state", "end"],
+    "miss": ["miss_state", "end"],
+    "merge": ["merge_done", "end"],
+}
+
+
+def role_ranges(H, n_score, nchunks, group, schedule, late):
+    """Workgroup index ranges of each role in a fused launch's grid (role-major: every KV
+    head's score workgroups, then every head's select workgroup, ...)."""
+    roles = [("score", H * n_score), ("select", H)]
+    if schedule != 0:
+        roles.append(("predict", H))
+    if schedule == 1:
+        roles += [("spec", H * nchunks), ("late", H * nchunks if late else 0)]
+    if schedule != 2:
+        roles += [("miss", H * nchunks), ("merge", H * group)]
+    out, b = {}, 0
+    for name, n in roles:
+        if n:
+            out[name] = (b, b + n)
+        b += n
+    return out
+
+
+def phase_table(args, cfg, layers, stack, stack_serial, cur, run, torch, dev, L, n_layers):
+    """Per-role phase times of the fused launches (device clock, 100 MHz), in us from the
+    launch's first workgroup start: for each role and phase, the median over launches (tokens
+    x layers) of [median over the role's workgroups, latest workgroup]."""
+    stamps = torch.zeros(n_layers, 16, 1024, dtype=torch.int64, device=dev)
+    out = {}
+    for label, sched, late, stk in (("fused_prr_late", L.PRR_SCHED_FUSED_PRR, 1, stack),
+                                    ("fused_serial", L.PRR_SCHED_FUSED_SERIAL, 0, stack_serial)):
+        cur[0] = stk
+        stk.params.late_spec = late
+        st0 = stk.layers[0]
+        nchunks = -(-st0.cap // st0.cfg.chunk_pages)
+        ranges = role_ranges(cfg.num_kv_heads, -(-cfg.num_pages // 128), nchunks, cfg.group,
+                             1 if sched == L.PRR_SCHED_FUSED_PRR else 0, late)
+        acc = {(r, p): [] for r in ranges for p in ROLE_PHASES[r]}
+        ends = []
+        stk.params.phase_stamps = stamps.data_ptr()
+        for _ in range(args.phases):
+            stamps.zero_()
+            torch.cuda.synchronize()
+            run(1, sched)
+            torch.cuda.synchronize()
+            a = stamps.cpu().numpy()
+            for l in range(n_layers):
+                st = a[l, 0][a[l, 0] > 0]
+                t0 = st.min()
+                e = a[l, STAMP_SLOTS["end"]]
+                ends.append((e[e > 0].max() - t0) / 100.0)
+                for (r, p), lst in acc.items():
+                    lo, hi = ranges[r]
+                    v = a[l, STAMP_SLOTS[p], lo:hi]
+                    v = v[v > 0]
+                    if v.size:
+                        lst.append(((np.median(v) - t0) / 100.0, (v.max() - t0) / 100.0))
+        stk.params.phase_stamps = None
+        if args.phases_raw:
+            raw = stamps.cpu().numpy()[0]
+            t0 = raw[0][raw[0] > 0].min()
+            out[label + "_raw_layer0"] = [[int((x - t0) // 10) if x > 0 else -1 for x in raw[k][:1024]]
+                                          for k in range(15)]
+        tab = {}
+        for (r, p), lst in acc.items():
+            if lst:
+                arr = np.asarray(lst)
+                tab.setdefault(r, {})[p] = [round(float(np.median(arr[:, 0])), 2), round(float(np.median(arr[:, 1])), 2)]
+        tab["launch_end"] = round(float(np.median(ends)), 2)
+        tab["workgroups"] = {r: hi - lo for r, (lo, hi) in ranges.items()}
+        out[label] = tab
+    return out
+
+
 def late_spec_of(schedule):
     """prr_step_params.late_spec of a schedule label: fused_prr_late* speculate late pages
     (with the read-ahead; *_nora without it)."""
@@ -436,6 +520,31 @@ def extra_measurements(args, cfg, pc, layers, stack, s, dev, L, R, torch, n_laye
     with torch.cuda.stream(s):
         floor["graph_us"] = round(1000.0 * _timed_ms(torch, s, g.replay, 20) / n_layers, 3)
     floor["fused_prr_grid_without_late"] = grid
+    # a dependency between two streams: empty one-workgroup kernels chained on one stream,
+    # against the same chain alternating between two streams with an event wait per hop
+    p2 = torch.cuda.Stream(device=dev)
+    n_hop = 200
+    one = _timed_ms(torch, s, lambda: L.prr_empty_launch(1, 64, s), n_hop)
+    evs = [torch.cuda.Event() for _ in range(n_hop + 1)]
+
+    def hops():
+        for i in range(n_hop):
+            st_a, st_b = (s, p2) if i % 2 == 0 else (p2, s)
+            L.prr_empty_launch(1, 64, st_a)
+            evs[i].record(st_a)
+            st_b.wait_event(evs[i])
+        p2.wait_stream(s)
+        s.wait_stream(p2)
+
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(s)
+    hops()
+    b.record(s)
+    torch.cuda.synchronize()
+    floor["one_stream_chain_us"] = round(1000.0 * one, 3)
+    floor["two_stream_chain_us"] = round(1000.0 * a.elapsed_time(b) / n_hop, 3)
+    floor["cross_stream_dependency_us"] = round(floor["two_stream_chain_us"] - floor["one_stream_chain_us"], 3)
     out["launch_floor"] = floor
     # HBM: a plain device copy (read + write) and a read-only reduction of 2 GiB
     nbytes = 2 << 30
@@ -759,43 +868,7 @@ def main():
         run(1, L.PRR_SCHED_FUSED_PREFILL)
     phases = None
     if args.phases > 0:
-        # per-layer phase timestamps of the fused launches (device clock, 100 MHz), in us
-        # from the first workgroup's start; medians over the tokens and layers
-        names = ["scores", "candidates_stored", "candidates_gathered", "threshold", "missed_count", "spec_state",
-                 "late_state", "miss_state", "merge_done", "select_done", "predict_done", "end", "attended",
-                 "late_list"]
-        stamps = torch.zeros(n_layers, 16, 1024, dtype=torch.int64, device=dev)
-        phases = {}
-        for label, sched, late, stk in (("fused_prr_late", L.PRR_SCHED_FUSED_PRR, 1, stack),
-                                        ("fused_serial", L.PRR_SCHED_FUSED_SERIAL, 0, stack_serial)):
-            cur[0] = stk
-            stk.params.late_spec = late
-            stk.params.phase_stamps = stamps.data_ptr()
-            rows = []
-            for _ in range(args.phases):
-                stamps.zero_()
-                torch.cuda.synchronize()
-                run(1, sched)
-                torch.cuda.synchronize()
-                st_np = stamps.cpu().numpy()
-                for l in range(n_layers):
-                    started = st_np[l, 0][st_np[l, 0] > 0]
-                    t0 = started.min()
-                    row = []
-                    for i in range(len(names)):
-                        v = st_np[l, i + 1][st_np[l, i + 1] > 0]
-                        row.append(((np.median(v) - t0) / 100.0, (v.max() - t0) / 100.0) if v.size else (np.nan, np.nan))
-                    rows.append(row)
-            stk.params.phase_stamps = None
-            if args.phases_raw:
-                raw = stamps.cpu().numpy()[0]
-                t0 = raw[0][raw[0] > 0].min()
-                phases[label + "_raw_layer0"] = [[int((x - t0) // 10) if x > 0 else -1 for x in raw[k][:1024]]
-                                                 for k in range(15)]
-            arr = np.asarray(rows, dtype=np.float64)  # [launch][phase][median over workgroups, last]
-            phases[label] = {n: ([round(float(np.nanmedian(arr[:, i, j])), 2) for j in range(2)]
-                                 if np.isfinite(arr[:, i, 1]).any() else None)
-                             for i, n in enumerate(names)}
+        phases = phase_table(args, cfg, layers, stack, stack_serial, cur, run, torch, dev, L, n_layers)
         cur[0] = stack
         stack.params.late_spec = 0
     flags = [int(st.workspace[:1].cpu()[0]) for st in layers]
