@@ -1933,11 +1933,15 @@ __device__ __forceinline__ void fused_roles(const FusedLaunch& a, uint32_t ep, F
   }
   b -= H;
   if (a.schedule != 0) {
-    if (b < H) {
-      role_predict<BF16>(a, ep, b, U);
+    // the predict workgroups (whose result is the next step's) come after the speculation
+    // roles when the grid does not fit the chip at once, so that those are dispatched
+    // first; one call site keeps the role inlined
+    const int at = (a.schedule == 1 && a.predict_last) ? H * (a.n_spec + a.n_late) : 0;
+    if (b >= at && b < at + H) {
+      role_predict<BF16>(a, ep, b - at, U);
       return;
     }
-    b -= H;
+    if (b >= at) b -= H;
   }
   if (a.schedule == 2) return;
   if (a.schedule == 1) {
@@ -1984,24 +1988,30 @@ __global__ __launch_bounds__(kFT) void fused_step_kernel(const FusedLaunch a) {
 // The late read-ahead keeps a score workgroup resident until its loads return.  It is
 // used only when the whole grid is resident at once: otherwise the workgroups dispatched
 // last (late, missed-page and merge roles) wait for those slots.
+// Workgroups of this instance resident at once on the current device (cached per device),
+// or 0 when the runtime cannot tell.
 template <bool BF16, int PS, int NPW>
-hipError_t launch_fused_inst(int grid, const FusedLaunch& a, hipStream_t stream) {
+int resident_inst() {
   constexpr int kMaxDevices = 64;
-  static int resident[kMaxDevices];  // workgroups of this kernel resident at once (0 = not known yet)
+  static int resident[kMaxDevices];  // (0 = not known yet)
   int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
   int cap = dev >= 0 && dev < kMaxDevices ? resident[dev] : 0;
   if (cap == 0) {
     int per_cu = 0, cus = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fused_step_kernel<BF16, PS, NPW>),
-                                                     kFT, 0);
-    if (e != hipSuccess) return e;
-    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e != hipSuccess) return e;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fused_step_kernel<BF16, PS, NPW>),
+                                                     kFT, 0) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
     cap = per_cu * cus;
     if (dev >= 0 && dev < kMaxDevices) resident[dev] = cap;
   }
+  return cap;
+}
+
+template <bool BF16, int PS, int NPW>
+hipError_t launch_fused_inst(int grid, const FusedLaunch& a, hipStream_t stream) {
+  const int cap = resident_inst<BF16, PS, NPW>();
   FusedLaunch b = a;
   b.readahead = a.readahead && grid <= cap;
   void* args[] = {&b};

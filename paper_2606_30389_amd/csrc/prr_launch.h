@@ -137,6 +137,7 @@ struct FusedLaunch {
   int n_score, n_spec, n_miss, n_late, nparts;  // workgroups per KV head; partial slots per KV head
   int late;  // late speculation on (PRR schedule)
   int readahead;  // score workgroups read the first late pages ahead (allowed; decided at launch)
+  int predict_last;  // predict workgroups after the speculation roles in the grid (it is not resident at once)
   int n_forced;
   bool meta_mean;
   int32_t forced[PRR_MAX_FORCED];
@@ -171,6 +172,8 @@ template <bool BF16, int PS, int NPW>
 hipError_t launch_fused_inst(int grid, const FusedLaunch& a, hipStream_t stream);
 hipError_t launch_fused(const FusedLaunch& a, bool bf16, int page_size, hipStream_t stream);
 int fused_grid(const FusedLaunch& a);
+// workgroups of the fused kernel resident at once on the current device (0: unknown)
+int fused_resident(bool bf16, int page_size, int chunk);
 
 // The argument checks of prr_score_topk (everything but the workspace), filling the launch
 // descriptor; shared with the entry point that allocates nothing.  Errors are recorded
