@@ -61,33 +61,50 @@ def _grid(row, gx, wx):
     return int(row[gx]) // max(1, int(row[wx]))
 
 
-def trace_table(directory, kernel="fused_step", names=None):
-    """Markdown table of the kernel trace by launch shape, and the durations by shape (us)."""
-    names = names or {}
-    by = {}
-    for r in _rows(directory, "kernel_trace.csv"):
-        if kernel not in r["Kernel_Name"]:
-            continue
+def trace_table(directory, kernel="fused_step", names=None, splits=None):
+    """Markdown table of the kernel trace by launch shape, and the durations by shape (us).
+    splits: {grid: [(label, count), .., (label, None)]} labels consecutive launches of one
+    shape in launch order (schedules of the same grid run one after another)."""
+    names, splits = names or {}, splits or {}
+    rows = [r for r in _rows(directory, "kernel_trace.csv") if kernel in r["Kernel_Name"]]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    by, seen, first = {}, {}, {}
+    for r in rows:
         g = _grid(r, "Grid_Size_X", "Workgroup_Size_X")
-        by.setdefault(g, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0)
+        i = seen.get(g, 0)
+        seen[g] = i + 1
+        label = names.get(g, "?")
+        if g in splits:
+            acc = 0
+            for lab, cnt in splits[g]:
+                if cnt is None or i < acc + cnt:
+                    label = lab
+                    break
+                acc += cnt
+        first.setdefault((g, label), len(first))
+        by.setdefault((g, label), []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0)
     lines = ["| launch | workgroups | launches | avg us | median us | min us | max us |", "|---|---|---|---|---|---|---|"]
-    for g in sorted(by):
-        v = by[g]
-        lines.append(f"| {names.get(g, '?')} | {g} | {len(v)} | {st.mean(v):.2f} | {st.median(v):.2f} | "
+    for (g, label) in sorted(by, key=lambda k: (k[0], first[k])):
+        v = by[(g, label)]
+        lines.append(f"| {label} | {g} | {len(v)} | {st.mean(v):.2f} | {st.median(v):.2f} | "
                      f"{min(v):.2f} | {max(v):.2f} |")
     return "\n".join(lines), by
 
 
-def counter_medians(directory, kernel="fused_step", copy_min_threads=131072):
-    """(copy values, {grid: median}) of the one counter a --pmc run collected, in KiB."""
-    copy, by = [], {}
+def counter_medians(directory, kernel="fused_step"):
+    """(values of the calibration copy, {grid: median}) of the one counter a --pmc run
+    collected, in KiB.  The calibration copies are the copyBuffer dispatches that moved the
+    most (other, smaller device copies of the run are ignored)."""
+    copies, by = [], {}
     for r in _rows(directory, "counter_collection.csv"):
         name = r["Kernel_Name"]
         val = float(r["Counter_Value"])
-        if "copyBuffer" in name and int(r["Grid_Size"]) >= copy_min_threads:
-            copy.append(val)
+        if "copyBuffer" in name:
+            copies.append((int(r["Grid_Size"]), val))
         elif kernel in name:
             by.setdefault(_grid(r, "Grid_Size", "Workgroup_Size"), []).append(val)
+    top = max((v for _, v in copies), default=0.0)
+    copy = [v for _, v in copies if v >= 0.5 * top] if top > 0 else []
     return copy, {g: st.median(v) for g, v in by.items()}
 
 
@@ -115,6 +132,8 @@ def main(argv=None):
     t.add_argument("dir")
     t.add_argument("--kernel", default="fused_step")
     t.add_argument("--names", nargs="*", default=[], help="GRID=label")
+    t.add_argument("--split", nargs="*", default=[],
+                   help="GRID=label:count,label:count,..,label (consecutive launches of one shape)")
     c = sub.add_parser("counters")
     c.add_argument("--fetch", required=True)
     c.add_argument("--write", required=True)
@@ -128,7 +147,15 @@ def main(argv=None):
     a = ap.parse_args(argv)
     if a.cmd == "trace":
         names = dict((int(x.split("=")[0]), x.split("=", 1)[1]) for x in a.names)
-        print(trace_table(a.dir, a.kernel, names)[0])
+        splits = {}
+        for x in a.split:
+            g, spec = x.split("=", 1)
+            parts = []
+            for item in spec.split(","):
+                lab, _, cnt = item.partition(":")
+                parts.append((lab, int(cnt) if cnt else None))
+            splits[int(g)] = parts
+        print(trace_table(a.dir, a.kernel, names, splits)[0])
         return 0
     res, ff, wf, fcopy, wcopy = counters(a.fetch, a.write, a.copy_mib, a.kernel)
     labels = dict(zip(a.grid, a.label))
