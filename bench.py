@@ -407,7 +407,8 @@ STAMP_SLOTS = {"start": 0, "scores": 1, "candidates_stored": 2, "candidates_gath
 ROLE_PHASES = {
     "score": ["scores", "candidates_stored", "end"],
     "select": ["candidates_gathered", "threshold", "missed_count", "miss_state", "select_done", "end"],
-    "predict": ["candidates_gathered", "threshold", "predict_done", "end"],
+    # (predict: "missed_count" / "select_done" mark its middle path / full gather)
+    "predict": ["candidates_gathered", "threshold", "missed_count", "select_done", "predict_done", "end"],
     "spec": ["attended", "spec_state", "end"],
     "late": ["late_list", "attended", "late_state", "end"],
     "miss": ["miss_state", "end"],
@@ -439,7 +440,8 @@ def role_ranges(H, n_score, nchunks, group, schedule, late, n_late, predict_last
 def phase_table(args, cfg, layers, stack, stack_serial, cur, run, torch, dev, L, n_layers):
     """Per-role phase times of the fused launches (device clock, 100 MHz), in us from the
     launch's first workgroup start: for each role and phase, the median over launches (tokens
-    x layers) of [median over the role's workgroups, latest workgroup]."""
+    x layers) of [median over the role's workgroups, latest workgroup], and the share of
+    launches in which some workgroup of the role reached the phase."""
     stamps = torch.zeros(n_layers, 16, 1024, dtype=torch.int64, device=dev)
     out = {}
     for label, sched, late, stk in (("fused_prr_late", L.PRR_SCHED_FUSED_PRR, 1, stack),
@@ -486,8 +488,10 @@ def phase_table(args, cfg, layers, stack, stack_serial, cur, run, torch, dev, L,
         tab = {}
         for (r, p), lst in acc.items():
             if lst:
+                # [median workgroup, latest workgroup, share of launches in which the phase occurred]
                 arr = np.asarray(lst)
-                tab.setdefault(r, {})[p] = [round(float(np.median(arr[:, 0])), 2), round(float(np.median(arr[:, 1])), 2)]
+                tab.setdefault(r, {})[p] = [round(float(np.median(arr[:, 0])), 2), round(float(np.median(arr[:, 1])), 2),
+                                            round(len(lst) / len(ends), 3)]
         tab["launch_end"] = round(float(np.median(ends)), 2)
         tab["workgroups"] = {r: hi - lo for r, (lo, hi) in ranges.items()}
         out[label] = tab

@@ -305,13 +305,15 @@ typedef struct {
                                   (100 MHz, s_memrealtime) when workgroup w of layer l's launch
                                   reached phase k (0 = never): 0 start; 1 scores computed; 2
                                   candidate lists stored; 3 candidates gathered (select and
-                                  predict workgroups); 4 threshold published (predict: found); 5 missed count published; 6, 7, 8 a speculation,
-                                  late or missed-page state published; 9 an output row written;
-                                  10 select done; 11 next prediction written; 12 the
-                                  workgroup's last wave ended; 13 an attending workgroup's page
-                                  states computed; 14 a late workgroup holds its list.  One
-                                  plain store per entry (12: an atomic maximum per wave).
-                                  Grids above 1024 workgroups give PRR_ERR_UNSUPPORTED. */
+                                  predict workgroups); 4 threshold published (predict: found);
+                                  5 missed count published (predict: its middle path taken);
+                                  6, 7, 8 a speculation, late or missed-page state published; 9
+                                  an output row written; 10 select done (predict: its full
+                                  gather taken); 11 next prediction written; 12 the workgroup's
+                                  last wave ended; 13 an attending workgroup's page states
+                                  computed; 14 a late workgroup holds its list.  One plain store
+                                  per entry (12: an atomic maximum per wave).  Grids above 1024
+                                  workgroups give PRR_ERR_UNSUPPORTED. */
 } prr_step_params;
 
 #define PRR_SCHED_SERIAL 0     /* per layer: select, then attend every page of A (one stream) */

@@ -1420,6 +1420,14 @@ __device__ __forceinline__ void role_select(const FusedLaunch& a, uint32_t ep, i
   if (t == 0) stamp(a, kStampSelectDone);
 }
 
+// The rank that sets the next step's candidate window of the prediction: 2.5 |P|, wider
+// with a trend term (gamma > 0), whose keys move more from step to step (at gamma = 0.25,
+// 2.5 |P| left 7 % of launches with too few or too many candidates, each falling back to
+// all 8192 keys at ~8 us; 4 |P| leaves about 1 %).  At most 6 |P|, within the middle path.
+__device__ __forceinline__ int pred_window_rank(const FusedLaunch& a) {
+  return (int)((float)a.kextra_p * fminf(2.5f + 6.0f * a.gamma, 6.0f));
+}
+
 // ------------------------------------------------------------------------ predict
 
 template <int J>
@@ -1438,7 +1446,7 @@ __device__ __forceinline__ void predict_finish(const FusedLaunch& a, uint32_t ep
     if ((in >> j) & 1ull) atomicOr(&L.bitP[page[j] >> 5], 1u << (page[j] & 31));
   __syncthreads();
   for (int i = threadIdx.x; i < nw; i += kFT) a.pbits_nxt[(size_t)h * nwmax + i] = L.bitP[i];
-  update_window<J>(a, a.win + 4 * h + 1, qe, key, cand, (5 * a.kextra_p) / 2, keep_window, L.sel);
+  update_window<J>(a, a.win + 4 * h + 1, qe, key, cand, pred_window_rank(a), keep_window, L.sel);
 }
 
 // The next prediction from a short candidate list and the workgroup's threshold, as
@@ -1482,7 +1490,7 @@ __device__ __forceinline__ void predict_wave(const FusedLaunch& a, int h, int to
     }
     if (lane == 0) a.pred_nxt_count[h] = min(n, a.cap);
   } else if (w == 1) {
-    const SelThreshold th = wsel_threshold<NK>(key, cand, max((5 * a.kextra_p) / 2, 1), L.ws[1], true);
+    const SelThreshold th = wsel_threshold<NK>(key, cand, max(pred_window_rank(a), 1), L.ws[1], true);
     if (lane == 0 && th.mode == 2 && qe > 0.0f) a.win[4 * h + 1] = __float_as_uint(key_value(th.T) / qe);
   } else {
     for (int i = t - 2 * kWave; i < nw; i += kFT - 2 * kWave) L.bitP[i] = 0u;
@@ -1537,12 +1545,14 @@ __device__ __forceinline__ void role_predict(const FusedLaunch& a, uint32_t ep, 
     if (t == 0) stamp(a, kStampThreshold);
     predict_wave(a, h, c.total, qe, th, L);
   } else if (a.kextra_p <= c.total - c.nforced && c.total <= kCandMax) {
+    if (t == 0) stamp(a, kStampMissed);  // (predict workgroups: the middle path was taken)
     uint32_t key[4];
     int page[4];
     uint64_t cand, force;
     cand_slots<4>(c.total, L.ck, L.cpg, key, page, cand, force, nullptr);
     predict_finish<4>(a, ep, h, key, page, cand, force, true, qe, L);
   } else {
+    if (t == 0) stamp(a, kStampSelectDone);  // (predict workgroups: the full gather was taken)
     uint32_t key[16];
     int page[16];
     uint64_t cand, force;
