@@ -210,6 +210,16 @@ def kernel_sweep(args):
 
 LUT_PATH = os.path.join(ROOT, "paper_2606_30389_amd", "delta_lut.json")
 
+# Pages per attending workgroup of the fused step, measured best per page size:
+# (speculation schedules, serial schedule).  128 tokens per speculation workgroup either
+# way; the serial step prefers 64 tokens at 16-token pages and 128 at 64-token pages.
+BEST_CHUNK = {16: (8, 4), 64: (2, 2)}
+
+
+def best_chunk(page_size, serial=False):
+    spec, ser = BEST_CHUNK.get(page_size, (max(1, 128 // page_size), max(1, 64 // page_size)))
+    return ser if serial else spec
+
 
 def delta_sweep(args, cfg):
     """Section 4.4's offline profiling on the fused PRR step (with late speculation): for
@@ -240,7 +250,7 @@ def delta_sweep(args, cfg):
                               num_tokens=ctx, k_select=cfg.k_select, forced=cfg.forced_pages(npg),
                               forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
                               alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma,
-                              chunk_pages=min(8, 256 // cfg.page_size), p_select=p_sel)
+                              chunk_pages=best_chunk(cfg.page_size), p_select=p_sel)
             pc.max_pages = cfg.num_pages
             st = R.LayerState(pc, dev, k=k, v=v)
             st.build_meta()
@@ -600,7 +610,7 @@ def other_workload(args, name, L, R, torch, dev, pool):
     pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
                       num_tokens=cfg.context, k_select=cfg.k_select, forced=cfg.forced_pages(),
                       forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
-                      alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma, chunk_pages=min(8, 256 // cfg.page_size))
+                      alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma, chunk_pages=best_chunk(cfg.page_size))
     layers = [None] * cfg.layers
     t0 = time.time()
     jobs = [(name, l) for l in range(cfg.layers)]
@@ -614,32 +624,42 @@ def other_workload(args, name, L, R, torch, dev, pool):
                       for l in range(cfg.layers)], dim=1).contiguous()
     q_static = torch.empty_like(qs[0])
     stack = R.DecodeStack(layers, [q_static[l] for l in range(cfg.layers)], dev)
+    # the serial step at its own best chunk, on layer states that share the K/V and metadata
+    pc_s = dataclasses.replace(pc, chunk_pages=best_chunk(cfg.page_size, serial=True))
+    layers_s = []
+    for st in layers:
+        st2 = R.LayerState(pc_s, dev, k=st.k, v=st.v, page_table=st.page_table)
+        st2.meta.copy_(st.meta)
+        layers_s.append(st2)
+    stack_serial = R.DecodeStack(layers_s, [q_static[l] for l in range(cfg.layers)], dev)
     s = torch.cuda.Stream(device=dev)
     tok = [0]
+    cur = [stack]
 
     def step(schedule):
         with torch.cuda.stream(s):
             q_static.copy_(qs[tok[0]])
-        stack.step(schedule, s)
+        cur[0].step(schedule, s)
         tok[0] += 1
 
     s.wait_stream(torch.cuda.current_stream())
     step(L.PRR_SCHED_FUSED_PREFILL)
-    res = {"layers": cfg.layers}
+    res = {"layers": cfg.layers, "chunk_pages": pc.chunk_pages, "serial_chunk_pages": pc_s.chunk_pages}
     for label, sched, late in (("fused_prr_late", L.PRR_SCHED_FUSED_PRR, 1), ("fused_serial", L.PRR_SCHED_FUSED_SERIAL, 0)):
-        stack.params.late_spec = late
+        cur[0] = stack_serial if sched == L.PRR_SCHED_FUSED_SERIAL else stack
+        cur[0].params.late_spec = late
         for _ in range(4):
             step(sched)
         ms = _timed_ms(torch, s, lambda: step(sched), steps)
         res[label] = {"us_per_layer": round(1000.0 * ms / cfg.layers, 3), "us_per_token": round(1000.0 * ms, 1)}
-        flags = [int(st.workspace[:1].cpu()[0]) for st in layers]
+        flags = [int(st.workspace[:1].cpu()[0]) for st in cur[0].layers]
         if any(flags):
             res[label]["error_flags"] = flags
     b_alg = algorithmic_bytes(cfg, cfg.num_pages)
     res["alg_bytes_per_layer_step"] = b_alg
     res["roofline_frac"] = round(b_alg / (res["fused_prr_late"]["us_per_layer"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
     res["speedup_vs_serial"] = round(res["fused_serial"]["us_per_layer"] / res["fused_prr_late"]["us_per_layer"], 3)
-    del stack, layers
+    del stack, stack_serial, layers, layers_s
     torch.cuda.empty_cache()
     return res
 
@@ -718,7 +738,7 @@ def main():
                       num_tokens=cfg.context, k_select=cfg.k_select, forced=cfg.forced_pages(),
                       forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
                       alpha=theta[0], beta=theta[1], gamma=theta[2],
-                      chunk_pages=args.chunk or min(8, 256 // cfg.page_size), mode=mode, p_select=p_select)
+                      chunk_pages=args.chunk or best_chunk(cfg.page_size), mode=mode, p_select=p_select)
     schedules = [x for x in args.schedules.split(",") if x]
     sched_id = {"fused_prr": L.PRR_SCHED_FUSED_PRR, "fused_prr_late": L.PRR_SCHED_FUSED_PRR,
                 "fused_prr_late_nora": L.PRR_SCHED_FUSED_PRR,
@@ -763,7 +783,7 @@ def main():
     serial_chunk = pc.chunk_pages
     stack_serial = stack
     if "fused_serial" in args.schedules.split(",") and args.chunk is None:
-        serial_chunk = min(4, 256 // cfg.page_size)
+        serial_chunk = best_chunk(cfg.page_size, serial=True)
         if serial_chunk != pc.chunk_pages:
             pc_s = dataclasses.replace(pc, chunk_pages=serial_chunk)
             layers_s = []

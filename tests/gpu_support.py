@@ -34,7 +34,7 @@ def torch_and_lib():
 def path_config(cfg: W.Config, num_pages=None, chunk_pages=None, mode=0, num_tokens=None):
     _, P, R = torch_and_lib()
     if chunk_pages is None:
-        chunk_pages = min(8, 256 // cfg.page_size)
+        chunk_pages = max(1, 128 // cfg.page_size)  # (128 tokens per attending workgroup, as the bench runs it)
     n = cfg.num_pages if num_pages is None else num_pages
     nt = n * cfg.page_size if num_tokens is None else num_tokens
     return R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,

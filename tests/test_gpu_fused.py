@@ -74,6 +74,7 @@ CASES = [
     Case("glm32k", tail=5, nan_tail=True, late=True, steps=3),
     Case("glm32k", page_table=True, tail=11, nan_tail=True, steps=3, chunk=16),
     Case("infllm128k", page_table=True, tail=37, nan_tail=True, late=True, steps=3),
+    Case("infllm128k", chunk=4, late=True, steps=3),
     Case("glm128k", page_table=True, tail=3, nan_tail=True, late=True, steps=2),
     # the select's fallback paths in PRR steps: all 2048 pages of glm32k become candidates
     # (the one-workgroup middle path), all 4096 / 8192 of llama64k / glm128k (full gather)
