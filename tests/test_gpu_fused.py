@@ -39,6 +39,7 @@ class Case:
     layers: int = 1
     steps: int = 4
     late: bool = False
+    nora: bool = False          # late speculation without the read-ahead (late_spec 2)
     page_table: bool = False
     nan_tail: bool = False
     reinit: tuple = ()          # steps before which the workspace is zeroed again
@@ -48,7 +49,7 @@ class Case:
 
     def id(self):
         bits = [self.name, f"p{self.npages}" if self.npages else "full", f"m{self.mode}", f"s{self.steps}"]
-        for flag in ("late", "page_table", "nan_tail", "drift"):
+        for flag in ("late", "nora", "page_table", "nan_tail", "drift"):
             if getattr(self, flag):
                 bits.append(flag)
         if self.tail:
@@ -66,7 +67,7 @@ class Case:
 
 CASES = [
     # the workloads at full size, with and without late speculation
-    Case("glm32k", steps=4), Case("glm32k", steps=4, late=True),
+    Case("glm32k", steps=4), Case("glm32k", steps=4, late=True), Case("glm32k", steps=4, late=True, nora=True),
     Case("llama64k", steps=3), Case("llama64k", steps=3, late=True), Case("llama64k", mode=1, steps=2, late=True),
     Case("infllm128k", steps=4), Case("infllm128k", steps=4, late=True),
     # paged layout and a partial last page whose unwritten tail holds NaN / Inf
@@ -152,7 +153,7 @@ def test_fused_full_size(torch, case):
     pc = layers[0].cfg
     forced = list(pc.forced)
     stack = R.DecodeStack(layers, queries, torch.device("cuda:0"))
-    stack.params.late_spec = int(case.late)
+    stack.params.late_spec = (2 if case.nora else 1) if case.late else 0
     thetas = list(case.thetas) if case.thetas else [(pc.alpha, pc.beta, pc.gamma)] * case.layers
     if case.thetas:
         stack.set_layer_theta(case.thetas)
