@@ -358,15 +358,20 @@ def causal_calibration(args, cfg, pc, layers, s, dev, L, R, torch):
     thetas, objective = [None] * n_layers, [0.0] * n_layers
     nthreads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
 
+    failure = []
+
     def search():
-        for l in range(n_layers):
-            events[l].synchronize()
-            ready[l] = time.perf_counter()
-            traj = host[l].numpy()
-            best, obj = L.prr_calibrate(traj, cfg.k_select, grid, p_select=pc.p_select or cfg.k_select,
-                                        n_threads=nthreads, form_row=born)
-            thetas[l], objective[l] = tuple(float(x) for x in best), float(obj.max())
-            done[l] = time.perf_counter()
+        try:
+            for l in range(n_layers):
+                events[l].synchronize()
+                ready[l] = time.perf_counter()
+                traj = host[l].numpy()
+                best, obj = L.prr_calibrate(traj, cfg.k_select, grid, p_select=pc.p_select or cfg.k_select,
+                                            n_threads=nthreads, form_row=born)
+                thetas[l], objective[l] = tuple(float(x) for x in best), float(obj.max())
+                done[l] = time.perf_counter()
+        except BaseException as e:  # (re-raised by the main thread after the join)
+            failure.append(e)
 
     worker = threading.Thread(target=search)
     torch.cuda.synchronize()
@@ -388,6 +393,8 @@ def causal_calibration(args, cfg, pc, layers, s, dev, L, R, torch):
     events[-1].synchronize()
     t_gpu = time.perf_counter()
     worker.join()
+    if failure:
+        raise failure[0]
     t_end = time.perf_counter()
     per_layer_gpu = [a.elapsed_time(b) for a, b in gpu_ms]
     search_ms = [1000.0 * (done[l] - max(ready[l], done[l - 1] if l else 0.0)) for l in range(n_layers)]
