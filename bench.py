@@ -433,17 +433,14 @@ ROLE_PHASES = {
 }
 
 
-def role_ranges(H, n_score, nchunks, group, schedule, late, n_late, predict_last):
+def role_ranges(H, n_score, nchunks, group, schedule, late, n_late):
     """Workgroup index ranges of each role in a fused launch's grid (role-major: every KV
-    head's score workgroups, then every head's select workgroup, ...; the predict
-    workgroups after the speculation roles when the grid exceeds the resident workgroups)."""
+    head's score workgroups, then every head's select workgroup, ...)."""
     roles = [("score", H * n_score), ("select", H)]
-    if schedule != 0 and not predict_last:
+    if schedule != 0:
         roles.append(("predict", H))
     if schedule == 1:
         roles += [("spec", H * nchunks), ("late", H * n_late if late else 0)]
-    if schedule != 0 and predict_last:
-        roles.append(("predict", H))
     if schedule != 2:
         roles += [("miss", H * nchunks), ("merge", H * group)]
     out, b = {}, 0
@@ -473,9 +470,7 @@ def phase_table(args, cfg, layers, stack, stack_serial, cur, run, torch, dev, L,
         grid = L.prr_fused_grid(stk.dims, stk.params, sched)
         per = grid // cfg.num_kv_heads
         n_late = per - (n_score + 2 + 2 * nchunks + cfg.group) if schedule == 1 and late else 0
-        # (this kernel holds 2 workgroups per CU: 512 on MI355X's 256 CUs)
-        ranges = role_ranges(cfg.num_kv_heads, n_score, nchunks, cfg.group, schedule, late, n_late,
-                             schedule == 1 and grid > 512)
+        ranges = role_ranges(cfg.num_kv_heads, n_score, nchunks, cfg.group, schedule, late, n_late)
         acc = {(r, p): [] for r in ranges for p in ROLE_PHASES[r]}
         ends = []
         stk.params.phase_stamps = stamps.data_ptr()

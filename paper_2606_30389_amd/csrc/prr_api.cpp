@@ -152,14 +152,14 @@ prr_status check_theta(const float* th) {
 }
 
 // Late-speculation workgroups per KV head: one per chunk of the list capacity, or fewer
-// when that keeps every role dispatched before the predict workgroups (score, select,
-// speculation, late) within the workgroups the chip holds at once, so that no late
-// workgroup waits for a slot.  Late pages beyond the capacity are attended after the
+// when that keeps every role dispatched up to the late workgroups (score, select,
+// predict, speculation, late) within the workgroups the chip holds at once, so that no
+// late workgroup waits for a slot.  Late pages beyond the capacity are attended after the
 // threshold, as missed pages; a cut deeper than half is not made.
 int late_slots(const prr_dims* d, int n_score, int nchunks, int chunk) {
   const int resident = prr::fused_resident(d->dtype == PRR_BF16, d->page_size, chunk);
   if (resident <= 0) return nchunks;
-  const int fit = resident / d->num_kv_heads - n_score - 1 - nchunks;
+  const int fit = resident / d->num_kv_heads - n_score - 2 - nchunks;
   if (fit >= nchunks || fit < (nchunks + 1) / 2) return nchunks;
   return fit;
 }
@@ -708,10 +708,6 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.late = prr && sp->late_spec && sp->mode != PRR_RECOMPUTE_ON_MISS;
   a.readahead = a.late && sp->late_spec == 1;  // (kept only if the grid is resident at once)
   a.n_late = a.late ? late_slots(dims, a.n_score, L.nchunks, sp->chunk_pages) : 0;
-  {
-    const int resident = prr::fused_resident(dims->dtype == PRR_BF16, dims->page_size, sp->chunk_pages);
-    a.predict_last = prr && resident > 0 && prr::fused_grid(a) > resident;
-  }
   a.nparts = L.nparts;
   a.n_forced = sp->n_forced;
   a.meta_mean = dims->meta_kind == PRR_META_MEAN;

@@ -1943,15 +1943,11 @@ __device__ __forceinline__ void fused_roles(const FusedLaunch& a, uint32_t ep, F
   }
   b -= H;
   if (a.schedule != 0) {
-    // the predict workgroups (whose result is the next step's) come after the speculation
-    // roles when the grid does not fit the chip at once, so that those are dispatched
-    // first; one call site keeps the role inlined
-    const int at = (a.schedule == 1 && a.predict_last) ? H * (a.n_spec + a.n_late) : 0;
-    if (b >= at && b < at + H) {
-      role_predict<BF16>(a, ep, b - at, U);
+    if (b < H) {
+      role_predict<BF16>(a, ep, b, U);
       return;
     }
-    if (b >= at) b -= H;
+    b -= H;
   }
   if (a.schedule == 2) return;
   if (a.schedule == 1) {

@@ -137,7 +137,6 @@ struct FusedLaunch {
   int n_score, n_spec, n_miss, n_late, nparts;  // workgroups per KV head; partial slots per KV head
   int late;  // late speculation on (PRR schedule)
   int readahead;  // score workgroups read the first late pages ahead (allowed; decided at launch)
-  int predict_last;  // predict workgroups after the speculation roles in the grid (it is not resident at once)
   int n_forced;
   bool meta_mean;
   int32_t forced[PRR_MAX_FORCED];
