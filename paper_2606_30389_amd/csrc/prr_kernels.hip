@@ -18,6 +18,7 @@
 
 #include "prr_device.h"
 #include "prr_launch.h"
+#include "prr_select.h"
 
 namespace prr {
 
@@ -237,63 +238,63 @@ hipError_t launch_meta(const MetaLaunch& a, hipStream_t stream) {
 // =====================================================================================
 // block top-K select (shared by score_topk and predict)
 // =====================================================================================
-// 1024 threads; thread (wave w, lane) owns pages p_j = w*J*64 + j*64 + lane, j < J, with
-// their keys in registers.  Candidates have their bit set in `cand`, pages in `force`
-// are always selected.  The threshold key T (the kextra-th largest candidate key) is
-// found by radix passes over the key range [lo, hi] with 8192 LDS bins: each pass keeps
-// only the bin that holds the wanted rank, so at most three passes are needed and two
-// whenever the candidate scores span less than a factor of eight.  Every candidate above T and the lowest-indexed candidates equal to T
-// are then emitted in ascending page order by ballot compaction.
+// 1024 threads; thread (wave w, lane) owns pages w*J*64 + j*64 + lane, j < J, with their
+// keys in registers, so that (w, j, lane) is ascending page order.  Candidates have their
+// bit set in `cand`, pages in `force` are always selected.
+//
+// All pages of a KV head are candidates here, so their keys span the whole range of the
+// scores (negative and positive), and radix bins over the key bits put most keys into a
+// few bins, whose LDS atomics then serialise.  The first pass therefore bins the values
+// linearly between the smallest and the largest candidate (a non-decreasing map, so a
+// higher bin holds only larger values); the key-space radix select of prr_select.h then
+// ranks the keys of the one bin that holds rank kextra.  Keys of NaN or infinite values
+// fall back to the key-space select.  The selection is emitted in ascending page order
+// by ballot compaction.
 
 constexpr int kSelThreads = 1024;
-constexpr int kSelLog2Bins = 13;
-constexpr int kSelBins = 1 << kSelLog2Bins;
 
-struct SelectScratch {
-  uint32_t hist[kSelBins];
+struct __align__(16) SelectScratch {
+  Sel2Lds sel;
   uint32_t forceb[PRR_MAX_PAGES_DEV / 32];
-  int red[64];
-  uint32_t ured[64];
+  int wcnt[kSelThreads / kWave];  // selected pages per wave
 };
 
-__host__ __device__ inline int select_j(int n) {
-  int j = 1;
-  while (j * kSelThreads < n) j <<= 1;
-  return j;
-}
+__host__ __device__ inline int select_j(int n) { return sel2_j(n, kSelThreads); }
 
-__device__ __forceinline__ int sel_page(int j, int J) {
-  return (threadIdx.x / kWave) * J * kWave + j * kWave + lane_id();
+// the float whose score_key is k
+__device__ __forceinline__ float key_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
 }
 
 template <int J>
-__device__ __forceinline__ void select_topk_regs(const uint32_t (&key)[J], uint64_t cand, uint64_t force, int n,
-                                                 int kextra, int32_t* __restrict__ out, int cap,
-                                                 int32_t* __restrict__ out_count, SelectScratch& ss) {
-  constexpr int MAXJ = J;
+__device__ __forceinline__ void select_topk_regs(const uint32_t (&key)[J], uint64_t cand, uint64_t force, int kextra,
+                                                 int32_t* __restrict__ out, int cap, int32_t* __restrict__ out_count,
+                                                 SelectScratch& ss) {
   constexpr int NT = kSelThreads, NW = NT / kWave;
+  Sel2Lds& S = ss.sel;
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  int page[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) page[j] = sel2_page<J>(j);
 
   int cnt = __popcll(cand);
   uint32_t lo = 0xffffffffu, hi = 0u;
 #pragma unroll
-  for (int j = 0; j < MAXJ; ++j) {
+  for (int j = 0; j < J; ++j) {
     if ((cand >> j) & 1ull) {
       lo = min(lo, key[j]);
       hi = max(hi, key[j]);
     }
   }
-  // one exchange for count, min and max
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    cnt += __shfl_xor(cnt, o);
-    lo = min(lo, (uint32_t)__shfl_xor((int)lo, o));
-    hi = max(hi, (uint32_t)__shfl_xor((int)hi, o));
-  }
+  cnt = wave_isum(cnt);
+  lo = wave_umin(lo);
+  hi = wave_umax(hi);
+  for (int b = t; b < kSel2Bins / 4; b += NT) reinterpret_cast<uint4*>(S.hist[0])[b] = make_uint4(0, 0, 0, 0);
+  if (t == 0) S.nsmall = 0;
   if (lane == 0) {
-    ss.red[w] = cnt;
-    ss.ured[w] = lo;
-    ss.ured[NW + w] = hi;
+    S.red[0][w] = cnt;
+    S.red[1][w] = (int)lo;
+    S.red[2][w] = (int)hi;
   }
   __syncthreads();
   cnt = 0;
@@ -301,124 +302,132 @@ __device__ __forceinline__ void select_topk_regs(const uint32_t (&key)[J], uint6
   hi = 0u;
 #pragma unroll
   for (int i = 0; i < NW; ++i) {
-    cnt += ss.red[i];
-    lo = min(lo, ss.ured[i]);
-    hi = max(hi, ss.ured[NW + i]);
+    cnt += S.red[0][i];
+    lo = min(lo, (uint32_t)S.red[1][i]);
+    hi = max(hi, (uint32_t)S.red[2][i]);
   }
-  __syncthreads();
+  const float vlo = key_value(lo), span = key_value(hi) - vlo;
+  const float scale = (float)kSel2Bins / span;
 
-  int mode;  // 0: no candidate taken, 1: all candidates, 2: threshold
-  uint32_t T = 0;
-  int need_eq = 0;
+  // S.red is next written by the list compaction (after the barriers of the passes below)
+  // or, on the key-space path, right at its start, hence the barrier there
+  uint64_t in;
+  int eq_cut = -1;
   if (kextra <= 0 || cnt == 0) {
-    mode = 0;
+    in = force;
   } else if (kextra >= cnt) {
-    mode = 1;
+    in = cand | force;
+  } else if (!(span > 0.0f) || !__builtin_isfinite(span) || !__builtin_isfinite(scale)) {
+    __syncthreads();
+    const SelThreshold th = sel2_threshold<NT, J>(key, cand, kextra, S);
+    in = sel2_membership<NT, J>(key, page, cand, force, th, &eq_cut, S);
   } else {
-    mode = 2;
-    int r = kextra;  // rank (1 = largest) of the threshold among keys in [lo, hi]
-    for (int pass = 0; pass < 4; ++pass) {
-      const uint32_t range = hi - lo;
-      if (range == 0) {
-        T = lo;
-        break;
-      }
-      const int bits = 32 - __clz(range);
-      const int shift = bits > kSelLog2Bins ? bits - kSelLog2Bins : 0;
-      for (int b = t; b < kSelBins; b += NT) ss.hist[b] = 0u;
-      __syncthreads();
+    int bin[J];
 #pragma unroll
-      for (int j = 0; j < MAXJ; ++j) {
-        if (((cand >> j) & 1ull) && key[j] >= lo && key[j] <= hi) atomicAdd(&ss.hist[(key[j] - lo) >> shift], 1u);
+    for (int j = 0; j < J; ++j) {
+      bin[j] = min(kSel2Bins - 1, (int)((key_value(key[j]) - vlo) * scale));
+      if ((cand >> j) & 1ull) atomicAdd(&S.hist[0][bin[j]], 1u);
+    }
+    __syncthreads();
+    if (w == 0) {
+      // lane l owns bins [2048 - 32(l+1), 2048 - 32l); the lane holding rank kextra, then
+      // its bin (the scan of prr_select.h's first pass)
+      const int base = kSel2Bins - 32 * (lane + 1);
+      const uint4* hb = reinterpret_cast<const uint4*>(S.hist[0] + base);
+      int sum = 0;
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        const uint4 x = hb[v];
+        sum += (int)(x.x + x.y + x.z + x.w);
+      }
+      const int incl = wave_inclusive_scan(sum);
+      const int excl = incl - sum;
+      const uint64_t hit = __ballot(excl < kextra && kextra <= incl);
+      const int ls = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit) - 1);
+      const int ex = __builtin_amdgcn_readlane(excl, ls);
+      const int lbase = kSel2Bins - 32 * (ls + 1);
+      const int cj = lane < 32 ? (int)S.hist[0][lbase + 31 - lane] : 0;
+      const int cinc = wave_inclusive_scan(cj);
+      const uint64_t hit2 = __ballot(lane < 32 && ex + cinc >= kextra);
+      const int js = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit2) - 1);
+      if (lane == js) {
+        S.res[0] = lbase + 31 - js;
+        S.res[1] = ex + cinc - cj;
+        S.res[2] = cj;
+      }
+    }
+    __syncthreads();
+    const int bstar = S.res[0], above = S.res[1], cbin = S.res[2];
+    const int rank = kextra - above;  // of the threshold among the boundary bin's keys
+    uint64_t inbin = 0, upper = 0;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      if ((cand >> j) & 1ull) {
+        if (bin[j] == bstar) inbin |= 1ull << j;
+        if (bin[j] > bstar) upper |= 1ull << j;
+      }
+    }
+    // every value in a higher bin is larger than every value of the boundary bin, and
+    // keys equal to the threshold share its bin, so the tie cut is the boundary bin's
+    SelThreshold th;
+    if (cbin <= kSel2Small) {
+      // the few keys of the boundary bin, ranked directly by one wave
+      const int mine = __popcll(inbin);
+      if (mine) {
+        int slot = atomicAdd(&S.nsmall, mine);
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+          if ((inbin >> j) & 1ull) S.small[slot++] = key[j];
       }
       __syncthreads();
-      constexpr int BPT = kSelBins / NT;
-      const int top = kSelBins - t * BPT;  // this thread owns bins [top - BPT, top)
-      int local = 0;
-#pragma unroll
-      for (int i = 0; i < BPT; ++i) local += (int)ss.hist[top - 1 - ((i + t) & (BPT - 1))];  // rotated: few bank conflicts
-      int tot;
-      const int before = block_exclusive_scan<NT>(local, ss.red, tot);
-      if (before < r && before + local >= r) {
-        int run = before;
-        for (int i = 1; i <= BPT; ++i) {
-          const int b = top - i;
-          const int c = (int)ss.hist[b];
-          if (run + c >= r) {
-            ss.red[NW] = b;
-            ss.red[NW + 1] = run;
-            break;
-          }
-          run += c;
+      if (w == 0) {
+        const uint32_t kx = S.small[lane < cbin ? lane : 0];
+        int gt = 0, ge = 0;
+        for (int x = 0; x < cbin; ++x) {
+          const uint32_t ky = (uint32_t)__builtin_amdgcn_readlane((int)kx, x);
+          gt += ky > kx ? 1 : 0;
+          ge += ky >= kx ? 1 : 0;
+        }
+        const uint64_t hit = __ballot(lane < cbin && gt < rank && rank <= ge);
+        const int ls = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit) - 1);
+        if (lane == ls) {
+          S.res[3] = (int)kx;
+          S.res[4] = rank - gt;
+          S.res[5] = ge - gt;
         }
       }
       __syncthreads();
-      const int bstar = ss.red[NW];
-      const int above = ss.red[NW + 1];
-      __syncthreads();
-      r -= above;
-      const uint32_t nlo = lo + ((uint32_t)bstar << shift);
-      const uint64_t nhi = (uint64_t)nlo + ((1ull << shift) - 1ull);
-      hi = (uint32_t)min((uint64_t)hi, nhi);
-      lo = nlo;
-      if (shift == 0) {
-        T = lo;
-        break;
-      }
+      th.mode = 2;
+      th.T = (uint32_t)S.res[3];
+      th.need_eq = S.res[4];
+      th.eq_total = S.res[5];
+    } else {
+      __syncthreads();  // S.res and the histogram are reused by the select of the boundary bin
+      th = sel2_threshold<NT, J>(key, inbin, rank, S);
     }
-    need_eq = r;
+    in = sel2_membership<NT, J>(key, page, inbin, force | upper, th, &eq_cut, S);
   }
-
-  // compaction in ascending page order: wave w owns pages [w*J*64, (w+1)*J*64)
-  uint64_t gt = 0, eq = 0;
-#pragma unroll
-  for (int j = 0; j < MAXJ; ++j) {
-    if ((cand >> j) & 1ull) {
-      if (mode == 1 || (mode == 2 && key[j] > T)) gt |= 1ull << j;
-      if (mode == 2 && key[j] == T) eq |= 1ull << j;
-    }
-  }
-  gt |= force;
-  int gtf = __popcll(gt), eqc = __popcll(eq);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    gtf += __shfl_xor(gtf, o);
-    eqc += __shfl_xor(eqc, o);
-  }
-  if (lane == 0) {
-    ss.red[w] = gtf;
-    ss.red[NW + w] = eqc;
-  }
+  // ascending page order: the waves before this one, then ballot ranks within the wave
+  // (ss.wcnt is not read before this point, so one barrier suffices)
+  const int c = wave_isum(__popcll(in));
+  if (lane == 0) ss.wcnt[w] = c;
   __syncthreads();
-  int eq_run = 0, sel_run = 0, total = 0;
-  {
-    int eb = 0, sb = 0;
+  int run = 0, total = 0;
 #pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const int gi = ss.red[i], ei = ss.red[NW + i];
-      const int take = max(0, min(ei, need_eq - eb));
-      if (i == w) {
-        eq_run = eb;
-        sel_run = sb;
-      }
-      eb += ei;
-      sb += gi + take;
-    }
-    total = sb;
+  for (int i = 0; i < NW; ++i) {
+    const int ci = ss.wcnt[i];
+    run += i < w ? ci : 0;
+    total += ci;
   }
 #pragma unroll
-  for (int j = 0; j < MAXJ; ++j) {
-    const bool e = (eq >> j) & 1ull;
-    const uint64_t em = __ballot(e);
-    const bool take_eq = e && (eq_run + lanes_below(em) < need_eq);
-    const bool sel = ((gt >> j) & 1ull) || take_eq;
-    const uint64_t sm = __ballot(sel);
+  for (int j = 0; j < J; ++j) {
+    const bool sel = (in >> j) & 1ull;
+    const uint64_t bm = __ballot(sel);
     if (sel) {
-      const int pos = sel_run + lanes_below(sm);
-      if (pos < cap) out[pos] = sel_page(j, J);
+      const int pos = run + lanes_below(bm);
+      if (pos < cap) out[pos] = page[j];
     }
-    eq_run += __popcll(em);
-    sel_run += __popcll(sm);
+    run += __popcll(bm);
   }
   if (t == 0) *out_count = min(total, cap);
 }
@@ -438,8 +447,9 @@ __device__ __forceinline__ uint64_t forced_mask(const int32_t* forced, int n_for
   uint64_t m = 0;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
-    const int p = min(sel_page(j, J), n - 1);
-    if (sel_page(j, J) < n && ((forceb[p >> 5] >> (p & 31)) & 1u)) m |= 1ull << j;
+    const int pj = sel2_page<J>(j);
+    const int p = min(pj, n - 1);
+    if (pj < n && ((forceb[p >> 5] >> (p & 31)) & 1u)) m |= 1ull << j;
   }
   return m;
 }
@@ -460,19 +470,18 @@ __device__ __forceinline__ void select_scores(const float* scores, int n, const 
   uint64_t cand = 0;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
-    const int p = sel_page(j, J);
+    const int p = sel2_page<J>(j);
     key[j] = score_key(ld_dev(&scores[min(p, n - 1)]));
     if (p < n) cand |= 1ull << j;
   }
   const uint64_t force = forced_mask<J>(a.forced, a.n_forced, n, ss.forceb);
   cand &= ~force;
-  select_topk_regs<J>(key, cand, force, n, a.kextra, a.selected + (size_t)h * a.cap, a.cap, a.selected_count + h,
-                      ss);
+  select_topk_regs<J>(key, cand, force, a.kextra, a.selected + (size_t)h * a.cap, a.cap, a.selected_count + h, ss);
 }
 
 template <bool BF16, bool MEAN>
 __global__ __launch_bounds__(1024) void score_topk_kernel(const ScoreLaunch a) {
-  __shared__ uint32_t dyn_lds[sizeof(SelectScratch) / 4];
+  __shared__ SelectScratch ss;
   __shared__ float qbar[kHeadDim];
   __shared__ float qpart[16][kHeadDim];
   __shared__ int s_last;
@@ -545,7 +554,6 @@ __global__ __launch_bounds__(1024) void score_topk_kernel(const ScoreLaunch a) {
   if (!s_last) return;
 
   const int n = a.num_pages;
-  SelectScratch& ss = *reinterpret_cast<SelectScratch*>(dyn_lds);
   switch (select_j(n)) {
     case 1: select_scores<1>(scores, n, a, h, ss); break;
     case 2: select_scores<2>(scores, n, a, h, ss); break;
@@ -574,7 +582,7 @@ __device__ __forceinline__ void predict_head(const PredictLaunch& a, int h, Sele
   uint32_t bw[J];
 #pragma unroll
   for (int j = 0; j < J; ++j) {
-    const int p = min(sel_page(j, J), n - 1);
+    const int p = min(sel2_page<J>(j), n - 1);
     lv[j] = level[p];
     tv[j] = trend[p];
     sc[j] = scores ? scores[p] : 0.0f;
@@ -584,7 +592,7 @@ __device__ __forceinline__ void predict_head(const PredictLaunch& a, int h, Sele
   uint64_t cand = 0;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
-    const int p = sel_page(j, J);
+    const int p = sel2_page<J>(j);
     const bool inr = p < n;
     bool has = inr && ((bw[j] >> (p & 31)) & 1u);
     float l = lv[j], v = tv[j];
@@ -613,8 +621,8 @@ __device__ __forceinline__ void predict_head(const PredictLaunch& a, int h, Sele
   }
   const uint64_t force = forced_mask<J>(a.forced, a.n_forced, n, ss.forceb);
   cand &= ~force;
-  select_topk_regs<J>(key, cand, force, n, a.kextra, a.predicted + (size_t)h * a.cap, a.cap,
-                      a.predicted_count + h, ss);
+  select_topk_regs<J>(key, cand, force, a.kextra, a.predicted + (size_t)h * a.cap, a.cap, a.predicted_count + h,
+                      ss);
 }
 
 __global__ __launch_bounds__(1024) void predict_kernel(const PredictLaunch a) {
@@ -887,11 +895,18 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
 template <bool BF16, int PS>
 __global__ __launch_bounds__(256) void spec_attn_kernel(const SpecLaunch a) {
   __shared__ UnitLds sm;
+  __shared__ int32_t ids[16];
   const int c = blockIdx.x, h = blockIdx.y;
-  const int total = min(max(a.page_count[h], 0), a.cap);
   const int start = c * a.chunk;
+  // the chunk's page ids (at most 16) are loaded together with the count, clamped to the
+  // capacity, so that the count costs no round trip of its own
+  int id = -1;
+  if ((int)threadIdx.x < a.chunk) id = a.pages[(size_t)h * a.cap + min(start + (int)threadIdx.x, a.cap - 1)];
+  const int total = min(max(a.page_count[h], 0), a.cap);
   if (start >= total) return;
   const int cnt = min(a.chunk, total - start);
+  if ((int)threadIdx.x < a.chunk) ids[threadIdx.x] = id;
+  __syncthreads();
   const int G = a.group;
   AttnCtx ctx;
   ctx.q = static_cast<const uint16_t*>(a.q) + (size_t)h * G * kHeadDim;
@@ -904,7 +919,7 @@ __global__ __launch_bounds__(256) void spec_attn_kernel(const SpecLaunch a) {
   ctx.G = G;
   UnitResult r;
   float* pmo = a.page_m ? a.page_m + ((size_t)h * a.cap + start) * G : nullptr;
-  attend_unit<BF16, PS>(ctx, a.pages + (size_t)h * a.cap + start, cnt, pmo, sm, nullptr, r);
+  attend_unit<BF16, PS>(ctx, ids, cnt, pmo, sm, nullptr, r);
   const int t = threadIdx.x, hh = t >> 4, c0 = (t & 15) * 8;
   if (hh < G) {
     const size_t row = ((size_t)h * a.nchunks + c) * G + hh;
@@ -952,58 +967,47 @@ struct RepairLds {
   int nWp, nXp;
   union {
     UnitLds unit;  // work workgroups
-    struct {       // merge workgroups: (m, l) then weight of each state, for two query heads
-      float m[2][2 * PRR_MAX_CAP_DEV];
-      float w[2][2 * PRR_MAX_CAP_DEV];
+    struct {       // merge workgroups: each wave's running state
+      float acc[4][kHeadDim];
+      float ml[4][2];
     } merge;
   };
 };
 
-// Merge-workgroup helper: for the two query heads of this workgroup, states
-// [0, count) with (m, l) staged in S.merge; returns the max and turns l into weights
-// relative to it; the sum of the weights goes to `lsum`.
-__device__ __forceinline__ void merge_weights(RepairLds& S, int count, float (&ms)[2], float (&lsum)[2]) {
-  const int t = threadIdx.x, lane = lane_id(), wv = t / kWave;
+// A wave's share of a merge: the states i = par, par + 2, .. < n folded into the running
+// (M, L, ax, ay), where ml(i, m, l) loads state i's (m, l) and out(i) its outputs at
+// columns 2 lane and 2 lane + 1.  Each batch issues the loads of up to 32 states before
+// using any of them, so it costs one memory round trip.
+template <class ML, class OUT>
+__device__ __forceinline__ void fold_states(int n, int par, const ML& ml, const OUT& out, float& M, float& L, float& ax,
+                                            float& ay) {
   const float kNegInf = -__builtin_inff();
-  float mx0 = kNegInf, mx1 = kNegInf;
-  for (int i = t; i < count; i += 256) {
-    mx0 = fmaxf(mx0, S.merge.m[0][i]);
-    mx1 = fmaxf(mx1, S.merge.m[1][i]);
-  }
+  const int lane = lane_id();
+  const int nk = n > par ? (n - par + 1) / 2 : 0;
+  for (int k0 = 0; k0 < nk; k0 += 32) {
+    const int nb = min(32, nk - k0);
+    float mi, li;
+    ml(par + 2 * (k0 + min(lane, nb - 1)), mi, li);
+    float2 ov[32];
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    mx0 = fmaxf(mx0, __shfl_xor(mx0, o));
-    mx1 = fmaxf(mx1, __shfl_xor(mx1, o));
-  }
-  if (lane == 0) {
-    S.fred[0][wv] = mx0;
-    S.fred[1][wv] = mx1;
-  }
-  __syncthreads();
-  ms[0] = fmaxf(fmaxf(S.fred[0][0], S.fred[0][1]), fmaxf(S.fred[0][2], S.fred[0][3]));
-  ms[1] = fmaxf(fmaxf(S.fred[1][0], S.fred[1][1]), fmaxf(S.fred[1][2], S.fred[1][3]));
-  __syncthreads();
-  float l0 = 0.f, l1 = 0.f;
-  for (int i = t; i < count; i += 256) {
-    const float w0 = S.merge.w[0][i] > 0.f ? S.merge.w[0][i] * exp2f((S.merge.m[0][i] - ms[0]) * kLog2e) : 0.f;
-    const float w1 = S.merge.w[1][i] > 0.f ? S.merge.w[1][i] * exp2f((S.merge.m[1][i] - ms[1]) * kLog2e) : 0.f;
-    S.merge.w[0][i] = w0;
-    S.merge.w[1][i] = w1;
-    l0 += w0;
-    l1 += w1;
-  }
+    for (int r = 0; r < 32; ++r) ov[r] = out(par + 2 * (k0 + min(r, nb - 1)));
+    li = lane < nb ? li : 0.0f;
+    mi = li > 0.0f ? mi : kNegInf;
+    const float Mn = fmaxf(M, wave_max(mi));
+    if (Mn == kNegInf) continue;  // no state of this batch holds anything
+    const float sc = L > 0.0f ? exp2f((M - Mn) * kLog2e) : 0.0f;
+    const float wi = li > 0.0f ? li * exp2f((mi - Mn) * kLog2e) : 0.0f;
+    ax *= sc;
+    ay *= sc;
+    L = L * sc + wave_sum(wi);
+    M = Mn;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    l0 += __shfl_xor(l0, o);
-    l1 += __shfl_xor(l1, o);
+    for (int r = 0; r < 32; ++r) {
+      const float wr = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wi), r));
+      ax += wr * ov[r].x;
+      ay += wr * ov[r].y;
+    }
   }
-  if (lane == 0) {
-    S.fred[0][4 + wv] = l0;
-    S.fred[1][4 + wv] = l1;
-  }
-  __syncthreads();
-  lsum[0] = (S.fred[0][4] + S.fred[0][5]) + (S.fred[0][6] + S.fred[0][7]);
-  lsum[1] = (S.fred[1][4] + S.fred[1][5]) + (S.fred[1][6] + S.fred[1][7]);
 }
 
 template <bool BF16, int PS>
@@ -1036,12 +1040,20 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
     S.bitA[i] = 0u;
     S.bitP[i] = 0u;
   }
+  // the list entries are loaded together with the counts (clamped to the capacity) and
+  // masked afterwards, so the plan costs one memory round trip
   int ea[4], ep[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
+    const size_t ic = (size_t)h * a.cap + min(r * 256 + t, a.cap - 1);
+    ea[r] = a.selected[ic];
+    ep[r] = a.predicted ? a.predicted[ic] : -1;
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
     const int i = r * 256 + t;
-    ea[r] = i < nA ? a.selected[(size_t)h * a.cap + i] : -1;
-    ep[r] = i < nP ? a.predicted[(size_t)h * a.cap + i] : -1;
+    ea[r] = i < nA ? ea[r] : -1;
+    ep[r] = i < nP ? ep[r] : -1;
   }
   __syncthreads();
   bool bad_entry = false;
@@ -1182,16 +1194,24 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
       const int nwp = S.nWp, nxp = S.nXp;
       bool recompute = true;
       if (a.page_m && nxp > 0 && nwp > 0) {
-        attend_unit<BF16, PS>(ctx, S.wpages, nwp, nullptr, S.unit, a.flags, r);
+        // the chunk's speculative state and its kept pages' maxima are loaded before the
+        // wasted pages are attended, so that their round trip overlaps the attention's
         const size_t crow = ((size_t)h * a.nchunks + ch) * G;
-        bool bad = false;
         float mx = kNegInf, mc = 0.f, lc = 0.f;
+        float4 o0 = make_float4(0.f, 0.f, 0.f, 0.f), o1 = o0;
         if (hh < G) {
           mc = a.part_m[crow + hh];
           lc = a.part_l[crow + hh];
+          const float4* oc = reinterpret_cast<const float4*>(a.part_o + (crow + hh) * kHeadDim + c0);
+          o0 = oc[0];
+          o1 = oc[1];
+          for (int x = 0; x < nxp; ++x) mx = fmaxf(mx, a.page_m[((size_t)h * a.cap + S.xslots[x]) * G + hh]);
+        }
+        attend_unit<BF16, PS>(ctx, S.wpages, nwp, nullptr, S.unit, a.flags, r);
+        bool bad = false;
+        if (hh < G) {
           const float share = (lc > 0.f && r.l > 0.f) ? r.l * exp2f((r.m - mc) * kLog2e) / lc : (r.l > 0.f ? 2.f : 0.f);
           bad = !(share <= kMaxWastedShare);
-          for (int x = 0; x < nxp; ++x) mx = fmaxf(mx, a.page_m[((size_t)h * a.cap + S.xslots[x]) * G + hh]);
         }
         bad = __syncthreads_or(bad);
         if (!bad) {
@@ -1201,8 +1221,6 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
             const float ew = r.l > 0.f ? r.l * exp2f((r.m - mx) * kLog2e) : 0.f;
             const float lx = ec - ew;
             const float inv = 1.0f / lx;
-            const float4* oc = reinterpret_cast<const float4*>(a.part_o + (crow + hh) * kHeadDim + c0);
-            const float4 o0 = oc[0], o1 = oc[1];
             const float ocv[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
 #pragma unroll
             for (int e = 0; e < 8; ++e) r.o[e] = (ec * ocv[e] - ew * r.o[e]) * inv;
@@ -1238,40 +1256,29 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
     return;
   }
 
-  // ---- merge.  The clean speculative chunks are ready at launch: merge them while the
-  // work workgroups run, then wait and fold in the unit states.
+  // ---- merge.  Wave w folds, for query head pair * 2 + (w & 1), every other state
+  // (w >> 1 picks the parity): first the clean speculative chunks, which are ready at
+  // launch (folded while the work workgroups run), then, once every work workgroup of the
+  // KV head has published, the unit states; the two waves of a head are combined at the end.
   const int nUnits = nMU + (exact ? nCont : 0);
-  const int gi = t >> 7, g = pair * 2 + gi, ch = t & 127;
-  for (int i = t; i < nch; i += 256) {
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      const int gk = pair * 2 + k;
-      float m = kNegInf, l = 0.f;
-      if (gk < G && !(exact && ((S.contam_bits[i >> 5] >> (i & 31)) & 1u))) {
-        const size_t row = ((size_t)h * a.nchunks + i) * G + gk;
-        m = a.part_m[row];
-        l = a.part_l[row];
-      }
-      S.merge.m[k][i] = l > 0.f ? m : kNegInf;
-      S.merge.w[k][i] = l;
-    }
-  }
-  __syncthreads();
-  float ms_s[2], ls_s[2];
-  merge_weights(S, nch, ms_s, ls_s);
-  float Os = 0.f;
+  const int gi = w & 1, par = w >> 1, g = pair * 2 + gi;
+  const size_t crow0 = ((size_t)h * a.nchunks) * G + min(g, G - 1);
+  const size_t urow0 = ((size_t)h * a.nwork) * G + min(g, G - 1);
+  float Mw = kNegInf, Lw = 0.f, ax = 0.f, ay = 0.f;
   if (g < G) {
-    const float* wts = S.merge.w[gi];
-    const float* po = a.part_o + ((size_t)h * a.nchunks * G + g) * kHeadDim + ch;
-#pragma unroll 8
-    for (int c = 0; c < nch; ++c) {
-      const float v = po[(size_t)c * G * kHeadDim];
-      const float wgt = wts[c];
-      Os += wgt != 0.f ? wgt * v : 0.f;
-    }
+    fold_states(
+        nch, par,
+        [&](int c, float& m, float& l) {
+          const size_t row = crow0 + (size_t)c * G;
+          const bool clean = !(exact && ((S.contam_bits[c >> 5] >> (c & 31)) & 1u));
+          m = a.part_m[row];
+          l = clean ? a.part_l[row] : 0.0f;
+        },
+        [&](int c) {
+          return *reinterpret_cast<const float2*>(a.part_o + (crow0 + (size_t)c * G) * kHeadDim + 2 * lane);
+        },
+        Mw, Lw, ax, ay);
   }
-  __syncthreads();
-
   if (t == 0) {
     int it = 0;
     while (ld_dev(&a.ws_cnt[h]) < (uint32_t)a.nwork) {
@@ -1283,45 +1290,44 @@ __global__ __launch_bounds__(256) void repair_kernel(const RepairLaunch a) {
     }
   }
   __syncthreads();
-  for (int i = t; i < nUnits; i += 256) {
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      const int gk = pair * 2 + k;
-      float m = kNegInf, l = 0.f;
-      if (gk < G) {
-        const size_t row = ((size_t)h * a.nwork + i) * G + gk;
-        m = ld_dev(a.ws_ml + row * 2);
-        l = ld_dev(a.ws_ml + row * 2 + 1);
-      }
-      S.merge.m[k][i] = l > 0.f ? m : kNegInf;
-      S.merge.w[k][i] = l;
-    }
+  if (g < G) {
+    fold_states(
+        nUnits, par,
+        [&](int u, float& m, float& l) {
+          const size_t row = urow0 + (size_t)u * G;
+          m = ld_dev(a.ws_ml + row * 2);
+          l = ld_dev(a.ws_ml + row * 2 + 1);
+        },
+        [&](int u) {
+          const uint64_t v = __hip_atomic_load(
+              reinterpret_cast<uint64_t*>(a.ws_o + (urow0 + (size_t)u * G) * kHeadDim) + lane, __ATOMIC_RELAXED,
+              __HIP_MEMORY_SCOPE_AGENT);
+          return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+        },
+        Mw, Lw, ax, ay);
+  }
+  *reinterpret_cast<float2*>(&S.merge.acc[w][2 * lane]) = make_float2(ax, ay);
+  if (lane == 0) {
+    S.merge.ml[w][0] = Mw;
+    S.merge.ml[w][1] = Lw;
   }
   __syncthreads();
-  float ms_u[2], ls_u[2];
-  merge_weights(S, nUnits, ms_u, ls_u);
-  if (g < G) {
-    const float* wts = S.merge.w[gi];
-    const float* wo = a.ws_o + ((size_t)h * a.nwork * G + g) * kHeadDim + ch;
-    float Ou = 0.f;
-#pragma unroll 8
-    for (int uu = 0; uu < nUnits; ++uu) {
-      const float v = ld_dev(wo + (size_t)uu * G * kHeadDim);
-      const float wgt = wts[uu];
-      Ou += wgt != 0.f ? wgt * v : 0.f;
-    }
-    // combine the two partial merges (each relative to its own maximum)
-    const float m1 = ms_s[gi], m2 = ms_u[gi];
-    const float ms = fmaxf(m1, m2);
-    const float f1 = ls_s[gi] > 0.f ? exp2f((m1 - ms) * kLog2e) : 0.f;
-    const float f2 = ls_u[gi] > 0.f ? exp2f((m2 - ms) * kLog2e) : 0.f;
-    const float L = ls_s[gi] * f1 + ls_u[gi] * f2;
-    const float O = Os * f1 + Ou * f2;
-    const float o = L > 0.f ? O / L : 0.f;
+  if (par == 0 && g < G) {
+    const float m1 = S.merge.ml[w][0], l1 = S.merge.ml[w][1];
+    const float m2 = S.merge.ml[w + 2][0], l2 = S.merge.ml[w + 2][1];
+    const float ms = fmaxf(l1 > 0.f ? m1 : kNegInf, l2 > 0.f ? m2 : kNegInf);
+    const float f1 = l1 > 0.f ? exp2f((m1 - ms) * kLog2e) : 0.f;
+    const float f2 = l2 > 0.f ? exp2f((m2 - ms) * kLog2e) : 0.f;
+    const float L = l1 * f1 + l2 * f2;
+    const float inv = L > 0.f ? 1.0f / L : 0.f;
+    const float2 o1 = *reinterpret_cast<const float2*>(&S.merge.acc[w][2 * lane]);
+    const float2 o2 = *reinterpret_cast<const float2*>(&S.merge.acc[w + 2][2 * lane]);
+    const float ox = (o1.x * f1 + o2.x * f2) * inv, oy = (o1.y * f1 + o2.y * f2) * inv;
     const size_t orow = (size_t)h * G + g;
-    a.out_o32[orow * kHeadDim + ch] = o;
-    if (a.out_o) static_cast<uint16_t*>(a.out_o)[orow * kHeadDim + ch] = (uint16_t)f2h_rne<BF16>(o);
-    if (ch == 0) {
+    *reinterpret_cast<float2*>(a.out_o32 + orow * kHeadDim + 2 * lane) = make_float2(ox, oy);
+    if (a.out_o)
+      reinterpret_cast<uint32_t*>(a.out_o)[(orow * kHeadDim) / 2 + lane] = f2h_rne<BF16>(ox) | (f2h_rne<BF16>(oy) << 16);
+    if (lane == 0) {
       a.out_m[orow] = L > 0.f ? ms : kNegInf;
       a.out_l[orow] = L;
     }
