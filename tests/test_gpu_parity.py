@@ -207,6 +207,69 @@ def test_predict_trend_and_uninitialised_pages(torch):
         assert all(p >= 128 or p in pc.forced for p in lst)
 
 
+def _select_values(dist, n, rng):
+    """float32 keys of one KV head with the structure `dist` asks for."""
+    f32 = np.float32
+    if dist == "gauss":
+        return rng.standard_normal(n).astype(f32)
+    if dist == "extreme":  # the range overflows float32: the key-space select
+        return rng.uniform(-3.0e38, 3.0e38, n).astype(f32)
+    if dist == "inf":
+        v = rng.standard_normal(n).astype(f32)
+        v[rng.choice(n, 7, replace=False)] = np.inf
+        v[rng.choice(n, 5, replace=False)] = -np.inf
+        return v
+    if dist == "equal_at_threshold":  # rank K falls inside a group of 500 equal keys
+        v = np.where(rng.random(n) < 0.5, rng.uniform(2.0, 3.0, n), rng.uniform(-3.0, 0.5, n)).astype(f32)
+        grp = rng.choice(n, 500, replace=False)
+        v[grp] = 1.0
+        return v
+    if dist == "dense_bin":  # 600 distinct keys inside one of the 2048 value bins
+        v = rng.uniform(-1000.0, 1000.0, n).astype(f32)
+        grp = rng.choice(n, 600, replace=False)
+        v[grp] = (1.0 + rng.random(600) * 1e-4).astype(f32)
+        v[rng.choice(np.setdiff1d(np.arange(n), grp), 40, replace=False)] = 2000.0
+        return v
+    if dist == "constant":  # every key equal: the lowest page indices win
+        return np.full(n, -0.75, dtype=f32)
+    if dist == "tiny":  # normal floats so close together that 2048 / span overflows
+        mag = 1e-36 * (1.0 + np.abs(rng.standard_normal(n)))
+        return np.where(rng.random(n) < 0.5, -mag, mag).astype(f32)
+    if dist == "negative_zero":  # -0.0 and +0.0 are the same key
+        v = np.zeros(n, dtype=f32)
+        v[rng.random(n) < 0.5] = -0.0
+        v[rng.choice(n, 30, replace=False)] = 1.0
+        return v
+    raise ValueError(dist)
+
+
+SELECT_DISTS = ["gauss", "extreme", "inf", "equal_at_threshold", "dense_bin", "constant", "tiny", "negative_zero"]
+
+
+@pytest.mark.parametrize("dist", SELECT_DISTS)
+@pytest.mark.parametrize("n,k", [(8192, 256), (3001, 1000), (16384, 1024), (700, 900)])
+def test_predict_select_key_structures(torch, dist, n, k):
+    """The separate kernels' top-K (shared by prr_score_topk and prr_predict) on keys set
+    directly (gamma = 0, so the predicted key is the level): every path of the select
+    (value bins, a crowded boundary bin, the key-space fallback for non-finite or
+    underflowing spans, ties cut by page index) against the oracle's ranking, exactly."""
+    from paper_2606_30389_amd import runtime as R
+    S.log(f"select structure {dist}: n={n} k={k}")
+    pc = R.PathConfig(num_q_heads=8, num_kv_heads=2, page_size=16, num_tokens=n * 16, k_select=k,
+                      forced=[0, n - 1], forced_in_budget=True, dtype="bf16")
+    st = R.LayerState(pc, torch.device("cuda:0"))
+    rng = np.random.default_rng(zlib.crc32(f"{dist}/{n}".encode()))
+    vals = np.stack([_select_values(dist, n, rng) for _ in range(2)])
+    st.level[:, :n].copy_(torch.from_numpy(vals))
+    st.trend.zero_()
+    st.init_bits.fill_(-1)
+    st.predict(with_scores=False)
+    torch.cuda.synchronize()
+    for h, got in enumerate(S.lists(st, 1 - st.cur)):
+        want = O.select_topk(vals[h].astype(np.float64), k, [0, n - 1], True)
+        assert np.array_equal(np.sort(got), want), f"head {h}: {len(set(got) ^ set(want))} pages differ"
+
+
 # ----------------------------------------------------------------------------- attention
 
 def _upload_lists(torch, lists, cap):
