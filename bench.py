@@ -242,6 +242,7 @@ def delta_sweep(args, cfg):
     s = torch.cuda.Stream(device=dev)
     stamps = torch.zeros(1, 16, 1024, dtype=torch.int64, device=dev)
     contexts = [c for c in (4096, 8192, 16384, 32768, 65536, 131072) if c <= cfg.context]
+    serial_us = {}
     for ctx in contexts:
         for delta in (1.0, 1.25, 1.5, 2.0):
             npg = ctx // cfg.page_size
@@ -299,10 +300,37 @@ def delta_sweep(args, cfg):
                          "hit_rate": round(float(np.mean(hits)), 4)})
             print(f"[sweep] {rows[-1]}", file=sys.stderr, flush=True)
             del stack, st
+        # the select-then-attend step at this context (no speculation), for comparison
+        npg = ctx // cfg.page_size
+        pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
+                          num_tokens=ctx, k_select=cfg.k_select, forced=cfg.forced_pages(npg),
+                          forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
+                          alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma,
+                          chunk_pages=best_chunk(cfg.page_size, serial=True))
+        pc.max_pages = cfg.num_pages
+        st = R.LayerState(pc, dev, k=k, v=v)
+        st.build_meta()
+        qs = R.bits_tensor(qb, pc.torch_dtype, dev)
+        q = qs[0].clone()
+        stack = R.DecodeStack([st], [q], dev)
+        with torch.cuda.stream(s):
+            for i in range(8):
+                q.copy_(qs[i])
+                stack.step(L.PRR_SCHED_FUSED_SERIAL, s)
+            a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a_ev.record(s)
+            for i in range(n_tok):
+                q.copy_(qs[8 + i])
+                stack.step(L.PRR_SCHED_FUSED_SERIAL, s)
+            b_ev.record(s)
+        torch.cuda.synchronize()
+        serial_us[ctx] = round(1000.0 * a_ev.elapsed_time(b_ev) / n_tok, 2)
+        print(f"[sweep] context {ctx}: fused serial {serial_us[ctx]} us", file=sys.stderr, flush=True)
+        del stack, st
     pick = {c: R.pick_delta(rows, c) for c in contexts}
     out = {"sweep": "speculation budget (Section 4.4) on the fused PRR step with late speculation",
            "config": cfg.name, "workload": f"{cfg.name} layer 0, context prefixes", "kernel_source": kernel_source_hash(),
-           "table": rows, "picked_delta": pick}
+           "table": rows, "picked_delta": pick, "fused_serial_us": serial_us}
     if args.write_lut:
         with open(args.write_lut, "w") as f:
             json.dump({k: out[k] for k in ("sweep", "config", "workload", "kernel_source", "table")}, f, indent=1)
