@@ -733,7 +733,7 @@ def main():
     ap.add_argument("--schedules", default="fused_prr,fused_prr_late,fused_prr_late_nora,fused_serial,fused_prr_late_graph,"
                                            "two_stream,serial")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--kernel-reps", type=int, default=2, help="tokens per kernel-timing pass (separate kernels)")
+    ap.add_argument("--kernel-reps", type=int, default=2, help="batches of 20 back-to-back calls per separate kernel (kernel_us)")
     ap.add_argument("--workers", type=int, default=16, help="input-generation processes (0 = in-process)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device copy of this size (calibrates HBM byte counters)")
@@ -940,38 +940,31 @@ def main():
         print(json.dumps({"error": f"device error flags {flags}"}), flush=True)
         sys.exit(3)
 
-    # per-kernel durations of the separate-kernel path: HIP events around each launch
+    # per-call time of each separate kernel: back-to-back calls on one stream between two HIP
+    # events (an event pair around a single launch adds several microseconds of its own), on
+    # layer 0 after one full separate-kernel step of the current token
     def kernel_times(reps):
-        names = ("score_topk", "spec_attn", "repair", "predict", "repair_serial")
-        acc = {k: [] for k in names}
-        for _ in range(reps):
-            q_static.copy_(q_all[tok[0]])
+        n = 20 * reps
+        st, q = layers[0], q_static[0]
+        q_static.copy_(q_all[tok[0]])
+        torch.cuda.synchronize()
+        st.select(q, stream=s)
+        st.speculate(q, stream=s)
+        st.repair(q, stream=s)
+        calls = {"score_topk": lambda: st.select(q, stream=s), "spec_attn": lambda: st.speculate(q, stream=s),
+                 "repair": lambda: st.repair(q, stream=s), "predict": lambda: st.predict(stream=s),
+                 "repair_serial": lambda: st.repair(q, stream=s, serial=True)}
+        out = {}
+        for name, fn in calls.items():
+            fn()
+            a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a_ev.record(s)
+            for _ in range(n):
+                fn()
+            b_ev.record(s)
             torch.cuda.synchronize()
-            for l, st in enumerate(layers):
-                q = q_static[l]
-                evs = [torch.cuda.Event(enable_timing=True) for _ in range(10)]
-                evs[0].record(s)
-                st.select(q, stream=s)
-                evs[1].record(s)
-                evs[2].record(s)
-                st.speculate(q, stream=s)
-                evs[3].record(s)
-                evs[4].record(s)
-                st.repair(q, stream=s)
-                evs[5].record(s)
-                evs[6].record(s)
-                st.predict(stream=s)
-                evs[7].record(s)
-                evs[8].record(s)
-                st.repair(q, stream=s, serial=True)
-                evs[9].record(s)
-                torch.cuda.synchronize()
-                for i, k in enumerate(names):
-                    acc[k].append(1000.0 * evs[2 * i].elapsed_time(evs[2 * i + 1]))
-            for st in layers:
-                st.advance()
-            tok[0] += 1
-        return {k: float(np.mean(v)) for k, v in acc.items()}
+            out[name] = 1000.0 * a_ev.elapsed_time(b_ev) / n
+        return out
 
     ktimes = kernel_times(args.kernel_reps) if args.kernel_reps > 0 else {}
 
