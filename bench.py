@@ -461,7 +461,7 @@ ROLE_PHASES = {
 }
 
 
-def role_ranges(H, n_score, nchunks, group, schedule, late, n_late):
+def role_ranges(H, n_score, nchunks, group, schedule, late, n_late, n_miss):
     """Workgroup index ranges of each role in a fused launch's grid (role-major: every KV
     head's score workgroups, then every head's select workgroup, ...)."""
     roles = [("score", H * n_score), ("select", H)]
@@ -470,7 +470,7 @@ def role_ranges(H, n_score, nchunks, group, schedule, late, n_late):
     if schedule == 1:
         roles += [("spec", H * nchunks), ("late", H * n_late if late else 0)]
     if schedule != 2:
-        roles += [("miss", H * nchunks), ("merge", H * group)]
+        roles += [("miss", H * n_miss), ("merge", H * group)]
     out, b = {}, 0
     for name, n in roles:
         if n:
@@ -494,11 +494,14 @@ def phase_table(args, cfg, layers, stack, stack_serial, cur, run, torch, dev, L,
         nchunks = -(-st0.cap // st0.cfg.chunk_pages)
         n_score = -(-cfg.num_pages // 128)
         schedule = 1 if sched == L.PRR_SCHED_FUSED_PRR else 0
-        # the late workgroups per KV head: what the grid holds beyond the other roles
+        # the missed-list workgroups per KV head (four take the chunks in turn with late
+        # speculation at one page per wave), and the late ones: what the grid holds beyond
+        # the other roles
+        n_miss = min(nchunks, 4) if schedule == 1 and late and st0.cfg.chunk_pages <= 8 else nchunks
         grid = L.prr_fused_grid(stk.dims, stk.params, sched)
         per = grid // cfg.num_kv_heads
-        n_late = per - (n_score + 2 + 2 * nchunks + cfg.group) if schedule == 1 and late else 0
-        ranges = role_ranges(cfg.num_kv_heads, n_score, nchunks, cfg.group, schedule, late, n_late)
+        n_late = per - (n_score + 2 + nchunks + n_miss + cfg.group) if schedule == 1 and late else 0
+        ranges = role_ranges(cfg.num_kv_heads, n_score, nchunks, cfg.group, schedule, late, n_late, n_miss)
         acc = {(r, p): [] for r in ranges for p in ROLE_PHASES[r]}
         ends = []
         stk.params.phase_stamps = stamps.data_ptr()

@@ -164,6 +164,17 @@ int late_slots(const prr_dims* d, int n_score, int nchunks, int chunk) {
   return fit;
 }
 
+// Missed-list workgroups per KV head.  With late speculation the missed list is short (the
+// pages of A that neither P nor the late window attended before the threshold), so a few
+// workgroups take its chunks in turn instead of one idle workgroup per chunk of the list
+// capacity; without it every chunk has a workgroup of its own.
+// (Instances of two pages per wave, chunks above kFusedWaves pages, take one chunk per
+// workgroup.)
+constexpr int kLateMissWorkgroups = 4;
+int miss_workgroups(bool late, int nchunks, int chunk) {
+  return late && chunk <= prr::kFusedWaves ? std::min(nchunks, kLateMissWorkgroups) : nchunks;
+}
+
 // |A| for a budget and forced set, and the number of non-forced pages to pick.
 void budget(int k_select, int n_forced, int forced_in_budget, int num_pages, int& total, int& kextra) {
   kextra = forced_in_budget ? std::max(0, k_select - n_forced) : k_select;
@@ -279,6 +290,7 @@ int32_t prr_fused_grid(const prr_dims* dims, const prr_step_params* sp, int32_t 
   a.n_miss = L.nchunks;
   a.late = a.schedule == 1 && sp->late_spec && sp->mode != PRR_RECOMPUTE_ON_MISS;
   a.n_late = a.late ? late_slots(dims, a.n_score, L.nchunks, sp->chunk_pages) : 0;
+  a.miss_wgs = miss_workgroups(a.late, L.nchunks, sp->chunk_pages);
   return prr::fused_grid(a);
 }
 
@@ -708,6 +720,7 @@ static prr_status fused_layer(const prr_dims* dims, const prr_step_params* sp, c
   a.late = prr && sp->late_spec && sp->mode != PRR_RECOMPUTE_ON_MISS;
   a.readahead = a.late && sp->late_spec == 1;  // (kept only if the grid is resident at once)
   a.n_late = a.late ? late_slots(dims, a.n_score, L.nchunks, sp->chunk_pages) : 0;
+  a.miss_wgs = miss_workgroups(a.late, L.nchunks, sp->chunk_pages);
   a.nparts = L.nparts;
   a.n_forced = sp->n_forced;
   a.meta_mean = dims->meta_kind == PRR_META_MEAN;

@@ -13,7 +13,7 @@ int fused_grid(const FusedLaunch& a) {
   int per = a.n_score + 1;
   if (a.schedule != 0) per += 1;
   if (a.schedule == 1) per += a.n_spec + a.n_late;
-  if (a.schedule != 2) per += a.n_miss + a.group;
+  if (a.schedule != 2) per += a.miss_wgs + a.group;
   return H * per;
 }
 

@@ -541,20 +541,28 @@ __device__ __forceinline__ float v_elem(const u32x4_t& v, int e) {
 // waves each reading the whole of q put eight times the traffic through the CU's memory
 // pipeline at the launch's start, where the attending workgroups share CUs with score
 // workgroups that are still reading metadata.  Called by every thread (one barrier).
-__device__ __forceinline__ void load_q(const FusedLaunch& a, int h, u32x4_t (&qf)[4], u32x4_t* qs) {
-  const int t = threadIdx.x, lane = lane_id(), j = lane >> 4, n = lane & 15;
-  const int G = a.group;
+// this lane's MFMA operand of q (query head n of the group, channels 32j + 8s ..) from the
+// rows staged in LDS
+__device__ __forceinline__ void fetch_q(const FusedLaunch& a, u32x4_t (&qf)[4], const u32x4_t* qs) {
+  const int lane = lane_id(), j = lane >> 4, n = lane & 15;
   constexpr int kRow = kHeadDim / 8;  // 16-byte words per row
-  const u32x4_t* qh = reinterpret_cast<const u32x4_t*>(static_cast<const uint16_t*>(a.q) + (size_t)h * G * kHeadDim);
-  if (t < G * kRow) qs[t] = qh[t];
-  __syncthreads();
-  if (n < G) {
+  if (n < a.group) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) qf[s] = qs[n * kRow + 4 * j + s];
   } else {
 #pragma unroll
     for (int s = 0; s < 4; ++s) qf[s] = u32x4_t{0, 0, 0, 0};
   }
+}
+
+__device__ __forceinline__ void load_q(const FusedLaunch& a, int h, u32x4_t (&qf)[4], u32x4_t* qs) {
+  const int t = threadIdx.x;
+  const int G = a.group;
+  constexpr int kRow = kHeadDim / 8;
+  const u32x4_t* qh = reinterpret_cast<const u32x4_t*>(static_cast<const uint16_t*>(a.q) + (size_t)h * G * kHeadDim);
+  if (t < G * kRow) qs[t] = qh[t];
+  __syncthreads();
+  fetch_q(a, qf, qs);
 }
 
 template <bool BF16, int PS, int NPW>
@@ -1755,14 +1763,16 @@ __device__ __forceinline__ void role_late(const FusedLaunch& a, uint32_t ep, int
   }
 }
 
+// Chunk c of the missed list (its state to slot n_spec + c); false once the list holds no
+// chunk c.  The count and the chunk's entries are loaded together; the entries are
+// published before the count, so they are usually valid when the count is.
 template <bool BF16, int PS, int NPW>
-__device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int h, int u, FLds& U) {
-  // the count and this wave's list entries are loaded together; the entries are
-  // published before the count, so they are usually valid when the count is
-  const int start = u * a.chunk;
+__device__ __forceinline__ bool miss_chunk(const FusedLaunch& a, uint32_t ep, int h, int c, bool first, FLds& U) {
+  const int start = c * a.chunk;
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
-  u32x4_t qf[4];
-  load_q(a, h, qf, U.qs);
+  u32x4_t qf[4];  // (q is staged once; a later chunk reads it from LDS again)
+  if (first) load_q(a, h, qf, U.qs);
+  else fetch_q(a, qf, U.qs);
   static_assert(1 + kFW * NPW <= 2 + 2 * kFW, "broadcast area");
   const uint64_t* ml = a.t_mlist + (size_t)h * a.cap;
   if (w == 0) {
@@ -1771,7 +1781,7 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int
     const int i = start + lane;
     uint64_t vm = 0, ve = 0;
     for (int it = 0; it < kFSpin; ++it) {
-      vm = get_tag(rep_at(a.t_mcnt, h, u));
+      vm = get_tag(rep_at(a.t_mcnt, h, c));
       if (lane < kFW * NPW) ve = get_tag(&ml[min(i, a.cap - 1)]);  // (only the entries of this chunk)
       if (tag_is(vm, ep)) {
         const uint32_t mv = (uint32_t)vm;
@@ -1784,11 +1794,11 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int
     if (lane == 0) U.bc[0] = (uint32_t)vm;
     if (lane < kFW * NPW) U.bc[1 + lane] = (uint32_t)ve;
   }
-  __syncthreads();
+  __syncthreads();  // (a previous chunk's readers of U.bc are past its publishing barrier)
   const uint32_t mv = U.bc[0];
-  if (mv & kSelfMiss) return;
+  if (mv & kSelfMiss) return false;
   const int nM = (int)(mv & kCountMask);
-  if (start >= nM) return;
+  if (start >= nM) return false;
   const int cnt = min(a.chunk, nM - start);
   int pg[NPW];
   uint32_t keep = 0;
@@ -1806,7 +1816,22 @@ __device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int
   }
   WaveStates<NPW> st;
   wave_attend<BF16, PS, NPW>(a, h, qf, pg, st);
-  fold_publish<NPW>(a, kStampMiss, pub_dst(a, h, a.n_spec + u), ep, st, keep, U.attn);
+  fold_publish<NPW>(a, kStampMiss, pub_dst(a, h, a.n_spec + c), ep, st, keep, U.attn);
+  return true;
+}
+
+// Missed-list workgroup u of a KV head: chunks u, u + miss_wgs, .. (one pass when the list
+// is short, as it is once late speculation covers most of A).  Instances of two pages per
+// wave take one chunk each (the launcher gives them a workgroup per chunk): a loop around
+// their attention would cost them occupancy.
+template <bool BF16, int PS, int NPW>
+__device__ __forceinline__ void role_miss(const FusedLaunch& a, uint32_t ep, int h, int u, FLds& U) {
+  if constexpr (NPW == 1) {
+    for (int c = u; c < a.n_miss; c += a.miss_wgs)
+      if (!miss_chunk<BF16, PS, NPW>(a, ep, h, c, c == u, U)) return;
+  } else {
+    miss_chunk<BF16, PS, NPW>(a, ep, h, u, true, U);
+  }
 }
 
 // ------------------------------------------------------------------------ merge
@@ -1962,11 +1987,11 @@ __device__ __forceinline__ void fused_roles(const FusedLaunch& a, uint32_t ep, F
     }
     b -= H * a.n_late;
   }
-  if (b < H * a.n_miss) {
-    role_miss<BF16, PS, NPW>(a, ep, b / a.n_miss, b % a.n_miss, U);
+  if (b < H * a.miss_wgs) {
+    role_miss<BF16, PS, NPW>(a, ep, b / a.miss_wgs, b % a.miss_wgs, U);
     return;
   }
-  b -= H * a.n_miss;
+  b -= H * a.miss_wgs;
   if (b < H * a.group) role_merge<BF16>(a, ep, b / a.group, b % a.group, U.merge, U.bc);
 }
 

@@ -135,6 +135,7 @@ struct FusedLaunch {
   int num_kv_heads, group, max_pages, num_pages, num_tokens;
   int kextra_a, kextra_p, cap, chunk;
   int n_score, n_spec, n_miss, n_late, nparts;  // workgroups per KV head; partial slots per KV head
+  int miss_wgs;  // workgroups per KV head for the missed list (n_miss chunks, taken in turn)
   int late;  // late speculation on (PRR schedule)
   int readahead;  // score workgroups read the first late pages ahead (allowed; decided at launch)
   int n_forced;

@@ -219,14 +219,18 @@ def test_fused_schedules_need_page_16_or_64(P, ps):
 def test_fused_grid_counts_the_roles(P):
     """prr_fused_grid: per KV head, the score workgroups (128 pages each), the select, the
     predict (PRR and prefill), the speculation and late workgroups (PRR, one per chunk of the
-    list capacity), the missed-page workgroups and the merge (one per query head)."""
+    list capacity), the missed-page workgroups (one per chunk, or four taking the chunks in
+    turn with late speculation at one page per wave) and the merge (one per query head)."""
     d = P.make_dims(32, 2, 16, 8192, P.PRR_BF16)
     p = P.prr_step_params()
     p.num_tokens, p.num_pages, p.k_select, p.p_select, p.cap, p.chunk_pages, p.epoch = 131072, 8192, 256, 256, 256, 8, 1
     p.alpha, p.beta, p.gamma = 0.5, 0.5, 0.0
     n_score, nch, g = 64, 32, 16
     p.late_spec = 1
-    assert P.prr_fused_grid(d, p, P.PRR_SCHED_FUSED_PRR) == 2 * (n_score + 2 + 3 * nch + g)
+    assert P.prr_fused_grid(d, p, P.PRR_SCHED_FUSED_PRR) == 2 * (n_score + 2 + 2 * nch + 4 + g)
+    p.chunk_pages = 16  # (two pages per wave: a missed-page workgroup per chunk)
+    assert P.prr_fused_grid(d, p, P.PRR_SCHED_FUSED_PRR) == 2 * (n_score + 2 + 3 * 16 + g)
+    p.chunk_pages = 8
     p.late_spec = 0
     assert P.prr_fused_grid(d, p, P.PRR_SCHED_FUSED_PRR) == 2 * (n_score + 2 + 2 * nch + g)
     assert P.prr_fused_grid(d, p, P.PRR_SCHED_FUSED_PREFILL) == 2 * (n_score + 2)
