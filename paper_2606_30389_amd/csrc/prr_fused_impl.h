@@ -52,9 +52,11 @@ constexpr int kCandWave = 12 * kWave;  // candidates ranked by one wave (12 per 
 // different memory channels, so polls of many lists do not queue on one channel.
 constexpr int kCandStride = kFScorePages + 4;
 // Rank, among this step's candidates, whose key bounds the next step's late pages from
-// below: 1.375 |A|.  A lower rank leaves pages of A to the missed list (1.125 |A| does on
-// 128K contexts), a higher one attends more pages that turn out not to be in A.
-__host__ __device__ constexpr int kLateRank(int a) { return (11 * a) / 8; }
+// below: 1.25 |A|.  A lower rank leaves pages of A to the missed list (1.125 |A| does on
+// 128K contexts); a higher one attends more pages that turn out not to be in A, and once
+// the late pages outnumber what the late workgroups hold the surplus goes to the missed
+// list as well.
+__host__ __device__ constexpr int kLateRank(int a) { return (5 * a) / 4; }
 
 __device__ __forceinline__ void put_tag(uint64_t* p, uint32_t v, uint32_t epoch) {
   __hip_atomic_store(p, ((uint64_t)epoch << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1019,7 +1021,7 @@ __device__ __forceinline__ void full_gather(const FusedLaunch& a, uint32_t ep, c
 }
 
 // Lower bound of the next step's candidates: the score of rank `k` (2.5 |A| for the
-// candidates, 1.375 |A| for late speculation) among this step's candidates, kept as a
+// candidates, 1.25 |A| for late speculation) among this step's candidates, kept as a
 // ratio to |q-bar|_1 (unchanged when fewer candidates exist and `keep` is set; -inf,
 // i.e. every page, after a fallback that found fewer).
 __device__ __forceinline__ float key_value(uint32_t k) {
@@ -1267,7 +1269,7 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
       if (a.covered_count) a.covered_count[h] = prr ? max(nMiss - nM, 0) : 0;  // (0 when M = A)
     }
   } else if (w == 1 || (w == 2 && a.late)) {
-    // the next step's lower bounds: rank 2.5|A| (candidates of A) and 1.375|A| (late pages)
+    // the next step's lower bounds: rank 2.5|A| (candidates of A) and 1.25|A| (late pages)
     const int k = w == 1 ? (5 * a.kextra_a) / 2 : kLateRank(a.kextra_a);
     const SelThreshold th = wsel_threshold<NK>(key, cand, max(k, 1), L.ws[w], true);
     if (lane == 0 && th.mode == 2 && qn > 0.0f) a.win[4 * h + (w == 1 ? 0 : 2)] = __float_as_uint(key_value(th.T) / qn);
