@@ -223,41 +223,55 @@ def best_chunk(page_size, serial=False):
 
 def delta_sweep(args, cfg):
     """Section 4.4's offline profiling on the fused PRR step (with late speculation): for
-    each context length (a prefix of layer 0's cache) and budget delta = |P| / |A|, the
+    each context length (a prefix of the layers' caches) and budget delta = |P| / |A|, the
     selection window (launch start to the threshold's publication, as the select
     workgroup stamps it) and the speculation latency (launch start to the last
     speculation workgroup holding its pages' states), both from the launch's phase
-    timestamps, medians over tokens; plus the step's latency from HIP events."""
+    timestamps, medians over layers and tokens; plus the step's latency from HIP events.
+    Four layers with caches of their own are stepped in turn, so that, as in a model, a
+    layer's K/V is not still in the memory-side cache from its previous step."""
     import torch
     from paper_2606_30389_amd import _lib as L
     from paper_2606_30389_amd import runtime as R
     from paper_2606_30389_amd.profile_summary import kernel_source_hash
     dev = torch.device("cuda:0")
-    li = W.layer_inputs(cfg, 0)
-    k = R.bits_tensor(li.k_bits, {"bf16": torch.bfloat16, "f16": torch.float16}[cfg.dtype], dev)
-    v = R.bits_tensor(li.v_bits, k.dtype, dev)
+    n_lay = 4
+    tdt = {"bf16": torch.bfloat16, "f16": torch.float16}[cfg.dtype]
+    kv = []
+    for layer in range(n_lay):
+        li = W.layer_inputs(cfg, layer)
+        kv.append((R.bits_tensor(li.k_bits, tdt, dev), R.bits_tensor(li.v_bits, tdt, dev)))
+        del li
     n_tok = 24
     _, qb = W.query_trajectory(cfg, 0, steps=8 + 2 * n_tok + 40)
     rows = []
     s = torch.cuda.Stream(device=dev)
-    stamps = torch.zeros(1, 16, 1024, dtype=torch.int64, device=dev)
+    stamps = torch.zeros(n_lay, 16, 1024, dtype=torch.int64, device=dev)
     contexts = [c for c in (4096, 8192, 16384, 32768, 65536, 131072) if c <= cfg.context]
     serial_us = {}
+
+    def make_stack(ctx, **kw):
+        npg = ctx // cfg.page_size
+        pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
+                          num_tokens=ctx, k_select=cfg.k_select, forced=cfg.forced_pages(npg),
+                          forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
+                          alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma, **kw)
+        pc.max_pages = cfg.num_pages
+        sts = []
+        for k, v in kv:
+            st = R.LayerState(pc, dev, k=k, v=v)
+            st.build_meta()
+            sts.append(st)
+        qs = R.bits_tensor(qb, pc.torch_dtype, dev)
+        q = qs[0].clone()
+        return R.DecodeStack(sts, [q] * n_lay, dev), sts, qs, q
+
     for ctx in contexts:
         for delta in (1.0, 1.25, 1.5, 2.0):
             npg = ctx // cfg.page_size
             p_sel = int(round(delta * cfg.k_select))
-            pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
-                              num_tokens=ctx, k_select=cfg.k_select, forced=cfg.forced_pages(npg),
-                              forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
-                              alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma,
-                              chunk_pages=best_chunk(cfg.page_size), p_select=p_sel)
-            pc.max_pages = cfg.num_pages
-            st = R.LayerState(pc, dev, k=k, v=v)
-            st.build_meta()
-            qs = R.bits_tensor(qb, pc.torch_dtype, dev)
-            q = qs[0].clone()
-            stack = R.DecodeStack([st], [q], dev)
+            stack, sts, qs, q = make_stack(ctx, chunk_pages=best_chunk(cfg.page_size), p_select=p_sel)
+            st = sts[0]
             stack.params.late_spec = 1
             t = [0]
 
@@ -271,7 +285,7 @@ def delta_sweep(args, cfg):
                     step()
                 # roles in grid order: score, select, predict, speculation, late, missed, merge
                 H, nsc = cfg.num_kv_heads, -(-npg // 128)
-                nspec = -(-st.cap // pc.chunk_pages)
+                nspec = -(-st.cap // st.cfg.chunk_pages)
                 sel0, spec0 = H * nsc, H * (nsc + 2)
                 win, spec, hits = [], [], []
                 stack.params.phase_stamps = stamps.data_ptr()
@@ -279,13 +293,13 @@ def delta_sweep(args, cfg):
                     stamps.zero_()
                     step()
                     torch.cuda.synchronize()
-                    a = stamps[0].cpu().numpy()
-                    t0 = a[0][a[0] > 0].min()
-                    thr = a[4, sel0:sel0 + H]
-                    att = a[13, spec0:spec0 + H * nspec]
-                    win.append((thr.max() - t0) / 100.0)
-                    spec.append((att[att > 0].max() - t0) / 100.0 if (att > 0).any() else 0.0)
-                    hits.append(1.0 - st.missed.sum().item() / (H * cfg.selected_count))
+                    for a in stamps.cpu().numpy():
+                        t0 = a[0][a[0] > 0].min()
+                        thr = a[4, sel0:sel0 + H]
+                        att = a[13, spec0:spec0 + H * nspec]
+                        win.append((thr.max() - t0) / 100.0)
+                        spec.append((att[att > 0].max() - t0) / 100.0 if (att > 0).any() else 0.0)
+                    hits.append(1.0 - sum(x.missed.sum().item() for x in sts) / (n_lay * H * cfg.selected_count))
                 stack.params.phase_stamps = None
                 torch.cuda.synchronize()
                 a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -296,23 +310,12 @@ def delta_sweep(args, cfg):
             torch.cuda.synchronize()
             rows.append({"context": ctx, "delta": delta, "select_us": round(float(np.median(win)), 2),
                          "spec_us": round(float(np.median(spec)), 2),
-                         "fused_prr_late_us": round(1000.0 * a_ev.elapsed_time(b_ev) / n_tok, 2),
+                         "fused_prr_late_us": round(1000.0 * a_ev.elapsed_time(b_ev) / (n_tok * n_lay), 2),
                          "hit_rate": round(float(np.mean(hits)), 4)})
             print(f"[sweep] {rows[-1]}", file=sys.stderr, flush=True)
-            del stack, st
+            del stack, sts, st
         # the select-then-attend step at this context (no speculation), for comparison
-        npg = ctx // cfg.page_size
-        pc = R.PathConfig(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, page_size=cfg.page_size,
-                          num_tokens=ctx, k_select=cfg.k_select, forced=cfg.forced_pages(npg),
-                          forced_in_budget=cfg.forced_in_budget, dtype=cfg.dtype, meta_kind=cfg.meta_kind,
-                          alpha=cfg.alpha, beta=cfg.beta, gamma=cfg.gamma,
-                          chunk_pages=best_chunk(cfg.page_size, serial=True))
-        pc.max_pages = cfg.num_pages
-        st = R.LayerState(pc, dev, k=k, v=v)
-        st.build_meta()
-        qs = R.bits_tensor(qb, pc.torch_dtype, dev)
-        q = qs[0].clone()
-        stack = R.DecodeStack([st], [q], dev)
+        stack, sts, qs, q = make_stack(ctx, chunk_pages=best_chunk(cfg.page_size, serial=True))
         with torch.cuda.stream(s):
             for i in range(8):
                 q.copy_(qs[i])
@@ -324,9 +327,9 @@ def delta_sweep(args, cfg):
                 stack.step(L.PRR_SCHED_FUSED_SERIAL, s)
             b_ev.record(s)
         torch.cuda.synchronize()
-        serial_us[ctx] = round(1000.0 * a_ev.elapsed_time(b_ev) / n_tok, 2)
+        serial_us[ctx] = round(1000.0 * a_ev.elapsed_time(b_ev) / (n_tok * n_lay), 2)
         print(f"[sweep] context {ctx}: fused serial {serial_us[ctx]} us", file=sys.stderr, flush=True)
-        del stack, st
+        del stack, sts
     pick = {c: R.pick_delta(rows, c) for c in contexts}
     out = {"sweep": "speculation budget (Section 4.4) on the fused PRR step with late speculation",
            "config": cfg.name, "workload": f"{cfg.name} layer 0, context prefixes", "kernel_source": kernel_source_hash(),
