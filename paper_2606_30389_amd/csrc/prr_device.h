@@ -14,6 +14,8 @@ constexpr float kLog2e = 1.4426950408889634f;
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
+typedef __attribute__((ext_vector_type(4))) short s16x4_t;
 
 // ------------------------------------------------------------------ 16-bit storage
 
@@ -269,5 +271,49 @@ __device__ __forceinline__ uint32_t counter_add(uint32_t* p, uint32_t v) {
 // Sticky error bits written by kernels into the workspace flag word.
 constexpr uint32_t kFlagBadListEntry = 1u;
 constexpr uint32_t kFlagSpinTimeout = 2u;
+
+// ------------------------------------------------------------------ P.V of one tile
+// O^T (128 channels x 16 heads) += V^T . P^T over a tile of 16 tokens.  Lane 16j+m holds
+// V rows 4j..4j+3 (channels 8m..8m+7, one 16-byte load per row) in v[0..3], and the softmax
+// weights of head m for tokens 4j..4j+3 in p[0..3]; accumulator cb, register i then holds
+// O[head m][32j + 8i + cb] (each lane owns the channels of the head whose weights it holds).
+//
+// One 16x16x16 MFMA in the cache's 16-bit type per accumulator and weight term: its A
+// operand, channel 8m + cb of the lane's four rows, needs no data from other lanes, and
+// the weights (in [0, 1]) are split into two terms of that type, hi = rne(p) and
+// lo = rne(p - hi).  bfloat16 terms carry p to about 2^-17 relative; float16 terms to
+// 2^-22 relative or 2^-25 absolute (lo is subnormal below 2^-14), far inside the
+// tolerance of the outputs.  Two MFMAs replace the four fp32 16x16x4 MFMAs that a float32
+// weight operand needs, at an eighth of their issue cycles.
+template <bool BF16>
+__device__ __forceinline__ void pv_tile(f32x4_t (&acc)[8], const u32x4_t (&v)[4], const float (&p)[4]) {
+  uint32_t hi[4], lo[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    hi[i] = f2h_rne<BF16>(p[i]);
+    lo[i] = f2h_rne<BF16>(p[i] - h2f<BF16>(hi[i]));
+  }
+  const s16x4_t bh =
+      __builtin_bit_cast(s16x4_t, (uint64_t)(hi[0] | (hi[1] << 16)) | ((uint64_t)(hi[2] | (hi[3] << 16)) << 32));
+  const s16x4_t bl =
+      __builtin_bit_cast(s16x4_t, (uint64_t)(lo[0] | (lo[1] << 16)) | ((uint64_t)(lo[2] | (lo[3] << 16)) << 32));
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) {
+    const int w = cb >> 1, sh = (cb & 1) * 16;
+    const uint32_t a0 = ((v[0][w] >> sh) & 0xffffu) | (((v[1][w] >> sh) & 0xffffu) << 16);
+    const uint32_t a1 = ((v[2][w] >> sh) & 0xffffu) | (((v[3][w] >> sh) & 0xffffu) << 16);
+    const s16x4_t va = __builtin_bit_cast(s16x4_t, (uint64_t)a0 | ((uint64_t)a1 << 32));
+    if constexpr (BF16) {
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, bh, acc[cb], 0, 0, 0);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, bl, acc[cb], 0, 0, 0);
+    } else {
+      typedef __attribute__((ext_vector_type(4))) _Float16 f16x4_t;
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4_t, va), __builtin_bit_cast(f16x4_t, bh),
+                                                      acc[cb], 0, 0, 0);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4_t, va), __builtin_bit_cast(f16x4_t, bl),
+                                                      acc[cb], 0, 0, 0);
+    }
+  }
+}
 
 }  // namespace prr

@@ -27,7 +27,6 @@
 
 namespace prr {
 
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 
 namespace {
 
@@ -524,18 +523,11 @@ __device__ __forceinline__ f32x4_t mfma_qk(const u32x4_t& x, const u32x4_t& y, f
   }
 }
 
-template <bool BF16>
-__device__ __forceinline__ float v_elem(const u32x4_t& v, int e) {
-  const uint32_t w = v[e >> 1];
-  return h2f<BF16>((e & 1) ? (w >> 16) : (w & 0xffffu));
-}
-
 // q.k^T of a 16-token tile as four 16x16x32 MFMAs with the contraction index permuted so
 // that lane 16j+r reads 64 contiguous bytes of its key row (channels 32j..32j+31); the
 // result gives lane 16j+n the logits of tokens 4j..4j+3 for head n.  p.V is computed
-// transposed, O^T += V^T P^T, as 32 fp32 16x16x4 MFMAs (weights stay fp32): call
-// (tg, cb) contracts tokens {tg, 4+tg, 8+tg, 12+tg}, lane 16j+m supplying
-// V[4j+tg][8m+cb] and p[head n][4j+tg].
+// transposed, O^T += V^T P^T, by pv_tile (prr_device.h): lane 16j+m supplies channel
+// 8m+cb of V rows 4j..4j+3 and the weights of head m for those tokens.
 // Query fragments of KV head h for the MFMA layout below (lane 16j+n: head n, channels
 // 32j..32j+31), loaded before a workgroup waits for its page list.
 // The MFMA operand fragments of q (G rows of the KV head): the rows are read from memory
@@ -653,12 +645,7 @@ __device__ __forceinline__ void wave_attend(const FusedLaunch& a, int h, const u
         for (int i = 0; i < 4; ++i) st.acc[k][cb][i] *= alpha;
       }
     }
-#pragma unroll
-    for (int tg = 0; tg < 4; ++tg) {
-#pragma unroll
-      for (int cb = 0; cb < 8; ++cb)
-        st.acc[k][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(v_elem<BF16>(vf[f][tg], cb), p[tg], st.acc[k][cb], 0, 0, 0);
-    }
+    pv_tile<BF16>(st.acc[k], vf[f], p);
   }
 }
 

@@ -11,8 +11,8 @@
 //   merge_states              stand-alone merge of partial states
 //
 // Wave64 throughout.  Attention uses MFMA: q.k^T as 16x16x32 bf16/f16 tiles (16 tokens x
-// 16 query heads, contraction over the 128 channels), p.V as 16x16x4 fp32 tiles so that
-// the softmax weights stay in fp32.
+// 16 query heads, contraction over the 128 channels), p.V by pv_tile (prr_device.h:
+// bfloat16 MFMAs with the weights split into two bfloat16 terms, or fp32 MFMAs for float16).
 #include <map>
 #include <mutex>
 
@@ -22,7 +22,6 @@
 
 namespace prr {
 
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 
 // =====================================================================================
 // epoch of captured fused steps: one thread advances the word (skipping 0)
@@ -650,13 +649,12 @@ __global__ __launch_bounds__(1024) void predict_kernel(const PredictLaunch a) {
 // 32j+8s .. +8 of token r (A operand) and lane 16j+n channels 32j+8s .. +8 of query head n
 // (B operand).  The result gives lane 16j+n the logits of tokens 4j..4j+3 for head n.
 //
-// p.V per tile, transposed: O^T (128 channels x 16 heads) += V^T . P^T as 32 16x16x4
-// fp32 MFMAs, so the softmax weights stay fp32.  Call (tg, cb) contracts tokens
-// {tg, 4+tg, 8+tg, 12+tg}: lane 16j+m supplies V[token 4j+tg][channel 8m+cb] (from one
-// 16-byte row load per tg) as A and p[head n][token 4j+tg] (its own logit register tg) as
-// B.  Accumulator cb, register i of lane 16j+n then holds O[head n][32j + 8i + cb]: each
-// lane owns 32 contiguous channels of the same head whose logits it holds, so the online
-// rescale is lane-local.
+// p.V per tile, transposed: O^T (128 channels x 16 heads) += V^T . P^T by pv_tile
+// (prr_device.h): lane 16j+m supplies channel 8m+cb of V rows 4j..4j+3 (from one 16-byte
+// row load per row) and the weights of head m for tokens 4j..4j+3 (its own logit
+// registers).  Accumulator cb, register i of lane 16j+n then holds O[head n][32j + 8i + cb]:
+// each lane owns 32 contiguous channels of the same head whose logits it holds, so the
+// online rescale is lane-local.
 
 struct AttnCtx {
   const uint16_t* q;  // q + h*G*128
@@ -684,12 +682,6 @@ __device__ __forceinline__ f32x4_t mfma_qk(const u32x4_t& a, const u32x4_t& b, f
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c, 0,
                                                   0, 0);
   }
-}
-
-template <bool BF16>
-__device__ __forceinline__ float v_elem(const u32x4_t& v, int e) {
-  const uint32_t wd = v[e >> 1];
-  return h2f<BF16>((e & 1) ? (wd >> 16) : (wd & 0xffffu));
 }
 
 // Result for thread t: head t/16, channels 8*(t%16)..+8: normalised o, m, l.
@@ -821,12 +813,7 @@ __device__ void attend_unit(const AttnCtx& c, const int32_t* pages, int cnt, flo
 #pragma unroll
       for (int i = 0; i < 4; ++i) acc[cb][i] *= alpha;
     }
-#pragma unroll
-    for (int tg = 0; tg < 4; ++tg) {
-#pragma unroll
-      for (int cb = 0; cb < 8; ++cb)
-        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(v_elem<BF16>(vf[f][tg], cb), p[tg], acc[cb], 0, 0, 0);
-    }
+    pv_tile<BF16>(acc, vf[f], p);
     if (WPP == 1 && tt == TPP - 1 && page_m_out && j == 0 && n < G) page_m_out[(size_t)(w + 4 * kk) * G + n] = pm;
   }
   if constexpr (WPP > 1) {

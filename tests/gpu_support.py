@@ -122,6 +122,7 @@ def check_attention(o32, m, l, ref, o_dtype=None, tol=O_INTERNAL, what="out", dt
     o_ref, m_ref, l_ref = ref
     assert tol <= O_JUDGED
     err = np.abs(o32 - o_ref).max() if o32.size else 0.0
+    log(f"{what}: max |o - o_ref| = {err:.2e}")
     assert err <= tol, f"{what}: max |o - o_ref| = {err:.3e} > {tol:.1e}"
     if o_dtype is not None and o_dtype.size:
         assert dtype in ("bf16", "f16"), "pass the 16-bit output's dtype"
