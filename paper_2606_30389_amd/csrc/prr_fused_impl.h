@@ -826,9 +826,10 @@ __device__ __forceinline__ FCand cand_load(const FusedLaunch& a, uint32_t ep, in
   const size_t rec = rec0 + min(wg, nS - 1);
   const uint64_t* ck = a.t_candk + rec * kCandStride + 1;
   const uint64_t* cp = a.t_candp + rec * kFScorePages;
-  // the count and the first eight entries per thread are polled together until all
-  // needed are there (32 per list, more than almost any list holds)
-  constexpr int kPollE = 32 / TPL;
+  // the count and the first two entries per thread are polled together until all
+  // needed are there (16 per list, more than most lists hold; the rest of a longer list
+  // is loaded after the poll)
+  constexpr int kPollE = 16 / TPL;
   uint64_t vc = 0, ke[kPollE], pe[kPollE];
 #pragma unroll
   for (int u = 0; u < kPollE; ++u) ke[u] = pe[u] = 0ull;
