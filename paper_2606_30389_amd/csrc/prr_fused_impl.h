@@ -1008,7 +1008,7 @@ __device__ __forceinline__ void full_gather(const FusedLaunch& a, uint32_t ep, c
   }
 }
 
-// Lower bound of the next step's candidates: the score of rank `k` (2.5 |A| for the
+// Lower bound of the next step's candidates: the score of rank `k` (2.25 |A| for the
 // candidates, 1.25 |A| for late speculation) among this step's candidates, kept as a
 // ratio to |q-bar|_1 (unchanged when fewer candidates exist and `keep` is set; -inf,
 // i.e. every page, after a fallback that found fewer).
@@ -1148,7 +1148,7 @@ __device__ __forceinline__ void select_finish(const FusedLaunch& a, uint32_t ep,
     wave_attend<BF16, PS, 1>(a, h, qf, pg, st);
     fold_publish<1>(a, kStampMiss, pub_dst(a, h, a.n_spec), ep, st, 1u, U.attn);
   }
-  update_window<J>(a, a.win + 4 * h, qn, key, cand, (5 * a.kextra_a) / 2, keep_window, U.sel.sel);
+  update_window<J>(a, a.win + 4 * h, qn, key, cand, (9 * a.kextra_a) / 4, keep_window, U.sel.sel);
   if (a.late) update_window<J>(a, a.win + 4 * h + 2, qn, key, cand, kLateRank(a.kextra_a), true, U.sel.sel);
 }
 
@@ -1257,8 +1257,8 @@ __device__ __forceinline__ void select_wave(const FusedLaunch& a, uint32_t ep, i
       if (a.covered_count) a.covered_count[h] = prr ? max(nMiss - nM, 0) : 0;  // (0 when M = A)
     }
   } else if (w == 1 || (w == 2 && a.late)) {
-    // the next step's lower bounds: rank 2.5|A| (candidates of A) and 1.25|A| (late pages)
-    const int k = w == 1 ? (5 * a.kextra_a) / 2 : kLateRank(a.kextra_a);
+    // the next step's lower bounds: rank 2.25|A| (candidates of A) and 1.25|A| (late pages)
+    const int k = w == 1 ? (9 * a.kextra_a) / 4 : kLateRank(a.kextra_a);
     const SelThreshold th = wsel_threshold<NK>(key, cand, max(k, 1), L.ws[w], true);
     if (lane == 0 && th.mode == 2 && qn > 0.0f) a.win[4 * h + (w == 1 ? 0 : 2)] = __float_as_uint(key_value(th.T) / qn);
   }
