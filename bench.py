@@ -580,31 +580,21 @@ def extra_measurements(args, cfg, pc, layers, stack, s, dev, L, R, torch, n_laye
     with torch.cuda.stream(s):
         floor["graph_us"] = round(1000.0 * _timed_ms(torch, s, g.replay, 20) / n_layers, 3)
     floor["fused_prr_grid_without_late"] = grid
-    # a dependency between two streams: empty one-workgroup kernels chained on one stream,
-    # against the same chain alternating between two streams with an event wait per hop
+    # a dependency between two streams: a chain of empty one-workgroup kernels on one stream,
+    # against the same chain alternating between two streams with a dependency per hop (an
+    # event, or a stream memory write and wait); the library enqueues each chain in one call,
+    # so the host's enqueue cost stays out of the per-hop time
     p2 = torch.cuda.Stream(device=dev)
     n_hop = 200
-    one = _timed_ms(torch, s, lambda: L.prr_empty_launch(1, 64, s), n_hop)
-    evs = [torch.cuda.Event() for _ in range(n_hop + 1)]
-
-    def hops():
-        for i in range(n_hop):
-            st_a, st_b = (s, p2) if i % 2 == 0 else (p2, s)
-            L.prr_empty_launch(1, 64, st_a)
-            evs[i].record(st_a)
-            st_b.wait_event(evs[i])
-        p2.wait_stream(s)
-        s.wait_stream(p2)
-
-    torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record(s)
-    hops()
-    b.record(s)
-    torch.cuda.synchronize()
-    floor["one_stream_chain_us"] = round(1000.0 * one, 3)
-    floor["two_stream_chain_us"] = round(1000.0 * a.elapsed_time(b) / n_hop, 3)
-    floor["cross_stream_dependency_us"] = round(floor["two_stream_chain_us"] - floor["one_stream_chain_us"], 3)
+    chain = {}
+    for name, mode in (("one", L.PRR_CHAIN_ONE_STREAM), ("events", L.PRR_CHAIN_EVENTS),
+                       ("memory", L.PRR_CHAIN_STREAM_MEMORY)):
+        L.prr_stream_chain(n_hop, mode, s, p2)  # (first use makes the events and words)
+        chain[name] = 1000.0 * _timed_ms(torch, s, lambda: L.prr_stream_chain(n_hop, mode, s, p2), 5) / n_hop
+    floor["one_stream_chain_us"] = round(chain["one"], 3)
+    floor["two_stream_chain_us"] = round(chain["events"], 3)
+    floor["cross_stream_dependency_us"] = round(chain["events"] - chain["one"], 3)
+    floor["stream_memory_dependency_us"] = round(chain["memory"] - chain["one"], 3)
     out["launch_floor"] = floor
     # HBM: a plain device copy (read + write) and a read-only reduction of 2 GiB
     nbytes = 2 << 30

@@ -364,6 +364,24 @@ prr_status prr_empty_launch(int32_t grid, int32_t threads, hipStream_t stream);
  * not a positive multiple of 16, or a grid outside [1, 2^20]. */
 prr_status prr_read_stream(const void* buf, size_t bytes, uint32_t* sink, int32_t grid, hipStream_t stream);
 
+/* Measurement helper: the cost of a dependency between two streams.  `n_hops` one-workgroup
+ * empty launches alternate between streams `a` and `b`, each followed by a dependency of
+ * the other stream on it: PRR_CHAIN_EVENTS records an event that the other stream waits
+ * for (hipStreamWaitEvent); PRR_CHAIN_STREAM_MEMORY writes a 64-bit value that the other
+ * stream waits for (hipStreamWriteValue64 / hipStreamWaitValue64, greater-or-equal);
+ * PRR_CHAIN_ONE_STREAM launches all of them on `a` without dependencies (`b` unused).  The
+ * chain ends on `a`, and all of it is enqueued here, so a timing on `a` around the call
+ * measures the device's cost per hop, not the caller's.  The events and the two
+ * stream-memory words are made on first use, once per device, and kept until the process
+ * ends; values only grow, so calls made one after the other share them, but chains that run
+ * at the same time on one device (from several host threads) must not be enqueued.  Errors:
+ * PRR_ERR_INVALID_ARG for n_hops odd or outside [2, 256], an unknown mode, or a == b with a
+ * dependency; PRR_ERR_UNSUPPORTED when the device has no stream memory waits; PRR_ERR_HIP. */
+#define PRR_CHAIN_ONE_STREAM 0
+#define PRR_CHAIN_EVENTS 1
+#define PRR_CHAIN_STREAM_MEMORY 2
+prr_status prr_stream_chain(int32_t n_hops, int32_t mode, hipStream_t a, hipStream_t b);
+
 /* Advance the device epoch word of captured fused steps (prr_step_params.epoch_dev)
  * by one, skipping 0: one single-thread launch on `stream`, so it can be captured with
  * the steps it precedes.  Errors: PRR_ERR_INVALID_ARG for a NULL or misaligned pointer. */

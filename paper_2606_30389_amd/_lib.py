@@ -45,7 +45,7 @@ EXPORTED = (
     "prr_spec_state_floats", "prr_build_page_meta", "prr_score_topk", "prr_predict",
     "prr_spec_attn", "prr_repair", "prr_merge_states", "prr_decode_step", "prr_calibrate",
     "prr_epoch_advance", "prr_pick_delta", "prr_score_topk_static", "prr_empty_launch", "prr_fused_grid",
-    "prr_read_stream",
+    "prr_read_stream", "prr_stream_chain",
 )
 
 
@@ -114,6 +114,7 @@ _SIGS = {
     "prr_epoch_advance": (_I, [_P, _P]),
     "prr_empty_launch": (_I, [_I, _I, _P]),
     "prr_read_stream": (_I, [_P, _S, _P, _I, _P]),
+    "prr_stream_chain": (_I, [_I, _I, _P, _P]),
     "prr_fused_grid": (_I, [_DIMS, _P, _I]),
     "prr_pick_delta": (_I, [_P, _P, _P, _P, _I, _I, _I, _P, _P, _P]),
 }
@@ -282,6 +283,15 @@ def prr_empty_launch(grid, threads, stream=None):
 
 def prr_read_stream(buf, nbytes, sink, grid, stream=None):
     _check(_lib.prr_read_stream(_ptr(buf), int(nbytes), _ptr(sink), int(grid), _stream(stream)))
+
+
+PRR_CHAIN_ONE_STREAM = 0
+PRR_CHAIN_EVENTS = 1
+PRR_CHAIN_STREAM_MEMORY = 2
+
+
+def prr_stream_chain(n_hops, mode, a=None, b=None):
+    _check(_lib.prr_stream_chain(int(n_hops), int(mode), _stream(a), _stream(b) if b is not None else None))
 
 
 def prr_fused_grid(dims, params, schedule):

@@ -7,6 +7,7 @@
 #include <stddef.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "prr.h"
 #include "prr_launch.h"
@@ -181,6 +182,19 @@ void budget(int k_select, int n_forced, int forced_in_budget, int num_pages, int
   total = std::min(num_pages, n_forced + kextra);
 }
 
+// prr_stream_chain's events and stream-memory words, made once per device and kept until
+// the process ends (a stream may still wait on them when the call returns).
+constexpr int kChainMaxHops = 256;
+constexpr int kChainMaxDevices = 16;
+struct ChainState {
+  bool events = false, words = false;
+  hipEvent_t ev[kChainMaxHops] = {};
+  void* word[2] = {nullptr, nullptr};
+  uint64_t value = 0;  // the last value written (values only grow)
+};
+std::mutex g_chain_mu;
+ChainState g_chain[kChainMaxDevices];
+
 }  // namespace
 
 namespace prr {
@@ -272,6 +286,51 @@ prr_status prr_read_stream(const void* buf, size_t bytes, uint32_t* sink, int32_
   if (bytes == 0 || bytes % 16 != 0) return fail(PRR_ERR_INVALID_ARG, "bytes %zu is not a positive multiple of 16", bytes);
   if (grid < 1 || grid > (1 << 20)) return fail(PRR_ERR_INVALID_ARG, "grid %d outside [1, 2^20]", grid);
   return hip_status(prr::launch_read_stream(buf, bytes, sink, grid, stream), "read stream");
+}
+
+prr_status prr_stream_chain(int32_t n_hops, int32_t mode, hipStream_t a, hipStream_t b) {
+  if (n_hops < 2 || n_hops > kChainMaxHops || n_hops % 2 != 0)
+    return fail(PRR_ERR_INVALID_ARG, "n_hops %d is not even in [2, %d]", n_hops, kChainMaxHops);
+  if (mode < PRR_CHAIN_ONE_STREAM || mode > PRR_CHAIN_STREAM_MEMORY) return fail(PRR_ERR_INVALID_ARG, "mode %d", mode);
+  if (mode == PRR_CHAIN_ONE_STREAM) {
+    for (int i = 0; i < n_hops; ++i) PRR_TRY(hip_status(prr::launch_empty(1, 64, a), "empty launch"));
+    return ok();
+  }
+  if (a == b) return fail(PRR_ERR_INVALID_ARG, "a dependency needs two different streams");
+  int dev = 0;
+  PRR_TRY(hip_status(hipGetDevice(&dev), "get device"));
+  if (dev < 0 || dev >= kChainMaxDevices) return fail(PRR_ERR_UNSUPPORTED, "device %d", dev);
+  std::lock_guard<std::mutex> guard(g_chain_mu);
+  ChainState& st = g_chain[dev];
+  if (!st.events) {
+    for (int i = 0; i < kChainMaxHops; ++i)
+      PRR_TRY(hip_status(hipEventCreateWithFlags(&st.ev[i], hipEventDisableTiming), "event create"));
+    st.events = true;
+  }
+  if (mode == PRR_CHAIN_STREAM_MEMORY && !st.words) {
+    int can = 0;
+    PRR_TRY(hip_status(hipDeviceGetAttribute(&can, hipDeviceAttributeCanUseStreamWaitValue, dev), "attribute"));
+    if (!can) return fail(PRR_ERR_UNSUPPORTED, "the device has no stream memory waits");
+    for (int k = 0; k < 2; ++k) {
+      PRR_TRY(hip_status(hipExtMallocWithFlags(&st.word[k], sizeof(uint64_t), hipMallocSignalMemory),
+                         "stream memory word"));
+      PRR_TRY(hip_status(hipStreamWriteValue64(a, st.word[k], 0ull, 0), "stream write"));
+    }
+    st.words = true;
+  }
+  for (int i = 0; i < n_hops; ++i) {
+    hipStream_t x = (i & 1) ? b : a, y = (i & 1) ? a : b;
+    PRR_TRY(hip_status(prr::launch_empty(1, 64, x), "empty launch"));
+    if (mode == PRR_CHAIN_EVENTS) {
+      PRR_TRY(hip_status(hipEventRecord(st.ev[i], x), "event record"));
+      PRR_TRY(hip_status(hipStreamWaitEvent(y, st.ev[i], 0), "stream wait"));
+    } else {
+      const uint64_t v = ++st.value;
+      PRR_TRY(hip_status(hipStreamWriteValue64(x, st.word[i & 1], v, 0), "stream write"));
+      PRR_TRY(hip_status(hipStreamWaitValue64(y, st.word[i & 1], v, hipStreamWaitValueGte, ~0ull), "stream wait"));
+    }
+  }
+  return ok();
 }
 
 int32_t prr_fused_grid(const prr_dims* dims, const prr_step_params* sp, int32_t schedule) {

@@ -147,6 +147,16 @@ def test_bad_spec_and_repair_args(P):
     _expect(P, 1, P.prr_workspace_init, FAKE + 16, 256)
 
 
+def test_stream_chain_rejects_bad_arguments(P):
+    # (fake stream handles: every case fails before the HIP runtime is called)
+    for n_hops, mode, a, b in ((3, P.PRR_CHAIN_EVENTS, 16, 32), (0, P.PRR_CHAIN_EVENTS, 16, 32),
+                               (258, P.PRR_CHAIN_ONE_STREAM, 16, 32), (4, 3, 16, 32),
+                               (4, P.PRR_CHAIN_EVENTS, 16, 16), (4, P.PRR_CHAIN_STREAM_MEMORY, 16, 16)):
+        with pytest.raises(P.PrrError) as e:
+            P.prr_stream_chain(n_hops, mode, a, b)
+        assert e.value.status == P.PRR_ERR_INVALID_ARG, (n_hops, mode)
+
+
 def test_last_error_is_thread_local(P):
     import threading
     d = P.make_dims(32, 2, 16, 100, P.PRR_BF16)

@@ -1,6 +1,7 @@
 """The library's measurement helpers on the GPU: the read-stream kernel reads every word
-once (the XOR of its per-workgroup words equals the XOR of the buffer), and the empty
-launch runs for the fused grid's shape."""
+once (the XOR of its per-workgroup words equals the XOR of the buffer), the empty
+launch runs for the fused grid's shape, and the chains of dependencies between two
+streams complete in every mode."""
 import numpy as np
 import pytest
 
@@ -43,3 +44,12 @@ def test_empty_launch_of_the_fused_grid(torch):
     torch.cuda.synchronize()
     with pytest.raises(L.PrrError):
         L.prr_empty_launch(0, 512)
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_stream_chain_completes(torch, mode):
+    from paper_2606_30389_amd import _lib as L
+    s, p2 = torch.cuda.current_stream(), torch.cuda.Stream()
+    for n in (2, 40, 256):  # (repeated calls reuse the events and the growing stream-memory values)
+        L.prr_stream_chain(n, mode, s, p2)
+    torch.cuda.synchronize()
