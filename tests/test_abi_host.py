@@ -212,6 +212,33 @@ def test_fused_step_rejects_bad_stamps_and_epoch(P):
     assert P.prr_fused_grid(d, params(), P.PRR_SCHED_FUSED_PRR) > 0
 
 
+def test_fused_step_page_cap(P):
+    """The fused schedules take at most 8192 pages per KV head (the select workgroup's
+    fallback holds every score of a KV head); a longer context is PRR_ERR_UNSUPPORTED before
+    any launch, while the separate kernels' workspace still covers it."""
+    d = P.make_dims(32, 2, 16, 16384, P.PRR_BF16)
+    assert P.prr_workspace_size(d, 256, 8) > 0
+    y = P.prr_layer_io()
+    for name, _ in P.prr_layer_io._fields_:
+        if name in ("predicted", "predicted_count"):
+            getattr(y, name)[0] = FAKE
+            getattr(y, name)[1] = FAKE
+        elif name == "ws_bytes":
+            y.ws_bytes = P.prr_workspace_size(d, 256, 8)
+        elif name in ("page_table", "out_o", "missed_count", "wasted_count", "covered_count", "theta"):
+            setattr(y, name, None)
+        else:
+            setattr(y, name, FAKE)
+    layers = (P.prr_layer_io * 1)(y)
+    for npages, status in ((8193, 2), (16384, 2)):
+        p = P.prr_step_params()
+        p.num_tokens, p.num_pages, p.k_select, p.p_select, p.cap = 16 * npages, npages, 256, 256, 256
+        p.chunk_pages, p.alpha, p.beta, p.epoch, p.late_spec = 8, 0.5, 0.5, 1, 1
+        for sched in (P.PRR_SCHED_FUSED_SERIAL, P.PRR_SCHED_FUSED_PRR, P.PRR_SCHED_FUSED_PREFILL):
+            _expect(P, status, P.prr_decode_step, d, p, layers, 0, sched)
+            assert "8192" in P.last_error()
+
+
 @pytest.mark.parametrize("ps", [32, 128, 256])
 def test_fused_schedules_need_page_16_or_64(P, ps):
     """The separate kernels take pages of 16 to 256 tokens; the fused schedules only 16
