@@ -82,7 +82,11 @@ CASES = [
     Case("glm32k", reinit=(2, 3), late=True, steps=4),
     Case("llama64k", reinit=(2,), late=True, steps=3),
     Case("glm128k", reinit=(2,), steps=3, late=True),
+    # the other output modes at full size: attention over P u A, and recomputation of A on any miss
+    Case("glm128k", mode=1, steps=3, late=True), Case("glm128k", mode=2, steps=3),
+    Case("infllm128k", mode=1, steps=3, late=True),
     # long runs: candidate windows and the late bound are learned across steps
+    Case("glm128k", steps=12, late=True, serial=False),
     Case("glm32k", steps=64, late=True, serial=False),
     Case("glm32k", steps=24, delta=1.5, late=True, serial=False),
     # the Llama-shaped workload's hot set re-drawn every 16 steps
