@@ -302,20 +302,22 @@ prr_status prr_stream_chain(int32_t n_hops, int32_t mode, hipStream_t a, hipStre
   if (dev < 0 || dev >= kChainMaxDevices) return fail(PRR_ERR_UNSUPPORTED, "device %d", dev);
   std::lock_guard<std::mutex> guard(g_chain_mu);
   ChainState& st = g_chain[dev];
-  if (!st.events) {
+  if (!st.events) {  // (a set-up that failed part-way resumes where it stopped)
     for (int i = 0; i < kChainMaxHops; ++i)
-      PRR_TRY(hip_status(hipEventCreateWithFlags(&st.ev[i], hipEventDisableTiming), "event create"));
+      if (!st.ev[i]) PRR_TRY(hip_status(hipEventCreateWithFlags(&st.ev[i], hipEventDisableTiming), "event create"));
     st.events = true;
   }
   if (mode == PRR_CHAIN_STREAM_MEMORY && !st.words) {
     int can = 0;
     PRR_TRY(hip_status(hipDeviceGetAttribute(&can, hipDeviceAttributeCanUseStreamWaitValue, dev), "attribute"));
     if (!can) return fail(PRR_ERR_UNSUPPORTED, "the device has no stream memory waits");
-    for (int k = 0; k < 2; ++k) {
-      PRR_TRY(hip_status(hipExtMallocWithFlags(&st.word[k], sizeof(uint64_t), hipMallocSignalMemory),
-                         "stream memory word"));
-      PRR_TRY(hip_status(hipStreamWriteValue64(a, st.word[k], 0ull, 0), "stream write"));
-    }
+    for (int k = 0; k < 2; ++k)
+      if (!st.word[k])
+        PRR_TRY(hip_status(hipExtMallocWithFlags(&st.word[k], sizeof(uint64_t), hipMallocSignalMemory),
+                           "stream memory word"));
+    // zero both words and wait, so that no first wait compares against what the new memory held
+    for (int k = 0; k < 2; ++k) PRR_TRY(hip_status(hipStreamWriteValue64(a, st.word[k], 0ull, 0), "stream write"));
+    PRR_TRY(hip_status(hipStreamSynchronize(a), "stream synchronize"));
     st.words = true;
   }
   for (int i = 0; i < n_hops; ++i) {
