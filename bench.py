@@ -11,7 +11,8 @@ its own K/V, so a token touches far more than the 256 MB last-level cache.
 Schedules timed (all launched natively by prr_decode_step):
   fused_prr     one launch per layer: select while speculating over P, repair, EMA update
   fused_serial  one launch per layer: select, then attend every page of A
-  two_stream    separate kernels, selection and speculation on two streams
+  two_stream    separate kernels, selection and speculation on two streams (event fork/join)
+  two_stream_mem  the same, the streams ordered by stream memory writes and waits
   serial        separate kernels on one stream: select, then attend A
 
 Prints one JSON line.  `value` is microseconds per decode step per layer of fused_prr
@@ -727,7 +728,7 @@ def main():
                     help="|P| / |A| (speculation budget); 'rule': Section 4.4's rule over the profiled table; "
                          "'auto': of the budgets that rule allows, the one with the shortest profiled step")
     ap.add_argument("--schedules", default="fused_prr,fused_prr_late,fused_prr_late_nora,fused_serial,fused_prr_late_graph,"
-                                           "two_stream,serial")
+                                           "two_stream,two_stream_mem,serial")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--kernel-reps", type=int, default=2, help="batches of 20 back-to-back calls per separate kernel (kernel_us)")
     ap.add_argument("--workers", type=int, default=16, help="input-generation processes (0 = in-process)")
@@ -769,6 +770,7 @@ def main():
     sched_id = {"fused_prr": L.PRR_SCHED_FUSED_PRR, "fused_prr_late": L.PRR_SCHED_FUSED_PRR,
                 "fused_prr_late_nora": L.PRR_SCHED_FUSED_PRR,
                 "fused_serial": L.PRR_SCHED_FUSED_SERIAL, "two_stream": L.PRR_SCHED_TWO_STREAM,
+                "two_stream_mem": L.PRR_SCHED_TWO_STREAM,
                 "serial": L.PRR_SCHED_SERIAL, "fused_prr_late_graph": L.PRR_SCHED_FUSED_PRR}
     n_abl = (3 if args.ablation else 0) + (2 if args.calibrate > 1 else 0)
     total_tokens = 2 + max(2, args.warmup) + 2 * (len(schedules) + n_abl) * (args.steps + 2) + \
@@ -867,6 +869,7 @@ def main():
     for name in schedules:  # warm each schedule, then two timed passes (the better one counts)
         cur[0] = stack_serial if name == "fused_serial" else stack
         stack.params.late_spec = late_spec_of(name)
+        stack.two_stream_events = name != "two_stream_mem"
         run(2, sched_id[name])
         # *_graph: the token's launches are captured as HIP graphs (one per parity of the
         # prediction buffers) and replayed; otherwise launched directly

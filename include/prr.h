@@ -336,7 +336,14 @@ typedef struct {
  * written on `stream`): the select / speculate / repair / predict steps of Fig. 1 and
  * Section 4 launched from native code with the fork/join of two streams.
  *   events      host [3 * n_layers + 1] hipEvent_t created by the caller (timing may be
- *               disabled); used for the fork/join of PRR_SCHED_TWO_STREAM, else ignored
+ *               disabled) for the fork/join of PRR_SCHED_TWO_STREAM, else ignored; NULL
+ *               with PRR_SCHED_TWO_STREAM orders the two streams with stream memory writes
+ *               and waits instead (hipStreamWriteValue64 / hipStreamWaitValue64 on four
+ *               64-bit words that the library allocates once per device and keeps until the
+ *               process ends; a dependency costs about half an event wait here).  Those
+ *               words are shared: two-stream steps without events that run at the same time
+ *               on one device (from several host threads) must not be enqueued; with events
+ *               they may.  PRR_ERR_UNSUPPORTED when the device has no stream memory waits.
  *   parity      0 or 1: which predicted buffer holds P^t
  * When the call returns every launch is enqueued; all work of the step is ordered
  * before any later work on `stream` (the speculation stream is joined back).  The

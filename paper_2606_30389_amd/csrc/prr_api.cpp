@@ -182,15 +182,18 @@ void budget(int k_select, int n_forced, int forced_in_budget, int num_pages, int
   total = std::min(num_pages, n_forced + kextra);
 }
 
-// prr_stream_chain's events and stream-memory words, made once per device and kept until
-// the process ends (a stream may still wait on them when the call returns).
+// Events and stream-memory words of prr_stream_chain (words 0, 1) and of the two-stream
+// step without events (words 2-5: fork, selection, speculation, join), made once per device
+// and kept until the process ends (a stream may still wait on them when a call returns).
+// Every value written is larger than the one before, so each word only grows.
 constexpr int kChainMaxHops = 256;
 constexpr int kChainMaxDevices = 16;
+constexpr int kStreamWords = 6;
 struct ChainState {
   bool events = false, words = false;
   hipEvent_t ev[kChainMaxHops] = {};
-  void* word[2] = {nullptr, nullptr};
-  uint64_t value = 0;  // the last value written (values only grow)
+  void* word[kStreamWords] = {};
+  uint64_t value = 0;  // the last value written
 };
 std::mutex g_chain_mu;
 ChainState g_chain[kChainMaxDevices];
@@ -288,6 +291,54 @@ prr_status prr_read_stream(const void* buf, size_t bytes, uint32_t* sink, int32_
   return hip_status(prr::launch_read_stream(buf, bytes, sink, grid, stream), "read stream");
 }
 
+}  // extern "C"
+
+namespace {
+
+// This device's events and stream-memory words (the caller locks g_chain_mu to use them).
+prr_status chain_state(ChainState*& st) {
+  int dev = 0;
+  PRR_TRY(hip_status(hipGetDevice(&dev), "get device"));
+  if (dev < 0 || dev >= kChainMaxDevices) return fail(PRR_ERR_UNSUPPORTED, "device %d", dev);
+  st = &g_chain[dev];
+  return ok();
+}
+
+// The stream-memory words, allocated and zeroed on first use (a set-up that failed
+// part-way resumes where it stopped); called with g_chain_mu held.
+prr_status stream_words(ChainState& st, hipStream_t s) {
+  if (st.words) return ok();
+  int dev = 0, can = 0;
+  PRR_TRY(hip_status(hipGetDevice(&dev), "get device"));
+  PRR_TRY(hip_status(hipDeviceGetAttribute(&can, hipDeviceAttributeCanUseStreamWaitValue, dev), "attribute"));
+  if (!can) return fail(PRR_ERR_UNSUPPORTED, "the device has no stream memory waits");
+  for (int k = 0; k < kStreamWords; ++k)
+    if (!st.word[k])
+      PRR_TRY(hip_status(hipExtMallocWithFlags(&st.word[k], sizeof(uint64_t), hipMallocSignalMemory),
+                         "stream memory word"));
+  // zero every word and wait, so that no first wait compares against what the new memory held
+  for (int k = 0; k < kStreamWords; ++k)
+    PRR_TRY(hip_status(hipStreamWriteValue64(s, st.word[k], 0ull, 0), "stream write"));
+  PRR_TRY(hip_status(hipStreamSynchronize(s), "stream synchronize"));
+  st.words = true;
+  return ok();
+}
+
+// `to` waits until `from` has reached this point: an event, or a stream-memory word.
+prr_status stream_dep(hipStream_t from, hipStream_t to, hipEvent_t ev, ChainState* mem, int word) {
+  if (!mem) {
+    PRR_TRY(hip_status(hipEventRecord(ev, from), "event record"));
+    return hip_status(hipStreamWaitEvent(to, ev, 0), "stream wait");
+  }
+  const uint64_t v = ++mem->value;
+  PRR_TRY(hip_status(hipStreamWriteValue64(from, mem->word[word], v, 0), "stream write"));
+  return hip_status(hipStreamWaitValue64(to, mem->word[word], v, hipStreamWaitValueGte, ~0ull), "stream wait");
+}
+
+}  // namespace
+
+extern "C" {
+
 prr_status prr_stream_chain(int32_t n_hops, int32_t mode, hipStream_t a, hipStream_t b) {
   if (n_hops < 2 || n_hops > kChainMaxHops || n_hops % 2 != 0)
     return fail(PRR_ERR_INVALID_ARG, "n_hops %d is not even in [2, %d]", n_hops, kChainMaxHops);
@@ -297,29 +348,16 @@ prr_status prr_stream_chain(int32_t n_hops, int32_t mode, hipStream_t a, hipStre
     return ok();
   }
   if (a == b) return fail(PRR_ERR_INVALID_ARG, "a dependency needs two different streams");
-  int dev = 0;
-  PRR_TRY(hip_status(hipGetDevice(&dev), "get device"));
-  if (dev < 0 || dev >= kChainMaxDevices) return fail(PRR_ERR_UNSUPPORTED, "device %d", dev);
+  ChainState* stp = nullptr;
+  PRR_TRY(chain_state(stp));
   std::lock_guard<std::mutex> guard(g_chain_mu);
-  ChainState& st = g_chain[dev];
+  ChainState& st = *stp;
   if (!st.events) {  // (a set-up that failed part-way resumes where it stopped)
     for (int i = 0; i < kChainMaxHops; ++i)
       if (!st.ev[i]) PRR_TRY(hip_status(hipEventCreateWithFlags(&st.ev[i], hipEventDisableTiming), "event create"));
     st.events = true;
   }
-  if (mode == PRR_CHAIN_STREAM_MEMORY && !st.words) {
-    int can = 0;
-    PRR_TRY(hip_status(hipDeviceGetAttribute(&can, hipDeviceAttributeCanUseStreamWaitValue, dev), "attribute"));
-    if (!can) return fail(PRR_ERR_UNSUPPORTED, "the device has no stream memory waits");
-    for (int k = 0; k < 2; ++k)
-      if (!st.word[k])
-        PRR_TRY(hip_status(hipExtMallocWithFlags(&st.word[k], sizeof(uint64_t), hipMallocSignalMemory),
-                           "stream memory word"));
-    // zero both words and wait, so that no first wait compares against what the new memory held
-    for (int k = 0; k < 2; ++k) PRR_TRY(hip_status(hipStreamWriteValue64(a, st.word[k], 0ull, 0), "stream write"));
-    PRR_TRY(hip_status(hipStreamSynchronize(a), "stream synchronize"));
-    st.words = true;
-  }
+  if (mode == PRR_CHAIN_STREAM_MEMORY) PRR_TRY(stream_words(st, a));
   for (int i = 0; i < n_hops; ++i) {
     hipStream_t x = (i & 1) ? b : a, y = (i & 1) ? a : b;
     PRR_TRY(hip_status(prr::launch_empty(1, 64, x), "empty launch"));
@@ -808,7 +846,14 @@ prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* sp, cons
     for (int l = 0; l < n_layers; ++l) PRR_TRY(fused_layer(dims, sp, layers[l], parity, schedule, stream, l));
     return ok();
   }
-  if (schedule == PRR_SCHED_TWO_STREAM && !events) return fail(PRR_ERR_INVALID_ARG, "events is NULL");
+  // PRR_SCHED_TWO_STREAM without events: the library's stream-memory words order the streams
+  ChainState* mem = nullptr;
+  std::unique_lock<std::mutex> mem_lock(g_chain_mu, std::defer_lock);
+  if (schedule == PRR_SCHED_TWO_STREAM && !events) {
+    PRR_TRY(chain_state(mem));
+    mem_lock.lock();
+    PRR_TRY(stream_words(*mem, stream));
+  }
   const int nxt = 1 - parity;
   for (int l = 0; l < n_layers; ++l) {
     const prr_layer_io& y = layers[l];
@@ -830,33 +875,34 @@ prr_status prr_decode_step(const prr_dims* dims, const prr_step_params* sp, cons
                           th[2], sp->p_select, sp->forced, sp->n_forced, sp->forced_in_budget,
                           y.predicted[nxt], y.predicted_count[nxt], sp->cap, stream));
     } else {
-      hipEvent_t fork = events[3 * l], sel = events[3 * l + 1], spec = events[3 * l + 2];
-      PRR_TRY(hip_status(hipEventRecord(fork, stream), "event record"));
-      PRR_TRY(hip_status(hipStreamWaitEvent(spec_stream, fork, 0), "stream wait"));
+      hipEvent_t fork = mem ? nullptr : events[3 * l], sel = mem ? nullptr : events[3 * l + 1],
+                 spec = mem ? nullptr : events[3 * l + 2];
+      PRR_TRY(stream_dep(stream, spec_stream, fork, mem, 2));
       PRR_TRY(prr_score_topk(dims, y.q, y.meta, sp->num_pages, sp->k_select, sp->forced, sp->n_forced,
                              sp->forced_in_budget, y.scores, y.selected, y.selected_count, sp->cap, y.workspace,
                              y.ws_bytes, stream));
-      PRR_TRY(hip_status(hipEventRecord(sel, stream), "event record"));
+      // (the selection's point on `stream`, waited for by the prediction below)
+      const uint64_t sel_value = mem ? ++mem->value : 0;
+      if (mem) PRR_TRY(hip_status(hipStreamWriteValue64(stream, mem->word[3], sel_value, 0), "stream write"));
+      else PRR_TRY(hip_status(hipEventRecord(sel, stream), "event record"));
       PRR_TRY(prr_spec_attn(dims, y.q, y.k_cache, y.v_cache, y.page_table, sp->num_tokens, y.predicted[parity],
                             y.predicted_count[parity], sp->cap, sp->chunk_pages, y.part_o, y.part_m, y.part_l,
                             y.page_m, spec_stream));
-      PRR_TRY(hip_status(hipEventRecord(spec, spec_stream), "event record"));
-      PRR_TRY(hip_status(hipStreamWaitEvent(stream, spec, 0), "stream wait"));
+      PRR_TRY(stream_dep(spec_stream, stream, spec, mem, 4));
       PRR_TRY(prr_repair(dims, y.q, y.k_cache, y.v_cache, y.page_table, sp->num_tokens, sp->num_pages, y.selected,
                          y.selected_count, y.predicted[parity], y.predicted_count[parity], sp->cap, sp->chunk_pages,
                          y.part_o, y.part_m, y.part_l, y.page_m, sp->mode, y.out_o32, y.out_o, y.out_m, y.out_l,
                          y.missed_count, y.wasted_count, y.workspace, y.ws_bytes, stream));
-      PRR_TRY(hip_status(hipStreamWaitEvent(spec_stream, sel, 0), "stream wait"));
+      if (mem)
+        PRR_TRY(hip_status(hipStreamWaitValue64(spec_stream, mem->word[3], sel_value, hipStreamWaitValueGte, ~0ull),
+                           "stream wait"));
+      else PRR_TRY(hip_status(hipStreamWaitEvent(spec_stream, sel, 0), "stream wait"));
       PRR_TRY(prr_predict(dims, y.ema_level, y.ema_trend, y.ema_init_bits, y.scores, sp->num_pages, th[0], th[1],
                           th[2], sp->p_select, sp->forced, sp->n_forced, sp->forced_in_budget,
                           y.predicted[nxt], y.predicted_count[nxt], sp->cap, spec_stream));
     }
   }
-  if (schedule == PRR_SCHED_TWO_STREAM) {
-    hipEvent_t join = events[3 * n_layers];
-    PRR_TRY(hip_status(hipEventRecord(join, spec_stream), "event record"));
-    PRR_TRY(hip_status(hipStreamWaitEvent(stream, join, 0), "stream wait"));
-  }
+  if (schedule == PRR_SCHED_TWO_STREAM) PRR_TRY(stream_dep(spec_stream, stream, mem ? nullptr : events[3 * n_layers], mem, 5));
   return ok();
 }
 

@@ -250,6 +250,9 @@ class DecodeStack:
         p.alpha, p.beta, p.gamma = cfg.alpha, cfg.beta, cfg.gamma
         self.params = p
         self.events = L.hip_events(3 * len(layers) + 1)
+        # the two-stream schedule's fork/join: the caller's events, or (False) the library's
+        # stream-memory words
+        self.two_stream_events = True
 
     def set_layer_theta(self, thetas):
         """Per-layer EMA parameters (Section 4.2 calibrates one per layer): a sequence of
@@ -273,7 +276,8 @@ class DecodeStack:
         parity = self._parity()
         self.params.epoch = next_epoch()
         self.params.epoch_dev = None
-        L.prr_decode_step(self.dims, self.params, self.io, parity, schedule, stream, spec_stream, self.events)
+        events = self.events if (schedule != L.PRR_SCHED_TWO_STREAM or self.two_stream_events) else None
+        L.prr_decode_step(self.dims, self.params, self.io, parity, schedule, stream, spec_stream, events)
         self._advance(schedule, parity)
 
     def capture(self, schedule, stream, tag=None):

@@ -615,10 +615,12 @@ def test_merge_states(torch):
     assert np.allclose(S.to_np(out_l), ref[2], rtol=1e-5)
 
 
+@pytest.mark.parametrize("sync", ["events", "memory"])
 @pytest.mark.parametrize("name,npages,mode", [("glm32k", 512, 0), ("llama64k", 300, 1), ("infllm128k", 200, 0)])
-def test_native_decode_step(torch, name, npages, mode):
+def test_native_decode_step(torch, name, npages, mode, sync):
     """prr_decode_step over a stack of layers: step 0 (select + EMA init), then the
-    two-stream PRR schedule and the serial schedule, every layer against the oracle."""
+    two-stream PRR schedule (its streams ordered by the caller's events, or by the library's
+    stream-memory words) and the serial schedule, every layer against the oracle."""
     from paper_2606_30389_amd import _lib as L
     from paper_2606_30389_amd import runtime as R
     cfg = W.CONFIGS[name]
@@ -637,6 +639,7 @@ def test_native_decode_step(torch, name, npages, mode):
         queries.append(S.q_tensor(qb[0], pc))
     pc = layers[0].cfg
     stack = R.DecodeStack(layers, queries, torch.device("cuda:0"))
+    stack.two_stream_events = sync == "events"
     s, p = torch.cuda.Stream(), torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     stack.step(L.PRR_SCHED_PREFILL, s)
@@ -651,7 +654,7 @@ def test_native_decode_step(torch, name, npages, mode):
             queries[layer].copy_(S.q_tensor(qs[layer][t], pc))
         torch.cuda.synchronize()
         preds = [S.lists(st, st.cur) for st in layers]
-        S.log(f"native two-stream step {t}")
+        S.log(f"native two-stream step {t} ({sync})")
         s.wait_stream(torch.cuda.current_stream())
         stack.step(L.PRR_SCHED_TWO_STREAM, s, p)
         torch.cuda.synchronize()
