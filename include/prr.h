@@ -340,7 +340,8 @@ typedef struct {
  *               with PRR_SCHED_TWO_STREAM orders the two streams with stream memory writes
  *               and waits instead (hipStreamWriteValue64 / hipStreamWaitValue64 on four
  *               64-bit words that the library allocates once per device and keeps until the
- *               process ends; a dependency costs about half an event wait here).  Those
+ *               process ends; the first such call on a device zeroes them and waits for
+ *               `stream`; a dependency costs about half an event wait here).  Those
  *               words are shared: two-stream steps without events that run at the same time
  *               on one device (from several host threads) must not be enqueued; with events
  *               they may.  PRR_ERR_UNSUPPORTED when the device has no stream memory waits.
